@@ -1,0 +1,128 @@
+"""Seeded synthetic inputs for the LaCT fast-weight layer forward.
+
+This module is shared by the tests, the benchmark and the oracle checks. It
+holds no arithmetic of the method itself: it only draws random tensors, puts
+them in the shapes of the paper's workloads and rounds them to the I/O
+precision. Both the HIP path and the oracle consume exactly the arrays it
+returns.
+
+Recipe (one (seed, config) -> one set of host arrays):
+
+* independent sub-streams for q, k, v, eta, W1, W2, W3 from
+  ``numpy.random.SeedSequence(seed).spawn(7)``;
+* q, k, v ~ N(0, 1), L2-normalised per token per head (the layer normalises q
+  and k before the fast-weight path, Alg. 1; v is normalised too so that all
+  three share one scale), then rounded to bfloat16 (round-to-nearest-even)
+  for bf16 workloads;
+* eta = 0.01 * softplus(N(0, 1)) per token per head, float32 (a per-token
+  learning rate, eq. of the chunk gradient; the 0.01 scale is the paper's
+  constant learning-rate bias magnitude);
+* W1, W3 in R^{h x d}, W2 in R^{d x h} ~ N(0, 1/d), then every row (the input
+  dimension of that matrix) scaled to unit L2 norm, float32, one copy per
+  head repeated over the batch (Alg. 1 repeats the per-head initial fast
+  weight over the batch).
+"""
+from __future__ import annotations
+
+import dataclasses
+import numpy as np
+
+__all__ = ["LactConfig", "CONFIGS", "make_inputs", "round_to_bf16", "bf16_bits"]
+
+
+@dataclasses.dataclass(frozen=True)
+class LactConfig:
+    name: str
+    B: int
+    H: int
+    d: int
+    h: int
+    n_kv: int
+    n_q: int
+    chunk: int
+    order: int            # 0 = apply-then-update, 1 = update-then-apply
+    use_muon: int
+    ns_steps: int
+    io: str               # "bf16" or "fp32"
+
+    @property
+    def BH(self) -> int:
+        return self.B * self.H
+
+    @property
+    def n_chunks(self) -> int:
+        return (self.n_kv + self.chunk - 1) // self.chunk
+
+    def with_(self, **kw) -> "LactConfig":
+        return dataclasses.replace(self, **kw)
+
+
+# The paper's workload shapes (language model, novel-view synthesis, video).
+CONFIGS = {
+    "tiny_fp32": LactConfig("tiny_fp32", 1, 2, 64, 64, 1024, 1024, 256, 0, 0, 0, "fp32"),
+    "lm32k": LactConfig("lm32k", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16"),
+    "lm32k_muon": LactConfig("lm32k_muon", 4, 4, 512, 512, 32768, 32768, 2048, 0, 1, 5, "bf16"),
+    "nvs256k": LactConfig("nvs256k", 1, 1, 768, 1536, 262144, 262144 + 4096, 262144, 1, 0, 0, "bf16"),
+    "nvs1m": LactConfig("nvs1m", 1, 1, 768, 1536, 1048576, 1048576 + 4096, 1048576, 1, 0, 0, "bf16"),
+    "video": LactConfig("video", 1, 40, 128, 256, 56160, 56160, 3120, 0, 1, 5, "bf16"),
+}
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 array -> uint16 bfloat16 bit patterns, round-to-nearest-even."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    r = (u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)
+    nan = np.isnan(x)
+    if nan.any():
+        r = np.where(nan, np.uint32(0x7FC0), r)
+    return r.astype(np.uint16)
+
+
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """float32 array rounded (RNE) to the nearest bfloat16, returned as float32."""
+    return (bf16_bits(x).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _unit_rows(x: np.ndarray) -> np.ndarray:
+    n = np.sqrt(np.sum(x.astype(np.float64) ** 2, axis=-1, keepdims=True))
+    return (x / n).astype(np.float32)
+
+
+def make_inputs(cfg: LactConfig, seed: int = 0, heads: list | None = None):
+    """Draw the inputs of one workload.
+
+    Returns a dict of float32 numpy arrays (bf16 workloads hold values that are
+    exactly representable in bfloat16):
+      q [B*H, n_q, d], k, v [B*H, n_kv, d], eta [B*H, n_kv],
+      W1, W3 [B*H, h, d], W2 [B*H, d, h].
+    ``heads`` restricts the draw to a subset of the flattened (b, h) instances;
+    the values of each kept instance are the same as in the full draw only for
+    the weights (token tensors are drawn for the kept instances only).
+    """
+    ss = np.random.SeedSequence(seed).spawn(7)
+    rq, rk, rv, re, r1, r2, r3 = (np.random.default_rng(s) for s in ss)
+    BH = cfg.BH
+    inst = list(range(BH)) if heads is None else list(heads)
+    n = len(inst)
+
+    def tok(rng, ntok):
+        x = rng.standard_normal((n, ntok, cfg.d), dtype=np.float32)
+        x /= np.sqrt(np.sum(np.square(x, dtype=np.float32), axis=-1, keepdims=True))
+        return round_to_bf16(x) if cfg.io == "bf16" else x
+
+    q = tok(rq, cfg.n_q)
+    k = tok(rk, cfg.n_kv)
+    v = tok(rv, cfg.n_kv)
+    z = re.standard_normal((n, cfg.n_kv), dtype=np.float32).astype(np.float64)
+    eta = (0.01 * np.logaddexp(0.0, z)).astype(np.float32)
+
+    std = 1.0 / np.sqrt(cfg.d)
+    w1 = _unit_rows(r1.standard_normal((cfg.H, cfg.h, cfg.d), dtype=np.float32) * std)
+    w2 = _unit_rows(r2.standard_normal((cfg.H, cfg.d, cfg.h), dtype=np.float32) * std)
+    w3 = _unit_rows(r3.standard_normal((cfg.H, cfg.h, cfg.d), dtype=np.float32) * std)
+    head_of = [i % cfg.H for i in inst]
+    W1 = np.ascontiguousarray(w1[head_of])
+    W2 = np.ascontiguousarray(w2[head_of])
+    W3 = np.ascontiguousarray(w3[head_of])
+    return dict(q=q, k=k, v=v, eta=eta, W1=W1, W2=W2, W3=W3)

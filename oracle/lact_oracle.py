@@ -1,0 +1,222 @@
+"""Oracle for the LaCT fast-weight layer forward: plain, slow, fp64, CPU.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the benchmark's
+CPU-baseline leg may import this module. The product (the HIP library and its
+Python binding) never calls it and shares no code with it.
+
+It follows "Test-Time Training Done Right" (LaCT) step by step, per
+(batch, head) instance, in float64 NumPy:
+
+* fast weight      f_W(x) = W2 [SiLU(W1 x) o (W3 x)]           (§3.1, SwiGLU eq.)
+* loss             L(f_W(k), v) = -f_W(k)^T v                   (§3.1, loss eq.)
+* chunk gradient   g = grad_W sum_i eta_i L(f_W(k_i), v_i)      (§3.1, chunk-gradient eq.)
+* weight update    W <- L2-Normalize(W - g)  or  W - Muon(g)    (§3.2, both update eqs.)
+                   normalisation per row along the input dimension, rescaled
+                   to the row norm W had before the update (Alg. 1, update)
+* Muon(g)          Newton-Schulz quintic iteration on g/||g||_F  (App. A, Details of Muon)
+* chunk schedule   apply-then-update / update-then-apply         (§3.1 orders; Alg. 1)
+
+Math layout (one instance): W1, W3 in R^{h x d}, W2 in R^{d x h}; a "row" is
+the input dimension of the matrix (d for W1 and W3, h for W2). Tokens are rows
+of q, k, v in R^{n x d}.
+
+Readings taken where the paper is silent or ambiguous (each one is also a
+test):
+  R1 norm target: the pseudocode rescales W - g to the row norms of the
+     pre-update W; this oracle does that (it coincides with unit rows when the
+     initial rows are unit-norm).
+  R2 one learning rate eta_i per token scales the loss of token i; the three
+     per-matrix rates of the pseudocode are the same number here.
+  R3 Newton-Schulz divides by ||G||_F + 1e-7 (the paper writes ||G||_F), so a
+     zero gradient gives a zero update instead of 0/0.
+  R4 Newton-Schulz works on the wide orientation (transpose when rows > cols,
+     transpose back); the iteration is identical in exact arithmetic either way.
+  R5 (G G^T)^2 G is evaluated as (b A + c A A) X with A = X X^T.
+  R6 the last chunk may be partial; the final update is always performed, so
+     the returned fast weights include it; query tokens past the last key
+     token (a "tail") are applied with the final fast weights.
+  R7 a chunk's gradient is summed over token blocks of at most ``token_block``
+     tokens; the gradient is a sum over tokens (the linearity that §3.4 uses
+     to shard a chunk over devices), so this only bounds host memory.
+
+parity: pinned (see tests/test_oracle_pins.py for each pin).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "NS_COEFFS", "NS_EPS", "sigmoid", "silu", "swiglu_apply", "chunk_gradient",
+    "newton_schulz", "weight_update", "update", "lact_forward_instance",
+    "lact_forward", "layer_flops",
+]
+
+# Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
+NS_COEFFS = (3.4445, -4.7750, 2.0315)
+NS_STEPS_DEFAULT = 5
+NS_EPS = 1e-7  # reading R3
+
+
+def sigmoid(z: np.ndarray) -> np.ndarray:
+    # Written in the two stable branches so large |z| does not overflow exp.
+    out = np.empty_like(z, dtype=np.float64)
+    pos = z >= 0
+    out[pos] = 1.0 / (1.0 + np.exp(-z[pos]))
+    ez = np.exp(z[~pos])
+    out[~pos] = ez / (1.0 + ez)
+    return out
+
+
+def silu(z: np.ndarray) -> np.ndarray:
+    """SiLU(z) = z * sigmoid(z) (the activation of the SwiGLU fast weight)."""
+    return z * sigmoid(z)
+
+
+def swiglu_apply(W1, W2, W3, X):
+    """Apply operation o = f_W(x) for every row x of X (§2.1 apply eq.; §3.1 SwiGLU eq.).
+
+    W1, W3: [h, d]; W2: [d, h]; X: [n, d] -> [n, d].
+    """
+    X = np.asarray(X, dtype=np.float64)
+    Z1 = X @ W1.T             # W1 x for every token, [n, h]
+    Z3 = X @ W3.T             # W3 x, [n, h]
+    H = silu(Z1) * Z3         # SiLU(W1 x) o (W3 x)
+    return H @ W2.T           # W2 [ ... ], [n, d]
+
+
+def chunk_gradient(W1, W2, W3, K, V, eta, token_block: int = 65536):
+    """Gradient of sum_i eta_i * (-f_W(k_i)^T v_i) w.r.t. (W1, W2, W3).
+
+    §3.1 chunk-gradient and loss eqs.; the backward follows the update of
+    Alg. 1: forward on the keys, then the hidden gradient W2^T v_i pushed
+    through the gate product and the SiLU derivative
+    SiLU'(z) = s (1 + z (1 - s)), s = sigmoid(z).
+
+    Returns (g1 [h, d], g2 [d, h], g3 [h, d]) in float64.
+    """
+    h, d = W1.shape
+    g1 = np.zeros((h, d))
+    g2 = np.zeros((d, h))
+    g3 = np.zeros((h, d))
+    n = K.shape[0]
+    for s in range(0, n, token_block):   # reading R7
+        e = min(n, s + token_block)
+        k = np.asarray(K[s:e], dtype=np.float64)
+        v = np.asarray(V[s:e], dtype=np.float64)
+        lr = np.asarray(eta[s:e], dtype=np.float64)[:, None]
+        z1 = k @ W1.T                      # pre-activation of the gate, [b, h]
+        z3 = k @ W3.T                      # ungated hidden, [b, h]
+        sg = sigmoid(z1)
+        a = z1 * sg                        # SiLU(z1)
+        hid = a * z3                       # hidden state of f_W(k)
+        dhid = v @ W2                      # d(f^T v)/d hidden = W2^T v, [b, h]
+        dz3 = dhid * a                     # through the gate product, W3 branch
+        da = dhid * z3                     # through the gate product, W1 branch
+        dz1 = da * sg * (1.0 + z1 * (1.0 - sg))   # SiLU derivative
+        # L = -eta f^T v, so every gradient carries a minus sign.
+        g2 -= (v * lr).T @ hid             # dL/dW2 = -sum eta v hid^T
+        g1 -= (dz1 * lr).T @ k             # dL/dW1 = -sum eta dz1 k^T
+        g3 -= (dz3 * lr).T @ k             # dL/dW3 = -sum eta dz3 k^T
+    return g1, g2, g3
+
+
+def newton_schulz(G, steps: int = NS_STEPS_DEFAULT, coeffs=NS_COEFFS, eps: float = NS_EPS):
+    """Muon's orthogonalisation of a matrix gradient (App. A, Details of Muon; §3.2).
+
+    X_0 = G / (||G||_F + eps);  X_k = a X + b (X X^T) X + c (X X^T)^2 X.
+    Readings R3 (eps), R4 (orientation) and R5 (evaluation order).
+    """
+    a, b, c = coeffs
+    X = np.asarray(G, dtype=np.float64)
+    transposed = X.shape[0] > X.shape[1]
+    if transposed:
+        X = X.T
+    X = X / (np.linalg.norm(X) + eps)
+    for _ in range(steps):
+        A = X @ X.T
+        Bm = b * A + c * (A @ A)
+        X = a * X + Bm @ X
+    return X.T if transposed else X
+
+
+def weight_update(W, step):
+    """W <- L2-Normalize(W - step), per row along the input dimension (§3.2).
+
+    Rows are rescaled to the norm they had before the update (reading R1).
+    """
+    U = W - step
+    n_old = np.sqrt(np.sum(W * W, axis=1, keepdims=True))
+    n_new = np.sqrt(np.sum(U * U, axis=1, keepdims=True))
+    return U * (n_old / n_new)
+
+
+def update(W, K, V, eta, use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT,
+           token_block: int = 65536):
+    """Update operation on one chunk: gradient, optional Muon, normalised step."""
+    W1, W2, W3 = W
+    g1, g2, g3 = chunk_gradient(W1, W2, W3, K, V, eta, token_block)
+    if use_muon:
+        g1, g2, g3 = (newton_schulz(g, ns_steps) for g in (g1, g2, g3))
+    return weight_update(W1, g1), weight_update(W2, g2), weight_update(W3, g3)
+
+
+def lact_forward_instance(q, k, v, eta, W1, W2, W3, chunk: int, order: int,
+                          use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT,
+                          token_block: int = 65536, trace: list | None = None):
+    """One (batch, head) instance of the layer's fast-weight path.
+
+    q [n_q, d], k, v [n_kv, d], eta [n_kv]; W1, W3 [h, d], W2 [d, h].
+    order 0 = apply-then-update (shifted block-causal), 1 = update-then-apply
+    (§3.1, execution orders; Alg. 1). Returns (o [n_q, d], (W1, W2, W3)).
+    If ``trace`` is a list, the fast weights entering every chunk are appended.
+    """
+    W = tuple(np.asarray(w, dtype=np.float64).copy() for w in (W1, W2, W3))
+    n_q, n_kv = q.shape[0], k.shape[0]
+    assert n_q >= n_kv and chunk > 0
+    o = np.zeros((n_q, q.shape[1]))
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        if trace is not None:
+            trace.append(W)
+        if order == 0:
+            o[s:e] = swiglu_apply(*W, q[s:e])
+            W = update(W, k[s:e], v[s:e], eta[s:e], use_muon, ns_steps, token_block)
+        else:
+            W = update(W, k[s:e], v[s:e], eta[s:e], use_muon, ns_steps, token_block)
+            o[s:e] = swiglu_apply(*W, q[s:e])
+    if n_q > n_kv:                       # reading R6: apply-only tail
+        o[n_kv:] = swiglu_apply(*W, q[n_kv:])
+    return o, W
+
+
+def lact_forward(q, k, v, eta, W1, W2, W3, chunk: int, order: int, use_muon: bool = False,
+                 ns_steps: int = NS_STEPS_DEFAULT, instances=None, token_block: int = 65536):
+    """Batched driver over the (batch*head) instances (Alg. 1 merges heads into batch).
+
+    Arrays carry a leading instance axis. ``instances`` optionally selects a
+    subset. Returns (o, W1, W2, W3) stacked over the selected instances.
+    """
+    idx = range(q.shape[0]) if instances is None else instances
+    outs, w1s, w2s, w3s = [], [], [], []
+    for i in idx:
+        o, (a, b, c) = lact_forward_instance(q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i],
+                                             chunk, order, use_muon, ns_steps, token_block)
+        outs.append(o); w1s.append(a); w2s.append(b); w3s.append(c)
+    return np.stack(outs), np.stack(w1s), np.stack(w2s), np.stack(w3s)
+
+
+def layer_flops(BH: int, d: int, h: int, n_kv: int, n_q: int, n_chunks: int,
+                use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT) -> float:
+    """Algorithmic FLOPs of the path (App. A, FLOPs calculation).
+
+    Per head: an updated token costs 2 forward matmuls on the key (4dh),
+    4 gradient matmuls including the hidden gradient (8dh); an applied token
+    costs 3 matmuls (6dh), so a token that is both updated and applied costs
+    18dh. Muon adds per matrix and iteration 3 matmuls on the m x n matrix
+    (m <= n): X X^T (2 m^2 n), A A (2 m^3), B X (2 m^2 n).
+    """
+    f = BH * (12.0 * d * h * n_kv + 6.0 * d * h * n_q)
+    if use_muon:
+        m, n = min(d, h), max(d, h)
+        f += BH * n_chunks * 3 * ns_steps * (4.0 * m * m * n + 2.0 * m ** 3)
+    return f

@@ -1,0 +1,383 @@
+"""Pins of the fp64 oracle against facts fixed by the paper and by mathematics.
+
+None of these re-types the oracle's own formula: each compares it with an
+independent route (autograd, finite differences, SVD, a library SwiGLU, a
+per-token loop, brute-force invariants) so that a dropped term, a wrong sign,
+a wrong index or a transposed operand in the oracle fails at least one test.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import lact_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+torch.set_default_dtype(torch.float64)
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _weights(rng, h, d, unit=False, scale=1.0):
+    W1 = rng.standard_normal((h, d)) * scale
+    W2 = rng.standard_normal((d, h)) * scale
+    W3 = rng.standard_normal((h, d)) * scale
+    if unit:
+        W1, W2, W3 = (w / np.linalg.norm(w, axis=1, keepdims=True) for w in (W1, W2, W3))
+    return W1, W2, W3
+
+
+def _tokens(rng, n, d):
+    x = rng.standard_normal((n, d))
+    return x / np.linalg.norm(x, axis=1, keepdims=True)
+
+
+def _torch_swiglu(W1, W2, W3, X):
+    """Library SwiGLU MLP without biases: F.linear + F.silu (independent of the oracle)."""
+    t = lambda a: torch.as_tensor(np.asarray(a, dtype=np.float64))
+    x = t(X)
+    return F.linear(F.silu(F.linear(x, t(W1))) * F.linear(x, t(W3)), t(W2))
+
+
+def _torch_loss(W1, W2, W3, K, V, eta):
+    """sum_i eta_i * (-f_W(k_i)^T v_i), built from library ops."""
+    f = _torch_swiglu(W1, W2, W3, K) if not isinstance(W1, torch.Tensor) else \
+        F.linear(F.silu(F.linear(K, W1)) * F.linear(K, W3), W2)
+    Vt = V if isinstance(V, torch.Tensor) else torch.as_tensor(V)
+    et = eta if isinstance(eta, torch.Tensor) else torch.as_tensor(eta)
+    return -(et * (f * Vt).sum(-1)).sum()
+
+
+# ----------------------------------------------------------------------------- apply
+
+
+def test_swiglu_apply_matches_library_mlp():
+    rng = _rng(1)
+    h, d = 7, 5                                   # non-square catches transposes
+    W1, W2, W3 = _weights(rng, h, d)
+    X = rng.standard_normal((9, d))
+    ref = _torch_swiglu(W1, W2, W3, X).numpy()
+    np.testing.assert_allclose(O.swiglu_apply(W1, W2, W3, X), ref, rtol=1e-13, atol=1e-13)
+
+
+def test_sigmoid_silu_extremes():
+    z = np.array([-800.0, -30.0, -1.0, 0.0, 1.0, 30.0, 800.0])
+    np.testing.assert_allclose(O.sigmoid(z), torch.sigmoid(torch.as_tensor(z)).numpy(), rtol=1e-15)
+    np.testing.assert_allclose(O.silu(z), F.silu(torch.as_tensor(z)).numpy(), rtol=1e-15, atol=1e-300)
+
+
+# ----------------------------------------------------------------------------- gradient
+
+
+@pytest.mark.parametrize("h,d,n", [(3, 5, 7), (8, 3, 4), (5, 5, 8)])
+def test_chunk_gradient_autograd(h, d, n):
+    rng = _rng(10 + h + d + n)
+    W = _weights(rng, h, d)
+    K, V = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    eta = rng.uniform(0.1, 2.0, n)
+    tw = [torch.tensor(w, requires_grad=True) for w in W]
+    _torch_loss(*tw, torch.as_tensor(K), torch.as_tensor(V), torch.as_tensor(eta)).backward()
+    g = O.chunk_gradient(*W, K, V, eta)
+    for gi, twi in zip(g, tw):
+        np.testing.assert_allclose(gi, twi.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("h,d,n", [(3, 5, 7), (8, 3, 4)])
+def test_chunk_gradient_finite_differences(h, d, n):
+    rng = _rng(20 + h + d + n)
+    W = list(_weights(rng, h, d))
+    K, V = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    eta = rng.uniform(0.1, 2.0, n)
+    loss = lambda ws: float(_torch_loss(*ws, K, V, eta))
+    g = O.chunk_gradient(*W, K, V, eta)
+    step = 1e-6
+    for j in range(3):
+        fd = np.zeros_like(W[j])
+        for idx in np.ndindex(*W[j].shape):
+            wp = [w.copy() for w in W]; wm = [w.copy() for w in W]
+            wp[j][idx] += step; wm[j][idx] -= step
+            fd[idx] = (loss(wp) - loss(wm)) / (2 * step)
+        err = np.max(np.abs(fd - g[j])) / np.max(np.abs(g[j]))
+        assert err < 1e-7, (j, err)
+
+
+def test_gradient_is_additive_over_token_shards():
+    """§3.4: the chunk gradient is a sum over its tokens, so shards add up."""
+    rng = _rng(3)
+    h, d, n = 6, 4, 23
+    W = _weights(rng, h, d)
+    K, V, eta = _tokens(rng, n, d), _tokens(rng, n, d), rng.uniform(0, 0.1, n)
+    full = O.chunk_gradient(*W, K, V, eta)
+    cuts = [0, 5, 6, 17, n]
+    parts = [O.chunk_gradient(*W, K[a:b], V[a:b], eta[a:b]) for a, b in zip(cuts[:-1], cuts[1:])]
+    for j in range(3):
+        np.testing.assert_allclose(sum(p[j] for p in parts), full[j], rtol=1e-12, atol=1e-15)
+    blocked = O.chunk_gradient(*W, K, V, eta, token_block=4)   # reading R7
+    for j in range(3):
+        np.testing.assert_allclose(blocked[j], full[j], rtol=1e-12, atol=1e-15)
+
+
+def test_gradient_token_permutation_invariance():
+    """A chunk is a set of tokens: permuting (k, v, eta) leaves the gradient unchanged."""
+    rng = _rng(4)
+    W = _weights(rng, 5, 6)
+    K, V, eta = _tokens(rng, 11, 6), _tokens(rng, 11, 6), rng.uniform(0, 0.1, 11)
+    p = rng.permutation(11)
+    a = O.chunk_gradient(*W, K, V, eta)
+    b = O.chunk_gradient(*W, K[p], V[p], eta[p])
+    for j in range(3):
+        np.testing.assert_allclose(a[j], b[j], rtol=1e-12, atol=1e-16)
+
+
+# ----------------------------------------------------------------------------- Newton-Schulz
+
+
+def _golden_ns():
+    vals = {}
+    with open(os.path.join(GOLDEN, "ns_coefficients.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                k, v = line.split()
+                vals[k] = float(v)
+    return vals
+
+
+def test_ns_coefficients_match_paper():
+    g = _golden_ns()
+    assert O.NS_COEFFS == (g["a"], g["b"], g["c"])
+    assert O.NS_STEPS_DEFAULT == int(g["steps"])
+
+
+def _scalar_quintic(s, steps):
+    g = _golden_ns()
+    for _ in range(steps):
+        s = g["a"] * s + g["b"] * s ** 3 + g["c"] * s ** 5
+    return s
+
+
+@pytest.mark.parametrize("shape", [(5, 8), (8, 5), (6, 6), (1, 4)])
+@pytest.mark.parametrize("steps", [0, 1, 5])
+def test_ns_commutes_with_svd(shape, steps):
+    """NS acts on singular values only: NS(G) = U p^T(S / (||G||_F + eps)) V^T."""
+    rng = _rng(5 + shape[0] * 10 + shape[1])
+    G = rng.standard_normal(shape)
+    U, S, Vt = np.linalg.svd(G, full_matrices=False)
+    s = _scalar_quintic(S / (np.linalg.norm(G) + O.NS_EPS), steps)
+    ref = (U * s) @ Vt
+    np.testing.assert_allclose(O.newton_schulz(G, steps), ref, rtol=1e-10, atol=1e-12)
+
+
+def test_ns_rank_one_closed_form():
+    rng = _rng(6)
+    u = rng.standard_normal(7); u /= np.linalg.norm(u)
+    v = rng.standard_normal(3); v /= np.linalg.norm(v)
+    G = 2.5 * np.outer(u, v)
+    p5 = _scalar_quintic(2.5 / (2.5 + O.NS_EPS), 5)
+    np.testing.assert_allclose(O.newton_schulz(G, 5), p5 * np.outer(u, v), rtol=1e-12, atol=1e-14)
+    assert abs(p5 - 0.6964) < 1e-3
+
+
+@pytest.mark.parametrize("shape", [(16, 32), (32, 16), (24, 64)])
+def test_ns_spectrum_near_one(shape):
+    """Muon(g) ~ U V^T: the singular values of the 5-step output sit near 1."""
+    rng = _rng(7 + shape[0])
+    G = rng.standard_normal(shape)
+    s = np.linalg.svd(O.newton_schulz(G, 5), compute_uv=False)
+    assert s.min() > 0.6 and s.max() < 1.2, s
+
+
+def test_ns_zero_gradient_is_zero():
+    assert np.all(O.newton_schulz(np.zeros((4, 6)), 5) == 0.0)   # reading R3
+
+
+# ----------------------------------------------------------------------------- weight update
+
+
+def test_weight_update_preserves_row_norms_nonsquare():
+    rng = _rng(8)
+    W = rng.standard_normal((7, 4)) * 3.0
+    g = rng.standard_normal((7, 4))
+    Wn = O.weight_update(W, g)
+    np.testing.assert_allclose(np.linalg.norm(Wn, axis=1), np.linalg.norm(W, axis=1), rtol=1e-13)
+    # direction of every row is that of W - g
+    U = W - g
+    cos = np.sum(Wn * U, axis=1) / (np.linalg.norm(Wn, axis=1) * np.linalg.norm(U, axis=1))
+    np.testing.assert_allclose(cos, 1.0, rtol=1e-13)
+
+
+# ----------------------------------------------------------------------------- layer
+
+
+def _layer_inputs(seed, n_q, n_kv, d, h, unit=True, eta_scale=0.05):
+    rng = _rng(seed)
+    W = _weights(rng, h, d, unit=unit, scale=1 / np.sqrt(d))
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = eta_scale * np.log1p(np.exp(rng.standard_normal(n_kv)))
+    return q, k, v, eta, W
+
+
+@pytest.mark.parametrize("order", [0, 1])
+@pytest.mark.parametrize("muon", [0, 1])
+def test_eta_zero_layer_is_plain_swiglu_mlp(order, muon):
+    q, k, v, eta, W = _layer_inputs(9, 40, 33, 6, 10)
+    o, Wf = O.lact_forward_instance(q, k, v, np.zeros_like(eta), *W, chunk=8, order=order,
+                                    use_muon=bool(muon), ns_steps=5)
+    np.testing.assert_allclose(o, _torch_swiglu(*W, q).numpy(), rtol=1e-13, atol=1e-14)
+    for a, b in zip(Wf, W):
+        np.testing.assert_allclose(a, b, rtol=1e-14, atol=1e-16)
+
+
+@pytest.mark.parametrize("muon", [0, 1])
+def test_row_norms_after_every_update(muon):
+    q, k, v, eta, W = _layer_inputs(10, 30, 30, 5, 9, unit=False, eta_scale=0.5)
+    W = tuple(w * np.arange(1, w.shape[0] + 1)[:, None] for w in W)   # distinct norms
+    trace = []
+    _, Wf = O.lact_forward_instance(q, k, v, eta, *W, chunk=7, order=0, use_muon=bool(muon),
+                                    trace=trace)
+    for Ws in trace[1:] + [Wf]:
+        for a, b in zip(Ws, W):
+            np.testing.assert_allclose(np.linalg.norm(a, axis=1), np.linalg.norm(b, axis=1),
+                                       rtol=1e-12)
+    q, k, v, eta, Wu = _layer_inputs(11, 30, 30, 5, 9, unit=True, eta_scale=0.5)
+    _, Wf = O.lact_forward_instance(q, k, v, eta, *Wu, chunk=7, order=1, use_muon=bool(muon))
+    for a in Wf:
+        np.testing.assert_allclose(np.linalg.norm(a, axis=1), 1.0, rtol=1e-12)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_dependency_mask(order):
+    """Apply-then-update is shifted block-causal, update-then-apply block-causal;
+    the tail sees every key (§3.1, execution orders)."""
+    C, n_kv, n_q = 4, 12, 15
+    q, k, v, eta, W = _layer_inputs(12, n_q, n_kv, 4, 6, eta_scale=0.5)
+    o0, _ = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=order)
+    for j in range(n_kv):
+        k2 = k.copy(); k2[j] += 0.3
+        o1, _ = O.lact_forward_instance(q, k2, v, eta, *W, chunk=C, order=order)
+        changed = np.any(np.abs(o1 - o0) > 1e-13, axis=1)
+        for i in range(n_q):
+            if i >= n_kv:
+                expect = True
+            elif order == 0:
+                expect = j // C < i // C
+            else:
+                expect = j // C <= i // C
+            assert changed[i] == expect, (order, i, j)
+
+
+def test_single_chunk_orders():
+    q, k, v, eta, W = _layer_inputs(13, 10, 10, 4, 8, eta_scale=0.5)
+    o0, W0f = O.lact_forward_instance(q, k, v, eta, *W, chunk=10, order=0)
+    o1, W1f = O.lact_forward_instance(q, k, v, eta, *W, chunk=10, order=1)
+    np.testing.assert_allclose(o0, _torch_swiglu(*W, q).numpy(), rtol=1e-13)
+    np.testing.assert_allclose(o1, _torch_swiglu(*W1f, q).numpy(), rtol=1e-13)
+    for a, b in zip(W0f, W1f):
+        np.testing.assert_allclose(a, b, rtol=1e-14)
+
+
+def test_query_permutation_within_chunk_permutes_output():
+    q, k, v, eta, W = _layer_inputs(14, 16, 16, 4, 6, eta_scale=0.5)
+    p = np.concatenate([np.arange(8), 8 + _rng(0).permutation(8)])
+    o, _ = O.lact_forward_instance(q, k, v, eta, *W, chunk=8, order=0)
+    op, _ = O.lact_forward_instance(q[p], k, v, eta, *W, chunk=8, order=0)
+    np.testing.assert_allclose(op, o[p], rtol=1e-13)
+
+
+@pytest.mark.parametrize("muon", [0, 1])
+def test_resume_from_returned_state(muon):
+    """The fast weight is the only state carried between chunks (§3, Fig. 2)."""
+    q, k, v, eta, W = _layer_inputs(15, 24, 24, 5, 7, eta_scale=0.3)
+    o, Wf = O.lact_forward_instance(q, k, v, eta, *W, chunk=6, order=0, use_muon=bool(muon))
+    oa, Wa = O.lact_forward_instance(q[:12], k[:12], v[:12], eta[:12], *W, chunk=6, order=0,
+                                     use_muon=bool(muon))
+    ob, Wb = O.lact_forward_instance(q[12:], k[12:], v[12:], eta[12:], *Wa, chunk=6, order=0,
+                                     use_muon=bool(muon))
+    np.testing.assert_allclose(np.concatenate([oa, ob]), o, rtol=1e-12, atol=1e-15)
+    for a, b in zip(Wb, Wf):
+        np.testing.assert_allclose(a, b, rtol=1e-12)
+
+
+def test_ns_is_scale_free():
+    """Muon normalises the absolute scale of the gradient (§3.2): without the
+    reading-R3 epsilon NS(alpha G) == NS(G) exactly up to rounding."""
+    rng = _rng(16)
+    G = rng.standard_normal((6, 9))
+    for alpha in (1e-3, 0.5, 40.0):
+        np.testing.assert_allclose(O.newton_schulz(alpha * G, 5, eps=0.0),
+                                   O.newton_schulz(G, 5, eps=0.0), rtol=1e-12, atol=1e-14)
+
+
+def test_muon_makes_lr_scale_irrelevant():
+    """With Muon, eta only sets the relative weight of tokens in a chunk (§3.2);
+    the only scale left is the 1e-7 of reading R3, amplified at most a^5 ~ 484x."""
+    q, k, v, eta, W = _layer_inputs(16, 20, 20, 6, 6, eta_scale=5.0)
+    _, Wa = O.lact_forward_instance(q, k, v, eta, *W, chunk=10, order=0, use_muon=True)
+    for alpha in (0.5, 4.0):
+        _, Wb = O.lact_forward_instance(q, k, v, alpha * eta, *W, chunk=10, order=0, use_muon=True)
+        for a, b in zip(Wa, Wb):
+            np.testing.assert_allclose(a, b, rtol=1e-3, atol=1e-4)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_chunk_one_is_per_token_ttt(order):
+    """Chunk size 1 is the per-token TTT layer of §2.1 (update eq. per token, then
+    the normalised step), computed here with autograd in a separate loop."""
+    n, d, h = 9, 4, 5
+    q, k, v, eta, W = _layer_inputs(17, n, n, d, h, eta_scale=0.7)
+    o_ref = np.zeros((n, d))
+    tw = [torch.tensor(w) for w in W]
+    for i in range(n):
+        if order == 0:
+            o_ref[i] = F.linear(F.silu(F.linear(torch.as_tensor(q[i]), tw[0])) *
+                                F.linear(torch.as_tensor(q[i]), tw[2]), tw[1]).numpy()
+        req = [w.clone().requires_grad_(True) for w in tw]
+        _torch_loss(*req, torch.as_tensor(k[i:i + 1]), torch.as_tensor(v[i:i + 1]),
+                    torch.as_tensor(eta[i:i + 1])).backward()
+        new = []
+        for w, r in zip(tw, req):
+            u = w - r.grad
+            new.append(u / u.norm(dim=1, keepdim=True) * w.norm(dim=1, keepdim=True))
+        tw = new
+        if order == 1:
+            o_ref[i] = F.linear(F.silu(F.linear(torch.as_tensor(q[i]), tw[0])) *
+                                F.linear(torch.as_tensor(q[i]), tw[2]), tw[1]).numpy()
+    o, Wf = O.lact_forward_instance(q, k, v, eta, *W, chunk=1, order=order)
+    np.testing.assert_allclose(o, o_ref, rtol=1e-11, atol=1e-14)
+    for a, b in zip(Wf, tw):
+        np.testing.assert_allclose(a, b.numpy(), rtol=1e-11)
+
+
+def test_partial_last_chunk_and_tail():
+    q, k, v, eta, W = _layer_inputs(18, 19, 13, 4, 6, eta_scale=0.4)
+    o, Wf = O.lact_forward_instance(q, k, v, eta, *W, chunk=5, order=0)
+    # chunks [0,5) [5,10) [10,13): the last partial chunk still updates W
+    Wm = tuple(W)
+    for s, e in ((0, 5), (5, 10), (10, 13)):
+        Wm = O.update(Wm, k[s:e], v[s:e], eta[s:e])
+    for a, b in zip(Wf, Wm):
+        np.testing.assert_allclose(a, b, rtol=1e-13)
+    np.testing.assert_allclose(o[13:], _torch_swiglu(*Wm, q[13:]).numpy(), rtol=1e-13)
+
+
+# ----------------------------------------------------------------------------- flops
+
+
+def test_layer_flops_match_paper_counts():
+    vals = {}
+    with open(os.path.join(GOLDEN, "flops_per_token.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                a, b = line.split()
+                vals[a] = float(b)
+    d, h = 64, 64
+    assert O.layer_flops(1, d, h, 1, 1, 1) == vals["total"] * d * h
+    assert O.layer_flops(1, d, h, 0, 1, 1) == vals["query_apply"] * d * h
+    assert O.layer_flops(1, d, h, 1, 0, 1) == (vals["key_forward"] + vals["gradients"]) * d * h
+    for r in (1, 2):
+        m = 32
+        mu = O.layer_flops(1, m, r * m, 0, 0, 1, use_muon=True, ns_steps=1)
+        assert mu == 3 * vals[f"muon_r{r}_per_iter_over_m3"] * m ** 3

@@ -1,0 +1,157 @@
+"""Benchmark of the LaCT fast-weight layer forward on one MI355X.
+
+One step = one full forward of the layer's fast-weight path (every chunk:
+apply, key forward/backward, gradient contractions, weight update) over one
+batch of seeded synthetic input already resident in HBM. The fast weights
+carry over from step to step (a longer sequence of the same shape); the work
+per step does not depend on their values.
+
+Prints ONE JSON line (see the keys below). `value` is algorithmic TFLOP/s of
+the whole path (App. A FLOP count: 18*d*h per token per head, plus Muon);
+tokens/s and the fraction of the bf16 MFMA peak are reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "LaCT layer fwd TFLOP/s + tokens/s at 32K ctx; % of bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="lm32k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    return ap.parse_args()
+
+
+def describe(cfg):
+    order = "apply-then-update" if cfg.order == 0 else "update-then-apply"
+    muon = f", Muon {cfg.ns_steps} NS steps" if cfg.use_muon else ""
+    return (f"{cfg.name}: B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} n_kv={cfg.n_kv} n_q={cfg.n_q} "
+            f"chunk={cfg.chunk} {order}{muon}, io {cfg.io}, fp32 state")
+
+
+def cpu_baseline(cfg, min_seconds):
+    """The fp64 oracle, as it is, on a bounded sample of the same workload:
+    whole (b, h) instances (every chunk), one after another, until at least
+    `min_seconds` of host time have passed; timed on this host's cores."""
+    from threadpoolctl import threadpool_info
+    from lact_synth import make_inputs
+    from oracle import lact_oracle as O
+
+    done, dt = 0, 0.0
+    while done < cfg.BH and dt < min_seconds:
+        x = make_inputs(cfg, 0, heads=[done])
+        t0 = time.perf_counter()
+        O.lact_forward(x["q"], x["k"], x["v"], x["eta"], x["W1"], x["W2"], x["W3"], chunk=cfg.chunk,
+                       order=cfg.order, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps)
+        dt += time.perf_counter() - t0
+        done += 1
+    fl = done * O.layer_flops(1, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.n_chunks, bool(cfg.use_muon),
+                              cfg.ns_steps)
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {cfg.BH} (b,h) instances, all {cfg.n_chunks} chunks each "
+                      f"({done * cfg.n_q} tokens), fp64 NumPy, {dt:.1f} s",
+            "tokens_per_s": round(done * cfg.n_q / dt, 1)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2505_23884_amd as P
+    from lact_synth import CONFIGS, make_inputs
+
+    cfg = CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    x = make_inputs(cfg, 0)
+    io = torch.bfloat16 if cfg.io == "bf16" else torch.float32
+    sh = lambda a: a.reshape(cfg.B, cfg.H, *a.shape[1:])
+    q, k, v = (torch.from_numpy(sh(x[n])).to(dev, io) for n in ("q", "k", "v"))
+    eta = torch.from_numpy(sh(x["eta"])).to(dev, torch.float32)
+    W = [torch.from_numpy(sh(x[n])).to(dev, torch.float32) for n in ("W1", "W2", "W3")]
+    del x
+    out = torch.empty_like(q)
+    desc = P.binding.make_desc(cfg.B, cfg.H, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.chunk, cfg.order,
+                               cfg.use_muon, cfg.ns_steps, P.IO_BF16 if cfg.io == "bf16" else P.IO_FP32)
+    ws = torch.empty(P.workspace_bytes(desc), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        P.forward(q, k, v, eta, *W, chunk=cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
+                  ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=stream.cuda_stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / max(args.steps, 1)
+
+    from oracle.lact_oracle import layer_flops  # FLOP count only (App. A formula)
+    flops = layer_flops(cfg.BH, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.n_chunks, bool(cfg.use_muon),
+                        cfg.ns_steps)
+    tflops = flops / dt / 1e12
+    tokens = cfg.B * cfg.n_q
+    peak = PEAK_BF16_TFLOPS if cfg.io == "bf16" else PEAK_FP32_MFMA_TFLOPS
+    res = {
+        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if cfg.io == "bf16" else "fp32", "data": "synthetic",
+        "config": {"workload": describe(cfg), "tokens_per_step": tokens, "flops_per_step": flops},
+        "tokens_per_s": round(tokens / dt, 1),
+        "pct_of_peak": round(100.0 * tflops / peak, 2),
+    }
+
+    if not args.no_roofline:
+        P.timing_reset()
+        P.timing_enable(True)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        P.timing_enable(False)
+        per = {}
+        for kc, name in enumerate(P.KCLASS_NAMES):
+            n, ms, fl = P.timing_read(kc)
+            if n:
+                per[name] = {"launches": n, "avg_us": round(1e3 * ms / n, 3), "total_ms": round(ms, 4),
+                             "tflops": round(fl / (ms * 1e-3) / 1e12, 2) if ms > 0 and fl > 0 else None}
+        P.timing_reset()
+        dom = max(per, key=lambda kname: per[kname]["total_ms"])
+        d = per[dom]
+        achieved = d["tflops"] or 0.0
+        res["roofline"] = {"bound": "mfma", "kernel": f"lact {dom} kernel class",
+                           "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                           "frac": round(achieved / peak, 4), "traffic": None,
+                           "avg_launch_us": d["avg_us"], "per_class": per}
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

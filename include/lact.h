@@ -1,0 +1,143 @@
+/*
+ * lact.h -- C ABI of the MI355X (gfx950) LaCT fast-weight layer forward.
+ *
+ * The library computes, for every (batch, head) instance independently, the
+ * fast-weight path of a Large-Chunk Test-Time Training layer ("Test-Time
+ * Training Done Right", LaCT):
+ *
+ *   apply   o_i = f_W(q_i),  f_W(x) = W2 [SiLU(W1 x) o (W3 x)]
+ *           (§2.1 apply eq.; §3.1 SwiGLU eq.)
+ *   update  g = grad_W sum_{i in chunk} eta_i * (-f_W(k_i)^T v_i)
+ *           (§3.1 chunk-gradient and loss eqs.; Alg. 1, update)
+ *           W <- L2-Normalize(W - g) or L2-Normalize(W - Muon(g))     (§3.2)
+ *           with Muon(g) the Newton-Schulz quintic on g / (||g||_F + 1e-7),
+ *           coefficients (3.4445, -4.7750, 2.0315)          (App. A, Muon)
+ *           and the normalisation taken per row along the input dimension,
+ *           each row rescaled to the norm it had before the update (Alg. 1).
+ *   order   per chunk of `chunk` key tokens: apply-then-update (shifted
+ *           block-causal) or update-then-apply (block-causal)  (§3.1 orders)
+ *   tail    query tokens [n_kv, n_q) carry no key/value; they are applied
+ *           with the final fast weights (the novel-view-synthesis layout:
+ *           update on the input views, apply to the target views, §4).
+ *
+ * Math layout per instance: W1, W3 are h x d, W2 is d x h, row-major, fp32.
+ * The fast weights are the recurrent state; they are read and written in
+ * place, so the caller owns them as the checkpoint between calls.
+ *
+ * Conventions common to every entry point:
+ *  - Every pointer argument except `desc` and `stream` is a DEVICE pointer
+ *    owned by the caller; the library never frees or keeps it.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *    stream) and never synchronise the host, except when the environment
+ *    variable LACT_SYNC=1 is set (debugging).
+ *  - No allocation happens inside lact_forward: all scratch memory is the
+ *    caller's `workspace`.
+ *  - Arguments are validated before any HIP call, so every error below is
+ *    reported without touching the GPU. Errors are negative return codes;
+ *    nothing is thrown across the ABI. On an error no output is written.
+ *  - Inputs must not alias `o` or `workspace`.
+ */
+#ifndef LACT_H_
+#define LACT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define LACT_OK 0
+#define LACT_EINVAL (-1)        /* bad descriptor value or NULL pointer            */
+#define LACT_EALIGN (-2)        /* a tensor pointer is not 16-byte aligned          */
+#define LACT_EWORKSPACE (-3)    /* workspace NULL or smaller than required          */
+#define LACT_EUNSUPPORTED (-4)  /* shape outside the kernels' envelope (see below)  */
+#define LACT_EHIP (-5)          /* a HIP call failed; lact_last_hip_error() has it   */
+
+/* lact_desc.order */
+#define LACT_APPLY_THEN_UPDATE 0
+#define LACT_UPDATE_THEN_APPLY 1
+
+/* lact_desc.io_dtype: element type of q, k, v and o. eta and W are fp32. */
+#define LACT_IO_BF16 0          /* bf16 MFMA operands, fp32 accumulate, fp32 state */
+#define LACT_IO_FP32 1          /* fp32 MFMA throughout                            */
+
+typedef struct lact_desc {
+  int32_t B, H;       /* batch and heads; instances = B*H, all independent      */
+  int32_t d, h;       /* head dim and fast-weight hidden dim; envelope:         */
+                      /* multiples of 8 in [8, 4096]                            */
+  int64_t n_kv;       /* tokens carrying k, v, eta (>= 0)                       */
+  int64_t n_q;        /* tokens carrying q (>= n_kv)                            */
+  int64_t chunk;      /* key tokens per update (>= 1); the last chunk may be    */
+                      /* partial                                                 */
+  int32_t order;      /* LACT_APPLY_THEN_UPDATE or LACT_UPDATE_THEN_APPLY       */
+  int32_t use_muon;   /* 0 or 1                                                  */
+  int32_t ns_steps;   /* Newton-Schulz iterations when use_muon, in [0, 16]     */
+  int32_t io_dtype;   /* LACT_IO_BF16 or LACT_IO_FP32                           */
+} lact_desc;
+
+/*
+ * Bytes of device workspace lact_forward needs for `desc` (a pure function of
+ * the descriptor). Returns 0 and sets *err (if err != NULL) to a negative code
+ * when the descriptor is invalid; *err = LACT_OK otherwise.
+ */
+size_t lact_workspace_bytes(const lact_desc* desc, int* err);
+
+/* Validate a descriptor without running anything: LACT_OK or an error code. */
+int lact_check_desc(const lact_desc* desc);
+
+/*
+ * The layer's fast-weight path, all chunks, on `stream`.
+ *
+ *   q    [B*H, n_q,  d]  io_dtype, row-major (token rows)      in
+ *   k    [B*H, n_kv, d]  io_dtype                               in
+ *   v    [B*H, n_kv, d]  io_dtype                               in
+ *   eta  [B*H, n_kv]     fp32, per-token learning rate          in
+ *   W1   [B*H, h, d]     fp32   initial fast weights in, final fast weights out
+ *   W2   [B*H, d, h]     fp32   (updated in place)
+ *   W3   [B*H, h, d]     fp32
+ *   o    [B*H, n_q, d]   io_dtype, every element written        out
+ *   workspace            >= lact_workspace_bytes(desc), 256-byte aligned
+ *
+ * q, k, v are used as given (the layer's per-token L2 normalisation of q and
+ * k happens before this path, Alg. 1). Returns LACT_OK or an error code;
+ * kernel faults surface asynchronously on the stream like any HIP kernel.
+ */
+int lact_forward(const lact_desc* desc,
+                 const void* q, const void* k, const void* v, const float* eta,
+                 float* W1, float* W2, float* W3,
+                 void* o,
+                 void* workspace, size_t workspace_bytes,
+                 void* stream);
+
+/*
+ * Kernel timing (instrumentation for benchmarks). While enabled, lact_forward
+ * brackets every kernel launch with HIP events on its stream, grouped by
+ * kernel class (LACT_KCLASS_*). lact_timing_read synchronises on the recorded
+ * events and returns the number of launches, their summed duration in
+ * milliseconds and their summed algorithmic FLOPs. Not thread-safe; at most
+ * 65536 launches are recorded between resets (later ones are not timed).
+ */
+#define LACT_KCLASS_FWD 0      /* apply GEMM-1 and key forward + hidden backward */
+#define LACT_KCLASS_BWD 1      /* apply GEMM-2 and the gradient contractions      */
+#define LACT_KCLASS_UPDATE 2   /* weight update, row norms, bf16 operand copies   */
+#define LACT_KCLASS_NS 3       /* Newton-Schulz (Muon) kernels                    */
+#define LACT_KCLASS_PREP 4     /* initial fp32 -> bf16 operand copies             */
+#define LACT_KCLASS_COUNT 5
+int lact_timing_enable(int enable);
+int lact_timing_reset(void);
+int lact_timing_read(int kclass, int64_t* launches, double* total_ms, double* flops);
+
+/* Message for a return code (static storage). */
+const char* lact_strerror(int code);
+/* Last HIP error string seen by the library in this thread ("" if none). */
+const char* lact_last_hip_error(void);
+/* Library version string, e.g. "lact-gfx950 0.1.0". */
+const char* lact_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LACT_H_ */

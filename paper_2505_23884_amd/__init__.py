@@ -1,0 +1,12 @@
+"""MI355X (gfx950) LaCT fast-weight layer forward.
+
+Thin ctypes binding over ``liblact.so`` (see ``include/lact.h``): it only
+marshals torch tensors into device pointers, picks the current HIP stream and
+allocates the workspace. Every step of the path runs in the library's HIP
+kernels; there is no CPU or PyTorch fallback.
+"""
+from .binding import (  # noqa: F401
+    LactError, LactDesc, lib, load_library, workspace_bytes, forward, check_desc,
+    timing_enable, timing_reset, timing_read, KCLASS_NAMES,
+    APPLY_THEN_UPDATE, UPDATE_THEN_APPLY, IO_BF16, IO_FP32,
+)

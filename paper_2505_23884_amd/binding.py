@@ -1,0 +1,169 @@
+"""ctypes binding of liblact.so with the names of the C ABI (include/lact.h)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liblact.so")
+
+APPLY_THEN_UPDATE, UPDATE_THEN_APPLY = 0, 1
+IO_BF16, IO_FP32 = 0, 1
+KCLASS_NAMES = ("fwd", "bwd", "update", "ns", "prep")
+
+_ERRORS = {0: "LACT_OK", -1: "LACT_EINVAL", -2: "LACT_EALIGN", -3: "LACT_EWORKSPACE",
+           -4: "LACT_EUNSUPPORTED", -5: "LACT_EHIP"}
+
+
+class LactError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class LactDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("h", ctypes.c_int32), ("n_kv", ctypes.c_int64), ("n_q", ctypes.c_int64),
+                ("chunk", ctypes.c_int64), ("order", ctypes.c_int32), ("use_muon", ctypes.c_int32),
+                ("ns_steps", ctypes.c_int32), ("io_dtype", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str | None = None):
+    """Load liblact.so (raises if it has not been built: there is no fallback)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise LactError(-5, f"{p} is missing; build it with paper_2505_23884_amd.build.build()")
+    L = ctypes.CDLL(p)
+    vp, sz, i32, i64 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int64
+    dp = ctypes.POINTER(LactDesc)
+    L.lact_workspace_bytes.argtypes = [dp, ctypes.POINTER(i32)]
+    L.lact_workspace_bytes.restype = sz
+    L.lact_check_desc.argtypes = [dp]
+    L.lact_check_desc.restype = i32
+    L.lact_forward.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.lact_forward.restype = i32
+    L.lact_timing_enable.argtypes = [i32]
+    L.lact_timing_enable.restype = i32
+    L.lact_timing_reset.argtypes = []
+    L.lact_timing_reset.restype = i32
+    L.lact_timing_read.argtypes = [i32, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(ctypes.c_double)]
+    L.lact_timing_read.restype = i32
+    for f in ("lact_strerror",):
+        getattr(L, f).argtypes = [i32]
+        getattr(L, f).restype = ctypes.c_char_p
+    for f in ("lact_last_hip_error", "lact_version"):
+        getattr(L, f).argtypes = []
+        getattr(L, f).restype = ctypes.c_char_p
+    if path is None:
+        _lib = L
+    return L
+
+
+def lib():
+    return load_library()
+
+
+def _raise(code: int):
+    L = lib()
+    msg = L.lact_strerror(code).decode()
+    if code == -5:
+        msg += ": " + L.lact_last_hip_error().decode()
+    raise LactError(code, msg)
+
+
+def make_desc(B, H, d, h, n_kv, n_q, chunk, order=0, use_muon=False, ns_steps=5, io_dtype=IO_BF16):
+    return LactDesc(int(B), int(H), int(d), int(h), int(n_kv), int(n_q), int(chunk), int(order),
+                    int(bool(use_muon)), int(ns_steps), int(io_dtype))
+
+
+def check_desc(desc: LactDesc) -> int:
+    return lib().lact_check_desc(ctypes.byref(desc))
+
+
+def workspace_bytes(desc: LactDesc) -> int:
+    err = ctypes.c_int(0)
+    n = lib().lact_workspace_bytes(ctypes.byref(desc), ctypes.byref(err))
+    if err.value:
+        _raise(err.value)
+    return int(n)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def forward(q, k, v, eta, W1, W2, W3, chunk, order=APPLY_THEN_UPDATE, use_muon=False,
+            ns_steps=5, out=None, workspace=None, stream=None):
+    """LaCT fast-weight path on the GPU (see include/lact.h for the semantics).
+
+    q [B, H, n_q, d] (or [BH, n_q, d]); k, v [.., n_kv, d]; bf16 or fp32 (same dtype);
+    eta [.., n_kv] fp32; W1, W3 [.., h, d], W2 [.., d, h] fp32, updated IN PLACE.
+    Returns o with q's shape and dtype. Runs on torch's current stream unless a
+    stream is given; allocates the workspace unless one is passed.
+    """
+    import torch
+    if q.dim() == 4:
+        B, H = q.shape[0], q.shape[1]
+    elif q.dim() == 3:
+        B, H = q.shape[0], 1
+    else:
+        raise LactError(-1, "q must be [B, H, n_q, d] or [BH, n_q, d]")
+    n_q, d = q.shape[-2], q.shape[-1]
+    n_kv = k.shape[-2]
+    h = W1.shape[-2]
+    if q.dtype == torch.bfloat16:
+        io = IO_BF16
+    elif q.dtype == torch.float32:
+        io = IO_FP32
+    else:
+        raise LactError(-1, f"unsupported q dtype {q.dtype}")
+    for t, name in ((q, "q"), (k, "k"), (v, "v"), (eta, "eta"), (W1, "W1"), (W2, "W2"), (W3, "W3")):
+        if not t.is_cuda or not t.is_contiguous():
+            raise LactError(-1, f"{name} must be a contiguous device tensor")
+    if k.dtype != q.dtype or v.dtype != q.dtype:
+        raise LactError(-1, "q, k, v must share one dtype")
+    if eta.dtype != torch.float32 or any(w.dtype != torch.float32 for w in (W1, W2, W3)):
+        raise LactError(-1, "eta and the fast weights are fp32")
+    BH = B * H
+    if (k.numel() != BH * n_kv * d or v.numel() != BH * n_kv * d or eta.numel() != BH * n_kv
+            or W1.numel() != BH * h * d or W3.numel() != BH * h * d or W2.numel() != BH * d * h
+            or W2.shape[-2] != d or W2.shape[-1] != h or W1.shape[-1] != d):
+        raise LactError(-1, "inconsistent tensor shapes")
+    desc = make_desc(B, H, d, h, n_kv, n_q, chunk, order, use_muon, ns_steps, io)
+    nbytes = workspace_bytes(desc)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device).cuda_stream
+    rc = lib().lact_forward(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(W1),
+                            _ptr(W2), _ptr(W3), _ptr(out), _ptr(workspace),
+                            ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                            ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return out
+
+
+def timing_enable(on: bool = True):
+    lib().lact_timing_enable(int(on))
+
+
+def timing_reset():
+    lib().lact_timing_reset()
+
+
+def timing_read(kclass: int):
+    n, ms, fl = ctypes.c_int64(0), ctypes.c_double(0), ctypes.c_double(0)
+    rc = lib().lact_timing_read(int(kclass), ctypes.byref(n), ctypes.byref(ms), ctypes.byref(fl))
+    if rc:
+        _raise(rc)
+    return int(n.value), float(ms.value), float(fl.value)

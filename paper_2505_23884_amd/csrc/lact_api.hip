@@ -1,0 +1,453 @@
+// Host side of the C ABI: validation, workspace layout, the chunk schedule
+// and kernel timing. Everything in here runs on the host; all arithmetic of
+// the path runs in lact_kernels.hip.
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "lact.h"
+#include "lact_internal.h"
+
+namespace lact {
+namespace {
+
+thread_local char g_hip_err[256] = "";
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Shape-derived plan shared by lact_workspace_bytes and lact_forward.
+struct Plan {
+  int BH, d, h;
+  bool bf16;
+  int esz;
+  int64_t C;          // tokens of the largest chunk (0 when n_kv == 0)
+  int64_t cap;        // rows of the applied-hidden buffer
+  int nsplit;         // split-K ways of the gradient contraction
+  int64_t split_len;  // tokens per split
+  // workspace offsets (bytes)
+  size_t off_wb[3], off_hq, off_upd[3], off_step, total;
+};
+
+int check_desc(const lact_desc* d) {
+  if (!d) return LACT_EINVAL;
+  if (d->B < 1 || d->H < 1) return LACT_EINVAL;
+  if (d->n_kv < 0 || d->n_q < d->n_kv || d->chunk < 1) return LACT_EINVAL;
+  if (d->order != LACT_APPLY_THEN_UPDATE && d->order != LACT_UPDATE_THEN_APPLY) return LACT_EINVAL;
+  if (d->use_muon != 0 && d->use_muon != 1) return LACT_EINVAL;
+  if (d->ns_steps < 0 || d->ns_steps > 16) return LACT_EINVAL;
+  if (d->io_dtype != LACT_IO_BF16 && d->io_dtype != LACT_IO_FP32) return LACT_EINVAL;
+  if (d->d < 1 || d->h < 1) return LACT_EINVAL;
+  if (d->d % 8 || d->h % 8 || d->d > kMaxDim || d->h > kMaxDim) return LACT_EUNSUPPORTED;
+  if ((int64_t)d->B * d->H > (1 << 20)) return LACT_EUNSUPPORTED;
+  if (d->n_q > ((int64_t)1 << 40)) return LACT_EUNSUPPORTED;
+  if (d->use_muon) return LACT_EUNSUPPORTED;   // Newton-Schulz kernels: not in this build yet
+  return LACT_OK;
+}
+
+Plan make_plan(const lact_desc* dsc) {
+  Plan p{};
+  p.BH = dsc->B * dsc->H;
+  p.d = dsc->d;
+  p.h = dsc->h;
+  p.bf16 = dsc->io_dtype == LACT_IO_BF16;
+  p.esz = p.bf16 ? 2 : 4;
+  p.C = std::min<int64_t>(dsc->chunk, dsc->n_kv);
+  const int64_t tail = dsc->n_q - dsc->n_kv;
+  // The applied-hidden buffer holds one chunk plus (bounded) tail rows so that
+  // update-then-apply can apply its last chunk together with the tail.
+  p.cap = std::min<int64_t>(dsc->n_q, p.C + std::min<int64_t>(tail, std::max<int64_t>(p.C, 65536)));
+  if (p.cap < 1) p.cap = 1;
+  // Split-K of the gradient contraction: enough blocks to fill the chip
+  // (~512), each split at least 256 tokens, lengths a multiple of 32.
+  const int64_t tiles = (int64_t)p.BH * 2 * cdiv(p.h, kTile) * cdiv(p.d, kTile);
+  int64_t ns = std::max<int64_t>(1, cdiv(512, tiles));
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.C / 256));
+  ns = std::min<int64_t>(ns, kMaxSplit);
+  p.split_len = std::max<int64_t>(32, cdiv(cdiv(std::max<int64_t>(p.C, 1), ns), 32) * 32);
+  p.nsplit = (int)std::max<int64_t>(1, cdiv(std::max<int64_t>(p.C, 1), p.split_len));
+  const size_t dh = (size_t)p.d * p.h;
+  size_t o = 0;
+  for (int m = 0; m < 3; ++m) {
+    p.off_wb[m] = o;
+    if (p.bf16) o = align_up(o + (size_t)p.BH * dh * 2);
+  }
+  p.off_hq = o;
+  o = align_up(o + (size_t)p.BH * p.cap * p.h * p.esz);
+  for (int m = 0; m < 3; ++m) {
+    p.off_upd[m] = o;
+    o = align_up(o + (size_t)p.BH * std::max<int64_t>(p.C, 1) * p.h * p.esz);
+  }
+  p.off_step = o;
+  o = align_up(o + (size_t)p.nsplit * p.BH * 3 * dh * 4);
+  p.total = o;
+  return p;
+}
+
+bool misaligned(const void* p) { return ((uintptr_t)p & 15) != 0; }
+
+// ---------------------------------------------------------------- timing
+struct TimedLaunch {
+  hipEvent_t a, b;
+  int kclass;
+  double flops;
+};
+struct Timing {
+  bool enabled = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<TimedLaunch> pending;
+  int64_t launches[LACT_KCLASS_COUNT] = {};
+  double ms[LACT_KCLASS_COUNT] = {};
+  double flops[LACT_KCLASS_COUNT] = {};
+};
+Timing g_timing;
+constexpr size_t kMaxTimed = 65536;
+
+hipEvent_t pool_event() {
+  if (!g_timing.pool.empty()) {
+    hipEvent_t e = g_timing.pool.back();
+    g_timing.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+int record_hip(hipError_t e) {
+  if (e == hipSuccess) return LACT_OK;
+  snprintf(g_hip_err, sizeof g_hip_err, "%s", hipGetErrorString(e));
+  return LACT_EHIP;
+}
+
+// Runs `launch` on `s`, bracketed by events when timing is enabled.
+template <class F>
+int timed(int kclass, double flops, hipStream_t s, F&& launch) {
+  hipEvent_t ea = nullptr, eb = nullptr;
+  const bool t = g_timing.enabled && g_timing.pending.size() < kMaxTimed;
+  if (t) {
+    ea = pool_event();
+    eb = pool_event();
+    if (ea && eb && hipEventRecord(ea, s) != hipSuccess) ea = nullptr;
+  }
+  int rc = record_hip(launch());
+  if (t && ea && eb && hipEventRecord(eb, s) == hipSuccess)
+    g_timing.pending.push_back({ea, eb, kclass, flops});
+  if (rc == LACT_OK && getenv("LACT_SYNC") && getenv("LACT_SYNC")[0] == '1')
+    rc = record_hip(hipStreamSynchronize(s));
+  return rc;
+}
+
+// ---------------------------------------------------------------- schedule
+struct Ctx {
+  const lact_desc* dsc;
+  Plan p;
+  const uint8_t *q, *k, *v;
+  const float* eta;
+  float* W[3];
+  uint8_t* o;
+  uint8_t* ws;
+  hipStream_t s;
+  Operand wop[3];   // operand copies of W1, W2, W3 (bf16 copies or the fp32 state)
+};
+
+Operand op(const void* base, int64_t ld, int64_t inst) { return Operand{base, ld, inst}; }
+
+// Applies the current fast weights to query rows [s0, s1), in pieces that fit.
+int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
+  const Plan& p = c.p;
+  for (int64_t a = s0; a < s1; a += p.cap) {
+    const int64_t n = std::min<int64_t>(p.cap, s1 - a);
+    FwdArgs f{};
+    FwdSeg& g = f.seg[0];
+    g.kind = FWD_APPLY;
+    g.tiles_m = (int)cdiv(n, kTile);
+    g.tiles_n = (int)cdiv(p.h, kTile);
+    g.nblocks = p.BH * g.tiles_m * g.tiles_n;
+    g.rows = n;
+    g.a0 = op(c.q + a * p.d * p.esz, p.d, c.dsc->n_q * p.d);
+    g.out0 = c.ws + p.off_hq;
+    g.out_inst = p.cap * p.h;
+    f.nseg = 1;
+    f.total_blocks = g.nblocks;
+    f.d = p.d;
+    f.h = p.h;
+    f.w1 = c.wop[0];
+    f.w2 = c.wop[1];
+    f.w3 = c.wop[2];
+    const double fl1 = 4.0 * p.BH * n * p.d * p.h;
+    int rc = timed(LACT_KCLASS_FWD, fl1, c.s, [&] { return launch_fwd(f, p.bf16, c.s); });
+    if (rc) return rc;
+    BwdArgs b{};
+    BwdSeg& o = b.seg[0];
+    o.kind = BWD_OUT;
+    o.tiles_m = (int)cdiv(n, kTile);
+    o.tiles_n = (int)cdiv(p.d, kTile);
+    o.nsplit = 1;
+    o.nblocks = p.BH * o.tiles_m * o.tiles_n;
+    o.rows = n;
+    o.a0 = op(c.ws + p.off_hq, p.h, p.cap * p.h);
+    o.b0 = c.wop[1];
+    o.out = c.o + a * p.d * p.esz;
+    o.out_inst = c.dsc->n_q * p.d;
+    b.nseg = 1;
+    b.total_blocks = o.nblocks;
+    b.d = p.d;
+    b.h = p.h;
+    rc = timed(LACT_KCLASS_BWD, 2.0 * p.BH * n * p.d * p.h, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
+    if (rc) return rc;
+  }
+  return LACT_OK;
+}
+
+// One update on key rows [s0, s1); with apply_too, the same launches also
+// apply the current (pre-update) weights to query rows [s0, s1).
+int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
+  const Plan& p = c.p;
+  const int64_t n = s1 - s0;
+  const int64_t dh = (int64_t)p.d * p.h;
+  FwdArgs f{};
+  int ns = 0;
+  if (apply_too) {
+    FwdSeg& g = f.seg[ns++];
+    g.kind = FWD_APPLY;
+    g.tiles_m = (int)cdiv(n, kTile);
+    g.tiles_n = (int)cdiv(p.h, kTile);
+    g.nblocks = p.BH * g.tiles_m * g.tiles_n;
+    g.rows = n;
+    g.a0 = op(c.q + s0 * p.d * p.esz, p.d, c.dsc->n_q * p.d);
+    g.out0 = c.ws + p.off_hq;
+    g.out_inst = p.cap * p.h;
+  }
+  {
+    FwdSeg& g = f.seg[ns++];
+    g.kind = FWD_UPDATE;
+    g.tiles_m = (int)cdiv(n, kTile);
+    g.tiles_n = (int)cdiv(p.h, kTile);
+    g.nblocks = p.BH * g.tiles_m * g.tiles_n;
+    g.rows = n;
+    g.a0 = op(c.k + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
+    g.a1 = op(c.v + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
+    g.out1 = c.ws + p.off_upd[0];
+    g.out2 = c.ws + p.off_upd[1];
+    g.out3 = c.ws + p.off_upd[2];
+    g.out_inst = p.C * p.h;
+    g.eta = c.eta + s0;
+    g.eta_inst = c.dsc->n_kv;
+  }
+  f.nseg = ns;
+  f.total_blocks = f.seg[0].nblocks + (ns > 1 ? f.seg[1].nblocks : 0);
+  f.d = p.d;
+  f.h = p.h;
+  f.w1 = c.wop[0];
+  f.w2 = c.wop[1];
+  f.w3 = c.wop[2];
+  const double ffl = (apply_too ? 4.0 : 0.0) * p.BH * n * dh + 6.0 * p.BH * n * dh;
+  int rc = timed(LACT_KCLASS_FWD, ffl, c.s, [&] { return launch_fwd(f, p.bf16, c.s); });
+  if (rc) return rc;
+
+  BwdArgs b{};
+  int nb = 0;
+  if (apply_too) {
+    BwdSeg& o = b.seg[nb++];
+    o.kind = BWD_OUT;
+    o.tiles_m = (int)cdiv(n, kTile);
+    o.tiles_n = (int)cdiv(p.d, kTile);
+    o.nsplit = 1;
+    o.nblocks = p.BH * o.tiles_m * o.tiles_n;
+    o.rows = n;
+    o.a0 = op(c.ws + p.off_hq, p.h, p.cap * p.h);
+    o.b0 = c.wop[1];
+    o.out = c.o + s0 * p.d * p.esz;
+    o.out_inst = c.dsc->n_q * p.d;
+  }
+  // Gradient contractions, split over tokens; a split past the chunk's end
+  // writes zeros so the update always sums p.nsplit partials.
+  const int64_t tj = cdiv(p.h, kTile), tm = cdiv(p.d, kTile);
+  {
+    BwdSeg& g = b.seg[nb++];
+    g.kind = BWD_GRAD13;
+    g.tiles_m = (int)tj;
+    g.tiles_n = (int)tm;
+    g.nsplit = p.nsplit;
+    g.nblocks = (int)(p.BH * tj * tm * p.nsplit);
+    g.rows = n;
+    g.split_len = p.split_len;
+    g.a0 = op(c.ws + p.off_upd[1], p.h, p.C * p.h);   // eta dz1
+    g.a1 = op(c.ws + p.off_upd[2], p.h, p.C * p.h);   // eta dz3
+    g.b0 = op(c.k + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
+    g.out = c.ws + p.off_step;
+    g.out_inst = 3 * dh;
+    g.out_split = (int64_t)p.BH * 3 * dh;
+  }
+  {
+    BwdSeg& g = b.seg[nb++];
+    g.kind = BWD_GRAD2;
+    g.tiles_m = (int)tm;
+    g.tiles_n = (int)tj;
+    g.nsplit = p.nsplit;
+    g.nblocks = (int)(p.BH * tj * tm * p.nsplit);
+    g.rows = n;
+    g.split_len = p.split_len;
+    g.a0 = op(c.v + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
+    g.b0 = op(c.ws + p.off_upd[0], p.h, p.C * p.h);   // eta hidden
+    g.out = c.ws + p.off_step;
+    g.out_inst = 3 * dh;
+    g.out_split = (int64_t)p.BH * 3 * dh;
+  }
+  b.nseg = nb;
+  b.total_blocks = 0;
+  for (int i = 0; i < nb; ++i) b.total_blocks += b.seg[i].nblocks;
+  b.d = p.d;
+  b.h = p.h;
+  const double bfl = (apply_too ? 2.0 : 0.0) * p.BH * n * dh + 6.0 * p.BH * n * dh;
+  rc = timed(LACT_KCLASS_BWD, bfl, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
+  if (rc) return rc;
+
+  UpdArgs u{};
+  for (int m = 0; m < 3; ++m) {
+    u.W[m] = c.W[m];
+    u.Wb[m] = p.bf16 ? (void*)(c.ws + p.off_wb[m]) : nullptr;
+  }
+  u.step = reinterpret_cast<const float*>(c.ws + p.off_step);
+  u.nsplit = p.nsplit;
+  u.step_split = (int64_t)p.BH * 3 * dh;
+  u.BH = p.BH;
+  u.d = p.d;
+  u.h = p.h;
+  u.rows_total = p.BH * (2 * p.h + p.d);
+  return timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] { return launch_update(u, p.bf16, c.s); });
+}
+
+}  // namespace
+}  // namespace lact
+
+using namespace lact;
+
+extern "C" {
+
+int lact_check_desc(const lact_desc* desc) { return check_desc(desc); }
+
+size_t lact_workspace_bytes(const lact_desc* desc, int* err) {
+  const int rc = check_desc(desc);
+  if (err) *err = rc;
+  if (rc) return 0;
+  return make_plan(desc).total;
+}
+
+int lact_forward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                 float* W1, float* W2, float* W3, void* o, void* workspace, size_t workspace_bytes,
+                 void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
+  if (!W1 || !W2 || !W3) return LACT_EINVAL;
+  if (any_q && (!q || !o)) return LACT_EINVAL;
+  if (any_kv && (!k || !v || !eta)) return LACT_EINVAL;
+  if (misaligned(W1) || misaligned(W2) || misaligned(W3)) return LACT_EALIGN;
+  if (any_q && (misaligned(q) || misaligned(o))) return LACT_EALIGN;
+  if (any_kv && (misaligned(k) || misaligned(v) || ((uintptr_t)eta & 3))) return LACT_EALIGN;
+  Ctx c{};
+  c.dsc = desc;
+  c.p = make_plan(desc);
+  if (!workspace || workspace_bytes < c.p.total) return LACT_EWORKSPACE;
+  if ((uintptr_t)workspace & (kAlign - 1)) return LACT_EALIGN;
+  c.q = (const uint8_t*)q;
+  c.k = (const uint8_t*)k;
+  c.v = (const uint8_t*)v;
+  c.eta = eta;
+  c.W[0] = W1;
+  c.W[1] = W2;
+  c.W[2] = W3;
+  c.o = (uint8_t*)o;
+  c.ws = (uint8_t*)workspace;
+  c.s = (hipStream_t)stream;
+  const Plan& p = c.p;
+  const int64_t dh = (int64_t)p.d * p.h;
+  if (p.bf16) {
+    const float* Wf[3] = {W1, W2, W3};
+    void* Wb[3] = {c.ws + p.off_wb[0], c.ws + p.off_wb[1], c.ws + p.off_wb[2]};
+    rc = timed(LACT_KCLASS_PREP, 0.0, c.s, [&] { return launch_prep(Wf, Wb, p.BH, p.d, p.h, c.s); });
+    if (rc) return rc;
+    c.wop[0] = op(Wb[0], p.d, dh);
+    c.wop[1] = op(Wb[1], p.h, dh);
+    c.wop[2] = op(Wb[2], p.d, dh);
+  } else {
+    c.wop[0] = op(W1, p.d, dh);
+    c.wop[1] = op(W2, p.h, dh);
+    c.wop[2] = op(W3, p.d, dh);
+  }
+  const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk;
+  for (int64_t s0 = 0; s0 < n_kv; s0 += C) {
+    const int64_t s1 = std::min(n_kv, s0 + C);
+    if (desc->order == LACT_APPLY_THEN_UPDATE) {
+      rc = update_chunk(c, s0, s1, true);
+    } else {
+      rc = update_chunk(c, s0, s1, false);
+      if (!rc) rc = apply_rows(c, s0, s1 == n_kv ? n_q : s1);
+    }
+    if (rc) return rc;
+  }
+  if (desc->order == LACT_APPLY_THEN_UPDATE || n_kv == 0) rc = apply_rows(c, n_kv, n_q);
+  return rc;
+}
+
+int lact_timing_enable(int enable) {
+  g_timing.enabled = enable != 0;
+  return LACT_OK;
+}
+
+int lact_timing_reset(void) {
+  for (auto& t : g_timing.pending) {
+    g_timing.pool.push_back(t.a);
+    g_timing.pool.push_back(t.b);
+  }
+  g_timing.pending.clear();
+  for (int i = 0; i < LACT_KCLASS_COUNT; ++i) {
+    g_timing.launches[i] = 0;
+    g_timing.ms[i] = 0;
+    g_timing.flops[i] = 0;
+  }
+  return LACT_OK;
+}
+
+int lact_timing_read(int kclass, int64_t* launches, double* total_ms, double* flops) {
+  if (kclass < 0 || kclass >= LACT_KCLASS_COUNT) return LACT_EINVAL;
+  // Fold every recorded launch into the totals.
+  for (auto& t : g_timing.pending) {
+    if (hipEventSynchronize(t.b) != hipSuccess) return record_hip(hipGetLastError());
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.a, t.b) != hipSuccess) return record_hip(hipGetLastError());
+    g_timing.launches[t.kclass] += 1;
+    g_timing.ms[t.kclass] += ms;
+    g_timing.flops[t.kclass] += t.flops;
+    g_timing.pool.push_back(t.a);
+    g_timing.pool.push_back(t.b);
+  }
+  g_timing.pending.clear();
+  if (launches) *launches = g_timing.launches[kclass];
+  if (total_ms) *total_ms = g_timing.ms[kclass];
+  if (flops) *flops = g_timing.flops[kclass];
+  return LACT_OK;
+}
+
+const char* lact_strerror(int code) {
+  switch (code) {
+    case LACT_OK: return "ok";
+    case LACT_EINVAL: return "invalid argument";
+    case LACT_EALIGN: return "pointer not 16-byte aligned (workspace: 256-byte)";
+    case LACT_EWORKSPACE: return "workspace missing or too small";
+    case LACT_EUNSUPPORTED: return "shape or option outside the kernels' envelope";
+    case LACT_EHIP: return "HIP runtime error (see lact_last_hip_error)";
+    default: return "unknown error";
+  }
+}
+
+const char* lact_last_hip_error(void) { return g_hip_err; }
+
+const char* lact_version(void) { return "lact-gfx950 0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,93 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2505_23884_amd as P
+from paper_2505_23884_amd.binding import make_desc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lact.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(lact_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = P.lib()
+    names = _declared()
+    assert "lact_forward" in names and "lact_workspace_bytes" in names
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version():
+    assert P.lib().lact_version().decode().startswith("lact-gfx950")
+
+
+GOOD = dict(B=2, H=2, d=64, h=128, n_kv=1000, n_q=1100, chunk=256, order=0, use_muon=False,
+            ns_steps=5, io_dtype=0)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("B", 0, -1), ("H", -1, -1), ("d", 0, -1), ("d", 12, -4), ("h", 4100, -4), ("h", 20, -4),
+    ("n_kv", -1, -1), ("n_q", 999, -1), ("chunk", 0, -1), ("order", 2, -1),
+    ("ns_steps", 17, -1), ("ns_steps", -1, -1), ("io_dtype", 3, -1),
+])
+def test_descriptor_validation(field, value, code):
+    kw = dict(GOOD)
+    kw[field] = value
+    d = make_desc(**kw)
+    assert P.check_desc(d) == code
+    err = ctypes.c_int(0)
+    assert P.lib().lact_workspace_bytes(ctypes.byref(d), ctypes.byref(err)) == 0
+    assert err.value == code
+
+
+def test_workspace_grows_with_the_chunk():
+    a = P.workspace_bytes(make_desc(**GOOD))
+    b = P.workspace_bytes(make_desc(**dict(GOOD, chunk=512)))
+    c = P.workspace_bytes(make_desc(**dict(GOOD, io_dtype=1)))
+    assert 0 < a < b and a < c and a % 256 == 0
+
+
+def _fwd(desc, q=0x1000, k=0x2000, v=0x3000, eta=0x4000, w1=0x5000, w2=0x6000, w3=0x7000,
+         o=0x8000, ws=0x10000, nbytes=None):
+    L = P.lib()
+    if nbytes is None:
+        nbytes = P.workspace_bytes(desc) if P.check_desc(desc) == 0 else 0
+    vp = ctypes.c_void_p
+    return L.lact_forward(ctypes.byref(desc), vp(q), vp(k), vp(v), vp(eta), vp(w1), vp(w2), vp(w3),
+                          vp(o), vp(ws), ctypes.c_size_t(nbytes), vp(0))
+
+
+def test_forward_argument_errors_before_any_hip_call():
+    d = make_desc(**GOOD)
+    assert _fwd(d, q=0) == -1
+    assert _fwd(d, w2=0) == -1
+    assert _fwd(d, eta=0) == -1
+    assert _fwd(d, k=0x2008) == -2          # misaligned tensor
+    assert _fwd(d, eta=0x4002) == -2        # eta needs 4-byte alignment
+    assert _fwd(d, ws=0x10010) == -2        # workspace needs 256-byte alignment
+    assert _fwd(d, ws=0) == -3
+    assert _fwd(d, nbytes=P.workspace_bytes(d) - 1) == -3
+    bad = make_desc(**dict(GOOD, d=12))
+    assert _fwd(bad, nbytes=1 << 30) == -4
+    assert ctypes.cast(P.lib().lact_strerror(-3), ctypes.c_char_p).value
+
+
+def test_timing_api_without_launches():
+    P.timing_reset()
+    assert P.timing_read(0) == (0, 0.0, 0.0)
+    assert P.lib().lact_timing_read(9, None, None, None) == -1
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(P.LactError):
+        P.load_library(str(tmp_path / "missing.so"))

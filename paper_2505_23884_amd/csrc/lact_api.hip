@@ -28,8 +28,14 @@ struct Plan {
   int64_t cap;        // rows of the applied-hidden buffer
   int nsplit;         // split-K ways of the gradient contraction
   int64_t split_len;  // tokens per split
+  bool muon;
+  bool ns_fp16;       // Newton-Schulz operand copies in fp16 (bf16 I/O) or fp32
+  int ns_esz;
+  int m;              // Newton-Schulz Gram size min(d, h)
+  int ns_bps;         // blocks of kNsBlockElems per gradient
   // workspace offsets (bytes)
   size_t off_wb[3], off_hq, off_upd[3], off_step, total;
+  size_t off_y32, off_yb[2], off_a32, off_ab, off_bb, off_ss;
 };
 
 int check_desc(const lact_desc* d) {
@@ -44,7 +50,6 @@ int check_desc(const lact_desc* d) {
   if (d->d % 8 || d->h % 8 || d->d > kMaxDim || d->h > kMaxDim) return LACT_EUNSUPPORTED;
   if ((int64_t)d->B * d->H > (1 << 20)) return LACT_EUNSUPPORTED;
   if (d->n_q > ((int64_t)1 << 40)) return LACT_EUNSUPPORTED;
-  if (d->use_muon) return LACT_EUNSUPPORTED;   // Newton-Schulz kernels: not in this build yet
   return LACT_OK;
 }
 
@@ -83,6 +88,28 @@ Plan make_plan(const lact_desc* dsc) {
   }
   p.off_step = o;
   o = align_up(o + (size_t)p.nsplit * p.BH * 3 * dh * 4);
+  p.muon = dsc->use_muon != 0;
+  p.m = std::min(p.d, p.h);
+  p.ns_bps = (int)cdiv((int64_t)dh, kNsBlockElems);
+  p.ns_fp16 = p.bf16;
+  p.ns_esz = p.ns_fp16 ? 2 : 4;
+  if (p.muon) {
+    const size_t slots = (size_t)p.BH * 3, mm = (size_t)p.m * p.m;
+    p.off_y32 = o;
+    o = align_up(o + slots * dh * 4);
+    for (int i = 0; i < 2; ++i) {
+      p.off_yb[i] = o;
+      o = align_up(o + slots * dh * p.ns_esz);
+    }
+    p.off_a32 = o;
+    o = align_up(o + slots * mm * 4);
+    p.off_ab = o;
+    o = align_up(o + slots * mm * p.ns_esz);
+    p.off_bb = o;
+    o = align_up(o + slots * mm * p.ns_esz);
+    p.off_ss = o;
+    o = align_up(o + slots * p.ns_bps * 4);
+  }
   p.total = o;
   return p;
 }
@@ -203,6 +230,81 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
   return LACT_OK;
 }
 
+// Muon (§3.2; App. A): Newton-Schulz on the three summed gradients of every
+// instance, in their stored orientation; leaves NS(P) in the fp32 iterate.
+int newton_schulz(Ctx& c) {
+  const Plan& p = c.p;
+  const int64_t dh = (int64_t)p.d * p.h;
+  NsPrepArgs pa{};
+  pa.part = reinterpret_cast<const float*>(c.ws + p.off_step);
+  pa.nsplit = p.nsplit;
+  pa.part_split = (int64_t)p.BH * 3 * dh;
+  pa.Y32 = reinterpret_cast<float*>(c.ws + p.off_y32);
+  pa.sumsq = reinterpret_cast<float*>(c.ws + p.off_ss);
+  pa.nslots = p.BH * 3;
+  pa.dh = dh;
+  pa.blocks_per_slot = p.ns_bps;
+  int rc = timed(LACT_KCLASS_NS, 0.0, c.s, [&] { return launch_ns_prep(pa, c.s); });
+  if (rc) return rc;
+  rc = timed(LACT_KCLASS_NS, 0.0, c.s,
+             [&] { return launch_ns_scale(pa, c.ws + p.off_yb[0], p.ns_fp16, 1e-7f, c.s); });
+  if (rc) return rc;
+  const int m = p.m, d = p.d, h = p.h;
+  // segment 0: W1 and W3 stored h x d; segment 1: W2 stored d x h
+  const int rows[2] = {h, d}, cols[2] = {d, h};
+  const int64_t mm = (int64_t)m * m;
+  for (int t = 0; t < c.dsc->ns_steps; ++t) {
+    NsArgs a{};
+    a.Y32 = pa.Y32;
+    a.Yin = c.ws + p.off_yb[t & 1];
+    a.Yout = c.ws + p.off_yb[(t + 1) & 1];
+    a.A32 = reinterpret_cast<float*>(c.ws + p.off_a32);
+    a.Ab = c.ws + p.off_ab;
+    a.Bb = c.ws + p.off_bb;
+    a.ystride = dh;
+    a.astride = mm;
+    a.m = m;
+    a.ca = 3.4445f;
+    a.cb = -4.7750f;
+    a.cc = 2.0315f;
+    a.nseg = 2;
+    for (int phase = 0; phase < 3; ++phase) {
+      a.total_blocks = 0;
+      double fl = 0.0;
+      for (int g = 0; g < 2; ++g) {
+        NsSeg& sg = a.seg[g];
+        sg.group = g == 0 ? 2 : 1;
+        sg.slot_off[0] = g == 0 ? 0 : 1;
+        sg.slot_off[1] = 2;
+        sg.ldy = cols[g];
+        const bool wide = rows[g] <= cols[g];
+        const int n = std::max(rows[g], cols[g]);
+        if (phase == 0) {
+          sg.kind = wide ? NS_GRAM_K : NS_GRAM_MN;
+          sg.M = sg.N = m;
+          sg.K = n;
+        } else if (phase == 1) {
+          sg.kind = NS_POLY;
+          sg.M = sg.N = sg.K = m;
+        } else {
+          sg.kind = wide ? NS_UPD_BY : NS_UPD_YB;
+          sg.M = rows[g];
+          sg.N = cols[g];
+          sg.K = m;
+        }
+        sg.tiles_m = (int)cdiv(sg.M, kTile);
+        sg.tiles_n = (int)cdiv(sg.N, kTile);
+        sg.nblocks = p.BH * sg.group * sg.tiles_m * sg.tiles_n;
+        a.total_blocks += sg.nblocks;
+        fl += 2.0 * p.BH * sg.group * (double)sg.M * sg.N * sg.K;
+      }
+      rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns(a, p.ns_fp16, c.s); });
+      if (rc) return rc;
+    }
+  }
+  return LACT_OK;
+}
+
 // One update on key rows [s0, s1); with apply_too, the same launches also
 // apply the current (pre-update) weights to query rows [s0, s1).
 int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
@@ -312,9 +414,17 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     u.W[m] = c.W[m];
     u.Wb[m] = p.bf16 ? (void*)(c.ws + p.off_wb[m]) : nullptr;
   }
-  u.step = reinterpret_cast<const float*>(c.ws + p.off_step);
-  u.nsplit = p.nsplit;
-  u.step_split = (int64_t)p.BH * 3 * dh;
+  if (p.muon) {
+    rc = newton_schulz(c);
+    if (rc) return rc;
+    u.step = reinterpret_cast<const float*>(c.ws + p.off_y32);
+    u.nsplit = 1;
+    u.step_split = 0;
+  } else {
+    u.step = reinterpret_cast<const float*>(c.ws + p.off_step);
+    u.nsplit = p.nsplit;
+    u.step_split = (int64_t)p.BH * 3 * dh;
+  }
   u.BH = p.BH;
   u.d = p.d;
   u.h = p.h;

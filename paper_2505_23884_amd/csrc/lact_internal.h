@@ -82,11 +82,61 @@ struct UpdArgs {
   int rows_total;       // BH * (2h + d)
 };
 
+// ---- Muon: Newton-Schulz on the three gradients of every instance ----------
+// Matrices live in "slots" s = inst*3 + j (j = 0: W1, 1: W2, 2: W3), each in
+// its stored orientation Y [r x c] (W1, W3: h x d; W2: d x h). The iteration
+// runs on the wide orientation of Y:
+//   wide (r <= c):  A = Y Y^T,  B = b A + c A A,  Y <- a Y + B Y
+//   tall (r >  c):  A = Y^T Y,  B = b A + c A A,  Y <- a Y + Y B
+enum NsKind : int { NS_GRAM_K = 0, NS_GRAM_MN = 1, NS_POLY = 2, NS_UPD_BY = 3, NS_UPD_YB = 4 };
+
+struct NsSeg {
+  int kind;
+  int nblocks;
+  int tiles_m, tiles_n;
+  int group;            // matrices per instance in this segment (1 or 2)
+  int slot_off[2];      // j of each matrix of the group
+  int M, N, K;          // output rows, output columns, contraction length
+  int ldy;              // columns c of the stored Y
+};
+
+struct NsArgs {
+  NsSeg seg[2];
+  int nseg;
+  int total_blocks;
+  float* Y32;           // fp32 iterate (in place), slot stride ystride
+  const void* Yin;      // operand copy read this iteration (fp16 or fp32)
+  void* Yout;           // operand copy written this iteration
+  float* A32;           // fp32 Gram, slot stride astride
+  void* Ab;             // Gram operand copy
+  void* Bb;             // polynomial operand copy
+  int64_t ystride, astride;
+  int m;                // Gram size min(d, h)
+  float ca, cb, cc;     // quintic coefficients
+};
+
+struct NsPrepArgs {
+  const float* part;    // gradient partials [split][inst][3][d*h]
+  int nsplit;
+  int64_t part_split;   // elements between splits
+  float* Y32;           // summed gradient, [inst*3 + j][d*h]
+  float* sumsq;         // per-slot, per-block partial sums of squares
+  int nslots;
+  int64_t dh;
+  int blocks_per_slot;  // blocks of 4096 elements per slot
+};
+
 // Launchers (io_bf16 selects bf16 MFMA operands, otherwise fp32).
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, bool io_bf16, hipStream_t s);
 hipError_t launch_update(const UpdArgs& a, bool io_bf16, hipStream_t s);
 hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d, int h,
                        hipStream_t s);
+// Newton-Schulz operand copies are fp16 (bf16 I/O: 4x finer rounding than bf16
+// at the same MFMA rate; the iterates are O(1)) or fp32 (fp32 I/O).
+hipError_t launch_ns(const NsArgs& a, bool fp16, hipStream_t s);
+hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s);
+hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s);
+constexpr int kNsBlockElems = 4096;
 
 }  // namespace lact

@@ -25,6 +25,7 @@ namespace lact {
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
@@ -35,6 +36,9 @@ constexpr int kTileBytes = kTile * kRowBytes;   // one operand tile in LDS
 
 template <typename T> struct Tr;
 template <> struct Tr<__bf16> {   // 32 K per tile, 8 elements per 16 bytes
+  static constexpr int BK = 32, E = 8, KG = 8;
+};
+template <> struct Tr<_Float16> { // fp16 operands (Newton-Schulz): as bf16
   static constexpr int BK = 32, E = 8, KG = 8;
 };
 template <> struct Tr<float> {    // 16 K per tile, 4 elements per 16 bytes
@@ -178,6 +182,15 @@ struct KGrad2 : KindBase<1, 1, 1, 3u> {
   static constexpr int pb(int) { return 0; }
 };
 
+// Newton-Schulz products: both operands K-contiguous, both row-contiguous, or
+// only the second row-contiguous (B Y with Y read down its columns).
+using KNsK = KOut;
+using KNsMN = KGrad2;
+struct KNsBY : KindBase<1, 1, 1, 2u> {
+  static constexpr int pa(int) { return 0; }
+  static constexpr int pb(int) { return 0; }
+};
+
 template <typename T, class K>
 __device__ __forceinline__ void compute_ktile(const uint8_t* buf, f32x16_t (&acc)[K::NACC][2][2]) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -204,9 +217,14 @@ __device__ __forceinline__ void compute_ktile(const uint8_t* buf, f32x16_t (&acc
         for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
           for (int ni = 0; ni < 2; ++ni)
-            acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8_t, af[K::pa(p)][mi]),
-                __builtin_bit_cast(bf16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
+            if constexpr (__is_same(T, _Float16))
+              acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+                  __builtin_bit_cast(f16x8_t, af[K::pa(p)][mi]),
+                  __builtin_bit_cast(f16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
+            else
+              acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  __builtin_bit_cast(bf16x8_t, af[K::pa(p)][mi]),
+                  __builtin_bit_cast(bf16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
     }
   } else {
     // fp32: lanes 0-31 hold K 0..7 of the tile, lanes 32-63 K 8..15; MFMA s
@@ -323,8 +341,7 @@ __device__ __forceinline__ int acc_col(int ni) {
 
 template <typename T>
 __device__ __forceinline__ void st_elem(void* base, int64_t idx, float v) {
-  if constexpr (sizeof(T) == 2) reinterpret_cast<__bf16*>(base)[idx] = (__bf16)v;
-  else reinterpret_cast<float*>(base)[idx] = v;
+  reinterpret_cast<T*>(base)[idx] = (T)v;
 }
 
 __device__ __forceinline__ float sigmoidf_fast(float z) {
@@ -588,7 +605,158 @@ __global__ __launch_bounds__(kThreads) void k_prep(const float* w1, const float*
   }
 }
 
+// One Newton-Schulz product over every matrix of the chunk (see NsKind).
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_ns(const NsArgs args) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * 2 * kTileBytes];
+  constexpr int esz = sizeof(T);
+  int bid = xcd_remap(blockIdx.x, args.total_blocks);
+  const bool first = bid < args.seg[0].nblocks;
+  const NsSeg& sg = first ? args.seg[0] : args.seg[1];
+  if (!first) bid -= args.seg[0].nblocks;
+  const int per = sg.tiles_m * sg.tiles_n;
+  const int q = bid / per;
+  const int rr = bid - q * per;
+  const int64_t i0 = (int64_t)(rr / sg.tiles_n) * kTile, j0 = (int64_t)(rr % sg.tiles_n) * kTile;
+  const int64_t slot = (int64_t)(q / sg.group) * 3 + sg.slot_off[q % sg.group];
+  const int m = args.m, ldy = sg.ldy;
+  const int64_t mrows = sg.M - i0, ncols = sg.N - j0;
+  float* Y32 = args.Y32 + slot * args.ystride;
+  const uint8_t* Yin = reinterpret_cast<const uint8_t*>(args.Yin) + slot * args.ystride * esz;
+  void* Yout = reinterpret_cast<uint8_t*>(args.Yout) + slot * args.ystride * esz;
+  float* A32 = args.A32 + slot * args.astride;
+  const uint8_t* Ab = reinterpret_cast<const uint8_t*>(args.Ab) + slot * args.astride * esz;
+  void* Abw = reinterpret_cast<uint8_t*>(args.Ab) + slot * args.astride * esz;
+  const uint8_t* Bb = reinterpret_cast<const uint8_t*>(args.Bb) + slot * args.astride * esz;
+  void* Bbw = reinterpret_cast<uint8_t*>(args.Bb) + slot * args.astride * esz;
+  f32x16_t acc[1][2][2];
+  const int kind = sg.kind;
+  if (kind == NS_GRAM_K) {          // A = Y Y^T
+    const View ops[2] = {View{Yin + i0 * ldy * esz, (int64_t)ldy * esz, mrows, sg.K},
+                         View{Yin + j0 * ldy * esz, (int64_t)ldy * esz, ncols, sg.K}};
+    mainloop<T, KNsK>(smem, ops, sg.K, acc);
+  } else if (kind == NS_GRAM_MN) {  // A = Y^T Y
+    const View ops[2] = {View{Yin + i0 * esz, (int64_t)ldy * esz, mrows, sg.K},
+                         View{Yin + j0 * esz, (int64_t)ldy * esz, ncols, sg.K}};
+    mainloop<T, KNsMN>(smem, ops, sg.K, acc);
+  } else if (kind == NS_POLY) {     // A A (A symmetric, so A A^T)
+    const View ops[2] = {View{Ab + i0 * m * esz, (int64_t)m * esz, mrows, sg.K},
+                         View{Ab + j0 * m * esz, (int64_t)m * esz, ncols, sg.K}};
+    mainloop<T, KNsK>(smem, ops, sg.K, acc);
+  } else if (kind == NS_UPD_BY) {   // B Y
+    const View ops[2] = {View{Bb + i0 * m * esz, (int64_t)m * esz, mrows, sg.K},
+                         View{Yin + j0 * esz, (int64_t)ldy * esz, ncols, sg.K}};
+    mainloop<T, KNsBY>(smem, ops, sg.K, acc);
+  } else {                          // Y B (B symmetric)
+    const View ops[2] = {View{Yin + i0 * ldy * esz, (int64_t)ldy * esz, mrows, sg.K},
+                         View{Bb + j0 * m * esz, (int64_t)m * esz, ncols, sg.K}};
+    mainloop<T, KNsK>(smem, ops, sg.K, acc);
+  }
+#pragma unroll
+  for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      const int j = acc_col(ni);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = acc_row(mi, r);
+        if (i < mrows && j < ncols) {
+          const float v = acc[0][mi][ni][r];
+          if (kind == NS_GRAM_K || kind == NS_GRAM_MN) {
+            const int64_t idx = (i0 + i) * m + j0 + j;
+            A32[idx] = v;
+            st_elem<T>(Abw, idx, v);
+          } else if (kind == NS_POLY) {
+            const int64_t idx = (i0 + i) * m + j0 + j;
+            st_elem<T>(Bbw, idx, args.cb * A32[idx] + args.cc * v);
+          } else {
+            const int64_t idx = (i0 + i) * ldy + j0 + j;
+            const float y = args.ca * Y32[idx] + v;
+            Y32[idx] = y;
+            st_elem<T>(Yout, idx, y);
+          }
+        }
+      }
+    }
+}
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int i = 0; i < kThreads / 64; ++i) t += red[i];
+  __syncthreads();
+  return t;
+}
+
+// Sum the split-K partials of every gradient and the per-block sums of squares.
+__global__ __launch_bounds__(kThreads) void k_ns_prep(const NsPrepArgs a) {
+  __shared__ float red[kThreads / 64];
+  const int slot = blockIdx.x / a.blocks_per_slot;
+  const int blk = blockIdx.x - slot * a.blocks_per_slot;
+  const int64_t base = (int64_t)slot * a.dh;
+  float ss = 0.f;
+  for (int e = threadIdx.x; e < kNsBlockElems; e += kThreads) {
+    const int64_t idx = (int64_t)blk * kNsBlockElems + e;
+    if (idx < a.dh) {
+      float g = 0.f;
+      for (int s = 0; s < a.nsplit; ++s) g += a.part[s * a.part_split + base + idx];
+      a.Y32[base + idx] = g;
+      ss += g * g;
+    }
+  }
+  ss = block_sum(ss, red);
+  if (threadIdx.x == 0) a.sumsq[(int64_t)slot * a.blocks_per_slot + blk] = ss;
+}
+
+// X0 = G / (||G||_F + eps), fp32 iterate and operand copy.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_ns_scale(const NsPrepArgs a, void* yb, float eps) {
+  __shared__ float red[kThreads / 64];
+  const int slot = blockIdx.x / a.blocks_per_slot;
+  const int blk = blockIdx.x - slot * a.blocks_per_slot;
+  const int64_t base = (int64_t)slot * a.dh;
+  float t = 0.f;
+  for (int b = threadIdx.x; b < a.blocks_per_slot; b += kThreads)
+    t += a.sumsq[(int64_t)slot * a.blocks_per_slot + b];
+  t = block_sum(t, red);
+  const float inv = 1.0f / (sqrtf(t) + eps);
+  for (int e = threadIdx.x; e < kNsBlockElems; e += kThreads) {
+    const int64_t idx = (int64_t)blk * kNsBlockElems + e;
+    if (idx < a.dh) {
+      const float y = a.Y32[base + idx] * inv;
+      a.Y32[base + idx] = y;
+      st_elem<T>(yb, base + idx, y);
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_ns(const NsArgs& a, bool fp16, hipStream_t s) {
+  if (a.total_blocks <= 0) return hipSuccess;
+  if (fp16) k_ns<_Float16><<<a.total_blocks, kThreads, 0, s>>>(a);
+  else k_ns<float><<<a.total_blocks, kThreads, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.nslots * a.blocks_per_slot;
+  if (blocks <= 0) return hipSuccess;
+  k_ns_prep<<<(unsigned)blocks, kThreads, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.nslots * a.blocks_per_slot;
+  if (blocks <= 0) return hipSuccess;
+  if (fp16) k_ns_scale<_Float16><<<(unsigned)blocks, kThreads, 0, s>>>(a, Yb, eps);
+  else k_ns_scale<float><<<(unsigned)blocks, kThreads, 0, s>>>(a, Yb, eps);
+  return hipGetLastError();
+}
 
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;

@@ -185,3 +185,95 @@ def test_kernel_timing_counts_launches():
     assert n_fwd == 2 and n_upd == 2 and ms_fwd > 0
     assert fl_fwd == pytest.approx(2 * 10.0 * 256 * 128 * 128)
     P.timing_reset()
+
+
+# ----------------------------------------------------------------------------- Muon
+#
+# With Muon the chunk recurrence is chaotic: a perturbation of W grows ~2x per
+# chunk in exact arithmetic, so any bf16 path drifts away from the fp64 oracle
+# after a few chunks whatever its per-chunk accuracy. Parity is therefore
+# checked per chunk, teacher-forced: the oracle starts every chunk from the
+# GPU's own fp32 fast weights entering that chunk, and o, W and dW of the chunk
+# are compared at the I/O tolerance. The first two chunks are also compared
+# end to end from W0.
+
+
+def teacher_forced(cfg, x, instances, max_chunks=None):
+    B, H = cfg.B, cfg.H
+    n = len(x["q"])
+    if n != cfg.BH:
+        B, H = n, 1
+    sh = lambda a: a.reshape(B, H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    W = [to_dev(sh(x[w]), cfg, torch.float32) for w in ("W1", "W2", "W3")]
+    C = cfg.chunk
+    nch = cfg.n_chunks if max_chunks is None else min(cfg.n_chunks, max_chunks)
+    flat = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    worst = {}
+    for c in range(nch):
+        s, e = c * C, min(cfg.n_kv, (c + 1) * C)
+        w_in = [flat(w) for w in W]
+        cut = lambda t: t[:, :, s:e].contiguous()
+        print(f"[gpu] {cfg.name} chunk {c} tokens [{s},{e})", flush=True)
+        o = P.forward(cut(q), cut(k), cut(v), eta[:, :, s:e].contiguous(), *W, chunk=C,
+                      order=cfg.order, use_muon=True, ns_steps=cfg.ns_steps)
+        torch.cuda.synchronize()
+        og, w_out = flat(o), [flat(w) for w in W]
+        for i in instances:
+            o_ref, w_ref = O.lact_forward_instance(
+                x["q"][i, s:e], x["k"][i, s:e], x["v"][i, s:e], x["eta"][i, s:e],
+                *[w[i].astype(np.float64) for w in w_in], chunk=C, order=cfg.order,
+                use_muon=True, ns_steps=cfg.ns_steps)
+            errs = {"o": rel(og[i], o_ref)}
+            for j, name in enumerate(("W1", "W2", "W3")):
+                errs[name] = rel(w_out[j][i], w_ref[j])
+                errs["d" + name] = rel(w_out[j][i] - w_in[j][i], w_ref[j] - w_in[j][i])
+            for kk, vv in errs.items():
+                worst[kk] = max(worst.get(kk, 0.0), vv)
+    print("[gpu] worst per-chunk rel-L2", {k: f"{v:.2e}" for k, v in worst.items()}, flush=True)
+    for kk, vv in worst.items():
+        assert vv <= TOL[cfg.io], (kk, vv)
+    return worst
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_muon_small_teacher_forced_and_two_chunks(order):
+    # h > d: W1, W3 iterate on their transpose (tall), W2 on itself (wide)
+    cfg = CONFIGS["video"].with_(name="muon_small", B=1, H=2, d=128, h=256, n_kv=700, n_q=700,
+                                 chunk=256, order=order)
+    x = make_inputs(cfg, 8)
+    teacher_forced(cfg, x, [0, 1])
+    two = cfg.with_(n_kv=512, n_q=512)
+    x2 = {kk: (vv[:, :512] if kk in ("q", "k", "v", "eta") else vv) for kk, vv in x.items()}
+    check(two, x2, run_gpu(two, x2), run_oracle(two, x2))
+
+
+def test_muon_fp32_teacher_forced():
+    cfg = CONFIGS["tiny_fp32"].with_(name="muon_fp32", B=1, H=2, d=64, h=96, n_kv=512, n_q=512,
+                                     chunk=256, use_muon=1, ns_steps=5)
+    x = make_inputs(cfg, 9)
+    teacher_forced(cfg, x, [0, 1])
+
+
+def test_muon_zero_steps_is_normalised_gradient():
+    cfg = CONFIGS["video"].with_(name="muon0", B=1, H=1, d=64, h=64, n_kv=256, n_q=256, chunk=128,
+                                 ns_steps=0)
+    x = make_inputs(cfg, 10)
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
+def test_lm32k_muon_teacher_forced_sampled():
+    cfg = CONFIGS["lm32k_muon"]
+    x = make_inputs(cfg, 0)
+    teacher_forced(cfg, x, [0, 9])
+    two = cfg.with_(n_kv=2 * cfg.chunk, n_q=2 * cfg.chunk)
+    x2 = {kk: (np.ascontiguousarray(vv[:, :two.n_kv]) if kk in ("q", "k", "v", "eta") else vv)
+          for kk, vv in x.items()}
+    check(two, x2, run_gpu(two, x2), run_oracle(two, x2, instances=[0, 9]), instances=[0, 9])
+
+
+def test_video_muon_teacher_forced_sampled():
+    cfg = CONFIGS["video"]
+    x = make_inputs(cfg, 0)
+    teacher_forced(cfg, x, [0, 39])

@@ -162,22 +162,27 @@ struct KindBase {
   static constexpr int mn_half(int o) { return __builtin_popcount(MN & ((1u << o) - 1u)) & 1; }
 };
 struct KApply : KindBase<1, 2, 2, 0u> {
+  static constexpr int NSTAGE = 4;
   static constexpr int pa(int) { return 0; }
   static constexpr int pb(int p) { return p; }
 };
 struct KUpdate : KindBase<2, 3, 3, 1u << 4> {     // W2 (operand 4) is read transposed
+  static constexpr int NSTAGE = 3;
   static constexpr int pa(int p) { return p == 2 ? 1 : 0; }
   static constexpr int pb(int p) { return p; }
 };
 struct KOut : KindBase<1, 1, 1, 0u> {
+  static constexpr int NSTAGE = 4;
   static constexpr int pa(int) { return 0; }
   static constexpr int pb(int) { return 0; }
 };
 struct KGrad13 : KindBase<2, 1, 2, 7u> {
+  static constexpr int NSTAGE = 3;
   static constexpr int pa(int p) { return p; }
   static constexpr int pb(int) { return 0; }
 };
 struct KGrad2 : KindBase<1, 1, 1, 3u> {
+  static constexpr int NSTAGE = 4;
   static constexpr int pa(int) { return 0; }
   static constexpr int pb(int) { return 0; }
 };
@@ -187,6 +192,7 @@ struct KGrad2 : KindBase<1, 1, 1, 3u> {
 using KNsK = KOut;
 using KNsMN = KGrad2;
 struct KNsBY : KindBase<1, 1, 1, 2u> {
+  static constexpr int NSTAGE = 4;
   static constexpr int pa(int) { return 0; }
   static constexpr int pb(int) { return 0; }
 };
@@ -274,10 +280,11 @@ __device__ __forceinline__ void compute_ktile(const uint8_t* buf, f32x16_t (&acc
   }
 }
 
-// acc[p] = sum over K of A[pa(p)] B[pb(p)]^T for this block's 128 x 128 tile.
+// fp32 operands: register-staged double buffer (global -> VGPR -> LDS, with
+// the in-register transposition of row-contiguous operands).
 template <typename T, class K>
-__device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk,
-                                         f32x16_t (&acc)[K::NACC][2][2]) {
+__device__ __forceinline__ void mainloop_regs(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk,
+                                              f32x16_t (&acc)[K::NACC][2][2]) {
   constexpr int BK = Tr<T>::BK;
 #pragma unroll
   for (int p = 0; p < K::NACC; ++p)
@@ -329,6 +336,200 @@ __device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOP
   }
 }
 
+// ---------------------------------------------------------------------------
+// 16-bit operands: direct global -> LDS DMA (global_load_lds_dwordx4) into a
+// ring of K::NSTAGE stages, K::NSTAGE - 1 k-tiles in flight, no register
+// staging. Row-contiguous operands keep their HBM layout in LDS (32 K rows x
+// 256 bytes) and are read with ds_read_b64_tr_b16, which hands every lane
+// four consecutive K of one row of the operand.
+
+// A 16-byte page of zeros: out-of-range lanes load from it, so partial tiles
+// arrive zero-padded in LDS.
+__device__ __attribute__((aligned(64))) uint32_t g_zero_page[16];
+
+// XOR swizzle of the 16-byte chunks of a row-contiguous tile (256-byte rows):
+// the four K rows read by one 16-lane group of a transpose read land on
+// distinct chunk positions.
+__device__ __forceinline__ int swz_mn(int kr) { return (kr & 3) << 2; }
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // gfx9 s_waitcnt: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt_hi[15:14]
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | (((N >> 4) & 3) << 14));
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) const void gbl_void_t;
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+__device__ __forceinline__ lds_void_t* to_lds(const void* p) {
+  return (lds_void_t*)(p);
+}
+
+// Issue this wave's two 1 KiB DMA loads of one operand tile (512 chunks).
+template <bool MN>
+__device__ __forceinline__ void dma_tile(uint8_t* tile, const View& v, int64_t k0) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int base = w * 128 + i * 64;     // first 16-byte slot of this instruction
+    const int p = base + lane;
+    const uint8_t* src;
+    if (!MN) {
+      const int row = p >> 2;
+      const int c = (p & 3) ^ (((row >> 1) ^ (row >> 3)) & 3);
+      const int64_t k = k0 + c * 8;
+      src = (row < v.nrows && k < v.nk) ? v.p + row * v.ld_b + k * 2
+                                        : reinterpret_cast<const uint8_t*>(g_zero_page);
+    } else {
+      const int kr = p >> 4;
+      const int c = (p & 15) ^ swz_mn(kr);
+      const int64_t k = k0 + kr;
+      src = (k < v.nk && c * 8 < v.nrows) ? v.p + k * v.ld_b + c * 16
+                                          : reinterpret_cast<const uint8_t*>(g_zero_page);
+    }
+    __builtin_amdgcn_global_load_lds((gbl_void_t*)src, to_lds(tile + base * 16), 16, 0, 0);
+  }
+}
+
+// MFMA fragment (8 consecutive K of row rb + lane%32, K block 8*(lane/32) of
+// substep s) from a row-contiguous tile, by two transpose reads. Issued as
+// inline asm so the compiler does not drain the in-flight DMA before it (it
+// cannot tell which stage the read touches); the result is not ready until a
+// lgkm_ready() on it.
+__device__ __forceinline__ u32x4_t frag_tr(const uint8_t* tile, int rb, int s) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, sl = lane & 15;
+  const int mn = rb + 16 * (g & 1) + 4 * (sl & 3);
+  const int c = mn >> 3, hb = (mn >> 2) & 1;
+  const uint32_t base = (uint32_t)(uintptr_t)to_lds(tile);
+  u32x2_t lo, hi;
+  {
+    const int kr = 16 * s + 8 * (g >> 1) + (sl >> 2);
+    const uint32_t a = base + kr * 256 + ((c ^ swz_mn(kr)) << 4) + (hb << 3);
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a));
+  }
+  {
+    const int kr = 16 * s + 8 * (g >> 1) + 4 + (sl >> 2);
+    const uint32_t a = base + kr * 256 + ((c ^ swz_mn(kr)) << 4) + (hb << 3);
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(a));
+  }
+  return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+}
+
+// Waits for outstanding LDS reads and makes `x` depend on the wait, so no use
+// of a transpose-read result is scheduled before its data has arrived.
+__device__ __forceinline__ void lgkm_ready(u32x4_t& x) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x));
+}
+
+template <typename T, class K>
+__device__ __forceinline__ void compute_ktile16(const uint8_t* buf, f32x16_t (&acc)[K::NACC][2][2]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int ab = (w >> 1) * 64, bb = (w & 1) * 64;
+  const int arow = ab + (lane & 31), brow = bb + (lane & 31);
+  const int half = lane >> 5;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    u32x4_t af[K::NA][2], bf[K::NB][2];
+#pragma unroll
+    for (int o = 0; o < K::NA; ++o)
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+        af[o][mi] = K::is_mn(o) ? frag_tr(buf + o * kTileBytes, ab + mi * 32, s)
+                                : frag<T>(buf + o * kTileBytes, arow + mi * 32, 2 * s + half, false);
+#pragma unroll
+    for (int o = 0; o < K::NB; ++o)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni)
+        bf[o][ni] = K::is_mn(K::NA + o)
+                        ? frag_tr(buf + (K::NA + o) * kTileBytes, bb + ni * 32, s)
+                        : frag<T>(buf + (K::NA + o) * kTileBytes, brow + ni * 32, 2 * s + half, false);
+    if constexpr (K::MN != 0u) {
+#pragma unroll
+      for (int o = 0; o < K::NA; ++o)
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+          if (K::is_mn(o)) lgkm_ready(af[o][mi]);
+#pragma unroll
+      for (int o = 0; o < K::NB; ++o)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+          if (K::is_mn(K::NA + o)) lgkm_ready(bf[o][ni]);
+    }
+#pragma unroll
+    for (int p = 0; p < K::NACC; ++p)
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) {
+          if constexpr (__is_same(T, _Float16))
+            acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+                __builtin_bit_cast(f16x8_t, af[K::pa(p)][mi]),
+                __builtin_bit_cast(f16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
+          else
+            acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8_t, af[K::pa(p)][mi]),
+                __builtin_bit_cast(bf16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
+        }
+  }
+}
+
+template <typename T, class K>
+__device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk,
+                                             f32x16_t (&acc)[K::NACC][2][2]) {
+  constexpr int BK = 32, NS = K::NSTAGE, STAGE = K::NOPS * kTileBytes;
+  constexpr int L = 2 * K::NOPS;   // DMA instructions per wave per k-tile
+#pragma unroll
+  for (int p = 0; p < K::NACC; ++p)
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[p][mi][ni][r] = 0.f;
+  const int nkt = (int)((nk + BK - 1) / BK);
+  if (nkt <= 0) return;
+  auto issue = [&](int kt) {
+    uint8_t* st = smem + (kt % NS) * STAGE;
+#pragma unroll
+    for (int o = 0; o < K::NOPS; ++o) {
+      if (K::is_mn(o)) dma_tile<true>(st + o * kTileBytes, ops[o], (int64_t)kt * BK);
+      else dma_tile<false>(st + o * kTileBytes, ops[o], (int64_t)kt * BK);
+    }
+  };
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < nkt) issue(t);
+  for (int kt = 0; kt < nkt; ++kt) {
+    // this wave's loads of tile kt are done once at most the later tiles' are pending
+    if (kt + NS - 2 < nkt) wait_vmcnt<L * (NS - 2)>();
+    else wait_vmcnt<0>();
+    // every wave's tile kt is in LDS and tile kt-1's stage is free; a bare
+    // barrier (a fenced one would drain all DMA still in flight)
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (kt + NS - 1 < nkt) issue(kt + NS - 1);
+    compute_ktile16<T, K>(smem + (kt % NS) * STAGE, acc);
+  }
+  __syncthreads();     // the caller may reuse LDS after the loop
+}
+
+template <typename T, class K>
+__device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk,
+                                         f32x16_t (&acc)[K::NACC][2][2]) {
+  if constexpr (sizeof(T) == 2) mainloop_dma<T, K>(smem, ops, nk, acc);
+  else mainloop_regs<T, K>(smem, ops, nk, acc);
+}
+
+template <class K>
+constexpr int smem_bytes() {
+  const int dma = K::NSTAGE * K::NOPS * kTileBytes, regs = 2 * K::NOPS * kTileBytes;
+  return dma > regs ? dma : regs;
+}
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
 // Epilogue coordinates of accumulator register r of block (mi, ni).
 __device__ __forceinline__ int acc_row(int mi, int r) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -362,7 +563,7 @@ __device__ __forceinline__ View view_mn(const Operand& op, int inst, int64_t row
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_fwd(const FwdArgs args) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * 5 * kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(smem_bytes<KApply>(), smem_bytes<KUpdate>())];
   constexpr int esz = sizeof(T);
   int bid = xcd_remap(blockIdx.x, args.total_blocks);
   const bool first = bid < args.seg[0].nblocks;
@@ -439,7 +640,8 @@ __global__ __launch_bounds__(kThreads) void k_fwd(const FwdArgs args) {
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_bwd(const BwdArgs args) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * 3 * kTileBytes];
+  __shared__ __attribute__((aligned(16)))
+  uint8_t smem[cmax(smem_bytes<KOut>(), cmax(smem_bytes<KGrad13>(), smem_bytes<KGrad2>()))];
   constexpr int esz = sizeof(T);
   int bid = xcd_remap(blockIdx.x, args.total_blocks);
   int si = 0;
@@ -608,7 +810,7 @@ __global__ __launch_bounds__(kThreads) void k_prep(const float* w1, const float*
 // One Newton-Schulz product over every matrix of the chunk (see NsKind).
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_ns(const NsArgs args) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * 2 * kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(smem_bytes<KNsK>(), smem_bytes<KNsBY>())];
   constexpr int esz = sizeof(T);
   int bid = xcd_remap(blockIdx.x, args.total_blocks);
   const bool first = bid < args.seg[0].nblocks;

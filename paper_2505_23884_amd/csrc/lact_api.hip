@@ -48,6 +48,8 @@ int check_desc(const lact_desc* d) {
   if (d->io_dtype != LACT_IO_BF16 && d->io_dtype != LACT_IO_FP32) return LACT_EINVAL;
   if (d->d < 1 || d->h < 1) return LACT_EINVAL;
   if (d->d % 8 || d->h % 8 || d->d > kMaxDim || d->h > kMaxDim) return LACT_EUNSUPPORTED;
+  // 16-bit MFMA tiles take K in whole steps of 32 along d and h
+  if (d->io_dtype == LACT_IO_BF16 && (d->d % 32 || d->h % 32)) return LACT_EUNSUPPORTED;
   if ((int64_t)d->B * d->H > (1 << 20)) return LACT_EUNSUPPORTED;
   if (d->n_q > ((int64_t)1 << 40)) return LACT_EUNSUPPORTED;
   return LACT_OK;
@@ -68,8 +70,12 @@ Plan make_plan(const lact_desc* dsc) {
   if (p.cap < 1) p.cap = 1;
   // Split-K of the gradient contraction: enough blocks to fill the chip
   // (~512), each split at least 256 tokens, lengths a multiple of 32.
-  const int64_t tiles = (int64_t)p.BH * 2 * cdiv(p.h, kTile) * cdiv(p.d, kTile);
-  int64_t ns = std::max<int64_t>(1, cdiv(512, tiles));
+  const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
+  const int64_t tiles = (int64_t)p.BH * (cdiv(p.h, g13.rows) * cdiv(p.d, g13.cols) +
+                                         cdiv(p.d, g2.rows) * cdiv(p.h, g2.cols));
+  // one wave of big gradient tiles fills the chip when the apply GEMM-2 tiles
+  // share the launch (they take the remaining CUs)
+  int64_t ns = std::max<int64_t>(1, cdiv(256, tiles));
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.C / 256));
   ns = std::min<int64_t>(ns, kMaxSplit);
   p.split_len = std::max<int64_t>(32, cdiv(cdiv(std::max<int64_t>(p.C, 1), ns), 32) * 32);
@@ -191,8 +197,8 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
     FwdArgs f{};
     FwdSeg& g = f.seg[0];
     g.kind = FWD_APPLY;
-    g.tiles_m = (int)cdiv(n, kTile);
-    g.tiles_n = (int)cdiv(p.h, kTile);
+    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_APPLY, p.bf16).rows);
+    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_APPLY, p.bf16).cols);
     g.nblocks = p.BH * g.tiles_m * g.tiles_n;
     g.rows = n;
     g.a0 = op(c.q + a * p.d * p.esz, p.d, c.dsc->n_q * p.d);
@@ -211,8 +217,8 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
     BwdArgs b{};
     BwdSeg& o = b.seg[0];
     o.kind = BWD_OUT;
-    o.tiles_m = (int)cdiv(n, kTile);
-    o.tiles_n = (int)cdiv(p.d, kTile);
+    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16).rows);
+    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16).cols);
     o.nsplit = 1;
     o.nblocks = p.BH * o.tiles_m * o.tiles_n;
     o.rows = n;
@@ -313,22 +319,11 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   const int64_t dh = (int64_t)p.d * p.h;
   FwdArgs f{};
   int ns = 0;
-  if (apply_too) {
-    FwdSeg& g = f.seg[ns++];
-    g.kind = FWD_APPLY;
-    g.tiles_m = (int)cdiv(n, kTile);
-    g.tiles_n = (int)cdiv(p.h, kTile);
-    g.nblocks = p.BH * g.tiles_m * g.tiles_n;
-    g.rows = n;
-    g.a0 = op(c.q + s0 * p.d * p.esz, p.d, c.dsc->n_q * p.d);
-    g.out0 = c.ws + p.off_hq;
-    g.out_inst = p.cap * p.h;
-  }
   {
     FwdSeg& g = f.seg[ns++];
     g.kind = FWD_UPDATE;
-    g.tiles_m = (int)cdiv(n, kTile);
-    g.tiles_n = (int)cdiv(p.h, kTile);
+    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_UPDATE, p.bf16).rows);
+    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_UPDATE, p.bf16).cols);
     g.nblocks = p.BH * g.tiles_m * g.tiles_n;
     g.rows = n;
     g.a0 = op(c.k + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
@@ -340,8 +335,19 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.eta = c.eta + s0;
     g.eta_inst = c.dsc->n_kv;
   }
+  if (apply_too) {
+    FwdSeg& g = f.seg[ns++];
+    g.kind = FWD_APPLY;
+    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_APPLY, p.bf16).rows);
+    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_APPLY, p.bf16).cols);
+    g.nblocks = p.BH * g.tiles_m * g.tiles_n;
+    g.rows = n;
+    g.a0 = op(c.q + s0 * p.d * p.esz, p.d, c.dsc->n_q * p.d);
+    g.out0 = c.ws + p.off_hq;
+    g.out_inst = p.cap * p.h;
+  }
   f.nseg = ns;
-  f.total_blocks = f.seg[0].nblocks + (ns > 1 ? f.seg[1].nblocks : 0);
+  f.total_blocks = f.seg[0].nblocks + (ns > 1 ? f.seg[1].nblocks : 0);   // long tiles first
   f.d = p.d;
   f.h = p.h;
   f.w1 = c.wop[0];
@@ -353,29 +359,16 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
 
   BwdArgs b{};
   int nb = 0;
-  if (apply_too) {
-    BwdSeg& o = b.seg[nb++];
-    o.kind = BWD_OUT;
-    o.tiles_m = (int)cdiv(n, kTile);
-    o.tiles_n = (int)cdiv(p.d, kTile);
-    o.nsplit = 1;
-    o.nblocks = p.BH * o.tiles_m * o.tiles_n;
-    o.rows = n;
-    o.a0 = op(c.ws + p.off_hq, p.h, p.cap * p.h);
-    o.b0 = c.wop[1];
-    o.out = c.o + s0 * p.d * p.esz;
-    o.out_inst = c.dsc->n_q * p.d;
-  }
   // Gradient contractions, split over tokens; a split past the chunk's end
   // writes zeros so the update always sums p.nsplit partials.
-  const int64_t tj = cdiv(p.h, kTile), tm = cdiv(p.d, kTile);
+  const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
   {
     BwdSeg& g = b.seg[nb++];
     g.kind = BWD_GRAD13;
-    g.tiles_m = (int)tj;
-    g.tiles_n = (int)tm;
+    g.tiles_m = (int)cdiv(p.h, g13.rows);
+    g.tiles_n = (int)cdiv(p.d, g13.cols);
     g.nsplit = p.nsplit;
-    g.nblocks = (int)(p.BH * tj * tm * p.nsplit);
+    g.nblocks = p.BH * g.tiles_m * g.tiles_n * p.nsplit;
     g.rows = n;
     g.split_len = p.split_len;
     g.a0 = op(c.ws + p.off_upd[1], p.h, p.C * p.h);   // eta dz1
@@ -388,10 +381,10 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   {
     BwdSeg& g = b.seg[nb++];
     g.kind = BWD_GRAD2;
-    g.tiles_m = (int)tm;
-    g.tiles_n = (int)tj;
+    g.tiles_m = (int)cdiv(p.d, g2.rows);
+    g.tiles_n = (int)cdiv(p.h, g2.cols);
     g.nsplit = p.nsplit;
-    g.nblocks = (int)(p.BH * tj * tm * p.nsplit);
+    g.nblocks = p.BH * g.tiles_m * g.tiles_n * p.nsplit;
     g.rows = n;
     g.split_len = p.split_len;
     g.a0 = op(c.v + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
@@ -399,6 +392,19 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.out = c.ws + p.off_step;
     g.out_inst = 3 * dh;
     g.out_split = (int64_t)p.BH * 3 * dh;
+  }
+  if (apply_too) {
+    BwdSeg& o = b.seg[nb++];
+    o.kind = BWD_OUT;
+    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16).rows);
+    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16).cols);
+    o.nsplit = 1;
+    o.nblocks = p.BH * o.tiles_m * o.tiles_n;
+    o.rows = n;
+    o.a0 = op(c.ws + p.off_hq, p.h, p.cap * p.h);
+    o.b0 = c.wop[1];
+    o.out = c.o + s0 * p.d * p.esz;
+    o.out_inst = c.dsc->n_q * p.d;
   }
   b.nseg = nb;
   b.total_blocks = 0;

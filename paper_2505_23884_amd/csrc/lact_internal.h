@@ -7,8 +7,7 @@
 
 namespace lact {
 
-constexpr int kTile = 128;        // output tile edge of every MFMA contraction
-constexpr int kThreads = 256;     // 4 waves of 64 lanes
+constexpr int kTile = 128;        // output tile edge of the Newton-Schulz products lanes
 constexpr int kMaxDim = 4096;     // envelope for d and h
 constexpr int kMaxSplit = 64;     // split-K ways of the gradient contraction
 
@@ -27,7 +26,7 @@ enum FwdKind : int { FWD_APPLY = 0, FWD_UPDATE = 1 };
 struct FwdSeg {
   int kind;
   int nblocks;          // instances * tiles_m * tiles_n
-  int tiles_m, tiles_n; // token tiles, hidden tiles
+  int tiles_m, tiles_n; // hidden tiles (output rows), token tiles
   int64_t rows;         // tokens in this segment
   Operand a0, a1;       // APPLY: q;  UPDATE: k, v            (token-major, kmajor)
   void* out0;           // APPLY: hidden of the queries [rows x h]
@@ -125,6 +124,14 @@ struct NsPrepArgs {
   int64_t dh;
   int blocks_per_slot;  // blocks of 4096 elements per slot
 };
+
+// Workgroup tile of a contraction kind: output rows x output columns, threads.
+struct TileShape {
+  int rows, cols, threads;
+};
+TileShape fwd_tile(int kind, bool io_bf16);   // rows = hidden units, cols = tokens
+TileShape bwd_tile(int kind, bool io_bf16);   // OUT: features x tokens; GRAD13: hidden x
+                                              // features; GRAD2: features x hidden
 
 // Launchers (io_bf16 selects bf16 MFMA operands, otherwise fp32).
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s);

@@ -1,24 +1,29 @@
 // gfx950 kernels of the LaCT fast-weight layer forward.
 //
-// Every contraction of the path is one 128 x 128 output tile per workgroup
-// (256 threads = 4 waves, each wave a 64 x 64 quarter built from 2 x 2
-// v_mfma_f32_32x32x16_bf16 blocks, or 32x32x2_f32 in fp32 mode), with fp32
+// Every contraction of the path is a batched GEMM tile loop with fp32
 // accumulation and a fused epilogue per kind:
 //
-//   FWD_APPLY   Z = Q W1^T, Q W3^T          -> hidden SiLU(Z1) o Z3       (apply, §3.1 SwiGLU eq.)
-//   FWD_UPDATE  Z = K W1^T, K W3^T, D = V W2 -> eta*hidden, eta*dz1, eta*dz3
-//               the key forward and the backward to the hidden units of
-//               grad sum_i eta_i (-f_W(k_i)^T v_i)               (§3.1 loss and chunk-gradient eqs.)
-//   BWD_OUT     O = hidden W2^T                                    (apply, second matmul)
+//   FWD_APPLY   Z^T = W1 Q^T, W3 Q^T          -> hidden SiLU(Z1) o Z3        (apply, §3.1 SwiGLU eq.)
+//   FWD_UPDATE  Z^T = W1 K^T, W3 K^T, D^T = (V W2)^T
+//               -> eta*hidden, eta*dz1, eta*dz3: the key forward and the
+//               backward to the hidden units of grad sum_i eta_i (-f_W(k_i)^T v_i)
+//               (§3.1 loss and chunk-gradient eqs.; Alg. 1, update)
+//   BWD_OUT     O^T = W2 hidden^T                                  (apply, second matmul)
 //   BWD_GRAD13  P1 = (eta dz1)^T K,  P3 = (eta dz3)^T K             (gradient matmuls, -g1, -g3)
 //   BWD_GRAD2   P2 = V^T (eta hidden)                              (-g2)
+//   NS_*        Newton-Schulz products (Muon, §3.2; App. A)
 //
-// Operands live in HBM either K-contiguous ("kmajor", row-major [rows x K])
-// or row-contiguous ("mn", row-major [K x rows], the token-major layout of
-// the gradient contractions). Both are staged through LDS as 128 rows x 64
-// bytes (32 bf16 or 16 fp32 of K) per operand, double-buffered; mn operands
-// are transposed in registers on the way (4 K rows x 8 or 4 elements per
-// thread) so that every MFMA fragment is one 16-byte LDS read.
+// 16-bit operands (bf16 I/O; fp16 for Newton-Schulz) run on
+// v_mfma_f32_32x32x16_{bf16,f16}. A workgroup of WM x WN waves owns a tile of
+// (32*MI*WM) x (32*NI*WN) outputs, every wave (32*MI) x (32*NI). Operand tiles
+// of 32 K go from HBM to LDS by raw-buffer DMA (buffer_load_dwordx4 ... lds)
+// into a ring of NSTAGE stages. An operand is either K-contiguous in HBM
+// ("k": row-major [rows x K], kept as 64-byte rows in LDS) or row-contiguous
+// ("mn": row-major [K x rows], the token-major layout; kept as 32 K rows in
+// LDS and read with ds_read_b64_tr_b16, which returns MFMA fragments of the
+// transposed operand). fp32 I/O runs on v_mfma_f32_32x32x2_f32 with a
+// register-staged double buffer (the transposition of mn operands happens in
+// registers there).
 #include "lact_internal.h"
 
 namespace lact {
@@ -32,7 +37,7 @@ typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 constexpr int kRowBytes = 64;
-constexpr int kTileBytes = kTile * kRowBytes;   // one operand tile in LDS
+constexpr int kTileBytes = kTile * kRowBytes;   // a 128-row operand tile (fp32 path)
 
 template <typename T> struct Tr;
 template <> struct Tr<__bf16> {   // 32 K per tile, 8 elements per 16 bytes
@@ -45,21 +50,24 @@ template <> struct Tr<float> {    // 16 K per tile, 4 elements per 16 bytes
   static constexpr int BK = 16, E = 4, KG = 4;
 };
 
-// LDS byte offset of 16-byte chunk `chunk` (0..3) of tile row `row`. The XOR
-// keeps the 16 (or 8) lanes that read one MFMA fragment column on distinct
-// banks both for a 64-bank and a 32-bank LDS.
+// LDS byte offset of 16-byte chunk `chunk` (0..3) of row `row` of a
+// K-contiguous tile. The XOR with row bits 2-3 keeps the 16-lane groups that
+// serve one MFMA fragment read (16 consecutive rows, one chunk) free of bank
+// conflicts (measured on gfx950 with SQ_LDS_BANK_CONFLICT).
+__device__ __forceinline__ int lds_swz(int row) { return (row >> 2) & 3; }
 __device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * kRowBytes + ((chunk ^ (((row >> 1) ^ (row >> 3)) & 3)) << 4);
+  return row * kRowBytes + ((chunk ^ lds_swz(row)) << 4);
 }
 
-// Row permutation of mn-operand tiles: the transposing store writes 8 (bf16)
-// or 4 (fp32) rows per thread; rotating rows by the thread's row block puts
-// the lanes of one store instruction on distinct bank groups.
-template <typename T>
-__device__ __forceinline__ int mn_row(int r) {
-  if constexpr (sizeof(T) == 2) return r ^ ((r >> 3) & 3);
-  else return r ^ ((r >> 2) & 3);
-}
+// XOR swizzle of the 16-byte chunks of a row-contiguous tile: the four K rows
+// read by one 16-lane group of a transpose read land on distinct chunk
+// positions (measured conflict-free).
+__device__ __forceinline__ int swz_mn(int kr) { return (kr & 3) << 2; }
+
+// Row permutation of fp32 row-contiguous tiles (register path): the
+// transposing store writes 4 rows per thread; rotating rows by the thread's
+// row block spreads one store instruction over distinct bank groups.
+__device__ __forceinline__ int mn_row32(int r) { return r ^ ((r >> 2) & 3); }
 
 __device__ __forceinline__ int xcd_remap(int bid, int n) {
   // Workgroups are dispatched round-robin over the 8 XCDs; give every XCD a
@@ -71,17 +79,116 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
 // One operand restricted to the current output tile.
 struct View {
   const uint8_t* p;   // element (tile row 0, k 0)
-  int64_t ld_b;       // bytes between rows (kmajor) or between K rows (mn)
+  int64_t ld_b;       // bytes between rows (k) or between K rows (mn)
   int64_t nrows;      // valid rows from tile row 0
   int64_t nk;         // valid K from k 0
 };
+
+// ---------------------------------------------------------------------------
+// Contraction kinds. Operands 0..NA-1 are A (tile rows = output rows),
+// NA..NA+NB-1 are B (tile rows = output columns); accumulator p multiplies
+// A[pa(p)] by B[pb(p)]. Bit o of MN marks operand o as row-contiguous.
+// WM x WN waves, each (32*MI) x (32*NI); NSTAGE LDS stages; DBUF: fragment
+// registers double-buffered across K-substeps.
+template <int NA_, int NB_, int NACC_, uint32_t MN_, int WM_, int WN_, int MI_, int NI_, int NSTAGE_,
+          bool DBUF_>
+struct KindBase {
+  static constexpr int NA = NA_, NB = NB_, NACC = NACC_, NOPS = NA_ + NB_;
+  static constexpr uint32_t MN = MN_;
+  static constexpr int WM = WM_, WN = WN_, MI = MI_, NI = NI_, NSTAGE = NSTAGE_;
+  static constexpr bool DBUF = DBUF_;
+  static constexpr int THREADS = 64 * WM * WN;
+  static constexpr int ROWS_A = 32 * MI * WM, ROWS_B = 32 * NI * WN;   // workgroup tile
+  static constexpr bool is_mn(int o) { return (MN >> o) & 1u; }
+  static constexpr int rows(int o) { return o < NA ? ROWS_A : ROWS_B; }
+  // 16-bit stage layout: 32 K x rows x 2 bytes per operand
+  static constexpr int op_bytes(int o) { return rows(o) * 64; }
+  static constexpr int op_off(int o) {
+    int s = 0;
+    for (int i = 0; i < o; ++i) s += op_bytes(i);
+    return s;
+  }
+  static constexpr int STAGE = op_off(NOPS);
+  // which half of the block (threads 0-127 / 128-255) loads mn operand o (fp32 path)
+  static constexpr int mn_half(int o) { return __builtin_popcount(MN & ((1u << o) - 1u)) & 1; }
+};
+
+#define LACT_KIND(NAME, NA, NB, NACC, MNMASK, WM, WN, MI, NI, NS, DBUF, PA, PB) \
+  struct NAME : KindBase<NA, NB, NACC, MNMASK, WM, WN, MI, NI, NS, DBUF> {         \
+    static constexpr int pa(int p) { return PA; }                                  \
+    static constexpr int pb(int p) { return PB; }                                  \
+  }
+
+// 16-bit shapes: 8 waves (2 per SIMD); multi-accumulator kinds use 64 x 64
+// waves (128 x 256 tiles), single-accumulator kinds 128 x 64 (256 x 256).
+// Apply GEMM-1, hidden-major: A = W1, W3 (hidden rows), B = Q (token rows).
+LACT_KIND(KApply16, 2, 1, 2, 0u, 2, 4, 2, 2, 4, true, p, 0 * p);
+// Key forward + hidden backward: A = W1, W3, W2 (W2 read down its columns),
+// B = K, V; accumulators Z1^T, Z3^T and D^T = (V W2)^T.
+LACT_KIND(KUpdate16, 3, 2, 3, 1u << 2, 2, 4, 2, 2, 2, false, p, (p == 2 ? 1 : 0));
+// Apply GEMM-2, feature-major: A = W2 (feature rows), B = hidden (token rows).
+LACT_KIND(KOut16, 1, 1, 1, 0u, 2, 4, 4, 2, 4, true, 0 * p, 0 * p);
+// Gradients: A = eta dz1, eta dz3 (hidden rows), B = K (feature rows), all token-major.
+LACT_KIND(KGrad13_16, 2, 1, 2, 7u, 2, 4, 2, 2, 4, true, p, 0 * p);
+// A = V (feature rows), B = eta hidden (hidden rows), token-major.
+LACT_KIND(KGrad2_16, 1, 1, 1, 3u, 2, 4, 4, 2, 4, true, 0 * p, 0 * p);
+// fp32 shapes: 4 waves of 64 x 64 (128 x 128 tiles), register path.
+LACT_KIND(KApply32, 2, 1, 2, 0u, 2, 2, 2, 2, 2, false, p, 0 * p);
+LACT_KIND(KUpdate32, 3, 2, 3, 1u << 2, 2, 2, 2, 2, 2, false, p, (p == 2 ? 1 : 0));
+LACT_KIND(KOut32, 1, 1, 1, 0u, 2, 2, 2, 2, 2, false, 0 * p, 0 * p);
+LACT_KIND(KGrad13_32, 2, 1, 2, 7u, 2, 2, 2, 2, 2, false, p, 0 * p);
+LACT_KIND(KGrad2_32, 1, 1, 1, 3u, 2, 2, 2, 2, 2, false, 0 * p, 0 * p);
+// Newton-Schulz products (4 waves, 128 x 128): both operands K-contiguous,
+// both row-contiguous, or only the second (B Y read down the columns of Y).
+LACT_KIND(KNsK, 1, 1, 1, 0u, 2, 2, 2, 2, 4, true, 0 * p, 0 * p);
+LACT_KIND(KNsMN, 1, 1, 1, 3u, 2, 2, 2, 2, 4, true, 0 * p, 0 * p);
+LACT_KIND(KNsBY, 1, 1, 1, 2u, 2, 2, 2, 2, 4, true, 0 * p, 0 * p);
+#undef LACT_KIND
+
+template <typename T> struct Kinds;
+template <> struct Kinds<__bf16> {
+  using Apply = KApply16;
+  using Update = KUpdate16;
+  using Out = KOut16;
+  using Grad13 = KGrad13_16;
+  using Grad2 = KGrad2_16;
+};
+template <> struct Kinds<float> {
+  using Apply = KApply32;
+  using Update = KUpdate32;
+  using Out = KOut32;
+  using Grad13 = KGrad13_32;
+  using Grad2 = KGrad2_32;
+};
+
+template <class K>
+using Acc = f32x16_t[K::NACC][K::MI][K::NI];
+
+// Wave coordinates inside the workgroup and the epilogue map of accumulator
+// register r of block (mi, ni) (32x32 MFMA output layout).
+template <class K>
+__device__ __forceinline__ int wave_m() { return (threadIdx.x >> 6) / K::WN; }
+template <class K>
+__device__ __forceinline__ int wave_n() { return (threadIdx.x >> 6) % K::WN; }
+template <class K>
+__device__ __forceinline__ int acc_row(int mi, int r) {
+  const int lane = threadIdx.x & 63;
+  return wave_m<K>() * 32 * K::MI + mi * 32 + ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3);
+}
+template <class K>
+__device__ __forceinline__ int acc_col(int ni) {
+  return wave_n<K>() * 32 * K::NI + ni * 32 + (threadIdx.x & 31);
+}
+
+// ===========================================================================
+// fp32 register path (4 waves, 128 x 128, MI = NI = 2)
 
 template <typename T>
 __device__ __forceinline__ void gload_k(u32x4_t (&r)[4], const View& v, int64_t k0) {
   constexpr int E = Tr<T>::E;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int q = threadIdx.x + i * kThreads;
+    const int q = threadIdx.x + i * 256;
     const int row = q >> 2, c = q & 3;
     const int64_t k = k0 + c * E;
     u32x4_t x = {0u, 0u, 0u, 0u};
@@ -91,11 +198,10 @@ __device__ __forceinline__ void gload_k(u32x4_t (&r)[4], const View& v, int64_t 
   }
 }
 
-template <typename T>
 __device__ __forceinline__ void sstore_k(uint8_t* tile, const u32x4_t (&r)[4]) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int q = threadIdx.x + i * kThreads;
+    const int q = threadIdx.x + i * 256;
     *reinterpret_cast<u32x4_t*>(tile + lds_off(q >> 2, q & 3)) = r[i];
   }
 }
@@ -115,199 +221,84 @@ __device__ __forceinline__ void gload_mn(u32x4_t (&r)[4], const View& v, int64_t
   }
 }
 
-template <typename T>
-__device__ __forceinline__ void sstore_mn(uint8_t* tile, const u32x4_t (&r)[4], int tt) {
-  if constexpr (sizeof(T) == 2) {
-    const int kg = tt & 7, mb = tt >> 3;
+// fp32: a thread holds 4 K rows x 4 elements; write 4 rows x 4 K.
+__device__ __forceinline__ void sstore_mn32(uint8_t* tile, const u32x4_t (&r)[4], int tt) {
+  const int kg = tt & 3, mb = tt >> 2;
 #pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      const uint32_t x0 = r[0][m >> 1], x1 = r[1][m >> 1], x2 = r[2][m >> 1], x3 = r[3][m >> 1];
-      uint32_t lo, hi;
-      if (m & 1) {
-        lo = (x0 >> 16) | (x1 & 0xFFFF0000u);
-        hi = (x2 >> 16) | (x3 & 0xFFFF0000u);
-      } else {
-        lo = (x0 & 0xFFFFu) | (x1 << 16);
-        hi = (x2 & 0xFFFFu) | (x3 << 16);
-      }
-      const int row = mn_row<T>(mb * 8 + m);
-      *reinterpret_cast<u32x2_t*>(tile + lds_off(row, kg >> 1) + ((kg & 1) << 3)) = u32x2_t{lo, hi};
-    }
-  } else {
-    const int kg = tt & 3, mb = tt >> 2;
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      const int row = mn_row<T>(mb * 4 + m);
-      *reinterpret_cast<u32x4_t*>(tile + lds_off(row, kg)) = u32x4_t{r[0][m], r[1][m], r[2][m], r[3][m]};
-    }
+  for (int m = 0; m < 4; ++m) {
+    const int row = mn_row32(mb * 4 + m);
+    *reinterpret_cast<u32x4_t*>(tile + lds_off(row, kg)) = u32x4_t{r[0][m], r[1][m], r[2][m], r[3][m]};
   }
 }
 
-template <typename T>
-__device__ __forceinline__ u32x4_t frag(const uint8_t* tile, int row, int chunk, bool mn) {
-  const int pr = mn ? mn_row<T>(row) : row;
+__device__ __forceinline__ u32x4_t frag32(const uint8_t* tile, int row, int chunk, bool mn) {
+  const int pr = mn ? mn_row32(row) : row;
   return *reinterpret_cast<const u32x4_t*>(tile + lds_off(pr, chunk));
 }
 
-// ---------------------------------------------------------------------------
-// Contraction kinds: operands 0..NA-1 are A (tile rows = output rows),
-// NA..NA+NB-1 are B (tile rows = output columns); accumulator p multiplies
-// A[pa(p)] by B[pb(p)]. Bit o of MN marks operand o as row-contiguous.
-template <int NA_, int NB_, int NACC_, uint32_t MN_>
-struct KindBase {
-  static constexpr int NA = NA_, NB = NB_, NACC = NACC_, NOPS = NA_ + NB_;
-  static constexpr uint32_t MN = MN_;
-  static constexpr bool is_mn(int o) { return (MN >> o) & 1u; }
-  // which half of the block (threads 0-127 / 128-255) loads mn operand o
-  static constexpr int mn_half(int o) { return __builtin_popcount(MN & ((1u << o) - 1u)) & 1; }
-};
-struct KApply : KindBase<1, 2, 2, 0u> {
-  static constexpr int NSTAGE = 4;
-  static constexpr int pa(int) { return 0; }
-  static constexpr int pb(int p) { return p; }
-};
-struct KUpdate : KindBase<2, 3, 3, 1u << 4> {     // W2 (operand 4) is read transposed
-  static constexpr int NSTAGE = 3;
-  static constexpr int pa(int p) { return p == 2 ? 1 : 0; }
-  static constexpr int pb(int p) { return p; }
-};
-struct KOut : KindBase<1, 1, 1, 0u> {
-  static constexpr int NSTAGE = 4;
-  static constexpr int pa(int) { return 0; }
-  static constexpr int pb(int) { return 0; }
-};
-struct KGrad13 : KindBase<2, 1, 2, 7u> {
-  static constexpr int NSTAGE = 3;
-  static constexpr int pa(int p) { return p; }
-  static constexpr int pb(int) { return 0; }
-};
-struct KGrad2 : KindBase<1, 1, 1, 3u> {
-  static constexpr int NSTAGE = 4;
-  static constexpr int pa(int) { return 0; }
-  static constexpr int pb(int) { return 0; }
-};
-
-// Newton-Schulz products: both operands K-contiguous, both row-contiguous, or
-// only the second row-contiguous (B Y with Y read down its columns).
-using KNsK = KOut;
-using KNsMN = KGrad2;
-struct KNsBY : KindBase<1, 1, 1, 2u> {
-  static constexpr int NSTAGE = 4;
-  static constexpr int pa(int) { return 0; }
-  static constexpr int pb(int) { return 0; }
-};
-
-template <typename T, class K>
-__device__ __forceinline__ void compute_ktile(const uint8_t* buf, f32x16_t (&acc)[K::NACC][2][2]) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int arow = (w >> 1) * 64 + (lane & 31), brow = (w & 1) * 64 + (lane & 31);
+template <class K>
+__device__ __forceinline__ void compute_ktile32(const uint8_t* buf, Acc<K>& acc) {
+  static_assert(K::MI == 2 && K::NI == 2 && K::THREADS == 256, "fp32 path shape");
+  const int lane = threadIdx.x & 63;
+  const int arow = wave_m<K>() * 64 + (lane & 31), brow = wave_n<K>() * 64 + (lane & 31);
   const int half = lane >> 5;
-  if constexpr (sizeof(T) == 2) {
+  // lanes 0-31 hold K 0..7 of the tile, lanes 32-63 K 8..15; MFMA s contracts
+  // K s (first half-wave) and K 8+s (second half-wave)
+  float af[K::NA][2][8], bf[K::NB][2][8];
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      u32x4_t af[K::NA][2], bf[K::NB][2];
+  for (int o = 0; o < K::NA; ++o)
 #pragma unroll
-      for (int o = 0; o < K::NA; ++o)
+    for (int mi = 0; mi < 2; ++mi) {
+      // whole-vector bit casts: a bit cast of one vector element is not
+      // reliable with this compiler (it reads element 0)
+      const f32x4_t lo = __builtin_bit_cast(f32x4_t, frag32(buf + o * kTileBytes, arow + mi * 32, 2 * half, K::is_mn(o)));
+      const f32x4_t hi =
+          __builtin_bit_cast(f32x4_t, frag32(buf + o * kTileBytes, arow + mi * 32, 2 * half + 1, K::is_mn(o)));
 #pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-          af[o][mi] = frag<T>(buf + o * kTileBytes, arow + mi * 32, 2 * s + half, K::is_mn(o));
+      for (int e = 0; e < 4; ++e) {
+        af[o][mi][e] = lo[e];
+        af[o][mi][4 + e] = hi[e];
+      }
+    }
 #pragma unroll
-      for (int o = 0; o < K::NB; ++o)
+  for (int o = 0; o < K::NB; ++o)
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      const uint8_t* t = buf + (K::NA + o) * kTileBytes;
+      const f32x4_t lo = __builtin_bit_cast(f32x4_t, frag32(t, brow + ni * 32, 2 * half, K::is_mn(K::NA + o)));
+      const f32x4_t hi = __builtin_bit_cast(f32x4_t, frag32(t, brow + ni * 32, 2 * half + 1, K::is_mn(K::NA + o)));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        bf[o][ni][e] = lo[e];
+        bf[o][ni][4 + e] = hi[e];
+      }
+    }
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+#pragma unroll
+    for (int p = 0; p < K::NACC; ++p)
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
         for (int ni = 0; ni < 2; ++ni)
-          bf[o][ni] = frag<T>(buf + (K::NA + o) * kTileBytes, brow + ni * 32, 2 * s + half,
-                                      K::is_mn(K::NA + o));
-#pragma unroll
-      for (int p = 0; p < K::NACC; ++p)
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-          for (int ni = 0; ni < 2; ++ni)
-            if constexpr (__is_same(T, _Float16))
-              acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
-                  __builtin_bit_cast(f16x8_t, af[K::pa(p)][mi]),
-                  __builtin_bit_cast(f16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
-            else
-              acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                  __builtin_bit_cast(bf16x8_t, af[K::pa(p)][mi]),
-                  __builtin_bit_cast(bf16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
-    }
-  } else {
-    // fp32: lanes 0-31 hold K 0..7 of the tile, lanes 32-63 K 8..15; MFMA s
-    // contracts K s (first half-wave) and K 8+s (second half-wave).
-    float af[K::NA][2][8], bf[K::NB][2][8];
-#pragma unroll
-    for (int o = 0; o < K::NA; ++o)
-#pragma unroll
-      for (int mi = 0; mi < 2; ++mi) {
-        // whole-vector bit casts: a bit cast of one vector element is not
-        // reliable with this compiler (it reads element 0)
-        const f32x4_t lo = __builtin_bit_cast(
-            f32x4_t, frag<T>(buf + o * kTileBytes, arow + mi * 32, 2 * half, K::is_mn(o)));
-        const f32x4_t hi = __builtin_bit_cast(
-            f32x4_t, frag<T>(buf + o * kTileBytes, arow + mi * 32, 2 * half + 1, K::is_mn(o)));
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          af[o][mi][e] = lo[e];
-          af[o][mi][4 + e] = hi[e];
-        }
-      }
-#pragma unroll
-    for (int o = 0; o < K::NB; ++o)
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const uint8_t* t = buf + (K::NA + o) * kTileBytes;
-        const f32x4_t lo =
-            __builtin_bit_cast(f32x4_t, frag<T>(t, brow + ni * 32, 2 * half, K::is_mn(K::NA + o)));
-        const f32x4_t hi =
-            __builtin_bit_cast(f32x4_t, frag<T>(t, brow + ni * 32, 2 * half + 1, K::is_mn(K::NA + o)));
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          bf[o][ni][e] = lo[e];
-          bf[o][ni][4 + e] = hi[e];
-        }
-      }
-#pragma unroll
-    for (int s = 0; s < 8; ++s)
-#pragma unroll
-      for (int p = 0; p < K::NACC; ++p)
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-          for (int ni = 0; ni < 2; ++ni)
-            acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                af[K::pa(p)][mi][s], bf[K::pb(p)][ni][s], acc[p][mi][ni], 0, 0, 0);
-  }
+          acc[p][mi][ni] =
+              __builtin_amdgcn_mfma_f32_32x32x2f32(af[K::pa(p)][mi][s], bf[K::pb(p)][ni][s], acc[p][mi][ni], 0, 0, 0);
 }
 
-// fp32 operands: register-staged double buffer (global -> VGPR -> LDS, with
-// the in-register transposition of row-contiguous operands).
-template <typename T, class K>
-__device__ __forceinline__ void mainloop_regs(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk,
-                                              f32x16_t (&acc)[K::NACC][2][2]) {
-  constexpr int BK = Tr<T>::BK;
-#pragma unroll
-  for (int p = 0; p < K::NACC; ++p)
-#pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[p][mi][ni][r] = 0.f;
+template <class K>
+__device__ __forceinline__ void mainloop_regs(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk, Acc<K>& acc) {
+  constexpr int BK = 16;
   const int nkt = (int)((nk + BK - 1) / BK);
   if (nkt <= 0) return;
-
   u32x4_t st[K::NOPS][4];
   auto gload = [&](int64_t k0) {
 #pragma unroll
     for (int o = 0; o < K::NOPS; ++o) {
-      if constexpr (true) {
-        if (K::is_mn(o)) {
-          const int tt = threadIdx.x - 128 * K::mn_half(o);
-          if (tt >= 0 && tt < 128) gload_mn<T>(st[o], ops[o], k0, tt);
-        } else {
-          gload_k<T>(st[o], ops[o], k0);
-        }
+      if (K::is_mn(o)) {
+        const int tt = threadIdx.x - 128 * K::mn_half(o);
+        if (tt >= 0 && tt < 128) gload_mn<float>(st[o], ops[o], k0, tt);
+      } else {
+        gload_k<float>(st[o], ops[o], k0);
       }
     }
   };
@@ -316,13 +307,12 @@ __device__ __forceinline__ void mainloop_regs(uint8_t* smem, const View (&ops)[K
     for (int o = 0; o < K::NOPS; ++o) {
       if (K::is_mn(o)) {
         const int tt = threadIdx.x - 128 * K::mn_half(o);
-        if (tt >= 0 && tt < 128) sstore_mn<T>(buf + o * kTileBytes, st[o], tt);
+        if (tt >= 0 && tt < 128) sstore_mn32(buf + o * kTileBytes, st[o], tt);
       } else {
-        sstore_k<T>(buf + o * kTileBytes, st[o]);
+        sstore_k(buf + o * kTileBytes, st[o]);
       }
     }
   };
-
   gload(0);
   sstore(smem);
   __syncthreads();
@@ -330,27 +320,14 @@ __device__ __forceinline__ void mainloop_regs(uint8_t* smem, const View (&ops)[K
     const uint8_t* cur = smem + (kt & 1) * K::NOPS * kTileBytes;
     const bool more = kt + 1 < nkt;
     if (more) gload((int64_t)(kt + 1) * BK);
-    compute_ktile<T, K>(cur, acc);
+    compute_ktile32<K>(cur, acc);
     if (more) sstore(smem + ((kt + 1) & 1) * K::NOPS * kTileBytes);
     __syncthreads();
   }
 }
 
-// ---------------------------------------------------------------------------
-// 16-bit operands: direct global -> LDS DMA (global_load_lds_dwordx4) into a
-// ring of K::NSTAGE stages, K::NSTAGE - 1 k-tiles in flight, no register
-// staging. Row-contiguous operands keep their HBM layout in LDS (32 K rows x
-// 256 bytes) and are read with ds_read_b64_tr_b16, which hands every lane
-// four consecutive K of one row of the operand.
-
-// A 16-byte page of zeros: out-of-range lanes load from it, so partial tiles
-// arrive zero-padded in LDS.
-__device__ __attribute__((aligned(64))) uint32_t g_zero_page[16];
-
-// XOR swizzle of the 16-byte chunks of a row-contiguous tile (256-byte rows):
-// the four K rows read by one 16-lane group of a transpose read land on
-// distinct chunk positions.
-__device__ __forceinline__ int swz_mn(int kr) { return (kr & 3) << 2; }
+// ===========================================================================
+// 16-bit DMA path
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -360,290 +337,421 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) const void gbl_void_t;
-typedef __attribute__((ext_vector_type(4))) short s16x4_t;
-typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+__device__ __forceinline__ lds_void_t* to_lds(const void* p) { return (lds_void_t*)(p); }
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)to_lds(p); }
 
-__device__ __forceinline__ lds_void_t* to_lds(const void* p) {
-  return (lds_void_t*)(p);
-}
+// Out-of-range buffer offset: the load returns zeros, so partial tiles arrive
+// zero-padded in LDS.
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr int kRawBufferFlags = 0x00020000;
 
-// Issue this wave's two 1 KiB DMA loads of one operand tile (512 chunks).
-template <bool MN>
-__device__ __forceinline__ void dma_tile(uint8_t* tile, const View& v, int64_t k0) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+// Slots: an operand tile of R rows is R*4 slots of 16 bytes; lane `tid` of
+// the workgroup fills slots tid, tid + THREADS, ... (so each wave instruction
+// writes 1 KiB of consecutive LDS).
+template <class K, int O>
+struct Dma {
+  static constexpr bool MN = K::is_mn(O);
+  static constexpr int ROWS = K::rows(O);
+  static constexpr int SLOTS = ROWS * 4 / K::THREADS;   // per lane
+  static_assert(SLOTS >= 1 && SLOTS <= 4 && ROWS * 4 % K::THREADS == 0, "slot split");
+  static constexpr int CPR = ROWS / 8;                   // chunks per K row (mn)
+
+  static __device__ __forceinline__ void offsets(uint32_t (&vo)[4], const View& v) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int base = w * 128 + i * 64;     // first 16-byte slot of this instruction
-    const int p = base + lane;
-    const uint8_t* src;
-    if (!MN) {
-      const int row = p >> 2;
-      const int c = (p & 3) ^ (((row >> 1) ^ (row >> 3)) & 3);
-      const int64_t k = k0 + c * 8;
-      src = (row < v.nrows && k < v.nk) ? v.p + row * v.ld_b + k * 2
-                                        : reinterpret_cast<const uint8_t*>(g_zero_page);
-    } else {
-      const int kr = p >> 4;
-      const int c = (p & 15) ^ swz_mn(kr);
-      const int64_t k = k0 + kr;
-      src = (k < v.nk && c * 8 < v.nrows) ? v.p + k * v.ld_b + c * 16
-                                          : reinterpret_cast<const uint8_t*>(g_zero_page);
+    for (int i = 0; i < SLOTS; ++i) {
+      const int p = i * K::THREADS + threadIdx.x;
+      if (!MN) {
+        const int row = p >> 2, c = (p & 3) ^ lds_swz(p >> 2);
+        vo[i] = row < v.nrows ? (uint32_t)(row * v.ld_b + c * 16) : kOOB;
+      } else {
+        const int kr = p / CPR, c = (p % CPR) ^ swz_mn(p / CPR);
+        vo[i] = c * 8 < v.nrows ? (uint32_t)(kr * v.ld_b + c * 16) : kOOB;
+      }
     }
-    __builtin_amdgcn_global_load_lds((gbl_void_t*)src, to_lds(tile + base * 16), 16, 0, 0);
   }
+
+  // DMA of k-tile kt into `tile`: a raw buffer descriptor whose base advances
+  // with kt and whose size covers only the valid data, so K rows past the end
+  // (row-contiguous operands) load as zeros.
+  static __device__ __forceinline__ void issue(uint8_t* tile, const View& v, const uint32_t (&vo)[4], int kt) {
+    const uint8_t* base;
+    int64_t span;
+    if (!MN) {
+      base = v.p + (int64_t)kt * 64;
+      const int64_t rows = v.nrows < ROWS ? v.nrows : ROWS;
+      span = rows > 0 ? (rows - 1) * v.ld_b + 64 : 0;
+    } else {
+      base = v.p + (int64_t)kt * 32 * v.ld_b;
+      int64_t rows = v.nk - (int64_t)kt * 32;
+      rows = rows < 0 ? 0 : (rows > 32 ? 32 : rows);
+      span = rows * v.ld_b;
+    }
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)span, kRawBufferFlags);
+    const int w = threadIdx.x >> 6;
+#pragma unroll
+    for (int i = 0; i < SLOTS; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, to_lds(tile + (i * K::THREADS + w * 64) * 16), 16, vo[i], 0,
+                                               0, 0);
+  }
+};
+
+// Every operand of kind K, unrolled at compile time.
+template <class K, int O = 0>
+struct DmaAll {
+  static __device__ __forceinline__ void offsets(uint32_t (&vo)[K::NOPS][4], const View (&ops)[K::NOPS]) {
+    if constexpr (O < K::NOPS) {
+      Dma<K, O>::offsets(vo[O], ops[O]);
+      DmaAll<K, O + 1>::offsets(vo, ops);
+    }
+  }
+  static __device__ __forceinline__ void issue(uint8_t* st, const View (&ops)[K::NOPS],
+                                               const uint32_t (&vo)[K::NOPS][4], int kt) {
+    if constexpr (O < K::NOPS) {
+      Dma<K, O>::issue(st + K::op_off(O), ops[O], vo[O], kt);
+      DmaAll<K, O + 1>::issue(st, ops, vo, kt);
+    }
+  }
+};
+
+// LDS fragment reads are issued as inline asm, in program order, so that
+// lgkmcnt can be counted exactly (wait for one substep's fragments while the
+// next substep's reads are still in flight) and so that the compiler does not
+// drain the in-flight DMA before them (it cannot tell which stage they touch).
+__device__ __forceinline__ u32x4_t lds_read_b128(uint32_t a) {
+  u32x4_t r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(a));
+  return r;
 }
 
-// MFMA fragment (8 consecutive K of row rb + lane%32, K block 8*(lane/32) of
-// substep s) from a row-contiguous tile, by two transpose reads. Issued as
-// inline asm so the compiler does not drain the in-flight DMA before it (it
-// cannot tell which stage the read touches); the result is not ready until a
-// lgkm_ready() on it.
-__device__ __forceinline__ u32x4_t frag_tr(const uint8_t* tile, int rb, int s) {
+// K-contiguous fragment: 8 K of row `row`, 16-byte chunk `chunk`.
+__device__ __forceinline__ u32x4_t frag_k(const uint8_t* tile, int row, int chunk) {
+  return lds_read_b128(lds_addr(tile) + lds_off(row, chunk));
+}
+
+// Row-contiguous fragment (8 consecutive K of row rb + lane%32, K block
+// 8*(lane/32) of substep s) by two transpose reads from a tile with `pitch`
+// bytes per K row: within each 16-lane group source lane sl points at K row
+// k0 + sl/4, columns 4*(sl%4)..+3, and output lane i receives column i, rows
+// k0..k0+3.
+__device__ __forceinline__ u32x4_t frag_tr(const uint8_t* tile, int rb, int s, int pitch) {
   const int lane = threadIdx.x & 63, g = lane >> 4, sl = lane & 15;
   const int mn = rb + 16 * (g & 1) + 4 * (sl & 3);
   const int c = mn >> 3, hb = (mn >> 2) & 1;
-  const uint32_t base = (uint32_t)(uintptr_t)to_lds(tile);
+  const uint32_t base = lds_addr(tile);
   u32x2_t lo, hi;
   {
     const int kr = 16 * s + 8 * (g >> 1) + (sl >> 2);
-    const uint32_t a = base + kr * 256 + ((c ^ swz_mn(kr)) << 4) + (hb << 3);
+    const uint32_t a = base + kr * pitch + ((c ^ swz_mn(kr)) << 4) + (hb << 3);
     asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a));
   }
   {
     const int kr = 16 * s + 8 * (g >> 1) + 4 + (sl >> 2);
-    const uint32_t a = base + kr * 256 + ((c ^ swz_mn(kr)) << 4) + (hb << 3);
+    const uint32_t a = base + kr * pitch + ((c ^ swz_mn(kr)) << 4) + (hb << 3);
     asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(a));
   }
   return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
 }
 
-// Waits for outstanding LDS reads and makes `x` depend on the wait, so no use
-// of a transpose-read result is scheduled before its data has arrived.
-__device__ __forceinline__ void lgkm_ready(u32x4_t& x) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x));
-}
-
-template <typename T, class K>
-__device__ __forceinline__ void compute_ktile16(const uint8_t* buf, f32x16_t (&acc)[K::NACC][2][2]) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int ab = (w >> 1) * 64, bb = (w & 1) * 64;
-  const int arow = ab + (lane & 31), brow = bb + (lane & 31);
-  const int half = lane >> 5;
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    u32x4_t af[K::NA][2], bf[K::NB][2];
-#pragma unroll
-    for (int o = 0; o < K::NA; ++o)
-#pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
-        af[o][mi] = K::is_mn(o) ? frag_tr(buf + o * kTileBytes, ab + mi * 32, s)
-                                : frag<T>(buf + o * kTileBytes, arow + mi * 32, 2 * s + half, false);
-#pragma unroll
-    for (int o = 0; o < K::NB; ++o)
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
-        bf[o][ni] = K::is_mn(K::NA + o)
-                        ? frag_tr(buf + (K::NA + o) * kTileBytes, bb + ni * 32, s)
-                        : frag<T>(buf + (K::NA + o) * kTileBytes, brow + ni * 32, 2 * s + half, false);
-    if constexpr (K::MN != 0u) {
-#pragma unroll
-      for (int o = 0; o < K::NA; ++o)
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-          if (K::is_mn(o)) lgkm_ready(af[o][mi]);
-#pragma unroll
-      for (int o = 0; o < K::NB; ++o)
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-          if (K::is_mn(K::NA + o)) lgkm_ready(bf[o][ni]);
-    }
-#pragma unroll
-    for (int p = 0; p < K::NACC; ++p)
-#pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-          if constexpr (__is_same(T, _Float16))
-            acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
-                __builtin_bit_cast(f16x8_t, af[K::pa(p)][mi]),
-                __builtin_bit_cast(f16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
-          else
-            acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8_t, af[K::pa(p)][mi]),
-                __builtin_bit_cast(bf16x8_t, bf[K::pb(p)][ni]), acc[p][mi][ni], 0, 0, 0);
-        }
+// Fragments of one K-substep (16 K) for this wave's tile.
+template <class K>
+struct Frags {
+  u32x4_t a[K::NA][K::MI], b[K::NB][K::NI];
+  // LDS instructions issued by load_frags (a transpose fragment takes two)
+  static constexpr int kReads() {
+    int n = 0;
+    for (int o = 0; o < K::NOPS; ++o) n += (o < K::NA ? K::MI : K::NI) * (K::is_mn(o) ? 2 : 1);
+    return n;
   }
+};
+
+template <class K>
+__device__ __forceinline__ void load_frags(Frags<K>& f, const uint8_t* buf, int s) {
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int ab = wave_m<K>() * 32 * K::MI, bb = wave_n<K>() * 32 * K::NI;
+#pragma unroll
+  for (int o = 0; o < K::NA; ++o)
+#pragma unroll
+    for (int mi = 0; mi < K::MI; ++mi)
+      f.a[o][mi] = K::is_mn(o) ? frag_tr(buf + K::op_off(o), ab + mi * 32, s, K::ROWS_A * 2)
+                               : frag_k(buf + K::op_off(o), ab + mi * 32 + (lane & 31), 2 * s + half);
+#pragma unroll
+  for (int o = 0; o < K::NB; ++o)
+#pragma unroll
+    for (int ni = 0; ni < K::NI; ++ni)
+      f.b[o][ni] = K::is_mn(K::NA + o) ? frag_tr(buf + K::op_off(K::NA + o), bb + ni * 32, s, K::ROWS_B * 2)
+                                       : frag_k(buf + K::op_off(K::NA + o), bb + ni * 32 + (lane & 31), 2 * s + half);
+}
+
+// Wait until at most N LDS instructions are outstanding and make every
+// fragment of f depend on that wait.
+template <int N, class K>
+__device__ __forceinline__ void frags_ready(Frags<K>& f) {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(f.a[0][0]) : "n"(N));
+#pragma unroll
+  for (int o = 0; o < K::NA; ++o)
+#pragma unroll
+    for (int mi = 0; mi < K::MI; ++mi) asm volatile("" : "+v"(f.a[o][mi]));
+#pragma unroll
+  for (int o = 0; o < K::NB; ++o)
+#pragma unroll
+    for (int ni = 0; ni < K::NI; ++ni) asm volatile("" : "+v"(f.b[o][ni]));
 }
 
 template <typename T, class K>
-__device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk,
-                                             f32x16_t (&acc)[K::NACC][2][2]) {
-  constexpr int BK = 32, NS = K::NSTAGE, STAGE = K::NOPS * kTileBytes;
-  constexpr int L = 2 * K::NOPS;   // DMA instructions per wave per k-tile
+__device__ __forceinline__ void mfma_frags(const Frags<K>& f, Acc<K>& acc) {
 #pragma unroll
   for (int p = 0; p < K::NACC; ++p)
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int mi = 0; mi < K::MI; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[p][mi][ni][r] = 0.f;
+      for (int ni = 0; ni < K::NI; ++ni) {
+        if constexpr (__is_same(T, _Float16))
+          acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+              __builtin_bit_cast(f16x8_t, f.a[K::pa(p)][mi]), __builtin_bit_cast(f16x8_t, f.b[K::pb(p)][ni]),
+              acc[p][mi][ni], 0, 0, 0);
+        else
+          acc[p][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, f.a[K::pa(p)][mi]), __builtin_bit_cast(bf16x8_t, f.b[K::pb(p)][ni]),
+              acc[p][mi][ni], 0, 0, 0);
+      }
+}
+
+// NSTAGE k-tiles in flight. Per k-tile kt (stage kt % NS), with DBUF:
+//   read substep 1 of kt | MFMA substep 0 | wait reads of kt and DMA of kt+1 |
+//   barrier | DMA kt+NS into the freed stage | read substep 0 of kt+1 |
+//   MFMA substep 1
+// without DBUF every substep reads, waits and multiplies in turn.
+template <typename T, class K>
+__device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk, Acc<K>& acc) {
+  constexpr int BK = 32, NS = K::NSTAGE;
+  constexpr int L = [] {          // DMA instructions per lane per k-tile
+    int n = 0;
+    for (int o = 0; o < K::NOPS; ++o) n += K::rows(o) * 4 / K::THREADS;
+    return n;
+  }();
+  constexpr int R = Frags<K>::kReads();
+  static_assert(!K::DBUF || R < 16, "substep reads exceed lgkmcnt");
+  static_assert(L * NS < 64, "DMA in flight exceeds vmcnt");
   const int nkt = (int)((nk + BK - 1) / BK);
   if (nkt <= 0) return;
-  auto issue = [&](int kt) {
-    uint8_t* st = smem + (kt % NS) * STAGE;
+  uint32_t vo[K::NOPS][4];
+  DmaAll<K>::offsets(vo, ops);
+  auto issue = [&](int kt) { DmaAll<K>::issue(smem + (kt % NS) * K::STAGE, ops, vo, kt); };
 #pragma unroll
-    for (int o = 0; o < K::NOPS; ++o) {
-      if (K::is_mn(o)) dma_tile<true>(st + o * kTileBytes, ops[o], (int64_t)kt * BK);
-      else dma_tile<false>(st + o * kTileBytes, ops[o], (int64_t)kt * BK);
-    }
-  };
-#pragma unroll
-  for (int t = 0; t < NS - 1; ++t)
+  for (int t = 0; t < NS; ++t)
     if (t < nkt) issue(t);
-  for (int kt = 0; kt < nkt; ++kt) {
-    // this wave's loads of tile kt are done once at most the later tiles' are pending
-    if (kt + NS - 2 < nkt) wait_vmcnt<L * (NS - 2)>();
-    else wait_vmcnt<0>();
-    // every wave's tile kt is in LDS and tile kt-1's stage is free; a bare
-    // barrier (a fenced one would drain all DMA still in flight)
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    if (kt + NS - 1 < nkt) issue(kt + NS - 1);
-    compute_ktile16<T, K>(smem + (kt % NS) * STAGE, acc);
+  if (nkt >= NS) wait_vmcnt<L * (NS - 1)>();
+  else wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  if constexpr (K::DBUF) {
+    Frags<K> f0, f1;
+    load_frags<K>(f0, smem, 0);
+    for (int kt = 0; kt < nkt; ++kt) {
+      const uint8_t* cur = smem + (kt % NS) * K::STAGE;
+      load_frags<K>(f1, cur, 1);
+      frags_ready<R, K>(f0);                  // substep 0 is in; substep 1 still in flight
+      mfma_frags<T, K>(f0, acc);
+      __builtin_amdgcn_sched_barrier(0);      // issue all of them before the next wait
+      frags_ready<0, K>(f1);                  // this wave is done reading tile kt
+      if (kt + 1 < nkt) {
+        if (kt + NS - 1 < nkt) wait_vmcnt<L * (NS - 2)>();   // tile kt+1 landed
+        else wait_vmcnt<0>();
+      }
+      __builtin_amdgcn_s_barrier();           // every wave is past tile kt and has tile kt+1
+      asm volatile("" ::: "memory");
+      if (kt + NS < nkt) issue(kt + NS);      // refill the stage tile kt used
+      if (kt + 1 < nkt) load_frags<K>(f0, smem + ((kt + 1) % NS) * K::STAGE, 0);
+      mfma_frags<T, K>(f1, acc);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+    Frags<K> f;
+    for (int kt = 0; kt < nkt; ++kt) {
+      const uint8_t* cur = smem + (kt % NS) * K::STAGE;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        load_frags<K>(f, cur, s);
+        frags_ready<0, K>(f);
+        mfma_frags<T, K>(f, acc);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (kt + 1 < nkt) {
+        if (kt + NS - 1 < nkt) wait_vmcnt<L * (NS - 2)>();
+        else wait_vmcnt<0>();
+      }
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      if (kt + NS < nkt) issue(kt + NS);
+    }
   }
   __syncthreads();     // the caller may reuse LDS after the loop
 }
 
+// acc = sum over K of A[pa(p)] B[pb(p)]^T for this workgroup's tile.
 template <typename T, class K>
-__device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk,
-                                         f32x16_t (&acc)[K::NACC][2][2]) {
+__device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk, Acc<K>& acc) {
+#pragma unroll
+  for (int p = 0; p < K::NACC; ++p)
+#pragma unroll
+    for (int mi = 0; mi < K::MI; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < K::NI; ++ni)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[p][mi][ni][r] = 0.f;
   if constexpr (sizeof(T) == 2) mainloop_dma<T, K>(smem, ops, nk, acc);
-  else mainloop_regs<T, K>(smem, ops, nk, acc);
+  else mainloop_regs<K>(smem, ops, nk, acc);
 }
 
-template <class K>
+template <typename T, class K>
 constexpr int smem_bytes() {
-  const int dma = K::NSTAGE * K::NOPS * kTileBytes, regs = 2 * K::NOPS * kTileBytes;
-  return dma > regs ? dma : regs;
+  return sizeof(T) == 2 ? K::NSTAGE * K::STAGE : 2 * K::NOPS * kTileBytes;
 }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
-// Epilogue coordinates of accumulator register r of block (mi, ni).
-__device__ __forceinline__ int acc_row(int mi, int r) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  return (w >> 1) * 64 + mi * 32 + ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3);
-}
-__device__ __forceinline__ int acc_col(int ni) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  return (w & 1) * 64 + ni * 32 + (lane & 31);
-}
+// ===========================================================================
+// Epilogue helpers
 
 template <typename T>
 __device__ __forceinline__ void st_elem(void* base, int64_t idx, float v) {
   reinterpret_cast<T*>(base)[idx] = (T)v;
 }
 
+// Four consecutive elements (8 bytes of 16-bit or 16 bytes of fp32) at idx.
+template <typename T>
+__device__ __forceinline__ void st4(void* base, int64_t idx, float a, float b, float c, float d) {
+  if constexpr (sizeof(T) == 2) {
+    typedef __attribute__((ext_vector_type(4))) T t4;
+    *reinterpret_cast<t4*>(reinterpret_cast<T*>(base) + idx) = t4{(T)a, (T)b, (T)c, (T)d};
+  } else {
+    *reinterpret_cast<float4*>(reinterpret_cast<float*>(base) + idx) = make_float4(a, b, c, d);
+  }
+}
+
 __device__ __forceinline__ float sigmoidf_fast(float z) {
   return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
 }
 
-__device__ __forceinline__ View view_k(const Operand& op, int inst, int64_t row0, int64_t k0,
-                                       int64_t nrows, int64_t nk, int esz) {
+__device__ __forceinline__ View view_k(const Operand& op, int inst, int64_t row0, int64_t k0, int64_t nrows,
+                                       int64_t nk, int esz) {
   const int64_t off = inst * op.inst_stride + row0 * op.ld + k0;
   return View{reinterpret_cast<const uint8_t*>(op.base) + off * esz, op.ld * esz, nrows, nk};
 }
-__device__ __forceinline__ View view_mn(const Operand& op, int inst, int64_t row0, int64_t k0,
-                                        int64_t nrows, int64_t nk, int esz) {
+__device__ __forceinline__ View view_mn(const Operand& op, int inst, int64_t row0, int64_t k0, int64_t nrows,
+                                        int64_t nk, int esz) {
   const int64_t off = inst * op.inst_stride + k0 * op.ld + row0;
   return View{reinterpret_cast<const uint8_t*>(op.base) + off * esz, op.ld * esz, nrows, nk};
 }
 
-// ---------------------------------------------------------------------------
+// ===========================================================================
+// First launch of a chunk. Accumulators are hidden-major (rows = hidden units
+// j, columns = tokens i): every lane holds four consecutive hidden units of
+// one token per register group, written as one packed store into the
+// token-major [tokens x h] output.
 template <typename T>
-__global__ __launch_bounds__(kThreads) void k_fwd(const FwdArgs args) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(smem_bytes<KApply>(), smem_bytes<KUpdate>())];
+__global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs args) {
+  using KA = typename Kinds<T>::Apply;
+  using KU = typename Kinds<T>::Update;
+  static_assert(KA::THREADS == KU::THREADS, "one block size per launch");
+  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(smem_bytes<T, KA>(), smem_bytes<T, KU>())];
   constexpr int esz = sizeof(T);
-  int bid = xcd_remap(blockIdx.x, args.total_blocks);
+  int bid = blockIdx.x;
   const bool first = bid < args.seg[0].nblocks;
   const FwdSeg& sg = first ? args.seg[0] : args.seg[1];
   if (!first) bid -= args.seg[0].nblocks;
+  bid = xcd_remap(bid, sg.nblocks);   // per segment: every XCD gets a share of each kind
   const int per = sg.tiles_m * sg.tiles_n;
   const int inst = bid / per;
   const int rr = bid - inst * per;
-  const int64_t i0 = (int64_t)(rr / sg.tiles_n) * kTile;   // token tile
-  const int64_t j0 = (int64_t)(rr % sg.tiles_n) * kTile;   // hidden tile
   const int d = args.d, h = args.h;
-  const int64_t mrows = sg.rows - i0, ncols = h - j0;
+  const int lane = threadIdx.x & 63;
 
   if (sg.kind == FWD_APPLY) {
-    const View ops[3] = {view_k(sg.a0, inst, i0, 0, mrows, d, esz),
-                         view_k(args.w1, inst, j0, 0, ncols, d, esz),
-                         view_k(args.w3, inst, j0, 0, ncols, d, esz)};
-    f32x16_t acc[2][2][2];
-    mainloop<T, KApply>(smem, ops, d, acc);
+    const int64_t j0 = (int64_t)(rr % sg.tiles_m) * KA::ROWS_A;   // hidden tile (fastest)
+    const int64_t i0 = (int64_t)(rr / sg.tiles_m) * KA::ROWS_B;   // token tile
+    const int64_t hrows = h - j0, ntok = sg.rows - i0;
+    const View ops[3] = {view_k(args.w1, inst, j0, 0, hrows, d, esz), view_k(args.w3, inst, j0, 0, hrows, d, esz),
+                         view_k(sg.a0, inst, i0, 0, ntok, d, esz)};
+    Acc<KA> acc;
+    mainloop<T, KA>(smem, ops, d, acc);
     void* out = reinterpret_cast<uint8_t*>(sg.out0) + (inst * sg.out_inst) * esz;
+    const int hrow0 = wave_m<KA>() * 32 * KA::MI + ((lane >> 5) << 2);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int ni = 0; ni < KA::NI; ++ni) {
+      const int tok = acc_col<KA>(ni);
+      if (tok >= ntok) continue;
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int j = acc_col(ni);
+      for (int mi = 0; mi < KA::MI; ++mi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int i = acc_row(mi, r);
-          if (i < mrows && j < ncols) {
-            const float z1 = acc[0][mi][ni][r], z3 = acc[1][mi][ni][r];
-            st_elem<T>(out, (i0 + i) * h + j0 + j, z1 * sigmoidf_fast(z1) * z3);
+        for (int g = 0; g < 4; ++g) {
+          const int hid = hrow0 + mi * 32 + 8 * g;
+          if (hid >= hrows) continue;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float z1 = acc[0][mi][ni][4 * g + e], z3 = acc[1][mi][ni][4 * g + e];
+            v[e] = z1 * sigmoidf_fast(z1) * z3;
           }
+          st4<T>(out, (i0 + tok) * h + j0 + hid, v[0], v[1], v[2], v[3]);
         }
-      }
+    }
   } else {
-    const View ops[5] = {view_k(sg.a0, inst, i0, 0, mrows, d, esz),
-                         view_k(sg.a1, inst, i0, 0, mrows, d, esz),
-                         view_k(args.w1, inst, j0, 0, ncols, d, esz),
-                         view_k(args.w3, inst, j0, 0, ncols, d, esz),
-                         view_mn(args.w2, inst, j0, 0, ncols, d, esz)};
-    f32x16_t acc[3][2][2];
-    mainloop<T, KUpdate>(smem, ops, d, acc);
+    const int64_t j0 = (int64_t)(rr % sg.tiles_m) * KU::ROWS_A;
+    const int64_t i0 = (int64_t)(rr / sg.tiles_m) * KU::ROWS_B;
+    const int64_t hrows = h - j0, ntok = sg.rows - i0;
+    const View ops[5] = {view_k(args.w1, inst, j0, 0, hrows, d, esz), view_k(args.w3, inst, j0, 0, hrows, d, esz),
+                         view_mn(args.w2, inst, j0, 0, hrows, d, esz), view_k(sg.a0, inst, i0, 0, ntok, d, esz),
+                         view_k(sg.a1, inst, i0, 0, ntok, d, esz)};
+    Acc<KU> acc;
+    mainloop<T, KU>(smem, ops, d, acc);
     const int64_t ob = inst * sg.out_inst;
     const float* eta = sg.eta + inst * sg.eta_inst + i0;
+    const int hrow0 = wave_m<KU>() * 32 * KU::MI + ((lane >> 5) << 2);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi) {
-      float e[16];
+    for (int ni = 0; ni < KU::NI; ++ni) {
+      const int tok = acc_col<KU>(ni);
+      if (tok >= ntok) continue;
+      const float et = eta[tok];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = acc_row(mi, r);
-        e[r] = i < mrows ? eta[i] : 0.f;
-      }
+      for (int mi = 0; mi < KU::MI; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int j = acc_col(ni);
+        for (int g = 0; g < 4; ++g) {
+          const int hid = hrow0 + mi * 32 + 8 * g;
+          if (hid >= hrows) continue;
+          float vh[4], vg[4], vb[4];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int i = acc_row(mi, r);
-          if (i < mrows && j < ncols) {
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * g + e;
             const float z1 = acc[0][mi][ni][r], z3 = acc[1][mi][ni][r], dh = acc[2][mi][ni][r];
             const float s = sigmoidf_fast(z1);
-            const float a = z1 * s;                       // SiLU(z1)
-            const float ed = e[r] * dh;                   // eta_i * (W2^T v_i)_j
-            const int64_t idx = ob + (i0 + i) * h + j0 + j;
-            st_elem<T>(sg.out1, idx, e[r] * a * z3);                          // eta * hidden
-            st_elem<T>(sg.out2, idx, ed * z3 * s * (1.0f + z1 * (1.0f - s))); // eta * dz1
-            st_elem<T>(sg.out3, idx, ed * a);                                 // eta * dz3
+            const float a = z1 * s;                     // SiLU(z1)
+            const float ed = et * dh;                   // eta_i * (W2^T v_i)_j
+            vh[e] = et * a * z3;                        // eta * hidden
+            vg[e] = ed * z3 * s * (1.0f + z1 * (1.0f - s));   // eta * dz1
+            vb[e] = ed * a;                             // eta * dz3
           }
+          const int64_t idx = ob + (i0 + tok) * h + j0 + hid;
+          st4<T>(sg.out1, idx, vh[0], vh[1], vh[2], vh[3]);
+          st4<T>(sg.out2, idx, vg[0], vg[1], vg[2], vg[3]);
+          st4<T>(sg.out3, idx, vb[0], vb[1], vb[2], vb[3]);
         }
-      }
     }
   }
 }
 
+// Second launch: apply GEMM-2 and the gradient contractions (split over tokens).
 template <typename T>
-__global__ __launch_bounds__(kThreads) void k_bwd(const BwdArgs args) {
+__global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs args) {
+  using KO = typename Kinds<T>::Out;
+  using K13 = typename Kinds<T>::Grad13;
+  using K2 = typename Kinds<T>::Grad2;
+  static_assert(KO::THREADS == K13::THREADS && KO::THREADS == K2::THREADS, "one block size per launch");
   __shared__ __attribute__((aligned(16)))
-  uint8_t smem[cmax(smem_bytes<KOut>(), cmax(smem_bytes<KGrad13>(), smem_bytes<KGrad2>()))];
+  uint8_t smem[cmax(smem_bytes<T, KO>(), cmax(smem_bytes<T, K13>(), smem_bytes<T, K2>()))];
   constexpr int esz = sizeof(T);
-  int bid = xcd_remap(blockIdx.x, args.total_blocks);
+  int bid = blockIdx.x;
   int si = 0;
   if (bid >= args.seg[0].nblocks) {
     bid -= args.seg[0].nblocks;
@@ -654,6 +762,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd(const BwdArgs args) {
     }
   }
   const BwdSeg& sg = si == 0 ? args.seg[0] : (si == 1 ? args.seg[1] : args.seg[2]);
+  bid = xcd_remap(bid, sg.nblocks);
   const int d = args.d, h = args.h;
   const int per = sg.tiles_m * sg.tiles_n;
   const int per_inst = per * sg.nsplit;
@@ -661,28 +770,33 @@ __global__ __launch_bounds__(kThreads) void k_bwd(const BwdArgs args) {
   int rr = bid - inst * per_inst;
   const int split = rr / per;
   rr -= split * per;
-  const int64_t r0 = (int64_t)(rr / sg.tiles_n) * kTile;
-  const int64_t c0 = (int64_t)(rr % sg.tiles_n) * kTile;
+  const int lane = threadIdx.x & 63;
 
   if (sg.kind == BWD_OUT) {
-    // O[i, m] = sum_j hidden[i, j] W2[m, j]
-    const int64_t mrows = sg.rows - r0, ncols = d - c0;
-    const View ops[2] = {view_k(sg.a0, inst, r0, 0, mrows, h, esz),
-                         view_k(sg.b0, inst, c0, 0, ncols, h, esz)};
-    f32x16_t acc[1][2][2];
-    mainloop<T, KOut>(smem, ops, h, acc);
+    // O^T[m, i] = sum_j W2[m, j] hidden[i, j]: feature-major accumulators, four
+    // consecutive features of one token per register group -> packed stores
+    const int64_t m0 = (int64_t)(rr % sg.tiles_m) * KO::ROWS_A;   // feature tile (fastest)
+    const int64_t t0 = (int64_t)(rr / sg.tiles_m) * KO::ROWS_B;   // token tile
+    const int64_t mrows = d - m0, ntok = sg.rows - t0;
+    const View ops[2] = {view_k(sg.b0, inst, m0, 0, mrows, h, esz), view_k(sg.a0, inst, t0, 0, ntok, h, esz)};
+    Acc<KO> acc;
+    mainloop<T, KO>(smem, ops, h, acc);
     const int64_t ob = inst * sg.out_inst;
+    const int mrow0 = wave_m<KO>() * 32 * KO::MI + ((lane >> 5) << 2);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int ni = 0; ni < KO::NI; ++ni) {
+      const int tok = acc_col<KO>(ni);
+      if (tok >= ntok) continue;
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int j = acc_col(ni);
+      for (int mi = 0; mi < KO::MI; ++mi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int i = acc_row(mi, r);
-          if (i < mrows && j < ncols) st_elem<T>(sg.out, ob + (r0 + i) * d + c0 + j, acc[0][mi][ni][r]);
+        for (int g = 0; g < 4; ++g) {
+          const int m = mrow0 + mi * 32 + 8 * g;
+          if (m >= mrows) continue;
+          const f32x16_t& a = acc[0][mi][ni];
+          st4<T>(sg.out, ob + (t0 + tok) * d + m0 + m, a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]);
         }
-      }
+    }
     return;
   }
 
@@ -694,20 +808,21 @@ __global__ __launch_bounds__(kThreads) void k_bwd(const BwdArgs args) {
   const int64_t dh = (int64_t)d * h;
   if (sg.kind == BWD_GRAD13) {
     // P1[j, m] = sum_i (eta dz1)[i, j] K[i, m];  P3 likewise with eta dz3
+    const int64_t r0 = (int64_t)(rr / sg.tiles_n) * K13::ROWS_A;
+    const int64_t c0 = (int64_t)(rr % sg.tiles_n) * K13::ROWS_B;
     const int64_t mrows = h - r0, ncols = d - c0;
-    const View ops[3] = {view_mn(sg.a0, inst, r0, kb, mrows, klen, esz),
-                         view_mn(sg.a1, inst, r0, kb, mrows, klen, esz),
+    const View ops[3] = {view_mn(sg.a0, inst, r0, kb, mrows, klen, esz), view_mn(sg.a1, inst, r0, kb, mrows, klen, esz),
                          view_mn(sg.b0, inst, c0, kb, ncols, klen, esz)};
-    f32x16_t acc[2][2][2];
-    mainloop<T, KGrad13>(smem, ops, klen, acc);
+    Acc<K13> acc;
+    mainloop<T, K13>(smem, ops, klen, acc);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int mi = 0; mi < K13::MI; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int j = acc_col(ni);
+      for (int ni = 0; ni < K13::NI; ++ni) {
+        const int j = acc_col<K13>(ni);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int i = acc_row(mi, r);
+          const int i = acc_row<K13>(mi, r);
           if (i < mrows && j < ncols) {
             const int64_t idx = (r0 + i) * d + c0 + j;
             part[idx] = acc[0][mi][ni][r];
@@ -717,24 +832,28 @@ __global__ __launch_bounds__(kThreads) void k_bwd(const BwdArgs args) {
       }
   } else {
     // P2[m, j] = sum_i V[i, m] (eta hidden)[i, j]
+    const int64_t r0 = (int64_t)(rr / sg.tiles_n) * K2::ROWS_A;
+    const int64_t c0 = (int64_t)(rr % sg.tiles_n) * K2::ROWS_B;
     const int64_t mrows = d - r0, ncols = h - c0;
-    const View ops[2] = {view_mn(sg.a0, inst, r0, kb, mrows, klen, esz),
-                         view_mn(sg.b0, inst, c0, kb, ncols, klen, esz)};
-    f32x16_t acc[1][2][2];
-    mainloop<T, KGrad2>(smem, ops, klen, acc);
+    const View ops[2] = {view_mn(sg.a0, inst, r0, kb, mrows, klen, esz), view_mn(sg.b0, inst, c0, kb, ncols, klen, esz)};
+    Acc<K2> acc;
+    mainloop<T, K2>(smem, ops, klen, acc);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int mi = 0; mi < K2::MI; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int j = acc_col(ni);
+      for (int ni = 0; ni < K2::NI; ++ni) {
+        const int j = acc_col<K2>(ni);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int i = acc_row(mi, r);
+          const int i = acc_row<K2>(mi, r);
           if (i < mrows && j < ncols) part[dh + (r0 + i) * h + c0 + j] = acc[0][mi][ni][r];
         }
       }
   }
 }
+
+// ===========================================================================
+// Weight update
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -745,9 +864,12 @@ __device__ __forceinline__ float wave_sum(float v) {
 // One wave per row of W1 (length d), W2 (length h) or W3 (length d):
 //   U = W + sum_split P  (P = -g, the negated gradient or its Newton-Schulz image)
 //   W <- U * ||W_row|| / ||U_row||       (§3.2 weight normalisation; Alg. 1)
-template <typename T>
-__global__ __launch_bounds__(kThreads) void k_update(const UpdArgs a) {
-  const int wave = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+// Lane l owns the float4 vectors l, l+64, ... of the row (NV per lane at most);
+// every load is issued unconditionally (clamped index, zeroed after) so a row
+// costs one round trip to memory, not one per vector.
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void k_update(const UpdArgs a) {
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (wave >= a.rows_total) return;
   const int rows_inst = 2 * a.h + a.d;
@@ -761,45 +883,59 @@ __global__ __launch_bounds__(kThreads) void k_update(const UpdArgs a) {
   } else {
     mat = 2; r -= a.h + a.d; L = a.d;
   }
+  const int nv = L >> 2;
   const int64_t dh = (int64_t)a.d * a.h;
   const int64_t off = inst * dh + (int64_t)r * L;
-  float* W = a.W[mat] + off;
-  const float* P = a.step + inst * 3 * dh + mat * dh + (int64_t)r * L;
-  constexpr int kPer = kMaxDim / 64;
-  float u[kPer];
+  float4* W = reinterpret_cast<float4*>(a.W[mat] + off);
+  const float4* P = reinterpret_cast<const float4*>(a.step + inst * 3 * dh + mat * dh + (int64_t)r * L);
+  const int64_t ps = a.step_split >> 2;
+  float4 w[NV], u[NV];
+#pragma unroll
+  for (int t = 0; t < NV; ++t) {
+    const int i = lane + 64 * t;
+    w[t] = W[i < nv ? i : 0];
+    u[t] = P[i < nv ? i : 0];
+  }
+  for (int s = 1; s < a.nsplit; ++s) {
+#pragma unroll
+    for (int t = 0; t < NV; ++t) {
+      const int i = lane + 64 * t;
+      const float4 q = P[s * ps + (i < nv ? i : 0)];
+      u[t].x += q.x; u[t].y += q.y; u[t].z += q.z; u[t].w += q.w;
+    }
+  }
   float sw = 0.f, su = 0.f;
 #pragma unroll
-  for (int t = 0; t < kPer; ++t) {
-    const int c = lane + 64 * t;
-    u[t] = 0.f;
-    if (c < L) {
-      const float w = W[c];
-      float p = 0.f;
-      for (int s = 0; s < a.nsplit; ++s) p += P[s * a.step_split + c];
-      const float x = w + p;
-      u[t] = x;
-      sw += w * w;
-      su += x * x;
+  for (int t = 0; t < NV; ++t) {
+    if (lane + 64 * t >= nv) {
+      w[t] = make_float4(0.f, 0.f, 0.f, 0.f);
+      u[t] = w[t];
     }
+    u[t].x += w[t].x; u[t].y += w[t].y; u[t].z += w[t].z; u[t].w += w[t].w;
+    sw += w[t].x * w[t].x + w[t].y * w[t].y + w[t].z * w[t].z + w[t].w * w[t].w;
+    su += u[t].x * u[t].x + u[t].y * u[t].y + u[t].z * u[t].z + u[t].w * u[t].w;
   }
   sw = wave_sum(sw);
   su = wave_sum(su);
   const float scale = sqrtf(sw) / sqrtf(su);
-  void* wb = a.Wb[mat];
 #pragma unroll
-  for (int t = 0; t < kPer; ++t) {
-    const int c = lane + 64 * t;
-    if (c < L) {
-      const float x = u[t] * scale;
-      W[c] = x;
-      if constexpr (sizeof(T) == 2) reinterpret_cast<__bf16*>(wb)[off + c] = (__bf16)x;
+  for (int t = 0; t < NV; ++t) {
+    const int i = lane + 64 * t;
+    if (i < nv) {
+      const float4 x = make_float4(u[t].x * scale, u[t].y * scale, u[t].z * scale, u[t].w * scale);
+      W[i] = x;
+      if constexpr (sizeof(T) == 2) {
+        typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_t;
+        const bf16x4_t b = {(__bf16)x.x, (__bf16)x.y, (__bf16)x.z, (__bf16)x.w};
+        reinterpret_cast<bf16x4_t*>(reinterpret_cast<__bf16*>(a.Wb[mat]) + off)[i] = b;
+      }
     }
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_prep(const float* w1, const float* w2, const float* w3,
-                                                   __bf16* b1, __bf16* b2, __bf16* b3, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+__global__ __launch_bounds__(256) void k_prep(const float* w1, const float* w2, const float* w3, __bf16* b1,
+                                              __bf16* b2, __bf16* b3, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n) {
     b1[i] = (__bf16)w1[i];
     b2[i] = (__bf16)w2[i];
@@ -807,15 +943,19 @@ __global__ __launch_bounds__(kThreads) void k_prep(const float* w1, const float*
   }
 }
 
+// ===========================================================================
+// Newton-Schulz (Muon)
+
 // One Newton-Schulz product over every matrix of the chunk (see NsKind).
 template <typename T>
-__global__ __launch_bounds__(kThreads) void k_ns(const NsArgs args) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(smem_bytes<KNsK>(), smem_bytes<KNsBY>())];
+__global__ __launch_bounds__(256) void k_ns(const NsArgs args) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(smem_bytes<T, KNsK>(), smem_bytes<T, KNsBY>())];
   constexpr int esz = sizeof(T);
-  int bid = xcd_remap(blockIdx.x, args.total_blocks);
+  int bid = blockIdx.x;
   const bool first = bid < args.seg[0].nblocks;
   const NsSeg& sg = first ? args.seg[0] : args.seg[1];
   if (!first) bid -= args.seg[0].nblocks;
+  bid = xcd_remap(bid, sg.nblocks);
   const int per = sg.tiles_m * sg.tiles_n;
   const int q = bid / per;
   const int rr = bid - q * per;
@@ -831,7 +971,7 @@ __global__ __launch_bounds__(kThreads) void k_ns(const NsArgs args) {
   void* Abw = reinterpret_cast<uint8_t*>(args.Ab) + slot * args.astride * esz;
   const uint8_t* Bb = reinterpret_cast<const uint8_t*>(args.Bb) + slot * args.astride * esz;
   void* Bbw = reinterpret_cast<uint8_t*>(args.Bb) + slot * args.astride * esz;
-  f32x16_t acc[1][2][2];
+  Acc<KNsK> acc;   // same accumulator shape for every NS kind
   const int kind = sg.kind;
   if (kind == NS_GRAM_K) {          // A = Y Y^T
     const View ops[2] = {View{Yin + i0 * ldy * esz, (int64_t)ldy * esz, mrows, sg.K},
@@ -858,10 +998,10 @@ __global__ __launch_bounds__(kThreads) void k_ns(const NsArgs args) {
   for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
     for (int ni = 0; ni < 2; ++ni) {
-      const int j = acc_col(ni);
+      const int j = acc_col<KNsK>(ni);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int i = acc_row(mi, r);
+        const int i = acc_row<KNsK>(mi, r);
         if (i < mrows && j < ncols) {
           const float v = acc[0][mi][ni][r];
           if (kind == NS_GRAM_K || kind == NS_GRAM_MN) {
@@ -889,19 +1029,19 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   __syncthreads();
   float t = 0.f;
 #pragma unroll
-  for (int i = 0; i < kThreads / 64; ++i) t += red[i];
+  for (int i = 0; i < 4; ++i) t += red[i];
   __syncthreads();
   return t;
 }
 
 // Sum the split-K partials of every gradient and the per-block sums of squares.
-__global__ __launch_bounds__(kThreads) void k_ns_prep(const NsPrepArgs a) {
-  __shared__ float red[kThreads / 64];
+__global__ __launch_bounds__(256) void k_ns_prep(const NsPrepArgs a) {
+  __shared__ float red[4];
   const int slot = blockIdx.x / a.blocks_per_slot;
   const int blk = blockIdx.x - slot * a.blocks_per_slot;
   const int64_t base = (int64_t)slot * a.dh;
   float ss = 0.f;
-  for (int e = threadIdx.x; e < kNsBlockElems; e += kThreads) {
+  for (int e = threadIdx.x; e < kNsBlockElems; e += 256) {
     const int64_t idx = (int64_t)blk * kNsBlockElems + e;
     if (idx < a.dh) {
       float g = 0.f;
@@ -916,17 +1056,16 @@ __global__ __launch_bounds__(kThreads) void k_ns_prep(const NsPrepArgs a) {
 
 // X0 = G / (||G||_F + eps), fp32 iterate and operand copy.
 template <typename T>
-__global__ __launch_bounds__(kThreads) void k_ns_scale(const NsPrepArgs a, void* yb, float eps) {
-  __shared__ float red[kThreads / 64];
+__global__ __launch_bounds__(256) void k_ns_scale(const NsPrepArgs a, void* yb, float eps) {
+  __shared__ float red[4];
   const int slot = blockIdx.x / a.blocks_per_slot;
   const int blk = blockIdx.x - slot * a.blocks_per_slot;
   const int64_t base = (int64_t)slot * a.dh;
   float t = 0.f;
-  for (int b = threadIdx.x; b < a.blocks_per_slot; b += kThreads)
-    t += a.sumsq[(int64_t)slot * a.blocks_per_slot + b];
+  for (int b = threadIdx.x; b < a.blocks_per_slot; b += 256) t += a.sumsq[(int64_t)slot * a.blocks_per_slot + b];
   t = block_sum(t, red);
   const float inv = 1.0f / (sqrtf(t) + eps);
-  for (int e = threadIdx.x; e < kNsBlockElems; e += kThreads) {
+  for (int e = threadIdx.x; e < kNsBlockElems; e += 256) {
     const int64_t idx = (int64_t)blk * kNsBlockElems + e;
     if (idx < a.dh) {
       const float y = a.Y32[base + idx] * inv;
@@ -938,58 +1077,88 @@ __global__ __launch_bounds__(kThreads) void k_ns_scale(const NsPrepArgs a, void*
 
 }  // namespace
 
+// ===========================================================================
+// Host-visible shapes and launchers
+
+TileShape fwd_tile(int kind, bool io_bf16) {
+  if (io_bf16) return kind == FWD_APPLY ? TileShape{KApply16::ROWS_A, KApply16::ROWS_B, KApply16::THREADS}
+                                        : TileShape{KUpdate16::ROWS_A, KUpdate16::ROWS_B, KUpdate16::THREADS};
+  return kind == FWD_APPLY ? TileShape{KApply32::ROWS_A, KApply32::ROWS_B, KApply32::THREADS}
+                           : TileShape{KUpdate32::ROWS_A, KUpdate32::ROWS_B, KUpdate32::THREADS};
+}
+
+TileShape bwd_tile(int kind, bool io_bf16) {
+  if (io_bf16) {
+    if (kind == BWD_OUT) return TileShape{KOut16::ROWS_A, KOut16::ROWS_B, KOut16::THREADS};
+    if (kind == BWD_GRAD13) return TileShape{KGrad13_16::ROWS_A, KGrad13_16::ROWS_B, KGrad13_16::THREADS};
+    return TileShape{KGrad2_16::ROWS_A, KGrad2_16::ROWS_B, KGrad2_16::THREADS};
+  }
+  if (kind == BWD_OUT) return TileShape{KOut32::ROWS_A, KOut32::ROWS_B, KOut32::THREADS};
+  if (kind == BWD_GRAD13) return TileShape{KGrad13_32::ROWS_A, KGrad13_32::ROWS_B, KGrad13_32::THREADS};
+  return TileShape{KGrad2_32::ROWS_A, KGrad2_32::ROWS_B, KGrad2_32::THREADS};
+}
+
 hipError_t launch_ns(const NsArgs& a, bool fp16, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;
-  if (fp16) k_ns<_Float16><<<a.total_blocks, kThreads, 0, s>>>(a);
-  else k_ns<float><<<a.total_blocks, kThreads, 0, s>>>(a);
+  if (fp16) k_ns<_Float16><<<a.total_blocks, 256, 0, s>>>(a);
+  else k_ns<float><<<a.total_blocks, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.nslots * a.blocks_per_slot;
   if (blocks <= 0) return hipSuccess;
-  k_ns_prep<<<(unsigned)blocks, kThreads, 0, s>>>(a);
+  k_ns_prep<<<(unsigned)blocks, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s) {
   const int64_t blocks = (int64_t)a.nslots * a.blocks_per_slot;
   if (blocks <= 0) return hipSuccess;
-  if (fp16) k_ns_scale<_Float16><<<(unsigned)blocks, kThreads, 0, s>>>(a, Yb, eps);
-  else k_ns_scale<float><<<(unsigned)blocks, kThreads, 0, s>>>(a, Yb, eps);
+  if (fp16) k_ns_scale<_Float16><<<(unsigned)blocks, 256, 0, s>>>(a, Yb, eps);
+  else k_ns_scale<float><<<(unsigned)blocks, 256, 0, s>>>(a, Yb, eps);
   return hipGetLastError();
 }
 
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;
-  if (io_bf16) k_fwd<__bf16><<<a.total_blocks, kThreads, 0, s>>>(a);
-  else k_fwd<float><<<a.total_blocks, kThreads, 0, s>>>(a);
+  if (io_bf16) k_fwd<__bf16><<<a.total_blocks, KApply16::THREADS, 0, s>>>(a);
+  else k_fwd<float><<<a.total_blocks, KApply32::THREADS, 0, s>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_bwd(const BwdArgs& a, bool io_bf16, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;
-  if (io_bf16) k_bwd<__bf16><<<a.total_blocks, kThreads, 0, s>>>(a);
-  else k_bwd<float><<<a.total_blocks, kThreads, 0, s>>>(a);
+  if (io_bf16) k_bwd<__bf16><<<a.total_blocks, KOut16::THREADS, 0, s>>>(a);
+  else k_bwd<float><<<a.total_blocks, KOut32::THREADS, 0, s>>>(a);
   return hipGetLastError();
 }
 
+template <int NV>
+static void launch_update_nv(const UpdArgs& a, bool io_bf16, int blocks, hipStream_t s) {
+  if (io_bf16) k_update<__bf16, NV><<<blocks, 256, 0, s>>>(a);
+  else k_update<float, NV><<<blocks, 256, 0, s>>>(a);
+}
+
 hipError_t launch_update(const UpdArgs& a, bool io_bf16, hipStream_t s) {
-  const int waves_per_block = kThreads / 64;
-  const int blocks = (a.rows_total + waves_per_block - 1) / waves_per_block;
+  const int blocks = (a.rows_total + 3) / 4;   // a wave per row
   if (blocks <= 0) return hipSuccess;
-  if (io_bf16) k_update<__bf16><<<blocks, kThreads, 0, s>>>(a);
-  else k_update<float><<<blocks, kThreads, 0, s>>>(a);
+  const int L = a.d > a.h ? a.d : a.h;        // longest row, floats
+  const int per_lane = (L / 4 + 63) / 64;      // float4 vectors per lane
+  if (per_lane <= 1) launch_update_nv<1>(a, io_bf16, blocks, s);
+  else if (per_lane <= 2) launch_update_nv<2>(a, io_bf16, blocks, s);
+  else if (per_lane <= 4) launch_update_nv<4>(a, io_bf16, blocks, s);
+  else if (per_lane <= 8) launch_update_nv<8>(a, io_bf16, blocks, s);
+  else launch_update_nv<16>(a, io_bf16, blocks, s);
   return hipGetLastError();
 }
 
 hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d, int h, hipStream_t s) {
   const int64_t n = (int64_t)BH * d * h;
-  const int64_t blocks = (n + kThreads - 1) / kThreads;
+  const int64_t blocks = (n + 255) / 256;
   if (blocks <= 0) return hipSuccess;
-  k_prep<<<(unsigned)blocks, kThreads, 0, s>>>(W[0], W[1], W[2], reinterpret_cast<__bf16*>(Wb[0]),
-                                              reinterpret_cast<__bf16*>(Wb[1]),
-                                              reinterpret_cast<__bf16*>(Wb[2]), n);
+  k_prep<<<(unsigned)blocks, 256, 0, s>>>(W[0], W[1], W[2], reinterpret_cast<__bf16*>(Wb[0]),
+                                         reinterpret_cast<__bf16*>(Wb[1]), reinterpret_cast<__bf16*>(Wb[2]), n);
   return hipGetLastError();
 }
 

@@ -59,6 +59,18 @@ __device__ __forceinline__ int lds_off(int row, int chunk) {
   return row * kRowBytes + ((chunk ^ lds_swz(row)) << 4);
 }
 
+// 16-bit K-contiguous tiles of BK K: rows of 2*BK bytes. The 16 lanes that
+// serve one fragment read touch 16 consecutive rows at one logical chunk; the
+// XOR spreads them over all 16 16-byte positions of a 256-byte bank window.
+template <int BK>
+__device__ __forceinline__ int swz_k(int row) {
+  return BK == 32 ? (row >> 2) & 3 : (row >> 1) & 7;
+}
+template <int BK>
+__device__ __forceinline__ int lds_off_k(int row, int chunk) {
+  return row * (2 * BK) + ((chunk ^ swz_k<BK>(row)) << 4);
+}
+
 // XOR swizzle of the 16-byte chunks of a row-contiguous tile: the four K rows
 // read by one 16-lane group of a transpose read land on distinct chunk
 // positions (measured conflict-free).
@@ -91,18 +103,20 @@ struct View {
 // WM x WN waves, each (32*MI) x (32*NI); NSTAGE LDS stages; DBUF: fragment
 // registers double-buffered across K-substeps.
 template <int NA_, int NB_, int NACC_, uint32_t MN_, int WM_, int WN_, int MI_, int NI_, int NSTAGE_,
-          bool DBUF_>
+          bool DBUF_, int BK_>
 struct KindBase {
   static constexpr int NA = NA_, NB = NB_, NACC = NACC_, NOPS = NA_ + NB_;
   static constexpr uint32_t MN = MN_;
   static constexpr int WM = WM_, WN = WN_, MI = MI_, NI = NI_, NSTAGE = NSTAGE_;
   static constexpr bool DBUF = DBUF_;
+  static constexpr int BK = BK_;             // K per LDS stage (16-bit path: 32 or 64)
+  static_assert(BK == 32 || BK == 64, "K tile");
   static constexpr int THREADS = 64 * WM * WN;
   static constexpr int ROWS_A = 32 * MI * WM, ROWS_B = 32 * NI * WN;   // workgroup tile
   static constexpr bool is_mn(int o) { return (MN >> o) & 1u; }
   static constexpr int rows(int o) { return o < NA ? ROWS_A : ROWS_B; }
-  // 16-bit stage layout: 32 K x rows x 2 bytes per operand
-  static constexpr int op_bytes(int o) { return rows(o) * 64; }
+  // 16-bit stage layout: BK K x rows x 2 bytes per operand
+  static constexpr int op_bytes(int o) { return rows(o) * BK * 2; }
   static constexpr int op_off(int o) {
     int s = 0;
     for (int i = 0; i < o; ++i) s += op_bytes(i);
@@ -113,42 +127,48 @@ struct KindBase {
   static constexpr int mn_half(int o) { return __builtin_popcount(MN & ((1u << o) - 1u)) & 1; }
 };
 
-#define LACT_KIND(NAME, NA, NB, NACC, MNMASK, WM, WN, MI, NI, NS, DBUF, PA, PB) \
-  struct NAME : KindBase<NA, NB, NACC, MNMASK, WM, WN, MI, NI, NS, DBUF> {         \
+#define LACT_KIND(NAME, NA, NB, NACC, MNMASK, WM, WN, MI, NI, NS, DBUF, BK, PA, PB) \
+  struct NAME : KindBase<NA, NB, NACC, MNMASK, WM, WN, MI, NI, NS, DBUF, BK> {         \
     static constexpr int pa(int p) { return PA; }                                  \
     static constexpr int pb(int p) { return PB; }                                  \
   }
 
-// 16-bit shapes: 8 waves (2 per SIMD); multi-accumulator kinds use 64 x 64
-// waves (128 x 256 tiles), single-accumulator kinds 128 x 64 (256 x 256).
-// Apply GEMM-1, hidden-major: A = W1, W3 (hidden rows), B = Q (token rows).
-LACT_KIND(KApply16, 2, 1, 2, 0u, 2, 4, 2, 2, 4, true, p, 0 * p);
-// Key forward + hidden backward: A = W1, W3, W2 (W2 read down its columns),
-// B = K, V; accumulators Z1^T, Z3^T and D^T = (V W2)^T.
-LACT_KIND(KUpdate16, 3, 2, 3, 1u << 2, 2, 4, 2, 2, 2, false, p, (p == 2 ? 1 : 0));
+// 16-bit shapes: 8 waves (2 per SIMD); two-accumulator kinds use 64 x 64
+// waves (128 x 256 tiles), one-accumulator kinds 128 x 64 (256 x 256).
+// Kinds whose operands are all K-contiguous take 64 K per stage, so that every
+// DMA fetches whole 128-byte lines; the gradient kinds (row-contiguous, 512
+// bytes and more per K row) keep 32 K and twice the stages.
+// Apply GEMM-1 and the key forward, hidden-major: A = W1, W3 (hidden rows),
+// B = Q or K (token rows).
+LACT_KIND(KApply16, 2, 1, 2, 0u, 2, 4, 2, 2, 2, true, 64, p, 0 * p);
+// Hidden backward of the key forward: A = W2 read down its columns (hidden
+// rows), B = V; accumulator D^T = (V W2)^T. Runs after KApply16 in the same
+// workgroup, whose accumulators stay live.
+LACT_KIND(KDual16, 1, 1, 1, 1u, 2, 4, 2, 2, 2, true, 64, 0 * p, 0 * p);
 // Apply GEMM-2, feature-major: A = W2 (feature rows), B = hidden (token rows).
-LACT_KIND(KOut16, 1, 1, 1, 0u, 2, 4, 4, 2, 4, true, 0 * p, 0 * p);
+LACT_KIND(KOut16, 1, 1, 1, 0u, 2, 4, 4, 2, 2, true, 64, 0 * p, 0 * p);
 // Gradients: A = eta dz1, eta dz3 (hidden rows), B = K (feature rows), all token-major.
-LACT_KIND(KGrad13_16, 2, 1, 2, 7u, 2, 4, 2, 2, 4, true, p, 0 * p);
+LACT_KIND(KGrad13_16, 2, 1, 2, 7u, 2, 4, 2, 2, 4, true, 32, p, 0 * p);
 // A = V (feature rows), B = eta hidden (hidden rows), token-major.
-LACT_KIND(KGrad2_16, 1, 1, 1, 3u, 2, 4, 4, 2, 4, true, 0 * p, 0 * p);
-// fp32 shapes: 4 waves of 64 x 64 (128 x 128 tiles), register path.
-LACT_KIND(KApply32, 2, 1, 2, 0u, 2, 2, 2, 2, 2, false, p, 0 * p);
-LACT_KIND(KUpdate32, 3, 2, 3, 1u << 2, 2, 2, 2, 2, 2, false, p, (p == 2 ? 1 : 0));
-LACT_KIND(KOut32, 1, 1, 1, 0u, 2, 2, 2, 2, 2, false, 0 * p, 0 * p);
-LACT_KIND(KGrad13_32, 2, 1, 2, 7u, 2, 2, 2, 2, 2, false, p, 0 * p);
-LACT_KIND(KGrad2_32, 1, 1, 1, 3u, 2, 2, 2, 2, 2, false, 0 * p, 0 * p);
+LACT_KIND(KGrad2_16, 1, 1, 1, 3u, 2, 4, 4, 2, 4, true, 32, 0 * p, 0 * p);
+// fp32 shapes: 4 waves of 64 x 64 (128 x 128 tiles), register path; the key
+// forward and its hidden backward share one loop (A = W1, W3, W2; B = K, V).
+LACT_KIND(KApply32, 2, 1, 2, 0u, 2, 2, 2, 2, 2, false, 32, p, 0 * p);
+LACT_KIND(KUpdate32, 3, 2, 3, 1u << 2, 2, 2, 2, 2, 2, false, 32, p, (p == 2 ? 1 : 0));
+LACT_KIND(KOut32, 1, 1, 1, 0u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
+LACT_KIND(KGrad13_32, 2, 1, 2, 7u, 2, 2, 2, 2, 2, false, 32, p, 0 * p);
+LACT_KIND(KGrad2_32, 1, 1, 1, 3u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
 // Newton-Schulz products (4 waves, 128 x 128): both operands K-contiguous,
 // both row-contiguous, or only the second (B Y read down the columns of Y).
-LACT_KIND(KNsK, 1, 1, 1, 0u, 2, 2, 2, 2, 4, true, 0 * p, 0 * p);
-LACT_KIND(KNsMN, 1, 1, 1, 3u, 2, 2, 2, 2, 4, true, 0 * p, 0 * p);
-LACT_KIND(KNsBY, 1, 1, 1, 2u, 2, 2, 2, 2, 4, true, 0 * p, 0 * p);
+LACT_KIND(KNsK, 1, 1, 1, 0u, 2, 2, 2, 2, 4, true, 32, 0 * p, 0 * p);
+LACT_KIND(KNsMN, 1, 1, 1, 3u, 2, 2, 2, 2, 4, true, 32, 0 * p, 0 * p);
+LACT_KIND(KNsBY, 1, 1, 1, 2u, 2, 2, 2, 2, 4, true, 32, 0 * p, 0 * p);
 #undef LACT_KIND
 
 template <typename T> struct Kinds;
 template <> struct Kinds<__bf16> {
   using Apply = KApply16;
-  using Update = KUpdate16;
+  using Update = KApply16;   // followed by KDual16
   using Out = KOut16;
   using Grad13 = KGrad13_16;
   using Grad2 = KGrad2_16;
@@ -345,23 +365,25 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(
 constexpr uint32_t kOOB = 0x80000000u;
 constexpr int kRawBufferFlags = 0x00020000;
 
-// Slots: an operand tile of R rows is R*4 slots of 16 bytes; lane `tid` of
-// the workgroup fills slots tid, tid + THREADS, ... (so each wave instruction
-// writes 1 KiB of consecutive LDS).
+// Slots: an operand tile of R rows and BK K is R*BK/8 slots of 16 bytes; lane
+// `tid` of the workgroup fills slots tid, tid + THREADS, ... (so each wave
+// instruction writes 1 KiB of consecutive LDS).
 template <class K, int O>
 struct Dma {
   static constexpr bool MN = K::is_mn(O);
   static constexpr int ROWS = K::rows(O);
-  static constexpr int SLOTS = ROWS * 4 / K::THREADS;   // per lane
-  static_assert(SLOTS >= 1 && SLOTS <= 4 && ROWS * 4 % K::THREADS == 0, "slot split");
-  static constexpr int CPR = ROWS / 8;                   // chunks per K row (mn)
+  static constexpr int BK = K::BK;
+  static constexpr int SLOTS = ROWS * BK / 8 / K::THREADS;   // per lane
+  static_assert(SLOTS >= 1 && SLOTS <= 4 && ROWS * BK / 8 % K::THREADS == 0, "slot split");
+  static constexpr int CPK = BK / 8;                          // chunks per row (k)
+  static constexpr int CPR = ROWS / 8;                        // chunks per K row (mn)
 
   static __device__ __forceinline__ void offsets(uint32_t (&vo)[4], const View& v) {
 #pragma unroll
     for (int i = 0; i < SLOTS; ++i) {
       const int p = i * K::THREADS + threadIdx.x;
       if (!MN) {
-        const int row = p >> 2, c = (p & 3) ^ lds_swz(p >> 2);
+        const int row = p / CPK, c = (p % CPK) ^ swz_k<BK>(p / CPK);
         vo[i] = row < v.nrows ? (uint32_t)(row * v.ld_b + c * 16) : kOOB;
       } else {
         const int kr = p / CPR, c = (p % CPR) ^ swz_mn(p / CPR);
@@ -372,27 +394,36 @@ struct Dma {
 
   // DMA of k-tile kt into `tile`: a raw buffer descriptor whose base advances
   // with kt and whose size covers only the valid data, so K rows past the end
-  // (row-contiguous operands) load as zeros.
+  // (row-contiguous operands) load as zeros. K-contiguous operands whose K is
+  // not a multiple of BK zero the chunks past K in their last tile.
   static __device__ __forceinline__ void issue(uint8_t* tile, const View& v, const uint32_t (&vo)[4], int kt) {
     const uint8_t* base;
     int64_t span;
     if (!MN) {
-      base = v.p + (int64_t)kt * 64;
+      base = v.p + (int64_t)kt * BK * 2;
       const int64_t rows = v.nrows < ROWS ? v.nrows : ROWS;
-      span = rows > 0 ? (rows - 1) * v.ld_b + 64 : 0;
+      span = rows > 0 ? (rows - 1) * v.ld_b + BK * 2 : 0;
     } else {
-      base = v.p + (int64_t)kt * 32 * v.ld_b;
-      int64_t rows = v.nk - (int64_t)kt * 32;
-      rows = rows < 0 ? 0 : (rows > 32 ? 32 : rows);
+      base = v.p + (int64_t)kt * BK * v.ld_b;
+      int64_t rows = v.nk - (int64_t)kt * BK;
+      rows = rows < 0 ? 0 : (rows > BK ? BK : rows);
       span = rows * v.ld_b;
     }
     const __amdgpu_buffer_rsrc_t rsrc =
         __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)span, kRawBufferFlags);
     const int w = threadIdx.x >> 6;
+    const int64_t kleft = v.nk - (int64_t)kt * BK;   // K left from this tile's start
 #pragma unroll
-    for (int i = 0; i < SLOTS; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, to_lds(tile + (i * K::THREADS + w * 64) * 16), 16, vo[i], 0,
-                                               0, 0);
+    for (int i = 0; i < SLOTS; ++i) {
+      uint32_t off = vo[i];
+      if (!MN && kleft < BK) {
+        const int p = i * K::THREADS + threadIdx.x;
+        const int c = (p % CPK) ^ swz_k<BK>(p / CPK);
+        if (c * 8 >= kleft) off = kOOB;
+      }
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, to_lds(tile + (i * K::THREADS + w * 64) * 16), 16, off, 0, 0,
+                                               0);
+    }
   }
 };
 
@@ -425,8 +456,9 @@ __device__ __forceinline__ u32x4_t lds_read_b128(uint32_t a) {
 }
 
 // K-contiguous fragment: 8 K of row `row`, 16-byte chunk `chunk`.
+template <int BK>
 __device__ __forceinline__ u32x4_t frag_k(const uint8_t* tile, int row, int chunk) {
-  return lds_read_b128(lds_addr(tile) + lds_off(row, chunk));
+  return lds_read_b128(lds_addr(tile) + lds_off_k<BK>(row, chunk));
 }
 
 // Row-contiguous fragment (8 consecutive K of row rb + lane%32, K block
@@ -474,13 +506,14 @@ __device__ __forceinline__ void load_frags(Frags<K>& f, const uint8_t* buf, int 
 #pragma unroll
     for (int mi = 0; mi < K::MI; ++mi)
       f.a[o][mi] = K::is_mn(o) ? frag_tr(buf + K::op_off(o), ab + mi * 32, s, K::ROWS_A * 2)
-                               : frag_k(buf + K::op_off(o), ab + mi * 32 + (lane & 31), 2 * s + half);
+                               : frag_k<K::BK>(buf + K::op_off(o), ab + mi * 32 + (lane & 31), 2 * s + half);
 #pragma unroll
   for (int o = 0; o < K::NB; ++o)
 #pragma unroll
     for (int ni = 0; ni < K::NI; ++ni)
       f.b[o][ni] = K::is_mn(K::NA + o) ? frag_tr(buf + K::op_off(K::NA + o), bb + ni * 32, s, K::ROWS_B * 2)
-                                       : frag_k(buf + K::op_off(K::NA + o), bb + ni * 32 + (lane & 31), 2 * s + half);
+                                       : frag_k<K::BK>(buf + K::op_off(K::NA + o), bb + ni * 32 + (lane & 31),
+                                                       2 * s + half);
 }
 
 // Wait until at most N LDS instructions are outstanding and make every
@@ -518,22 +551,24 @@ __device__ __forceinline__ void mfma_frags(const Frags<K>& f, Acc<K>& acc) {
       }
 }
 
-// NSTAGE k-tiles in flight. Per k-tile kt (stage kt % NS), with DBUF:
-//   read substep 1 of kt | MFMA substep 0 | wait reads of kt and DMA of kt+1 |
-//   barrier | DMA kt+NS into the freed stage | read substep 0 of kt+1 |
-//   MFMA substep 1
+// NSTAGE k-tiles in flight, S = BK/16 MFMA substeps per tile. Per k-tile kt
+// (stage kt % NS), with DBUF the fragment reads of substep s+1 are in flight
+// while substep s multiplies; after the last reads of kt:
+//   wait DMA of kt+1 | barrier | DMA kt+NS into the freed stage |
+//   read substep 0 of kt+1 | MFMA substep S-1 of kt
 // without DBUF every substep reads, waits and multiplies in turn.
 template <typename T, class K>
 __device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk, Acc<K>& acc) {
-  constexpr int BK = 32, NS = K::NSTAGE;
+  constexpr int BK = K::BK, NS = K::NSTAGE, S = BK / 16;
   constexpr int L = [] {          // DMA instructions per lane per k-tile
     int n = 0;
-    for (int o = 0; o < K::NOPS; ++o) n += K::rows(o) * 4 / K::THREADS;
+    for (int o = 0; o < K::NOPS; ++o) n += K::rows(o) * K::BK / 8 / K::THREADS;
     return n;
   }();
   constexpr int R = Frags<K>::kReads();
   static_assert(!K::DBUF || R < 16, "substep reads exceed lgkmcnt");
   static_assert(L * NS < 64, "DMA in flight exceeds vmcnt");
+  static_assert(S % 2 == 0, "substeps per tile");
   const int nkt = (int)((nk + BK - 1) / BK);
   if (nkt <= 0) return;
   uint32_t vo[K::NOPS][4];
@@ -547,24 +582,27 @@ __device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K:
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   if constexpr (K::DBUF) {
-    Frags<K> f0, f1;
-    load_frags<K>(f0, smem, 0);
+    Frags<K> f[2];
+    load_frags<K>(f[0], smem, 0);
     for (int kt = 0; kt < nkt; ++kt) {
       const uint8_t* cur = smem + (kt % NS) * K::STAGE;
-      load_frags<K>(f1, cur, 1);
-      frags_ready<R, K>(f0);                  // substep 0 is in; substep 1 still in flight
-      mfma_frags<T, K>(f0, acc);
-      __builtin_amdgcn_sched_barrier(0);      // issue all of them before the next wait
-      frags_ready<0, K>(f1);                  // this wave is done reading tile kt
+#pragma unroll
+      for (int s = 0; s + 1 < S; ++s) {
+        load_frags<K>(f[(s + 1) & 1], cur, s + 1);
+        frags_ready<R, K>(f[s & 1]);           // substep s is in; s+1 still in flight
+        mfma_frags<T, K>(f[s & 1], acc);
+        __builtin_amdgcn_sched_barrier(0);     // issue all of them before the next wait
+      }
+      frags_ready<0, K>(f[(S - 1) & 1]);       // this wave is done reading tile kt
       if (kt + 1 < nkt) {
         if (kt + NS - 1 < nkt) wait_vmcnt<L * (NS - 2)>();   // tile kt+1 landed
         else wait_vmcnt<0>();
       }
-      __builtin_amdgcn_s_barrier();           // every wave is past tile kt and has tile kt+1
+      __builtin_amdgcn_s_barrier();            // every wave is past tile kt and has tile kt+1
       asm volatile("" ::: "memory");
-      if (kt + NS < nkt) issue(kt + NS);      // refill the stage tile kt used
-      if (kt + 1 < nkt) load_frags<K>(f0, smem + ((kt + 1) % NS) * K::STAGE, 0);
-      mfma_frags<T, K>(f1, acc);
+      if (kt + NS < nkt) issue(kt + NS);       // refill the stage tile kt used
+      if (kt + 1 < nkt) load_frags<K>(f[0], smem + ((kt + 1) % NS) * K::STAGE, 0);
+      mfma_frags<T, K>(f[(S - 1) & 1], acc);
       __builtin_amdgcn_sched_barrier(0);
     }
   } else {
@@ -572,7 +610,7 @@ __device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K:
     for (int kt = 0; kt < nkt; ++kt) {
       const uint8_t* cur = smem + (kt % NS) * K::STAGE;
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
+      for (int s = 0; s < S; ++s) {
         load_frags<K>(f, cur, s);
         frags_ready<0, K>(f);
         mfma_frags<T, K>(f, acc);
@@ -645,6 +683,141 @@ __device__ __forceinline__ View view_mn(const Operand& op, int inst, int64_t row
   return View{reinterpret_cast<const uint8_t*>(op.base) + off * esz, op.ld * esz, nrows, nk};
 }
 
+// Output staging (16-bit): an accumulator tile of R output rows (hidden units
+// or features, the MFMA row index) x C tokens is written to LDS token-major,
+// R*2 bytes per token row, and then copied to the token-major output with
+// 16-byte lanes, 16 or 32 lanes per token row: every store instruction writes
+// whole 128-byte lines instead of 16-byte pieces of 32 lines. The 16-byte
+// chunks of a row are XOR-rotated by the token's low 4 bits, so that the 32
+// tokens of one accumulator write and the 16 chunks of one row read spread
+// over all banks.
+template <int R>
+__device__ __forceinline__ void stage_put(uint8_t* buf, int tok, int row, float a, float b, float c, float d) {
+  typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_t;
+  const int off = tok * (2 * R) + ((((row >> 3) ^ (tok & 15))) << 4) + (((row >> 2) & 1) << 3);
+  *reinterpret_cast<bf16x4_t*>(buf + off) = bf16x4_t{(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+}
+
+// Copy the staged tile to out (element (token 0, row 0) of the tile, ld
+// elements between tokens): tokens < ntok, rows < nrow (a multiple of 8).
+template <int R, int C, int THREADS>
+__device__ __forceinline__ void stage_flush(const uint8_t* buf, __bf16* out, int64_t ld, int64_t ntok, int64_t nrow) {
+  constexpr int CPR = R / 8, TOTAL = C * CPR;
+  static_assert(CPR >= 16 && TOTAL % THREADS == 0, "staging shape");
+#pragma unroll
+  for (int i = 0; i < TOTAL / THREADS; ++i) {
+    const int q = i * THREADS + threadIdx.x;
+    const int tok = q / CPR, c = q % CPR;
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(buf + tok * (2 * R) + ((c ^ (tok & 15)) << 4));
+    if (tok < ntok && c * 8 < nrow) *reinterpret_cast<u32x4_t*>(out + tok * ld + c * 8) = v;
+  }
+}
+
+// Key-forward epilogue: from Z1, Z3 and D = W2^T v (hidden-major tiles) write
+// eta*hidden, eta*dz1 and eta*dz3 token-major, four hidden units per store.
+template <typename T, class K>
+__device__ __forceinline__ void update_epilogue(const f32x16_t (&z1a)[K::MI][K::NI], const f32x16_t (&z3a)[K::MI][K::NI],
+                                                const f32x16_t (&dda)[K::MI][K::NI], const FwdSeg& sg, int inst,
+                                                int64_t j0, int64_t i0, int64_t hrows, int64_t ntok, int h) {
+  const int lane = threadIdx.x & 63;
+  const int64_t ob = inst * sg.out_inst;
+  const float* eta = sg.eta + inst * sg.eta_inst + i0;
+  const int hrow0 = wave_m<K>() * 32 * K::MI + ((lane >> 5) << 2);
+#pragma unroll
+  for (int ni = 0; ni < K::NI; ++ni) {
+    const int tok = acc_col<K>(ni);
+    if (tok >= ntok) continue;
+    const float et = eta[tok];
+#pragma unroll
+    for (int mi = 0; mi < K::MI; ++mi)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int hid = hrow0 + mi * 32 + 8 * g;
+        if (hid >= hrows) continue;
+        float vh[4], vg[4], vb[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;
+          const float z1 = z1a[mi][ni][r], z3 = z3a[mi][ni][r], dh = dda[mi][ni][r];
+          const float s = sigmoidf_fast(z1);
+          const float a = z1 * s;                     // SiLU(z1)
+          const float ed = et * dh;                   // eta_i * (W2^T v_i)_j
+          vh[e] = et * a * z3;                        // eta * hidden
+          vg[e] = ed * z3 * s * (1.0f + z1 * (1.0f - s));   // eta * dz1
+          vb[e] = ed * a;                             // eta * dz3
+        }
+        const int64_t idx = ob + (i0 + tok) * h + j0 + hid;
+        st4<T>(sg.out1, idx, vh[0], vh[1], vh[2], vh[3]);
+        st4<T>(sg.out2, idx, vg[0], vg[1], vg[2], vg[3]);
+        st4<T>(sg.out3, idx, vb[0], vb[1], vb[2], vb[3]);
+      }
+  }
+}
+
+// The same for 16-bit outputs, staged through LDS (two 64 KiB buffers):
+// eta*hidden and eta*dz1 first, then eta*dz3.
+template <class K>
+__device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::MI][K::NI],
+                                                       const f32x16_t (&z3a)[K::MI][K::NI],
+                                                       const f32x16_t (&dda)[K::MI][K::NI], const FwdSeg& sg,
+                                                       int inst, int64_t j0, int64_t i0, int64_t hrows,
+                                                       int64_t ntok, int h, uint8_t* smem) {
+  constexpr int R = K::ROWS_A, C = K::ROWS_B;
+  uint8_t* buf0 = smem;
+  uint8_t* buf1 = smem + R * C * 2;
+  const int lane = threadIdx.x & 63;
+  const float* eta = sg.eta + inst * sg.eta_inst + i0;
+  const int hrow0 = wave_m<K>() * 32 * K::MI + ((lane >> 5) << 2);
+  float et[K::NI];
+#pragma unroll
+  for (int ni = 0; ni < K::NI; ++ni) {
+    const int tok = acc_col<K>(ni);
+    et[ni] = tok < ntok ? eta[tok] : 0.0f;
+  }
+#pragma unroll
+  for (int ni = 0; ni < K::NI; ++ni)
+#pragma unroll
+    for (int mi = 0; mi < K::MI; ++mi)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float vh[4], vg[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;
+          const float z1 = z1a[mi][ni][r], z3 = z3a[mi][ni][r];
+          const float s = sigmoidf_fast(z1);
+          const float ed = et[ni] * dda[mi][ni][r];
+          vh[e] = et[ni] * z1 * s * z3;
+          vg[e] = ed * z3 * s * (1.0f + z1 * (1.0f - s));
+        }
+        const int tok = acc_col<K>(ni), row = hrow0 + mi * 32 + 8 * g;
+        stage_put<R>(buf0, tok, row, vh[0], vh[1], vh[2], vh[3]);
+        stage_put<R>(buf1, tok, row, vg[0], vg[1], vg[2], vg[3]);
+      }
+  __syncthreads();
+  const int64_t tile = inst * sg.out_inst + i0 * h + j0;
+  stage_flush<R, C, K::THREADS>(buf0, reinterpret_cast<__bf16*>(sg.out1) + tile, h, ntok, hrows);
+  stage_flush<R, C, K::THREADS>(buf1, reinterpret_cast<__bf16*>(sg.out2) + tile, h, ntok, hrows);
+  __syncthreads();
+#pragma unroll
+  for (int ni = 0; ni < K::NI; ++ni)
+#pragma unroll
+    for (int mi = 0; mi < K::MI; ++mi)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float vb[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;
+          const float z1 = z1a[mi][ni][r];
+          vb[e] = et[ni] * dda[mi][ni][r] * z1 * sigmoidf_fast(z1);
+        }
+        stage_put<R>(buf0, acc_col<K>(ni), hrow0 + mi * 32 + 8 * g, vb[0], vb[1], vb[2], vb[3]);
+      }
+  __syncthreads();
+  stage_flush<R, C, K::THREADS>(buf0, reinterpret_cast<__bf16*>(sg.out3) + tile, h, ntok, hrows);
+}
+
 // ===========================================================================
 // First launch of a chunk. Accumulators are hidden-major (rows = hidden units
 // j, columns = tokens i): every lane holds four consecutive hidden units of
@@ -655,7 +828,8 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
   using KA = typename Kinds<T>::Apply;
   using KU = typename Kinds<T>::Update;
   static_assert(KA::THREADS == KU::THREADS, "one block size per launch");
-  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(smem_bytes<T, KA>(), smem_bytes<T, KU>())];
+  __shared__ __attribute__((aligned(16)))
+  uint8_t smem[cmax(smem_bytes<T, KA>(), cmax(smem_bytes<T, KU>(), sizeof(T) == 2 ? smem_bytes<T, KDual16>() : 0))];
   constexpr int esz = sizeof(T);
   int bid = blockIdx.x;
   const bool first = bid < args.seg[0].nblocks;
@@ -678,6 +852,27 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
     mainloop<T, KA>(smem, ops, d, acc);
     void* out = reinterpret_cast<uint8_t*>(sg.out0) + (inst * sg.out_inst) * esz;
     const int hrow0 = wave_m<KA>() * 32 * KA::MI + ((lane >> 5) << 2);
+    if constexpr (sizeof(T) == 2) {
+      static_assert(KA::ROWS_A * KA::ROWS_B * 2 <= sizeof(smem), "staging fits");
+#pragma unroll
+      for (int ni = 0; ni < KA::NI; ++ni)
+#pragma unroll
+        for (int mi = 0; mi < KA::MI; ++mi)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float z1 = acc[0][mi][ni][4 * g + e], z3 = acc[1][mi][ni][4 * g + e];
+              v[e] = z1 * sigmoidf_fast(z1) * z3;
+            }
+            stage_put<KA::ROWS_A>(smem, acc_col<KA>(ni), hrow0 + mi * 32 + 8 * g, v[0], v[1], v[2], v[3]);
+          }
+      __syncthreads();
+      stage_flush<KA::ROWS_A, KA::ROWS_B, KA::THREADS>(smem, reinterpret_cast<__bf16*>(out) + i0 * h + j0, h, ntok,
+                                                         hrows);
+      return;
+    }
 #pragma unroll
     for (int ni = 0; ni < KA::NI; ++ni) {
       const int tok = acc_col<KA>(ni);
@@ -701,42 +896,28 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
     const int64_t j0 = (int64_t)(rr % sg.tiles_m) * KU::ROWS_A;
     const int64_t i0 = (int64_t)(rr / sg.tiles_m) * KU::ROWS_B;
     const int64_t hrows = h - j0, ntok = sg.rows - i0;
-    const View ops[5] = {view_k(args.w1, inst, j0, 0, hrows, d, esz), view_k(args.w3, inst, j0, 0, hrows, d, esz),
-                         view_mn(args.w2, inst, j0, 0, hrows, d, esz), view_k(sg.a0, inst, i0, 0, ntok, d, esz),
-                         view_k(sg.a1, inst, i0, 0, ntok, d, esz)};
-    Acc<KU> acc;
-    mainloop<T, KU>(smem, ops, d, acc);
-    const int64_t ob = inst * sg.out_inst;
-    const float* eta = sg.eta + inst * sg.eta_inst + i0;
-    const int hrow0 = wave_m<KU>() * 32 * KU::MI + ((lane >> 5) << 2);
-#pragma unroll
-    for (int ni = 0; ni < KU::NI; ++ni) {
-      const int tok = acc_col<KU>(ni);
-      if (tok >= ntok) continue;
-      const float et = eta[tok];
-#pragma unroll
-      for (int mi = 0; mi < KU::MI; ++mi)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int hid = hrow0 + mi * 32 + 8 * g;
-          if (hid >= hrows) continue;
-          float vh[4], vg[4], vb[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * g + e;
-            const float z1 = acc[0][mi][ni][r], z3 = acc[1][mi][ni][r], dh = acc[2][mi][ni][r];
-            const float s = sigmoidf_fast(z1);
-            const float a = z1 * s;                     // SiLU(z1)
-            const float ed = et * dh;                   // eta_i * (W2^T v_i)_j
-            vh[e] = et * a * z3;                        // eta * hidden
-            vg[e] = ed * z3 * s * (1.0f + z1 * (1.0f - s));   // eta * dz1
-            vb[e] = ed * a;                             // eta * dz3
-          }
-          const int64_t idx = ob + (i0 + tok) * h + j0 + hid;
-          st4<T>(sg.out1, idx, vh[0], vh[1], vh[2], vh[3]);
-          st4<T>(sg.out2, idx, vg[0], vg[1], vg[2], vg[3]);
-          st4<T>(sg.out3, idx, vb[0], vb[1], vb[2], vb[3]);
-        }
+    const View w1 = view_k(args.w1, inst, j0, 0, hrows, d, esz), w3 = view_k(args.w3, inst, j0, 0, hrows, d, esz);
+    const View w2 = view_mn(args.w2, inst, j0, 0, hrows, d, esz);
+    const View kk = view_k(sg.a0, inst, i0, 0, ntok, d, esz), vv = view_k(sg.a1, inst, i0, 0, ntok, d, esz);
+    if constexpr (sizeof(T) == 2) {
+      // Z1^T, Z3^T first, then D^T with the Z accumulators held: one
+      // accumulator set per loop keeps the loops free of register spills.
+      using KD = KDual16;
+      static_assert(KD::ROWS_A == KU::ROWS_A && KD::ROWS_B == KU::ROWS_B && KD::WM == KU::WM &&
+                        KD::MI == KU::MI && KD::NI == KU::NI, "accumulator layouts match");
+      Acc<KU> az;
+      Acc<KD> ad;
+      const View opz[3] = {w1, w3, kk};
+      mainloop<T, KU>(smem, opz, d, az);
+      const View opd[2] = {w2, vv};
+      mainloop<T, KD>(smem, opd, d, ad);
+      static_assert(2 * KU::ROWS_A * KU::ROWS_B * 2 <= sizeof(smem), "staging fits");
+      update_epilogue_staged<KU>(az[0], az[1], ad[0], sg, inst, j0, i0, hrows, ntok, h, smem);
+    } else {
+      const View ops[5] = {w1, w3, w2, kk, vv};
+      Acc<KU> acc;
+      mainloop<T, KU>(smem, ops, d, acc);
+      update_epilogue<T, KU>(acc[0], acc[1], acc[2], sg, inst, j0, i0, hrows, ntok, h);
     }
   }
 }
@@ -783,6 +964,23 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
     mainloop<T, KO>(smem, ops, h, acc);
     const int64_t ob = inst * sg.out_inst;
     const int mrow0 = wave_m<KO>() * 32 * KO::MI + ((lane >> 5) << 2);
+    if constexpr (sizeof(T) == 2) {
+      static_assert(KO::ROWS_A * KO::ROWS_B * 2 <= sizeof(smem), "staging fits");
+#pragma unroll
+      for (int ni = 0; ni < KO::NI; ++ni)
+#pragma unroll
+        for (int mi = 0; mi < KO::MI; ++mi)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x16_t& a = acc[0][mi][ni];
+            stage_put<KO::ROWS_A>(smem, acc_col<KO>(ni), mrow0 + mi * 32 + 8 * g, a[4 * g], a[4 * g + 1],
+                                  a[4 * g + 2], a[4 * g + 3]);
+          }
+      __syncthreads();
+      stage_flush<KO::ROWS_A, KO::ROWS_B, KO::THREADS>(smem, reinterpret_cast<__bf16*>(sg.out) + ob + t0 * d + m0, d,
+                                                         ntok, mrows);
+      return;
+    }
 #pragma unroll
     for (int ni = 0; ni < KO::NI; ++ni) {
       const int tok = acc_col<KO>(ni);
@@ -1082,7 +1280,7 @@ __global__ __launch_bounds__(256) void k_ns_scale(const NsPrepArgs a, void* yb, 
 
 TileShape fwd_tile(int kind, bool io_bf16) {
   if (io_bf16) return kind == FWD_APPLY ? TileShape{KApply16::ROWS_A, KApply16::ROWS_B, KApply16::THREADS}
-                                        : TileShape{KUpdate16::ROWS_A, KUpdate16::ROWS_B, KUpdate16::THREADS};
+                                        : TileShape{KApply16::ROWS_A, KApply16::ROWS_B, KApply16::THREADS};
   return kind == FWD_APPLY ? TileShape{KApply32::ROWS_A, KApply32::ROWS_B, KApply32::THREADS}
                            : TileShape{KUpdate32::ROWS_A, KUpdate32::ROWS_B, KUpdate32::THREADS};
 }

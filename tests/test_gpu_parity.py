@@ -94,6 +94,17 @@ def test_bf16_ragged_multi_tile(order):
 
 
 @pytest.mark.parametrize("order", [0, 1])
+def test_bf16_dims_of_32_mod_64(order):
+    # d and h are multiples of 32 but not of 64: contraction tiles that take
+    # 64 K per stage end on a half-empty tile (over d in the key forward and
+    # apply, over h in the output contraction)
+    cfg = CONFIGS["video"].with_(name="k32tail", B=1, H=2, d=96, h=160, n_kv=300, n_q=333,
+                                 chunk=128, use_muon=0, order=order)
+    x = make_inputs(cfg, 6)
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
+@pytest.mark.parametrize("order", [0, 1])
 def test_fp32_ragged_small_dims(order):
     cfg = CONFIGS["tiny_fp32"].with_(name="fp32small", B=2, H=1, d=40, h=24, n_kv=300, n_q=333,
                                      chunk=100, order=order)

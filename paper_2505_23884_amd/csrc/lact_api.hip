@@ -68,14 +68,16 @@ Plan make_plan(const lact_desc* dsc) {
   // update-then-apply can apply its last chunk together with the tail.
   p.cap = std::min<int64_t>(dsc->n_q, p.C + std::min<int64_t>(tail, std::max<int64_t>(p.C, 65536)));
   if (p.cap < 1) p.cap = 1;
-  // Split-K of the gradient contraction: enough blocks to fill the chip
-  // (~512), each split at least 256 tokens, lengths a multiple of 32.
+  // Split-K of the gradient contraction (fp32 partials, summed by the weight
+  // update) only when the gradient tiles alone would leave most of the chip
+  // idle: each split adds a full read and write of d*h*3 fp32 per instance,
+  // which costs more than the parallelism gains once the tiles (with the
+  // apply GEMM-2 tiles sharing the launch) cover half of the 256 CUs.
+  // Splits are at least 256 tokens, lengths a multiple of 32.
   const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
   const int64_t tiles = (int64_t)p.BH * (cdiv(p.h, g13.rows) * cdiv(p.d, g13.cols) +
                                          cdiv(p.d, g2.rows) * cdiv(p.h, g2.cols));
-  // one wave of big gradient tiles fills the chip when the apply GEMM-2 tiles
-  // share the launch (they take the remaining CUs)
-  int64_t ns = std::max<int64_t>(1, cdiv(256, tiles));
+  int64_t ns = std::max<int64_t>(1, cdiv(128, tiles));
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.C / 256));
   ns = std::min<int64_t>(ns, kMaxSplit);
   p.split_len = std::max<int64_t>(32, cdiv(cdiv(std::max<int64_t>(p.C, 1), ns), 32) * 32);

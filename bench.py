@@ -9,10 +9,20 @@ per step does not depend on their values.
 Prints ONE JSON line (see the keys below). `value` is algorithmic TFLOP/s of
 the whole path (App. A FLOP count: 18*d*h per token per head, plus Muon);
 tokens/s and the fraction of the bf16 MFMA peak are reported beside it.
+
+Two helper modes serve the HBM-traffic figure of the roofline:
+  --copy-calibration        runs a plain device copy of known size (for the
+                            rocprofv3 FETCH_SIZE / WRITE_SIZE scale factor)
+  --traffic-report F W CF CW  turns four rocprofv3 --pmc CSVs (FETCH_SIZE and
+                            WRITE_SIZE of this bench and of the copy) into
+                            profiles/lact_<config>_traffic.json, stamped with
+                            the hash of the kernel source it was taken on
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -25,6 +35,10 @@ METRIC = "LaCT layer fwd TFLOP/s + tokens/s at 32K ctx; % of bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+KERNEL_SOURCES = ("paper_2505_23884_amd/csrc/lact_kernels.hip", "paper_2505_23884_amd/csrc/lact_api.hip",
+                  "paper_2505_23884_amd/csrc/lact_internal.h")
+DOMINANT_KERNEL = {"fwd": "k_fwd", "bwd": "k_bwd", "update": "k_update", "ns": "k_ns"}
+COPY_MIB = 1024
 
 
 def parse():
@@ -36,7 +50,94 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--traffic-report", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"))
     return ap.parse_args()
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def copy_calibration():
+    """A plain elementwise copy of COPY_MIB MiB (read once, written once), five times."""
+    import torch
+    n = COPY_MIB << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        torch.mul(src, 1, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "reps": 5}), flush=True)
+
+
+def _pmc(path, counter):
+    """Per-dispatch values of one counter from a rocprofv3 counter_collection CSV:
+    {kernel name: [values]}."""
+    out = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return out
+
+
+def kernel_short_name(name):
+    """k_fwd, k_bwd, ... from a mangled (…5k_fwdI…) or demangled (…::k_fwd<…) kernel name."""
+    for k in ("k_fwd", "k_bwd", "k_update", "k_prep", "k_ns_prep", "k_ns_scale", "k_ns"):
+        m = str(len(k)) + k
+        if m + "I" in name or m + "E" in name or "::" + k + "<" in name or "::" + k + "(" in name:
+            return k
+    return None
+
+
+def traffic_report(cfg_name, fetch_csv, write_csv, cfetch_csv, cwrite_csv):
+    """HBM bytes per launch of every lact kernel: the counter's median per
+    dispatch, scaled by copy_bytes / (the same counter for the copy kernel)."""
+    import statistics
+    cf, cw = _pmc(cfetch_csv, "FETCH_SIZE"), _pmc(cwrite_csv, "WRITE_SIZE")
+    copy_fetch = max(max(v) for v in cf.values())
+    copy_write = max(max(v) for v in cw.values())
+    n = COPY_MIB << 20
+    scale = {"fetch": n / copy_fetch, "write": n / copy_write}
+    f, w = _pmc(fetch_csv, "FETCH_SIZE"), _pmc(write_csv, "WRITE_SIZE")
+    kernels = {}
+    for name in f:
+        short = kernel_short_name(name)
+        if short is None or name not in w:
+            continue
+        fb = statistics.median(f[name]) * scale["fetch"]
+        wb = statistics.median(w[name]) * scale["write"]
+        kernels[short] = {"fetch_bytes": round(fb), "write_bytes": round(wb), "traffic_bytes": round(fb + wb),
+                          "dispatches": len(f[name])}
+    rep = {"config": cfg_name, "kernels_source_sha256": source_hash(),
+           "calibration": {"copy_bytes": n, "copy_fetch_counter": copy_fetch, "copy_write_counter": copy_write,
+                           "fetch_scale": scale["fetch"], "write_scale": scale["write"]},
+           "kernels": kernels}
+    out = os.path.join(ROOT, "profiles", f"lact_{cfg_name}_traffic.json")
+    with open(out, "w") as fh:
+        json.dump(rep, fh, indent=1)
+    print(json.dumps(rep), flush=True)
+
+
+def measured_traffic(cfg_name, kernel):
+    """Calibrated HBM bytes per launch of `kernel` from the committed counter
+    report, or None when there is none or the kernels changed since."""
+    path = os.path.join(ROOT, "profiles", f"lact_{cfg_name}_traffic.json")
+    try:
+        with open(path) as fh:
+            rep = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rep.get("kernels_source_sha256") != source_hash():
+        return None
+    k = rep.get("kernels", {}).get(kernel)
+    return k["traffic_bytes"] if k else None
 
 
 def describe(cfg):
@@ -73,11 +174,16 @@ def cpu_baseline(cfg, min_seconds):
 
 def main():
     args = parse()
+    if args.traffic_report:
+        traffic_report(args.config, *args.traffic_report)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
-    import numpy as np
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
 
     import paper_2505_23884_amd as P
@@ -144,10 +250,15 @@ def main():
         dom = max(per, key=lambda kname: per[kname]["total_ms"])
         d = per[dom]
         achieved = d["tflops"] or 0.0
-        res["roofline"] = {"bound": "mfma", "kernel": f"lact {dom} kernel class",
+        kname = DOMINANT_KERNEL.get(dom, dom)
+        traffic = measured_traffic(cfg.name, kname)
+        res["roofline"] = {"bound": "mfma", "kernel": kname,
                            "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                           "frac": round(achieved / peak, 4), "traffic": None,
-                           "avg_launch_us": d["avg_us"], "per_class": per}
+                           "frac": round(achieved / peak, 4), "traffic": traffic,
+                           "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                           "avg_launch_us": d["avg_us"],
+                           "flops_per_launch": round(achieved * 1e12 * d["avg_us"] * 1e-6),
+                           "per_class": per}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(res), flush=True)

@@ -37,6 +37,7 @@ GOOD = dict(B=2, H=2, d=64, h=128, n_kv=1000, n_q=1100, chunk=256, order=0, use_
 
 @pytest.mark.parametrize("field,value,code", [
     ("B", 0, -1), ("H", -1, -1), ("d", 0, -1), ("d", 12, -4), ("h", 4100, -4), ("h", 20, -4),
+    ("d", 40, -4), ("h", 160 + 8, -4), ("B", 1 << 20, -4),
     ("n_kv", -1, -1), ("n_q", 999, -1), ("chunk", 0, -1), ("order", 2, -1),
     ("ns_steps", 17, -1), ("ns_steps", -1, -1), ("io_dtype", 3, -1),
 ])
@@ -48,6 +49,14 @@ def test_descriptor_validation(field, value, code):
     err = ctypes.c_int(0)
     assert P.lib().lact_workspace_bytes(ctypes.byref(d), ctypes.byref(err)) == 0
     assert err.value == code
+
+
+def test_fp32_envelope_is_multiples_of_8():
+    # bf16 I/O needs multiples of 32 (d = 40 is rejected above); fp32 I/O takes 8
+    kw = dict(GOOD, d=40, h=24, io_dtype=1)
+    assert P.check_desc(make_desc(**kw)) == 0
+    kw = dict(GOOD, d=96, h=160)
+    assert P.check_desc(make_desc(**kw)) == 0
 
 
 def test_workspace_grows_with_the_chunk():

@@ -261,6 +261,8 @@ int newton_schulz(Ctx& c) {
   // segment 0: W1 and W3 stored h x d; segment 1: W2 stored d x h
   const int rows[2] = {h, d}, cols[2] = {d, h};
   const int64_t mm = (int64_t)m * m;
+  // 256 x 256 tiles for Gram matrices larger than 128, else 128 x 128
+  const bool big = p.ns_fp16 && m > 128;
   for (int t = 0; t < c.dsc->ns_steps; ++t) {
     NsArgs a{};
     a.Y32 = pa.Y32;
@@ -295,18 +297,19 @@ int newton_schulz(Ctx& c) {
           sg.kind = NS_POLY;
           sg.M = sg.N = sg.K = m;
         } else {
+          // tile space of the update: rows = columns of Y, columns = rows of Y
           sg.kind = wide ? NS_UPD_BY : NS_UPD_YB;
-          sg.M = rows[g];
-          sg.N = cols[g];
+          sg.M = cols[g];
+          sg.N = rows[g];
           sg.K = m;
         }
-        sg.tiles_m = (int)cdiv(sg.M, kTile);
-        sg.tiles_n = (int)cdiv(sg.N, kTile);
+        sg.tiles_m = (int)cdiv(sg.M, ns_tile(p.ns_fp16, big).rows);
+        sg.tiles_n = (int)cdiv(sg.N, ns_tile(p.ns_fp16, big).cols);
         sg.nblocks = p.BH * sg.group * sg.tiles_m * sg.tiles_n;
         a.total_blocks += sg.nblocks;
         fl += 2.0 * p.BH * sg.group * (double)sg.M * sg.N * sg.K;
       }
-      rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns(a, p.ns_fp16, c.s); });
+      rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns(a, p.ns_fp16, big, c.s); });
       if (rc) return rc;
     }
   }

@@ -7,7 +7,6 @@
 
 namespace lact {
 
-constexpr int kTile = 128;        // output tile edge of the Newton-Schulz products lanes
 constexpr int kMaxDim = 4096;     // envelope for d and h
 constexpr int kMaxSplit = 64;     // split-K ways of the gradient contraction
 
@@ -87,6 +86,9 @@ struct UpdArgs {
 // runs on the wide orientation of Y:
 //   wide (r <= c):  A = Y Y^T,  B = b A + c A A,  Y <- a Y + B Y
 //   tall (r >  c):  A = Y^T Y,  B = b A + c A A,  Y <- a Y + Y B
+// Each product is computed in "tile space", the transpose of what is stored
+// (NsSeg M, N are tile-space rows and columns): A and B are symmetric; for
+// the update, tile rows are the columns of Y and tile columns its rows.
 enum NsKind : int { NS_GRAM_K = 0, NS_GRAM_MN = 1, NS_POLY = 2, NS_UPD_BY = 3, NS_UPD_YB = 4 };
 
 struct NsSeg {
@@ -132,6 +134,7 @@ struct TileShape {
 TileShape fwd_tile(int kind, bool io_bf16);   // rows = hidden units, cols = tokens
 TileShape bwd_tile(int kind, bool io_bf16);   // OUT: features x tokens; GRAD13: hidden x
                                               // features; GRAD2: features x hidden
+TileShape ns_tile(bool fp16, bool big);       // tile-space rows x columns of the NS products
 
 // Launchers (io_bf16 selects bf16 MFMA operands, otherwise fp32).
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s);
@@ -141,7 +144,7 @@ hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d
                        hipStream_t s);
 // Newton-Schulz operand copies are fp16 (bf16 I/O: 4x finer rounding than bf16
 // at the same MFMA rate; the iterates are O(1)) or fp32 (fp32 I/O).
-hipError_t launch_ns(const NsArgs& a, bool fp16, hipStream_t s);
+hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s);
 hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s);
 hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s);
 constexpr int kNsBlockElems = 4096;

@@ -37,7 +37,7 @@ typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 constexpr int kRowBytes = 64;
-constexpr int kTileBytes = kTile * kRowBytes;   // a 128-row operand tile (fp32 path)
+constexpr int kTileBytes = 128 * kRowBytes;   // a 128-row operand tile (fp32 path)
 
 template <typename T> struct Tr;
 template <> struct Tr<__bf16> {   // 32 K per tile, 8 elements per 16 bytes
@@ -158,12 +158,38 @@ LACT_KIND(KUpdate32, 3, 2, 3, 1u << 2, 2, 2, 2, 2, 2, false, 32, p, (p == 2 ? 1 
 LACT_KIND(KOut32, 1, 1, 1, 0u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
 LACT_KIND(KGrad13_32, 2, 1, 2, 7u, 2, 2, 2, 2, 2, false, 32, p, 0 * p);
 LACT_KIND(KGrad2_32, 1, 1, 1, 3u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
-// Newton-Schulz products (4 waves, 128 x 128): both operands K-contiguous,
-// both row-contiguous, or only the second (B Y read down the columns of Y).
-LACT_KIND(KNsK, 1, 1, 1, 0u, 2, 2, 2, 2, 4, true, 32, 0 * p, 0 * p);
-LACT_KIND(KNsMN, 1, 1, 1, 3u, 2, 2, 2, 2, 4, true, 32, 0 * p, 0 * p);
-LACT_KIND(KNsBY, 1, 1, 1, 2u, 2, 2, 2, 2, 4, true, 32, 0 * p, 0 * p);
+// Newton-Schulz products, each computed in the orientation whose transpose is
+// stored (see k_ns): both operands K-contiguous (K), both row-contiguous (MN),
+// or the first row-contiguous (TY: Y read down its columns). fp16 operands:
+// 8 waves of 128 x 64 (256 x 256 tiles) for large Gram matrices, 4 waves of
+// 64 x 64 (128 x 128) for small ones; fp32: 4 waves of 64 x 64.
+LACT_KIND(KNsK16B, 1, 1, 1, 0u, 2, 4, 4, 2, 2, true, 64, 0 * p, 0 * p);
+LACT_KIND(KNsMN16B, 1, 1, 1, 3u, 2, 4, 4, 2, 2, true, 64, 0 * p, 0 * p);
+LACT_KIND(KNsTY16B, 1, 1, 1, 1u, 2, 4, 4, 2, 2, true, 64, 0 * p, 0 * p);
+LACT_KIND(KNsK16S, 1, 1, 1, 0u, 2, 2, 2, 2, 2, true, 64, 0 * p, 0 * p);
+LACT_KIND(KNsMN16S, 1, 1, 1, 3u, 2, 2, 2, 2, 2, true, 64, 0 * p, 0 * p);
+LACT_KIND(KNsTY16S, 1, 1, 1, 1u, 2, 2, 2, 2, 2, true, 64, 0 * p, 0 * p);
+LACT_KIND(KNsK32, 1, 1, 1, 0u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
+LACT_KIND(KNsMN32, 1, 1, 1, 3u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
+LACT_KIND(KNsTY32, 1, 1, 1, 1u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
 #undef LACT_KIND
+
+template <typename T, bool BIG> struct NsKinds;
+template <> struct NsKinds<_Float16, true> {
+  using K = KNsK16B;
+  using MN = KNsMN16B;
+  using TY = KNsTY16B;
+};
+template <> struct NsKinds<_Float16, false> {
+  using K = KNsK16S;
+  using MN = KNsMN16S;
+  using TY = KNsTY16S;
+};
+template <> struct NsKinds<float, false> {
+  using K = KNsK32;
+  using MN = KNsMN32;
+  using TY = KNsTY32;
+};
 
 template <typename T> struct Kinds;
 template <> struct Kinds<__bf16> {
@@ -1145,9 +1171,23 @@ __global__ __launch_bounds__(256) void k_prep(const float* w1, const float* w2, 
 // Newton-Schulz (Muon)
 
 // One Newton-Schulz product over every matrix of the chunk (see NsKind).
-template <typename T>
-__global__ __launch_bounds__(256) void k_ns(const NsArgs args) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(smem_bytes<T, KNsK>(), smem_bytes<T, KNsBY>())];
+// Newton-Schulz products. Every product is computed as the transpose of
+// what is stored: element (r, c) of the tile-space product goes to row c,
+// column r of the destination, so that the four consecutive accumulator rows
+// a lane holds become four consecutive elements of one stored row (one 16-byte
+// fp32 / 8-byte 16-bit access). The Gram and polynomial products are
+// symmetric, so their transposes are themselves; the update product runs with
+// swapped operands (tile rows = Y columns, tile columns = Y rows).
+template <typename T, bool BIG>
+__global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsArgs args) {
+  using KK = typename NsKinds<T, BIG>::K;
+  using KM = typename NsKinds<T, BIG>::MN;
+  using KT = typename NsKinds<T, BIG>::TY;
+  static_assert(KK::THREADS == KM::THREADS && KK::THREADS == KT::THREADS && KK::ROWS_A == KM::ROWS_A &&
+                    KK::ROWS_A == KT::ROWS_A && KK::ROWS_B == KT::ROWS_B && KK::MI == KT::MI && KK::NI == KM::NI,
+                "one tile and accumulator shape per launch");
+  __shared__ __attribute__((aligned(16)))
+  uint8_t smem[cmax(smem_bytes<T, KK>(), cmax(smem_bytes<T, KM>(), smem_bytes<T, KT>()))];
   constexpr int esz = sizeof(T);
   int bid = blockIdx.x;
   const bool first = bid < args.seg[0].nblocks;
@@ -1157,7 +1197,7 @@ __global__ __launch_bounds__(256) void k_ns(const NsArgs args) {
   const int per = sg.tiles_m * sg.tiles_n;
   const int q = bid / per;
   const int rr = bid - q * per;
-  const int64_t i0 = (int64_t)(rr / sg.tiles_n) * kTile, j0 = (int64_t)(rr % sg.tiles_n) * kTile;
+  const int64_t i0 = (int64_t)(rr / sg.tiles_n) * KK::ROWS_A, j0 = (int64_t)(rr % sg.tiles_n) * KK::ROWS_B;
   const int64_t slot = (int64_t)(q / sg.group) * 3 + sg.slot_off[q % sg.group];
   const int m = args.m, ldy = sg.ldy;
   const int64_t mrows = sg.M - i0, ncols = sg.N - j0;
@@ -1169,52 +1209,57 @@ __global__ __launch_bounds__(256) void k_ns(const NsArgs args) {
   void* Abw = reinterpret_cast<uint8_t*>(args.Ab) + slot * args.astride * esz;
   const uint8_t* Bb = reinterpret_cast<const uint8_t*>(args.Bb) + slot * args.astride * esz;
   void* Bbw = reinterpret_cast<uint8_t*>(args.Bb) + slot * args.astride * esz;
-  Acc<KNsK> acc;   // same accumulator shape for every NS kind
+  Acc<KK> acc;   // same accumulator shape for every NS kind
   const int kind = sg.kind;
-  if (kind == NS_GRAM_K) {          // A = Y Y^T
+  if (kind == NS_GRAM_K) {          // A = Y Y^T (Y wide)
     const View ops[2] = {View{Yin + i0 * ldy * esz, (int64_t)ldy * esz, mrows, sg.K},
                          View{Yin + j0 * ldy * esz, (int64_t)ldy * esz, ncols, sg.K}};
-    mainloop<T, KNsK>(smem, ops, sg.K, acc);
-  } else if (kind == NS_GRAM_MN) {  // A = Y^T Y
+    mainloop<T, KK>(smem, ops, sg.K, acc);
+  } else if (kind == NS_GRAM_MN) {  // A = Y^T Y (Y tall)
     const View ops[2] = {View{Yin + i0 * esz, (int64_t)ldy * esz, mrows, sg.K},
                          View{Yin + j0 * esz, (int64_t)ldy * esz, ncols, sg.K}};
-    mainloop<T, KNsMN>(smem, ops, sg.K, acc);
+    mainloop<T, KM>(smem, ops, sg.K, acc);
   } else if (kind == NS_POLY) {     // A A (A symmetric, so A A^T)
     const View ops[2] = {View{Ab + i0 * m * esz, (int64_t)m * esz, mrows, sg.K},
                          View{Ab + j0 * m * esz, (int64_t)m * esz, ncols, sg.K}};
-    mainloop<T, KNsK>(smem, ops, sg.K, acc);
-  } else if (kind == NS_UPD_BY) {   // B Y
-    const View ops[2] = {View{Bb + i0 * m * esz, (int64_t)m * esz, mrows, sg.K},
-                         View{Yin + j0 * esz, (int64_t)ldy * esz, ncols, sg.K}};
-    mainloop<T, KNsBY>(smem, ops, sg.K, acc);
-  } else {                          // Y B (B symmetric)
-    const View ops[2] = {View{Yin + i0 * ldy * esz, (int64_t)ldy * esz, mrows, sg.K},
+    mainloop<T, KK>(smem, ops, sg.K, acc);
+  } else if (kind == NS_UPD_BY) {   // (B Y)^T = Y^T B (Y wide, B symmetric): rows = Y columns
+    const View ops[2] = {View{Yin + i0 * esz, (int64_t)ldy * esz, mrows, sg.K},
                          View{Bb + j0 * m * esz, (int64_t)m * esz, ncols, sg.K}};
-    mainloop<T, KNsK>(smem, ops, sg.K, acc);
+    mainloop<T, KT>(smem, ops, sg.K, acc);
+  } else {                          // (Y B)^T = B Y^T (Y tall): rows = Y columns
+    const View ops[2] = {View{Bb + i0 * m * esz, (int64_t)m * esz, mrows, sg.K},
+                         View{Yin + j0 * ldy * esz, (int64_t)ldy * esz, ncols, sg.K}};
+    mainloop<T, KK>(smem, ops, sg.K, acc);
   }
+  const bool gram = kind == NS_GRAM_K || kind == NS_GRAM_MN;
+  const int64_t ld = (gram || kind == NS_POLY) ? m : ldy;
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int mi = 0; mi < KK::MI; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      const int j = acc_col<KNsK>(ni);
+    for (int ni = 0; ni < KK::NI; ++ni) {
+      const int c = acc_col<KK>(ni);
+      if (c >= ncols) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = acc_row<KNsK>(mi, r);
-        if (i < mrows && j < ncols) {
-          const float v = acc[0][mi][ni][r];
-          if (kind == NS_GRAM_K || kind == NS_GRAM_MN) {
-            const int64_t idx = (i0 + i) * m + j0 + j;
-            A32[idx] = v;
-            st_elem<T>(Abw, idx, v);
-          } else if (kind == NS_POLY) {
-            const int64_t idx = (i0 + i) * m + j0 + j;
-            st_elem<T>(Bbw, idx, args.cb * A32[idx] + args.cc * v);
-          } else {
-            const int64_t idx = (i0 + i) * ldy + j0 + j;
-            const float y = args.ca * Y32[idx] + v;
-            Y32[idx] = y;
-            st_elem<T>(Yout, idx, y);
-          }
+      for (int g = 0; g < 4; ++g) {
+        const int r = acc_row<KK>(mi, 4 * g);    // rows r .. r+3 of the tile
+        if (r >= mrows) continue;
+        const f32x16_t& a = acc[0][mi][ni];
+        const float v0 = a[4 * g], v1 = a[4 * g + 1], v2 = a[4 * g + 2], v3 = a[4 * g + 3];
+        const int64_t idx = (j0 + c) * ld + i0 + r;   // stored row j0+c, columns i0+r ..
+        if (gram) {
+          *reinterpret_cast<float4*>(A32 + idx) = make_float4(v0, v1, v2, v3);
+          st4<T>(Abw, idx, v0, v1, v2, v3);
+        } else if (kind == NS_POLY) {
+          const float4 o = *reinterpret_cast<const float4*>(A32 + idx);
+          st4<T>(Bbw, idx, args.cb * o.x + args.cc * v0, args.cb * o.y + args.cc * v1, args.cb * o.z + args.cc * v2,
+                 args.cb * o.w + args.cc * v3);
+        } else {
+          const float4 o = *reinterpret_cast<const float4*>(Y32 + idx);
+          const float4 y =
+              make_float4(args.ca * o.x + v0, args.ca * o.y + v1, args.ca * o.z + v2, args.ca * o.w + v3);
+          *reinterpret_cast<float4*>(Y32 + idx) = y;
+          st4<T>(Yout, idx, y.x, y.y, y.z, y.w);
         }
       }
     }
@@ -1296,10 +1341,17 @@ TileShape bwd_tile(int kind, bool io_bf16) {
   return TileShape{KGrad2_32::ROWS_A, KGrad2_32::ROWS_B, KGrad2_32::THREADS};
 }
 
-hipError_t launch_ns(const NsArgs& a, bool fp16, hipStream_t s) {
+TileShape ns_tile(bool fp16, bool big) {
+  if (fp16 && big) return TileShape{KNsK16B::ROWS_A, KNsK16B::ROWS_B, KNsK16B::THREADS};
+  if (fp16) return TileShape{KNsK16S::ROWS_A, KNsK16S::ROWS_B, KNsK16S::THREADS};
+  return TileShape{KNsK32::ROWS_A, KNsK32::ROWS_B, KNsK32::THREADS};
+}
+
+hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;
-  if (fp16) k_ns<_Float16><<<a.total_blocks, 256, 0, s>>>(a);
-  else k_ns<float><<<a.total_blocks, 256, 0, s>>>(a);
+  if (fp16 && big) k_ns<_Float16, true><<<a.total_blocks, KNsK16B::THREADS, 0, s>>>(a);
+  else if (fp16) k_ns<_Float16, false><<<a.total_blocks, KNsK16S::THREADS, 0, s>>>(a);
+  else k_ns<float, false><<<a.total_blocks, KNsK32::THREADS, 0, s>>>(a);
   return hipGetLastError();
 }
 

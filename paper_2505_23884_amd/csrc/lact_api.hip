@@ -69,16 +69,32 @@ Plan make_plan(const lact_desc* dsc) {
   p.cap = std::min<int64_t>(dsc->n_q, p.C + std::min<int64_t>(tail, std::max<int64_t>(p.C, 65536)));
   if (p.cap < 1) p.cap = 1;
   // Split-K of the gradient contraction (fp32 partials, summed by the weight
-  // update) only when the gradient tiles alone would leave most of the chip
-  // idle: each split adds a full read and write of d*h*3 fp32 per instance,
-  // which costs more than the parallelism gains once the tiles (with the
-  // apply GEMM-2 tiles sharing the launch) cover half of the 256 CUs.
-  // Splits are at least 256 tokens, lengths a multiple of 32.
+  // update). Each split adds a full write and read of 3*d*h fp32 per instance,
+  // worth about 500 tokens of the gradient's own work, so short chunks (the
+  // LM workload's 2048) split only when the gradient tiles alone would leave
+  // most of the chip idle (measured: 2 splits cost 8% there). Long chunks
+  // (NVS: one chunk of up to 1M tokens) take the split count, with splits of
+  // at least 1024 tokens, that minimises the makespan of equal blocks over the
+  // 256 CUs: rounds(tiles * ns) / ns. Lengths are a multiple of 32.
   const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
   const int64_t tiles = (int64_t)p.BH * (cdiv(p.h, g13.rows) * cdiv(p.d, g13.cols) +
                                          cdiv(p.d, g2.rows) * cdiv(p.h, g2.cols));
-  int64_t ns = std::max<int64_t>(1, cdiv(128, tiles));
-  ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.C / 256));
+  int64_t ns;
+  if (p.C >= 8192) {
+    const int64_t top = std::min<int64_t>(kMaxSplit, std::max<int64_t>(1, p.C / 1024));
+    ns = 1;
+    double best = 1e30;
+    for (int64_t t = 1; t <= top; ++t) {
+      const double cost = (double)cdiv(tiles * t, 256) / (double)t + 0.002 * (double)t;
+      if (cost < best - 1e-12) {
+        best = cost;
+        ns = t;
+      }
+    }
+  } else {
+    ns = std::max<int64_t>(1, cdiv(128, tiles));
+    ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.C / 256));
+  }
   ns = std::min<int64_t>(ns, kMaxSplit);
   p.split_len = std::max<int64_t>(32, cdiv(cdiv(std::max<int64_t>(p.C, 1), ns), 32) * 32);
   p.nsplit = (int)std::max<int64_t>(1, cdiv(std::max<int64_t>(p.C, 1), p.split_len));

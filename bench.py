@@ -150,26 +150,37 @@ def describe(cfg):
 def cpu_baseline(cfg, min_seconds):
     """The fp64 oracle, as it is, on a bounded sample of the same workload:
     whole (b, h) instances (every chunk), one after another, until at least
-    `min_seconds` of host time have passed; timed on this host's cores."""
+    `min_seconds` of host time have passed; timed on this host's cores. When
+    one instance is too large for that budget (NVS: 1M tokens in one chunk is
+    ~22 TFLOP), the sample is the first tokens of one instance with the same
+    d, h, order and options, chunked at the same size up to the sample length."""
     from threadpoolctl import threadpool_info
     from lact_synth import make_inputs
     from oracle import lact_oracle as O
 
+    one = O.layer_flops(1, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.n_chunks, bool(cfg.use_muon), cfg.ns_steps)
+    scfg, note = cfg, ""
+    if one > 4e12:   # roughly 30 s or more of fp64 NumPy for one instance
+        n = 16384
+        scfg = cfg.with_(name=cfg.name + "_sample", B=1, H=1, n_kv=min(cfg.n_kv, n),
+                         n_q=min(cfg.n_q, n) + min(cfg.n_q - cfg.n_kv, 4096), chunk=min(cfg.chunk, n))
+        note = (f"; token sample of one instance: n_kv={scfg.n_kv}, n_q={scfg.n_q}, chunk={scfg.chunk} "
+                f"(same d, h, order, options)")
     done, dt = 0, 0.0
-    while done < cfg.BH and dt < min_seconds:
-        x = make_inputs(cfg, 0, heads=[done])
+    while done < scfg.BH and dt < min_seconds:
+        x = make_inputs(scfg, 0, heads=[done])
         t0 = time.perf_counter()
-        O.lact_forward(x["q"], x["k"], x["v"], x["eta"], x["W1"], x["W2"], x["W3"], chunk=cfg.chunk,
-                       order=cfg.order, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps)
+        O.lact_forward(x["q"], x["k"], x["v"], x["eta"], x["W1"], x["W2"], x["W3"], chunk=scfg.chunk,
+                       order=scfg.order, use_muon=bool(scfg.use_muon), ns_steps=scfg.ns_steps)
         dt += time.perf_counter() - t0
         done += 1
-    fl = done * O.layer_flops(1, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.n_chunks, bool(cfg.use_muon),
-                              cfg.ns_steps)
+    fl = done * O.layer_flops(1, scfg.d, scfg.h, scfg.n_kv, scfg.n_q, scfg.n_chunks, bool(scfg.use_muon),
+                              scfg.ns_steps)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of {cfg.BH} (b,h) instances, all {cfg.n_chunks} chunks each "
-                      f"({done * cfg.n_q} tokens), fp64 NumPy, {dt:.1f} s",
-            "tokens_per_s": round(done * cfg.n_q / dt, 1)}
+            "sample": f"{done} of {scfg.BH} (b,h) instances, all {scfg.n_chunks} chunks each "
+                      f"({done * scfg.n_q} tokens), fp64 NumPy, {dt:.1f} s{note}",
+            "tokens_per_s": round(done * scfg.n_q / dt, 1)}
 
 
 def main():

@@ -583,8 +583,34 @@ __device__ __forceinline__ void mfma_frags(const Frags<K>& f, Acc<K>& acc) {
 //   wait DMA of kt+1 | barrier | DMA kt+NS into the freed stage |
 //   read substep 0 of kt+1 | MFMA substep S-1 of kt
 // without DBUF every substep reads, waits and multiplies in turn.
-template <typename T, class K>
-__device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk, Acc<K>& acc) {
+// Hand-over of a free stage from one loop to the next one on the same LDS:
+// in its last iteration a loop issues the first tile of the next loop into
+// the stage it has just finished with, so the next loop starts with its first
+// tile in flight instead of a cold prologue.
+struct NoNext {
+  __device__ __forceinline__ void first(int) {}
+};
+template <class K2, int SLOT>
+struct ChainNext {
+  uint8_t* smem;
+  const View (&ops)[K2::NOPS];
+  int slot;   // stage the first tile went to, -1 if none
+  __device__ __forceinline__ ChainNext(uint8_t* s, const View (&o)[K2::NOPS]) : smem(s), ops(o), slot(-1) {}
+  __device__ __forceinline__ void first(int s) {
+    uint32_t vo[K2::NOPS][4];
+    DmaAll<K2>::offsets(vo, ops);
+    DmaAll<K2>::issue(smem + s * SLOT, ops, vo, 0);
+    slot = s;
+  }
+};
+
+// Stage t of this loop lives at smem + ((t + shift) % NSTAGE) * SLOT; with
+// first_issued, tile 0 is already in flight there (issued by the previous
+// loop's hand-over).
+template <typename T, class K, int SLOT = K::STAGE, class Next = NoNext>
+__device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk, Acc<K>& acc,
+                                             int shift = 0, bool first_issued = false, Next* next = nullptr) {
+  static_assert(SLOT >= K::STAGE, "stage slot");
   constexpr int BK = K::BK, NS = K::NSTAGE, S = BK / 16;
   constexpr int L = [] {          // DMA instructions per lane per k-tile
     int n = 0;
@@ -599,19 +625,20 @@ __device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K:
   if (nkt <= 0) return;
   uint32_t vo[K::NOPS][4];
   DmaAll<K>::offsets(vo, ops);
-  auto issue = [&](int kt) { DmaAll<K>::issue(smem + (kt % NS) * K::STAGE, ops, vo, kt); };
+  auto stage = [&](int kt) { return smem + ((kt + shift) % NS) * SLOT; };
+  auto issue = [&](int kt) { DmaAll<K>::issue(stage(kt), ops, vo, kt); };
 #pragma unroll
   for (int t = 0; t < NS; ++t)
-    if (t < nkt) issue(t);
+    if (t < nkt && !(t == 0 && first_issued)) issue(t);
   if (nkt >= NS) wait_vmcnt<L * (NS - 1)>();
   else wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   if constexpr (K::DBUF) {
     Frags<K> f[2];
-    load_frags<K>(f[0], smem, 0);
+    load_frags<K>(f[0], stage(0), 0);
     for (int kt = 0; kt < nkt; ++kt) {
-      const uint8_t* cur = smem + (kt % NS) * K::STAGE;
+      const uint8_t* cur = stage(kt);
 #pragma unroll
       for (int s = 0; s + 1 < S; ++s) {
         load_frags<K>(f[(s + 1) & 1], cur, s + 1);
@@ -627,14 +654,15 @@ __device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K:
       __builtin_amdgcn_s_barrier();            // every wave is past tile kt and has tile kt+1
       asm volatile("" ::: "memory");
       if (kt + NS < nkt) issue(kt + NS);       // refill the stage tile kt used
-      if (kt + 1 < nkt) load_frags<K>(f[0], smem + ((kt + 1) % NS) * K::STAGE, 0);
+      else if (kt + NS == nkt && next) next->first((kt + shift) % NS);
+      if (kt + 1 < nkt) load_frags<K>(f[0], stage(kt + 1), 0);
       mfma_frags<T, K>(f[(S - 1) & 1], acc);
       __builtin_amdgcn_sched_barrier(0);
     }
   } else {
     Frags<K> f;
     for (int kt = 0; kt < nkt; ++kt) {
-      const uint8_t* cur = smem + (kt % NS) * K::STAGE;
+      const uint8_t* cur = stage(kt);
 #pragma unroll
       for (int s = 0; s < S; ++s) {
         load_frags<K>(f, cur, s);
@@ -649,14 +677,18 @@ __device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K:
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
       if (kt + NS < nkt) issue(kt + NS);
+      else if (kt + NS == nkt && next) next->first((kt + shift) % NS);
     }
   }
-  __syncthreads();     // the caller may reuse LDS after the loop
+  // The caller may reuse LDS after the loop: every wave has waited for its
+  // own LDS reads, and this loop's DMA has landed (the tail waits drain it).
+  // A DMA handed over to the next loop keeps running: no vmcnt wait here.
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
-// acc = sum over K of A[pa(p)] B[pb(p)]^T for this workgroup's tile.
-template <typename T, class K>
-__device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk, Acc<K>& acc) {
+template <class K>
+__device__ __forceinline__ void zero_acc(Acc<K>& acc) {
 #pragma unroll
   for (int p = 0; p < K::NACC; ++p)
 #pragma unroll
@@ -665,8 +697,27 @@ __device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOP
       for (int ni = 0; ni < K::NI; ++ni)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[p][mi][ni][r] = 0.f;
+}
+
+// acc = sum over K of A[pa(p)] B[pb(p)]^T for this workgroup's tile.
+template <typename T, class K>
+__device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOPS], int64_t nk, Acc<K>& acc) {
+  zero_acc<K>(acc);
   if constexpr (sizeof(T) == 2) mainloop_dma<T, K>(smem, ops, nk, acc);
   else mainloop_regs<K>(smem, ops, nk, acc);
+}
+
+// Two loops on one LDS ring of 2-stage slots of SLOT bytes: the first hands
+// its last free stage to the second (16-bit path).
+template <typename T, class K1, class K2, int SLOT>
+__device__ __forceinline__ void mainloop_chain(uint8_t* smem, const View (&ops1)[K1::NOPS], int64_t nk1, Acc<K1>& acc1,
+                                               const View (&ops2)[K2::NOPS], int64_t nk2, Acc<K2>& acc2) {
+  static_assert(sizeof(T) == 2 && K1::NSTAGE == 2 && K2::NSTAGE == 2, "chained loops: 16-bit, two stages");
+  zero_acc<K1>(acc1);
+  zero_acc<K2>(acc2);
+  ChainNext<K2, SLOT> nx(smem, ops2);
+  mainloop_dma<T, K1, SLOT, ChainNext<K2, SLOT>>(smem, ops1, nk1, acc1, 0, false, &nx);
+  mainloop_dma<T, K2, SLOT>(smem, ops2, nk2, acc2, nx.slot < 0 ? 0 : nx.slot, nx.slot >= 0);
 }
 
 template <typename T, class K>
@@ -934,9 +985,10 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
       Acc<KU> az;
       Acc<KD> ad;
       const View opz[3] = {w1, w3, kk};
-      mainloop<T, KU>(smem, opz, d, az);
       const View opd[2] = {w2, vv};
-      mainloop<T, KD>(smem, opd, d, ad);
+      constexpr int kSlot = KU::STAGE > KD::STAGE ? KU::STAGE : KD::STAGE;
+      static_assert(2 * kSlot <= smem_bytes<T, KU>(), "chained ring fits");
+      mainloop_chain<T, KU, KD, kSlot>(smem, opz, d, az, opd, d, ad);
       static_assert(2 * KU::ROWS_A * KU::ROWS_B * 2 <= sizeof(smem), "staging fits");
       update_epilogue_staged<KU>(az[0], az[1], ad[0], sg, inst, j0, i0, hrows, ntok, h, smem);
     } else {

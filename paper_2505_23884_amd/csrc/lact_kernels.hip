@@ -760,6 +760,14 @@ __device__ __forceinline__ View view_mn(const Operand& op, int inst, int64_t row
   return View{reinterpret_cast<const uint8_t*>(op.base) + off * esz, op.ld * esz, nrows, nk};
 }
 
+// Workgroup barrier for LDS hand-offs only: waits for this wave's LDS
+// operations, not for its global stores (which __syncthreads would drain).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Output staging (16-bit): an accumulator tile of R output rows (hidden units
 // or features, the MFMA row index) x C tokens is written to LDS token-major,
 // R*2 bytes per token row, and then copied to the token-major output with
@@ -871,11 +879,11 @@ __device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::
         stage_put<R>(buf0, tok, row, vh[0], vh[1], vh[2], vh[3]);
         stage_put<R>(buf1, tok, row, vg[0], vg[1], vg[2], vg[3]);
       }
-  __syncthreads();
+  lds_barrier();
   const int64_t tile = inst * sg.out_inst + i0 * h + j0;
   stage_flush<R, C, K::THREADS>(buf0, reinterpret_cast<__bf16*>(sg.out1) + tile, h, ntok, hrows);
   stage_flush<R, C, K::THREADS>(buf1, reinterpret_cast<__bf16*>(sg.out2) + tile, h, ntok, hrows);
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int ni = 0; ni < K::NI; ++ni)
 #pragma unroll
@@ -891,7 +899,7 @@ __device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::
         }
         stage_put<R>(buf0, acc_col<K>(ni), hrow0 + mi * 32 + 8 * g, vb[0], vb[1], vb[2], vb[3]);
       }
-  __syncthreads();
+  lds_barrier();
   stage_flush<R, C, K::THREADS>(buf0, reinterpret_cast<__bf16*>(sg.out3) + tile, h, ntok, hrows);
 }
 
@@ -945,7 +953,7 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
             }
             stage_put<KA::ROWS_A>(smem, acc_col<KA>(ni), hrow0 + mi * 32 + 8 * g, v[0], v[1], v[2], v[3]);
           }
-      __syncthreads();
+      lds_barrier();
       stage_flush<KA::ROWS_A, KA::ROWS_B, KA::THREADS>(smem, reinterpret_cast<__bf16*>(out) + i0 * h + j0, h, ntok,
                                                          hrows);
       return;
@@ -1054,7 +1062,7 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
             stage_put<KO::ROWS_A>(smem, acc_col<KO>(ni), mrow0 + mi * 32 + 8 * g, a[4 * g], a[4 * g + 1],
                                   a[4 * g + 2], a[4 * g + 3]);
           }
-      __syncthreads();
+      lds_barrier();
       stage_flush<KO::ROWS_A, KO::ROWS_B, KO::THREADS>(smem, reinterpret_cast<__bf16*>(sg.out) + ob + t0 * d + m0, d,
                                                          ntok, mrows);
       return;

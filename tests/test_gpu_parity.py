@@ -104,6 +104,17 @@ def test_bf16_dims_of_32_mod_64(order):
     check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
 
 
+@pytest.mark.parametrize("d,h", [(64, 96), (32, 32)])
+def test_bf16_single_k_tile_and_smallest_dims(d, h):
+    # d <= 64: the key forward's first loop is a single 64-K tile, so it hands
+    # no free stage to its second loop (cold start path); d = h = 32 is the
+    # smallest bf16 shape, a half-empty K tile in every contraction
+    cfg = CONFIGS["video"].with_(name="k1tile", B=2, H=1, d=d, h=h, n_kv=300, n_q=333, chunk=128,
+                                 use_muon=0, order=1)
+    x = make_inputs(cfg, 11)
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
 @pytest.mark.parametrize("order", [0, 1])
 def test_fp32_ragged_small_dims(order):
     cfg = CONFIGS["tiny_fp32"].with_(name="fp32small", B=2, H=1, d=40, h=24, n_kv=300, n_q=333,
@@ -258,6 +269,15 @@ def test_muon_small_teacher_forced_and_two_chunks(order):
     two = cfg.with_(n_kv=512, n_q=512)
     x2 = {kk: (vv[:, :512] if kk in ("q", "k", "v", "eta") else vv) for kk, vv in x.items()}
     check(two, x2, run_gpu(two, x2), run_oracle(two, x2))
+
+
+def test_muon_large_gram_ragged_tiles():
+    # Gram size 256 > 128 takes the 256 x 256 Newton-Schulz tiles; h = 384 gives
+    # a ragged second tile; W1, W3 (384 x 256) iterate tall, W2 (256 x 384) wide
+    cfg = CONFIGS["lm32k_muon"].with_(name="muon_big", B=1, H=1, d=256, h=384, n_kv=512, n_q=512,
+                                      chunk=256)
+    x = make_inputs(cfg, 12)
+    teacher_forced(cfg, x, [0])
 
 
 def test_muon_fp32_teacher_forced():

@@ -276,6 +276,30 @@ int newton_schulz(Ctx& c) {
   const int m = p.m, d = p.d, h = p.h;
   // segment 0: W1 and W3 stored h x d; segment 1: W2 stored d x h
   const int rows[2] = {h, d}, cols[2] = {d, h};
+  if (p.ns_fp16 && m <= kNsFusedM && std::max(d, h) <= kNsFusedN) {
+    // small matrices: every step of one matrix in one workgroup
+    const int n = std::max(d, h);
+    for (int g = 0; g < 2; ++g) {
+      NsFusedArgs f{};
+      f.Y32 = pa.Y32;
+      f.Yb = c.ws + p.off_yb[0];
+      f.ystride = dh;
+      f.group = g == 0 ? 2 : 1;
+      f.slot_off[0] = g == 0 ? 0 : 1;
+      f.slot_off[1] = 2;
+      f.rows = rows[g];
+      f.cols = cols[g];
+      f.nblocks = p.BH * f.group;
+      f.steps = c.dsc->ns_steps;
+      f.ca = 3.4445f;
+      f.cb = -4.7750f;
+      f.cc = 2.0315f;
+      const double fl = (double)f.steps * f.nblocks * (4.0 * m * m * n + 2.0 * m * m * m);
+      rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns_fused(f, c.s); });
+      if (rc) return rc;
+    }
+    return LACT_OK;
+  }
   const int64_t mm = (int64_t)m * m;
   // 256 x 256 tiles for Gram matrices larger than 128, else 128 x 128
   const bool big = p.ns_fp16 && m > 128;

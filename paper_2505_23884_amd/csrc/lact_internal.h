@@ -127,6 +127,21 @@ struct NsPrepArgs {
   int blocks_per_slot;  // blocks of 4096 elements per slot
 };
 
+// Whole Newton-Schulz iteration of small matrices, one workgroup per matrix:
+// Gram size m <= 128 and long side n <= 256 (fp16 operands).
+constexpr int kNsFusedM = 128, kNsFusedN = 256;
+struct NsFusedArgs {
+  float* Y32;           // fp32 iterate, slot stride ystride: in = scaled gradient, out = NS result
+  const void* Yb;       // fp16 copy of the scaled gradient, same layout
+  int64_t ystride;
+  int group;            // matrices per instance in this launch (1 or 2)
+  int slot_off[2];      // j of each matrix of the group
+  int rows, cols;       // stored orientation Y [rows x cols]
+  int nblocks;          // instances * group
+  int steps;
+  float ca, cb, cc;     // quintic coefficients
+};
+
 // Workgroup tile of a contraction kind: output rows x output columns, threads.
 struct TileShape {
   int rows, cols, threads;
@@ -147,6 +162,7 @@ hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d
 hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s);
 hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s);
 hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s);
+hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s);
 constexpr int kNsBlockElems = 4096;
 
 }  // namespace lact

@@ -1325,6 +1325,233 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
     }
 }
 
+// ---------------------------------------------------------------------------
+// Whole Newton-Schulz iteration of one small matrix per workgroup (Gram size
+// m <= 128, long side n <= 256): the fp16 iterate X, Gram A and polynomial B
+// stay in LDS (64 + 32 + 32 KiB), the fp32 iterate in registers. Per step:
+//   A = X X^T   (kept in fp32 registers, fp16 copy to LDS)
+//   B = b A + c A A
+//   X <- a X + B X
+// X is held in its stored orientation Y [SR x SC] (wide: Y = X, tall: Y =
+// X^T), zero-padded to 128 x 256 (or 256 x 128). Every product is computed in
+// the orientation whose lanes own four consecutive elements of a stored row:
+// A and B are symmetric, and the last product's tile rows are Y's columns.
+// LDS rows are XOR-swizzled by fsw(row) on their 16-byte chunks, which keeps
+// both the K-contiguous fragment reads (16 consecutive rows, one chunk) and
+// the transposed reads (4 consecutive rows, two adjacent chunks) conflict-free.
+__device__ __forceinline__ int fsw(int row) { return ((row & 7) << 1) | ((row >> 3) & 1); }
+__device__ __forceinline__ uint32_t fs_off(int row, int chunk, int pitch) {
+  return (uint32_t)(row * pitch + ((chunk ^ fsw(row)) << 4));
+}
+// K-contiguous fragment: row `row`, 8 K from chunk `chunk`.
+__device__ __forceinline__ u32x4_t fs_frag_k(uint32_t base, int row, int chunk, int pitch) {
+  return lds_read_b128(base + fs_off(row, chunk, pitch));
+}
+// Transposed fragment (8 consecutive K of column rb + lane%32 of a tile whose
+// K runs down the rows, substep s).
+__device__ __forceinline__ u32x4_t fs_frag_tr(uint32_t base, int rb, int s, int pitch) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, sl = lane & 15;
+  const int mn = rb + 16 * (g & 1) + 4 * (sl & 3);
+  const int c = mn >> 3, hb = (mn >> 2) & 1;
+  u32x2_t lo, hi;
+  {
+    const int kr = 16 * s + 8 * (g >> 1) + (sl >> 2);
+    const uint32_t a = base + kr * pitch + ((c ^ fsw(kr)) << 4) + (hb << 3);
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a));
+  }
+  {
+    const int kr = 16 * s + 8 * (g >> 1) + 4 + (sl >> 2);
+    const uint32_t a = base + kr * pitch + ((c ^ fsw(kr)) << 4) + (hb << 3);
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(a));
+  }
+  return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+}
+// Wait for every LDS read of this wave and make the fragments depend on the
+// wait, so that no MFMA reading them can be scheduled above it.
+template <int NA, int NB>
+__device__ __forceinline__ void lds_ready(u32x4_t (&fa)[NA], u32x4_t (&fb)[NB]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < NA; ++i) asm volatile("" : "+v"(fa[i]));
+#pragma unroll
+  for (int i = 0; i < NB; ++i) asm volatile("" : "+v"(fb[i]));
+}
+__device__ __forceinline__ f32x16_t mfma16(u32x4_t a, u32x4_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c, 0,
+                                                0, 0);
+}
+// four fp16 values at (row, cols col .. col+3) of a swizzled LDS matrix
+__device__ __forceinline__ void fs_put4(uint8_t* base, int row, int col, int pitch, float a, float b, float c, float d) {
+  typedef __attribute__((ext_vector_type(4))) _Float16 h4;
+  *reinterpret_cast<h4*>(base + fs_off(row, col >> 3, pitch) + (((col >> 2) & 1) << 3)) =
+      h4{(_Float16)a, (_Float16)b, (_Float16)c, (_Float16)d};
+}
+
+template <bool TALL>
+__global__ __launch_bounds__(512) void k_ns_fused(const NsFusedArgs a) {
+  constexpr int M = kNsFusedM, N = kNsFusedN;
+  constexpr int SR = TALL ? N : M, SC = TALL ? M : N;   // padded stored orientation
+  constexpr int PX = SC * 2, PA = M * 2;                // LDS pitches (bytes)
+  __shared__ __attribute__((aligned(16))) uint8_t xs[SR * PX];
+  __shared__ __attribute__((aligned(16))) uint8_t as_[M * PA];
+  __shared__ __attribute__((aligned(16))) uint8_t bs[M * PA];
+  const uint32_t xb = lds_addr(xs), ab = lds_addr(as_), bb = lds_addr(bs);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, half = lane >> 5;
+  const int q = blockIdx.x;
+  const int64_t slot = (int64_t)(q / a.group) * 3 + a.slot_off[q % a.group];
+  float* Y32 = a.Y32 + slot * a.ystride;
+  const _Float16* Yb = reinterpret_cast<const _Float16*>(a.Yb) + slot * a.ystride;
+  const int sr = a.rows, sc = a.cols;                   // valid stored rows, columns
+
+  // X (fp16) into LDS, zero padded
+  for (int i = tid; i < SR * PX / 16; i += 512) *reinterpret_cast<u32x4_t*>(xs + i * 16) = u32x4_t{0u, 0u, 0u, 0u};
+  __syncthreads();
+  for (int i = tid; i < sr * (sc / 8); i += 512) {
+    const int row = i / (sc / 8), ch = i % (sc / 8);
+    *reinterpret_cast<u32x4_t*>(xs + fs_off(row, ch, PX)) =
+        *reinterpret_cast<const u32x4_t*>(Yb + (int64_t)row * sc + ch * 8);
+  }
+  // X (fp32) into registers, in the tile layout of the update product: tile
+  // rows = stored columns (TR rows), tile columns = stored rows (TC)
+  constexpr int WM3 = TALL ? 2 : 4, WN3 = TALL ? 4 : 2;   // waves: 64 x 64 each
+  const int r3 = (w / WN3) * 64, c3 = (w % WN3) * 64;
+  f32x16_t x32[2][2];
+#pragma unroll
+  for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      const int c = c3 + ni * 32 + (lane & 31);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int r = r3 + mi * 32 + 8 * g + 4 * half;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (c < sr && r < sc) v = *reinterpret_cast<const float4*>(Y32 + (int64_t)c * sc + r);
+        x32[mi][ni][4 * g] = v.x;
+        x32[mi][ni][4 * g + 1] = v.y;
+        x32[mi][ni][4 * g + 2] = v.z;
+        x32[mi][ni][4 * g + 3] = v.w;
+      }
+    }
+  __syncthreads();
+
+  // Gram tile layout: waves 2 x 4 of 64 x 32
+  const int r1 = (w >> 2) * 64, c1 = (w & 3) * 32;
+  for (int step = 0; step < a.steps; ++step) {
+    // ---- A = X X^T (K = N) ----
+    f32x16_t a32[2];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) a32[mi][e] = 0.f;
+    for (int s = 0; s < N / 16; ++s) {
+      u32x4_t fa[2], fb[1];
+      if constexpr (!TALL) {
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi) fa[mi] = fs_frag_k(xb, r1 + mi * 32 + (lane & 31), 2 * s + half, PX);
+        fb[0] = fs_frag_k(xb, c1 + (lane & 31), 2 * s + half, PX);
+      } else {
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi) fa[mi] = fs_frag_tr(xb, r1 + mi * 32, s, PX);
+        fb[0] = fs_frag_tr(xb, c1, s, PX);
+      }
+      lds_ready(fa, fb);
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi) a32[mi] = mfma16(fa[mi], fb[0], a32[mi]);
+    }
+    // A is symmetric: lane's rows i..i+3 at column j go to row j, columns i..i+3
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        fs_put4(as_, c1 + (lane & 31), r1 + mi * 32 + 8 * g + 4 * half, PA, a32[mi][4 * g], a32[mi][4 * g + 1],
+                a32[mi][4 * g + 2], a32[mi][4 * g + 3]);
+    lds_barrier();
+    // ---- B = b A + c A A (K = M) ----
+    f32x16_t t[2];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) t[mi][e] = 0.f;
+    for (int s = 0; s < M / 16; ++s) {
+      u32x4_t fa[2], fb[1];
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi) fa[mi] = fs_frag_k(ab, r1 + mi * 32 + (lane & 31), 2 * s + half, PA);
+      fb[0] = fs_frag_k(ab, c1 + (lane & 31), 2 * s + half, PA);
+      lds_ready(fa, fb);
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi) t[mi] = mfma16(fa[mi], fb[0], t[mi]);
+    }
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = a.cb * a32[mi][4 * g + e] + a.cc * t[mi][4 * g + e];
+        fs_put4(bs, c1 + (lane & 31), r1 + mi * 32 + 8 * g + 4 * half, PA, v[0], v[1], v[2], v[3]);
+      }
+    lds_barrier();
+    // ---- X <- a X + B X (K = M), tile rows = stored columns ----
+    f32x16_t u[2][2];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) u[mi][ni][e] = 0.f;
+    for (int s = 0; s < M / 16; ++s) {
+      u32x4_t fa[2], fb[2];
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi) {
+        if constexpr (!TALL) fa[mi] = fs_frag_tr(xb, r3 + mi * 32, s, PX);   // X[k][j], k down the rows
+        else fa[mi] = fs_frag_k(bb, r3 + mi * 32 + (lane & 31), 2 * s + half, PA);   // B[i][k]
+      }
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni) {
+        if constexpr (!TALL) fb[ni] = fs_frag_k(bb, c3 + ni * 32 + (lane & 31), 2 * s + half, PA);   // B[i][k]
+        else fb[ni] = fs_frag_k(xb, c3 + ni * 32 + (lane & 31), 2 * s + half, PX);   // Y[j][k] = X[k][j]
+      }
+      lds_ready(fa, fb);
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) u[mi][ni] = mfma16(fa[mi], fb[ni], u[mi][ni]);
+    }
+    lds_barrier();   // every wave is done reading X before it is overwritten
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni) {
+        const int c = c3 + ni * 32 + (lane & 31);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int r = r3 + mi * 32 + 8 * g + 4 * half;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = a.ca * x32[mi][ni][4 * g + e] + u[mi][ni][4 * g + e];
+            x32[mi][ni][4 * g + e] = v[e];
+          }
+          fs_put4(xs, c, r, PX, v[0], v[1], v[2], v[3]);
+        }
+      }
+    lds_barrier();
+  }
+#pragma unroll
+  for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      const int c = c3 + ni * 32 + (lane & 31);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int r = r3 + mi * 32 + 8 * g + 4 * half;
+        if (c < sr && r < sc)
+          *reinterpret_cast<float4*>(Y32 + (int64_t)c * sc + r) =
+              make_float4(x32[mi][ni][4 * g], x32[mi][ni][4 * g + 1], x32[mi][ni][4 * g + 2], x32[mi][ni][4 * g + 3]);
+      }
+    }
+}
+
 __device__ __forceinline__ float block_sum(float v, float* red) {
   v = wave_sum(v);
   const int w = threadIdx.x >> 6;
@@ -1412,6 +1639,13 @@ hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s) {
   if (fp16 && big) k_ns<_Float16, true><<<a.total_blocks, KNsK16B::THREADS, 0, s>>>(a);
   else if (fp16) k_ns<_Float16, false><<<a.total_blocks, KNsK16S::THREADS, 0, s>>>(a);
   else k_ns<float, false><<<a.total_blocks, KNsK32::THREADS, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s) {
+  if (a.nblocks <= 0 || a.steps <= 0) return hipSuccess;
+  if (a.rows > a.cols) k_ns_fused<true><<<a.nblocks, 512, 0, s>>>(a);
+  else k_ns_fused<false><<<a.nblocks, 512, 0, s>>>(a);
   return hipGetLastError();
 }
 

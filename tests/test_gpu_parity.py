@@ -252,7 +252,9 @@ def teacher_forced(cfg, x, instances, max_chunks=None):
                 errs[name] = rel(w_out[j][i], w_ref[j])
                 errs["d" + name] = rel(w_out[j][i] - w_in[j][i], w_ref[j] - w_in[j][i])
             for kk, vv in errs.items():
-                worst[kk] = max(worst.get(kk, 0.0), vv)
+                # a NaN must survive the running maximum (max() would drop it)
+                if kk not in worst or not vv <= worst[kk]:
+                    worst[kk] = vv
     print("[gpu] worst per-chunk rel-L2", {k: f"{v:.2e}" for k, v in worst.items()}, flush=True)
     for kk, vv in worst.items():
         assert vv <= TOL[cfg.io], (kk, vv)

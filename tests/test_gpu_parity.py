@@ -253,8 +253,8 @@ def teacher_forced(cfg, x, instances, max_chunks=None):
                 errs["d" + name] = rel(w_out[j][i] - w_in[j][i], w_ref[j] - w_in[j][i])
             for kk, vv in errs.items():
                 # a NaN must survive the running maximum (max() would drop it)
-                if kk not in worst or not vv <= worst[kk]:
-                    worst[kk] = vv
+                prev = worst.get(kk, 0.0)
+                worst[kk] = prev if (np.isnan(prev) or vv <= prev) else vv
     print("[gpu] worst per-chunk rel-L2", {k: f"{v:.2e}" for k, v in worst.items()}, flush=True)
     for kk, vv in worst.items():
         assert vv <= TOL[cfg.io], (kk, vv)

@@ -15,6 +15,9 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
                    to the row norm W had before the update (Alg. 1, update)
 * Muon(g)          Newton-Schulz quintic iteration on g/||g||_F  (App. A, Details of Muon)
 * chunk schedule   apply-then-update / update-then-apply         (§3.1 orders; Alg. 1)
+* momentum         M <- M * mean_i(beta_i) + g, then the update with M in
+                   place of g: W - M, or W - Muon(M)                (App. A, implementing
+                   momentum for test-time optimizers; Table 3, Momentum and Muon rows)
 
 Math layout (one instance): W1, W3 in R^{h x d}, W2 in R^{d x h}; a "row" is
 the input dimension of the matrix (d for W1 and W3, h for W2). Tokens are rows
@@ -38,6 +41,10 @@ test):
   R7 a chunk's gradient is summed over token blocks of at most ``token_block``
      tokens; the gradient is a sum over tokens (the linearity that §3.4 uses
      to shard a chunk over devices), so this only bounds host memory.
+  R8 momentum: beta_i in (0, 1) is an input per token (its projection and
+     sigmoid are outside the fast-weight path, like eta); a chunk's factor is
+     the mean of its own tokens' beta_i; M starts at zero unless given, and
+     the returned M is the state after the last update.
 
 parity: pinned (see tests/test_oracle_pins.py for each pin).
 """
@@ -47,8 +54,8 @@ import numpy as np
 
 __all__ = [
     "NS_COEFFS", "NS_EPS", "sigmoid", "silu", "swiglu_apply", "chunk_gradient",
-    "newton_schulz", "weight_update", "update", "lact_forward_instance",
-    "lact_forward", "layer_flops",
+    "newton_schulz", "weight_update", "update", "momentum_update", "lact_forward_instance",
+    "lact_forward", "lact_forward_momentum", "layer_flops",
 ]
 
 # Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
@@ -160,19 +167,48 @@ def update(W, K, V, eta, use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAUL
     return weight_update(W1, g1), weight_update(W2, g2), weight_update(W3, g3)
 
 
+def momentum_update(W, M, K, V, eta, beta, use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT,
+                    token_block: int = 65536):
+    """Update with momentum on one chunk (App. A, implementing momentum; Table 3):
+
+    g = grad_W sum_i eta_i L_i;  M <- M * (sum_i beta_i / b) + g;
+    W <- weight-update(W, M), or weight-update(W, Muon(M)).
+    Returns (W, M) (reading R8).
+    """
+    W1, W2, W3 = W
+    g = chunk_gradient(W1, W2, W3, K, V, eta, token_block)
+    bbar = float(np.mean(np.asarray(beta, dtype=np.float64)))
+    M = tuple(bbar * np.asarray(m, dtype=np.float64) + gj for m, gj in zip(M, g))
+    steps = tuple(newton_schulz(m, ns_steps) for m in M) if use_muon else M
+    return tuple(weight_update(w, st) for w, st in zip(W, steps)), M
+
+
 def lact_forward_instance(q, k, v, eta, W1, W2, W3, chunk: int, order: int,
                           use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT,
-                          token_block: int = 65536, trace: list | None = None):
+                          token_block: int = 65536, trace: list | None = None,
+                          beta=None, M=None):
     """One (batch, head) instance of the layer's fast-weight path.
 
     q [n_q, d], k, v [n_kv, d], eta [n_kv]; W1, W3 [h, d], W2 [d, h].
     order 0 = apply-then-update (shifted block-causal), 1 = update-then-apply
     (§3.1, execution orders; Alg. 1). Returns (o [n_q, d], (W1, W2, W3)).
+    With ``beta`` [n_kv] the updates use momentum (``M`` = initial
+    (M1, M2, M3), zeros if omitted) and the return is (o, W, M).
     If ``trace`` is a list, the fast weights entering every chunk are appended.
     """
     W = tuple(np.asarray(w, dtype=np.float64).copy() for w in (W1, W2, W3))
+    mom = beta is not None
+    if mom:
+        M = tuple(np.zeros_like(w) for w in W) if M is None else tuple(
+            np.asarray(m, dtype=np.float64).copy() for m in M)
     n_q, n_kv = q.shape[0], k.shape[0]
     assert n_q >= n_kv and chunk > 0
+
+    def step(W, M, s, e):
+        if mom:
+            return momentum_update(W, M, k[s:e], v[s:e], eta[s:e], beta[s:e], use_muon, ns_steps, token_block)
+        return update(W, k[s:e], v[s:e], eta[s:e], use_muon, ns_steps, token_block), M
+
     o = np.zeros((n_q, q.shape[1]))
     for s in range(0, n_kv, chunk):
         e = min(n_kv, s + chunk)
@@ -180,13 +216,13 @@ def lact_forward_instance(q, k, v, eta, W1, W2, W3, chunk: int, order: int,
             trace.append(W)
         if order == 0:
             o[s:e] = swiglu_apply(*W, q[s:e])
-            W = update(W, k[s:e], v[s:e], eta[s:e], use_muon, ns_steps, token_block)
+            W, M = step(W, M, s, e)
         else:
-            W = update(W, k[s:e], v[s:e], eta[s:e], use_muon, ns_steps, token_block)
+            W, M = step(W, M, s, e)
             o[s:e] = swiglu_apply(*W, q[s:e])
     if n_q > n_kv:                       # reading R6: apply-only tail
         o[n_kv:] = swiglu_apply(*W, q[n_kv:])
-    return o, W
+    return (o, W, M) if mom else (o, W)
 
 
 def lact_forward(q, k, v, eta, W1, W2, W3, chunk: int, order: int, use_muon: bool = False,
@@ -203,6 +239,22 @@ def lact_forward(q, k, v, eta, W1, W2, W3, chunk: int, order: int, use_muon: boo
                                              chunk, order, use_muon, ns_steps, token_block)
         outs.append(o); w1s.append(a); w2s.append(b); w3s.append(c)
     return np.stack(outs), np.stack(w1s), np.stack(w2s), np.stack(w3s)
+
+
+def lact_forward_momentum(q, k, v, eta, beta, W1, W2, W3, M1=None, M2=None, M3=None, *, chunk: int,
+                          order: int, use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT, instances=None,
+                          token_block: int = 65536):
+    """Batched driver with momentum: returns (o, W1, W2, W3, M1, M2, M3) stacked
+    over the selected instances; M1..M3 default to zeros."""
+    idx = range(q.shape[0]) if instances is None else instances
+    res = [[] for _ in range(7)]
+    for i in idx:
+        M = None if M1 is None else (M1[i], M2[i], M3[i])
+        o, W, Mo = lact_forward_instance(q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], chunk, order, use_muon,
+                                         ns_steps, token_block, beta=beta[i], M=M)
+        for j, x in enumerate((o, *W, *Mo)):
+            res[j].append(x)
+    return tuple(np.stack(r) for r in res)
 
 
 def layer_flops(BH: int, d: int, h: int, n_kv: int, n_q: int, n_chunks: int,

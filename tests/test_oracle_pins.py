@@ -381,3 +381,143 @@ def test_layer_flops_match_paper_counts():
         m = 32
         mu = O.layer_flops(1, m, r * m, 0, 0, 1, use_muon=True, ns_steps=1)
         assert mu == 3 * vals[f"muon_r{r}_per_iter_over_m3"] * m ** 3
+
+
+# ----------------------------------------------------------------------------- momentum
+# App. A (implementing momentum for test-time optimizers) and Table 3:
+#   M <- M * mean_chunk(beta) + g,  W <- L2norm(W - M)  or  L2norm(W - Muon(M)).
+
+
+def _beta(seed, n, lo=0.05, hi=0.95):
+    return _rng(seed).uniform(lo, hi, n)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+@pytest.mark.parametrize("muon", [0, 1])
+def test_momentum_beta_zero_is_gradient_descent(order, muon):
+    """beta = 0 keeps no memory: M is the chunk's own gradient and the layer is
+    the plain update (a sign error or a beta on the wrong term fails here)."""
+    q, k, v, eta, W = _layer_inputs(30, 27, 24, 5, 7, eta_scale=0.4)
+    o, Wf = O.lact_forward_instance(q, k, v, eta, *W, chunk=8, order=order, use_muon=bool(muon))
+    trace = []
+    om, Wm, M = O.lact_forward_instance(q, k, v, eta, *W, chunk=8, order=order, use_muon=bool(muon),
+                                        beta=np.zeros(24), trace=trace)
+    np.testing.assert_array_equal(om, o)
+    for a, b in zip(Wm, Wf):
+        np.testing.assert_array_equal(a, b)
+    g = O.chunk_gradient(*trace[-1], k[16:], v[16:], eta[16:])
+    for a, b in zip(M, g):
+        np.testing.assert_allclose(a, b, rtol=1e-14, atol=1e-16)
+
+
+def test_momentum_single_chunk_is_gradient_descent():
+    q, k, v, eta, W = _layer_inputs(31, 12, 12, 4, 6, eta_scale=0.4)
+    o, Wf = O.lact_forward_instance(q, k, v, eta, *W, chunk=12, order=1)
+    om, Wm, _ = O.lact_forward_instance(q, k, v, eta, *W, chunk=12, order=1, beta=_beta(0, 12))
+    np.testing.assert_allclose(om, o, rtol=1e-14)
+    for a, b in zip(Wm, Wf):
+        np.testing.assert_allclose(a, b, rtol=1e-14)
+
+
+def test_momentum_factor_is_the_current_chunks_mean():
+    """The factor of chunk c is the mean of chunk c's own beta: zero beta in the
+    second chunk gives two plain updates whatever the first chunk's beta; any
+    beta with the same per-chunk means (or permuted in a chunk) gives the same
+    layer."""
+    C = 8
+    q, k, v, eta, W = _layer_inputs(32, 16, 16, 5, 6, eta_scale=0.4)
+    beta = np.concatenate([_beta(1, C), np.zeros(C)])
+    o, Wf = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=0)
+    om, Wm, _ = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=0, beta=beta)
+    np.testing.assert_allclose(om, o, rtol=1e-14)
+    for a, b in zip(Wm, Wf):
+        np.testing.assert_allclose(a, b, rtol=1e-14)
+    q, k, v, eta, W = _layer_inputs(33, 24, 24, 5, 6, eta_scale=0.4)
+    b1 = _beta(2, 24)
+    b2 = b1.copy()
+    for s in range(0, 24, C):                     # same means, different tokens
+        seg = b2[s:s + C]
+        seg[:] = seg.mean() + 0.5 * (_rng(s).uniform(-1, 1, C) * min(seg.mean(), 1 - seg.mean()))
+        seg += b1[s:s + C].mean() - seg.mean()
+    b3 = np.concatenate([_rng(7).permutation(b1[s:s + C]) for s in range(0, 24, C)])
+    ref = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=1, beta=b1)
+    for bb in (b2, b3):
+        got = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=1, beta=bb)
+        np.testing.assert_allclose(got[0], ref[0], rtol=1e-12)
+        for a, b in zip(got[1] + got[2], ref[1] + ref[2]):
+            np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-15)
+    bad = b1.copy(); bad[C] += 0.3               # a different mean (after M0 = 0) changes it
+    got = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=1, beta=bad)
+    assert np.max(np.abs(got[1][0] - ref[1][0])) > 1e-8
+
+
+def _torch_ns(G, steps):
+    a, b, c = 3.4445, -4.7750, 2.0315
+    X = G.T if G.shape[0] > G.shape[1] else G
+    X = X / (torch.linalg.matrix_norm(X) + 1e-7)
+    for _ in range(steps):
+        A = X @ X.T
+        X = a * X + (b * A + c * A @ A) @ X
+    return X.T if G.shape[0] > G.shape[1] else X
+
+
+@pytest.mark.parametrize("muon", [0, 1])
+def test_momentum_matches_autograd_loop(muon):
+    """An independent loop: torch autograd for each chunk's gradient, the
+    recurrence of Table 3 and the row normalisation in torch ops."""
+    C, n = 6, 18
+    q, k, v, eta, W = _layer_inputs(34, n, n, 4, 7, unit=False, eta_scale=0.6)
+    beta = _beta(3, n)
+    o, Wf, Mf = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=0, use_muon=bool(muon), beta=beta)
+    Wt = [torch.as_tensor(w.copy()) for w in W]
+    Mt = [torch.zeros_like(w) for w in Wt]
+    outs = []
+    for s in range(0, n, C):
+        Kc, Vc, ec = (torch.as_tensor(a[s:s + C]) for a in (k, v, eta))
+        outs.append(_torch_swiglu(*[w.numpy() for w in Wt], q[s:s + C]).numpy())
+        Wg = [w.clone().requires_grad_(True) for w in Wt]
+        _torch_loss(*Wg, Kc, Vc, ec).backward()
+        bbar = float(np.mean(beta[s:s + C]))
+        Mt = [bbar * m + w.grad for m, w in zip(Mt, Wg)]
+        new = []
+        for w, m in zip(Wt, Mt):
+            st = _torch_ns(m, 5) if muon else m
+            u = w - st
+            new.append(u * (w.norm(dim=1, keepdim=True) / u.norm(dim=1, keepdim=True)))
+        Wt = new
+    np.testing.assert_allclose(o, np.concatenate(outs), rtol=1e-11, atol=1e-13)
+    for a, b in zip(Wf, Wt):
+        np.testing.assert_allclose(a, b.numpy(), rtol=1e-11, atol=1e-13)
+    for a, b in zip(Mf, Mt):
+        np.testing.assert_allclose(a, b.detach().numpy(), rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("muon", [0, 1])
+def test_momentum_resume_from_returned_state(muon):
+    """With momentum the carried state is (W, M)."""
+    q, k, v, eta, W = _layer_inputs(35, 24, 24, 5, 7, eta_scale=0.3)
+    beta = _beta(4, 24)
+    o, Wf, Mf = O.lact_forward_instance(q, k, v, eta, *W, chunk=6, order=0, use_muon=bool(muon), beta=beta)
+    oa, Wa, Ma = O.lact_forward_instance(q[:12], k[:12], v[:12], eta[:12], *W, chunk=6, order=0,
+                                         use_muon=bool(muon), beta=beta[:12])
+    ob, Wb, Mb = O.lact_forward_instance(q[12:], k[12:], v[12:], eta[12:], *Wa, chunk=6, order=0,
+                                         use_muon=bool(muon), beta=beta[12:], M=Ma)
+    np.testing.assert_allclose(np.concatenate([oa, ob]), o, rtol=1e-12, atol=1e-15)
+    for a, b in zip(Wb + Mb, Wf + Mf):
+        np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-15)
+
+
+def test_momentum_muon_acts_on_the_accumulated_state():
+    """Muon(M) rather than M + Muon(g): a global eta scale scales every M and
+    leaves W unchanged (up to the 1e-7 of reading R3), while scaling only the
+    second chunk's eta changes the mix inside M and so the update."""
+    C = 8
+    q, k, v, eta, W = _layer_inputs(36, 16, 16, 6, 6, eta_scale=5.0)
+    beta = np.full(16, 0.9)
+    _, Wa, _ = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=0, use_muon=True, beta=beta)
+    _, Wb, _ = O.lact_forward_instance(q, k, v, 3.0 * eta, *W, chunk=C, order=0, use_muon=True, beta=beta)
+    for a, b in zip(Wa, Wb):
+        np.testing.assert_allclose(a, b, rtol=1e-3, atol=1e-4)
+    e2 = eta.copy(); e2[C:] *= 3.0
+    _, Wc, _ = O.lact_forward_instance(q, k, v, e2, *W, chunk=C, order=0, use_muon=True, beta=beta)
+    assert max(np.max(np.abs(a - c)) for a, c in zip(Wa, Wc)) > 1e-3

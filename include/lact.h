@@ -30,8 +30,8 @@
  *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
  *    stream) and never synchronise the host, except when the environment
  *    variable LACT_SYNC=1 is set (debugging).
- *  - No allocation happens inside lact_forward: all scratch memory is the
- *    caller's `workspace`.
+ *  - No allocation happens inside lact_forward or lact_forward_momentum:
+ *    all scratch memory is the caller's `workspace`.
  *  - Arguments are validated before any HIP call, so every error below is
  *    reported without touching the GPU. Errors are negative return codes;
  *    nothing is thrown across the ABI. On an error no output is written.
@@ -114,6 +114,40 @@ int lact_forward(const lact_desc* desc,
                  void* stream);
 
 /*
+ * The same path with a momentum test-time optimizer (App. A, implementing
+ * momentum for test-time optimizers; Table 3, Momentum and Muon rows). Per
+ * chunk, with b the chunk's key tokens and g the chunk gradient above:
+ *
+ *   bbar = (sum_{i in chunk} beta_i) / b        (per instance, per chunk)
+ *   M    <- bbar * M + g
+ *   W    <- L2-Normalize(W - M)  or  L2-Normalize(W - Muon(M))   (use_muon)
+ *
+ * so each chunk's own tokens set its momentum factor, and Muon acts on the
+ * accumulated state. Arguments as lact_forward, plus:
+ *
+ *   beta [B*H, n_kv]     fp32, per-token momentum factor (the sigmoid of a
+ *                        projection of the token, computed by the caller),
+ *                        4-byte aligned; may be NULL only when n_kv == 0   in
+ *   M1   [B*H, h, d]     fp32 momentum of W1, W2, W3: initial state in,
+ *   M2   [B*H, d, h]     state after the last update out (updated in place;
+ *   M3   [B*H, h, d]     pass zeros to start), 16-byte aligned, never NULL
+ *
+ * beta is used as given (no clamping to (0, 1)). The workspace is
+ * lact_workspace_bytes(desc), the same as lact_forward's. Errors and
+ * validation as lact_forward; a NULL M or (with n_kv > 0) beta is
+ * LACT_EINVAL, a misaligned one LACT_EALIGN. M must not alias W, o or the
+ * workspace.
+ */
+int lact_forward_momentum(const lact_desc* desc,
+                          const void* q, const void* k, const void* v, const float* eta,
+                          const float* beta,
+                          float* W1, float* W2, float* W3,
+                          float* M1, float* M2, float* M3,
+                          void* o,
+                          void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/*
  * Kernel timing (instrumentation for benchmarks). While enabled, lact_forward
  * brackets every kernel launch with HIP events on its stream, grouped by
  * kernel class (LACT_KCLASS_*). lact_timing_read synchronises on the recorded
@@ -123,7 +157,8 @@ int lact_forward(const lact_desc* desc,
  */
 #define LACT_KCLASS_FWD 0      /* apply GEMM-1 and key forward + hidden backward */
 #define LACT_KCLASS_BWD 1      /* apply GEMM-2 and the gradient contractions      */
-#define LACT_KCLASS_UPDATE 2   /* weight update, row norms, bf16 operand copies   */
+#define LACT_KCLASS_UPDATE 2   /* weight update, row norms, bf16 operand copies,  */
+                               /* momentum chunk means                            */
 #define LACT_KCLASS_NS 3       /* Newton-Schulz (Muon) kernels                    */
 #define LACT_KCLASS_PREP 4     /* initial fp32 -> bf16 operand copies             */
 #define LACT_KCLASS_COUNT 5

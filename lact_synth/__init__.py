@@ -8,8 +8,8 @@ returns.
 
 Recipe (one (seed, config) -> one set of host arrays):
 
-* independent sub-streams for q, k, v, eta, W1, W2, W3 from
-  ``numpy.random.SeedSequence(seed).spawn(7)``;
+* independent sub-streams for q, k, v, eta, W1, W2, W3 (and beta) from
+  ``numpy.random.SeedSequence(seed).spawn(8)``;
 * q, k, v ~ N(0, 1), L2-normalised per token per head (the layer normalises q
   and k before the fast-weight path, Alg. 1; v is normalised too so that all
   three share one scale), then rounded to bfloat16 (round-to-nearest-even)
@@ -20,7 +20,11 @@ Recipe (one (seed, config) -> one set of host arrays):
 * W1, W3 in R^{h x d}, W2 in R^{d x h} ~ N(0, 1/d), then every row (the input
   dimension of that matrix) scaled to unit L2 norm, float32, one copy per
   head repeated over the batch (Alg. 1 repeats the per-head initial fast
-  weight over the batch).
+  weight over the batch);
+* momentum workloads only: beta = sigmoid(N(0, 1)) per token per head,
+  float32, from an eighth sub-stream (the factor is the sigmoid of a linear
+  projection of the token, App. A; a unit-variance logit stands in for the
+  projection), so the other seven draws are the same with or without it.
 """
 from __future__ import annotations
 
@@ -44,6 +48,7 @@ class LactConfig:
     use_muon: int
     ns_steps: int
     io: str               # "bf16" or "fp32"
+    momentum: int = 0     # 1: momentum test-time optimizer (inputs carry beta)
 
     @property
     def BH(self) -> int:
@@ -65,6 +70,8 @@ CONFIGS = {
     "nvs256k": LactConfig("nvs256k", 1, 1, 768, 1536, 262144, 262144 + 4096, 262144, 1, 0, 0, "bf16"),
     "nvs1m": LactConfig("nvs1m", 1, 1, 768, 1536, 1048576, 1048576 + 4096, 1048576, 1, 0, 0, "bf16"),
     "video": LactConfig("video", 1, 40, 128, 256, 56160, 56160, 3120, 0, 1, 5, "bf16"),
+    "lm32k_mom": LactConfig("lm32k_mom", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", 1),
+    "lm32k_muon_mom": LactConfig("lm32k_muon_mom", 4, 4, 512, 512, 32768, 32768, 2048, 0, 1, 5, "bf16", 1),
 }
 
 
@@ -95,13 +102,14 @@ def make_inputs(cfg: LactConfig, seed: int = 0, heads: list | None = None):
     Returns a dict of float32 numpy arrays (bf16 workloads hold values that are
     exactly representable in bfloat16):
       q [B*H, n_q, d], k, v [B*H, n_kv, d], eta [B*H, n_kv],
-      W1, W3 [B*H, h, d], W2 [B*H, d, h].
+      W1, W3 [B*H, h, d], W2 [B*H, d, h], and beta [B*H, n_kv] for momentum
+      workloads.
     ``heads`` restricts the draw to a subset of the flattened (b, h) instances;
     the values of each kept instance are the same as in the full draw only for
     the weights (token tensors are drawn for the kept instances only).
     """
-    ss = np.random.SeedSequence(seed).spawn(7)
-    rq, rk, rv, re, r1, r2, r3 = (np.random.default_rng(s) for s in ss)
+    ss = np.random.SeedSequence(seed).spawn(8)
+    rq, rk, rv, re, r1, r2, r3, rb = (np.random.default_rng(s) for s in ss)
     BH = cfg.BH
     inst = list(range(BH)) if heads is None else list(heads)
     n = len(inst)
@@ -125,4 +133,8 @@ def make_inputs(cfg: LactConfig, seed: int = 0, heads: list | None = None):
     W1 = np.ascontiguousarray(w1[head_of])
     W2 = np.ascontiguousarray(w2[head_of])
     W3 = np.ascontiguousarray(w3[head_of])
-    return dict(q=q, k=k, v=v, eta=eta, W1=W1, W2=W2, W3=W3)
+    out = dict(q=q, k=k, v=v, eta=eta, W1=W1, W2=W2, W3=W3)
+    if cfg.momentum:
+        zb = rb.standard_normal((n, cfg.n_kv), dtype=np.float32).astype(np.float64)
+        out["beta"] = (1.0 / (1.0 + np.exp(-zb))).astype(np.float32)
+    return out

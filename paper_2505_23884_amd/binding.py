@@ -48,6 +48,8 @@ def load_library(path: str | None = None):
     L.lact_check_desc.restype = i32
     L.lact_forward.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.lact_forward.restype = i32
+    L.lact_forward_momentum.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.lact_forward_momentum.restype = i32
     L.lact_timing_enable.argtypes = [i32]
     L.lact_timing_enable.restype = i32
     L.lact_timing_reset.argtypes = []
@@ -99,15 +101,8 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
-def forward(q, k, v, eta, W1, W2, W3, chunk, order=APPLY_THEN_UPDATE, use_muon=False,
-            ns_steps=5, out=None, workspace=None, stream=None):
-    """LaCT fast-weight path on the GPU (see include/lact.h for the semantics).
-
-    q [B, H, n_q, d] (or [BH, n_q, d]); k, v [.., n_kv, d]; bf16 or fp32 (same dtype);
-    eta [.., n_kv] fp32; W1, W3 [.., h, d], W2 [.., d, h] fp32, updated IN PLACE.
-    Returns o with q's shape and dtype. Runs on torch's current stream unless a
-    stream is given; allocates the workspace unless one is passed.
-    """
+def _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps, out, workspace, stream):
+    """Checks shapes and dtypes; returns (desc, out, workspace, stream handle)."""
     import torch
     if q.dim() == 4:
         B, H = q.shape[0], q.shape[1]
@@ -124,13 +119,14 @@ def forward(q, k, v, eta, W1, W2, W3, chunk, order=APPLY_THEN_UPDATE, use_muon=F
         io = IO_FP32
     else:
         raise LactError(-1, f"unsupported q dtype {q.dtype}")
-    for t, name in ((q, "q"), (k, "k"), (v, "v"), (eta, "eta"), (W1, "W1"), (W2, "W2"), (W3, "W3")):
+    named = [(q, "q"), (k, "k"), (v, "v"), (eta, "eta"), (W1, "W1"), (W2, "W2"), (W3, "W3"), *extra]
+    for t, name in named:
         if not t.is_cuda or not t.is_contiguous():
             raise LactError(-1, f"{name} must be a contiguous device tensor")
     if k.dtype != q.dtype or v.dtype != q.dtype:
         raise LactError(-1, "q, k, v must share one dtype")
-    if eta.dtype != torch.float32 or any(w.dtype != torch.float32 for w in (W1, W2, W3)):
-        raise LactError(-1, "eta and the fast weights are fp32")
+    if eta.dtype != torch.float32 or any(t.dtype != torch.float32 for t, _ in named[4:]):
+        raise LactError(-1, "eta, beta, the fast weights and the momentum are fp32")
     BH = B * H
     if (k.numel() != BH * n_kv * d or v.numel() != BH * n_kv * d or eta.numel() != BH * n_kv
             or W1.numel() != BH * h * d or W3.numel() != BH * h * d or W2.numel() != BH * d * h
@@ -144,6 +140,20 @@ def forward(q, k, v, eta, W1, W2, W3, chunk, order=APPLY_THEN_UPDATE, use_muon=F
         out = torch.empty_like(q)
     if stream is None:
         stream = torch.cuda.current_stream(q.device).cuda_stream
+    return desc, out, workspace, stream
+
+
+def forward(q, k, v, eta, W1, W2, W3, chunk, order=APPLY_THEN_UPDATE, use_muon=False,
+            ns_steps=5, out=None, workspace=None, stream=None):
+    """LaCT fast-weight path on the GPU (see include/lact.h for the semantics).
+
+    q [B, H, n_q, d] (or [BH, n_q, d]); k, v [.., n_kv, d]; bf16 or fp32 (same dtype);
+    eta [.., n_kv] fp32; W1, W3 [.., h, d], W2 [.., d, h] fp32, updated IN PLACE.
+    Returns o with q's shape and dtype. Runs on torch's current stream unless a
+    stream is given; allocates the workspace unless one is passed.
+    """
+    desc, out, workspace, stream = _marshal(q, k, v, eta, W1, W2, W3, [], chunk, order, use_muon,
+                                            ns_steps, out, workspace, stream)
     rc = lib().lact_forward(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(W1),
                             _ptr(W2), _ptr(W3), _ptr(out), _ptr(workspace),
                             ctypes.c_size_t(workspace.numel() * workspace.element_size()),
@@ -151,6 +161,38 @@ def forward(q, k, v, eta, W1, W2, W3, chunk, order=APPLY_THEN_UPDATE, use_muon=F
     if rc:
         _raise(rc)
     return out
+
+
+def forward_momentum(q, k, v, eta, beta, W1, W2, W3, M1=None, M2=None, M3=None, *, chunk,
+                     order=APPLY_THEN_UPDATE, use_muon=False, ns_steps=5, out=None, workspace=None,
+                     stream=None):
+    """The path with the momentum test-time optimizer (lact_forward_momentum).
+
+    beta [.., n_kv] fp32 per-token momentum factor; M1, M3 [.., h, d], M2 [.., d, h]
+    fp32 momentum, updated IN PLACE (zeros are allocated when omitted). W as in
+    forward(). Returns (o, (M1, M2, M3)).
+    """
+    import torch
+    if M1 is None and M2 is None and M3 is None:
+        M1, M2, M3 = (torch.zeros_like(w) for w in (W1, W2, W3))
+    if M1 is None or M2 is None or M3 is None:
+        raise LactError(-1, "pass all three momentum tensors or none")
+    for m, w, name in ((M1, W1, "M1"), (M2, W2, "M2"), (M3, W3, "M3")):
+        if m.shape != w.shape:
+            raise LactError(-1, f"{name} must have the shape of its fast weight")
+    if beta.numel() != eta.numel():
+        raise LactError(-1, "beta must have eta's shape")
+    extra = [(beta, "beta"), (M1, "M1"), (M2, "M2"), (M3, "M3")]
+    desc, out, workspace, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon,
+                                            ns_steps, out, workspace, stream)
+    rc = lib().lact_forward_momentum(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta),
+                                     _ptr(beta), _ptr(W1), _ptr(W2), _ptr(W3), _ptr(M1), _ptr(M2),
+                                     _ptr(M3), _ptr(out), _ptr(workspace),
+                                     ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                                     ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return out, (M1, M2, M3)
 
 
 def timing_enable(on: bool = True):

@@ -34,7 +34,7 @@ struct Plan {
   int m;              // Newton-Schulz Gram size min(d, h)
   int ns_bps;         // blocks of kNsBlockElems per gradient
   // workspace offsets (bytes)
-  size_t off_wb[3], off_hq, off_upd[3], off_step, total;
+  size_t off_wb[3], off_hq, off_upd[3], off_step, off_bbar, total;
   size_t off_y32, off_yb[2], off_a32, off_ab, off_bb, off_ss;
 };
 
@@ -112,6 +112,10 @@ Plan make_plan(const lact_desc* dsc) {
   }
   p.off_step = o;
   o = align_up(o + (size_t)p.nsplit * p.BH * 3 * dh * 4);
+  // chunk-mean momentum factors of up to kBetaBatch chunks (momentum entry
+  // point only; reserved always so both entry points share one size)
+  p.off_bbar = o;
+  o = align_up(o + (size_t)p.BH * kBetaBatch * 4);
   p.muon = dsc->use_muon != 0;
   p.m = std::min(p.d, p.h);
   p.ns_bps = (int)cdiv((int64_t)dh, kNsBlockElems);
@@ -203,7 +207,15 @@ struct Ctx {
   uint8_t* ws;
   hipStream_t s;
   Operand wop[3];   // operand copies of W1, W2, W3 (bf16 copies or the fp32 state)
+  const float* beta;   // momentum: per-token factor [BH][n_kv], or nullptr
+  float* M[3];         // momentum state (with beta)
+  int64_t chunk_idx;   // index of the chunk being updated
 };
+
+// Momentum factor of the current chunk for instance 0 (stride kBetaBatch).
+const float* bbar_of(const Ctx& c) {
+  return reinterpret_cast<const float*>(c.ws + c.p.off_bbar) + c.chunk_idx % kBetaBatch;
+}
 
 Operand op(const void* base, int64_t ld, int64_t inst) { return Operand{base, ld, inst}; }
 
@@ -268,6 +280,11 @@ int newton_schulz(Ctx& c) {
   pa.nslots = p.BH * 3;
   pa.dh = dh;
   pa.blocks_per_slot = p.ns_bps;
+  if (c.beta) {
+    for (int j = 0; j < 3; ++j) pa.M[j] = c.M[j];
+    pa.bbar = bbar_of(c);
+    pa.bbar_stride = kBetaBatch;
+  }
   int rc = timed(LACT_KCLASS_NS, 0.0, c.s, [&] { return launch_ns_prep(pa, c.s); });
   if (rc) return rc;
   rc = timed(LACT_KCLASS_NS, 0.0, c.s,
@@ -475,12 +492,98 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     u.step = reinterpret_cast<const float*>(c.ws + p.off_step);
     u.nsplit = p.nsplit;
     u.step_split = (int64_t)p.BH * 3 * dh;
+    if (c.beta) {   // with Muon the state was advanced before Newton-Schulz
+      for (int j = 0; j < 3; ++j) u.M[j] = c.M[j];
+      u.bbar = bbar_of(c);
+      u.bbar_stride = kBetaBatch;
+    }
   }
   u.BH = p.BH;
   u.d = p.d;
   u.h = p.h;
   u.rows_total = p.BH * (2 * p.h + p.d);
   return timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] { return launch_update(u, p.bf16, c.s); });
+}
+
+// Both entry points: validation, operand copies and the chunk schedule.
+// beta == nullptr: plain updates; otherwise momentum with state M.
+int run_forward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                const float* beta, float* W1, float* W2, float* W3, float* const M[3], void* o,
+                void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
+  if (!W1 || !W2 || !W3) return LACT_EINVAL;
+  if (any_q && (!q || !o)) return LACT_EINVAL;
+  if (any_kv && (!k || !v || !eta)) return LACT_EINVAL;
+  if (M && (!M[0] || !M[1] || !M[2] || (any_kv && !beta))) return LACT_EINVAL;
+  if (misaligned(W1) || misaligned(W2) || misaligned(W3)) return LACT_EALIGN;
+  if (any_q && (misaligned(q) || misaligned(o))) return LACT_EALIGN;
+  if (any_kv && (misaligned(k) || misaligned(v) || ((uintptr_t)eta & 3))) return LACT_EALIGN;
+  if (M && (misaligned(M[0]) || misaligned(M[1]) || misaligned(M[2]))) return LACT_EALIGN;
+  if (M && any_kv && ((uintptr_t)beta & 3)) return LACT_EALIGN;
+  Ctx c{};
+  c.dsc = desc;
+  c.p = make_plan(desc);
+  if (!workspace || workspace_bytes < c.p.total) return LACT_EWORKSPACE;
+  if ((uintptr_t)workspace & (kAlign - 1)) return LACT_EALIGN;
+  c.q = (const uint8_t*)q;
+  c.k = (const uint8_t*)k;
+  c.v = (const uint8_t*)v;
+  c.eta = eta;
+  c.W[0] = W1;
+  c.W[1] = W2;
+  c.W[2] = W3;
+  c.o = (uint8_t*)o;
+  c.ws = (uint8_t*)workspace;
+  c.s = (hipStream_t)stream;
+  if (M) {
+    c.beta = beta;
+    for (int j = 0; j < 3; ++j) c.M[j] = M[j];
+  }
+  const Plan& p = c.p;
+  const int64_t dh = (int64_t)p.d * p.h;
+  if (p.bf16) {
+    const float* Wf[3] = {W1, W2, W3};
+    void* Wb[3] = {c.ws + p.off_wb[0], c.ws + p.off_wb[1], c.ws + p.off_wb[2]};
+    rc = timed(LACT_KCLASS_PREP, 0.0, c.s, [&] { return launch_prep(Wf, Wb, p.BH, p.d, p.h, c.s); });
+    if (rc) return rc;
+    c.wop[0] = op(Wb[0], p.d, dh);
+    c.wop[1] = op(Wb[1], p.h, dh);
+    c.wop[2] = op(Wb[2], p.d, dh);
+  } else {
+    c.wop[0] = op(W1, p.d, dh);
+    c.wop[1] = op(W2, p.h, dh);
+    c.wop[2] = op(W3, p.d, dh);
+  }
+  const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk;
+  const int64_t nchunks = cdiv(n_kv, C);
+  for (int64_t s0 = 0; s0 < n_kv; s0 += C) {
+    const int64_t s1 = std::min(n_kv, s0 + C);
+    c.chunk_idx = s0 / C;
+    if (c.beta && c.chunk_idx % kBetaBatch == 0) {
+      BetaArgs ba{};
+      ba.beta = c.beta;
+      ba.n_kv = n_kv;
+      ba.chunk = C;
+      ba.c0 = c.chunk_idx;
+      ba.nchunks = (int)std::min<int64_t>(kBetaBatch, nchunks - c.chunk_idx);
+      ba.BH = p.BH;
+      ba.bbar = reinterpret_cast<float*>(c.ws + p.off_bbar);
+      ba.stride = kBetaBatch;
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] { return launch_beta_mean(ba, c.s); });
+      if (rc) return rc;
+    }
+    if (desc->order == LACT_APPLY_THEN_UPDATE) {
+      rc = update_chunk(c, s0, s1, true);
+    } else {
+      rc = update_chunk(c, s0, s1, false);
+      if (!rc) rc = apply_rows(c, s0, s1 == n_kv ? n_q : s1);
+    }
+    if (rc) return rc;
+  }
+  if (desc->order == LACT_APPLY_THEN_UPDATE || n_kv == 0) rc = apply_rows(c, n_kv, n_q);
+  return rc;
 }
 
 }  // namespace
@@ -502,58 +605,16 @@ size_t lact_workspace_bytes(const lact_desc* desc, int* err) {
 int lact_forward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
                  float* W1, float* W2, float* W3, void* o, void* workspace, size_t workspace_bytes,
                  void* stream) {
-  int rc = check_desc(desc);
-  if (rc) return rc;
-  const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
-  if (!W1 || !W2 || !W3) return LACT_EINVAL;
-  if (any_q && (!q || !o)) return LACT_EINVAL;
-  if (any_kv && (!k || !v || !eta)) return LACT_EINVAL;
-  if (misaligned(W1) || misaligned(W2) || misaligned(W3)) return LACT_EALIGN;
-  if (any_q && (misaligned(q) || misaligned(o))) return LACT_EALIGN;
-  if (any_kv && (misaligned(k) || misaligned(v) || ((uintptr_t)eta & 3))) return LACT_EALIGN;
-  Ctx c{};
-  c.dsc = desc;
-  c.p = make_plan(desc);
-  if (!workspace || workspace_bytes < c.p.total) return LACT_EWORKSPACE;
-  if ((uintptr_t)workspace & (kAlign - 1)) return LACT_EALIGN;
-  c.q = (const uint8_t*)q;
-  c.k = (const uint8_t*)k;
-  c.v = (const uint8_t*)v;
-  c.eta = eta;
-  c.W[0] = W1;
-  c.W[1] = W2;
-  c.W[2] = W3;
-  c.o = (uint8_t*)o;
-  c.ws = (uint8_t*)workspace;
-  c.s = (hipStream_t)stream;
-  const Plan& p = c.p;
-  const int64_t dh = (int64_t)p.d * p.h;
-  if (p.bf16) {
-    const float* Wf[3] = {W1, W2, W3};
-    void* Wb[3] = {c.ws + p.off_wb[0], c.ws + p.off_wb[1], c.ws + p.off_wb[2]};
-    rc = timed(LACT_KCLASS_PREP, 0.0, c.s, [&] { return launch_prep(Wf, Wb, p.BH, p.d, p.h, c.s); });
-    if (rc) return rc;
-    c.wop[0] = op(Wb[0], p.d, dh);
-    c.wop[1] = op(Wb[1], p.h, dh);
-    c.wop[2] = op(Wb[2], p.d, dh);
-  } else {
-    c.wop[0] = op(W1, p.d, dh);
-    c.wop[1] = op(W2, p.h, dh);
-    c.wop[2] = op(W3, p.d, dh);
-  }
-  const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk;
-  for (int64_t s0 = 0; s0 < n_kv; s0 += C) {
-    const int64_t s1 = std::min(n_kv, s0 + C);
-    if (desc->order == LACT_APPLY_THEN_UPDATE) {
-      rc = update_chunk(c, s0, s1, true);
-    } else {
-      rc = update_chunk(c, s0, s1, false);
-      if (!rc) rc = apply_rows(c, s0, s1 == n_kv ? n_q : s1);
-    }
-    if (rc) return rc;
-  }
-  if (desc->order == LACT_APPLY_THEN_UPDATE || n_kv == 0) rc = apply_rows(c, n_kv, n_q);
-  return rc;
+  return run_forward(desc, q, k, v, eta, nullptr, W1, W2, W3, nullptr, o, workspace, workspace_bytes,
+                     stream);
+}
+
+int lact_forward_momentum(const lact_desc* desc, const void* q, const void* k, const void* v,
+                          const float* eta, const float* beta, float* W1, float* W2, float* W3, float* M1,
+                          float* M2, float* M3, void* o, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  float* const M[3] = {M1, M2, M3};
+  return run_forward(desc, q, k, v, eta, beta, W1, W2, W3, M, o, workspace, workspace_bytes, stream);
 }
 
 int lact_timing_enable(int enable) {

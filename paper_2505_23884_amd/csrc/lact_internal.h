@@ -78,6 +78,10 @@ struct UpdArgs {
   int64_t step_split;   // elements between splits
   int BH, d, h;
   int rows_total;       // BH * (2h + d)
+  // momentum (nullptr M: none): M_j <- bbar * M_j + g_j, and the update uses M
+  float* M[3];          // fp32 momentum, same layout as W
+  const float* bbar;    // chunk-mean momentum factor of instance i at bbar[i * bbar_stride]
+  int bbar_stride;
 };
 
 // ---- Muon: Newton-Schulz on the three gradients of every instance ----------
@@ -125,6 +129,23 @@ struct NsPrepArgs {
   int nslots;
   int64_t dh;
   int blocks_per_slot;  // blocks of 4096 elements per slot
+  // momentum (nullptr M: none); M and the iterate take M <- bbar * M + g first
+  float* M[3];
+  const float* bbar;
+  int bbar_stride;
+};
+
+// Chunk means of the per-token momentum factor: for chunks c in [0, nchunks),
+// bbar[i * stride + c] = mean of beta[i * n_kv + t] over t in chunk c0 + c.
+constexpr int kBetaBatch = 32;   // chunks per launch (bbar holds BH * kBetaBatch)
+struct BetaArgs {
+  const float* beta;    // [BH][n_kv]
+  int64_t n_kv, chunk;
+  int64_t c0;           // first chunk of this launch
+  int nchunks;          // <= kBetaBatch
+  int BH;
+  float* bbar;
+  int stride;
 };
 
 // Whole Newton-Schulz iteration of small matrices, one workgroup per matrix:
@@ -163,6 +184,7 @@ hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s);
 hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s);
 hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s);
 hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s);
+hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s);
 constexpr int kNsBlockElems = 4096;
 
 }  // namespace lact

@@ -1148,6 +1148,9 @@ __device__ __forceinline__ float wave_sum(float v) {
 // One wave per row of W1 (length d), W2 (length h) or W3 (length d):
 //   U = W + sum_split P  (P = -g, the negated gradient or its Newton-Schulz image)
 //   W <- U * ||W_row|| / ||U_row||       (§3.2 weight normalisation; Alg. 1)
+// With momentum (App. A, momentum for test-time optimizers; Table 3) the sum
+// first goes through the state: Y = sum P - bbar M = -(bbar M + g), M <- -Y,
+// U = W + Y.
 // Lane l owns the float4 vectors l, l+64, ... of the row (NV per lane at most);
 // every load is issued unconditionally (clamped index, zeroed after) so a row
 // costs one round trip to memory, not one per vector.
@@ -1173,12 +1176,14 @@ __global__ __launch_bounds__(256) void k_update(const UpdArgs a) {
   float4* W = reinterpret_cast<float4*>(a.W[mat] + off);
   const float4* P = reinterpret_cast<const float4*>(a.step + inst * 3 * dh + mat * dh + (int64_t)r * L);
   const int64_t ps = a.step_split >> 2;
-  float4 w[NV], u[NV];
+  float4* Mv = a.M[0] ? reinterpret_cast<float4*>(a.M[mat] + off) : nullptr;
+  float4 w[NV], u[NV], m[NV];
 #pragma unroll
   for (int t = 0; t < NV; ++t) {
     const int i = lane + 64 * t;
     w[t] = W[i < nv ? i : 0];
     u[t] = P[i < nv ? i : 0];
+    if (Mv) m[t] = Mv[i < nv ? i : 0];
   }
   for (int s = 1; s < a.nsplit; ++s) {
 #pragma unroll
@@ -1186,6 +1191,18 @@ __global__ __launch_bounds__(256) void k_update(const UpdArgs a) {
       const int i = lane + 64 * t;
       const float4 q = P[s * ps + (i < nv ? i : 0)];
       u[t].x += q.x; u[t].y += q.y; u[t].z += q.z; u[t].w += q.w;
+    }
+  }
+  if (Mv) {
+    const float bb = a.bbar[(int64_t)inst * a.bbar_stride];
+#pragma unroll
+    for (int t = 0; t < NV; ++t) {
+      const int i = lane + 64 * t;
+      u[t].x = fmaf(-bb, m[t].x, u[t].x);
+      u[t].y = fmaf(-bb, m[t].y, u[t].y);
+      u[t].z = fmaf(-bb, m[t].z, u[t].z);
+      u[t].w = fmaf(-bb, m[t].w, u[t].w);
+      if (i < nv) Mv[i] = make_float4(-u[t].x, -u[t].y, -u[t].z, -u[t].w);
     }
   }
   float sw = 0.f, su = 0.f;
@@ -1565,17 +1582,26 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 }
 
 // Sum the split-K partials of every gradient and the per-block sums of squares.
+// With momentum the iterate is Y = sum P - bbar M = -(bbar M + g) and M <- -Y
+// (App. A, momentum; Table 3, Muon row): Newton-Schulz then runs on the state.
 __global__ __launch_bounds__(256) void k_ns_prep(const NsPrepArgs a) {
   __shared__ float red[4];
   const int slot = blockIdx.x / a.blocks_per_slot;
   const int blk = blockIdx.x - slot * a.blocks_per_slot;
   const int64_t base = (int64_t)slot * a.dh;
+  const int inst = slot / 3, j = slot - 3 * (slot / 3);
+  float* Ms = a.M[0] ? a.M[j] + (int64_t)inst * a.dh : nullptr;
+  const float bb = Ms ? a.bbar[(int64_t)inst * a.bbar_stride] : 0.f;
   float ss = 0.f;
   for (int e = threadIdx.x; e < kNsBlockElems; e += 256) {
     const int64_t idx = (int64_t)blk * kNsBlockElems + e;
     if (idx < a.dh) {
       float g = 0.f;
       for (int s = 0; s < a.nsplit; ++s) g += a.part[s * a.part_split + base + idx];
+      if (Ms) {
+        g = fmaf(-bb, Ms[idx], g);
+        Ms[idx] = -g;
+      }
       a.Y32[base + idx] = g;
       ss += g * g;
     }
@@ -1602,6 +1628,27 @@ __global__ __launch_bounds__(256) void k_ns_scale(const NsPrepArgs a, void* yb, 
       a.Y32[base + idx] = y;
       st_elem<T>(yb, base + idx, y);
     }
+  }
+}
+
+// Chunk mean of the per-token momentum factor (App. A, momentum): one block
+// per (instance, chunk), fp64 accumulation.
+__global__ __launch_bounds__(256) void k_beta_mean(const BetaArgs a) {
+  __shared__ double red[4];
+  const int inst = blockIdx.x / a.nchunks;
+  const int c = blockIdx.x - inst * a.nchunks;
+  const int64_t t0 = (a.c0 + c) * a.chunk;
+  const int64_t t1 = t0 + a.chunk < a.n_kv ? t0 + a.chunk : a.n_kv;
+  const float* b = a.beta + (int64_t)inst * a.n_kv;
+  double s = 0.0;
+  for (int64_t t = t0 + threadIdx.x; t < t1; t += 256) s += (double)b[t];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double tot = red[0] + red[1] + red[2] + red[3];
+    a.bbar[(int64_t)inst * a.stride + c] = (float)(tot / (double)(t1 - t0));
   }
 }
 
@@ -1661,6 +1708,13 @@ hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, 
   if (blocks <= 0) return hipSuccess;
   if (fp16) k_ns_scale<_Float16><<<(unsigned)blocks, 256, 0, s>>>(a, Yb, eps);
   else k_ns_scale<float><<<(unsigned)blocks, 256, 0, s>>>(a, Yb, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.BH * a.nchunks;
+  if (blocks <= 0) return hipSuccess;
+  k_beta_mean<<<(unsigned)blocks, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -22,7 +22,7 @@ def _declared():
 def test_library_exports_every_declared_symbol():
     L = P.lib()
     names = _declared()
-    assert "lact_forward" in names and "lact_workspace_bytes" in names
+    assert {"lact_forward", "lact_forward_momentum", "lact_workspace_bytes"} <= set(names)
     for n in names:
         assert hasattr(L, n), n
 
@@ -89,6 +89,33 @@ def test_forward_argument_errors_before_any_hip_call():
     bad = make_desc(**dict(GOOD, d=12))
     assert _fwd(bad, nbytes=1 << 30) == -4
     assert ctypes.cast(P.lib().lact_strerror(-3), ctypes.c_char_p).value
+
+
+def _fwd_mom(desc, beta=0x9000, m1=0xA000, m2=0xB000, m3=0xC000, nbytes=None, **kw):
+    L = P.lib()
+    a = dict(q=0x1000, k=0x2000, v=0x3000, eta=0x4000, w1=0x5000, w2=0x6000, w3=0x7000, o=0x8000,
+             ws=0x10000)
+    a.update(kw)
+    if nbytes is None:
+        nbytes = P.workspace_bytes(desc) if P.check_desc(desc) == 0 else 0
+    vp = ctypes.c_void_p
+    return L.lact_forward_momentum(ctypes.byref(desc), vp(a["q"]), vp(a["k"]), vp(a["v"]), vp(a["eta"]),
+                                   vp(beta), vp(a["w1"]), vp(a["w2"]), vp(a["w3"]), vp(m1), vp(m2), vp(m3),
+                                   vp(a["o"]), vp(a["ws"]), ctypes.c_size_t(nbytes), vp(0))
+
+
+def test_momentum_argument_errors_before_any_hip_call():
+    d = make_desc(**GOOD)
+    assert _fwd_mom(d, beta=0) == -1        # beta is required when there are key tokens
+    assert _fwd_mom(d, m2=0) == -1
+    assert _fwd_mom(d, m3=0xC008) == -2     # momentum is read as float4
+    assert _fwd_mom(d, beta=0x9002) == -2   # beta needs 4-byte alignment
+    assert _fwd_mom(d, q=0) == -1           # the checks of lact_forward apply too
+    assert _fwd_mom(d, ws=0) == -3
+    assert _fwd_mom(make_desc(**dict(GOOD, d=12)), nbytes=1 << 30) == -4
+    # no key tokens: beta may be NULL, the momentum may not
+    d0 = make_desc(**dict(GOOD, n_kv=0))
+    assert _fwd_mom(d0, m1=0, beta=0) == -1
 
 
 def test_timing_api_without_launches():

@@ -229,6 +229,10 @@ def teacher_forced(cfg, x, instances, max_chunks=None):
     q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
     eta = to_dev(sh(x["eta"]), cfg, torch.float32)
     W = [to_dev(sh(x[w]), cfg, torch.float32) for w in ("W1", "W2", "W3")]
+    mom = bool(cfg.momentum)
+    if mom:
+        beta = to_dev(sh(x["beta"]), cfg, torch.float32)
+        M = [torch.zeros_like(w) for w in W]
     C = cfg.chunk
     nch = cfg.n_chunks if max_chunks is None else min(cfg.n_chunks, max_chunks)
     flat = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
@@ -238,19 +242,31 @@ def teacher_forced(cfg, x, instances, max_chunks=None):
         w_in = [flat(w) for w in W]
         cut = lambda t: t[:, :, s:e].contiguous()
         print(f"[gpu] {cfg.name} chunk {c} tokens [{s},{e})", flush=True)
-        o = P.forward(cut(q), cut(k), cut(v), eta[:, :, s:e].contiguous(), *W, chunk=C,
-                      order=cfg.order, use_muon=True, ns_steps=cfg.ns_steps)
+        if mom:
+            m_in = [flat(m) for m in M]
+            o, _ = P.forward_momentum(cut(q), cut(k), cut(v), eta[:, :, s:e].contiguous(),
+                                      beta[:, :, s:e].contiguous(), *W, *M, chunk=C, order=cfg.order,
+                                      use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps)
+        else:
+            o = P.forward(cut(q), cut(k), cut(v), eta[:, :, s:e].contiguous(), *W, chunk=C,
+                          order=cfg.order, use_muon=True, ns_steps=cfg.ns_steps)
         torch.cuda.synchronize()
         og, w_out = flat(o), [flat(w) for w in W]
         for i in instances:
-            o_ref, w_ref = O.lact_forward_instance(
+            kw = {}
+            if mom:
+                kw = dict(beta=x["beta"][i, s:e], M=[m[i].astype(np.float64) for m in m_in])
+            ref = O.lact_forward_instance(
                 x["q"][i, s:e], x["k"][i, s:e], x["v"][i, s:e], x["eta"][i, s:e],
                 *[w[i].astype(np.float64) for w in w_in], chunk=C, order=cfg.order,
-                use_muon=True, ns_steps=cfg.ns_steps)
+                use_muon=bool(cfg.use_muon) or not mom, ns_steps=cfg.ns_steps, **kw)
+            o_ref, w_ref = ref[0], ref[1]
             errs = {"o": rel(og[i], o_ref)}
             for j, name in enumerate(("W1", "W2", "W3")):
                 errs[name] = rel(w_out[j][i], w_ref[j])
                 errs["d" + name] = rel(w_out[j][i] - w_in[j][i], w_ref[j] - w_in[j][i])
+                if mom:
+                    errs["M" + name[1]] = rel(flat(M[j])[i], ref[2][j])
             for kk, vv in errs.items():
                 # a NaN must survive the running maximum (max() would drop it)
                 prev = worst.get(kk, 0.0)
@@ -310,3 +326,124 @@ def test_video_muon_teacher_forced_sampled():
     cfg = CONFIGS["video"]
     x = make_inputs(cfg, 0)
     teacher_forced(cfg, x, [0, 39])
+
+
+
+# ----------------------------------------------------------------------------- momentum
+#
+# The momentum test-time optimizer: M <- mean_chunk(beta) M + g, then the update
+# with M (or Muon(M)) in place of g. Without Muon the recurrence is as stable as
+# plain updates and the whole run is compared with the oracle; with Muon it is
+# teacher-forced per chunk from the GPU's own (W, M) like the Muon tests above.
+
+
+def run_gpu_momentum(cfg, x, M0=None, chunk=None):
+    print(f"[gpu] momentum {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} n_kv={cfg.n_kv} "
+          f"n_q={cfg.n_q} C={chunk or cfg.chunk} order={cfg.order} muon={cfg.use_muon}", flush=True)
+    n = len(x["q"])
+    B, H = (cfg.B, cfg.H) if n == cfg.BH else (n, 1)
+    sh = lambda a: a.reshape(B, H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta, beta = (to_dev(sh(x[a]), cfg, torch.float32) for a in ("eta", "beta"))
+    W = [to_dev(sh(x[w]), cfg, torch.float32) for w in ("W1", "W2", "W3")]
+    M = None if M0 is None else [to_dev(sh(m), cfg, torch.float32) for m in M0]
+    o, M = P.forward_momentum(q, k, v, eta, beta, *W, *(M or (None, None, None)),
+                              chunk=chunk or cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
+                              ns_steps=cfg.ns_steps)
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    return f(o), [f(w) for w in W], [f(m) for m in M]
+
+
+def run_oracle_momentum(cfg, x, instances=None):
+    return O.lact_forward_momentum(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["W1"], x["W2"],
+                                   x["W3"], chunk=cfg.chunk, order=cfg.order,
+                                   use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
+                                   instances=instances)
+
+
+def check_momentum(cfg, x, got, ref, instances=None):
+    og, Wg, Mg = got
+    errs = check(cfg, x, (og, Wg), ref[:4], instances=instances)
+    idx = slice(None) if instances is None else list(instances)
+    merr = {f"M{j + 1}": rel(Mg[j][idx], ref[4 + j]) for j in range(3)}
+    print("[gpu] rel-L2", {k: f"{v:.2e}" for k, v in merr.items()}, flush=True)
+    for kk, vv in merr.items():
+        assert vv <= TOL[cfg.io], (kk, vv)
+    return {**errs, **merr}
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_momentum_bf16_ragged_multi_chunk(order):
+    cfg = CONFIGS["lm32k_mom"].with_(name="mom_ragged", B=1, H=2, d=128, h=256, n_kv=700, n_q=760,
+                                     chunk=256, order=order)
+    x = make_inputs(cfg, 21)
+    check_momentum(cfg, x, run_gpu_momentum(cfg, x), run_oracle_momentum(cfg, x))
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_momentum_fp32_ragged_small_dims(order):
+    cfg = CONFIGS["tiny_fp32"].with_(name="mom_fp32", B=2, H=1, d=40, h=24, n_kv=300, n_q=333,
+                                     chunk=100, order=order, momentum=1)
+    x = make_inputs(cfg, 22)
+    check_momentum(cfg, x, run_gpu_momentum(cfg, x), run_oracle_momentum(cfg, x))
+
+
+def test_momentum_beta_zero_matches_plain_path_bitwise():
+    # bbar = 0: M is the chunk's gradient, the weights follow the plain path exactly
+    cfg = CONFIGS["lm32k_mom"].with_(name="mom_beta0", B=1, H=2, d=128, h=128, n_kv=600, n_q=640,
+                                     chunk=256)
+    x = make_inputs(cfg, 23)
+    x["beta"][:] = 0.0
+    o_m, W_m, M_m = run_gpu_momentum(cfg, x)
+    o_p, W_p = run_gpu(cfg, x)
+    assert np.array_equal(o_m, o_p)
+    assert all(np.array_equal(a, b) for a, b in zip(W_m, W_p))
+    ref = run_oracle_momentum(cfg, x)
+    for j in range(3):
+        assert rel(M_m[j], ref[4 + j]) <= TOL["bf16"]
+
+
+def test_momentum_resume_from_returned_state_bitwise():
+    cfg = CONFIGS["lm32k_mom"].with_(name="mom_resume", B=1, H=2, d=128, h=256, n_kv=1024, n_q=1024,
+                                     chunk=256)
+    x = make_inputs(cfg, 24)
+    o1, W1, M1 = run_gpu_momentum(cfg, x)
+    half = cfg.with_(n_kv=512, n_q=512)
+    first = {k: (np.ascontiguousarray(v[:, :512]) if k in ("q", "k", "v", "eta", "beta") else v)
+             for k, v in x.items()}
+    oa, Wa, Ma = run_gpu_momentum(half, first)
+    second = {k: np.ascontiguousarray(v[:, 512:]) for k, v in x.items() if k in ("q", "k", "v", "eta", "beta")}
+    second.update({"W1": Wa[0], "W2": Wa[1], "W3": Wa[2]})
+    ob, Wb, Mb = run_gpu_momentum(half, second, M0=Ma)
+    assert np.array_equal(np.concatenate([oa, ob], axis=1), o1)
+    assert all(np.array_equal(a, b) for a, b in zip(Wb + Mb, W1 + M1))
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_momentum_muon_teacher_forced(order):
+    cfg = CONFIGS["lm32k_muon_mom"].with_(name="mom_muon", B=1, H=2, d=128, h=256, n_kv=700, n_q=700,
+                                          chunk=256, order=order)
+    x = make_inputs(cfg, 25)
+    teacher_forced(cfg, x, [0, 1])
+
+
+def test_momentum_muon_fp32_teacher_forced():
+    cfg = CONFIGS["tiny_fp32"].with_(name="mom_muon_fp32", B=1, H=2, d=64, h=96, n_kv=512, n_q=512,
+                                     chunk=128, use_muon=1, ns_steps=5, momentum=1)
+    x = make_inputs(cfg, 26)
+    teacher_forced(cfg, x, [0, 1])
+
+
+def test_lm32k_momentum_full_launch_sampled_instances():
+    cfg = CONFIGS["lm32k_mom"]
+    x = make_inputs(cfg, 0)
+    got = run_gpu_momentum(cfg, x)
+    inst = [0, 9]
+    check_momentum(cfg, x, got, run_oracle_momentum(cfg, x, instances=inst), instances=inst)
+
+
+def test_lm32k_muon_momentum_teacher_forced_sampled():
+    cfg = CONFIGS["lm32k_muon_mom"]
+    x = make_inputs(cfg, 0)
+    teacher_forced(cfg, x, [0, 9], max_chunks=6)

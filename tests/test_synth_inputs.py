@@ -43,3 +43,13 @@ def test_weights_repeat_over_batch():
     assert np.array_equal(a["W1"][0], a["W1"][4]) and not np.array_equal(a["W1"][0], a["W1"][1])
     sub = make_inputs(cfg, 0, heads=[5, 6])
     assert np.array_equal(sub["W2"][0], a["W2"][5])
+
+
+def test_momentum_factor_draw():
+    cfg = CONFIGS["lm32k_mom"].with_(n_kv=256, n_q=256, d=64, h=64)
+    a = make_inputs(cfg, 0)
+    b = make_inputs(cfg.with_(momentum=0), 0)
+    assert "beta" not in b and a["beta"].shape == (16, 256) and a["beta"].dtype == np.float32
+    assert np.all((a["beta"] > 0) & (a["beta"] < 1)) and abs(a["beta"].mean() - 0.5) < 0.02
+    for key in b:                       # the other draws do not move
+        assert np.array_equal(a[key], b[key])

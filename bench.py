@@ -143,8 +143,9 @@ def measured_traffic(cfg_name, kernel):
 def describe(cfg):
     order = "apply-then-update" if cfg.order == 0 else "update-then-apply"
     muon = f", Muon {cfg.ns_steps} NS steps" if cfg.use_muon else ""
+    mom = ", momentum (chunk-mean beta)" if cfg.momentum else ""
     return (f"{cfg.name}: B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} n_kv={cfg.n_kv} n_q={cfg.n_q} "
-            f"chunk={cfg.chunk} {order}{muon}, io {cfg.io}, fp32 state")
+            f"chunk={cfg.chunk} {order}{muon}{mom}, io {cfg.io}, fp32 state")
 
 
 def cpu_baseline(cfg, min_seconds):
@@ -170,8 +171,13 @@ def cpu_baseline(cfg, min_seconds):
     while done < scfg.BH and dt < min_seconds:
         x = make_inputs(scfg, 0, heads=[done])
         t0 = time.perf_counter()
-        O.lact_forward(x["q"], x["k"], x["v"], x["eta"], x["W1"], x["W2"], x["W3"], chunk=scfg.chunk,
-                       order=scfg.order, use_muon=bool(scfg.use_muon), ns_steps=scfg.ns_steps)
+        if scfg.momentum:
+            O.lact_forward_momentum(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["W1"], x["W2"], x["W3"],
+                                    chunk=scfg.chunk, order=scfg.order, use_muon=bool(scfg.use_muon),
+                                    ns_steps=scfg.ns_steps)
+        else:
+            O.lact_forward(x["q"], x["k"], x["v"], x["eta"], x["W1"], x["W2"], x["W3"], chunk=scfg.chunk,
+                           order=scfg.order, use_muon=bool(scfg.use_muon), ns_steps=scfg.ns_steps)
         dt += time.perf_counter() - t0
         done += 1
     fl = done * O.layer_flops(1, scfg.d, scfg.h, scfg.n_kv, scfg.n_q, scfg.n_chunks, bool(scfg.use_muon),
@@ -208,6 +214,9 @@ def main():
     q, k, v = (torch.from_numpy(sh(x[n])).to(dev, io) for n in ("q", "k", "v"))
     eta = torch.from_numpy(sh(x["eta"])).to(dev, torch.float32)
     W = [torch.from_numpy(sh(x[n])).to(dev, torch.float32) for n in ("W1", "W2", "W3")]
+    if cfg.momentum:
+        beta = torch.from_numpy(sh(x["beta"])).to(dev, torch.float32)
+        M = [torch.zeros_like(w) for w in W]
     del x
     out = torch.empty_like(q)
     desc = P.binding.make_desc(cfg.B, cfg.H, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.chunk, cfg.order,
@@ -216,8 +225,13 @@ def main():
     stream = torch.cuda.current_stream(dev)
 
     def step():
-        P.forward(q, k, v, eta, *W, chunk=cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
-                  ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=stream.cuda_stream)
+        if cfg.momentum:
+            P.forward_momentum(q, k, v, eta, beta, *W, *M, chunk=cfg.chunk, order=cfg.order,
+                               use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps, out=out, workspace=ws,
+                               stream=stream.cuda_stream)
+        else:
+            P.forward(q, k, v, eta, *W, chunk=cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
+                      ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=stream.cuda_stream)
 
     for _ in range(args.warmup):
         step()

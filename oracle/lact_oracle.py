@@ -18,6 +18,12 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
 * momentum         M <- M * mean_i(beta_i) + g, then the update with M in
                    place of g: W - M, or W - Muon(M)                (App. A, implementing
                    momentum for test-time optimizers; Table 3, Momentum and Muon rows)
+* per-matrix rates one learning rate per token for each of W1, W2, W3 (the
+                   lr of shape [b, l, 3] in the update of Alg. 1)
+* schedule         a list of (mode, begin, end) segments, each one of
+                   update-then-apply, apply-then-update, update-only or
+                   apply-only on its token range (the ttt_config loop of Alg. 1;
+                   §3.1 masks, including the strided video mask of §3.3)
 
 Math layout (one instance): W1, W3 in R^{h x d}, W2 in R^{d x h}; a "row" is
 the input dimension of the matrix (d for W1 and W3, h for W2). Tokens are rows
@@ -45,6 +51,13 @@ test):
      sigmoid are outside the fast-weight path, like eta); a chunk's factor is
      the mean of its own tokens' beta_i; M starts at zero unless given, and
      the returned M is the state after the last update.
+  R9 per-matrix rates: eta of shape [n, 3] holds (lr1, lr2, lr3) per token and
+     weights the W1, W2 and W3 gradients respectively; with equal columns it
+     is the single-rate gradient of the chunk-gradient eq.
+  R10 schedule: segments run in list order and each is one update (one
+     chunk) over its whole range; output rows of tokens that no apply
+     segment covers are zero (Alg. 1 starts o at zero); a token applied by
+     two segments keeps the later value; a segment is never empty.
 
 parity: pinned (see tests/test_oracle_pins.py for each pin).
 """
@@ -55,7 +68,8 @@ import numpy as np
 __all__ = [
     "NS_COEFFS", "NS_EPS", "sigmoid", "silu", "swiglu_apply", "chunk_gradient",
     "newton_schulz", "weight_update", "update", "momentum_update", "lact_forward_instance",
-    "lact_forward", "lact_forward_momentum", "layer_flops",
+    "lact_forward", "lact_forward_momentum", "SCHEDULE_MODES", "lact_forward_schedule_instance",
+    "lact_forward_schedule", "layer_flops",
 ]
 
 # Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
@@ -98,6 +112,8 @@ def chunk_gradient(W1, W2, W3, K, V, eta, token_block: int = 65536):
     Alg. 1: forward on the keys, then the hidden gradient W2^T v_i pushed
     through the gate product and the SiLU derivative
     SiLU'(z) = s (1 + z (1 - s)), s = sigmoid(z).
+    eta is [n] (one rate) or [n, 3]: column j weights the gradient of
+    W_{j+1} only (per-matrix rates of Alg. 1, reading R9).
 
     Returns (g1 [h, d], g2 [d, h], g3 [h, d]) in float64.
     """
@@ -110,7 +126,8 @@ def chunk_gradient(W1, W2, W3, K, V, eta, token_block: int = 65536):
         e = min(n, s + token_block)
         k = np.asarray(K[s:e], dtype=np.float64)
         v = np.asarray(V[s:e], dtype=np.float64)
-        lr = np.asarray(eta[s:e], dtype=np.float64)[:, None]
+        lr = np.asarray(eta[s:e], dtype=np.float64)
+        lr1, lr2, lr3 = (lr[:, j:j + 1] for j in range(3)) if lr.ndim == 2 else (lr[:, None],) * 3
         z1 = k @ W1.T                      # pre-activation of the gate, [b, h]
         z3 = k @ W3.T                      # ungated hidden, [b, h]
         sg = sigmoid(z1)
@@ -121,9 +138,9 @@ def chunk_gradient(W1, W2, W3, K, V, eta, token_block: int = 65536):
         da = dhid * z3                     # through the gate product, W1 branch
         dz1 = da * sg * (1.0 + z1 * (1.0 - sg))   # SiLU derivative
         # L = -eta f^T v, so every gradient carries a minus sign.
-        g2 -= (v * lr).T @ hid             # dL/dW2 = -sum eta v hid^T
-        g1 -= (dz1 * lr).T @ k             # dL/dW1 = -sum eta dz1 k^T
-        g3 -= (dz3 * lr).T @ k             # dL/dW3 = -sum eta dz3 k^T
+        g2 -= (v * lr2).T @ hid            # dL/dW2 = -sum eta v hid^T
+        g1 -= (dz1 * lr1).T @ k            # dL/dW1 = -sum eta dz1 k^T
+        g3 -= (dz3 * lr3).T @ k            # dL/dW3 = -sum eta dz3 k^T
     return g1, g2, g3
 
 
@@ -255,6 +272,68 @@ def lact_forward_momentum(q, k, v, eta, beta, W1, W2, W3, M1=None, M2=None, M3=N
         for j, x in enumerate((o, *W, *Mo)):
             res[j].append(x)
     return tuple(np.stack(r) for r in res)
+
+
+SCHEDULE_MODES = ("apply_then_update", "update_then_apply", "update_only", "apply_only")
+
+
+def lact_forward_schedule_instance(q, k, v, eta, W1, W2, W3, schedule, use_muon: bool = False,
+                                   ns_steps: int = NS_STEPS_DEFAULT, beta=None, M=None,
+                                   token_block: int = 65536):
+    """One instance under a general schedule (the ttt_config loop of Alg. 1).
+
+    schedule: sequence of (mode, begin, end), mode one of SCHEDULE_MODES (or its
+    index), each segment a single update and/or apply over tokens [begin, end)
+    (reading R10). q [n_q, d]; k, v [n_kv, d]; eta [n_kv] or [n_kv, 3]; with
+    ``beta`` the updates use momentum (state ``M``, zeros if omitted).
+    Returns (o [n_q, d], (W1, W2, W3)) or, with beta, (o, W, M).
+    """
+    W = tuple(np.asarray(w, dtype=np.float64).copy() for w in (W1, W2, W3))
+    mom = beta is not None
+    if mom:
+        M = tuple(np.zeros_like(w) for w in W) if M is None else tuple(
+            np.asarray(m, dtype=np.float64).copy() for m in M)
+    o = np.zeros((q.shape[0], q.shape[1]))
+
+    def upd(W, M, b, e):
+        assert e <= k.shape[0]
+        if mom:
+            return momentum_update(W, M, k[b:e], v[b:e], eta[b:e], beta[b:e], use_muon, ns_steps, token_block)
+        return update(W, k[b:e], v[b:e], eta[b:e], use_muon, ns_steps, token_block), M
+
+    for mode, b, e in schedule:
+        mode = SCHEDULE_MODES[mode] if not isinstance(mode, str) else mode
+        assert 0 <= b < e, "segments are non-empty"
+        if mode == "update_then_apply":
+            W, M = upd(W, M, b, e)
+            o[b:e] = swiglu_apply(*W, q[b:e])
+        elif mode == "apply_then_update":
+            o[b:e] = swiglu_apply(*W, q[b:e])
+            W, M = upd(W, M, b, e)
+        elif mode == "update_only":
+            W, M = upd(W, M, b, e)
+        elif mode == "apply_only":
+            o[b:e] = swiglu_apply(*W, q[b:e])
+        else:
+            raise ValueError(mode)
+    return (o, W, M) if mom else (o, W)
+
+
+def lact_forward_schedule(q, k, v, eta, W1, W2, W3, schedule, use_muon: bool = False,
+                          ns_steps: int = NS_STEPS_DEFAULT, beta=None, M1=None, M2=None, M3=None,
+                          instances=None, token_block: int = 65536):
+    """Batched driver of lact_forward_schedule_instance (one schedule for every
+    instance): returns (o, W1, W2, W3) stacked, plus (M1, M2, M3) with beta."""
+    idx = range(q.shape[0]) if instances is None else instances
+    res = []
+    for i in idx:
+        kw = {}
+        if beta is not None:
+            kw = dict(beta=beta[i], M=None if M1 is None else (M1[i], M2[i], M3[i]))
+        r = lact_forward_schedule_instance(q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], schedule,
+                                           use_muon, ns_steps, token_block=token_block, **kw)
+        res.append((r[0], *r[1]) + (tuple(r[2]) if beta is not None else ()))
+    return tuple(np.stack(col) for col in zip(*res))
 
 
 def layer_flops(BH: int, d: int, h: int, n_kv: int, n_q: int, n_chunks: int,

@@ -521,3 +521,140 @@ def test_momentum_muon_acts_on_the_accumulated_state():
     e2 = eta.copy(); e2[C:] *= 3.0
     _, Wc, _ = O.lact_forward_instance(q, k, v, e2, *W, chunk=C, order=0, use_muon=True, beta=beta)
     assert max(np.max(np.abs(a - c)) for a, c in zip(Wa, Wc)) > 1e-3
+
+
+# ----------------------------------------------------------------------------- per-matrix rates
+# Alg. 1 (update): lr [b, l, 3] = (lr1, lr2, lr3) weights the W1, W2, W3 gradients.
+
+
+def _lr3(seed, n, scale=0.3):
+    return scale * np.log1p(np.exp(_rng(seed).standard_normal((n, 3))))
+
+
+def test_per_matrix_rates_with_equal_columns_are_the_single_rate():
+    q, k, v, eta, W = _layer_inputs(40, 20, 20, 5, 7, eta_scale=0.3)
+    g = O.chunk_gradient(*W, k, v, eta)
+    g3 = O.chunk_gradient(*W, k, v, np.stack([eta] * 3, axis=1))
+    for a, b in zip(g, g3):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_per_matrix_rates_match_three_autograd_losses():
+    """g_j is the gradient w.r.t. W_j of the loss weighted by column j alone."""
+    rng = _rng(41)
+    d, h, n = 5, 7, 13
+    W = _weights(rng, h, d)
+    k, v = _tokens(rng, n, d), _tokens(rng, n, d)
+    lr = _lr3(42, n)
+    got = O.chunk_gradient(*W, k, v, lr)
+    for j in range(3):
+        Wt = [torch.as_tensor(w.copy()).requires_grad_(True) for w in W]
+        _torch_loss(*Wt, torch.as_tensor(k), torch.as_tensor(v), torch.as_tensor(lr[:, j])).backward()
+        np.testing.assert_allclose(got[j], Wt[j].grad.numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_zero_rate_column_leaves_that_matrix():
+    q, k, v, eta, W = _layer_inputs(43, 16, 16, 5, 7)
+    lr = _lr3(44, 16)
+    lr[:, 1] = 0.0
+    _, Wf = O.lact_forward_instance(q, k, v, lr, *W, chunk=8, order=0)
+    np.testing.assert_array_equal(Wf[1], W[1])
+    assert np.max(np.abs(Wf[0] - W[0])) > 1e-6 and np.max(np.abs(Wf[2] - W[2])) > 1e-6
+
+
+# ----------------------------------------------------------------------------- schedule
+# The ttt_config loop of Alg. 1: (mode, begin, end) segments in list order.
+
+
+@pytest.mark.parametrize("order", [0, 1])
+@pytest.mark.parametrize("muon", [0, 1])
+def test_uniform_schedule_is_the_chunk_loop(order, muon):
+    q, k, v, eta, W = _layer_inputs(45, 29, 22, 5, 6, eta_scale=0.3)
+    C = 8
+    sched = [(order, s, min(22, s + C)) for s in range(0, 22, C)] + [("apply_only", 22, 29)]
+    a = O.lact_forward_instance(q, k, v, eta, *W, chunk=C, order=order, use_muon=bool(muon))
+    b = O.lact_forward_schedule_instance(q, k, v, eta, *W, sched, use_muon=bool(muon))
+    np.testing.assert_array_equal(a[0], b[0])
+    for x, y in zip(a[1], b[1]):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_split_modes_compose_into_the_fused_modes():
+    q, k, v, eta, W = _layer_inputs(46, 24, 24, 5, 6, eta_scale=0.3)
+    pairs = [([("update_only", 3, 17), ("apply_only", 3, 17)], [("update_then_apply", 3, 17)]),
+             ([("apply_only", 3, 17), ("update_only", 3, 17)], [("apply_then_update", 3, 17)])]
+    for split, fused in pairs:
+        a = O.lact_forward_schedule_instance(q, k, v, eta, *W, split)
+        b = O.lact_forward_schedule_instance(q, k, v, eta, *W, fused)
+        np.testing.assert_array_equal(a[0], b[0])
+        for x, y in zip(a[1], b[1]):
+            np.testing.assert_array_equal(x, y)
+
+
+def test_uncovered_rows_are_zero_and_later_applies_win():
+    q, k, v, eta, W = _layer_inputs(47, 30, 20, 5, 6, eta_scale=0.3)
+    o, _ = O.lact_forward_schedule_instance(q, k, v, eta, *W, [("update_only", 0, 20)])
+    assert not o.any()
+    sched = [("apply_only", 0, 30), ("update_only", 0, 12), ("apply_only", 5, 18)]
+    o, Wf = O.lact_forward_schedule_instance(q, k, v, eta, *W, sched)
+    W1 = O.update(tuple(np.asarray(w) for w in W), k[:12], v[:12], eta[:12])
+    np.testing.assert_allclose(o[5:18], _torch_swiglu(*W1, q[5:18]).numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(np.concatenate([o[:5], o[18:]]),
+                               _torch_swiglu(*W, np.concatenate([q[:5], q[18:]])).numpy(), rtol=1e-12, atol=1e-14)
+
+
+def _video_schedule(C, n_clean):
+    """Teacher forcing of §3.3: [X1_noise, X1, X2_noise, X2, ..., XN_noise];
+    noisy chunks are applied only, clean chunks update then apply."""
+    sched, t = [], 0
+    for i in range(n_clean + 1):
+        sched.append(("apply_only", t, t + C))
+        t += C
+        if i < n_clean:
+            sched.append(("update_then_apply", t, t + C))
+            t += C
+    return sched, t
+
+
+def test_video_strided_mask_updates_on_clean_chunks_only():
+    C, N = 6, 3
+    sched, n = _video_schedule(C, N)
+    q, k, v, eta, W = _layer_inputs(48, n, n, 5, 6, eta_scale=0.4)
+    o, Wf = O.lact_forward_schedule_instance(q, k, v, eta, *W, sched)
+    noisy = np.concatenate([np.arange(s, e) for m, s, e in sched if m == "apply_only"])
+    clean = np.concatenate([np.arange(s, e) for m, s, e in sched if m != "apply_only"])
+    # noisy keys, values and rates never reach the fast weights
+    k2, v2, e2 = k.copy(), v.copy(), eta.copy()
+    k2[noisy] = _tokens(_rng(49), len(noisy), 5)
+    v2[noisy] *= -1.0
+    e2[noisy] *= 7.0
+    o2, W2 = O.lact_forward_schedule_instance(q, k2, v2, e2, *W, sched)
+    np.testing.assert_array_equal(o2, o)
+    for a, b in zip(W2, Wf):
+        np.testing.assert_array_equal(a, b)
+    # the clean chunks alone run an ordinary update-then-apply chunk loop, and
+    # each noisy chunk sees the weights after the clean chunks before it
+    oc, Wc = O.lact_forward_instance(q[clean], k[clean], v[clean], eta[clean], *W, chunk=C, order=1)
+    np.testing.assert_array_equal(o[clean], oc)
+    for a, b in zip(Wc, Wf):
+        np.testing.assert_array_equal(a, b)
+    Wi = tuple(np.asarray(w, dtype=np.float64) for w in W)
+    for i, (m, s, e) in enumerate(x for x in sched if x[0] == "apply_only"):
+        np.testing.assert_allclose(o[s:e], _torch_swiglu(*Wi, q[s:e]).numpy(), rtol=1e-12, atol=1e-14)
+        if i < N:
+            cs = s + C
+            Wi = O.update(Wi, k[cs:cs + C], v[cs:cs + C], eta[cs:cs + C])
+
+
+def test_schedule_with_momentum_and_per_matrix_rates():
+    q, k, v, _, W = _layer_inputs(50, 24, 24, 5, 6)
+    lr = _lr3(51, 24)
+    beta = _beta(52, 24)
+    sched = [("update_only", 0, 8), ("apply_then_update", 8, 16), ("update_then_apply", 16, 24)]
+    o, Wf, M = O.lact_forward_schedule_instance(q, k, v, lr, *W, sched, beta=beta)
+    Wr, Mr = tuple(np.asarray(w, dtype=np.float64) for w in W), tuple(np.zeros_like(w) for w in W)
+    for s in (0, 8, 16):
+        Wr, Mr = O.momentum_update(Wr, Mr, k[s:s + 8], v[s:s + 8], lr[s:s + 8], beta[s:s + 8])
+    for a, b in zip(Wf + M, Wr + Mr):
+        np.testing.assert_array_equal(a, b)
+    assert not o[:8].any()

@@ -77,6 +77,9 @@ typedef struct lact_desc {
   int32_t use_muon;   /* 0 or 1                                                  */
   int32_t ns_steps;   /* Newton-Schulz iterations when use_muon, in [0, 16]     */
   int32_t io_dtype;   /* LACT_IO_BF16 or LACT_IO_FP32                           */
+  int32_t eta_per_matrix; /* 0: eta is [B*H, n_kv], one rate per token;        */
+                      /* 1: eta is [B*H, n_kv, 3], (lr1, lr2, lr3) per token    */
+                      /* weighting the W1, W2, W3 gradients (Alg. 1, update)    */
 } lact_desc;
 
 /*
@@ -96,6 +99,7 @@ int lact_check_desc(const lact_desc* desc);
  *   k    [B*H, n_kv, d]  io_dtype                               in
  *   v    [B*H, n_kv, d]  io_dtype                               in
  *   eta  [B*H, n_kv]     fp32, per-token learning rate          in
+ *                        ([B*H, n_kv, 3] with desc->eta_per_matrix)
  *   W1   [B*H, h, d]     fp32   initial fast weights in, final fast weights out
  *   W2   [B*H, d, h]     fp32   (updated in place)
  *   W3   [B*H, h, d]     fp32
@@ -139,6 +143,50 @@ int lact_forward(const lact_desc* desc,
  * workspace.
  */
 int lact_forward_momentum(const lact_desc* desc,
+                          const void* q, const void* k, const void* v, const float* eta,
+                          const float* beta,
+                          float* W1, float* W2, float* W3,
+                          float* M1, float* M2, float* M3,
+                          void* o,
+                          void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/*
+ * General schedule: the fast-weight path over a caller-given list of segments
+ * (the ttt_config loop of Alg. 1; §3.1 masks and the strided mask of §3.3
+ * that updates on clean video chunks only). Segments run in list order; each
+ * is ONE update and/or apply over its token range [begin, end):
+ *
+ *   LACT_SEG_APPLY_THEN_UPDATE   o[range] = f_W(q[range]);  W <- update(range)
+ *   LACT_SEG_UPDATE_THEN_APPLY   W <- update(range);  o[range] = f_W(q[range])
+ *   LACT_SEG_UPDATE_ONLY         W <- update(range)
+ *   LACT_SEG_APPLY_ONLY          o[range] = f_W(q[range])
+ *
+ * A range is non-empty; an update range lies in [0, n_kv) and holds at most
+ * desc->chunk tokens (desc->chunk sizes the workspace); an apply range lies
+ * in [0, n_q) and may be of any length. Rows of o that no apply segment
+ * covers are written as zeros; a row applied twice keeps the later value.
+ * desc->order is ignored. `segs` is a HOST array of nseg entries (nseg >= 0,
+ * NULL allowed when nseg == 0), read before the call returns.
+ *
+ * Momentum: with M1 != NULL the updates use the momentum optimizer of
+ * lact_forward_momentum (each update segment's own mean of beta), and beta,
+ * M1, M2, M3 follow its rules; with M1 == NULL, beta, M2 and M3 are ignored
+ * and the updates are plain. Other arguments, the workspace
+ * (lact_workspace_bytes(desc)) and the errors are those of lact_forward; an
+ * invalid segment is LACT_EINVAL.
+ */
+#define LACT_SEG_APPLY_THEN_UPDATE 0
+#define LACT_SEG_UPDATE_THEN_APPLY 1
+#define LACT_SEG_UPDATE_ONLY 2
+#define LACT_SEG_APPLY_ONLY 3
+typedef struct lact_segment {
+  int32_t mode;       /* LACT_SEG_*                                              */
+  int32_t reserved;   /* must be 0                                               */
+  int64_t begin, end; /* token range [begin, end)                                */
+} lact_segment;
+int lact_forward_schedule(const lact_desc* desc,
+                          const lact_segment* segs, int64_t nseg,
                           const void* q, const void* k, const void* v, const float* eta,
                           const float* beta,
                           float* W1, float* W2, float* W3,

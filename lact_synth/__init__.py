@@ -21,6 +21,8 @@ Recipe (one (seed, config) -> one set of host arrays):
   dimension of that matrix) scaled to unit L2 norm, float32, one copy per
   head repeated over the batch (Alg. 1 repeats the per-head initial fast
   weight over the batch);
+* per-matrix-rate workloads: eta = 0.01 * softplus(N(0, 1)) drawn as
+  [B*H, n_kv, 3] (lr1, lr2, lr3) from the same sub-stream;
 * momentum workloads only: beta = sigmoid(N(0, 1)) per token per head,
   float32, from an eighth sub-stream (the factor is the sigmoid of a linear
   projection of the token, App. A; a unit-variance logit stands in for the
@@ -49,6 +51,7 @@ class LactConfig:
     ns_steps: int
     io: str               # "bf16" or "fp32"
     momentum: int = 0     # 1: momentum test-time optimizer (inputs carry beta)
+    lr3: int = 0          # 1: per-matrix learning rates, eta [B*H, n_kv, 3]
 
     @property
     def BH(self) -> int:
@@ -101,7 +104,7 @@ def make_inputs(cfg: LactConfig, seed: int = 0, heads: list | None = None):
 
     Returns a dict of float32 numpy arrays (bf16 workloads hold values that are
     exactly representable in bfloat16):
-      q [B*H, n_q, d], k, v [B*H, n_kv, d], eta [B*H, n_kv],
+      q [B*H, n_q, d], k, v [B*H, n_kv, d], eta [B*H, n_kv] (or [B*H, n_kv, 3]),
       W1, W3 [B*H, h, d], W2 [B*H, d, h], and beta [B*H, n_kv] for momentum
       workloads.
     ``heads`` restricts the draw to a subset of the flattened (b, h) instances;
@@ -122,7 +125,7 @@ def make_inputs(cfg: LactConfig, seed: int = 0, heads: list | None = None):
     q = tok(rq, cfg.n_q)
     k = tok(rk, cfg.n_kv)
     v = tok(rv, cfg.n_kv)
-    z = re.standard_normal((n, cfg.n_kv), dtype=np.float32).astype(np.float64)
+    z = re.standard_normal((n, cfg.n_kv, 3) if cfg.lr3 else (n, cfg.n_kv), dtype=np.float32).astype(np.float64)
     eta = (0.01 * np.logaddexp(0.0, z)).astype(np.float32)
 
     std = 1.0 / np.sqrt(cfg.d)

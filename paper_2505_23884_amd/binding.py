@@ -25,7 +25,16 @@ class LactDesc(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("h", ctypes.c_int32), ("n_kv", ctypes.c_int64), ("n_q", ctypes.c_int64),
                 ("chunk", ctypes.c_int64), ("order", ctypes.c_int32), ("use_muon", ctypes.c_int32),
-                ("ns_steps", ctypes.c_int32), ("io_dtype", ctypes.c_int32)]
+                ("ns_steps", ctypes.c_int32), ("io_dtype", ctypes.c_int32), ("eta_per_matrix", ctypes.c_int32)]
+
+
+SEG_APPLY_THEN_UPDATE, SEG_UPDATE_THEN_APPLY, SEG_UPDATE_ONLY, SEG_APPLY_ONLY = 0, 1, 2, 3
+SEG_MODES = {"apply_then_update": 0, "update_then_apply": 1, "update_only": 2, "apply_only": 3}
+
+
+class LactSegment(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("reserved", ctypes.c_int32), ("begin", ctypes.c_int64),
+                ("end", ctypes.c_int64)]
 
 
 _lib = None
@@ -50,6 +59,8 @@ def load_library(path: str | None = None):
     L.lact_forward.restype = i32
     L.lact_forward_momentum.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.lact_forward_momentum.restype = i32
+    L.lact_forward_schedule.argtypes = [dp, ctypes.POINTER(LactSegment), i64] + [vp] * 13 + [sz, vp]
+    L.lact_forward_schedule.restype = i32
     L.lact_timing_enable.argtypes = [i32]
     L.lact_timing_enable.restype = i32
     L.lact_timing_reset.argtypes = []
@@ -80,9 +91,10 @@ def _raise(code: int):
     raise LactError(code, msg)
 
 
-def make_desc(B, H, d, h, n_kv, n_q, chunk, order=0, use_muon=False, ns_steps=5, io_dtype=IO_BF16):
+def make_desc(B, H, d, h, n_kv, n_q, chunk, order=0, use_muon=False, ns_steps=5, io_dtype=IO_BF16,
+              eta_per_matrix=False):
     return LactDesc(int(B), int(H), int(d), int(h), int(n_kv), int(n_q), int(chunk), int(order),
-                    int(bool(use_muon)), int(ns_steps), int(io_dtype))
+                    int(bool(use_muon)), int(ns_steps), int(io_dtype), int(bool(eta_per_matrix)))
 
 
 def check_desc(desc: LactDesc) -> int:
@@ -128,11 +140,13 @@ def _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps, 
     if eta.dtype != torch.float32 or any(t.dtype != torch.float32 for t, _ in named[4:]):
         raise LactError(-1, "eta, beta, the fast weights and the momentum are fp32")
     BH = B * H
-    if (k.numel() != BH * n_kv * d or v.numel() != BH * n_kv * d or eta.numel() != BH * n_kv
+    # per-matrix rates: eta [.., n_kv, 3] (one more trailing dim than k's token axis)
+    lr3 = eta.dim() == k.dim() and eta.shape[-1] == 3
+    if (k.numel() != BH * n_kv * d or v.numel() != BH * n_kv * d or eta.numel() != BH * n_kv * (3 if lr3 else 1)
             or W1.numel() != BH * h * d or W3.numel() != BH * h * d or W2.numel() != BH * d * h
             or W2.shape[-2] != d or W2.shape[-1] != h or W1.shape[-1] != d):
         raise LactError(-1, "inconsistent tensor shapes")
-    desc = make_desc(B, H, d, h, n_kv, n_q, chunk, order, use_muon, ns_steps, io)
+    desc = make_desc(B, H, d, h, n_kv, n_q, chunk, order, use_muon, ns_steps, io, lr3)
     nbytes = workspace_bytes(desc)
     if workspace is None:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
@@ -180,8 +194,8 @@ def forward_momentum(q, k, v, eta, beta, W1, W2, W3, M1=None, M2=None, M3=None, 
     for m, w, name in ((M1, W1, "M1"), (M2, W2, "M2"), (M3, W3, "M3")):
         if m.shape != w.shape:
             raise LactError(-1, f"{name} must have the shape of its fast weight")
-    if beta.numel() != eta.numel():
-        raise LactError(-1, "beta must have eta's shape")
+    if beta.numel() != k.numel() // k.shape[-1]:
+        raise LactError(-1, "beta must be [.., n_kv]")
     extra = [(beta, "beta"), (M1, "M1"), (M2, "M2"), (M3, "M3")]
     desc, out, workspace, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon,
                                             ns_steps, out, workspace, stream)
@@ -193,6 +207,42 @@ def forward_momentum(q, k, v, eta, beta, W1, W2, W3, M1=None, M2=None, M3=None, 
     if rc:
         _raise(rc)
     return out, (M1, M2, M3)
+
+
+def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_steps=5, beta=None,
+                     M1=None, M2=None, M3=None, chunk=None, out=None, workspace=None, stream=None):
+    """The path over a general schedule (lact_forward_schedule): ``schedule`` is a
+    sequence of (mode, begin, end) with mode a name of SEG_MODES or its code.
+    ``chunk`` (the workspace bound) defaults to the longest update segment.
+    With ``beta`` the updates use momentum (M1..M3 updated in place, zeros
+    allocated when omitted). Returns o, or (o, (M1, M2, M3)) with beta.
+    """
+    import torch
+    segs = (LactSegment * max(len(schedule), 1))()
+    longest = 1
+    for i, (mode, b, e) in enumerate(schedule):
+        m = SEG_MODES[mode] if isinstance(mode, str) else int(mode)
+        segs[i] = LactSegment(m, 0, int(b), int(e))
+        if m != SEG_APPLY_ONLY:
+            longest = max(longest, int(e) - int(b))
+    extra = []
+    if beta is not None:
+        if M1 is None and M2 is None and M3 is None:
+            M1, M2, M3 = (torch.zeros_like(w) for w in (W1, W2, W3))
+        if M1 is None or M2 is None or M3 is None:
+            raise LactError(-1, "pass all three momentum tensors or none")
+        extra = [(beta, "beta"), (M1, "M1"), (M2, "M2"), (M3, "M3")]
+    desc, out, workspace, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk or longest, 0, use_muon,
+                                            ns_steps, out, workspace, stream)
+    M = (M1, M2, M3) if beta is not None else (None, None, None)
+    rc = lib().lact_forward_schedule(ctypes.byref(desc), segs, ctypes.c_int64(len(schedule)), _ptr(q), _ptr(k),
+                                     _ptr(v), _ptr(eta), _ptr(beta), _ptr(W1), _ptr(W2), _ptr(W3),
+                                     *[_ptr(m) for m in M], _ptr(out), _ptr(workspace),
+                                     ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                                     ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return (out, M) if beta is not None else out
 
 
 def timing_enable(on: bool = True):

@@ -24,6 +24,7 @@ struct Plan {
   int BH, d, h;
   bool bf16;
   int esz;
+  int es;             // floats of eta per token (1, or 3 with per-matrix rates)
   int64_t C;          // tokens of the largest chunk (0 when n_kv == 0)
   int64_t cap;        // rows of the applied-hidden buffer
   int nsplit;         // split-K ways of the gradient contraction
@@ -46,6 +47,7 @@ int check_desc(const lact_desc* d) {
   if (d->use_muon != 0 && d->use_muon != 1) return LACT_EINVAL;
   if (d->ns_steps < 0 || d->ns_steps > 16) return LACT_EINVAL;
   if (d->io_dtype != LACT_IO_BF16 && d->io_dtype != LACT_IO_FP32) return LACT_EINVAL;
+  if (d->eta_per_matrix != 0 && d->eta_per_matrix != 1) return LACT_EINVAL;
   if (d->d < 1 || d->h < 1) return LACT_EINVAL;
   if (d->d % 8 || d->h % 8 || d->d > kMaxDim || d->h > kMaxDim) return LACT_EUNSUPPORTED;
   // 16-bit MFMA tiles take K in whole steps of 32 along d and h
@@ -62,6 +64,7 @@ Plan make_plan(const lact_desc* dsc) {
   p.h = dsc->h;
   p.bf16 = dsc->io_dtype == LACT_IO_BF16;
   p.esz = p.bf16 ? 2 : 4;
+  p.es = dsc->eta_per_matrix ? 3 : 1;
   p.C = std::min<int64_t>(dsc->chunk, dsc->n_kv);
   const int64_t tail = dsc->n_q - dsc->n_kv;
   // The applied-hidden buffer holds one chunk plus (bounded) tail rows so that
@@ -394,8 +397,9 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.out2 = c.ws + p.off_upd[1];
     g.out3 = c.ws + p.off_upd[2];
     g.out_inst = p.C * p.h;
-    g.eta = c.eta + s0;
-    g.eta_inst = c.dsc->n_kv;
+    g.eta = c.eta + s0 * p.es;
+    g.eta_inst = c.dsc->n_kv * p.es;
+    g.eta_stride = p.es;
   }
   if (apply_too) {
     FwdSeg& g = f.seg[ns++];
@@ -505,11 +509,12 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   return timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] { return launch_update(u, p.bf16, c.s); });
 }
 
-// Both entry points: validation, operand copies and the chunk schedule.
-// beta == nullptr: plain updates; otherwise momentum with state M.
-int run_forward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
-                const float* beta, float* W1, float* W2, float* W3, float* const M[3], void* o,
-                void* workspace, size_t workspace_bytes, void* stream) {
+// Validation and context of every entry point (no HIP call); beta == nullptr
+// and M == nullptr: plain updates; M: momentum with state M (beta required
+// when there are key tokens).
+int setup(Ctx& c, const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+          const float* beta, float* W1, float* W2, float* W3, float* const M[3], void* o, void* workspace,
+          size_t workspace_bytes, void* stream) {
   int rc = check_desc(desc);
   if (rc) return rc;
   const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
@@ -522,7 +527,7 @@ int run_forward(const lact_desc* desc, const void* q, const void* k, const void*
   if (any_kv && (misaligned(k) || misaligned(v) || ((uintptr_t)eta & 3))) return LACT_EALIGN;
   if (M && (misaligned(M[0]) || misaligned(M[1]) || misaligned(M[2]))) return LACT_EALIGN;
   if (M && any_kv && ((uintptr_t)beta & 3)) return LACT_EALIGN;
-  Ctx c{};
+  c = Ctx{};
   c.dsc = desc;
   c.p = make_plan(desc);
   if (!workspace || workspace_bytes < c.p.total) return LACT_EWORKSPACE;
@@ -541,37 +546,62 @@ int run_forward(const lact_desc* desc, const void* q, const void* k, const void*
     c.beta = beta;
     for (int j = 0; j < 3; ++j) c.M[j] = M[j];
   }
+  return LACT_OK;
+}
+
+// Operand copies of the initial fast weights (bf16 I/O) or the fp32 state.
+int prepare_weights(Ctx& c) {
   const Plan& p = c.p;
   const int64_t dh = (int64_t)p.d * p.h;
   if (p.bf16) {
-    const float* Wf[3] = {W1, W2, W3};
+    const float* Wf[3] = {c.W[0], c.W[1], c.W[2]};
     void* Wb[3] = {c.ws + p.off_wb[0], c.ws + p.off_wb[1], c.ws + p.off_wb[2]};
-    rc = timed(LACT_KCLASS_PREP, 0.0, c.s, [&] { return launch_prep(Wf, Wb, p.BH, p.d, p.h, c.s); });
+    const int rc = timed(LACT_KCLASS_PREP, 0.0, c.s, [&] { return launch_prep(Wf, Wb, p.BH, p.d, p.h, c.s); });
     if (rc) return rc;
     c.wop[0] = op(Wb[0], p.d, dh);
     c.wop[1] = op(Wb[1], p.h, dh);
     c.wop[2] = op(Wb[2], p.d, dh);
   } else {
-    c.wop[0] = op(W1, p.d, dh);
-    c.wop[1] = op(W2, p.h, dh);
-    c.wop[2] = op(W3, p.d, dh);
+    c.wop[0] = op(c.W[0], p.d, dh);
+    c.wop[1] = op(c.W[1], p.h, dh);
+    c.wop[2] = op(c.W[2], p.d, dh);
   }
+  return LACT_OK;
+}
+
+// Momentum factors of `nchunks` chunks of `len` tokens from token t0 (the
+// last bounded by `end`) into slots 0.. of the chunk-mean section.
+int beta_means(Ctx& c, int64_t t0, int64_t len, int64_t end, int nchunks) {
+  BetaArgs ba{};
+  ba.beta = c.beta;
+  ba.n_kv = c.dsc->n_kv;
+  ba.chunk = len;
+  ba.t0 = t0;
+  ba.end = end;
+  ba.nchunks = nchunks;
+  ba.BH = c.p.BH;
+  ba.bbar = reinterpret_cast<float*>(c.ws + c.p.off_bbar);
+  ba.stride = kBetaBatch;
+  return timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] { return launch_beta_mean(ba, c.s); });
+}
+
+// lact_forward and lact_forward_momentum: uniform chunks of desc->chunk tokens
+// in desc->order, then the apply-only tail.
+int run_forward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                const float* beta, float* W1, float* W2, float* W3, float* const M[3], void* o,
+                void* workspace, size_t workspace_bytes, void* stream) {
+  Ctx c;
+  int rc = setup(c, desc, q, k, v, eta, beta, W1, W2, W3, M, o, workspace, workspace_bytes, stream);
+  if (rc) return rc;
+  rc = prepare_weights(c);
+  if (rc) return rc;
   const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk;
   const int64_t nchunks = cdiv(n_kv, C);
   for (int64_t s0 = 0; s0 < n_kv; s0 += C) {
     const int64_t s1 = std::min(n_kv, s0 + C);
     c.chunk_idx = s0 / C;
     if (c.beta && c.chunk_idx % kBetaBatch == 0) {
-      BetaArgs ba{};
-      ba.beta = c.beta;
-      ba.n_kv = n_kv;
-      ba.chunk = C;
-      ba.c0 = c.chunk_idx;
-      ba.nchunks = (int)std::min<int64_t>(kBetaBatch, nchunks - c.chunk_idx);
-      ba.BH = p.BH;
-      ba.bbar = reinterpret_cast<float*>(c.ws + p.off_bbar);
-      ba.stride = kBetaBatch;
-      rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] { return launch_beta_mean(ba, c.s); });
+      rc = beta_means(c, s0, C, n_kv, (int)std::min<int64_t>(kBetaBatch, nchunks - c.chunk_idx));
       if (rc) return rc;
     }
     if (desc->order == LACT_APPLY_THEN_UPDATE) {
@@ -584,6 +614,78 @@ int run_forward(const lact_desc* desc, const void* q, const void* k, const void*
   }
   if (desc->order == LACT_APPLY_THEN_UPDATE || n_kv == 0) rc = apply_rows(c, n_kv, n_q);
   return rc;
+}
+
+bool is_update(int mode) { return mode != LACT_SEG_APPLY_ONLY; }
+bool is_apply(int mode) { return mode != LACT_SEG_UPDATE_ONLY; }
+
+int check_segments(const lact_desc* desc, const lact_segment* segs, int64_t nseg) {
+  if (nseg < 0 || (nseg > 0 && !segs)) return LACT_EINVAL;
+  for (int64_t i = 0; i < nseg; ++i) {
+    const lact_segment& g = segs[i];
+    if (g.mode < LACT_SEG_APPLY_THEN_UPDATE || g.mode > LACT_SEG_APPLY_ONLY || g.reserved != 0) return LACT_EINVAL;
+    if (g.begin < 0 || g.end <= g.begin) return LACT_EINVAL;
+    if (is_update(g.mode) && (g.end > desc->n_kv || g.end - g.begin > desc->chunk)) return LACT_EINVAL;
+    if (is_apply(g.mode) && g.end > desc->n_q) return LACT_EINVAL;
+  }
+  return LACT_OK;
+}
+
+// lact_forward_schedule: caller-given segments; rows that no apply segment
+// covers are zeroed first.
+int run_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, const void* q, const void* k,
+                 const void* v, const float* eta, const float* beta, float* W1, float* W2, float* W3,
+                 float* const M[3], void* o, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  rc = check_segments(desc, segs, nseg);
+  if (rc) return rc;
+  Ctx c;
+  rc = setup(c, desc, q, k, v, eta, beta, W1, W2, W3, M, o, workspace, workspace_bytes, stream);
+  if (rc) return rc;
+  const Plan& p = c.p;
+  std::vector<std::pair<int64_t, int64_t>> cover;
+  for (int64_t i = 0; i < nseg; ++i)
+    if (is_apply(segs[i].mode)) cover.emplace_back(segs[i].begin, segs[i].end);
+  std::sort(cover.begin(), cover.end());
+  int64_t at = 0;
+  const int64_t row_bytes = (int64_t)p.d * p.esz;
+  for (size_t i = 0; i <= cover.size(); ++i) {
+    const int64_t b = i < cover.size() ? cover[i].first : desc->n_q;
+    if (b > at) {
+      const int64_t e = b;
+      rc = timed(LACT_KCLASS_PREP, 0.0, c.s,
+                 [&] { return launch_zero_rows(c.o, p.BH, row_bytes, desc->n_q, at, e, c.s); });
+      if (rc) return rc;
+    }
+    if (i < cover.size()) at = std::max(at, cover[i].second);
+  }
+  rc = prepare_weights(c);
+  if (rc) return rc;
+  c.chunk_idx = 0;
+  for (int64_t i = 0; i < nseg; ++i) {
+    const lact_segment& g = segs[i];
+    if (c.beta && is_update(g.mode)) {
+      rc = beta_means(c, g.begin, g.end - g.begin, g.end, 1);
+      if (rc) return rc;
+    }
+    switch (g.mode) {
+      case LACT_SEG_APPLY_THEN_UPDATE:
+        rc = update_chunk(c, g.begin, g.end, true);
+        break;
+      case LACT_SEG_UPDATE_THEN_APPLY:
+        rc = update_chunk(c, g.begin, g.end, false);
+        if (!rc) rc = apply_rows(c, g.begin, g.end);
+        break;
+      case LACT_SEG_UPDATE_ONLY:
+        rc = update_chunk(c, g.begin, g.end, false);
+        break;
+      default:
+        rc = apply_rows(c, g.begin, g.end);
+    }
+    if (rc) return rc;
+  }
+  return LACT_OK;
 }
 
 }  // namespace
@@ -607,6 +709,15 @@ int lact_forward(const lact_desc* desc, const void* q, const void* k, const void
                  void* stream) {
   return run_forward(desc, q, k, v, eta, nullptr, W1, W2, W3, nullptr, o, workspace, workspace_bytes,
                      stream);
+}
+
+int lact_forward_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, const void* q,
+                          const void* k, const void* v, const float* eta, const float* beta, float* W1, float* W2,
+                          float* W3, float* M1, float* M2, float* M3, void* o, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  float* const M[3] = {M1, M2, M3};
+  return run_schedule(desc, segs, nseg, q, k, v, eta, beta, W1, W2, W3, M1 ? M : nullptr, o, workspace,
+                      workspace_bytes, stream);
 }
 
 int lact_forward_momentum(const lact_desc* desc, const void* q, const void* k, const void* v,

@@ -33,8 +33,9 @@ struct FwdSeg {
   void* out2;
   void* out3;
   int64_t out_inst;     // elements between instances of each output
-  const float* eta;     // UPDATE: per-token learning rate of token row 0
-  int64_t eta_inst;
+  const float* eta;     // UPDATE: learning rate(s) of token row 0
+  int64_t eta_inst;     // floats between instances
+  int eta_stride;       // floats per token: 1 (one rate) or 3 (lr1, lr2, lr3 for W1, W2, W3)
 };
 
 struct FwdArgs {
@@ -136,12 +137,13 @@ struct NsPrepArgs {
 };
 
 // Chunk means of the per-token momentum factor: for chunks c in [0, nchunks),
-// bbar[i * stride + c] = mean of beta[i * n_kv + t] over t in chunk c0 + c.
+// bbar[i * stride + c] = mean of beta[i * n_kv + t] over t in
+// [t0 + c * chunk, min(t0 + (c + 1) * chunk, end)).
 constexpr int kBetaBatch = 32;   // chunks per launch (bbar holds BH * kBetaBatch)
 struct BetaArgs {
   const float* beta;    // [BH][n_kv]
   int64_t n_kv, chunk;
-  int64_t c0;           // first chunk of this launch
+  int64_t t0, end;      // first token of chunk 0; bound of the last chunk
   int nchunks;          // <= kBetaBatch
   int BH;
   float* bbar;
@@ -185,6 +187,10 @@ hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s);
 hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s);
 hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s);
 hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s);
+// Zero rows [r0, r1) of every instance of an output of `rows` rows of row_bytes
+// (a multiple of 16) each.
+hipError_t launch_zero_rows(void* out, int BH, int64_t row_bytes, int64_t rows, int64_t r0, int64_t r1,
+                            hipStream_t s);
 constexpr int kNsBlockElems = 4096;
 
 }  // namespace lact

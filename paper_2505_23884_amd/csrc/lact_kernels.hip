@@ -800,19 +800,22 @@ __device__ __forceinline__ void stage_flush(const uint8_t* buf, __bf16* out, int
 
 // Key-forward epilogue: from Z1, Z3 and D = W2^T v (hidden-major tiles) write
 // eta*hidden, eta*dz1 and eta*dz3 token-major, four hidden units per store.
+// With per-matrix rates (lr1, lr2, lr3) per token, hidden (the W2 gradient)
+// takes lr2, dz1 (W1) lr1 and dz3 (W3) lr3 (Alg. 1, update).
 template <typename T, class K>
 __device__ __forceinline__ void update_epilogue(const f32x16_t (&z1a)[K::MI][K::NI], const f32x16_t (&z3a)[K::MI][K::NI],
                                                 const f32x16_t (&dda)[K::MI][K::NI], const FwdSeg& sg, int inst,
                                                 int64_t j0, int64_t i0, int64_t hrows, int64_t ntok, int h) {
   const int lane = threadIdx.x & 63;
   const int64_t ob = inst * sg.out_inst;
-  const float* eta = sg.eta + inst * sg.eta_inst + i0;
+  const int es = sg.eta_stride, o2 = es > 1 ? 1 : 0;
+  const float* eta = sg.eta + inst * sg.eta_inst + i0 * es;
   const int hrow0 = wave_m<K>() * 32 * K::MI + ((lane >> 5) << 2);
 #pragma unroll
   for (int ni = 0; ni < K::NI; ++ni) {
     const int tok = acc_col<K>(ni);
     if (tok >= ntok) continue;
-    const float et = eta[tok];
+    const float e1 = eta[tok * es], e2 = eta[tok * es + o2], e3 = eta[tok * es + 2 * o2];
 #pragma unroll
     for (int mi = 0; mi < K::MI; ++mi)
 #pragma unroll
@@ -826,10 +829,9 @@ __device__ __forceinline__ void update_epilogue(const f32x16_t (&z1a)[K::MI][K::
           const float z1 = z1a[mi][ni][r], z3 = z3a[mi][ni][r], dh = dda[mi][ni][r];
           const float s = sigmoidf_fast(z1);
           const float a = z1 * s;                     // SiLU(z1)
-          const float ed = et * dh;                   // eta_i * (W2^T v_i)_j
-          vh[e] = et * a * z3;                        // eta * hidden
-          vg[e] = ed * z3 * s * (1.0f + z1 * (1.0f - s));   // eta * dz1
-          vb[e] = ed * a;                             // eta * dz3
+          vh[e] = e2 * a * z3;                        // eta * hidden
+          vg[e] = e1 * dh * z3 * s * (1.0f + z1 * (1.0f - s));   // eta * dz1
+          vb[e] = e3 * dh * a;                        // eta * dz3
         }
         const int64_t idx = ob + (i0 + tok) * h + j0 + hid;
         st4<T>(sg.out1, idx, vh[0], vh[1], vh[2], vh[3]);
@@ -851,13 +853,17 @@ __device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::
   uint8_t* buf0 = smem;
   uint8_t* buf1 = smem + R * C * 2;
   const int lane = threadIdx.x & 63;
-  const float* eta = sg.eta + inst * sg.eta_inst + i0;
+  const int es = sg.eta_stride, o2 = es > 1 ? 1 : 0;
+  const float* eta = sg.eta + inst * sg.eta_inst + i0 * es;
   const int hrow0 = wave_m<K>() * 32 * K::MI + ((lane >> 5) << 2);
-  float et[K::NI];
+  float e1[K::NI], e2[K::NI], e3[K::NI];   // rates of dz1 (W1), hidden (W2), dz3 (W3)
 #pragma unroll
   for (int ni = 0; ni < K::NI; ++ni) {
     const int tok = acc_col<K>(ni);
-    et[ni] = tok < ntok ? eta[tok] : 0.0f;
+    const bool in = tok < ntok;
+    e1[ni] = in ? eta[tok * es] : 0.0f;
+    e2[ni] = in ? eta[tok * es + o2] : 0.0f;
+    e3[ni] = in ? eta[tok * es + 2 * o2] : 0.0f;
   }
 #pragma unroll
   for (int ni = 0; ni < K::NI; ++ni)
@@ -871,9 +877,8 @@ __device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::
           const int r = 4 * g + e;
           const float z1 = z1a[mi][ni][r], z3 = z3a[mi][ni][r];
           const float s = sigmoidf_fast(z1);
-          const float ed = et[ni] * dda[mi][ni][r];
-          vh[e] = et[ni] * z1 * s * z3;
-          vg[e] = ed * z3 * s * (1.0f + z1 * (1.0f - s));
+          vh[e] = e2[ni] * z1 * s * z3;
+          vg[e] = e1[ni] * dda[mi][ni][r] * z3 * s * (1.0f + z1 * (1.0f - s));
         }
         const int tok = acc_col<K>(ni), row = hrow0 + mi * 32 + 8 * g;
         stage_put<R>(buf0, tok, row, vh[0], vh[1], vh[2], vh[3]);
@@ -895,7 +900,7 @@ __device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * g + e;
           const float z1 = z1a[mi][ni][r];
-          vb[e] = et[ni] * dda[mi][ni][r] * z1 * sigmoidf_fast(z1);
+          vb[e] = e3[ni] * dda[mi][ni][r] * z1 * sigmoidf_fast(z1);
         }
         stage_put<R>(buf0, acc_col<K>(ni), hrow0 + mi * 32 + 8 * g, vb[0], vb[1], vb[2], vb[3]);
       }
@@ -1637,8 +1642,8 @@ __global__ __launch_bounds__(256) void k_beta_mean(const BetaArgs a) {
   __shared__ double red[4];
   const int inst = blockIdx.x / a.nchunks;
   const int c = blockIdx.x - inst * a.nchunks;
-  const int64_t t0 = (a.c0 + c) * a.chunk;
-  const int64_t t1 = t0 + a.chunk < a.n_kv ? t0 + a.chunk : a.n_kv;
+  const int64_t t0 = a.t0 + c * a.chunk;
+  const int64_t t1 = t0 + a.chunk < a.end ? t0 + a.chunk : a.end;
   const float* b = a.beta + (int64_t)inst * a.n_kv;
   double s = 0.0;
   for (int64_t t = t0 + threadIdx.x; t < t1; t += 256) s += (double)b[t];
@@ -1649,6 +1654,17 @@ __global__ __launch_bounds__(256) void k_beta_mean(const BetaArgs a) {
   if (threadIdx.x == 0) {
     const double tot = red[0] + red[1] + red[2] + red[3];
     a.bbar[(int64_t)inst * a.stride + c] = (float)(tot / (double)(t1 - t0));
+  }
+}
+
+// Rows [r0, r1) of every instance of a row-major [BH, n, d] output set to zero
+// (tokens that no apply segment of a schedule covers): nvec 16-byte vectors
+// per instance, grid-stride over all instances.
+__global__ __launch_bounds__(256) void k_zero_rows(uint8_t* out, int64_t inst_bytes, int64_t off, int64_t nvec,
+                                                   int64_t total) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t inst = i / nvec, j = i - inst * nvec;
+    reinterpret_cast<u32x4_t*>(out + inst * inst_bytes + off)[j] = u32x4_t{0u, 0u, 0u, 0u};
   }
 }
 
@@ -1708,6 +1724,16 @@ hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, 
   if (blocks <= 0) return hipSuccess;
   if (fp16) k_ns_scale<_Float16><<<(unsigned)blocks, 256, 0, s>>>(a, Yb, eps);
   else k_ns_scale<float><<<(unsigned)blocks, 256, 0, s>>>(a, Yb, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_rows(void* out, int BH, int64_t row_bytes, int64_t rows, int64_t r0, int64_t r1,
+                            hipStream_t s) {
+  const int64_t nvec = (r1 - r0) * row_bytes / 16, total = nvec * BH;
+  if (nvec <= 0 || BH <= 0) return hipSuccess;
+  const int64_t need = (total + 255) / 256, blocks = need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20);
+  k_zero_rows<<<(unsigned)blocks, 256, 0, s>>>(reinterpret_cast<uint8_t*>(out), rows * row_bytes, r0 * row_bytes,
+                                               nvec, total);
   return hipGetLastError();
 }
 

@@ -22,7 +22,7 @@ def _declared():
 def test_library_exports_every_declared_symbol():
     L = P.lib()
     names = _declared()
-    assert {"lact_forward", "lact_forward_momentum", "lact_workspace_bytes"} <= set(names)
+    assert {"lact_forward", "lact_forward_momentum", "lact_forward_schedule", "lact_workspace_bytes"} <= set(names)
     for n in names:
         assert hasattr(L, n), n
 
@@ -116,6 +116,43 @@ def test_momentum_argument_errors_before_any_hip_call():
     # no key tokens: beta may be NULL, the momentum may not
     d0 = make_desc(**dict(GOOD, n_kv=0))
     assert _fwd_mom(d0, m1=0, beta=0) == -1
+
+
+def _fwd_sched(desc, segs, m1=0, beta=0, nbytes=None, ws=0x10000, q=0x1000):
+    from paper_2505_23884_amd.binding import LactSegment
+    L = P.lib()
+    arr = (LactSegment * max(len(segs), 1))(*[LactSegment(m, r, b, e) for m, r, b, e in segs])
+    if nbytes is None:
+        nbytes = P.workspace_bytes(desc) if P.check_desc(desc) == 0 else 0
+    vp = ctypes.c_void_p
+    m = [vp(m1), vp(0xB000 if m1 else 0), vp(0xC000 if m1 else 0)]
+    return L.lact_forward_schedule(ctypes.byref(desc), arr, ctypes.c_int64(len(segs)), vp(q), vp(0x2000),
+                                   vp(0x3000), vp(0x4000), vp(beta), vp(0x5000), vp(0x6000), vp(0x7000), *m,
+                                   vp(0x8000), vp(ws), ctypes.c_size_t(nbytes), vp(0))
+
+
+def test_schedule_segment_errors_before_any_hip_call():
+    d = make_desc(**dict(GOOD, n_kv=256, n_q=300, chunk=64))
+    assert _fwd_sched(d, [(4, 0, 0, 8)]) == -1            # unknown mode
+    assert _fwd_sched(d, [(0, 1, 0, 8)]) == -1            # reserved field set
+    assert _fwd_sched(d, [(3, 5, 5, 0)]) == -1            # empty range
+    assert _fwd_sched(d, [(3, 0, -1, 8)]) == -1           # negative begin
+    assert _fwd_sched(d, [(2, 0, 200, 265)]) == -1        # update past n_kv
+    assert _fwd_sched(d, [(2, 0, 0, 65)]) == -1           # update longer than chunk
+    assert _fwd_sched(d, [(3, 0, 0, 301)]) == -1          # apply past n_q
+    assert _fwd_sched(d, [(1, 0, 0, 64)], m1=0xA000) == -1   # momentum without beta
+    assert _fwd_sched(d, [(1, 0, 0, 64)], ws=0) == -3     # segments fine, workspace missing
+    assert _fwd_sched(d, [(3, 0, 0, 300)], q=0x1008, ws=0x10000) == -2
+    L = P.lib()
+    assert L.lact_forward_schedule(ctypes.byref(d), None, ctypes.c_int64(2), *([ctypes.c_void_p(0x1000)] * 13),
+                                   ctypes.c_size_t(1 << 30), ctypes.c_void_p(0)) == -1   # NULL segments
+
+
+def test_per_matrix_rate_flag_is_validated():
+    assert P.check_desc(make_desc(**dict(GOOD, eta_per_matrix=1))) == 0
+    bad = make_desc(**GOOD)
+    bad.eta_per_matrix = 2
+    assert P.check_desc(bad) == -1
 
 
 def test_timing_api_without_launches():

@@ -447,3 +447,141 @@ def test_lm32k_muon_momentum_teacher_forced_sampled():
     cfg = CONFIGS["lm32k_muon_mom"]
     x = make_inputs(cfg, 0)
     teacher_forced(cfg, x, [0, 9], max_chunks=6)
+
+
+# ----------------------------------------------------------------------------- per-matrix rates
+# eta [.., n_kv, 3] = (lr1, lr2, lr3) weights the W1, W2, W3 gradients (Alg. 1).
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_per_matrix_rates_bf16_ragged(order):
+    cfg = CONFIGS["lm32k"].with_(name="lr3", B=1, H=2, d=128, h=256, n_kv=700, n_q=760, chunk=256,
+                                 order=order, lr3=1)
+    x = make_inputs(cfg, 31)
+    assert x["eta"].shape == (2, 700, 3)
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
+def test_per_matrix_rates_fp32_small():
+    cfg = CONFIGS["tiny_fp32"].with_(name="lr3_fp32", B=2, H=1, d=40, h=24, n_kv=300, n_q=333, chunk=100,
+                                     lr3=1)
+    x = make_inputs(cfg, 32)
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
+def test_per_matrix_rates_with_equal_columns_match_single_rate_bitwise():
+    cfg = CONFIGS["lm32k"].with_(name="lr3_eq", B=1, H=2, d=128, h=128, n_kv=600, n_q=640, chunk=256)
+    x = make_inputs(cfg, 33)
+    x3 = dict(x, eta=np.ascontiguousarray(np.stack([x["eta"]] * 3, axis=-1)))
+    o1, W1 = run_gpu(cfg, x)
+    o3, W3 = run_gpu(cfg, x3)
+    assert np.array_equal(o1, o3) and all(np.array_equal(a, b) for a, b in zip(W1, W3))
+
+
+def test_per_matrix_rates_muon_teacher_forced():
+    cfg = CONFIGS["lm32k_muon"].with_(name="lr3_muon", B=1, H=2, d=128, h=256, n_kv=512, n_q=512,
+                                      chunk=256, lr3=1)
+    x = make_inputs(cfg, 34)
+    teacher_forced(cfg, x, [0, 1])
+
+
+# ----------------------------------------------------------------------------- schedule
+# lact_forward_schedule: (mode, begin, end) segments in list order (Alg. 1).
+
+
+def run_gpu_schedule(cfg, x, sched, momentum=False):
+    print(f"[gpu] schedule {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} n_kv={cfg.n_kv} "
+          f"n_q={cfg.n_q} segments={len(sched)} muon={cfg.use_muon} momentum={momentum}", flush=True)
+    n = len(x["q"])
+    B, H = (cfg.B, cfg.H) if n == cfg.BH else (n, 1)
+    sh = lambda a: a.reshape(B, H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    W = [to_dev(sh(x[w]), cfg, torch.float32) for w in ("W1", "W2", "W3")]
+    kw = {}
+    if momentum:
+        kw["beta"] = to_dev(sh(x["beta"]), cfg, torch.float32)
+    r = P.forward_schedule(q, k, v, eta, *W, sched, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps, **kw)
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    if momentum:
+        return f(r[0]), [f(w) for w in W], [f(m) for m in r[1]]
+    return f(r), [f(w) for w in W]
+
+
+def run_oracle_schedule(cfg, x, sched, momentum=False, instances=None):
+    return O.lact_forward_schedule(x["q"], x["k"], x["v"], x["eta"], x["W1"], x["W2"], x["W3"], sched,
+                                   use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
+                                   beta=x["beta"] if momentum else None, instances=instances)
+
+
+def _video_tf_schedule(C, n_clean):
+    sched, t = [], 0
+    for i in range(n_clean + 1):
+        sched.append(("apply_only", t, t + C))
+        t += C
+        if i < n_clean:
+            sched.append(("update_then_apply", t, t + C))
+            t += C
+    return sched, t
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_uniform_schedule_matches_chunk_loop_bitwise(order):
+    cfg = CONFIGS["lm32k"].with_(name="sched_uniform", B=1, H=2, d=128, h=256, n_kv=700, n_q=760,
+                                 chunk=256, order=order)
+    x = make_inputs(cfg, 35)
+    sched = [(order, s, min(700, s + 256)) for s in range(0, 700, 256)] + [("apply_only", 700, 760)]
+    o1, W1 = run_gpu(cfg, x)
+    o2, W2 = run_gpu_schedule(cfg, x, sched)
+    assert np.array_equal(o1, o2) and all(np.array_equal(a, b) for a, b in zip(W1, W2))
+
+
+def test_video_teacher_forcing_schedule_bf16():
+    # interleaved noisy and clean frame chunks (§3.3): noisy chunks are applied
+    # only, clean chunks update then apply
+    sched, n = _video_tf_schedule(312, 3)
+    cfg = CONFIGS["video"].with_(name="video_tf", B=1, H=2, n_kv=n, n_q=n, chunk=312, use_muon=0)
+    x = make_inputs(cfg, 36)
+    check(cfg, x, run_gpu_schedule(cfg, x, sched), run_oracle_schedule(cfg, x, sched))
+
+
+@pytest.mark.parametrize("io", ["bf16", "fp32"])
+def test_mixed_schedule_with_gaps_overlaps_and_zero_rows(io):
+    base = CONFIGS["lm32k"] if io == "bf16" else CONFIGS["tiny_fp32"]
+    cfg = base.with_(name="sched_mixed_" + io, B=1, H=2, d=64, h=96, n_kv=500, n_q=620, chunk=200)
+    x = make_inputs(cfg, 37)
+    sched = [("update_only", 0, 150), ("apply_only", 40, 300), ("apply_then_update", 150, 333),
+             ("update_then_apply", 333, 500), ("apply_only", 520, 600), ("update_only", 10, 77),
+             ("apply_only", 250, 270)]
+    got = run_gpu_schedule(cfg, x, sched)
+    ref = run_oracle_schedule(cfg, x, sched)
+    assert not got[0][:, :40].any() and not got[0][:, 500:520].any() and not got[0][:, 600:].any()
+    check(cfg, x, got, ref)
+
+
+def test_nvs_style_schedule_update_views_then_apply_targets():
+    cfg = CONFIGS["nvs256k"].with_(name="nvs_sched", n_kv=8192, n_q=8192 + 2048, chunk=8192)
+    x = make_inputs(cfg, 38)
+    sched = [("update_only", 0, 8192), ("apply_only", 8192, 8192 + 2048)]
+    check(cfg, x, run_gpu_schedule(cfg, x, sched), run_oracle_schedule(cfg, x, sched))
+
+
+@pytest.mark.parametrize("io", ["bf16", "fp32"])
+def test_schedule_with_momentum_and_per_matrix_rates(io):
+    base = CONFIGS["lm32k"] if io == "bf16" else CONFIGS["tiny_fp32"]
+    cfg = base.with_(name="sched_mom_" + io, B=1, H=2, d=64, h=128, n_kv=600, n_q=600, chunk=256,
+                     momentum=1, lr3=1)
+    x = make_inputs(cfg, 39)
+    sched = [("update_only", 0, 256), ("apply_then_update", 256, 400), ("update_then_apply", 400, 600),
+             ("apply_only", 0, 256)]
+    got = run_gpu_schedule(cfg, x, sched, momentum=True)
+    ref = run_oracle_schedule(cfg, x, sched, momentum=True)
+    check_momentum(cfg, x, got, ref)
+
+
+def test_schedule_muon_two_updates():
+    cfg = CONFIGS["video"].with_(name="sched_muon", B=1, H=2, d=128, h=256, n_kv=512, n_q=600, chunk=256)
+    x = make_inputs(cfg, 40)
+    sched = [("apply_then_update", 0, 256), ("update_only", 256, 512), ("apply_only", 256, 600)]
+    check(cfg, x, run_gpu_schedule(cfg, x, sched), run_oracle_schedule(cfg, x, sched))

@@ -140,12 +140,35 @@ def measured_traffic(cfg_name, kernel):
     return k["traffic_bytes"] if k else None
 
 
+def workload_flops(cfg, BH=None):
+    """Algorithmic FLOPs of one step (App. A, FLOPs calculation): 12*d*h per
+    updated token and 6*d*h per applied token per head, plus per update and
+    matrix 3*steps*(4*m^2*n + 2*m^3) with Muon (m <= n the sides)."""
+    BH = cfg.BH if BH is None else BH
+    dh = float(cfg.d) * cfg.h
+    m, n = min(cfg.d, cfg.h), max(cfg.d, cfg.h)
+    ns = 3.0 * cfg.ns_steps * (4.0 * m * m * n + 2.0 * m ** 3) if cfg.use_muon else 0.0
+    if cfg.schedule:
+        from lact_synth import make_schedule
+        f = 0.0
+        for mode, b, e in make_schedule(cfg):
+            if mode != "apply_only":
+                f += 12.0 * dh * (e - b) + ns
+            if mode != "update_only":
+                f += 6.0 * dh * (e - b)
+        return BH * f
+    return BH * (12.0 * dh * cfg.n_kv + 6.0 * dh * cfg.n_q + cfg.n_chunks * ns)
+
+
 def describe(cfg):
     order = "apply-then-update" if cfg.order == 0 else "update-then-apply"
     muon = f", Muon {cfg.ns_steps} NS steps" if cfg.use_muon else ""
     mom = ", momentum (chunk-mean beta)" if cfg.momentum else ""
+    lr3 = ", per-matrix rates" if cfg.lr3 else ""
+    if cfg.schedule:
+        order = f"schedule {cfg.schedule}"
     return (f"{cfg.name}: B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} n_kv={cfg.n_kv} n_q={cfg.n_q} "
-            f"chunk={cfg.chunk} {order}{muon}{mom}, io {cfg.io}, fp32 state")
+            f"chunk={cfg.chunk} {order}{muon}{mom}{lr3}, io {cfg.io}, fp32 state")
 
 
 def cpu_baseline(cfg, min_seconds):
@@ -159,7 +182,7 @@ def cpu_baseline(cfg, min_seconds):
     from lact_synth import make_inputs
     from oracle import lact_oracle as O
 
-    one = O.layer_flops(1, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.n_chunks, bool(cfg.use_muon), cfg.ns_steps)
+    one = workload_flops(cfg, BH=1)
     scfg, note = cfg, ""
     if one > 4e12:   # roughly 30 s or more of fp64 NumPy for one instance
         n = 16384
@@ -171,7 +194,12 @@ def cpu_baseline(cfg, min_seconds):
     while done < scfg.BH and dt < min_seconds:
         x = make_inputs(scfg, 0, heads=[done])
         t0 = time.perf_counter()
-        if scfg.momentum:
+        if scfg.schedule:
+            from lact_synth import make_schedule
+            O.lact_forward_schedule(x["q"], x["k"], x["v"], x["eta"], x["W1"], x["W2"], x["W3"],
+                                    make_schedule(scfg), use_muon=bool(scfg.use_muon), ns_steps=scfg.ns_steps,
+                                    beta=x.get("beta"))
+        elif scfg.momentum:
             O.lact_forward_momentum(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["W1"], x["W2"], x["W3"],
                                     chunk=scfg.chunk, order=scfg.order, use_muon=bool(scfg.use_muon),
                                     ns_steps=scfg.ns_steps)
@@ -180,8 +208,7 @@ def cpu_baseline(cfg, min_seconds):
                            order=scfg.order, use_muon=bool(scfg.use_muon), ns_steps=scfg.ns_steps)
         dt += time.perf_counter() - t0
         done += 1
-    fl = done * O.layer_flops(1, scfg.d, scfg.h, scfg.n_kv, scfg.n_q, scfg.n_chunks, bool(scfg.use_muon),
-                              scfg.ns_steps)
+    fl = done * workload_flops(scfg, BH=1)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{done} of {scfg.BH} (b,h) instances, all {scfg.n_chunks} chunks each "
@@ -220,12 +247,22 @@ def main():
     del x
     out = torch.empty_like(q)
     desc = P.binding.make_desc(cfg.B, cfg.H, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.chunk, cfg.order,
-                               cfg.use_muon, cfg.ns_steps, P.IO_BF16 if cfg.io == "bf16" else P.IO_FP32)
+                               cfg.use_muon, cfg.ns_steps, P.IO_BF16 if cfg.io == "bf16" else P.IO_FP32,
+                               bool(cfg.lr3))
     ws = torch.empty(P.workspace_bytes(desc), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
 
+    sched = None
+    if cfg.schedule:
+        from lact_synth import make_schedule
+        sched = make_schedule(cfg)
+
     def step():
-        if cfg.momentum:
+        if sched is not None:
+            P.forward_schedule(q, k, v, eta, *W, sched, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
+                               chunk=cfg.chunk, out=out, workspace=ws, stream=stream.cuda_stream,
+                               **({"beta": beta, "M1": M[0], "M2": M[1], "M3": M[2]} if cfg.momentum else {}))
+        elif cfg.momentum:
             P.forward_momentum(q, k, v, eta, beta, *W, *M, chunk=cfg.chunk, order=cfg.order,
                                use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps, out=out, workspace=ws,
                                stream=stream.cuda_stream)
@@ -242,9 +279,7 @@ def main():
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / max(args.steps, 1)
 
-    from oracle.lact_oracle import layer_flops  # FLOP count only (App. A formula)
-    flops = layer_flops(cfg.BH, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.n_chunks, bool(cfg.use_muon),
-                        cfg.ns_steps)
+    flops = workload_flops(cfg)
     tflops = flops / dt / 1e12
     tokens = cfg.B * cfg.n_q
     peak = PEAK_BF16_TFLOPS if cfg.io == "bf16" else PEAK_FP32_MFMA_TFLOPS

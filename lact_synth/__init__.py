@@ -33,7 +33,7 @@ from __future__ import annotations
 import dataclasses
 import numpy as np
 
-__all__ = ["LactConfig", "CONFIGS", "make_inputs", "round_to_bf16", "bf16_bits"]
+__all__ = ["LactConfig", "CONFIGS", "make_inputs", "make_schedule", "round_to_bf16", "bf16_bits"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -52,6 +52,7 @@ class LactConfig:
     io: str               # "bf16" or "fp32"
     momentum: int = 0     # 1: momentum test-time optimizer (inputs carry beta)
     lr3: int = 0          # 1: per-matrix learning rates, eta [B*H, n_kv, 3]
+    schedule: str = ""    # "": uniform chunks in `order`; else a make_schedule() recipe
 
     @property
     def BH(self) -> int:
@@ -75,7 +76,27 @@ CONFIGS = {
     "video": LactConfig("video", 1, 40, 128, 256, 56160, 56160, 3120, 0, 1, 5, "bf16"),
     "lm32k_mom": LactConfig("lm32k_mom", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", 1),
     "lm32k_muon_mom": LactConfig("lm32k_muon_mom", 4, 4, 512, 512, 32768, 32768, 2048, 0, 1, 5, "bf16", 1),
+    "lm32k_lr3": LactConfig("lm32k_lr3", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", lr3=1),
+    # video teacher forcing: 18 clean chunks of 3120 tokens interleaved with 19
+    # noisy ones, [X1n, X1, ..., X18, X19n] (115440 tokens in all)
+    "video_tf": LactConfig("video_tf", 1, 40, 128, 256, 37 * 3120, 37 * 3120, 3120, 0, 1, 5, "bf16",
+                           schedule="video_tf"),
 }
+
+
+def make_schedule(cfg: LactConfig):
+    """Segments (mode, begin, end) of a scheduled workload.
+
+    "video_tf": the strided mask of teacher-forced video diffusion: noisy
+    chunks of `chunk` tokens are applied only, clean ones update then apply,
+    alternating and starting and ending with a noisy chunk.
+    """
+    if cfg.schedule == "video_tf":
+        C = cfg.chunk
+        assert cfg.n_kv % (2 * C) == C, "odd number of chunks"
+        return [("apply_only" if (t // C) % 2 == 0 else "update_then_apply", t, t + C)
+                for t in range(0, cfg.n_kv, C)]
+    raise ValueError(f"unknown schedule {cfg.schedule!r}")
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:

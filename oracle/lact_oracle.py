@@ -20,6 +20,11 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
                    momentum for test-time optimizers; Table 3, Momentum and Muon rows)
 * per-matrix rates one learning rate per token for each of W1, W2, W3 (the
                    lr of shape [b, l, 3] in the update of Alg. 1)
+* prologue         per token and head: q, k, v = SiLU of the projections,
+                   q and k divided by their L2 norm, lr = softplus(raw + bias),
+                   beta = sigmoid(raw); heads moved next to the batch  (Alg. 1, layer)
+* output norm      per-head RMSNorm of o, heads moved back next to the
+                   channels                                          (Alg. 1, layer)
 * schedule         a list of (mode, begin, end) segments, each one of
                    update-then-apply, apply-then-update, update-only or
                    apply-only on its token range (the ttt_config loop of Alg. 1;
@@ -54,6 +59,12 @@ test):
   R9 per-matrix rates: eta of shape [n, 3] holds (lr1, lr2, lr3) per token and
      weights the W1, W2 and W3 gradients respectively; with equal columns it
      is the single-rate gradient of the chunk-gradient eq.
+  R11 prologue/epilogue layouts: the projections arrive as [B, L, 3, H, hd]
+     (q, k, v blocks of heads, the split of Alg. 1), raw rates as
+     [B, L, H, R] (R = 1 or 3), raw momentum logits as [B, L, H]; outputs are
+     [B*H, L, hd] and [B*H, L(, R)]. A zero vector normalises to zero (Alg. 1
+     divides by the norm without an epsilon). The RMSNorm weight is [H, hd]
+     (or none); y = x / sqrt(mean(x^2) + eps) * w, returned as [B, L, H, hd].
   R10 schedule: segments run in list order and each is one update (one
      chunk) over its whole range; output rows of tokens that no apply
      segment covers are zero (Alg. 1 starts o at zero); a token applied by
@@ -69,7 +80,7 @@ __all__ = [
     "NS_COEFFS", "NS_EPS", "sigmoid", "silu", "swiglu_apply", "chunk_gradient",
     "newton_schulz", "weight_update", "update", "momentum_update", "lact_forward_instance",
     "lact_forward", "lact_forward_momentum", "SCHEDULE_MODES", "lact_forward_schedule_instance",
-    "lact_forward_schedule", "layer_flops",
+    "lact_forward_schedule", "softplus", "qkv_prologue", "rmsnorm_out", "layer_flops",
 ]
 
 # Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
@@ -272,6 +283,55 @@ def lact_forward_momentum(q, k, v, eta, beta, W1, W2, W3, M1=None, M2=None, M3=N
         for j, x in enumerate((o, *W, *Mo)):
             res[j].append(x)
     return tuple(np.stack(r) for r in res)
+
+
+def softplus(x):
+    """log(1 + exp(x)), in the overflow-free form max(x, 0) + log1p(exp(-|x|))."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.maximum(x, 0.0) + np.log1p(np.exp(-np.abs(x)))
+
+
+def qkv_prologue(qkv, lr_raw, lr_bias: float, beta_raw=None):
+    """The steps of the layer before the fast-weight path (Alg. 1, layer; R11).
+
+    qkv [B, L, 3, H, hd]: projections; lr_raw [B, L, H, R]; beta_raw [B, L, H]
+    or None. Returns (q, k, v [B*H, L, hd], eta [B*H, L, R] (R = 3) or
+    [B*H, L] (R = 1), beta [B*H, L] or None), float64.
+    """
+    qkv = np.asarray(qkv, dtype=np.float64)
+    B, L, _, H, hd = qkv.shape
+    act = silu(qkv)                                    # qkv = silu(LinearQKV(x))
+    heads = lambda t: np.ascontiguousarray(t.transpose(0, 2, 1, 3).reshape(B * H, L, hd))
+    q, k, v = (heads(act[:, :, j]) for j in range(3))
+
+    def unit(x):
+        n = np.sqrt(np.sum(x * x, axis=-1, keepdims=True))
+        return np.divide(x, n, out=np.zeros_like(x), where=n > 0)
+
+    q, k = unit(q), unit(k)                            # q / ||q||, k / ||k||
+    lr = softplus(np.asarray(lr_raw, dtype=np.float64) + lr_bias)   # [B, L, H, R]
+    R = lr.shape[-1]
+    eta = np.ascontiguousarray(lr.transpose(0, 2, 1, 3).reshape(B * H, L, R))
+    if R == 1:
+        eta = eta[..., 0]
+    beta = None
+    if beta_raw is not None:
+        beta = sigmoid(np.asarray(beta_raw, dtype=np.float64).transpose(0, 2, 1).reshape(B * H, L))
+    return q, k, v, eta, beta
+
+
+def rmsnorm_out(o, B: int, H: int, weight=None, eps: float = 1e-6):
+    """Per-head RMSNorm of the path's output (Alg. 1, layer; R11).
+
+    o [B*H, L, hd] -> y [B, L, H, hd], y = o / sqrt(mean_hd(o^2) + eps) * w[h].
+    """
+    o = np.asarray(o, dtype=np.float64)
+    BH, L, hd = o.shape
+    y = o / np.sqrt(np.mean(o * o, axis=-1, keepdims=True) + eps)
+    y = y.reshape(B, H, L, hd)
+    if weight is not None:
+        y = y * np.asarray(weight, dtype=np.float64)[None, :, None, :]
+    return np.ascontiguousarray(y.transpose(0, 2, 1, 3))
 
 
 SCHEDULE_MODES = ("apply_then_update", "update_then_apply", "update_only", "apply_only")

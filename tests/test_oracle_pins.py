@@ -658,3 +658,60 @@ def test_schedule_with_momentum_and_per_matrix_rates():
     for a, b in zip(Wf + M, Wr + Mr):
         np.testing.assert_array_equal(a, b)
     assert not o[:8].any()
+
+
+# ----------------------------------------------------------------------------- prologue / output norm
+# The steps around the path in Alg. 1 (layer): silu(qkv), q/||q||, k/||k||,
+# softplus(lr + bias), per-head RMSNorm of o.
+
+
+def _raw(seed, B, L, H, hd, R):
+    rng = _rng(seed)
+    return (rng.standard_normal((B, L, 3, H, hd)), rng.standard_normal((B, L, H, R)),
+            rng.standard_normal((B, L, H)))
+
+
+@pytest.mark.parametrize("R", [1, 3])
+def test_prologue_matches_library_ops(R):
+    from einops import rearrange
+    B, L, H, hd = 2, 7, 3, 10
+    qkv, lr, br = _raw(60, B, L, H, hd, R)
+    q, k, v, eta, beta = O.qkv_prologue(qkv, lr, -1.5, br)
+    t = torch.as_tensor(qkv)
+    act = F.silu(t)
+    for j, (got, unit) in enumerate(((q, True), (k, True), (v, False))):
+        ref = rearrange(act[:, :, j], "b l h d -> (b h) l d")
+        if unit:
+            ref = F.normalize(ref, dim=-1, eps=0.0)
+        np.testing.assert_allclose(got, ref.numpy(), rtol=1e-13, atol=1e-15)
+    ref_eta = rearrange(F.softplus(torch.as_tensor(lr) - 1.5), "b l h r -> (b h) l r")
+    np.testing.assert_allclose(eta, ref_eta.numpy()[..., 0] if R == 1 else ref_eta.numpy(), rtol=1e-13)
+    np.testing.assert_allclose(beta, rearrange(torch.sigmoid(torch.as_tensor(br)), "b l h -> (b h) l").numpy(),
+                               rtol=1e-13)
+    np.testing.assert_allclose(np.linalg.norm(q, axis=-1), 1.0, rtol=1e-13)
+
+
+def test_prologue_zero_vector_and_softplus_range():
+    qkv, lr, _ = _raw(61, 1, 3, 1, 4, 1)
+    qkv[0, 1, 0] = 0.0                                   # q of token 1 is zero after SiLU
+    q, *_ = O.qkv_prologue(qkv, lr, 0.0)
+    assert not q[0, 1].any() and np.all(np.isfinite(q))
+    x = np.array([-800.0, -30.0, 0.0, 30.0, 800.0])
+    sp = O.softplus(x)
+    np.testing.assert_allclose(sp, F.softplus(torch.as_tensor(x)).numpy(), rtol=1e-14)
+    assert sp[-1] == 800.0 and sp[0] >= 0.0
+
+
+def test_output_rmsnorm_matches_library():
+    from einops import rearrange
+    B, H, L, hd = 2, 3, 5, 8
+    o = _rng(62).standard_normal((B * H, L, hd))
+    w = _rng(63).standard_normal((H, hd))
+    y = O.rmsnorm_out(o, B, H, w, eps=1e-5)
+    t = rearrange(torch.as_tensor(o), "(b h) l d -> b l h d", b=B)
+    ref = F.rms_norm(t, (hd,), eps=1e-5) * torch.as_tensor(w)
+    np.testing.assert_allclose(y, ref.numpy(), rtol=1e-13, atol=1e-15)
+    y0 = O.rmsnorm_out(o, B, H, None, eps=1e-5)
+    np.testing.assert_allclose(np.sqrt(np.mean(y0 ** 2, axis=-1)),
+                               np.sqrt(np.mean(o ** 2, -1) / (np.mean(o ** 2, -1) + 1e-5)).reshape(B, H, L)
+                               .transpose(0, 2, 1), rtol=1e-12)

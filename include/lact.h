@@ -196,6 +196,37 @@ int lact_forward_schedule(const lact_desc* desc,
                           void* stream);
 
 /*
+ * The layer's steps on either side of the path (Alg. 1, layer), each one pass
+ * over HBM. Only B, H, d, n_q, n_kv, io_dtype and eta_per_matrix of `desc`
+ * are used (the descriptor must still be valid).
+ *
+ * lact_prologue: from the projections to the path's inputs.
+ *   qkv      [B, n_q, 3, H, d]  io_dtype  q, k, v projections, blocks of heads  in
+ *   lr_raw   [B, n_q, H, R]     fp32      R = 3 with eta_per_matrix, else 1     in
+ *   lr_bias                     fp32      constant added before the softplus
+ *   beta_raw [B, n_q, H]        fp32      momentum logits, or NULL              in
+ *   q        [B*H, n_q, d]      io_dtype  SiLU(q_raw) / ||SiLU(q_raw)||         out
+ *   k        [B*H, n_kv, d]     io_dtype  SiLU(k_raw) / ||SiLU(k_raw)||         out
+ *   v        [B*H, n_kv, d]     io_dtype  SiLU(v_raw)                           out
+ *   eta      [B*H, n_kv(, 3)]   fp32      softplus(lr_raw + lr_bias)            out
+ *   beta     [B*H, n_kv]        fp32      sigmoid(beta_raw); NULL iff beta_raw  out
+ * Tokens l >= n_kv produce q only (their k, v and rates are not read). A zero
+ * vector normalises to zero. Norms and activations are computed in fp32.
+ *
+ * lact_rmsnorm_out: per-head RMSNorm of the path's output, heads moved back
+ * next to the channels:
+ *   o        [B*H, n_q, d]      io_dtype                                        in
+ *   weight   [H, d]             fp32, or NULL (no scale)                        in
+ *   y        [B, n_q, H, d]     io_dtype  o / sqrt(mean_d(o^2) + eps) * weight  out
+ * eps must be finite and >= 0. Inputs must not alias outputs.
+ */
+int lact_prologue(const lact_desc* desc, const void* qkv, const float* lr_raw, float lr_bias,
+                  const float* beta_raw, void* q, void* k, void* v, float* eta, float* beta,
+                  void* stream);
+int lact_rmsnorm_out(const lact_desc* desc, const void* o, const float* weight, float eps, void* y,
+                     void* stream);
+
+/*
  * Kernel timing (instrumentation for benchmarks). While enabled, lact_forward
  * brackets every kernel launch with HIP events on its stream, grouped by
  * kernel class (LACT_KCLASS_*). lact_timing_read synchronises on the recorded
@@ -208,8 +239,10 @@ int lact_forward_schedule(const lact_desc* desc,
 #define LACT_KCLASS_UPDATE 2   /* weight update, row norms, bf16 operand copies,  */
                                /* momentum chunk means                            */
 #define LACT_KCLASS_NS 3       /* Newton-Schulz (Muon) kernels                    */
-#define LACT_KCLASS_PREP 4     /* initial fp32 -> bf16 operand copies             */
-#define LACT_KCLASS_COUNT 5
+#define LACT_KCLASS_PREP 4     /* initial fp32 -> bf16 operand copies; schedule   */
+                               /* output rows zeroed                              */
+#define LACT_KCLASS_IO 5       /* lact_prologue and lact_rmsnorm_out              */
+#define LACT_KCLASS_COUNT 6
 int lact_timing_enable(int enable);
 int lact_timing_reset(void);
 int lact_timing_read(int kclass, int64_t* launches, double* total_ms, double* flops);

@@ -9,7 +9,7 @@ LIB_PATH = os.path.join(PKG, "liblact.so")
 
 APPLY_THEN_UPDATE, UPDATE_THEN_APPLY = 0, 1
 IO_BF16, IO_FP32 = 0, 1
-KCLASS_NAMES = ("fwd", "bwd", "update", "ns", "prep")
+KCLASS_NAMES = ("fwd", "bwd", "update", "ns", "prep", "io")
 
 _ERRORS = {0: "LACT_OK", -1: "LACT_EINVAL", -2: "LACT_EALIGN", -3: "LACT_EWORKSPACE",
            -4: "LACT_EUNSUPPORTED", -5: "LACT_EHIP"}
@@ -61,6 +61,11 @@ def load_library(path: str | None = None):
     L.lact_forward_momentum.restype = i32
     L.lact_forward_schedule.argtypes = [dp, ctypes.POINTER(LactSegment), i64] + [vp] * 13 + [sz, vp]
     L.lact_forward_schedule.restype = i32
+    f32 = ctypes.c_float
+    L.lact_prologue.argtypes = [dp, vp, vp, f32, vp, vp, vp, vp, vp, vp, vp]
+    L.lact_prologue.restype = i32
+    L.lact_rmsnorm_out.argtypes = [dp, vp, vp, f32, vp, vp]
+    L.lact_rmsnorm_out.restype = i32
     L.lact_timing_enable.argtypes = [i32]
     L.lact_timing_enable.restype = i32
     L.lact_timing_reset.argtypes = []
@@ -243,6 +248,71 @@ def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_s
     if rc:
         _raise(rc)
     return (out, M) if beta is not None else out
+
+
+def prologue(qkv, lr_raw, lr_bias, beta_raw=None, n_kv=None, out=None, stream=None):
+    """The layer's prologue (lact_prologue): qkv [B, L, 3, H, d] (bf16 or fp32),
+    lr_raw [B, L, H] or [B, L, H, 3] fp32, beta_raw [B, L, H] fp32 or None.
+    Returns (q [B, H, L, d], k, v [B, H, n_kv, d], eta [B, H, n_kv(, 3)], beta
+    [B, H, n_kv] or None); ``out`` may hold preallocated tensors of those shapes.
+    """
+    import torch
+    if qkv.dim() != 5 or qkv.shape[2] != 3:
+        raise LactError(-1, "qkv must be [B, L, 3, H, d]")
+    B, L, _, H, d = qkv.shape
+    n_kv = L if n_kv is None else int(n_kv)
+    lr3 = lr_raw.dim() == 4
+    if lr_raw.shape[:3] != (B, L, H) or (lr3 and lr_raw.shape[3] != 3):
+        raise LactError(-1, "lr_raw must be [B, L, H] or [B, L, H, 3]")
+    if beta_raw is not None and beta_raw.shape != (B, L, H):
+        raise LactError(-1, "beta_raw must be [B, L, H]")
+    for t, name in ((qkv, "qkv"), (lr_raw, "lr_raw"), (beta_raw, "beta_raw")):
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise LactError(-1, f"{name} must be a contiguous device tensor")
+    if lr_raw.dtype != torch.float32 or (beta_raw is not None and beta_raw.dtype != torch.float32):
+        raise LactError(-1, "lr_raw and beta_raw are fp32")
+    io = IO_BF16 if qkv.dtype == torch.bfloat16 else IO_FP32 if qkv.dtype == torch.float32 else None
+    if io is None:
+        raise LactError(-1, f"unsupported qkv dtype {qkv.dtype}")
+    if out is None:
+        e = lambda *sh, dt=qkv.dtype: torch.empty(*sh, dtype=dt, device=qkv.device)
+        out = (e(B, H, L, d), e(B, H, n_kv, d), e(B, H, n_kv, d),
+               e(B, H, n_kv, *((3,) if lr3 else ()), dt=torch.float32),
+               e(B, H, n_kv, dt=torch.float32) if beta_raw is not None else None)
+    q, k, v, eta, beta = out
+    desc = make_desc(B, H, d, d, n_kv, L, 1, 0, False, 0, io, lr3)   # h unused: any valid value
+    if stream is None:
+        stream = torch.cuda.current_stream(qkv.device).cuda_stream
+    rc = lib().lact_prologue(ctypes.byref(desc), _ptr(qkv), _ptr(lr_raw), ctypes.c_float(lr_bias), _ptr(beta_raw),
+                             _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(beta), ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return q, k, v, eta, beta
+
+
+def rmsnorm_out(o, weight=None, eps=1e-6, out=None, stream=None):
+    """Per-head RMSNorm of the path output (lact_rmsnorm_out): o [B, H, L, d]
+    -> y [B, L, H, d]; weight [H, d] fp32 or None."""
+    import torch
+    if o.dim() != 4:
+        raise LactError(-1, "o must be [B, H, L, d]")
+    B, H, L, d = o.shape
+    if not o.is_cuda or not o.is_contiguous():
+        raise LactError(-1, "o must be a contiguous device tensor")
+    if weight is not None and (weight.shape != (H, d) or weight.dtype != torch.float32 or not weight.is_contiguous()):
+        raise LactError(-1, "weight must be a contiguous fp32 [H, d] tensor")
+    io = IO_BF16 if o.dtype == torch.bfloat16 else IO_FP32 if o.dtype == torch.float32 else None
+    if io is None:
+        raise LactError(-1, f"unsupported o dtype {o.dtype}")
+    y = torch.empty(B, L, H, d, dtype=o.dtype, device=o.device) if out is None else out
+    desc = make_desc(B, H, d, d, 0, L, 1, 0, False, 0, io)
+    if stream is None:
+        stream = torch.cuda.current_stream(o.device).cuda_stream
+    rc = lib().lact_rmsnorm_out(ctypes.byref(desc), _ptr(o), _ptr(weight), ctypes.c_float(eps), _ptr(y),
+                                ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return y
 
 
 def timing_enable(on: bool = True):

@@ -711,6 +711,60 @@ int lact_forward(const lact_desc* desc, const void* q, const void* k, const void
                      stream);
 }
 
+int lact_prologue(const lact_desc* desc, const void* qkv, const float* lr_raw, float lr_bias, const float* beta_raw,
+                  void* q, void* k, void* v, float* eta, float* beta, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  const bool any_q = desc->n_q > 0, any_kv = desc->n_kv > 0;
+  if (any_q && (!qkv || !q || !lr_raw)) return LACT_EINVAL;
+  if (any_kv && (!k || !v || !eta)) return LACT_EINVAL;
+  if ((beta_raw == nullptr) != (beta == nullptr)) return LACT_EINVAL;
+  if (!(lr_bias == lr_bias) || lr_bias - lr_bias != 0.0f) return LACT_EINVAL;   // finite
+  if (any_q && (misaligned(qkv) || misaligned(q) || ((uintptr_t)lr_raw & 3))) return LACT_EALIGN;
+  if (any_kv && (misaligned(k) || misaligned(v) || ((uintptr_t)eta & 3))) return LACT_EALIGN;
+  if (beta && (((uintptr_t)beta & 3) || ((uintptr_t)beta_raw & 3))) return LACT_EALIGN;
+  PrologueArgs a{};
+  a.qkv = qkv;
+  a.lr_raw = lr_raw;
+  a.beta_raw = beta_raw;
+  a.lr_bias = lr_bias;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.eta = eta;
+  a.beta = beta;
+  a.B = desc->B;
+  a.H = desc->H;
+  a.hd = desc->d;
+  a.R = desc->eta_per_matrix ? 3 : 1;
+  a.L = desc->n_q;
+  a.n_kv = desc->n_kv;
+  const bool bf16 = desc->io_dtype == LACT_IO_BF16;
+  hipStream_t s = (hipStream_t)stream;
+  return timed(LACT_KCLASS_IO, 0.0, s, [&] { return launch_prologue(a, bf16, s); });
+}
+
+int lact_rmsnorm_out(const lact_desc* desc, const void* o, const float* weight, float eps, void* y, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  if (!(eps >= 0.0f) || eps - eps != 0.0f) return LACT_EINVAL;   // finite, >= 0
+  if (desc->n_q > 0 && (!o || !y)) return LACT_EINVAL;
+  if (desc->n_q > 0 && (misaligned(o) || misaligned(y))) return LACT_EALIGN;
+  if (weight && ((uintptr_t)weight & 3)) return LACT_EALIGN;
+  RmsArgs a{};
+  a.o = o;
+  a.weight = weight;
+  a.y = y;
+  a.eps = eps;
+  a.B = desc->B;
+  a.H = desc->H;
+  a.hd = desc->d;
+  a.L = desc->n_q;
+  const bool bf16 = desc->io_dtype == LACT_IO_BF16;
+  hipStream_t s = (hipStream_t)stream;
+  return timed(LACT_KCLASS_IO, 0.0, s, [&] { return launch_rmsnorm_out(a, bf16, s); });
+}
+
 int lact_forward_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, const void* q,
                           const void* k, const void* v, const float* eta, const float* beta, float* W1, float* W2,
                           float* W3, float* M1, float* M2, float* M3, void* o, void* workspace,

@@ -165,6 +165,31 @@ struct NsFusedArgs {
   float ca, cb, cc;     // quintic coefficients
 };
 
+// ---- the layer's prologue and output norm (lact_io.hip) ---------------------
+struct PrologueArgs {
+  const void* qkv;      // [B, L, 3, H, hd] io dtype
+  const float* lr_raw;  // [B, L, H, R]
+  const float* beta_raw;   // [B, L, H] or nullptr
+  float lr_bias;
+  void *q, *k, *v;      // [B*H, L, hd], [B*H, n_kv, hd] x 2
+  float* eta;           // [B*H, n_kv, R]
+  float* beta;          // [B*H, n_kv] or nullptr
+  int B, H, hd, R;
+  int64_t L, n_kv;
+  int group;            // set by the launcher
+};
+struct RmsArgs {
+  const void* o;        // [B*H, L, hd]
+  const float* weight;  // [H, hd] or nullptr
+  void* y;              // [B, L, H, hd]
+  float eps;
+  int B, H, hd;
+  int64_t L;
+  int group;            // set by the launcher
+};
+hipError_t launch_prologue(PrologueArgs a, bool io_bf16, hipStream_t s);
+hipError_t launch_rmsnorm_out(RmsArgs a, bool io_bf16, hipStream_t s);
+
 // Workgroup tile of a contraction kind: output rows x output columns, threads.
 struct TileShape {
   int rows, cols, threads;

@@ -22,7 +22,8 @@ def _declared():
 def test_library_exports_every_declared_symbol():
     L = P.lib()
     names = _declared()
-    assert {"lact_forward", "lact_forward_momentum", "lact_forward_schedule", "lact_workspace_bytes"} <= set(names)
+    assert {"lact_forward", "lact_forward_momentum", "lact_forward_schedule", "lact_prologue", "lact_rmsnorm_out",
+            "lact_workspace_bytes"} <= set(names)
     for n in names:
         assert hasattr(L, n), n
 
@@ -153,6 +154,30 @@ def test_per_matrix_rate_flag_is_validated():
     bad = make_desc(**GOOD)
     bad.eta_per_matrix = 2
     assert P.check_desc(bad) == -1
+
+
+def test_prologue_and_norm_errors_before_any_hip_call():
+    L = P.lib()
+    vp, f = ctypes.c_void_p, ctypes.c_float
+    d = make_desc(**GOOD)
+    pro = lambda qkv=0x1000, lr=0x2000, bias=0.0, braw=0, q=0x3000, k=0x4000, v=0x5000, eta=0x6000, beta=0: \
+        L.lact_prologue(ctypes.byref(d), vp(qkv), vp(lr), f(bias), vp(braw), vp(q), vp(k), vp(v), vp(eta), vp(beta),
+                        vp(0))
+    assert pro(qkv=0) == -1
+    assert pro(eta=0) == -1
+    assert pro(braw=0x7000) == -1                 # beta_raw without beta
+    assert pro(bias=float("nan")) == -1
+    assert pro(bias=float("inf")) == -1
+    assert pro(q=0x3008) == -2
+    assert pro(lr=0x2002) == -2
+    rms = lambda o=0x1000, w=0, eps=1e-6, y=0x2000: L.lact_rmsnorm_out(ctypes.byref(d), vp(o), vp(w), f(eps), vp(y), vp(0))
+    assert rms(o=0) == -1
+    assert rms(eps=-1.0) == -1
+    assert rms(eps=float("nan")) == -1
+    assert rms(y=0x2004) == -2
+    assert rms(w=0x3001) == -2
+    bad = make_desc(**dict(GOOD, d=12))
+    assert L.lact_rmsnorm_out(ctypes.byref(bad), vp(0x1000), vp(0), f(1e-6), vp(0x2000), vp(0)) == -4
 
 
 def test_timing_api_without_launches():

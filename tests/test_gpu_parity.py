@@ -585,3 +585,102 @@ def test_schedule_muon_two_updates():
     x = make_inputs(cfg, 40)
     sched = [("apply_then_update", 0, 256), ("update_only", 256, 512), ("apply_only", 256, 600)]
     check(cfg, x, run_gpu_schedule(cfg, x, sched), run_oracle_schedule(cfg, x, sched))
+
+
+# ----------------------------------------------------------------------------- prologue / output norm
+# lact_prologue and lact_rmsnorm_out (Alg. 1, layer) against the oracle. Both
+# are elementwise in fp32 with a per-vector reduction; outputs are rounded to
+# the I/O type once, so bf16 results sit within its rounding of the oracle.
+
+
+def _raw_inputs(seed, B, L, H, d, R, io, beta=True):
+    rng = np.random.default_rng(seed)
+    qkv = rng.standard_normal((B, L, 3, H, d), dtype=np.float32)
+    if io == "bf16":
+        from lact_synth import round_to_bf16
+        qkv = round_to_bf16(qkv)
+    lr = rng.standard_normal((B, L, H, R) if R == 3 else (B, L, H), dtype=np.float32)
+    br = rng.standard_normal((B, L, H), dtype=np.float32) if beta else None
+    return qkv, lr, br
+
+
+@pytest.mark.parametrize("io,d,R,n_kv_frac", [("bf16", 128, 1, 1.0), ("bf16", 96, 3, 0.5), ("bf16", 4096, 3, 1.0),
+                                              ("fp32", 40, 3, 0.7), ("fp32", 2048, 1, 1.0)])
+def test_prologue_matches_oracle(io, d, R, n_kv_frac):
+    B, H = 2, 3
+    L = 37 if d >= 2048 else 301
+    n_kv = int(L * n_kv_frac)
+    qkv, lr, br = _raw_inputs(50 + d, B, L, H, d, R, io)
+    print(f"[gpu] prologue io={io} B={B} L={L} H={H} d={d} R={R} n_kv={n_kv}", flush=True)
+    dt = torch.bfloat16 if io == "bf16" else torch.float32
+    dev = lambda a, t=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", t)
+    q, k, v, eta, beta = P.prologue(dev(qkv, dt), dev(lr), -0.7, dev(br), n_kv=n_kv)
+    torch.cuda.synchronize()
+    rq, rk, rv, reta, rbeta = O.qkv_prologue(qkv, lr if R == 3 else lr[..., None], -0.7, br)
+    f = lambda t: t.float().cpu().numpy().reshape(B * H, -1, *t.shape[3:])
+    tol = TOL[io]
+    assert rel(f(q), rq) <= tol
+    assert rel(f(k), rk[:, :n_kv]) <= tol and rel(f(v), rv[:, :n_kv]) <= tol
+    np.testing.assert_allclose(f(eta), reta[:, :n_kv], rtol=2e-6, atol=1e-7)
+    np.testing.assert_allclose(f(beta), rbeta[:, :n_kv], rtol=2e-6, atol=1e-7)
+    qn = np.linalg.norm(f(q).astype(np.float64), axis=-1)
+    np.testing.assert_allclose(qn, 1.0, atol=1e-2 if io == "bf16" else 1e-5)
+
+
+def test_prologue_lm_shape_sampled_tokens():
+    B, L, H, d = 4, 32768, 4, 512
+    rng = np.random.default_rng(55)
+    qkv = torch.randn(B, L, 3, H, d, generator=torch.Generator().manual_seed(55)).to("cuda", torch.bfloat16)
+    lr = torch.from_numpy(rng.standard_normal((B, L, H), dtype=np.float32)).cuda()
+    print(f"[gpu] prologue full LM shape B={B} L={L} H={H} d={d}", flush=True)
+    q, k, v, eta, _ = P.prologue(qkv, lr, 0.3)
+    torch.cuda.synchronize()
+    idx = np.sort(rng.choice(L, 97, replace=False))
+    raw = qkv[:, idx].float().cpu().numpy()
+    rq, rk, rv, reta, _ = O.qkv_prologue(raw, lr[:, idx].cpu().numpy()[..., None], 0.3)
+    f = lambda t: t[:, :, idx].float().cpu().numpy().reshape(B * H, len(idx), *t.shape[3:])
+    assert rel(f(q), rq) <= TOL["bf16"] and rel(f(k), rk) <= TOL["bf16"] and rel(f(v), rv) <= TOL["bf16"]
+    np.testing.assert_allclose(f(eta), reta, rtol=2e-6)
+
+
+@pytest.mark.parametrize("io,d,weighted", [("bf16", 128, True), ("bf16", 4096, False), ("fp32", 40, True),
+                                           ("fp32", 768, False)])
+def test_output_rmsnorm_matches_oracle(io, d, weighted):
+    B, H, L = 2, 3, 211 if d < 2048 else 19
+    rng = np.random.default_rng(70 + d)
+    o = rng.standard_normal((B, H, L, d), dtype=np.float32)
+    if io == "bf16":
+        from lact_synth import round_to_bf16
+        o = round_to_bf16(o)
+    w = rng.standard_normal((H, d), dtype=np.float32) if weighted else None
+    print(f"[gpu] rmsnorm io={io} B={B} H={H} L={L} d={d} weighted={weighted}", flush=True)
+    dt = torch.bfloat16 if io == "bf16" else torch.float32
+    y = P.rmsnorm_out(torch.from_numpy(o).to("cuda", dt), None if w is None else torch.from_numpy(w).cuda(), eps=1e-5)
+    torch.cuda.synchronize()
+    ref = O.rmsnorm_out(o.reshape(B * H, L, d), B, H, w, eps=1e-5)
+    assert y.shape == (B, L, H, d)
+    assert rel(y.float().cpu().numpy(), ref) <= TOL[io]
+
+
+def test_layer_chain_prologue_path_norm():
+    # projections -> prologue -> path (momentum, per-matrix rates) -> RMSNorm,
+    # all on the GPU, against the oracle's chain
+    B, H, L, d, h, C = 1, 2, 300, 64, 128, 128
+    qkv, lr, br = _raw_inputs(80, B, L, H, d, 3, "bf16")
+    dev = lambda a, t=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", t)
+    cfg = CONFIGS["lm32k"].with_(name="chain", B=B, H=H, d=d, h=h, n_kv=L, n_q=L, chunk=C)
+    x = make_inputs(cfg, 81)
+    print("[gpu] layer chain", flush=True)
+    q, k, v, eta, beta = P.prologue(dev(qkv, torch.bfloat16), dev(lr), -2.0, dev(br))
+    W = [dev(x[w].reshape(B, H, *x[w].shape[1:])) for w in ("W1", "W2", "W3")]
+    o, _ = P.forward_momentum(q, k, v, eta, beta, *W, chunk=C)
+    w = np.random.default_rng(82).standard_normal((H, d), dtype=np.float32)
+    y = P.rmsnorm_out(o, dev(w), eps=1e-6)
+    torch.cuda.synchronize()
+    rq, rk, rv, reta, rbeta = O.qkv_prologue(qkv, lr, -2.0, br)
+    # the oracle path starts from the GPU's own bf16 q, k, v (their rounding is the prologue's output)
+    g = lambda t: t.float().cpu().numpy().reshape(B * H, L, *t.shape[3:])
+    ref = O.lact_forward_momentum(g(q), g(k), g(v), reta, rbeta, x["W1"], x["W2"], x["W3"], chunk=C, order=0)
+    ry = O.rmsnorm_out(ref[0], B, H, w, eps=1e-6)
+    assert rel(g(q), rq) <= TOL["bf16"]
+    assert rel(y.float().cpu().numpy(), ry) <= TOL["bf16"]

@@ -36,7 +36,7 @@ PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FL
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 KERNEL_SOURCES = ("paper_2505_23884_amd/csrc/lact_kernels.hip", "paper_2505_23884_amd/csrc/lact_api.hip",
-                  "paper_2505_23884_amd/csrc/lact_internal.h")
+                  "paper_2505_23884_amd/csrc/lact_internal.h")   # the path's kernels (lact_io.hip is outside it)
 DOMINANT_KERNEL = {"fwd": "k_fwd", "bwd": "k_bwd", "update": "k_update", "ns": "k_ns"}
 COPY_MIB = 1024
 
@@ -165,6 +165,8 @@ def describe(cfg):
     muon = f", Muon {cfg.ns_steps} NS steps" if cfg.use_muon else ""
     mom = ", momentum (chunk-mean beta)" if cfg.momentum else ""
     lr3 = ", per-matrix rates" if cfg.lr3 else ""
+    if cfg.layer_io:
+        lr3 += ", with prologue (SiLU, q/k norm, softplus rates) and per-head RMSNorm"
     if cfg.schedule:
         order = f"schedule {cfg.schedule}"
     return (f"{cfg.name}: B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} n_kv={cfg.n_kv} n_q={cfg.n_q} "
@@ -252,12 +254,39 @@ def main():
     ws = torch.empty(P.workspace_bytes(desc), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
 
+    io_step = None
+    if cfg.layer_io:
+        # raw projections and rates, seeded on the device; the prologue makes q, k, v, eta
+        gen = torch.Generator(device=dev).manual_seed(0)
+        qkv_raw = torch.randn(cfg.B, cfg.n_q, 3, cfg.H, cfg.d, generator=gen, device=dev).to(io)
+        lr_raw = torch.randn(cfg.B, cfg.n_q, cfg.H, *((3,) if cfg.lr3 else ()), generator=gen, device=dev)
+        rms_w = torch.randn(cfg.H, cfg.d, generator=gen, device=dev)
+        y = torch.empty(cfg.B, cfg.n_q, cfg.H, cfg.d, dtype=io, device=dev)
+        io_step = {
+            "prologue": lambda: P.prologue(qkv_raw, lr_raw, -4.6, n_kv=cfg.n_kv, out=(q, k, v, eta, None),
+                                           stream=stream.cuda_stream),
+            "rmsnorm": lambda: P.rmsnorm_out(out, rms_w, 1e-6, out=y, stream=stream.cuda_stream),
+        }
+        esz = 2 if cfg.io == "bf16" else 4
+        R = 3 if cfg.lr3 else 1
+        io_bytes = {
+            "prologue": cfg.B * cfg.n_q * cfg.H * (3 * cfg.d * esz + 4 * R)
+                        + cfg.BH * (cfg.n_q * cfg.d * esz + cfg.n_kv * (2 * cfg.d * esz + 4 * R)),
+            "rmsnorm": 2 * cfg.BH * cfg.n_q * cfg.d * esz + cfg.H * cfg.d * 4,
+        }
     sched = None
     if cfg.schedule:
         from lact_synth import make_schedule
         sched = make_schedule(cfg)
 
     def step():
+        if io_step is not None:
+            io_step["prologue"]()
+        path()
+        if io_step is not None:
+            io_step["rmsnorm"]()
+
+    def path():
         if sched is not None:
             P.forward_schedule(q, k, v, eta, *W, sched, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
                                chunk=cfg.chunk, out=out, workspace=ws, stream=stream.cuda_stream,
@@ -319,6 +348,22 @@ def main():
                            "avg_launch_us": d["avg_us"],
                            "flops_per_launch": round(achieved * 1e12 * d["avg_us"] * 1e-6),
                            "per_class": per}
+        if io_step is not None:
+            res["io_kernels"] = {}
+            for name, fn in io_step.items():
+                P.timing_reset()
+                P.timing_enable(True)
+                for _ in range(args.steps):
+                    fn()
+                torch.cuda.synchronize()
+                P.timing_enable(False)
+                n, ms, _ = P.timing_read(P.KCLASS_NAMES.index("io"))
+                P.timing_reset()
+                avg = ms / n * 1e-3
+                gbs = io_bytes[name] / avg / 1e9
+                res["io_kernels"][name] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                                           "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                                           "bytes_per_launch": io_bytes[name], "avg_launch_us": round(avg * 1e6, 3)}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(res), flush=True)

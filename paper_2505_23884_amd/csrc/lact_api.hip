@@ -36,7 +36,7 @@ struct Plan {
   int ns_bps;         // blocks of kNsBlockElems per gradient
   // workspace offsets (bytes)
   size_t off_wb[3], off_hq, off_upd[3], off_step, off_bbar, total;
-  size_t off_y32, off_yb[2], off_a32, off_ab, off_bb, off_ss;
+  size_t off_y32, off_yb[2], off_ab, off_bb, off_ss;
 };
 
 int check_desc(const lact_desc* d) {
@@ -132,8 +132,6 @@ Plan make_plan(const lact_desc* dsc) {
       p.off_yb[i] = o;
       o = align_up(o + slots * dh * p.ns_esz);
     }
-    p.off_a32 = o;
-    o = align_up(o + slots * mm * 4);
     p.off_ab = o;
     o = align_up(o + slots * mm * p.ns_esz);
     p.off_bb = o;
@@ -328,7 +326,6 @@ int newton_schulz(Ctx& c) {
     a.Y32 = pa.Y32;
     a.Yin = c.ws + p.off_yb[t & 1];
     a.Yout = c.ws + p.off_yb[(t + 1) & 1];
-    a.A32 = reinterpret_cast<float*>(c.ws + p.off_a32);
     a.Ab = c.ws + p.off_ab;
     a.Bb = c.ws + p.off_bb;
     a.ystride = dh;

@@ -113,8 +113,7 @@ struct NsArgs {
   float* Y32;           // fp32 iterate (in place), slot stride ystride
   const void* Yin;      // operand copy read this iteration (fp16 or fp32)
   void* Yout;           // operand copy written this iteration
-  float* A32;           // fp32 Gram, slot stride astride
-  void* Ab;             // Gram operand copy
+  void* Ab;             // Gram (operand copy; also the b A term of the polynomial), slot stride astride
   void* Bb;             // polynomial operand copy
   int64_t ystride, astride;
   int m;                // Gram size min(d, h)

@@ -736,6 +736,17 @@ __device__ __forceinline__ void st_elem(void* base, int64_t idx, float v) {
 
 // Four consecutive elements (8 bytes of 16-bit or 16 bytes of fp32) at idx.
 template <typename T>
+__device__ __forceinline__ float4 ld4(const void* base, int64_t idx) {
+  if constexpr (sizeof(T) == 2) {
+    typedef __attribute__((ext_vector_type(4))) T t4;
+    const t4 v = *reinterpret_cast<const t4*>(reinterpret_cast<const T*>(base) + idx);
+    return make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+  } else {
+    return *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(base) + idx);
+  }
+}
+
+template <typename T>
 __device__ __forceinline__ void st4(void* base, int64_t idx, float a, float b, float c, float d) {
   if constexpr (sizeof(T) == 2) {
     typedef __attribute__((ext_vector_type(4))) T t4;
@@ -1260,6 +1271,79 @@ __global__ __launch_bounds__(256) void k_prep(const float* w1, const float* w2, 
 // fp32 / 8-byte 16-bit access). The Gram and polynomial products are
 // symmetric, so their transposes are themselves; the update product runs with
 // swapped operands (tile rows = Y columns, tile columns = Y rows).
+// Newton-Schulz epilogue (16-bit operand copies): the fp32 tile goes through
+// LDS in two halves (the wave columns of ni = 0, then ni = 1), WN * 32 stored
+// rows of ROWS_A floats each, so that every lane then moves 16 contiguous
+// bytes and a wave covers whole 1 KiB row segments: of A32 / Y32 (read and
+// written as fp32) and of the fp16 copies. Written straight from the MFMA
+// layout, each store instruction touched 32 rows 32 bytes at a time, and the
+// epilogue took longer than the product. 16-byte chunks are XOR-swizzled by
+// the staged row so that the column-wise writes and the row-wise reads are
+// both free of bank conflicts.
+template <typename T, class KK>
+__device__ __forceinline__ void ns_epilogue_staged(const Acc<KK>& acc, uint8_t* smem, const NsArgs& args, int kind,
+                                                   int64_t ld, int64_t i0, int64_t j0, int64_t mrows, int64_t ncols,
+                                                   void* Abw, float* Y32, void* Yout, void* Bbw) {
+  constexpr int R = KK::ROWS_A;                  // tile rows = stored columns
+  constexpr int SR = KK::WN * 32;                // staged stored rows per half
+  constexpr int CPR = R / 4;                     // 16-byte chunks per staged row
+  constexpr int PER = SR * CPR / KK::THREADS;    // chunks per thread per half
+  static_assert(KK::NI == 2 && SR * R * 4 <= KK::NSTAGE * KK::STAGE && (SR * CPR) % KK::THREADS == 0 &&
+                    (CPR & (CPR - 1)) == 0, "staging shape");
+  float* st = reinterpret_cast<float*>(smem);
+  const int lane = threadIdx.x & 63;
+  const bool gram = kind == NS_GRAM_K || kind == NS_GRAM_MN;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    // stage: lane holds rows r..r+3 (stored columns) of tile column c (stored row)
+    const int sr = wave_n<KK>() * 32 + (lane & 31);
+#pragma unroll
+    for (int mi = 0; mi < KK::MI; ++mi)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int r = acc_row<KK>(mi, 4 * g);
+        const f32x16_t& a = acc[0][mi][half];
+        *reinterpret_cast<float4*>(st + sr * R + (((r >> 2) ^ (sr & (CPR - 1))) << 2)) =
+            make_float4(a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]);
+      }
+    lds_barrier();
+    int64_t gidx[PER];
+    bool ok[PER];
+    float4 old[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = i * KK::THREADS + threadIdx.x;
+      const int srow = q / CPR, ch = q % CPR;
+      const int c = (srow / 32) * (KK::NI * 32) + half * 32 + (srow & 31);   // stored row in the tile
+      ok[i] = c < ncols && ch * 4 < mrows;
+      gidx[i] = (j0 + c) * ld + i0 + ch * 4;
+      if (ok[i] && kind == NS_POLY) old[i] = ld4<T>(Abw, gidx[i]);
+      else if (ok[i] && !gram) old[i] = *reinterpret_cast<const float4*>(Y32 + gidx[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = i * KK::THREADS + threadIdx.x;
+      const int srow = q / CPR, ch = q % CPR;
+      const float4 v = *reinterpret_cast<const float4*>(st + srow * R + ((ch ^ (srow & (CPR - 1))) << 2));
+      if (!ok[i]) continue;
+      if (gram) {
+        st4<T>(Abw, gidx[i], v.x, v.y, v.z, v.w);
+      } else if (kind == NS_POLY) {
+        const float4 o = old[i];
+        st4<T>(Bbw, gidx[i], args.cb * o.x + args.cc * v.x, args.cb * o.y + args.cc * v.y,
+               args.cb * o.z + args.cc * v.z, args.cb * o.w + args.cc * v.w);
+      } else {
+        const float4 o = old[i];
+        const float4 y = make_float4(args.ca * o.x + v.x, args.ca * o.y + v.y, args.ca * o.z + v.z,
+                                     args.ca * o.w + v.w);
+        *reinterpret_cast<float4*>(Y32 + gidx[i]) = y;
+        st4<T>(Yout, gidx[i], y.x, y.y, y.z, y.w);
+      }
+    }
+    if (half == 0) lds_barrier();   // every wave has read the first half
+  }
+}
+
 template <typename T, bool BIG>
 __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsArgs args) {
   using KK = typename NsKinds<T, BIG>::K;
@@ -1286,7 +1370,6 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
   float* Y32 = args.Y32 + slot * args.ystride;
   const uint8_t* Yin = reinterpret_cast<const uint8_t*>(args.Yin) + slot * args.ystride * esz;
   void* Yout = reinterpret_cast<uint8_t*>(args.Yout) + slot * args.ystride * esz;
-  float* A32 = args.A32 + slot * args.astride;
   const uint8_t* Ab = reinterpret_cast<const uint8_t*>(args.Ab) + slot * args.astride * esz;
   void* Abw = reinterpret_cast<uint8_t*>(args.Ab) + slot * args.astride * esz;
   const uint8_t* Bb = reinterpret_cast<const uint8_t*>(args.Bb) + slot * args.astride * esz;
@@ -1316,6 +1399,10 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
   }
   const bool gram = kind == NS_GRAM_K || kind == NS_GRAM_MN;
   const int64_t ld = (gram || kind == NS_POLY) ? m : ldy;
+  if constexpr (sizeof(T) == 2) {
+    ns_epilogue_staged<T, KK>(acc, smem, args, kind, ld, i0, j0, mrows, ncols, Abw, Y32, Yout, Bbw);
+    return;
+  }
 #pragma unroll
   for (int mi = 0; mi < KK::MI; ++mi)
 #pragma unroll
@@ -1330,10 +1417,9 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
         const float v0 = a[4 * g], v1 = a[4 * g + 1], v2 = a[4 * g + 2], v3 = a[4 * g + 3];
         const int64_t idx = (j0 + c) * ld + i0 + r;   // stored row j0+c, columns i0+r ..
         if (gram) {
-          *reinterpret_cast<float4*>(A32 + idx) = make_float4(v0, v1, v2, v3);
           st4<T>(Abw, idx, v0, v1, v2, v3);
         } else if (kind == NS_POLY) {
-          const float4 o = *reinterpret_cast<const float4*>(A32 + idx);
+          const float4 o = ld4<T>(Abw, idx);
           st4<T>(Bbw, idx, args.cb * o.x + args.cc * v0, args.cb * o.y + args.cc * v1, args.cb * o.z + args.cc * v2,
                  args.cb * o.w + args.cc * v3);
         } else {

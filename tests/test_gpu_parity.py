@@ -298,6 +298,15 @@ def test_muon_large_gram_ragged_tiles():
     teacher_forced(cfg, x, [0])
 
 
+def test_muon_small_gram_long_side_unfused():
+    # Gram size 96 <= 128 but the long side 384 > 256: the per-product
+    # Newton-Schulz launches with 128 x 128 tiles (not the one-workgroup kernel)
+    cfg = CONFIGS["lm32k_muon"].with_(name="muon_small_long", B=1, H=2, d=96, h=384, n_kv=512, n_q=512,
+                                      chunk=256)
+    x = make_inputs(cfg, 13)
+    teacher_forced(cfg, x, [0, 1])
+
+
 def test_muon_fp32_teacher_forced():
     cfg = CONFIGS["tiny_fp32"].with_(name="muon_fp32", B=1, H=2, d=64, h=96, n_kv=512, n_q=512,
                                      chunk=256, use_muon=1, ns_steps=5)

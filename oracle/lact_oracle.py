@@ -20,6 +20,9 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
                    momentum for test-time optimizers; Table 3, Momentum and Muon rows)
 * per-matrix rates one learning rate per token for each of W1, W2, W3 (the
                    lr of shape [b, l, 3] in the update of Alg. 1)
+* linear weight    f_W(x) = W x with W in R^{d x d}, the same loss and update
+                   rules (gradient -sum_i eta_i v_i k_i^T)          (§4.4 linear vs.
+                   nonlinear fast weight; §3.1 loss eq.)
 * prologue         per token and head: q, k, v = SiLU of the projections,
                    q and k divided by their L2 norm, lr = softplus(raw + bias),
                    beta = sigmoid(raw); heads moved next to the batch  (Alg. 1, layer)
@@ -80,7 +83,8 @@ __all__ = [
     "NS_COEFFS", "NS_EPS", "sigmoid", "silu", "swiglu_apply", "chunk_gradient",
     "newton_schulz", "weight_update", "update", "momentum_update", "lact_forward_instance",
     "lact_forward", "lact_forward_momentum", "SCHEDULE_MODES", "lact_forward_schedule_instance",
-    "lact_forward_schedule", "softplus", "qkv_prologue", "rmsnorm_out", "layer_flops",
+    "lact_forward_schedule", "softplus", "qkv_prologue", "rmsnorm_out", "linear_gradient",
+    "lact_forward_linear_instance", "lact_forward_linear", "linear_flops", "layer_flops",
 ]
 
 # Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
@@ -332,6 +336,70 @@ def rmsnorm_out(o, B: int, H: int, weight=None, eps: float = 1e-6):
     if weight is not None:
         y = y * np.asarray(weight, dtype=np.float64)[None, :, None, :]
     return np.ascontiguousarray(y.transpose(0, 2, 1, 3))
+
+
+def linear_gradient(W, K, V, eta):
+    """Gradient of sum_i eta_i * (-(W k_i)^T v_i) w.r.t. W for the linear fast
+    weight f_W(x) = W x (§4.4; §3.1 loss eq.): -sum_i eta_i v_i k_i^T, [d, d]."""
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    lr = np.asarray(eta, dtype=np.float64)[:, None]
+    return -(V * lr).T @ K
+
+
+def lact_forward_linear_instance(q, k, v, eta, W, chunk: int, order: int, use_muon: bool = False,
+                                 ns_steps: int = NS_STEPS_DEFAULT, beta=None, M=None):
+    """One instance with the linear fast weight: the chunk loop of
+    lact_forward_instance with o = W q, g = linear_gradient, the same
+    normalised (optionally Muon, optionally momentum) update. Returns
+    (o, W) or, with beta, (o, W, M)."""
+    W = np.asarray(W, dtype=np.float64).copy()
+    mom = beta is not None
+    if mom:
+        M = np.zeros_like(W) if M is None else np.asarray(M, dtype=np.float64).copy()
+    n_q, n_kv = q.shape[0], k.shape[0]
+    o = np.zeros((n_q, q.shape[1]))
+    apply = lambda W, X: np.asarray(X, dtype=np.float64) @ W.T
+
+    def upd(W, M, s, e):
+        g = linear_gradient(W, k[s:e], v[s:e], eta[s:e])
+        if mom:
+            M = float(np.mean(np.asarray(beta[s:e], dtype=np.float64))) * M + g
+            g = M
+        return weight_update(W, newton_schulz(g, ns_steps) if use_muon else g), M
+
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        if order == 0:
+            o[s:e] = apply(W, q[s:e])
+            W, M = upd(W, M, s, e)
+        else:
+            W, M = upd(W, M, s, e)
+            o[s:e] = apply(W, q[s:e])
+    if n_q > n_kv:
+        o[n_kv:] = apply(W, q[n_kv:])
+    return (o, W, M) if mom else (o, W)
+
+
+def lact_forward_linear(q, k, v, eta, W, chunk: int, order: int, use_muon: bool = False,
+                        ns_steps: int = NS_STEPS_DEFAULT, instances=None, beta=None, M=None):
+    """Batched driver of the linear fast weight: (o, W) stacked (and M with beta)."""
+    idx = range(q.shape[0]) if instances is None else instances
+    res = [lact_forward_linear_instance(q[i], k[i], v[i], eta[i], W[i], chunk, order, use_muon, ns_steps,
+                                        None if beta is None else beta[i],
+                                        None if (beta is None or M is None) else M[i]) for i in idx]
+    return tuple(np.stack(col) for col in zip(*res))
+
+
+def linear_flops(BH: int, d: int, n_kv: int, n_q: int, n_chunks: int, use_muon: bool = False,
+                 ns_steps: int = NS_STEPS_DEFAULT) -> float:
+    """FLOPs of the linear fast weight: the gradient V^T (eta K) costs 2 d^2 per
+    updated token and the apply W q 2 d^2 per applied token (the loss needs no
+    forward on the keys); Muon as in layer_flops with m = n = d, one matrix."""
+    f = BH * 2.0 * d * d * (n_kv + n_q)
+    if use_muon:
+        f += BH * n_chunks * ns_steps * 6.0 * d ** 3
+    return f
 
 
 SCHEDULE_MODES = ("apply_then_update", "update_then_apply", "update_only", "apply_only")

@@ -715,3 +715,65 @@ def test_output_rmsnorm_matches_library():
     np.testing.assert_allclose(np.sqrt(np.mean(y0 ** 2, axis=-1)),
                                np.sqrt(np.mean(o ** 2, -1) / (np.mean(o ** 2, -1) + 1e-5)).reshape(B, H, L)
                                .transpose(0, 2, 1), rtol=1e-12)
+
+
+# ----------------------------------------------------------------------------- linear fast weight
+# §4.4: f_W(x) = W x with the same dot-product loss and update rules.
+
+
+def test_linear_gradient_matches_autograd():
+    rng = _rng(90)
+    d, n = 6, 11
+    W = rng.standard_normal((d, d))
+    k, v = _tokens(rng, n, d), _tokens(rng, n, d)
+    eta = 0.3 * np.log1p(np.exp(rng.standard_normal(n)))
+    Wt = torch.as_tensor(W.copy()).requires_grad_(True)
+    loss = -(torch.as_tensor(eta) * (F.linear(torch.as_tensor(k), Wt) * torch.as_tensor(v)).sum(-1)).sum()
+    loss.backward()
+    np.testing.assert_allclose(O.linear_gradient(W, k, v, eta), Wt.grad.numpy(), rtol=1e-13, atol=1e-15)
+
+
+def test_linear_one_token_chunk_is_a_rank_one_step():
+    """A one-token chunk moves W by eta v k^T before the row rescaling."""
+    rng = _rng(91)
+    d = 5
+    W = _weights(rng, d, d, unit=True)[0]
+    q, k, v = _tokens(rng, 1, d), _tokens(rng, 1, d), _tokens(rng, 1, d)
+    eta = np.array([0.2])
+    o, Wf = O.lact_forward_linear_instance(q, k, v, eta, W, chunk=1, order=1)
+    U = W + 0.2 * np.outer(v[0], k[0])
+    ref = U * (np.linalg.norm(W, axis=1) / np.linalg.norm(U, axis=1))[:, None]
+    np.testing.assert_allclose(Wf, ref, rtol=1e-14)
+    np.testing.assert_allclose(o[0], ref @ q[0], rtol=1e-14)
+
+
+@pytest.mark.parametrize("muon", [0, 1])
+def test_linear_layer_eta_zero_and_autograd_loop(muon):
+    rng = _rng(92)
+    d, n, C = 6, 20, 7
+    W = _weights(rng, d, d, unit=True)[0]
+    q, k, v = _tokens(rng, n, d), _tokens(rng, n, d), _tokens(rng, n, d)
+    o0, W0 = O.lact_forward_linear_instance(q, k, v, np.zeros(n), W, chunk=C, order=0, use_muon=bool(muon))
+    np.testing.assert_array_equal(W0, W)
+    np.testing.assert_allclose(o0, q @ W.T, rtol=1e-14)
+    eta = 0.5 * np.log1p(np.exp(rng.standard_normal(n)))
+    o, Wf = O.lact_forward_linear_instance(q, k, v, eta, W, chunk=C, order=0, use_muon=bool(muon))
+    Wt = torch.as_tensor(W.copy())
+    outs = []
+    for s in range(0, n, C):
+        e = min(n, s + C)
+        outs.append((torch.as_tensor(q[s:e]) @ Wt.T).numpy())
+        Wg = Wt.clone().requires_grad_(True)
+        loss = -(torch.as_tensor(eta[s:e]) * (F.linear(torch.as_tensor(k[s:e]), Wg) *
+                                             torch.as_tensor(v[s:e])).sum(-1)).sum()
+        loss.backward()
+        g = _torch_ns(Wg.grad, 5) if muon else Wg.grad
+        u = Wt - g
+        Wt = u * (Wt.norm(dim=1, keepdim=True) / u.norm(dim=1, keepdim=True))
+    np.testing.assert_allclose(o, np.concatenate(outs), rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(Wf, Wt.numpy(), rtol=1e-11, atol=1e-13)
+
+
+def test_linear_flops():
+    assert O.linear_flops(2, 8, 10, 12, 3) == 2 * 2 * 64 * 22
+    assert O.linear_flops(1, 4, 4, 4, 2, True, 5) == 2 * 16 * 8 + 2 * 5 * 6 * 64

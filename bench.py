@@ -145,6 +145,9 @@ def workload_flops(cfg, BH=None):
     updated token and 6*d*h per applied token per head, plus per update and
     matrix 3*steps*(4*m^2*n + 2*m^3) with Muon (m <= n the sides)."""
     BH = cfg.BH if BH is None else BH
+    if cfg.linear:   # f_W(x) = W x: 2 d^2 per updated and per applied token; Muon on one d x d matrix
+        ns = cfg.n_chunks * cfg.ns_steps * 6.0 * float(cfg.d) ** 3 if cfg.use_muon else 0.0
+        return BH * (2.0 * cfg.d * cfg.d * (cfg.n_kv + cfg.n_q) + ns)
     dh = float(cfg.d) * cfg.h
     m, n = min(cfg.d, cfg.h), max(cfg.d, cfg.h)
     ns = 3.0 * cfg.ns_steps * (4.0 * m * m * n + 2.0 * m ** 3) if cfg.use_muon else 0.0
@@ -165,6 +168,8 @@ def describe(cfg):
     muon = f", Muon {cfg.ns_steps} NS steps" if cfg.use_muon else ""
     mom = ", momentum (chunk-mean beta)" if cfg.momentum else ""
     lr3 = ", per-matrix rates" if cfg.lr3 else ""
+    if cfg.linear:
+        lr3 += ", linear fast weight W x"
     if cfg.layer_io:
         lr3 += ", with prologue (SiLU, q/k norm, softplus rates) and per-head RMSNorm"
     if cfg.schedule:
@@ -196,7 +201,10 @@ def cpu_baseline(cfg, min_seconds):
     while done < scfg.BH and dt < min_seconds:
         x = make_inputs(scfg, 0, heads=[done])
         t0 = time.perf_counter()
-        if scfg.schedule:
+        if scfg.linear:
+            O.lact_forward_linear(x["q"], x["k"], x["v"], x["eta"], x["W1"], scfg.chunk, scfg.order,
+                                  bool(scfg.use_muon), scfg.ns_steps)
+        elif scfg.schedule:
             from lact_synth import make_schedule
             O.lact_forward_schedule(x["q"], x["k"], x["v"], x["eta"], x["W1"], x["W2"], x["W3"],
                                     make_schedule(scfg), use_muon=bool(scfg.use_muon), ns_steps=scfg.ns_steps,
@@ -250,7 +258,7 @@ def main():
     out = torch.empty_like(q)
     desc = P.binding.make_desc(cfg.B, cfg.H, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.chunk, cfg.order,
                                cfg.use_muon, cfg.ns_steps, P.IO_BF16 if cfg.io == "bf16" else P.IO_FP32,
-                               bool(cfg.lr3))
+                               bool(cfg.lr3), P.FW_LINEAR if cfg.linear else P.FW_SWIGLU)
     ws = torch.empty(P.workspace_bytes(desc), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
 
@@ -287,7 +295,10 @@ def main():
             io_step["rmsnorm"]()
 
     def path():
-        if sched is not None:
+        if cfg.linear:
+            P.forward_linear(q, k, v, eta, W[0], cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
+                             ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=stream.cuda_stream)
+        elif sched is not None:
             P.forward_schedule(q, k, v, eta, *W, sched, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
                                chunk=cfg.chunk, out=out, workspace=ws, stream=stream.cuda_stream,
                                **({"beta": beta, "M1": M[0], "M2": M[1], "M3": M[2]} if cfg.momentum else {}))

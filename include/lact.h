@@ -20,6 +20,9 @@
  *           with the final fast weights (the novel-view-synthesis layout:
  *           update on the input views, apply to the target views, §4).
  *
+ * With the linear fast weight (lact_desc.fast_weight, §4.4) the same path
+ * runs for f_W(x) = W1 x with W1 in R^{d x d}: o = W1 q, g = -sum eta v k^T.
+ *
  * Math layout per instance: W1, W3 are h x d, W2 is d x h, row-major, fp32.
  * The fast weights are the recurrent state; they are read and written in
  * place, so the caller owns them as the checkpoint between calls.
@@ -59,6 +62,12 @@ extern "C" {
 #define LACT_APPLY_THEN_UPDATE 0
 #define LACT_UPDATE_THEN_APPLY 1
 
+/* lact_desc.fast_weight */
+#define LACT_FW_SWIGLU 0        /* f_W(x) = W2 [SiLU(W1 x) o (W3 x)]                 */
+#define LACT_FW_LINEAR 1        /* f_W(x) = W1 x, W1 in R^{d x d} (§4.4): requires  */
+                                /* h == d and one rate per token; W2, W3 (and M2,  */
+                                /* M3) are unused and may be NULL                  */
+
 /* lact_desc.io_dtype: element type of q, k, v and o. eta and W are fp32. */
 #define LACT_IO_BF16 0          /* bf16 MFMA operands, fp32 accumulate, fp32 state */
 #define LACT_IO_FP32 1          /* fp32 MFMA throughout                            */
@@ -80,6 +89,7 @@ typedef struct lact_desc {
   int32_t eta_per_matrix; /* 0: eta is [B*H, n_kv], one rate per token;        */
                       /* 1: eta is [B*H, n_kv, 3], (lr1, lr2, lr3) per token    */
                       /* weighting the W1, W2, W3 gradients (Alg. 1, update)    */
+  int32_t fast_weight;  /* LACT_FW_SWIGLU (0) or LACT_FW_LINEAR                 */
 } lact_desc;
 
 /*

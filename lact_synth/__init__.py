@@ -54,6 +54,7 @@ class LactConfig:
     lr3: int = 0          # 1: per-matrix learning rates, eta [B*H, n_kv, 3]
     schedule: str = ""    # "": uniform chunks in `order`; else a make_schedule() recipe
     layer_io: int = 0     # 1: the step also runs the prologue and the output norm
+    linear: int = 0       # 1: linear fast weight f_W(x) = W1 x (h == d; W1 is the state)
 
     @property
     def BH(self) -> int:
@@ -78,6 +79,9 @@ CONFIGS = {
     "lm32k_mom": LactConfig("lm32k_mom", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", 1),
     "lm32k_muon_mom": LactConfig("lm32k_muon_mom", 4, 4, 512, 512, 32768, 32768, 2048, 0, 1, 5, "bf16", 1),
     "lm32k_layer": LactConfig("lm32k_layer", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", layer_io=1),
+    # linear fast weight at the NVS shape (a state of d^2 per head)
+    "nvs256k_linear": LactConfig("nvs256k_linear", 1, 1, 768, 768, 262144, 262144 + 4096, 262144, 1, 0, 0, "bf16",
+                                 linear=1),
     "lm32k_lr3": LactConfig("lm32k_lr3", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", lr3=1),
     # video teacher forcing: 18 clean chunks of 3120 tokens interleaved with 19
     # noisy ones, [X1n, X1, ..., X18, X19n] (115440 tokens in all)

@@ -25,7 +25,11 @@ class LactDesc(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("h", ctypes.c_int32), ("n_kv", ctypes.c_int64), ("n_q", ctypes.c_int64),
                 ("chunk", ctypes.c_int64), ("order", ctypes.c_int32), ("use_muon", ctypes.c_int32),
-                ("ns_steps", ctypes.c_int32), ("io_dtype", ctypes.c_int32), ("eta_per_matrix", ctypes.c_int32)]
+                ("ns_steps", ctypes.c_int32), ("io_dtype", ctypes.c_int32), ("eta_per_matrix", ctypes.c_int32),
+                ("fast_weight", ctypes.c_int32)]
+
+
+FW_SWIGLU, FW_LINEAR = 0, 1
 
 
 SEG_APPLY_THEN_UPDATE, SEG_UPDATE_THEN_APPLY, SEG_UPDATE_ONLY, SEG_APPLY_ONLY = 0, 1, 2, 3
@@ -97,9 +101,9 @@ def _raise(code: int):
 
 
 def make_desc(B, H, d, h, n_kv, n_q, chunk, order=0, use_muon=False, ns_steps=5, io_dtype=IO_BF16,
-              eta_per_matrix=False):
+              eta_per_matrix=False, fast_weight=FW_SWIGLU):
     return LactDesc(int(B), int(H), int(d), int(h), int(n_kv), int(n_q), int(chunk), int(order),
-                    int(bool(use_muon)), int(ns_steps), int(io_dtype), int(bool(eta_per_matrix)))
+                    int(bool(use_muon)), int(ns_steps), int(io_dtype), int(bool(eta_per_matrix)), int(fast_weight))
 
 
 def check_desc(desc: LactDesc) -> int:
@@ -118,7 +122,8 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
-def _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps, out, workspace, stream):
+def _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps, out, workspace, stream,
+             fast_weight=FW_SWIGLU):
     """Checks shapes and dtypes; returns (desc, out, workspace, stream handle)."""
     import torch
     if q.dim() == 4:
@@ -151,7 +156,7 @@ def _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps, 
             or W1.numel() != BH * h * d or W3.numel() != BH * h * d or W2.numel() != BH * d * h
             or W2.shape[-2] != d or W2.shape[-1] != h or W1.shape[-1] != d):
         raise LactError(-1, "inconsistent tensor shapes")
-    desc = make_desc(B, H, d, h, n_kv, n_q, chunk, order, use_muon, ns_steps, io, lr3)
+    desc = make_desc(B, H, d, h, n_kv, n_q, chunk, order, use_muon, ns_steps, io, lr3, fast_weight)
     nbytes = workspace_bytes(desc)
     if workspace is None:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
@@ -212,6 +217,38 @@ def forward_momentum(q, k, v, eta, beta, W1, W2, W3, M1=None, M2=None, M3=None, 
     if rc:
         _raise(rc)
     return out, (M1, M2, M3)
+
+
+def forward_linear(q, k, v, eta, W, chunk, order=APPLY_THEN_UPDATE, use_muon=False, ns_steps=5, beta=None, M=None,
+                   out=None, workspace=None, stream=None):
+    """The path with the linear fast weight f_W(x) = W x (lact_desc.fast_weight =
+    LACT_FW_LINEAR): W [.., d, d] fp32, updated IN PLACE; q, k, v, eta as in
+    forward(). With ``beta`` the updates use momentum (M [.., d, d] updated in
+    place, zeros allocated when omitted) and the return is (o, M); else o.
+    """
+    import torch
+    if W.shape[-1] != W.shape[-2]:
+        raise LactError(-1, "the linear fast weight is square, [.., d, d]")
+    extra = []
+    if beta is not None:
+        M = torch.zeros_like(W) if M is None else M
+        if M.shape != W.shape:
+            raise LactError(-1, "M must have W's shape")
+        extra = [(beta, "beta"), (M, "M")]
+    # W stands in for all three matrices in the shape checks (h = d)
+    desc, out, workspace, stream = _marshal(q, k, v, eta, W, W, W, extra, chunk, order, use_muon, ns_steps, out,
+                                            workspace, stream, FW_LINEAR)
+    wsb = ctypes.c_size_t(workspace.numel() * workspace.element_size())
+    if beta is None:
+        rc = lib().lact_forward(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(W), ctypes.c_void_p(0),
+                                ctypes.c_void_p(0), _ptr(out), _ptr(workspace), wsb, ctypes.c_void_p(stream))
+    else:
+        rc = lib().lact_forward_momentum(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(beta), _ptr(W),
+                                         ctypes.c_void_p(0), ctypes.c_void_p(0), _ptr(M), ctypes.c_void_p(0),
+                                         ctypes.c_void_p(0), _ptr(out), _ptr(workspace), wsb, ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return (out, M) if beta is not None else out
 
 
 def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_steps=5, beta=None,

@@ -25,6 +25,8 @@ struct Plan {
   bool bf16;
   int esz;
   int es;             // floats of eta per token (1, or 3 with per-matrix rates)
+  bool linear;        // linear fast weight: one d x d matrix per instance (h == d)
+  int nmat;           // fast-weight matrices per instance (3 or 1)
   int64_t C;          // tokens of the largest chunk (0 when n_kv == 0)
   int64_t cap;        // rows of the applied-hidden buffer
   int nsplit;         // split-K ways of the gradient contraction
@@ -48,6 +50,9 @@ int check_desc(const lact_desc* d) {
   if (d->ns_steps < 0 || d->ns_steps > 16) return LACT_EINVAL;
   if (d->io_dtype != LACT_IO_BF16 && d->io_dtype != LACT_IO_FP32) return LACT_EINVAL;
   if (d->eta_per_matrix != 0 && d->eta_per_matrix != 1) return LACT_EINVAL;
+  if (d->fast_weight != LACT_FW_SWIGLU && d->fast_weight != LACT_FW_LINEAR) return LACT_EINVAL;
+  // the linear fast weight is one d x d matrix with one learning rate per token
+  if (d->fast_weight == LACT_FW_LINEAR && (d->h != d->d || d->eta_per_matrix)) return LACT_EINVAL;
   if (d->d < 1 || d->h < 1) return LACT_EINVAL;
   if (d->d % 8 || d->h % 8 || d->d > kMaxDim || d->h > kMaxDim) return LACT_EUNSUPPORTED;
   // 16-bit MFMA tiles take K in whole steps of 32 along d and h
@@ -65,6 +70,8 @@ Plan make_plan(const lact_desc* dsc) {
   p.bf16 = dsc->io_dtype == LACT_IO_BF16;
   p.esz = p.bf16 ? 2 : 4;
   p.es = dsc->eta_per_matrix ? 3 : 1;
+  p.linear = dsc->fast_weight == LACT_FW_LINEAR;
+  p.nmat = p.linear ? 1 : 3;
   p.C = std::min<int64_t>(dsc->chunk, dsc->n_kv);
   const int64_t tail = dsc->n_q - dsc->n_kv;
   // The applied-hidden buffer holds one chunk plus (bounded) tail rows so that
@@ -80,7 +87,7 @@ Plan make_plan(const lact_desc* dsc) {
   // at least 1024 tokens, that minimises the makespan of equal blocks over the
   // 256 CUs: rounds(tiles * ns) / ns. Lengths are a multiple of 32.
   const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
-  const int64_t tiles = (int64_t)p.BH * (cdiv(p.h, g13.rows) * cdiv(p.d, g13.cols) +
+  const int64_t tiles = (int64_t)p.BH * ((p.linear ? 0 : cdiv(p.h, g13.rows) * cdiv(p.d, g13.cols)) +
                                          cdiv(p.d, g2.rows) * cdiv(p.h, g2.cols));
   int64_t ns;
   if (p.C >= 8192) {
@@ -105,16 +112,17 @@ Plan make_plan(const lact_desc* dsc) {
   size_t o = 0;
   for (int m = 0; m < 3; ++m) {
     p.off_wb[m] = o;
-    if (p.bf16) o = align_up(o + (size_t)p.BH * dh * 2);
+    if (p.bf16 && m < p.nmat) o = align_up(o + (size_t)p.BH * dh * 2);
   }
+  // linear: no applied hidden (the apply is one product); one update buffer (eta k)
   p.off_hq = o;
-  o = align_up(o + (size_t)p.BH * p.cap * p.h * p.esz);
+  if (!p.linear) o = align_up(o + (size_t)p.BH * p.cap * p.h * p.esz);
   for (int m = 0; m < 3; ++m) {
     p.off_upd[m] = o;
-    o = align_up(o + (size_t)p.BH * std::max<int64_t>(p.C, 1) * p.h * p.esz);
+    if (m < p.nmat) o = align_up(o + (size_t)p.BH * std::max<int64_t>(p.C, 1) * p.h * p.esz);
   }
   p.off_step = o;
-  o = align_up(o + (size_t)p.nsplit * p.BH * 3 * dh * 4);
+  o = align_up(o + (size_t)p.nsplit * p.BH * p.nmat * dh * 4);
   // chunk-mean momentum factors of up to kBetaBatch chunks (momentum entry
   // point only; reserved always so both entry points share one size)
   p.off_bbar = o;
@@ -125,7 +133,7 @@ Plan make_plan(const lact_desc* dsc) {
   p.ns_fp16 = p.bf16;
   p.ns_esz = p.ns_fp16 ? 2 : 4;
   if (p.muon) {
-    const size_t slots = (size_t)p.BH * 3, mm = (size_t)p.m * p.m;
+    const size_t slots = (size_t)p.BH * p.nmat, mm = (size_t)p.m * p.m;
     p.off_y32 = o;
     o = align_up(o + slots * dh * 4);
     for (int i = 0; i < 2; ++i) {
@@ -223,6 +231,31 @@ Operand op(const void* base, int64_t ld, int64_t inst) { return Operand{base, ld
 // Applies the current fast weights to query rows [s0, s1), in pieces that fit.
 int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
   const Plan& p = c.p;
+  if (p.linear) {   // o = W q: one contraction over d per piece of rows
+    for (int64_t a = s0; a < s1; a += 65536) {   // bounds the tile count of a launch
+      const int64_t n = std::min<int64_t>(65536, s1 - a);
+      BwdArgs b{};
+      BwdSeg& o = b.seg[0];
+      o.kind = BWD_OUT;
+      o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16).rows);
+      o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16).cols);
+      o.nsplit = 1;
+      o.nblocks = p.BH * o.tiles_m * o.tiles_n;
+      o.rows = n;
+      o.a0 = op(c.q + a * p.d * p.esz, p.d, c.dsc->n_q * p.d);
+      o.b0 = c.wop[0];
+      o.out = c.o + a * p.d * p.esz;
+      o.out_inst = c.dsc->n_q * p.d;
+      b.nseg = 1;
+      b.total_blocks = o.nblocks;
+      b.d = p.d;
+      b.h = p.d;
+      const int rc = timed(LACT_KCLASS_BWD, 2.0 * p.BH * n * p.d * p.d, c.s,
+                           [&] { return launch_bwd(b, p.bf16, c.s); });
+      if (rc) return rc;
+    }
+    return LACT_OK;
+  }
   for (int64_t a = s0; a < s1; a += p.cap) {
     const int64_t n = std::min<int64_t>(p.cap, s1 - a);
     FwdArgs f{};
@@ -275,14 +308,15 @@ int newton_schulz(Ctx& c) {
   NsPrepArgs pa{};
   pa.part = reinterpret_cast<const float*>(c.ws + p.off_step);
   pa.nsplit = p.nsplit;
-  pa.part_split = (int64_t)p.BH * 3 * dh;
+  pa.part_split = (int64_t)p.BH * p.nmat * dh;
   pa.Y32 = reinterpret_cast<float*>(c.ws + p.off_y32);
+  pa.spi = p.nmat;
   pa.sumsq = reinterpret_cast<float*>(c.ws + p.off_ss);
-  pa.nslots = p.BH * 3;
+  pa.nslots = p.BH * p.nmat;
   pa.dh = dh;
   pa.blocks_per_slot = p.ns_bps;
   if (c.beta) {
-    for (int j = 0; j < 3; ++j) pa.M[j] = c.M[j];
+    for (int j = 0; j < p.nmat; ++j) pa.M[j] = c.M[j];
     pa.bbar = bbar_of(c);
     pa.bbar_stride = kBetaBatch;
   }
@@ -293,17 +327,22 @@ int newton_schulz(Ctx& c) {
   if (rc) return rc;
   const int m = p.m, d = p.d, h = p.h;
   // segment 0: W1 and W3 stored h x d; segment 1: W2 stored d x h
+  // (linear: one segment, the d x d matrix)
   const int rows[2] = {h, d}, cols[2] = {d, h};
+  const int nseg = p.linear ? 1 : 2;
+  auto group_of = [&](int g) { return p.linear ? 1 : (g == 0 ? 2 : 1); };
+  auto slot_of = [&](int g) { return p.linear ? 0 : (g == 0 ? 0 : 1); };
   if (p.ns_fp16 && m <= kNsFusedM && std::max(d, h) <= kNsFusedN) {
     // small matrices: every step of one matrix in one workgroup
     const int n = std::max(d, h);
-    for (int g = 0; g < 2; ++g) {
+    for (int g = 0; g < nseg; ++g) {
       NsFusedArgs f{};
       f.Y32 = pa.Y32;
+      f.spi = p.nmat;
       f.Yb = c.ws + p.off_yb[0];
       f.ystride = dh;
-      f.group = g == 0 ? 2 : 1;
-      f.slot_off[0] = g == 0 ? 0 : 1;
+      f.group = group_of(g);
+      f.slot_off[0] = slot_of(g);
       f.slot_off[1] = 2;
       f.rows = rows[g];
       f.cols = cols[g];
@@ -324,6 +363,7 @@ int newton_schulz(Ctx& c) {
   for (int t = 0; t < c.dsc->ns_steps; ++t) {
     NsArgs a{};
     a.Y32 = pa.Y32;
+    a.spi = p.nmat;
     a.Yin = c.ws + p.off_yb[t & 1];
     a.Yout = c.ws + p.off_yb[(t + 1) & 1];
     a.Ab = c.ws + p.off_ab;
@@ -334,14 +374,14 @@ int newton_schulz(Ctx& c) {
     a.ca = 3.4445f;
     a.cb = -4.7750f;
     a.cc = 2.0315f;
-    a.nseg = 2;
+    a.nseg = nseg;
     for (int phase = 0; phase < 3; ++phase) {
       a.total_blocks = 0;
       double fl = 0.0;
-      for (int g = 0; g < 2; ++g) {
+      for (int g = 0; g < nseg; ++g) {
         NsSeg& sg = a.seg[g];
-        sg.group = g == 0 ? 2 : 1;
-        sg.slot_off[0] = g == 0 ? 0 : 1;
+        sg.group = group_of(g);
+        sg.slot_off[0] = slot_of(g);
         sg.slot_off[1] = 2;
         sg.ldy = cols[g];
         const bool wide = rows[g] <= cols[g];
@@ -373,9 +413,13 @@ int newton_schulz(Ctx& c) {
   return LACT_OK;
 }
 
+int finish_update(Ctx& c);
+int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too);
+
 // One update on key rows [s0, s1); with apply_too, the same launches also
 // apply the current (pre-update) weights to query rows [s0, s1).
 int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
+  if (c.p.linear) return update_chunk_linear(c, s0, s1, apply_too);
   const Plan& p = c.p;
   const int64_t n = s1 - s0;
   const int64_t dh = (int64_t)p.d * p.h;
@@ -455,6 +499,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.out = c.ws + p.off_step;
     g.out_inst = 3 * dh;
     g.out_split = (int64_t)p.BH * 3 * dh;
+    g.out_off = dh;   // W2's partials follow W1's
   }
   if (apply_too) {
     BwdSeg& o = b.seg[nb++];
@@ -478,11 +523,21 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   rc = timed(LACT_KCLASS_BWD, bfl, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
   if (rc) return rc;
 
+  return finish_update(c);
+}
+
+// The gradient partials are in place: Newton-Schulz (Muon) and the weight
+// update with its row normalisation and the operand copies.
+int finish_update(Ctx& c) {
+  const Plan& p = c.p;
+  const int64_t dh = (int64_t)p.d * p.h;
+  int rc = LACT_OK;
   UpdArgs u{};
-  for (int m = 0; m < 3; ++m) {
+  for (int m = 0; m < p.nmat; ++m) {
     u.W[m] = c.W[m];
     u.Wb[m] = p.bf16 ? (void*)(c.ws + p.off_wb[m]) : nullptr;
   }
+  u.nmat = p.nmat;
   if (p.muon) {
     rc = newton_schulz(c);
     if (rc) return rc;
@@ -492,9 +547,9 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   } else {
     u.step = reinterpret_cast<const float*>(c.ws + p.off_step);
     u.nsplit = p.nsplit;
-    u.step_split = (int64_t)p.BH * 3 * dh;
+    u.step_split = (int64_t)p.BH * p.nmat * dh;
     if (c.beta) {   // with Muon the state was advanced before Newton-Schulz
-      for (int j = 0; j < 3; ++j) u.M[j] = c.M[j];
+      for (int j = 0; j < p.nmat; ++j) u.M[j] = c.M[j];
       u.bbar = bbar_of(c);
       u.bbar_stride = kBetaBatch;
     }
@@ -502,8 +557,64 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   u.BH = p.BH;
   u.d = p.d;
   u.h = p.h;
-  u.rows_total = p.BH * (2 * p.h + p.d);
+  u.rows_total = p.BH * (p.linear ? p.d : 2 * p.h + p.d);
   return timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] { return launch_update(u, p.bf16, c.s); });
+}
+
+// Linear fast weight f_W(x) = W x (W: d x d): the gradient partials
+// P = sum_i v_i (eta_i k_i)^T (= -g) of key rows [s0, s1) from eta k and V in
+// one GRAD2 contraction, with the apply o = W q of the same rows in the same
+// launch when apply_too.
+int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
+  const Plan& p = c.p;
+  const int64_t n = s1 - s0;
+  const int64_t dd = (int64_t)p.d * p.d;
+  int rc = timed(LACT_KCLASS_FWD, 0.0, c.s, [&] {
+    return launch_scale_rows(c.k + s0 * p.d * p.esz, c.eta + s0, c.ws + p.off_upd[0], p.BH, n, p.d,
+                             c.dsc->n_kv * p.d, c.dsc->n_kv, p.C * p.d, p.bf16, c.s);
+  });
+  if (rc) return rc;
+  BwdArgs b{};
+  int nb = 0;
+  const TileShape g2 = bwd_tile(BWD_GRAD2, p.bf16);
+  {
+    BwdSeg& g = b.seg[nb++];
+    g.kind = BWD_GRAD2;
+    g.tiles_m = (int)cdiv(p.d, g2.rows);
+    g.tiles_n = (int)cdiv(p.d, g2.cols);
+    g.nsplit = p.nsplit;
+    g.nblocks = p.BH * g.tiles_m * g.tiles_n * p.nsplit;
+    g.rows = n;
+    g.split_len = p.split_len;
+    g.a0 = op(c.v + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);   // V
+    g.b0 = op(c.ws + p.off_upd[0], p.d, p.C * p.d);               // eta K
+    g.out = c.ws + p.off_step;
+    g.out_inst = dd;
+    g.out_split = (int64_t)p.BH * dd;
+    g.out_off = 0;
+  }
+  if (apply_too) {
+    BwdSeg& o = b.seg[nb++];
+    o.kind = BWD_OUT;
+    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16).rows);
+    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16).cols);
+    o.nsplit = 1;
+    o.nblocks = p.BH * o.tiles_m * o.tiles_n;
+    o.rows = n;
+    o.a0 = op(c.q + s0 * p.d * p.esz, p.d, c.dsc->n_q * p.d);
+    o.b0 = c.wop[0];
+    o.out = c.o + s0 * p.d * p.esz;
+    o.out_inst = c.dsc->n_q * p.d;
+  }
+  b.nseg = nb;
+  b.total_blocks = 0;
+  for (int i = 0; i < nb; ++i) b.total_blocks += b.seg[i].nblocks;
+  b.d = p.d;
+  b.h = p.d;   // OUT contracts over d; GRAD2's columns run over d
+  const double bfl = (apply_too ? 2.0 : 0.0) * p.BH * n * dd + 2.0 * p.BH * n * dd;
+  rc = timed(LACT_KCLASS_BWD, bfl, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
+  if (rc) return rc;
+  return finish_update(c);
 }
 
 // Validation and context of every entry point (no HIP call); beta == nullptr
@@ -515,14 +626,15 @@ int setup(Ctx& c, const lact_desc* desc, const void* q, const void* k, const voi
   int rc = check_desc(desc);
   if (rc) return rc;
   const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
-  if (!W1 || !W2 || !W3) return LACT_EINVAL;
+  const bool linear = desc->fast_weight == LACT_FW_LINEAR;   // W2, W3 (M2, M3) unused
+  if (!W1 || (!linear && (!W2 || !W3))) return LACT_EINVAL;
   if (any_q && (!q || !o)) return LACT_EINVAL;
   if (any_kv && (!k || !v || !eta)) return LACT_EINVAL;
-  if (M && (!M[0] || !M[1] || !M[2] || (any_kv && !beta))) return LACT_EINVAL;
-  if (misaligned(W1) || misaligned(W2) || misaligned(W3)) return LACT_EALIGN;
+  if (M && (!M[0] || (!linear && (!M[1] || !M[2])) || (any_kv && !beta))) return LACT_EINVAL;
+  if (misaligned(W1) || (!linear && (misaligned(W2) || misaligned(W3)))) return LACT_EALIGN;
   if (any_q && (misaligned(q) || misaligned(o))) return LACT_EALIGN;
   if (any_kv && (misaligned(k) || misaligned(v) || ((uintptr_t)eta & 3))) return LACT_EALIGN;
-  if (M && (misaligned(M[0]) || misaligned(M[1]) || misaligned(M[2]))) return LACT_EALIGN;
+  if (M && (misaligned(M[0]) || (!linear && (misaligned(M[1]) || misaligned(M[2]))))) return LACT_EALIGN;
   if (M && any_kv && ((uintptr_t)beta & 3)) return LACT_EALIGN;
   c = Ctx{};
   c.dsc = desc;
@@ -551,7 +663,7 @@ int prepare_weights(Ctx& c) {
   const Plan& p = c.p;
   const int64_t dh = (int64_t)p.d * p.h;
   if (p.bf16) {
-    const float* Wf[3] = {c.W[0], c.W[1], c.W[2]};
+    const float* Wf[3] = {c.W[0], p.linear ? nullptr : c.W[1], p.linear ? nullptr : c.W[2]};
     void* Wb[3] = {c.ws + p.off_wb[0], c.ws + p.off_wb[1], c.ws + p.off_wb[2]};
     const int rc = timed(LACT_KCLASS_PREP, 0.0, c.s, [&] { return launch_prep(Wf, Wb, p.BH, p.d, p.h, c.s); });
     if (rc) return rc;

@@ -61,6 +61,7 @@ struct BwdSeg {
   void* out;            // OUT: o rows; GRAD: fp32 partials
   int64_t out_inst;     // elements between instances
   int64_t out_split;    // GRAD: elements between splits
+  int64_t out_off;      // GRAD2: offset of its matrix in an instance's partials
 };
 
 struct BwdArgs {
@@ -78,7 +79,8 @@ struct UpdArgs {
   int nsplit;
   int64_t step_split;   // elements between splits
   int BH, d, h;
-  int rows_total;       // BH * (2h + d)
+  int nmat;             // fast-weight matrices per instance: 3 (SwiGLU) or 1 (linear, d x d with h = d)
+  int rows_total;       // BH * (2h + d), or BH * d
   // momentum (nullptr M: none): M_j <- bbar * M_j + g_j, and the update uses M
   float* M[3];          // fp32 momentum, same layout as W
   const float* bbar;    // chunk-mean momentum factor of instance i at bbar[i * bbar_stride]
@@ -111,6 +113,7 @@ struct NsArgs {
   int nseg;
   int total_blocks;
   float* Y32;           // fp32 iterate (in place), slot stride ystride
+  int spi;              // slots (matrices) per instance: 3 or 1
   const void* Yin;      // operand copy read this iteration (fp16 or fp32)
   void* Yout;           // operand copy written this iteration
   void* Ab;             // Gram (operand copy; also the b A term of the polynomial), slot stride astride
@@ -124,7 +127,8 @@ struct NsPrepArgs {
   const float* part;    // gradient partials [split][inst][3][d*h]
   int nsplit;
   int64_t part_split;   // elements between splits
-  float* Y32;           // summed gradient, [inst*3 + j][d*h]
+  float* Y32;           // summed gradient, [inst*spi + j][d*h]
+  int spi;              // slots per instance
   float* sumsq;         // per-slot, per-block partial sums of squares
   int nslots;
   int64_t dh;
@@ -154,6 +158,7 @@ struct BetaArgs {
 constexpr int kNsFusedM = 128, kNsFusedN = 256;
 struct NsFusedArgs {
   float* Y32;           // fp32 iterate, slot stride ystride: in = scaled gradient, out = NS result
+  int spi;              // slots per instance
   const void* Yb;       // fp16 copy of the scaled gradient, same layout
   int64_t ystride;
   int group;            // matrices per instance in this launch (1 or 2)
@@ -202,6 +207,10 @@ TileShape ns_tile(bool fp16, bool big);       // tile-space rows x columns of th
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, bool io_bf16, hipStream_t s);
 hipError_t launch_update(const UpdArgs& a, bool io_bf16, hipStream_t s);
+// out[i][t] = eta[i][t] * k[i][t] for t < n (rows of d elements, io dtype).
+hipError_t launch_scale_rows(const void* k, const float* eta, void* out, int BH, int64_t n, int d, int64_t k_inst,
+                             int64_t eta_inst, int64_t out_inst, bool io_bf16, hipStream_t s);
+// W[1] == nullptr: one matrix (W[0] -> Wb[0]).
 hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d, int h,
                        hipStream_t s);
 // Newton-Schulz operand copies are fp16 (bf16 I/O: 4x finer rounding than bf16

@@ -1146,7 +1146,7 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int i = acc_row<K2>(mi, r);
-          if (i < mrows && j < ncols) part[dh + (r0 + i) * h + c0 + j] = acc[0][mi][ni][r];
+          if (i < mrows && j < ncols) part[sg.out_off + (r0 + i) * h + c0 + j] = acc[0][mi][ni][r];
         }
       }
   }
@@ -1175,7 +1175,7 @@ __global__ __launch_bounds__(256) void k_update(const UpdArgs a) {
   const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (wave >= a.rows_total) return;
-  const int rows_inst = 2 * a.h + a.d;
+  const int rows_inst = a.nmat == 1 ? a.h : 2 * a.h + a.d;
   const int inst = wave / rows_inst;
   int r = wave - inst * rows_inst;
   int mat, L;
@@ -1190,7 +1190,7 @@ __global__ __launch_bounds__(256) void k_update(const UpdArgs a) {
   const int64_t dh = (int64_t)a.d * a.h;
   const int64_t off = inst * dh + (int64_t)r * L;
   float4* W = reinterpret_cast<float4*>(a.W[mat] + off);
-  const float4* P = reinterpret_cast<const float4*>(a.step + inst * 3 * dh + mat * dh + (int64_t)r * L);
+  const float4* P = reinterpret_cast<const float4*>(a.step + inst * a.nmat * dh + mat * dh + (int64_t)r * L);
   const int64_t ps = a.step_split >> 2;
   float4* Mv = a.M[0] ? reinterpret_cast<float4*>(a.M[mat] + off) : nullptr;
   float4 w[NV], u[NV], m[NV];
@@ -1255,8 +1255,30 @@ __global__ __launch_bounds__(256) void k_prep(const float* w1, const float* w2, 
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n) {
     b1[i] = (__bf16)w1[i];
-    b2[i] = (__bf16)w2[i];
-    b3[i] = (__bf16)w3[i];
+    if (w2) {   // null for a single fast-weight matrix
+      b2[i] = (__bf16)w2[i];
+      b3[i] = (__bf16)w3[i];
+    }
+  }
+}
+
+// eta_i * k_i for tokens [0, n) of every instance (the linear fast weight's
+// gradient operand), rows of d elements, 16 bytes per lane: out [BH][C][d].
+template <typename T>
+__global__ __launch_bounds__(256) void k_scale_rows(const T* k, const float* eta, T* out, int64_t n, int d,
+                                                    int64_t k_inst, int64_t eta_inst, int64_t out_inst, int64_t total) {
+  constexpr int EPV = 16 / sizeof(T);
+  const int vpr = d / EPV;   // 16-byte vectors per row
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t row = i / vpr, inst = row / n, t = row - inst * n;
+    const int c = (int)(i - row * vpr) * EPV;
+    const float e = eta[inst * eta_inst + t];
+    typedef __attribute__((ext_vector_type(EPV))) T tv;
+    const tv x = *reinterpret_cast<const tv*>(k + inst * k_inst + t * d + c);
+    tv y;
+#pragma unroll
+    for (int j = 0; j < EPV; ++j) y[j] = (T)(e * (float)x[j]);
+    *reinterpret_cast<tv*>(out + inst * out_inst + t * d + c) = y;
   }
 }
 
@@ -1364,7 +1386,7 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
   const int q = bid / per;
   const int rr = bid - q * per;
   const int64_t i0 = (int64_t)(rr / sg.tiles_n) * KK::ROWS_A, j0 = (int64_t)(rr % sg.tiles_n) * KK::ROWS_B;
-  const int64_t slot = (int64_t)(q / sg.group) * 3 + sg.slot_off[q % sg.group];
+  const int64_t slot = (int64_t)(q / sg.group) * args.spi + sg.slot_off[q % sg.group];
   const int m = args.m, ldy = sg.ldy;
   const int64_t mrows = sg.M - i0, ncols = sg.N - j0;
   float* Y32 = args.Y32 + slot * args.ystride;
@@ -1506,7 +1528,7 @@ __global__ __launch_bounds__(512) void k_ns_fused(const NsFusedArgs a) {
   const uint32_t xb = lds_addr(xs), ab = lds_addr(as_), bb = lds_addr(bs);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, half = lane >> 5;
   const int q = blockIdx.x;
-  const int64_t slot = (int64_t)(q / a.group) * 3 + a.slot_off[q % a.group];
+  const int64_t slot = (int64_t)(q / a.group) * a.spi + a.slot_off[q % a.group];
   float* Y32 = a.Y32 + slot * a.ystride;
   const _Float16* Yb = reinterpret_cast<const _Float16*>(a.Yb) + slot * a.ystride;
   const int sr = a.rows, sc = a.cols;                   // valid stored rows, columns
@@ -1680,7 +1702,7 @@ __global__ __launch_bounds__(256) void k_ns_prep(const NsPrepArgs a) {
   const int slot = blockIdx.x / a.blocks_per_slot;
   const int blk = blockIdx.x - slot * a.blocks_per_slot;
   const int64_t base = (int64_t)slot * a.dh;
-  const int inst = slot / 3, j = slot - 3 * (slot / 3);
+  const int inst = slot / a.spi, j = slot - a.spi * (slot / a.spi);
   float* Ms = a.M[0] ? a.M[j] + (int64_t)inst * a.dh : nullptr;
   const float bb = Ms ? a.bbar[(int64_t)inst * a.bbar_stride] : 0.f;
   float ss = 0.f;
@@ -1860,6 +1882,22 @@ hipError_t launch_update(const UpdArgs& a, bool io_bf16, hipStream_t s) {
   else if (per_lane <= 4) launch_update_nv<4>(a, io_bf16, blocks, s);
   else if (per_lane <= 8) launch_update_nv<8>(a, io_bf16, blocks, s);
   else launch_update_nv<16>(a, io_bf16, blocks, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_scale_rows(const void* k, const float* eta, void* out, int BH, int64_t n, int d, int64_t k_inst,
+                             int64_t eta_inst, int64_t out_inst, bool io_bf16, hipStream_t s) {
+  const int64_t total = (int64_t)BH * n * (d / (io_bf16 ? 8 : 4));
+  if (total <= 0) return hipSuccess;
+  const int64_t need = (total + 255) / 256, blocks = need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20);
+  if (io_bf16)
+    k_scale_rows<__bf16><<<(unsigned)blocks, 256, 0, s>>>(reinterpret_cast<const __bf16*>(k), eta,
+                                                          reinterpret_cast<__bf16*>(out), n, d, k_inst, eta_inst,
+                                                          out_inst, total);
+  else
+    k_scale_rows<float><<<(unsigned)blocks, 256, 0, s>>>(reinterpret_cast<const float*>(k), eta,
+                                                         reinterpret_cast<float*>(out), n, d, k_inst, eta_inst,
+                                                         out_inst, total);
   return hipGetLastError();
 }
 

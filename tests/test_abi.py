@@ -180,6 +180,18 @@ def test_prologue_and_norm_errors_before_any_hip_call():
     assert L.lact_rmsnorm_out(ctypes.byref(bad), vp(0x1000), vp(0), f(1e-6), vp(0x2000), vp(0)) == -4
 
 
+def test_linear_fast_weight_descriptor():
+    ok = make_desc(**dict(GOOD, h=64, fast_weight=1))
+    assert P.check_desc(ok) == 0
+    assert P.check_desc(make_desc(**dict(GOOD, fast_weight=1))) == -1               # h != d
+    assert P.check_desc(make_desc(**dict(GOOD, h=64, fast_weight=1, eta_per_matrix=1))) == -1
+    assert P.check_desc(make_desc(**dict(GOOD, fast_weight=2))) == -1
+    # W2, W3 may be NULL for the linear weight (validation reaches the workspace)
+    assert _fwd(ok, w2=0, w3=0, ws=0) == -3
+    assert _fwd(make_desc(**GOOD), w2=0, ws=0) == -1
+    assert P.workspace_bytes(ok) < P.workspace_bytes(make_desc(**dict(GOOD, h=64)))
+
+
 def test_timing_api_without_launches():
     P.timing_reset()
     assert P.timing_read(0) == (0, 0.0, 0.0)

@@ -17,7 +17,10 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 @pytest.mark.parametrize("name", [n for n, c in CONFIGS.items() if not c.schedule])
 def test_bench_flops_match_the_oracle_count(name):
     c = CONFIGS[name]
-    ref = O.layer_flops(c.BH, c.d, c.h, c.n_kv, c.n_q, c.n_chunks, bool(c.use_muon), c.ns_steps)
+    if c.linear:
+        ref = O.linear_flops(c.BH, c.d, c.n_kv, c.n_q, c.n_chunks, bool(c.use_muon), c.ns_steps)
+    else:
+        ref = O.layer_flops(c.BH, c.d, c.h, c.n_kv, c.n_q, c.n_chunks, bool(c.use_muon), c.ns_steps)
     assert bench.workload_flops(c) == pytest.approx(ref, rel=1e-12)
 
 

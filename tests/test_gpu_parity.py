@@ -693,3 +693,89 @@ def test_layer_chain_prologue_path_norm():
     ry = O.rmsnorm_out(ref[0], B, H, w, eps=1e-6)
     assert rel(g(q), rq) <= TOL["bf16"]
     assert rel(y.float().cpu().numpy(), ry) <= TOL["bf16"]
+
+
+
+# ----------------------------------------------------------------------------- linear fast weight
+# lact_desc.fast_weight = LACT_FW_LINEAR: f_W(x) = W x, W in R^{d x d} (§4.4).
+
+
+def run_gpu_linear(cfg, x, momentum=False):
+    print(f"[gpu] linear {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} n_kv={cfg.n_kv} n_q={cfg.n_q} C={cfg.chunk} "
+          f"order={cfg.order} muon={cfg.use_muon} momentum={momentum}", flush=True)
+    n = len(x["q"])
+    B, H = (cfg.B, cfg.H) if n == cfg.BH else (n, 1)
+    sh = lambda a: a.reshape(B, H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    W = to_dev(sh(x["W1"]), cfg, torch.float32)
+    kw = {"beta": to_dev(sh(x["beta"]), cfg, torch.float32)} if momentum else {}
+    r = P.forward_linear(q, k, v, eta, W, cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
+                         ns_steps=cfg.ns_steps, **kw)
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    return (f(r[0]), f(W), f(r[1])) if momentum else (f(r), f(W))
+
+
+def check_linear(cfg, x, got, instances=None, momentum=False):
+    idx = slice(None) if instances is None else list(instances)
+    ref = O.lact_forward_linear(x["q"], x["k"], x["v"], x["eta"], x["W1"], cfg.chunk, cfg.order,
+                                bool(cfg.use_muon), cfg.ns_steps, instances=instances,
+                                beta=x.get("beta") if momentum else None)
+    w0 = x["W1"][idx].astype(np.float64)
+    errs = {"o": rel(got[0][idx], ref[0]), "W": rel(got[1][idx], ref[1]),
+            "dW": rel(got[1][idx] - w0, ref[1] - w0)}
+    if momentum:
+        errs["M"] = rel(got[2][idx], ref[2])
+    print("[gpu] rel-L2", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for kk, vv in errs.items():
+        assert vv <= TOL[cfg.io], (kk, vv)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_linear_bf16_ragged(order):
+    cfg = CONFIGS["lm32k"].with_(name="linear", B=1, H=2, d=128, h=128, n_kv=700, n_q=760, chunk=256,
+                                 order=order, linear=1)
+    x = make_inputs(cfg, 41)
+    check_linear(cfg, x, run_gpu_linear(cfg, x))
+
+
+def test_linear_fp32_small():
+    cfg = CONFIGS["tiny_fp32"].with_(name="linear_fp32", B=2, H=1, d=40, h=40, n_kv=300, n_q=333, chunk=100,
+                                     linear=1)
+    x = make_inputs(cfg, 42)
+    check_linear(cfg, x, run_gpu_linear(cfg, x))
+
+
+@pytest.mark.parametrize("io", ["bf16", "fp32"])
+def test_linear_momentum(io):
+    base = CONFIGS["lm32k"] if io == "bf16" else CONFIGS["tiny_fp32"]
+    cfg = base.with_(name="linear_mom_" + io, B=1, H=2, d=64, h=64, n_kv=600, n_q=600, chunk=256, linear=1,
+                     momentum=1)
+    x = make_inputs(cfg, 43)
+    check_linear(cfg, x, run_gpu_linear(cfg, x, momentum=True), momentum=True)
+
+
+@pytest.mark.parametrize("d", [128, 512])
+def test_linear_muon_two_chunks(d):
+    # d = 128: the one-workgroup Newton-Schulz kernel; d = 512: the per-product launches
+    cfg = CONFIGS["lm32k_muon"].with_(name="linear_muon", B=1, H=2, d=d, h=d, n_kv=512, n_q=512, chunk=256,
+                                      linear=1)
+    x = make_inputs(cfg, 44)
+    check_linear(cfg, x, run_gpu_linear(cfg, x))
+
+
+def test_linear_nvs_shape_reduced_context():
+    cfg = CONFIGS["nvs256k_linear"].with_(name="nvs8k_linear", n_kv=8192, n_q=8192 + 2048, chunk=8192)
+    x = make_inputs(cfg, 45)
+    check_linear(cfg, x, run_gpu_linear(cfg, x))
+
+
+def test_linear_eta_zero_is_a_plain_product():
+    cfg = CONFIGS["lm32k"].with_(name="linear_eta0", B=1, H=2, d=128, h=128, n_kv=512, n_q=512, chunk=128,
+                                 linear=1)
+    x = make_inputs(cfg, 46)
+    x["eta"][:] = 0.0
+    o, W = run_gpu_linear(cfg, x)
+    assert np.array_equal(W, x["W1"])
+    assert rel(o, np.einsum("bnd,bed->bne", x["q"].astype(np.float64), x["W1"].astype(np.float64))) <= TOL["bf16"]

@@ -1264,14 +1264,17 @@ __global__ __launch_bounds__(256) void k_prep(const float* w1, const float* w2, 
 
 // eta_i * k_i for tokens [0, n) of every instance (the linear fast weight's
 // gradient operand), rows of d elements, 16 bytes per lane: out [BH][C][d].
-template <typename T>
+// IX: index type of the divisions (32 bits when every index fits; a 64-bit
+// division per 16-byte vector costs more than the vector's traffic).
+template <typename T, typename IX>
 __global__ __launch_bounds__(256) void k_scale_rows(const T* k, const float* eta, T* out, int64_t n, int d,
                                                     int64_t k_inst, int64_t eta_inst, int64_t out_inst, int64_t total) {
   constexpr int EPV = 16 / sizeof(T);
-  const int vpr = d / EPV;   // 16-byte vectors per row
+  const IX vpr = (IX)(d / EPV);   // 16-byte vectors per row
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
-    const int64_t row = i / vpr, inst = row / n, t = row - inst * n;
-    const int c = (int)(i - row * vpr) * EPV;
+    const IX ii = (IX)i, rowi = ii / vpr, insti = rowi / (IX)n;
+    const int64_t row = rowi, inst = insti, t = (int64_t)(rowi - insti * (IX)n);
+    const int c = (int)(ii - rowi * vpr) * EPV;
     const float e = eta[inst * eta_inst + t];
     typedef __attribute__((ext_vector_type(EPV))) T tv;
     const tv x = *reinterpret_cast<const tv*>(k + inst * k_inst + t * d + c);
@@ -1890,14 +1893,18 @@ hipError_t launch_scale_rows(const void* k, const float* eta, void* out, int BH,
   const int64_t total = (int64_t)BH * n * (d / (io_bf16 ? 8 : 4));
   if (total <= 0) return hipSuccess;
   const int64_t need = (total + 255) / 256, blocks = need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20);
-  if (io_bf16)
-    k_scale_rows<__bf16><<<(unsigned)blocks, 256, 0, s>>>(reinterpret_cast<const __bf16*>(k), eta,
-                                                          reinterpret_cast<__bf16*>(out), n, d, k_inst, eta_inst,
-                                                          out_inst, total);
-  else
-    k_scale_rows<float><<<(unsigned)blocks, 256, 0, s>>>(reinterpret_cast<const float*>(k), eta,
-                                                         reinterpret_cast<float*>(out), n, d, k_inst, eta_inst,
-                                                         out_inst, total);
+  const bool small = total < ((int64_t)1 << 31);
+  if (io_bf16) {
+    const __bf16* kk = reinterpret_cast<const __bf16*>(k);
+    __bf16* oo = reinterpret_cast<__bf16*>(out);
+    if (small) k_scale_rows<__bf16, uint32_t><<<(unsigned)blocks, 256, 0, s>>>(kk, eta, oo, n, d, k_inst, eta_inst, out_inst, total);
+    else k_scale_rows<__bf16, uint64_t><<<(unsigned)blocks, 256, 0, s>>>(kk, eta, oo, n, d, k_inst, eta_inst, out_inst, total);
+  } else {
+    const float* kk = reinterpret_cast<const float*>(k);
+    float* oo = reinterpret_cast<float*>(out);
+    if (small) k_scale_rows<float, uint32_t><<<(unsigned)blocks, 256, 0, s>>>(kk, eta, oo, n, d, k_inst, eta_inst, out_inst, total);
+    else k_scale_rows<float, uint64_t><<<(unsigned)blocks, 256, 0, s>>>(kk, eta, oo, n, d, k_inst, eta_inst, out_inst, total);
+  }
   return hipGetLastError();
 }
 

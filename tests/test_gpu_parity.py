@@ -779,3 +779,40 @@ def test_linear_eta_zero_is_a_plain_product():
     o, W = run_gpu_linear(cfg, x)
     assert np.array_equal(W, x["W1"])
     assert rel(o, np.einsum("bnd,bed->bne", x["q"].astype(np.float64), x["W1"].astype(np.float64))) <= TOL["bf16"]
+
+
+# ----------------------------------------------------------------------------- envelope limits
+# The largest head and hidden dims (4096), very many instances, the most
+# Newton-Schulz steps, and a chunk longer than the sequence.
+
+
+def test_largest_dims_bf16():
+    # d = h = 4096: 64 K tiles per contraction and 32 hidden tiles; two ragged chunks
+    cfg = CONFIGS["lm32k"].with_(name="dim4096", B=1, H=1, d=4096, h=4096, n_kv=96, n_q=130, chunk=64, order=1)
+    x = make_inputs(cfg, 51)
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
+def test_largest_dims_fp32_wide_hidden():
+    cfg = CONFIGS["tiny_fp32"].with_(name="dim4096_fp32", B=1, H=1, d=64, h=4096, n_kv=80, n_q=80, chunk=48)
+    x = make_inputs(cfg, 52)
+    # with 4096 hidden units each row of W1, W3 moves by ~1e-4 of its norm at
+    # the default rates, which the fp32 state resolves in dW only to ~1e-3;
+    # larger rates make the change measurable at the 1e-4 bar
+    x["eta"] *= 30.0
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
+def test_many_instances_sampled():
+    # 65536 (batch, head) instances of the smallest bf16 shape
+    cfg = CONFIGS["lm32k"].with_(name="many_inst", B=256, H=256, d=32, h=32, n_kv=64, n_q=70, chunk=32)
+    x = make_inputs(cfg, 53)
+    got = run_gpu(cfg, x)
+    inst = [0, 12345, 65535]
+    check(cfg, x, got, run_oracle(cfg, x, instances=inst), instances=inst)
+
+
+def test_most_newton_schulz_steps_and_chunk_longer_than_sequence():
+    cfg = CONFIGS["video"].with_(name="ns16", B=1, H=2, d=64, h=128, n_kv=200, n_q=220, chunk=1000, ns_steps=16)
+    x = make_inputs(cfg, 54)
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))

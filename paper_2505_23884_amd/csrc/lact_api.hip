@@ -38,7 +38,7 @@ struct Plan {
   int ns_bps;         // blocks of kNsBlockElems per gradient
   // workspace offsets (bytes)
   size_t off_wb[3], off_hq, off_upd[3], off_step, off_bbar, total;
-  size_t off_y32, off_yb[2], off_ab, off_bb, off_ss;
+  size_t off_y32, off_yb[2], off_ab, off_a2, off_bb, off_ss;
 };
 
 int check_desc(const lact_desc* d) {
@@ -141,6 +141,8 @@ Plan make_plan(const lact_desc* dsc) {
       o = align_up(o + slots * dh * p.ns_esz);
     }
     p.off_ab = o;
+    o = align_up(o + slots * mm * p.ns_esz);
+    p.off_a2 = o;
     o = align_up(o + slots * mm * p.ns_esz);
     p.off_bb = o;
     o = align_up(o + slots * mm * p.ns_esz);
@@ -367,6 +369,7 @@ int newton_schulz(Ctx& c) {
     a.Yin = c.ws + p.off_yb[t & 1];
     a.Yout = c.ws + p.off_yb[(t + 1) & 1];
     a.Ab = c.ws + p.off_ab;
+    a.A2b = c.ws + p.off_a2;
     a.Bb = c.ws + p.off_bb;
     a.ystride = dh;
     a.astride = mm;

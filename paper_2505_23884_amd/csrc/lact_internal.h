@@ -91,8 +91,8 @@ struct UpdArgs {
 // Matrices live in "slots" s = inst*3 + j (j = 0: W1, 1: W2, 2: W3), each in
 // its stored orientation Y [r x c] (W1, W3: h x d; W2: d x h). The iteration
 // runs on the wide orientation of Y:
-//   wide (r <= c):  A = Y Y^T,  B = b A + c A A,  Y <- a Y + B Y
-//   tall (r >  c):  A = Y^T Y,  B = b A + c A A,  Y <- a Y + Y B
+//   wide (r <= c):  A = Y Y^T,  B = A (c A + b I),  Y <- a Y + B Y
+//   tall (r >  c):  A = Y^T Y,  B = A (c A + b I),  Y <- a Y + Y B
 // Each product is computed in "tile space", the transpose of what is stored
 // (NsSeg M, N are tile-space rows and columns): A and B are symmetric; for
 // the update, tile rows are the columns of Y and tile columns its rows.
@@ -116,7 +116,8 @@ struct NsArgs {
   int spi;              // slots (matrices) per instance: 3 or 1
   const void* Yin;      // operand copy read this iteration (fp16 or fp32)
   void* Yout;           // operand copy written this iteration
-  void* Ab;             // Gram (operand copy; also the b A term of the polynomial), slot stride astride
+  void* Ab;             // Gram operand copy, slot stride astride
+  void* A2b;            // c A + b I (the polynomial's second factor), same layout
   void* Bb;             // polynomial operand copy
   int64_t ystride, astride;
   int m;                // Gram size min(d, h)

@@ -1308,7 +1308,7 @@ __global__ __launch_bounds__(256) void k_scale_rows(const T* k, const float* eta
 template <typename T, class KK>
 __device__ __forceinline__ void ns_epilogue_staged(const Acc<KK>& acc, uint8_t* smem, const NsArgs& args, int kind,
                                                    int64_t ld, int64_t i0, int64_t j0, int64_t mrows, int64_t ncols,
-                                                   void* Abw, float* Y32, void* Yout, void* Bbw) {
+                                                   void* Abw, void* A2w, float* Y32, void* Yout, void* Bbw) {
   constexpr int R = KK::ROWS_A;                  // tile rows = stored columns
   constexpr int SR = KK::WN * 32;                // staged stored rows per half
   constexpr int CPR = R / 4;                     // 16-byte chunks per staged row
@@ -1334,6 +1334,7 @@ __device__ __forceinline__ void ns_epilogue_staged(const Acc<KK>& acc, uint8_t* 
     lds_barrier();
     int64_t gidx[PER];
     bool ok[PER];
+    int dgn[PER];
     float4 old[PER];
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
@@ -1342,8 +1343,8 @@ __device__ __forceinline__ void ns_epilogue_staged(const Acc<KK>& acc, uint8_t* 
       const int c = (srow / 32) * (KK::NI * 32) + half * 32 + (srow & 31);   // stored row in the tile
       ok[i] = c < ncols && ch * 4 < mrows;
       gidx[i] = (j0 + c) * ld + i0 + ch * 4;
-      if (ok[i] && kind == NS_POLY) old[i] = ld4<T>(Abw, gidx[i]);
-      else if (ok[i] && !gram) old[i] = *reinterpret_cast<const float4*>(Y32 + gidx[i]);
+      dgn[i] = (int)(j0 + c - (i0 + ch * 4));
+      if (ok[i] && !gram && kind != NS_POLY) old[i] = *reinterpret_cast<const float4*>(Y32 + gidx[i]);
     }
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
@@ -1353,10 +1354,13 @@ __device__ __forceinline__ void ns_epilogue_staged(const Acc<KK>& acc, uint8_t* 
       if (!ok[i]) continue;
       if (gram) {
         st4<T>(Abw, gidx[i], v.x, v.y, v.z, v.w);
+        // c A + b I, the polynomial's second factor: element e of the four is
+        // on the diagonal when the stored row minus the first column is e
+        const int dg = dgn[i];
+        st4<T>(A2w, gidx[i], args.cc * v.x + (dg == 0 ? args.cb : 0.0f), args.cc * v.y + (dg == 1 ? args.cb : 0.0f),
+               args.cc * v.z + (dg == 2 ? args.cb : 0.0f), args.cc * v.w + (dg == 3 ? args.cb : 0.0f));
       } else if (kind == NS_POLY) {
-        const float4 o = old[i];
-        st4<T>(Bbw, gidx[i], args.cb * o.x + args.cc * v.x, args.cb * o.y + args.cc * v.y,
-               args.cb * o.z + args.cc * v.z, args.cb * o.w + args.cc * v.w);
+        st4<T>(Bbw, gidx[i], v.x, v.y, v.z, v.w);
       } else {
         const float4 o = old[i];
         const float4 y = make_float4(args.ca * o.x + v.x, args.ca * o.y + v.y, args.ca * o.z + v.z,
@@ -1397,6 +1401,8 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
   void* Yout = reinterpret_cast<uint8_t*>(args.Yout) + slot * args.ystride * esz;
   const uint8_t* Ab = reinterpret_cast<const uint8_t*>(args.Ab) + slot * args.astride * esz;
   void* Abw = reinterpret_cast<uint8_t*>(args.Ab) + slot * args.astride * esz;
+  const uint8_t* A2 = reinterpret_cast<const uint8_t*>(args.A2b) + slot * args.astride * esz;
+  void* A2w = reinterpret_cast<uint8_t*>(args.A2b) + slot * args.astride * esz;
   const uint8_t* Bb = reinterpret_cast<const uint8_t*>(args.Bb) + slot * args.astride * esz;
   void* Bbw = reinterpret_cast<uint8_t*>(args.Bb) + slot * args.astride * esz;
   Acc<KK> acc;   // same accumulator shape for every NS kind
@@ -1409,9 +1415,9 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
     const View ops[2] = {View{Yin + i0 * esz, (int64_t)ldy * esz, mrows, sg.K},
                          View{Yin + j0 * esz, (int64_t)ldy * esz, ncols, sg.K}};
     mainloop<T, KM>(smem, ops, sg.K, acc);
-  } else if (kind == NS_POLY) {     // A A (A symmetric, so A A^T)
+  } else if (kind == NS_POLY) {     // A (c A + b I) = b A + c A A (both symmetric: A A2^T)
     const View ops[2] = {View{Ab + i0 * m * esz, (int64_t)m * esz, mrows, sg.K},
-                         View{Ab + j0 * m * esz, (int64_t)m * esz, ncols, sg.K}};
+                         View{A2 + j0 * m * esz, (int64_t)m * esz, ncols, sg.K}};
     mainloop<T, KK>(smem, ops, sg.K, acc);
   } else if (kind == NS_UPD_BY) {   // (B Y)^T = Y^T B (Y wide, B symmetric): rows = Y columns
     const View ops[2] = {View{Yin + i0 * esz, (int64_t)ldy * esz, mrows, sg.K},
@@ -1425,7 +1431,7 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
   const bool gram = kind == NS_GRAM_K || kind == NS_GRAM_MN;
   const int64_t ld = (gram || kind == NS_POLY) ? m : ldy;
   if constexpr (sizeof(T) == 2) {
-    ns_epilogue_staged<T, KK>(acc, smem, args, kind, ld, i0, j0, mrows, ncols, Abw, Y32, Yout, Bbw);
+    ns_epilogue_staged<T, KK>(acc, smem, args, kind, ld, i0, j0, mrows, ncols, Abw, A2w, Y32, Yout, Bbw);
     return;
   }
 #pragma unroll
@@ -1443,10 +1449,11 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
         const int64_t idx = (j0 + c) * ld + i0 + r;   // stored row j0+c, columns i0+r ..
         if (gram) {
           st4<T>(Abw, idx, v0, v1, v2, v3);
+          const int dg = (int)(j0 + c - (i0 + r));   // c A + b I (see ns_epilogue_staged)
+          st4<T>(A2w, idx, args.cc * v0 + (dg == 0 ? args.cb : 0.0f), args.cc * v1 + (dg == 1 ? args.cb : 0.0f),
+                 args.cc * v2 + (dg == 2 ? args.cb : 0.0f), args.cc * v3 + (dg == 3 ? args.cb : 0.0f));
         } else if (kind == NS_POLY) {
-          const float4 o = ld4<T>(Abw, idx);
-          st4<T>(Bbw, idx, args.cb * o.x + args.cc * v0, args.cb * o.y + args.cc * v1, args.cb * o.z + args.cc * v2,
-                 args.cb * o.w + args.cc * v3);
+          st4<T>(Bbw, idx, v0, v1, v2, v3);
         } else {
           const float4 o = *reinterpret_cast<const float4*>(Y32 + idx);
           const float4 y =

@@ -10,20 +10,26 @@
 //               (§3.1 loss and chunk-gradient eqs.; Alg. 1, update)
 //   BWD_OUT     O^T = W2 hidden^T                                  (apply, second matmul)
 //   BWD_GRAD13  P1 = (eta dz1)^T K,  P3 = (eta dz3)^T K             (gradient matmuls, -g1, -g3)
-//   BWD_GRAD2   P2 = V^T (eta hidden)                              (-g2)
-//   NS_*        Newton-Schulz products (Muon, §3.2; App. A)
+//   BWD_GRAD2   P2 = V^T (eta hidden)                              (-g2; the linear
+//               fast weight's gradient V^T (eta K), §4.4, with OUT as its apply)
+//   NS_*        Newton-Schulz products (Muon, §3.2; App. A); k_ns_fused runs
+//               the whole iteration of a small matrix in one workgroup
+// plus the weight update with its row normalisation and momentum (k_update),
+// the Newton-Schulz prologue (k_ns_prep, k_ns_scale), the momentum chunk
+// means (k_beta_mean), operand copies (k_prep), eta k (k_scale_rows) and the
+// zeroing of uncovered output rows (k_zero_rows).
 //
 // 16-bit operands (bf16 I/O; fp16 for Newton-Schulz) run on
 // v_mfma_f32_32x32x16_{bf16,f16}. A workgroup of WM x WN waves owns a tile of
 // (32*MI*WM) x (32*NI*WN) outputs, every wave (32*MI) x (32*NI). Operand tiles
-// of 32 K go from HBM to LDS by raw-buffer DMA (buffer_load_dwordx4 ... lds)
-// into a ring of NSTAGE stages. An operand is either K-contiguous in HBM
-// ("k": row-major [rows x K], kept as 64-byte rows in LDS) or row-contiguous
-// ("mn": row-major [K x rows], the token-major layout; kept as 32 K rows in
-// LDS and read with ds_read_b64_tr_b16, which returns MFMA fragments of the
-// transposed operand). fp32 I/O runs on v_mfma_f32_32x32x2_f32 with a
-// register-staged double buffer (the transposition of mn operands happens in
-// registers there).
+// go from HBM to LDS by raw-buffer DMA (buffer_load_dwordx4 ... lds) into a
+// ring of NSTAGE stages of BK K each. An operand is either K-contiguous in HBM
+// ("k": row-major [rows x K], kept as BK*2-byte rows in LDS, BK = 64 so that
+// every DMA fetches whole 128-byte lines) or row-contiguous ("mn": row-major
+// [K x rows], the token-major layout; BK = 32 K rows in LDS, read with
+// ds_read_b64_tr_b16, which returns MFMA fragments of the transposed operand).
+// fp32 I/O runs on v_mfma_f32_32x32x2_f32 with a register-staged double
+// buffer (the transposition of mn operands happens in registers there).
 #include "lact_internal.h"
 
 namespace lact {
@@ -735,17 +741,6 @@ __device__ __forceinline__ void st_elem(void* base, int64_t idx, float v) {
 }
 
 // Four consecutive elements (8 bytes of 16-bit or 16 bytes of fp32) at idx.
-template <typename T>
-__device__ __forceinline__ float4 ld4(const void* base, int64_t idx) {
-  if constexpr (sizeof(T) == 2) {
-    typedef __attribute__((ext_vector_type(4))) T t4;
-    const t4 v = *reinterpret_cast<const t4*>(reinterpret_cast<const T*>(base) + idx);
-    return make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
-  } else {
-    return *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(base) + idx);
-  }
-}
-
 template <typename T>
 __device__ __forceinline__ void st4(void* base, int64_t idx, float a, float b, float c, float d) {
   if constexpr (sizeof(T) == 2) {

@@ -23,6 +23,12 @@
  * With the linear fast weight (lact_desc.fast_weight, §4.4) the same path
  * runs for f_W(x) = W1 x with W1 in R^{d x d}: o = W1 q, g = -sum eta v k^T.
  *
+ * Entry points: lact_forward (the path above), lact_forward_momentum (the
+ * momentum test-time optimizer, App. A), lact_forward_schedule (a caller-given
+ * list of update/apply segments, Alg. 1), lact_prologue and lact_rmsnorm_out
+ * (the layer's steps on either side of the path, Alg. 1); per-matrix learning
+ * rates through lact_desc.eta_per_matrix.
+ *
  * Math layout per instance: W1, W3 are h x d, W2 is d x h, row-major, fp32.
  * The fast weights are the recurrent state; they are read and written in
  * place, so the caller owns them as the checkpoint between calls.
@@ -33,8 +39,8 @@
  *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
  *    stream) and never synchronise the host, except when the environment
  *    variable LACT_SYNC=1 is set (debugging).
- *  - No allocation happens inside lact_forward or lact_forward_momentum:
- *    all scratch memory is the caller's `workspace`.
+ *  - No entry point allocates memory: all scratch memory is the caller's
+ *    `workspace` (lact_prologue and lact_rmsnorm_out need none).
  *  - Arguments are validated before any HIP call, so every error below is
  *    reported without touching the GPU. Errors are negative return codes;
  *    nothing is thrown across the ABI. On an error no output is written.

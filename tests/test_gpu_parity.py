@@ -177,6 +177,95 @@ def test_nvs_shape_reduced_context():
     check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
 
 
+# ----------------------------------------------------------------------------- full NVS context
+# The NVS workloads at their full sizes, in the launch bench.py times: one
+# update-then-apply chunk over 262144 or 1048576 context tokens, then the
+# 4096 target tokens. The fp64 oracle cannot afford a gradient over a million
+# tokens inside a test, so the tokens repeat with a period of 8191 (a prime: no
+# tile, split or block boundary of the kernels is a multiple of it, so a tile
+# that reads the wrong rows reads different tokens). The chunk gradient is a
+# plain sum over tokens (§3.1), so over n = reps * P + r repeated tokens it is
+# reps * g(first P tokens) + g(first r tokens); the output row i is f_W(q_{i mod P}).
+
+NVS_PERIOD = 8191
+
+
+def periodic(t, n):
+    """t [BH, P, ...] repeated along the token axis and cut to n tokens."""
+    reps = -(-n // t.shape[1])
+    return t.repeat(1, reps, *([1] * (t.dim() - 2)))[:, :n].contiguous()
+
+
+def rel_periodic_rows(o_dev, ref_period):
+    """rel-L2 of o_dev [n, d] (device) against the rows ref_period[i mod P] (fp64)."""
+    ref = torch.from_numpy(np.ascontiguousarray(ref_period, dtype=np.float64)).to("cuda")
+    n, per = o_dev.shape[0], ref.shape[0]
+    num = den = 0.0
+    for s in range(0, n, 1 << 16):
+        e = min(n, s + (1 << 16))
+        r = ref[torch.arange(s, e, device="cuda") % per]
+        num += float(((o_dev[s:e].double() - r) ** 2).sum())
+        den += float((r * r).sum())
+    return (num / den) ** 0.5
+
+
+def nvs_periodic_inputs(cfg, seed):
+    x = make_inputs(cfg.with_(name=cfg.name + "_period", n_kv=NVS_PERIOD, n_q=NVS_PERIOD), seed)
+    print(f"[gpu] {cfg.name} full context n_kv={cfg.n_kv} n_q={cfg.n_q} d={cfg.d} h={cfg.h} "
+          f"period={NVS_PERIOD} muon={cfg.use_muon} linear={cfg.linear}", flush=True)
+    q = periodic(to_dev(x["q"], cfg), cfg.n_q)
+    k, v = (periodic(to_dev(x[a], cfg), cfg.n_kv) for a in ("k", "v"))
+    eta = periodic(to_dev(x["eta"], cfg, torch.float32), cfg.n_kv)
+    return x, (q, k, v, eta)
+
+
+def assert_errs(errs, tol):
+    print("[gpu] rel-L2", {kk: f"{vv:.2e}" for kk, vv in errs.items()}, flush=True)
+    for kk, vv in errs.items():
+        assert vv <= tol, (kk, vv, tol)
+
+
+@pytest.mark.parametrize("name,use_muon", [("nvs256k", 0), ("nvs1m", 0), ("nvs256k", 1)])
+def test_nvs_full_context_periodic_tokens(name, use_muon):
+    cfg = CONFIGS[name].with_(use_muon=use_muon, ns_steps=5 if use_muon else 0)
+    x, (q, k, v, eta) = nvs_periodic_inputs(cfg, 61)
+    W = [to_dev(x[w], cfg, torch.float32) for w in ("W1", "W2", "W3")]
+    o = P.forward(q, k, v, eta, *W, chunk=cfg.chunk, order=cfg.order, use_muon=bool(use_muon),
+                  ns_steps=cfg.ns_steps)
+    torch.cuda.synchronize()
+    reps, r = divmod(cfg.n_kv, NVS_PERIOD)
+    W0 = [x[w][0].astype(np.float64) for w in ("W1", "W2", "W3")]
+    g_per = O.chunk_gradient(*W0, x["k"][0], x["v"][0], x["eta"][0])
+    g_r = O.chunk_gradient(*W0, x["k"][0][:r], x["v"][0][:r], x["eta"][0][:r])
+    g = [reps * a + b for a, b in zip(g_per, g_r)]
+    if use_muon:
+        g = [O.newton_schulz(gj, cfg.ns_steps) for gj in g]
+    Wref = [O.weight_update(w, gj) for w, gj in zip(W0, g)]
+    errs = {"o": rel_periodic_rows(o[0], O.swiglu_apply(*Wref, x["q"][0]))}
+    for j, wn in enumerate(("W1", "W2", "W3")):
+        wg = W[j][0].cpu().numpy().astype(np.float64)
+        errs[wn] = rel(wg, Wref[j])
+        errs["d" + wn] = rel(wg - W0[j], Wref[j] - W0[j])
+    assert_errs(errs, TOL[cfg.io])
+
+
+def test_linear_nvs_full_context_periodic_tokens():
+    cfg = CONFIGS["nvs256k_linear"]
+    x, (q, k, v, eta) = nvs_periodic_inputs(cfg, 62)
+    W = to_dev(x["W1"], cfg, torch.float32)
+    o = P.forward_linear(q, k, v, eta, W, cfg.chunk, order=cfg.order)
+    torch.cuda.synchronize()
+    reps, r = divmod(cfg.n_kv, NVS_PERIOD)
+    W0 = x["W1"][0].astype(np.float64)
+    g = reps * O.linear_gradient(W0, x["k"][0], x["v"][0], x["eta"][0]) + \
+        O.linear_gradient(W0, x["k"][0][:r], x["v"][0][:r], x["eta"][0][:r])
+    Wref = O.weight_update(W0, g)
+    wg = W[0].cpu().numpy().astype(np.float64)
+    errs = {"o": rel_periodic_rows(o[0], x["q"][0].astype(np.float64) @ Wref.T),
+            "W": rel(wg, Wref), "dW": rel(wg - W0, Wref - W0)}
+    assert_errs(errs, TOL[cfg.io])
+
+
 def test_deterministic_and_resumable():
     cfg = CONFIGS["lm32k"].with_(name="resume", B=1, H=2, d=128, h=256, n_kv=1024, n_q=1024, chunk=256)
     x = make_inputs(cfg, 6)

@@ -47,10 +47,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="lm32k")
+    ap.add_argument("--chunk", type=int, default=0,
+                    help="override the workload's chunk size (a chunk-size sweep of one shape)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--library-gemms", action="store_true",
+                    help="time the path's plain contractions as library GEMMs (torch.matmul), for context")
     ap.add_argument("--traffic-report", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"))
     return ap.parse_args()
 
@@ -73,6 +77,59 @@ def copy_calibration():
         torch.mul(src, 1, out=dst)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes": n, "reps": 5}), flush=True)
+
+
+def library_gemms(cfg, reps):
+    """The path's contractions of one step as plain bf16 library GEMMs
+    (torch.matmul, hipBLASLt), without any of the fused elementwise work:
+    per chunk of C tokens and instance, Z = X [W1; W3]^T for the queries and
+    for the keys, D = V W2, O = H W2^T, G13 = [dz1 | dz3]^T K, G2 = V^T H;
+    the apply-only tail adds its Z and O. Reported per contraction and summed
+    over the step, beside nothing else: a reference point for the kernels,
+    which do this work and the elementwise steps in three launches per chunk."""
+    import torch
+    if cfg.linear or cfg.schedule or cfg.io != "bf16":
+        raise SystemExit("--library-gemms covers the uniform-chunk SwiGLU bf16 workloads")
+    BH, d, h, C = cfg.BH, cfg.d, cfg.h, cfg.chunk
+    tail = cfg.n_q - cfg.n_kv
+    gen = torch.Generator(device="cuda:0").manual_seed(0)
+
+    def timed(m, k, n, count):
+        a = torch.randn(BH, m, k, generator=gen, device="cuda:0").to(torch.bfloat16)
+        b = torch.randn(BH, k, n, generator=gen, device="cuda:0").to(torch.bfloat16)
+        if BH == 1:
+            a, b = a[0], b[0]
+        for _ in range(3):
+            torch.matmul(a, b)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        fl = 2.0 * BH * m * k * n
+        del a, b
+        return {"shape": f"[{BH}] {m}x{k} . {k}x{n}", "us": round(us, 2), "tflops": round(fl / us / 1e6, 1),
+                "per_step": count, "step_us": round(us * count, 1)}
+
+    nc = cfg.n_chunks
+    rows = {
+        "Z_queries": timed(C, d, 2 * h, nc),
+        "Z_keys": timed(C, d, 2 * h, nc),
+        "D": timed(C, d, h, nc),
+        "O": timed(C, h, d, nc),
+        "G13": timed(2 * h, C, d, nc),
+        "G2": timed(d, C, h, nc),
+    }
+    if tail > 0:
+        rows["Z_tail"] = timed(tail, d, 2 * h, 1)
+        rows["O_tail"] = timed(tail, h, d, 1)
+    total = sum(r["step_us"] for r in rows.values())
+    print(json.dumps({"library_gemms": describe(cfg), "contractions": rows,
+                      "ms_per_step_gemms_only": round(total / 1e3, 4),
+                      "tflops_gemms_only": round(workload_flops(cfg.with_(use_muon=0)) / (total * 1e-6) / 1e12, 1)}),
+          flush=True)
 
 
 def _pmc(path, counter):
@@ -244,6 +301,13 @@ def main():
     from lact_synth import CONFIGS, make_inputs
 
     cfg = CONFIGS[args.config]
+    if args.chunk:
+        if cfg.schedule or cfg.layer_io:
+            raise SystemExit("--chunk applies to the uniform-chunk workloads")
+        cfg = cfg.with_(name=f"{cfg.name}_c{args.chunk}", chunk=args.chunk)
+    if args.library_gemms:
+        library_gemms(cfg, max(args.steps, 5))
+        return
     dev = torch.device("cuda:0")
     x = make_inputs(cfg, 0)
     io = torch.bfloat16 if cfg.io == "bf16" else torch.float32
@@ -332,6 +396,8 @@ def main():
         "tokens_per_s": round(tokens / dt, 1),
         "pct_of_peak": round(100.0 * tflops / peak, 2),
     }
+    if cfg.use_muon:   # the same time over the token FLOPs alone (Newton-Schulz FLOPs left out)
+        res["value_without_muon_flops"] = round(workload_flops(cfg.with_(use_muon=0)) / dt / 1e12, 3)
 
     if not args.no_roofline:
         P.timing_reset()

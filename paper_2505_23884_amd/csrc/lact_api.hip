@@ -31,13 +31,14 @@ struct Plan {
   int64_t cap;        // rows of the applied-hidden buffer
   int nsplit;         // split-K ways of the gradient contraction
   int64_t split_len;  // tokens per split
+  bool fused;         // gradient and weight update in one kind (BWD_GRAD_UPD)
   bool muon;
   bool ns_fp16;       // Newton-Schulz operand copies in fp16 (bf16 I/O) or fp32
   int ns_esz;
   int m;              // Newton-Schulz Gram size min(d, h)
   int ns_bps;         // blocks of kNsBlockElems per gradient
   // workspace offsets (bytes)
-  size_t off_wb[3], off_hq, off_upd[3], off_step, off_bbar, total;
+  size_t off_wb[3], off_wb2[3], off_hq, off_upd[3], off_step, off_bbar, total;
   size_t off_y32, off_yb[2], off_ab, off_a2, off_bb, off_ss;
 };
 
@@ -108,11 +109,24 @@ Plan make_plan(const lact_desc* dsc) {
   ns = std::min<int64_t>(ns, kMaxSplit);
   p.split_len = std::max<int64_t>(32, cdiv(cdiv(std::max<int64_t>(p.C, 1), ns), 32) * 32);
   p.nsplit = (int)std::max<int64_t>(1, cdiv(std::max<int64_t>(p.C, 1), p.split_len));
+  // The gradient and the weight update (with momentum or without) run as one
+  // kind (BWD_GRAD_UPD) when a tile holds whole rows of W1, W2 and W3
+  // (256 < d, h <= 512: narrower rows would leave most of the tile empty), the
+  // gradient is not split and no Newton-Schulz step sits between the two. The
+  // bf16 operand copies then alternate between two buffers: the apply tiles
+  // of the same launch still read the pre-update W2.
+  const int upd_cols = grad_upd_tile().cols;
+  p.fused = p.bf16 && !p.linear && !dsc->use_muon && p.nsplit == 1 && p.d > 256 && p.h > 256 &&
+            p.d <= upd_cols && p.h <= upd_cols;
   const size_t dh = (size_t)p.d * p.h;
   size_t o = 0;
   for (int m = 0; m < 3; ++m) {
     p.off_wb[m] = o;
     if (p.bf16 && m < p.nmat) o = align_up(o + (size_t)p.BH * dh * 2);
+  }
+  for (int m = 0; m < 3; ++m) {
+    p.off_wb2[m] = o;
+    if (p.fused) o = align_up(o + (size_t)p.BH * dh * 2);
   }
   // linear: no applied hidden (the apply is one product); one update buffer (eta k)
   p.off_hq = o;
@@ -218,6 +232,8 @@ struct Ctx {
   uint8_t* ws;
   hipStream_t s;
   Operand wop[3];   // operand copies of W1, W2, W3 (bf16 copies or the fp32 state)
+  void* wb[2][3];   // the two sets of bf16 copies (the second with BWD_GRAD_UPD)
+  int wset;         // the set wop points at
   const float* beta;   // momentum: per-token factor [BH][n_kv], or nullptr
   float* M[3];         // momentum state (with beta)
   int64_t chunk_idx;   // index of the chunk being updated
@@ -419,6 +435,15 @@ int newton_schulz(Ctx& c) {
 int finish_update(Ctx& c);
 int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too);
 
+// Points the operand views at bf16 copy set `set`.
+void use_wset(Ctx& c, int set) {
+  const int64_t dh = (int64_t)c.p.d * c.p.h;
+  c.wset = set;
+  c.wop[0] = op(c.wb[set][0], c.p.d, dh);
+  c.wop[1] = op(c.wb[set][1], c.p.h, dh);
+  c.wop[2] = op(c.wb[set][2], c.p.d, dh);
+}
+
 // One update on key rows [s0, s1); with apply_too, the same launches also
 // apply the current (pre-update) weights to query rows [s0, s1).
 int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
@@ -469,10 +494,38 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
 
   BwdArgs b{};
   int nb = 0;
+  const bool fused = p.fused;
+  if (fused) {
+    // gradient and update of whole rows (with the momentum state when there
+    // is one); the new bf16 copies go to the other set
+    BwdSeg& g = b.seg[nb++];
+    const int rt = grad_upd_tile().rows;
+    g.kind = BWD_GRAD_UPD;
+    g.tiles_m = (int)(2 * cdiv(p.h, rt) + cdiv(p.d, rt));
+    g.tiles_n = 1;
+    g.nsplit = 1;
+    g.nblocks = p.BH * g.tiles_m;
+    g.rows = n;
+    g.split_len = n;
+    g.a0 = op(c.ws + p.off_upd[1], p.h, p.C * p.h);   // eta dz1
+    g.a1 = op(c.ws + p.off_upd[2], p.h, p.C * p.h);   // eta dz3
+    g.b0 = op(c.k + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
+    g.a2 = op(c.v + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
+    g.b1 = op(c.ws + p.off_upd[0], p.h, p.C * p.h);   // eta hidden
+    for (int m = 0; m < 3; ++m) {
+      g.W[m] = c.W[m];
+      g.Wb[m] = c.wb[c.wset ^ 1][m];
+    }
+    if (c.beta) {
+      for (int m = 0; m < 3; ++m) g.M[m] = c.M[m];
+      g.bbar = bbar_of(c);
+      g.bbar_stride = kBetaBatch;
+    }
+  }
   // Gradient contractions, split over tokens; a split past the chunk's end
   // writes zeros so the update always sums p.nsplit partials.
   const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
-  {
+  if (!fused) {
     BwdSeg& g = b.seg[nb++];
     g.kind = BWD_GRAD13;
     g.tiles_m = (int)cdiv(p.h, g13.rows);
@@ -488,7 +541,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.out_inst = 3 * dh;
     g.out_split = (int64_t)p.BH * 3 * dh;
   }
-  {
+  if (!fused) {
     BwdSeg& g = b.seg[nb++];
     g.kind = BWD_GRAD2;
     g.tiles_m = (int)cdiv(p.d, g2.rows);
@@ -525,7 +578,10 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   const double bfl = (apply_too ? 2.0 : 0.0) * p.BH * n * dh + 6.0 * p.BH * n * dh;
   rc = timed(LACT_KCLASS_BWD, bfl, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
   if (rc) return rc;
-
+  if (fused) {   // the update is done; the next launches read the new copies
+    use_wset(c, c.wset ^ 1);
+    return LACT_OK;
+  }
   return finish_update(c);
 }
 
@@ -538,7 +594,7 @@ int finish_update(Ctx& c) {
   UpdArgs u{};
   for (int m = 0; m < p.nmat; ++m) {
     u.W[m] = c.W[m];
-    u.Wb[m] = p.bf16 ? (void*)(c.ws + p.off_wb[m]) : nullptr;
+    u.Wb[m] = p.bf16 ? c.wb[c.wset][m] : nullptr;
   }
   u.nmat = p.nmat;
   if (p.muon) {
@@ -667,12 +723,14 @@ int prepare_weights(Ctx& c) {
   const int64_t dh = (int64_t)p.d * p.h;
   if (p.bf16) {
     const float* Wf[3] = {c.W[0], p.linear ? nullptr : c.W[1], p.linear ? nullptr : c.W[2]};
-    void* Wb[3] = {c.ws + p.off_wb[0], c.ws + p.off_wb[1], c.ws + p.off_wb[2]};
-    const int rc = timed(LACT_KCLASS_PREP, 0.0, c.s, [&] { return launch_prep(Wf, Wb, p.BH, p.d, p.h, c.s); });
+    for (int m = 0; m < 3; ++m) {
+      c.wb[0][m] = c.ws + p.off_wb[m];
+      c.wb[1][m] = c.ws + p.off_wb2[m];
+    }
+    const int rc =
+        timed(LACT_KCLASS_PREP, 0.0, c.s, [&] { return launch_prep(Wf, c.wb[0], p.BH, p.d, p.h, c.s); });
     if (rc) return rc;
-    c.wop[0] = op(Wb[0], p.d, dh);
-    c.wop[1] = op(Wb[1], p.h, dh);
-    c.wop[2] = op(Wb[2], p.d, dh);
+    use_wset(c, 0);
   } else {
     c.wop[0] = op(c.W[0], p.d, dh);
     c.wop[1] = op(c.W[1], p.h, dh);

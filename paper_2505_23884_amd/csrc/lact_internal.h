@@ -48,7 +48,7 @@ struct FwdArgs {
 };
 
 // ---- second launch: apply GEMM-2 and/or the gradient contractions ---------
-enum BwdKind : int { BWD_OUT = 0, BWD_GRAD13 = 1, BWD_GRAD2 = 2 };
+enum BwdKind : int { BWD_OUT = 0, BWD_GRAD13 = 1, BWD_GRAD2 = 2, BWD_GRAD_UPD = 3 };
 
 struct BwdSeg {
   int kind;
@@ -62,6 +62,16 @@ struct BwdSeg {
   int64_t out_inst;     // elements between instances
   int64_t out_split;    // GRAD: elements between splits
   int64_t out_off;      // GRAD2: offset of its matrix in an instance's partials
+  // GRAD_UPD (16-bit I/O, whole rows per tile, no split): the gradients of
+  // W1 (a0 = eta dz1, b0 = K), W3 (a1 = eta dz3, b0) and W2 (a2 = V,
+  // b1 = eta hidden) and the weight update in one pass; tiles_m counts the
+  // row tiles of W1, W3 and W2 of one instance, in that order.
+  Operand a2, b1;
+  float* W[3];          // GRAD_UPD: fp32 state (W1, W2, W3), updated in place
+  void* Wb[3];          // GRAD_UPD: bf16 operand copies of the updated state
+  float* M[3];          // GRAD_UPD with momentum (else nullptr): the state, updated in place
+  const float* bbar;    // chunk-mean momentum factor of instance i at bbar[i * bbar_stride]
+  int bbar_stride;
 };
 
 struct BwdArgs {
@@ -203,6 +213,7 @@ TileShape fwd_tile(int kind, bool io_bf16);   // rows = hidden units, cols = tok
 TileShape bwd_tile(int kind, bool io_bf16);   // OUT: features x tokens; GRAD13: hidden x
                                               // features; GRAD2: features x hidden
 TileShape ns_tile(bool fp16, bool big);       // tile-space rows x columns of the NS products
+TileShape grad_upd_tile();                    // GRAD_UPD: rows of W x all columns (bf16)
 
 // Launchers (io_bf16 selects bf16 MFMA operands, otherwise fp32).
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s);

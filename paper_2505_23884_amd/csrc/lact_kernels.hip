@@ -12,6 +12,9 @@
 //   BWD_GRAD13  P1 = (eta dz1)^T K,  P3 = (eta dz3)^T K             (gradient matmuls, -g1, -g3)
 //   BWD_GRAD2   P2 = V^T (eta hidden)                              (-g2; the linear
 //               fast weight's gradient V^T (eta K), §4.4, with OUT as its apply)
+//   BWD_GRAD_UPD  P1, P3, P2 of whole rows (d, h <= 512) followed in the same
+//               workgroup by the weight update of those rows (no Muon, no
+//               momentum, no split): the gradient never goes to memory
 //   NS_*        Newton-Schulz products (Muon, §3.2; App. A); k_ns_fused runs
 //               the whole iteration of a small matrix in one workgroup
 // plus the weight update with its row normalisation and momentum (k_update),
@@ -157,6 +160,10 @@ LACT_KIND(KOut16, 1, 1, 1, 0u, 2, 4, 4, 2, 2, true, 64, 0 * p, 0 * p);
 LACT_KIND(KGrad13_16, 2, 1, 2, 7u, 2, 4, 2, 2, 4, true, 32, p, 0 * p);
 // A = V (feature rows), B = eta hidden (hidden rows), token-major.
 LACT_KIND(KGrad2_16, 1, 1, 1, 3u, 2, 4, 4, 2, 4, true, 32, 0 * p, 0 * p);
+// Gradient with the weight update of whole rows (GRAD_UPD): A = eta dz1,
+// eta dz3 or V (128 rows of W1, W3 or W2), B = K or eta hidden (every column,
+// up to 512), token-major; waves of 64 x 128, 4 stages of 40 KiB.
+LACT_KIND(KGradU16, 1, 1, 1, 3u, 2, 4, 2, 4, 4, true, 32, 0 * p, 0 * p);
 // fp32 shapes: 4 waves of 64 x 64 (128 x 128 tiles), register path; the key
 // forward and its hidden backward share one loop (A = W1, W3, W2; B = K, V).
 LACT_KIND(KApply32, 2, 1, 2, 0u, 2, 2, 2, 2, 2, false, 32, p, 0 * p);
@@ -1019,6 +1026,124 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
   }
 }
 
+// The weight update of a GRAD_UPD tile from its accumulators P (= -g):
+//   U = W + P,  W <- U ||W_row|| / ||U_row||   (§3.2 weight normalisation; Alg. 1)
+// or, with momentum (App. A; Table 3), Y = P - bbar M, M <- -Y, U = W + Y.
+// The tile goes through LDS in passes of RP rows, so that lanes stream W (and
+// M) along whole rows in 16-byte vectors, as the separate update kernel does:
+// the rows of a pass are staged by the waves that hold them, TPR lanes share a
+// row, and a row's squared norms are summed over those lanes by shuffles. A
+// pass issues its W (and M) loads before the hand-over through LDS.
+template <class KG, bool MOM>
+__device__ __forceinline__ void update_rows(Acc<KG>& acc, float* W, __bf16* Wb, float* M, float bb, int64_t mrows,
+                                            int cols, uint8_t* smem) {
+  constexpr int RP = MOM ? 32 : 64;                 // rows per pass
+  constexpr int TPR = KG::THREADS / RP;             // lanes per row
+  constexpr int NV = KG::ROWS_B / 4 / TPR;          // 16-byte vectors per lane
+  constexpr int PITCH = KG::ROWS_B + 4;             // floats per LDS row
+  static_assert(KG::NACC == 1 && TPR <= 64 && RP * PITCH * 4 <= KG::NSTAGE * KG::STAGE, "update passes");
+  typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_t;
+  float* st = reinterpret_cast<float*>(smem);
+  const int lr = threadIdx.x / TPR, part = threadIdx.x % TPR;
+  const int nv = cols >> 2;
+  const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int pass = 0; pass < KG::ROWS_A / RP; ++pass) {
+    const int64_t row = (int64_t)pass * RP + lr;
+    const bool rok = row < mrows;
+    float4 w[NV], m[MOM ? NV : 1];
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const int c4 = part + TPR * q;
+      const bool ok = rok && c4 < nv;
+      w[q] = ok ? reinterpret_cast<const float4*>(W + row * cols)[c4] : zero;
+      if constexpr (MOM) m[q] = ok ? reinterpret_cast<const float4*>(M + row * cols)[c4] : zero;
+    }
+    // stage the accumulator rows [pass*RP, pass*RP + RP) (32-row blocks mi of wave row wave_m)
+#pragma unroll
+    for (int mi = 0; mi < KG::MI; ++mi) {
+      const int blk = wave_m<KG>() * 32 * KG::MI + mi * 32;
+      if (blk >= pass * RP && blk < pass * RP + RP) {
+#pragma unroll
+        for (int ni = 0; ni < KG::NI; ++ni)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            st[(acc_row<KG>(mi, r) - pass * RP) * PITCH + acc_col<KG>(ni)] = acc[0][mi][ni][r];
+      }
+    }
+    lds_barrier();
+    float su = 0.f, sw = 0.f;
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      float4 y = reinterpret_cast<const float4*>(st + lr * PITCH)[part + TPR * q];
+      if constexpr (MOM) {
+        y = make_float4(fmaf(-bb, m[q].x, y.x), fmaf(-bb, m[q].y, y.y), fmaf(-bb, m[q].z, y.z),
+                        fmaf(-bb, m[q].w, y.w));
+        m[q] = make_float4(-y.x, -y.y, -y.z, -y.w);
+      }
+      const float4 x = w[q];
+      sw += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+      w[q] = make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
+      su += w[q].x * w[q].x + w[q].y * w[q].y + w[q].z * w[q].z + w[q].w * w[q].w;
+    }
+#pragma unroll
+    for (int off = 1; off < TPR; off <<= 1) {
+      su += __shfl_xor(su, off, TPR);
+      sw += __shfl_xor(sw, off, TPR);
+    }
+    const float f = sqrtf(sw) / sqrtf(su);
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const int c4 = part + TPR * q;
+      if (rok && c4 < nv) {
+        const float4 x = make_float4(w[q].x * f, w[q].y * f, w[q].z * f, w[q].w * f);
+        reinterpret_cast<float4*>(W + row * cols)[c4] = x;
+        reinterpret_cast<bf16x4_t*>(Wb + row * cols)[c4] = bf16x4_t{(__bf16)x.x, (__bf16)x.y, (__bf16)x.z, (__bf16)x.w};
+        if constexpr (MOM) reinterpret_cast<float4*>(M + row * cols)[c4] = m[q];
+      }
+    }
+    if (pass + 1 < KG::ROWS_A / RP) lds_barrier();   // the pass is read before the next is staged
+  }
+}
+
+// GRAD_UPD tile (16-bit operands): 128 rows of W1, W3 or W2 with all their
+// columns. The chunk's tokens are contracted into P = -g in fp32 registers
+// (P1 = (eta dz1)^T K, P3 = (eta dz3)^T K, P2 = V^T (eta hidden)); then the
+// weight update of the same rows (update_rows), in place on the fp32 state
+// (and the momentum state), with the bf16 operand copy of the result for the
+// next chunk.
+template <typename T>
+__device__ __forceinline__ void grad_update_tile(const BwdSeg& sg, int inst, int rr, int d, int h, uint8_t* smem) {
+  using KG = KGradU16;
+  const int t1 = (h + KG::ROWS_A - 1) / KG::ROWS_A;   // row tiles of W1 (and of W3)
+  int mat, tile;
+  if (rr < t1) {
+    mat = 0;
+    tile = rr;
+  } else if (rr < 2 * t1) {
+    mat = 2;
+    tile = rr - t1;
+  } else {
+    mat = 1;
+    tile = rr - 2 * t1;
+  }
+  const int cols = mat == 1 ? h : d;
+  const int64_t r0 = (int64_t)tile * KG::ROWS_A;
+  const int64_t mrows = (mat == 1 ? d : h) - r0;
+  const Operand& A = mat == 0 ? sg.a0 : (mat == 2 ? sg.a1 : sg.a2);
+  const Operand& B = mat == 1 ? sg.b1 : sg.b0;
+  const View ops[2] = {view_mn(A, inst, r0, 0, mrows, sg.rows, 2), view_mn(B, inst, 0, 0, cols, sg.rows, 2)};
+  Acc<KG> acc;
+  mainloop<T, KG>(smem, ops, sg.rows, acc);
+
+  const int64_t dh = (int64_t)d * h;
+  const int64_t base = inst * dh + r0 * cols;
+  if (sg.M[0]) update_rows<KG, true>(acc, sg.W[mat] + base, reinterpret_cast<__bf16*>(sg.Wb[mat]) + base,
+                                     sg.M[mat] + base, sg.bbar[(int64_t)inst * sg.bbar_stride], mrows, cols, smem);
+  else update_rows<KG, false>(acc, sg.W[mat] + base, reinterpret_cast<__bf16*>(sg.Wb[mat]) + base, nullptr, 0.f,
+                              mrows, cols, smem);
+}
+
 // Second launch: apply GEMM-2 and the gradient contractions (split over tokens).
 template <typename T>
 __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs args) {
@@ -1027,7 +1152,8 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
   using K2 = typename Kinds<T>::Grad2;
   static_assert(KO::THREADS == K13::THREADS && KO::THREADS == K2::THREADS, "one block size per launch");
   __shared__ __attribute__((aligned(16)))
-  uint8_t smem[cmax(smem_bytes<T, KO>(), cmax(smem_bytes<T, K13>(), smem_bytes<T, K2>()))];
+  uint8_t smem[cmax(cmax(smem_bytes<T, KO>(), sizeof(T) == 2 ? smem_bytes<T, KGradU16>() : 0),
+                    cmax(smem_bytes<T, K13>(), smem_bytes<T, K2>()))];
   constexpr int esz = sizeof(T);
   int bid = blockIdx.x;
   int si = 0;
@@ -1093,6 +1219,13 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
         }
     }
     return;
+  }
+
+  if constexpr (sizeof(T) == 2) {
+    if (sg.kind == BWD_GRAD_UPD) {
+      grad_update_tile<T>(sg, inst, rr, d, h, smem);
+      return;
+    }
   }
 
   const int64_t kb = (int64_t)split * sg.split_len;
@@ -1803,6 +1936,8 @@ TileShape bwd_tile(int kind, bool io_bf16) {
   if (kind == BWD_GRAD13) return TileShape{KGrad13_32::ROWS_A, KGrad13_32::ROWS_B, KGrad13_32::THREADS};
   return TileShape{KGrad2_32::ROWS_A, KGrad2_32::ROWS_B, KGrad2_32::THREADS};
 }
+
+TileShape grad_upd_tile() { return TileShape{KGradU16::ROWS_A, KGradU16::ROWS_B, KGradU16::THREADS}; }
 
 TileShape ns_tile(bool fp16, bool big) {
   if (fp16 && big) return TileShape{KNsK16B::ROWS_A, KNsK16B::ROWS_B, KNsK16B::THREADS};

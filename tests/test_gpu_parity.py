@@ -177,6 +177,84 @@ def test_nvs_shape_reduced_context():
     check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
 
 
+# ----------------------------------------------------------------------------- gradient + update in one kind
+# With 256 < d, h <= 512, no Muon and an unsplit gradient, one workgroup
+# contracts whole rows of W1, W3 or W2 and applies the weight update (and the
+# momentum step) to them: no separate update launch. d = 320, h = 288 leave ragged row and
+# column tiles; 13 instances give the gradient enough tiles not to split.
+
+
+def update_launches(fn):
+    P.timing_reset()
+    P.timing_enable(True)
+    try:
+        out = fn()
+    finally:
+        P.timing_enable(False)
+    n = P.timing_read(P.KCLASS_NAMES.index("update"))[0]
+    P.timing_reset()
+    return out, n
+
+
+FUSED = CONFIGS["lm32k"].with_(name="fused", B=1, H=13, d=320, h=288, n_kv=700, n_q=760, chunk=256)
+
+
+@pytest.mark.parametrize("order,lr3", [(0, 0), (1, 0), (0, 1)])
+def test_fused_gradient_update_ragged(order, lr3):
+    cfg = FUSED.with_(order=order, lr3=lr3)
+    x = make_inputs(cfg, 71)
+    got, n_upd = update_launches(lambda: run_gpu(cfg, x))
+    assert n_upd == 0, "the gradient and update kind was not taken"
+    check(cfg, x, got, run_oracle(cfg, x))
+
+
+def test_fused_gradient_update_deterministic_and_resumable():
+    cfg = FUSED.with_(n_kv=1024, n_q=1024)
+    x = make_inputs(cfg, 72)
+    o1, W1 = run_gpu(cfg, x)
+    o2, W2 = run_gpu(cfg, x)
+    assert np.array_equal(o1, o2) and all(np.array_equal(a, b) for a, b in zip(W1, W2))
+    first = {k: (np.ascontiguousarray(v[:, :512]) if k in ("q", "k", "v", "eta") else v) for k, v in x.items()}
+    half = cfg.with_(n_kv=512, n_q=512)
+    oa, Wa = run_gpu(half, first)
+    second = {k: np.ascontiguousarray(v[:, 512:]) for k, v in x.items() if k in ("q", "k", "v", "eta")}
+    second.update({"W1": Wa[0], "W2": Wa[1], "W3": Wa[2]})
+    ob, Wb = run_gpu(half, second)
+    assert np.array_equal(np.concatenate([oa, ob], axis=1), o1)
+    assert all(np.array_equal(a, b) for a, b in zip(Wb, W1))
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_fused_gradient_update_with_momentum(order):
+    cfg = FUSED.with_(name="fused_mom", momentum=1, order=order)
+    x = make_inputs(cfg, 73)
+    got, n_upd = update_launches(lambda: run_gpu_momentum(cfg, x))
+    # the update class then holds only the chunk-mean launch of the momentum factors
+    assert n_upd < cfg.n_chunks, "the gradient and update kind was not taken"
+    check_momentum(cfg, x, got, run_oracle_momentum(cfg, x))
+
+
+def test_fused_momentum_at_beta_zero_is_the_plain_path():
+    # bbar = 0: Y = P exactly, so the momentum update is the plain one; the
+    # two kernels sum a row's squares in different orders (16 lanes of 8
+    # vectors against 8 of 16), so the weights agree to fp32 rounding, and a
+    # rounding step can move a bf16 weight copy by one unit
+    cfg = FUSED.with_(name="fused_beta0", momentum=1)
+    x = make_inputs(cfg, 74)
+    x["beta"][:] = 0.0
+    o_m, W_m, M_m = run_gpu_momentum(cfg, x)
+    o_p, W_p = run_gpu(cfg, x)
+    errs = {"o": rel(o_m, o_p)}
+    for j, (a, b, w0) in enumerate(zip(W_m, W_p, (x["W1"], x["W2"], x["W3"]))):
+        errs[f"dW{j + 1}"] = rel(a - w0, b - w0)
+    print("[gpu] momentum(beta=0) vs plain rel-L2", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for kk, vv in errs.items():
+        assert vv <= 1e-3, (kk, vv)
+    ref = run_oracle_momentum(cfg, x)
+    for j in range(3):
+        assert rel(M_m[j], ref[4 + j]) <= TOL["bf16"]
+
+
 # ----------------------------------------------------------------------------- full NVS context
 # The NVS workloads at their full sizes, in the launch bench.py times: one
 # update-then-apply chunk over 262144 or 1048576 context tokens, then the
@@ -663,6 +741,19 @@ def test_nvs_style_schedule_update_views_then_apply_targets():
     x = make_inputs(cfg, 38)
     sched = [("update_only", 0, 8192), ("apply_only", 8192, 8192 + 2048)]
     check(cfg, x, run_gpu_schedule(cfg, x, sched), run_oracle_schedule(cfg, x, sched))
+
+
+def test_fused_gradient_update_in_a_mixed_schedule():
+    # the gradient and update kind alternates the bf16 weight copies; a
+    # schedule mixes updates, applies of other rows and gaps around it
+    cfg = FUSED.with_(name="fused_sched", n_kv=500, n_q=620)
+    x = make_inputs(cfg, 75)
+    sched = [("update_only", 0, 150), ("apply_only", 40, 300), ("apply_then_update", 150, 333),
+             ("update_then_apply", 333, 500), ("apply_only", 520, 600), ("update_only", 10, 77),
+             ("apply_only", 250, 270)]
+    got, n_upd = update_launches(lambda: run_gpu_schedule(cfg, x, sched))
+    assert n_upd == 0, "the gradient and update kind was not taken"
+    check(cfg, x, got, run_oracle_schedule(cfg, x, sched))
 
 
 @pytest.mark.parametrize("io", ["bf16", "fp32"])

@@ -90,8 +90,18 @@ Plan make_plan(const lact_desc* dsc) {
   const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
   const int64_t tiles = (int64_t)p.BH * ((p.linear ? 0 : cdiv(p.h, g13.rows) * cdiv(p.d, g13.cols)) +
                                          cdiv(p.d, g2.rows) * cdiv(p.h, g2.cols));
+  // The gradient and update kind (below) needs an unsplit gradient; it pays
+  // when its row tiles cover at least half the chip and, for long chunks, when
+  // apply tiles share the launch (apply-then-update, or more than one chunk)
+  // and take the CUs the row tiles leave.
+  const int upd_cols = grad_upd_tile().cols;
+  const bool upd_shape = p.bf16 && !p.linear && !dsc->use_muon && p.d > 256 && p.h > 256 && p.d <= upd_cols &&
+                         p.h <= upd_cols;
+  const bool apply_alongside = dsc->order == LACT_APPLY_THEN_UPDATE || dsc->n_kv > p.C;
   int64_t ns;
-  if (p.C >= 8192) {
+  if (upd_shape && tiles >= 128 && (p.C < 8192 || apply_alongside)) {
+    ns = 1;
+  } else if (p.C >= 8192) {
     const int64_t top = std::min<int64_t>(kMaxSplit, std::max<int64_t>(1, p.C / 1024));
     ns = 1;
     double best = 1e30;
@@ -115,9 +125,7 @@ Plan make_plan(const lact_desc* dsc) {
   // gradient is not split and no Newton-Schulz step sits between the two. The
   // bf16 operand copies then alternate between two buffers: the apply tiles
   // of the same launch still read the pre-update W2.
-  const int upd_cols = grad_upd_tile().cols;
-  p.fused = p.bf16 && !p.linear && !dsc->use_muon && p.nsplit == 1 && p.d > 256 && p.h > 256 &&
-            p.d <= upd_cols && p.h <= upd_cols;
+  p.fused = upd_shape && p.nsplit == 1;
   const size_t dh = (size_t)p.d * p.h;
   size_t o = 0;
   for (int m = 0; m < 3; ++m) {

@@ -32,6 +32,7 @@ struct Plan {
   int nsplit;         // split-K ways of the gradient contraction
   int64_t split_len;  // tokens per split
   bool fused;         // gradient and weight update in one kind (BWD_GRAD_UPD)
+  bool narrow;        // narrow tile shapes of the second launch (16-bit, d <= 128)
   bool muon;
   bool ns_fp16;       // Newton-Schulz operand copies in fp16 (bf16 I/O) or fp32
   int ns_esz;
@@ -74,6 +75,7 @@ Plan make_plan(const lact_desc* dsc) {
   p.linear = dsc->fast_weight == LACT_FW_LINEAR;
   p.nmat = p.linear ? 1 : 3;
   p.C = std::min<int64_t>(dsc->chunk, dsc->n_kv);
+  p.narrow = p.bf16 && p.d <= 128;
   const int64_t tail = dsc->n_q - dsc->n_kv;
   // The applied-hidden buffer holds one chunk plus (bounded) tail rows so that
   // update-then-apply can apply its last chunk together with the tail.
@@ -83,11 +85,12 @@ Plan make_plan(const lact_desc* dsc) {
   // update). Each split adds a full write and read of 3*d*h fp32 per instance,
   // worth about 500 tokens of the gradient's own work, so short chunks (the
   // LM workload's 2048) split only when the gradient tiles alone would leave
-  // most of the chip idle (measured: 2 splits cost 8% there). Long chunks
+  // most of the chip idle (measured: 2 splits cost 8% there; on the video
+  // shape 4 splits instead of 2 cost 7%). Long chunks
   // (NVS: one chunk of up to 1M tokens) take the split count, with splits of
   // at least 1024 tokens, that minimises the makespan of equal blocks over the
   // 256 CUs: rounds(tiles * ns) / ns. Lengths are a multiple of 32.
-  const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
+  const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16, p.narrow), g2 = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
   const int64_t tiles = (int64_t)p.BH * ((p.linear ? 0 : cdiv(p.h, g13.rows) * cdiv(p.d, g13.cols)) +
                                          cdiv(p.d, g2.rows) * cdiv(p.h, g2.cols));
   // The gradient and update kind (below) needs an unsplit gradient; it pays
@@ -263,8 +266,8 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
       BwdArgs b{};
       BwdSeg& o = b.seg[0];
       o.kind = BWD_OUT;
-      o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16).rows);
-      o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16).cols);
+      o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16, p.narrow).rows);
+      o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16, p.narrow).cols);
       o.nsplit = 1;
       o.nblocks = p.BH * o.tiles_m * o.tiles_n;
       o.rows = n;
@@ -276,6 +279,7 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
       b.total_blocks = o.nblocks;
       b.d = p.d;
       b.h = p.d;
+      b.narrow = p.narrow;
       const int rc = timed(LACT_KCLASS_BWD, 2.0 * p.BH * n * p.d * p.d, c.s,
                            [&] { return launch_bwd(b, p.bf16, c.s); });
       if (rc) return rc;
@@ -307,8 +311,8 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
     BwdArgs b{};
     BwdSeg& o = b.seg[0];
     o.kind = BWD_OUT;
-    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16).rows);
-    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16).cols);
+    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16, p.narrow).rows);
+    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16, p.narrow).cols);
     o.nsplit = 1;
     o.nblocks = p.BH * o.tiles_m * o.tiles_n;
     o.rows = n;
@@ -320,6 +324,7 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
     b.total_blocks = o.nblocks;
     b.d = p.d;
     b.h = p.h;
+    b.narrow = p.narrow;
     rc = timed(LACT_KCLASS_BWD, 2.0 * p.BH * n * p.d * p.h, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
     if (rc) return rc;
   }
@@ -532,7 +537,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   }
   // Gradient contractions, split over tokens; a split past the chunk's end
   // writes zeros so the update always sums p.nsplit partials.
-  const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16), g2 = bwd_tile(BWD_GRAD2, p.bf16);
+  const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16, p.narrow), g2 = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
   if (!fused) {
     BwdSeg& g = b.seg[nb++];
     g.kind = BWD_GRAD13;
@@ -568,8 +573,8 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   if (apply_too) {
     BwdSeg& o = b.seg[nb++];
     o.kind = BWD_OUT;
-    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16).rows);
-    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16).cols);
+    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16, p.narrow).rows);
+    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16, p.narrow).cols);
     o.nsplit = 1;
     o.nblocks = p.BH * o.tiles_m * o.tiles_n;
     o.rows = n;
@@ -583,6 +588,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   for (int i = 0; i < nb; ++i) b.total_blocks += b.seg[i].nblocks;
   b.d = p.d;
   b.h = p.h;
+  b.narrow = p.narrow;
   const double bfl = (apply_too ? 2.0 : 0.0) * p.BH * n * dh + 6.0 * p.BH * n * dh;
   rc = timed(LACT_KCLASS_BWD, bfl, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
   if (rc) return rc;
@@ -643,7 +649,7 @@ int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   if (rc) return rc;
   BwdArgs b{};
   int nb = 0;
-  const TileShape g2 = bwd_tile(BWD_GRAD2, p.bf16);
+  const TileShape g2 = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
   {
     BwdSeg& g = b.seg[nb++];
     g.kind = BWD_GRAD2;
@@ -663,8 +669,8 @@ int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   if (apply_too) {
     BwdSeg& o = b.seg[nb++];
     o.kind = BWD_OUT;
-    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16).rows);
-    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16).cols);
+    o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16, p.narrow).rows);
+    o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16, p.narrow).cols);
     o.nsplit = 1;
     o.nblocks = p.BH * o.tiles_m * o.tiles_n;
     o.rows = n;
@@ -678,6 +684,7 @@ int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   for (int i = 0; i < nb; ++i) b.total_blocks += b.seg[i].nblocks;
   b.d = p.d;
   b.h = p.d;   // OUT contracts over d; GRAD2's columns run over d
+  b.narrow = p.narrow;
   const double bfl = (apply_too ? 2.0 : 0.0) * p.BH * n * dd + 2.0 * p.BH * n * dd;
   rc = timed(LACT_KCLASS_BWD, bfl, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
   if (rc) return rc;

@@ -79,6 +79,7 @@ struct BwdArgs {
   int nseg;
   int total_blocks;
   int d, h;
+  int narrow;           // 16-bit I/O with d <= 128: the narrow tile shapes (bwd_tile)
 };
 
 // ---- weight update ----------------------------------------------------------
@@ -210,8 +211,8 @@ struct TileShape {
   int rows, cols, threads;
 };
 TileShape fwd_tile(int kind, bool io_bf16);   // rows = hidden units, cols = tokens
-TileShape bwd_tile(int kind, bool io_bf16);   // OUT: features x tokens; GRAD13: hidden x
-                                              // features; GRAD2: features x hidden
+TileShape bwd_tile(int kind, bool io_bf16, bool narrow);   // OUT: features x tokens; GRAD13:
+                                                           // hidden x features; GRAD2: features x hidden
 TileShape ns_tile(bool fp16, bool big);       // tile-space rows x columns of the NS products
 TileShape grad_upd_tile();                    // GRAD_UPD: rows of W x all columns (bf16)
 

@@ -164,6 +164,13 @@ LACT_KIND(KGrad2_16, 1, 1, 1, 3u, 2, 4, 4, 2, 4, true, 32, 0 * p, 0 * p);
 // eta dz3 or V (128 rows of W1, W3 or W2), B = K or eta hidden (every column,
 // up to 512), token-major; waves of 64 x 128, 4 stages of 40 KiB.
 LACT_KIND(KGradU16, 1, 1, 1, 3u, 2, 4, 2, 4, 4, true, 32, 0 * p, 0 * p);
+// Narrow shapes (16-bit, d <= 128): the feature dimension fills 128 tile rows
+// instead of half of 256. Apply GEMM-2: 128 features x 512 tokens; gradients
+// of W1, W3: 256 hidden x 128 features; gradient of W2: 128 features x 256
+// hidden.
+LACT_KIND(KOutN16, 1, 1, 1, 0u, 2, 4, 2, 4, 2, true, 64, 0 * p, 0 * p);
+LACT_KIND(KGrad13N16, 2, 1, 2, 7u, 4, 2, 2, 2, 4, true, 32, p, 0 * p);
+LACT_KIND(KGrad2N16, 1, 1, 1, 3u, 2, 4, 2, 2, 4, true, 32, 0 * p, 0 * p);
 // fp32 shapes: 4 waves of 64 x 64 (128 x 128 tiles), register path; the key
 // forward and its hidden backward share one loop (A = W1, W3, W2; B = K, V).
 LACT_KIND(KApply32, 2, 1, 2, 0u, 2, 2, 2, 2, 2, false, 32, p, 0 * p);
@@ -218,6 +225,20 @@ template <> struct Kinds<float> {
   using Out = KOut32;
   using Grad13 = KGrad13_32;
   using Grad2 = KGrad2_32;
+};
+
+// Kinds of the second launch: the narrow shapes for 16-bit I/O with d <= 128.
+template <typename T, bool NARROW>
+struct BwdKinds {
+  using Out = typename Kinds<T>::Out;
+  using Grad13 = typename Kinds<T>::Grad13;
+  using Grad2 = typename Kinds<T>::Grad2;
+};
+template <>
+struct BwdKinds<__bf16, true> {
+  using Out = KOutN16;
+  using Grad13 = KGrad13N16;
+  using Grad2 = KGrad2N16;
 };
 
 template <class K>
@@ -404,6 +425,8 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(
 constexpr uint32_t kOOB = 0x80000000u;
 constexpr int kRawBufferFlags = 0x00020000;
 
+constexpr int kMaxSlots = 8;   // 16-byte DMA slots per lane and operand tile
+
 // Slots: an operand tile of R rows and BK K is R*BK/8 slots of 16 bytes; lane
 // `tid` of the workgroup fills slots tid, tid + THREADS, ... (so each wave
 // instruction writes 1 KiB of consecutive LDS).
@@ -413,11 +436,11 @@ struct Dma {
   static constexpr int ROWS = K::rows(O);
   static constexpr int BK = K::BK;
   static constexpr int SLOTS = ROWS * BK / 8 / K::THREADS;   // per lane
-  static_assert(SLOTS >= 1 && SLOTS <= 4 && ROWS * BK / 8 % K::THREADS == 0, "slot split");
+  static_assert(SLOTS >= 1 && SLOTS <= kMaxSlots && ROWS * BK / 8 % K::THREADS == 0, "slot split");
   static constexpr int CPK = BK / 8;                          // chunks per row (k)
   static constexpr int CPR = ROWS / 8;                        // chunks per K row (mn)
 
-  static __device__ __forceinline__ void offsets(uint32_t (&vo)[4], const View& v) {
+  static __device__ __forceinline__ void offsets(uint32_t (&vo)[kMaxSlots], const View& v) {
 #pragma unroll
     for (int i = 0; i < SLOTS; ++i) {
       const int p = i * K::THREADS + threadIdx.x;
@@ -435,7 +458,7 @@ struct Dma {
   // with kt and whose size covers only the valid data, so K rows past the end
   // (row-contiguous operands) load as zeros. K-contiguous operands whose K is
   // not a multiple of BK zero the chunks past K in their last tile.
-  static __device__ __forceinline__ void issue(uint8_t* tile, const View& v, const uint32_t (&vo)[4], int kt) {
+  static __device__ __forceinline__ void issue(uint8_t* tile, const View& v, const uint32_t (&vo)[kMaxSlots], int kt) {
     const uint8_t* base;
     int64_t span;
     if (!MN) {
@@ -469,14 +492,14 @@ struct Dma {
 // Every operand of kind K, unrolled at compile time.
 template <class K, int O = 0>
 struct DmaAll {
-  static __device__ __forceinline__ void offsets(uint32_t (&vo)[K::NOPS][4], const View (&ops)[K::NOPS]) {
+  static __device__ __forceinline__ void offsets(uint32_t (&vo)[K::NOPS][kMaxSlots], const View (&ops)[K::NOPS]) {
     if constexpr (O < K::NOPS) {
       Dma<K, O>::offsets(vo[O], ops[O]);
       DmaAll<K, O + 1>::offsets(vo, ops);
     }
   }
   static __device__ __forceinline__ void issue(uint8_t* st, const View (&ops)[K::NOPS],
-                                               const uint32_t (&vo)[K::NOPS][4], int kt) {
+                                               const uint32_t (&vo)[K::NOPS][kMaxSlots], int kt) {
     if constexpr (O < K::NOPS) {
       Dma<K, O>::issue(st + K::op_off(O), ops[O], vo[O], kt);
       DmaAll<K, O + 1>::issue(st, ops, vo, kt);
@@ -610,7 +633,7 @@ struct ChainNext {
   int slot;   // stage the first tile went to, -1 if none
   __device__ __forceinline__ ChainNext(uint8_t* s, const View (&o)[K2::NOPS]) : smem(s), ops(o), slot(-1) {}
   __device__ __forceinline__ void first(int s) {
-    uint32_t vo[K2::NOPS][4];
+    uint32_t vo[K2::NOPS][kMaxSlots];
     DmaAll<K2>::offsets(vo, ops);
     DmaAll<K2>::issue(smem + s * SLOT, ops, vo, 0);
     slot = s;
@@ -636,7 +659,7 @@ __device__ __forceinline__ void mainloop_dma(uint8_t* smem, const View (&ops)[K:
   static_assert(S % 2 == 0, "substeps per tile");
   const int nkt = (int)((nk + BK - 1) / BK);
   if (nkt <= 0) return;
-  uint32_t vo[K::NOPS][4];
+  uint32_t vo[K::NOPS][kMaxSlots];
   DmaAll<K>::offsets(vo, ops);
   auto stage = [&](int kt) { return smem + ((kt + shift) % NS) * SLOT; };
   auto issue = [&](int kt) { DmaAll<K>::issue(stage(kt), ops, vo, kt); };
@@ -1145,14 +1168,14 @@ __device__ __forceinline__ void grad_update_tile(const BwdSeg& sg, int inst, int
 }
 
 // Second launch: apply GEMM-2 and the gradient contractions (split over tokens).
-template <typename T>
+template <typename T, bool NARROW>
 __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs args) {
-  using KO = typename Kinds<T>::Out;
-  using K13 = typename Kinds<T>::Grad13;
-  using K2 = typename Kinds<T>::Grad2;
+  using KO = typename BwdKinds<T, NARROW>::Out;
+  using K13 = typename BwdKinds<T, NARROW>::Grad13;
+  using K2 = typename BwdKinds<T, NARROW>::Grad2;
   static_assert(KO::THREADS == K13::THREADS && KO::THREADS == K2::THREADS, "one block size per launch");
   __shared__ __attribute__((aligned(16)))
-  uint8_t smem[cmax(cmax(smem_bytes<T, KO>(), sizeof(T) == 2 ? smem_bytes<T, KGradU16>() : 0),
+  uint8_t smem[cmax(cmax(smem_bytes<T, KO>(), (sizeof(T) == 2 && !NARROW) ? smem_bytes<T, KGradU16>() : 0),
                     cmax(smem_bytes<T, K13>(), smem_bytes<T, K2>()))];
   constexpr int esz = sizeof(T);
   int bid = blockIdx.x;
@@ -1221,7 +1244,7 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
     return;
   }
 
-  if constexpr (sizeof(T) == 2) {
+  if constexpr (sizeof(T) == 2 && !NARROW) {
     if (sg.kind == BWD_GRAD_UPD) {
       grad_update_tile<T>(sg, inst, rr, d, h, smem);
       return;
@@ -1926,7 +1949,12 @@ TileShape fwd_tile(int kind, bool io_bf16) {
                            : TileShape{KUpdate32::ROWS_A, KUpdate32::ROWS_B, KUpdate32::THREADS};
 }
 
-TileShape bwd_tile(int kind, bool io_bf16) {
+TileShape bwd_tile(int kind, bool io_bf16, bool narrow) {
+  if (io_bf16 && narrow) {
+    if (kind == BWD_OUT) return TileShape{KOutN16::ROWS_A, KOutN16::ROWS_B, KOutN16::THREADS};
+    if (kind == BWD_GRAD13) return TileShape{KGrad13N16::ROWS_A, KGrad13N16::ROWS_B, KGrad13N16::THREADS};
+    return TileShape{KGrad2N16::ROWS_A, KGrad2N16::ROWS_B, KGrad2N16::THREADS};
+  }
   if (io_bf16) {
     if (kind == BWD_OUT) return TileShape{KOut16::ROWS_A, KOut16::ROWS_B, KOut16::THREADS};
     if (kind == BWD_GRAD13) return TileShape{KGrad13_16::ROWS_A, KGrad13_16::ROWS_B, KGrad13_16::THREADS};
@@ -2001,8 +2029,9 @@ hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s) {
 
 hipError_t launch_bwd(const BwdArgs& a, bool io_bf16, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;
-  if (io_bf16) k_bwd<__bf16><<<a.total_blocks, KOut16::THREADS, 0, s>>>(a);
-  else k_bwd<float><<<a.total_blocks, KOut32::THREADS, 0, s>>>(a);
+  if (io_bf16 && a.narrow) k_bwd<__bf16, true><<<a.total_blocks, KOutN16::THREADS, 0, s>>>(a);
+  else if (io_bf16) k_bwd<__bf16, false><<<a.total_blocks, KOut16::THREADS, 0, s>>>(a);
+  else k_bwd<float, false><<<a.total_blocks, KOut32::THREADS, 0, s>>>(a);
   return hipGetLastError();
 }
 

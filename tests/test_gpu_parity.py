@@ -255,6 +255,45 @@ def test_fused_momentum_at_beta_zero_is_the_plain_path():
         assert rel(M_m[j], ref[4 + j]) <= TOL["bf16"]
 
 
+# ----------------------------------------------------------------------------- seeded shape sweep
+# Shapes drawn from a fixed seed: bf16 (d, h multiples of 32 up to 640) and
+# fp32 (multiples of 8 up to 160), 1-16 instances, 1-1200 key tokens, a query
+# tail, any chunk from 16 tokens and either order; every tile kind meets
+# ragged rows, columns and K tails in combinations no hand-picked case covers.
+
+
+def _sweep_cases(n=10, seed=2505):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        bf16 = i % 5 != 4
+        step, top = (32, 640) if bf16 else (8, 160)
+        d = int(rng.integers(1, top // step + 1)) * step
+        h = int(rng.integers(1, top // step + 1)) * step
+        B = int(rng.integers(1, 5))
+        H = int(rng.integers(1, 5))
+        n_kv = int(rng.integers(1, 1201))
+        n_q = n_kv + int(rng.integers(0, 101))
+        chunk = int(rng.integers(16, max(17, n_kv + 1)))
+        order = int(rng.integers(0, 2))
+        cases.append(pytest.param(("bf16" if bf16 else "fp32", B, H, d, h, n_kv, n_q, chunk, order),
+                                  id=f"{'bf16' if bf16 else 'fp32'}-B{B}H{H}-d{d}h{h}-n{n_kv}q{n_q}-c{chunk}-o{order}"))
+    return cases
+
+
+@pytest.mark.parametrize("shape", _sweep_cases())
+def test_seeded_shape_sweep(shape):
+    io, B, H, d, h, n_kv, n_q, chunk, order = shape
+    base = CONFIGS["lm32k"] if io == "bf16" else CONFIGS["tiny_fp32"]
+    cfg = base.with_(name="sweep", B=B, H=H, d=d, h=h, n_kv=n_kv, n_q=n_q, chunk=chunk, order=order)
+    x = make_inputs(cfg, 81)
+    if io == "fp32":
+        # fp32 resolves dW at 1e-4 only when a chunk moves W by more than ~1e-4
+        # of its size (see the chunk-of-one-token case)
+        x["eta"] *= 30.0
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
 # ----------------------------------------------------------------------------- full NVS context
 # The NVS workloads at their full sizes, in the launch bench.py times: one
 # update-then-apply chunk over 262144 or 1048576 context tokens, then the

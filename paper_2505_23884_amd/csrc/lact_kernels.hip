@@ -12,12 +12,16 @@
 //   BWD_GRAD13  P1 = (eta dz1)^T K,  P3 = (eta dz3)^T K             (gradient matmuls, -g1, -g3)
 //   BWD_GRAD2   P2 = V^T (eta hidden)                              (-g2; the linear
 //               fast weight's gradient V^T (eta K), §4.4, with OUT as its apply)
-//   BWD_GRAD_UPD  P1, P3, P2 of whole rows (d, h <= 512) followed in the same
-//               workgroup by the weight update of those rows (no Muon, no
-//               momentum, no split): the gradient never goes to memory
+//   BWD_GRAD_UPD  P1, P3, P2 of whole rows (256 < d, h <= 512) followed in the
+//               same workgroup by the weight update of those rows, with or
+//               without momentum (no Muon, no split): the gradient never goes
+//               to memory
+// (the second launch also has narrow shapes of OUT, GRAD13 and GRAD2 for
+// d <= 128, so that the feature dimension fills the tile)
 //   NS_*        Newton-Schulz products (Muon, §3.2; App. A); k_ns_fused runs
 //               the whole iteration of a small matrix in one workgroup
-// plus the weight update with its row normalisation and momentum (k_update),
+// plus the separate weight update with its row normalisation and momentum
+// (k_update, wherever the gradient and update kind does not apply),
 // the Newton-Schulz prologue (k_ns_prep, k_ns_scale), the momentum chunk
 // means (k_beta_mean), operand copies (k_prep), eta k (k_scale_rows) and the
 // zeroing of uncovered output rows (k_zero_rows).

@@ -1,5 +1,6 @@
 """Host-side checks of the benchmark: its FLOP count against the oracle's
-(App. A), the scheduled workloads' segments, and the one-GPU guard."""
+(App. A), the scheduled workloads' segments, the one-GPU guard and the key
+of the traffic figure."""
 import json
 import os
 import subprocess
@@ -45,3 +46,13 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
                        text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
+
+
+def test_source_hash_ignores_comments_and_whitespace_only():
+    # the traffic figure is keyed to the kernel sources as the compiler sees them
+    a = 'int x = 1; // rate\n/* tile */ const char* s = "a // b";  float y;'
+    b = 'int x = 1;\n\n   const char* s = "a // b"; /* other words */ float y; // end'
+    c = 'int x = 2; const char* s = "a // b"; float y;'
+    assert bench._code_only(a) == bench._code_only(b)
+    assert bench._code_only(a) != bench._code_only(c)
+    assert bench._code_only('char q = \'"\'; // "') == "char q = '\"';"

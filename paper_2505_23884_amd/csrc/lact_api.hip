@@ -34,6 +34,8 @@ struct Plan {
   bool fused;         // gradient and weight update in one kind (BWD_GRAD_UPD)
   bool narrow;        // narrow tile shapes of the second launch (16-bit, d <= 128)
   bool muon;
+  bool tile_sums;     // Muon without split: the gradient tiles leave the sums of squares
+  int t13, t2;        // gradient tiles per matrix (W1 or W3; W2 or the linear W)
   bool ns_fp16;       // Newton-Schulz operand copies in fp16 (bf16 I/O) or fp32
   int ns_esz;
   int m;              // Newton-Schulz Gram size min(d, h)
@@ -155,6 +157,13 @@ Plan make_plan(const lact_desc* dsc) {
   p.muon = dsc->use_muon != 0;
   p.m = std::min(p.d, p.h);
   p.ns_bps = (int)cdiv((int64_t)dh, kNsBlockElems);
+  p.t13 = p.linear ? 0 : (int)(cdiv(p.h, g13.rows) * cdiv(p.d, g13.cols));
+  p.t2 = (int)(cdiv(p.d, g2.rows) * cdiv(p.h, g2.cols));
+  // Without split the sums of squares that Newton-Schulz normalises by come
+  // from the gradient tiles' epilogues (one entry per tile), and the scaling
+  // reads the gradient directly: no separate pass over it (momentum keeps the
+  // pass, which also advances the state).
+  p.tile_sums = p.muon && p.nsplit == 1 && p.t13 <= p.ns_bps && p.t2 <= p.ns_bps;
   p.ns_fp16 = p.bf16;
   p.ns_esz = p.ns_fp16 ? 2 : 4;
   if (p.muon) {
@@ -351,8 +360,16 @@ int newton_schulz(Ctx& c) {
     pa.bbar = bbar_of(c);
     pa.bbar_stride = kBetaBatch;
   }
-  int rc = timed(LACT_KCLASS_NS, 0.0, c.s, [&] { return launch_ns_prep(pa, c.s); });
-  if (rc) return rc;
+  int rc = LACT_OK;
+  if (p.tile_sums && !c.beta) {
+    pa.src = reinterpret_cast<const float*>(c.ws + p.off_step);
+    pa.sum_n[0] = p.linear ? p.t2 : p.t13;
+    pa.sum_n[1] = p.t2;
+    pa.sum_n[2] = p.t13;
+  } else {
+    rc = timed(LACT_KCLASS_NS, 0.0, c.s, [&] { return launch_ns_prep(pa, c.s); });
+    if (rc) return rc;
+  }
   rc = timed(LACT_KCLASS_NS, 0.0, c.s,
              [&] { return launch_ns_scale(pa, c.ws + p.off_yb[0], p.ns_fp16, 1e-7f, c.s); });
   if (rc) return rc;
@@ -447,6 +464,16 @@ int newton_schulz(Ctx& c) {
 
 int finish_update(Ctx& c);
 int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too);
+
+// Gradient segments of a Muon update without split or momentum write their
+// tiles' sums of squares (GRAD2 for matrix j2: W2, or the linear W).
+void set_tile_sums(const Ctx& c, BwdSeg& g, int j2) {
+  if (!c.p.tile_sums || c.beta) return;
+  g.sumsq = reinterpret_cast<float*>(c.ws + c.p.off_ss);
+  g.sumsq_stride = c.p.ns_bps;
+  g.sumsq_j = j2;
+  g.spi = c.p.nmat;
+}
 
 // Points the operand views at bf16 copy set `set`.
 void use_wset(Ctx& c, int set) {
@@ -553,6 +580,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.out = c.ws + p.off_step;
     g.out_inst = 3 * dh;
     g.out_split = (int64_t)p.BH * 3 * dh;
+    set_tile_sums(c, g, 0);
   }
   if (!fused) {
     BwdSeg& g = b.seg[nb++];
@@ -569,6 +597,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.out_inst = 3 * dh;
     g.out_split = (int64_t)p.BH * 3 * dh;
     g.out_off = dh;   // W2's partials follow W1's
+    set_tile_sums(c, g, 1);
   }
   if (apply_too) {
     BwdSeg& o = b.seg[nb++];
@@ -665,6 +694,7 @@ int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.out_inst = dd;
     g.out_split = (int64_t)p.BH * dd;
     g.out_off = 0;
+    set_tile_sums(c, g, 0);
   }
   if (apply_too) {
     BwdSeg& o = b.seg[nb++];

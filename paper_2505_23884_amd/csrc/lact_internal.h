@@ -72,6 +72,11 @@ struct BwdSeg {
   float* M[3];          // GRAD_UPD with momentum (else nullptr): the state, updated in place
   const float* bbar;    // chunk-mean momentum factor of instance i at bbar[i * bbar_stride]
   int bbar_stride;
+  // GRAD13 / GRAD2 without split (else nullptr): each tile's sum of squares of
+  // its gradient block, at sumsq[(inst * spi + j) * sumsq_stride + tile] for
+  // matrix j (GRAD13: W1 and W3, j = 0 and 2; GRAD2: j = sumsq_j)
+  float* sumsq;
+  int sumsq_stride, sumsq_j, spi;
 };
 
 struct BwdArgs {
@@ -149,6 +154,12 @@ struct NsPrepArgs {
   float* M[3];
   const float* bbar;
   int bbar_stride;
+  // Without split and momentum the gradient tiles leave their sums of squares
+  // in sumsq (sum_n[j] entries per slot of matrix j) and k_ns_scale reads the
+  // gradient itself from src; nullptr src: Y32 and blocks_per_slot entries
+  // (filled by k_ns_prep)
+  const float* src;
+  int sum_n[3];
 };
 
 // Chunk means of the per-token momentum factor: for chunks c in [0, nchunks),

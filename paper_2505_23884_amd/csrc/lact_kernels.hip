@@ -1171,6 +1171,43 @@ __device__ __forceinline__ void grad_update_tile(const BwdSeg& sg, int inst, int
                               mrows, cols, smem);
 }
 
+// Sums of squares of accumulators 0 and NACC-1 of this workgroup's tile (for
+// the Frobenius norm of the gradient that Newton-Schulz divides by), in
+// thread 0; reuses the start of LDS, which the caller has finished with.
+template <class K>
+__device__ __forceinline__ float2 tile_sumsq(const Acc<K>& acc, uint8_t* smem) {
+  float a = 0.f, b = 0.f;
+#pragma unroll
+  for (int mi = 0; mi < K::MI; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < K::NI; ++ni)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        a = fmaf(acc[0][mi][ni][r], acc[0][mi][ni][r], a);
+        b = fmaf(acc[K::NACC - 1][mi][ni][r], acc[K::NACC - 1][mi][ni][r], b);
+      }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    a += __shfl_xor(a, off, 64);
+    b += __shfl_xor(b, off, 64);
+  }
+  float* red = reinterpret_cast<float*>(smem);
+  constexpr int NW = K::THREADS / 64;
+  if ((threadIdx.x & 63) == 0) {
+    red[threadIdx.x >> 6] = a;
+    red[NW + (threadIdx.x >> 6)] = b;
+  }
+  lds_barrier();
+  float2 t = make_float2(0.f, 0.f);
+  if (threadIdx.x == 0)
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      t.x += red[w];
+      t.y += red[NW + w];
+    }
+  return t;
+}
+
 // Second launch: apply GEMM-2 and the gradient contractions (split over tokens).
 template <typename T, bool NARROW>
 __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs args) {
@@ -1285,6 +1322,13 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
           }
         }
       }
+    if (sg.sumsq) {
+      const float2 t = tile_sumsq<K13>(acc, smem);
+      if (threadIdx.x == 0) {
+        sg.sumsq[((int64_t)inst * sg.spi + 0) * sg.sumsq_stride + rr] = t.x;
+        sg.sumsq[((int64_t)inst * sg.spi + 2) * sg.sumsq_stride + rr] = t.y;
+      }
+    }
   } else {
     // P2[m, j] = sum_i V[i, m] (eta hidden)[i, j]
     const int64_t r0 = (int64_t)(rr / sg.tiles_n) * K2::ROWS_A;
@@ -1304,6 +1348,10 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
           if (i < mrows && j < ncols) part[sg.out_off + (r0 + i) * h + c0 + j] = acc[0][mi][ni][r];
         }
       }
+    if (sg.sumsq) {
+      const float2 t = tile_sumsq<K2>(acc, smem);
+      if (threadIdx.x == 0) sg.sumsq[((int64_t)inst * sg.spi + sg.sumsq_j) * sg.sumsq_stride + rr] = t.x;
+    }
   }
 }
 
@@ -1888,21 +1936,24 @@ __global__ __launch_bounds__(256) void k_ns_prep(const NsPrepArgs a) {
   if (threadIdx.x == 0) a.sumsq[(int64_t)slot * a.blocks_per_slot + blk] = ss;
 }
 
-// X0 = G / (||G||_F + eps), fp32 iterate and operand copy.
+// X0 = G / (||G||_F + eps), fp32 iterate and operand copy; G is the summed
+// gradient (Y32) or, without split and momentum, the gradient partial itself.
 template <typename T>
 __global__ __launch_bounds__(256) void k_ns_scale(const NsPrepArgs a, void* yb, float eps) {
   __shared__ float red[4];
   const int slot = blockIdx.x / a.blocks_per_slot;
   const int blk = blockIdx.x - slot * a.blocks_per_slot;
   const int64_t base = (int64_t)slot * a.dh;
+  const int nsum = a.src ? a.sum_n[slot % a.spi] : a.blocks_per_slot;
   float t = 0.f;
-  for (int b = threadIdx.x; b < a.blocks_per_slot; b += 256) t += a.sumsq[(int64_t)slot * a.blocks_per_slot + b];
+  for (int b = threadIdx.x; b < nsum; b += 256) t += a.sumsq[(int64_t)slot * a.blocks_per_slot + b];
   t = block_sum(t, red);
   const float inv = 1.0f / (sqrtf(t) + eps);
+  const float* src = a.src ? a.src : a.Y32;
   for (int e = threadIdx.x; e < kNsBlockElems; e += 256) {
     const int64_t idx = (int64_t)blk * kNsBlockElems + e;
     if (idx < a.dh) {
-      const float y = a.Y32[base + idx] * inv;
+      const float y = src[base + idx] * inv;
       a.Y32[base + idx] = y;
       st_elem<T>(yb, base + idx, y);
     }

@@ -254,6 +254,7 @@ struct Ctx {
   Operand wop[3];   // operand copies of W1, W2, W3 (bf16 copies or the fp32 state)
   void* wb[2][3];   // the two sets of bf16 copies (the second with BWD_GRAD_UPD)
   int wset;         // the set wop points at
+  bool ns_updated;  // the last Newton-Schulz step has also applied the weight update
   const float* beta;   // momentum: per-token factor [BH][n_kv], or nullptr
   float* M[3];         // momentum state (with beta)
   int64_t chunk_idx;   // index of the chunk being updated
@@ -408,12 +409,17 @@ int newton_schulz(Ctx& c) {
   const int64_t mm = (int64_t)m * m;
   // 256 x 256 tiles for Gram matrices larger than 128, else 128 x 128
   const bool big = p.ns_fp16 && m > 128;
+  // Square matrices (d == h) of side up to 512 with 16-bit operands: the last
+  // step's update product and the weight update run as one launch
+  // (k_ns_final), which writes W and its copy instead of the iterate.
+  const bool fuse_last = p.ns_fp16 && d == h && m <= ns_final_tile().cols && c.dsc->ns_steps >= 1;
   for (int t = 0; t < c.dsc->ns_steps; ++t) {
     NsArgs a{};
     a.Y32 = pa.Y32;
     a.spi = p.nmat;
     a.Yin = c.ws + p.off_yb[t & 1];
-    a.Yout = c.ws + p.off_yb[(t + 1) & 1];
+    // the last step's operand copy would never be read: only the fp32 iterate
+    a.Yout = t + 1 < c.dsc->ns_steps ? (void*)(c.ws + p.off_yb[(t + 1) & 1]) : nullptr;
     a.Ab = c.ws + p.off_ab;
     a.A2b = c.ws + p.off_a2;
     a.Bb = c.ws + p.off_bb;
@@ -425,6 +431,27 @@ int newton_schulz(Ctx& c) {
     a.cc = 2.0315f;
     a.nseg = nseg;
     for (int phase = 0; phase < 3; ++phase) {
+      if (phase == 2 && fuse_last && t + 1 == c.dsc->ns_steps) {
+        NsFinalArgs f{};
+        f.Bb = c.ws + p.off_bb;
+        f.Yin = c.ws + p.off_yb[t & 1];
+        f.Y32 = pa.Y32;
+        for (int j = 0; j < p.nmat; ++j) {
+          f.W[j] = c.W[j];
+          f.Wb[j] = c.wb[c.wset][j];
+        }
+        f.spi = p.nmat;
+        f.m = m;
+        f.ystride = dh;
+        f.astride = mm;
+        f.nblocks = (int)(p.BH * p.nmat * cdiv(m, ns_final_tile().rows));
+        f.ca = 3.4445f;
+        const double fl = 2.0 * p.BH * p.nmat * (double)m * m * m;
+        rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns_final(f, c.s); });
+        if (rc) return rc;
+        c.ns_updated = true;
+        continue;
+      }
       a.total_blocks = 0;
       double fl = 0.0;
       for (int g = 0; g < nseg; ++g) {
@@ -641,8 +668,10 @@ int finish_update(Ctx& c) {
   }
   u.nmat = p.nmat;
   if (p.muon) {
+    c.ns_updated = false;
     rc = newton_schulz(c);
     if (rc) return rc;
+    if (c.ns_updated) return LACT_OK;
     u.step = reinterpret_cast<const float*>(c.ws + p.off_y32);
     u.nsplit = 1;
     u.step_split = 0;

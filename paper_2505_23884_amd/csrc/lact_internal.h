@@ -131,13 +131,29 @@ struct NsArgs {
   float* Y32;           // fp32 iterate (in place), slot stride ystride
   int spi;              // slots (matrices) per instance: 3 or 1
   const void* Yin;      // operand copy read this iteration (fp16 or fp32)
-  void* Yout;           // operand copy written this iteration
+  void* Yout;           // operand copy written this iteration (nullptr after the last)
   void* Ab;             // Gram operand copy, slot stride astride
   void* A2b;            // c A + b I (the polynomial's second factor), same layout
   void* Bb;             // polynomial operand copy
   int64_t ystride, astride;
   int m;                // Gram size min(d, h)
   float ca, cb, cc;     // quintic coefficients
+};
+
+// Last Newton-Schulz step fused with the weight update (square matrices of
+// side m <= 512, 16-bit operands): X5 = a X4 + B X4 for 128 whole rows per
+// workgroup, then U = W + X5, W <- U ||W_row|| / ||U_row|| and the bf16 copy.
+struct NsFinalArgs {
+  const void* Bb;       // polynomial B per slot (fp16, m x m), slot stride astride
+  const void* Yin;      // X4 per slot (fp16, m x m), slot stride ystride
+  const float* Y32;     // X4 per slot (fp32)
+  float* W[3];          // fp32 state of matrix j (instance stride ystride)
+  void* Wb[3];          // bf16 operand copies of matrix j
+  int spi;              // slots per instance (3, or 1 for the linear fast weight)
+  int m;                // side of every matrix
+  int64_t ystride, astride;
+  int nblocks;          // slots * row tiles
+  float ca;             // the quintic's a
 };
 
 struct NsPrepArgs {
@@ -240,6 +256,8 @@ hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d
 // Newton-Schulz operand copies are fp16 (bf16 I/O: 4x finer rounding than bf16
 // at the same MFMA rate; the iterates are O(1)) or fp32 (fp32 I/O).
 hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s);
+hipError_t launch_ns_final(const NsFinalArgs& a, hipStream_t s);
+TileShape ns_final_tile();   // k_ns_final: rows per workgroup x the largest side
 hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s);
 hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s);
 hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s);

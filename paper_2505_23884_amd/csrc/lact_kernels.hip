@@ -194,6 +194,10 @@ LACT_KIND(KNsK16S, 1, 1, 1, 0u, 2, 2, 2, 2, 2, true, 64, 0 * p, 0 * p);
 LACT_KIND(KNsMN16S, 1, 1, 1, 3u, 2, 2, 2, 2, 2, true, 64, 0 * p, 0 * p);
 LACT_KIND(KNsTY16S, 1, 1, 1, 1u, 2, 2, 2, 2, 2, true, 64, 0 * p, 0 * p);
 LACT_KIND(KNsK32, 1, 1, 1, 0u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
+// Last Newton-Schulz step with the weight update (k_ns_final): A = B (rows of
+// the polynomial, K-contiguous), B = X4 read down its columns; 128 rows x up
+// to 512 columns, waves of 64 x 128, 2 stages of 80 KiB.
+LACT_KIND(KNsRow16, 1, 1, 1, 2u, 2, 4, 2, 4, 2, true, 64, 0 * p, 0 * p);
 LACT_KIND(KNsMN32, 1, 1, 1, 3u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
 LACT_KIND(KNsTY32, 1, 1, 1, 1u, 2, 2, 2, 2, 2, false, 32, 0 * p, 0 * p);
 #undef LACT_KIND
@@ -1055,16 +1059,18 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
 
 // The weight update of a GRAD_UPD tile from its accumulators P (= -g):
 //   U = W + P,  W <- U ||W_row|| / ||U_row||   (§3.2 weight normalisation; Alg. 1)
-// or, with momentum (App. A; Table 3), Y = P - bbar M, M <- -Y, U = W + Y.
+// or, with momentum (App. A; Table 3), Y = P - bbar M, M <- -Y, U = W + Y;
+// with ADD (the last Newton-Schulz step) the step is P + xa X, X in W's layout.
 // The tile goes through LDS in passes of RP rows, so that lanes stream W (and
 // M) along whole rows in 16-byte vectors, as the separate update kernel does:
 // the rows of a pass are staged by the waves that hold them, TPR lanes share a
 // row, and a row's squared norms are summed over those lanes by shuffles. A
 // pass issues its W (and M) loads before the hand-over through LDS.
-template <class KG, bool MOM>
+template <class KG, bool MOM, bool ADD = false>
 __device__ __forceinline__ void update_rows(Acc<KG>& acc, float* W, __bf16* Wb, float* M, float bb, int64_t mrows,
-                                            int cols, uint8_t* smem) {
-  constexpr int RP = MOM ? 32 : 64;                 // rows per pass
+                                            int cols, uint8_t* smem, const float* X = nullptr, float xa = 0.f) {
+  static_assert(!(MOM && ADD), "one extra operand");
+  constexpr int RP = (MOM || ADD) ? 32 : 64;       // rows per pass
   constexpr int TPR = KG::THREADS / RP;             // lanes per row
   constexpr int NV = KG::ROWS_B / 4 / TPR;          // 16-byte vectors per lane
   constexpr int PITCH = KG::ROWS_B + 4;             // floats per LDS row
@@ -1078,13 +1084,14 @@ __device__ __forceinline__ void update_rows(Acc<KG>& acc, float* W, __bf16* Wb, 
   for (int pass = 0; pass < KG::ROWS_A / RP; ++pass) {
     const int64_t row = (int64_t)pass * RP + lr;
     const bool rok = row < mrows;
-    float4 w[NV], m[MOM ? NV : 1];
+    float4 w[NV], m[(MOM || ADD) ? NV : 1];
 #pragma unroll
     for (int q = 0; q < NV; ++q) {
       const int c4 = part + TPR * q;
       const bool ok = rok && c4 < nv;
       w[q] = ok ? reinterpret_cast<const float4*>(W + row * cols)[c4] : zero;
       if constexpr (MOM) m[q] = ok ? reinterpret_cast<const float4*>(M + row * cols)[c4] : zero;
+      if constexpr (ADD) m[q] = ok ? reinterpret_cast<const float4*>(X + row * cols)[c4] : zero;
     }
     // stage the accumulator rows [pass*RP, pass*RP + RP) (32-row blocks mi of wave row wave_m)
 #pragma unroll
@@ -1108,6 +1115,8 @@ __device__ __forceinline__ void update_rows(Acc<KG>& acc, float* W, __bf16* Wb, 
                         fmaf(-bb, m[q].w, y.w));
         m[q] = make_float4(-y.x, -y.y, -y.z, -y.w);
       }
+      if constexpr (ADD)
+        y = make_float4(fmaf(xa, m[q].x, y.x), fmaf(xa, m[q].y, y.y), fmaf(xa, m[q].z, y.z), fmaf(xa, m[q].w, y.w));
       const float4 x = w[q];
       sw += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
       w[q] = make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
@@ -1569,11 +1578,35 @@ __device__ __forceinline__ void ns_epilogue_staged(const Acc<KK>& acc, uint8_t* 
         const float4 y = make_float4(args.ca * o.x + v.x, args.ca * o.y + v.y, args.ca * o.z + v.z,
                                      args.ca * o.w + v.w);
         *reinterpret_cast<float4*>(Y32 + gidx[i]) = y;
-        st4<T>(Yout, gidx[i], y.x, y.y, y.z, y.w);
+        if (Yout) st4<T>(Yout, gidx[i], y.x, y.y, y.z, y.w);   // none after the last step
       }
     }
     if (half == 0) lds_barrier();   // every wave has read the first half
   }
+}
+
+// The last Newton-Schulz step of square matrices fused with the weight
+// update (Muon, §3.2; App. A): 128 whole rows of X5 = a X4 + B X4 per
+// workgroup (B X4 from the fp16 copies, a X4 from the fp32 iterate), then the
+// normalised update of the same rows of W with X5 as the step (update_rows):
+// X5 never goes to memory and no separate update launch runs.
+__global__ __launch_bounds__(KNsRow16::THREADS) void k_ns_final(const NsFinalArgs args) {
+  using KR = KNsRow16;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[smem_bytes<_Float16, KR>()];
+  const int tiles = (args.m + KR::ROWS_A - 1) / KR::ROWS_A;
+  const int bid = xcd_remap(blockIdx.x, args.nblocks);
+  const int slot = bid / tiles, tile = bid - slot * tiles;
+  const int inst = slot / args.spi, j = slot - inst * args.spi;
+  const int64_t r0 = (int64_t)tile * KR::ROWS_A;
+  const int64_t mrows = args.m - r0;
+  const Operand b = {reinterpret_cast<const uint8_t*>(args.Bb) + (int64_t)slot * args.astride * 2, args.m, 0};
+  const Operand x = {reinterpret_cast<const uint8_t*>(args.Yin) + (int64_t)slot * args.ystride * 2, args.m, 0};
+  const View ops[2] = {view_k(b, 0, r0, 0, mrows, args.m, 2), view_mn(x, 0, 0, 0, args.m, args.m, 2)};
+  Acc<KR> acc;
+  mainloop<_Float16, KR>(smem, ops, args.m, acc);
+  const int64_t off = (int64_t)inst * args.ystride + r0 * args.m;
+  update_rows<KR, false, true>(acc, args.W[j] + off, reinterpret_cast<__bf16*>(args.Wb[j]) + off, nullptr, 0.f, mrows,
+                               args.m, smem, args.Y32 + (int64_t)slot * args.ystride + r0 * args.m, args.ca);
 }
 
 template <typename T, bool BIG>
@@ -1601,7 +1634,7 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
   const int64_t mrows = sg.M - i0, ncols = sg.N - j0;
   float* Y32 = args.Y32 + slot * args.ystride;
   const uint8_t* Yin = reinterpret_cast<const uint8_t*>(args.Yin) + slot * args.ystride * esz;
-  void* Yout = reinterpret_cast<uint8_t*>(args.Yout) + slot * args.ystride * esz;
+  void* Yout = args.Yout ? reinterpret_cast<uint8_t*>(args.Yout) + slot * args.ystride * esz : nullptr;
   const uint8_t* Ab = reinterpret_cast<const uint8_t*>(args.Ab) + slot * args.astride * esz;
   void* Abw = reinterpret_cast<uint8_t*>(args.Ab) + slot * args.astride * esz;
   const uint8_t* A2 = reinterpret_cast<const uint8_t*>(args.A2b) + slot * args.astride * esz;
@@ -1662,7 +1695,7 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
           const float4 y =
               make_float4(args.ca * o.x + v0, args.ca * o.y + v1, args.ca * o.z + v2, args.ca * o.w + v3);
           *reinterpret_cast<float4*>(Y32 + idx) = y;
-          st4<T>(Yout, idx, y.x, y.y, y.z, y.w);
+          if (Yout) st4<T>(Yout, idx, y.x, y.y, y.z, y.w);
         }
       }
     }
@@ -2026,6 +2059,14 @@ TileShape ns_tile(bool fp16, bool big) {
   if (fp16 && big) return TileShape{KNsK16B::ROWS_A, KNsK16B::ROWS_B, KNsK16B::THREADS};
   if (fp16) return TileShape{KNsK16S::ROWS_A, KNsK16S::ROWS_B, KNsK16S::THREADS};
   return TileShape{KNsK32::ROWS_A, KNsK32::ROWS_B, KNsK32::THREADS};
+}
+
+TileShape ns_final_tile() { return TileShape{KNsRow16::ROWS_A, KNsRow16::ROWS_B, KNsRow16::THREADS}; }
+
+hipError_t launch_ns_final(const NsFinalArgs& a, hipStream_t s) {
+  if (a.nblocks <= 0) return hipSuccess;
+  k_ns_final<<<a.nblocks, KNsRow16::THREADS, 0, s>>>(a);
+  return hipGetLastError();
 }
 
 hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s) {

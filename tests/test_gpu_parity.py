@@ -513,6 +513,17 @@ def test_muon_small_gram_long_side_unfused():
     teacher_forced(cfg, x, [0, 1])
 
 
+@pytest.mark.parametrize("d", [160, 320])
+def test_muon_square_last_step_with_the_update(d):
+    # square matrices of side 128 < m <= 512: the last Newton-Schulz step and
+    # the weight update run as one launch (ragged last row tile: 160 = 128 + 32,
+    # 320 = 2 x 128 + 64); no separate update launch is left
+    cfg = CONFIGS["lm32k_muon"].with_(name="muon_square", B=1, H=2, d=d, h=d, n_kv=600, n_q=600, chunk=256)
+    x = make_inputs(cfg, 14)
+    _, n_upd = update_launches(lambda: teacher_forced(cfg, x, [0, 1]))
+    assert n_upd == 0
+
+
 def test_muon_fp32_teacher_forced():
     cfg = CONFIGS["tiny_fp32"].with_(name="muon_fp32", B=1, H=2, d=64, h=96, n_kv=512, n_q=512,
                                      chunk=256, use_muon=1, ns_steps=5)

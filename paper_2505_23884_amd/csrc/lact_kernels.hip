@@ -773,11 +773,6 @@ constexpr int cmax(int a, int b) { return a > b ? a : b; }
 // ===========================================================================
 // Epilogue helpers
 
-template <typename T>
-__device__ __forceinline__ void st_elem(void* base, int64_t idx, float v) {
-  reinterpret_cast<T*>(base)[idx] = (T)v;
-}
-
 // Four consecutive elements (8 bytes of 16-bit or 16 bytes of fp32) at idx.
 template <typename T>
 __device__ __forceinline__ void st4(void* base, int64_t idx, float a, float b, float c, float d) {
@@ -1951,18 +1946,23 @@ __global__ __launch_bounds__(256) void k_ns_prep(const NsPrepArgs a) {
   const int inst = slot / a.spi, j = slot - a.spi * (slot / a.spi);
   float* Ms = a.M[0] ? a.M[j] + (int64_t)inst * a.dh : nullptr;
   const float bb = Ms ? a.bbar[(int64_t)inst * a.bbar_stride] : 0.f;
+  // 16 bytes per lane (d*h is a multiple of 4, and so is every offset)
   float ss = 0.f;
-  for (int e = threadIdx.x; e < kNsBlockElems; e += 256) {
+  for (int e = 4 * threadIdx.x; e < kNsBlockElems; e += 4 * 256) {
     const int64_t idx = (int64_t)blk * kNsBlockElems + e;
     if (idx < a.dh) {
-      float g = 0.f;
-      for (int s = 0; s < a.nsplit; ++s) g += a.part[s * a.part_split + base + idx];
-      if (Ms) {
-        g = fmaf(-bb, Ms[idx], g);
-        Ms[idx] = -g;
+      float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int s = 0; s < a.nsplit; ++s) {
+        const float4 p = *reinterpret_cast<const float4*>(a.part + s * a.part_split + base + idx);
+        g = make_float4(g.x + p.x, g.y + p.y, g.z + p.z, g.w + p.w);
       }
-      a.Y32[base + idx] = g;
-      ss += g * g;
+      if (Ms) {
+        const float4 m = *reinterpret_cast<const float4*>(Ms + idx);
+        g = make_float4(fmaf(-bb, m.x, g.x), fmaf(-bb, m.y, g.y), fmaf(-bb, m.z, g.z), fmaf(-bb, m.w, g.w));
+        *reinterpret_cast<float4*>(Ms + idx) = make_float4(-g.x, -g.y, -g.z, -g.w);
+      }
+      *reinterpret_cast<float4*>(a.Y32 + base + idx) = g;
+      ss += g.x * g.x + g.y * g.y + g.z * g.z + g.w * g.w;
     }
   }
   ss = block_sum(ss, red);
@@ -1983,12 +1983,13 @@ __global__ __launch_bounds__(256) void k_ns_scale(const NsPrepArgs a, void* yb, 
   t = block_sum(t, red);
   const float inv = 1.0f / (sqrtf(t) + eps);
   const float* src = a.src ? a.src : a.Y32;
-  for (int e = threadIdx.x; e < kNsBlockElems; e += 256) {
+  for (int e = 4 * threadIdx.x; e < kNsBlockElems; e += 4 * 256) {
     const int64_t idx = (int64_t)blk * kNsBlockElems + e;
     if (idx < a.dh) {
-      const float y = src[base + idx] * inv;
-      a.Y32[base + idx] = y;
-      st_elem<T>(yb, base + idx, y);
+      const float4 g = *reinterpret_cast<const float4*>(src + base + idx);
+      const float4 y = make_float4(g.x * inv, g.y * inv, g.z * inv, g.w * inv);
+      *reinterpret_cast<float4*>(a.Y32 + base + idx) = y;
+      st4<T>(yb, base + idx, y.x, y.y, y.z, y.w);
     }
   }
 }

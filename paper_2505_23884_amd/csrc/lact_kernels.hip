@@ -1457,14 +1457,17 @@ __global__ __launch_bounds__(256) void k_update(const UpdArgs a) {
   }
 }
 
+// n4 16-byte vectors of every matrix (d*h is a multiple of 64).
 __global__ __launch_bounds__(256) void k_prep(const float* w1, const float* w2, const float* w3, __bf16* b1,
-                                              __bf16* b2, __bf16* b3, int64_t n) {
+                                              __bf16* b2, __bf16* b3, int64_t n4) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) {
-    b1[i] = (__bf16)w1[i];
+  if (i < n4) {
+    const float4 a = reinterpret_cast<const float4*>(w1)[i];
+    st4<__bf16>(b1, 4 * i, a.x, a.y, a.z, a.w);
     if (w2) {   // null for a single fast-weight matrix
-      b2[i] = (__bf16)w2[i];
-      b3[i] = (__bf16)w3[i];
+      const float4 b = reinterpret_cast<const float4*>(w2)[i], c = reinterpret_cast<const float4*>(w3)[i];
+      st4<__bf16>(b2, 4 * i, b.x, b.y, b.z, b.w);
+      st4<__bf16>(b3, 4 * i, c.x, c.y, c.z, c.w);
     }
   }
 }
@@ -2172,11 +2175,11 @@ hipError_t launch_scale_rows(const void* k, const float* eta, void* out, int BH,
 }
 
 hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d, int h, hipStream_t s) {
-  const int64_t n = (int64_t)BH * d * h;
-  const int64_t blocks = (n + 255) / 256;
+  const int64_t n4 = (int64_t)BH * d * h / 4;
+  const int64_t blocks = (n4 + 255) / 256;
   if (blocks <= 0) return hipSuccess;
   k_prep<<<(unsigned)blocks, 256, 0, s>>>(W[0], W[1], W[2], reinterpret_cast<__bf16*>(Wb[0]),
-                                         reinterpret_cast<__bf16*>(Wb[1]), reinterpret_cast<__bf16*>(Wb[2]), n);
+                                         reinterpret_cast<__bf16*>(Wb[1]), reinterpret_cast<__bf16*>(Wb[2]), n4);
   return hipGetLastError();
 }
 

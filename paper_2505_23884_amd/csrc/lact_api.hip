@@ -592,10 +592,11 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
       g.bbar_stride = kBetaBatch;
     }
   }
-  // Gradient contractions, split over tokens; a split past the chunk's end
-  // writes zeros so the update always sums p.nsplit partials.
+  // Otherwise the gradient contractions, split over tokens (a split past the
+  // chunk's end writes zeros so the update always sums p.nsplit partials),
+  // and the update in a launch of its own (finish_update).
   const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16, p.narrow), g2 = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
-  if (!fused) {
+  if (!fused) {   // W1's and W3's gradients
     BwdSeg& g = b.seg[nb++];
     g.kind = BWD_GRAD13;
     g.tiles_m = (int)cdiv(p.h, g13.rows);
@@ -612,7 +613,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.out_split = (int64_t)p.BH * 3 * dh;
     set_tile_sums(c, g, 0);
   }
-  if (!fused) {
+  if (!fused) {   // W2's gradient
     BwdSeg& g = b.seg[nb++];
     g.kind = BWD_GRAD2;
     g.tiles_m = (int)cdiv(p.d, g2.rows);

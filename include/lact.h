@@ -83,7 +83,9 @@ typedef struct lact_desc {
   int32_t d, h;       /* head dim and fast-weight hidden dim; envelope: in      */
                       /* [8, 4096], multiples of 8 (fp32 I/O) or of 32 (bf16    */
                       /* I/O: whole 16-byte DMA chunks of a 16-K MFMA step);     */
-                      /* B*H <= 2^20, n_q <= 2^40                               */
+                      /* B*H <= 2^20, n_q <= 2^40, and every launch grid under  */
+                      /* 2^31 workgroups (B*H x (max(d,h)/128)^2 x 128 bounds   */
+                      /* the largest; beyond any GPU memory well before)        */
   int64_t n_kv;       /* tokens carrying k, v, eta (>= 0)                       */
   int64_t n_q;        /* tokens carrying q (>= n_kv)                            */
   int64_t chunk;      /* key tokens per update (>= 1); the last chunk may be    */

@@ -63,6 +63,18 @@ int check_desc(const lact_desc* d) {
   if (d->io_dtype == LACT_IO_BF16 && (d->d % 32 || d->h % 32)) return LACT_EUNSUPPORTED;
   if ((int64_t)d->B * d->H > (1 << 20)) return LACT_EUNSUPPORTED;
   if (d->n_q > ((int64_t)1 << 40)) return LACT_EUNSUPPORTED;
+  // Every launch's grid must fit the 32-bit block count: bounds with the
+  // smallest tile edge (128) for the contractions, the most splits for the
+  // gradient, one wave per weight row for the update and 4096-element blocks
+  // for the Newton-Schulz prologue (such sizes exceed any GPU's memory long
+  // before they reach these bounds, but the check keeps the launches exact).
+  const int64_t BH = (int64_t)d->B * d->H, mx = std::max(d->d, d->h);
+  const int64_t C = std::min<int64_t>(d->chunk, d->n_kv);
+  const int64_t L = std::max<int64_t>(std::max<int64_t>(C, 1), std::min<int64_t>(d->n_q, C + std::max<int64_t>(C, 65536)));
+  const int64_t t = (mx + 127) / 128;
+  const double most = std::max({(double)BH * t * ((L + 127) / 128) * 2.0, (double)BH * t * t * 2.0 * kMaxSplit,
+                                (double)BH * 3.0 * mx, (double)BH * 3.0 * ((mx * mx + 4095) / 4096)});
+  if (most > 2147483647.0) return LACT_EUNSUPPORTED;
   return LACT_OK;
 }
 

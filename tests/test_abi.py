@@ -52,6 +52,15 @@ def test_descriptor_validation(field, value, code):
     assert err.value == code
 
 
+def test_launch_grids_that_overflow_are_rejected():
+    # 2^20 instances of 4096 x 4096 fast weights: the gradient's grid alone
+    # would pass 2^31 blocks; the largest realistic shapes stay accepted
+    big = dict(GOOD, B=1 << 10, H=1 << 10, d=4096, h=4096, n_kv=1024, n_q=1024)
+    assert P.check_desc(make_desc(**big)) == -4
+    nvs = dict(GOOD, B=1, H=1, d=768, h=1536, n_kv=1 << 30, n_q=(1 << 30) + 4096, chunk=1 << 30, order=1)
+    assert P.check_desc(make_desc(**nvs)) == 0
+
+
 def test_fp32_envelope_is_multiples_of_8():
     # bf16 I/O needs multiples of 32 (d = 40 is rejected above); fp32 I/O takes 8
     kw = dict(GOOD, d=40, h=24, io_dtype=1)

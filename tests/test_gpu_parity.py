@@ -255,6 +255,58 @@ def test_fused_momentum_at_beta_zero_is_the_plain_path():
         assert rel(M_m[j], ref[4 + j]) <= TOL["bf16"]
 
 
+# ----------------------------------------------------------------------------- HIP graph capture
+# The entry points launch kernels only (no allocation, copy, memset or sync),
+# so a caller can capture a whole forward in a HIP graph (torch.cuda.CUDAGraph
+# on ROCm) and replay it. Every replay, with eager work between replays, must
+# reproduce the eager result bitwise (the path is deterministic).
+
+
+@pytest.mark.parametrize("name,muon", [("lm32k", 0), ("video", 1)])
+def test_forward_captured_in_a_graph_replays_bitwise(name, muon):
+    base = CONFIGS[name]
+    cfg = base.with_(name="graph_" + name, B=1, H=13, d=base.d if name == "video" else 320,
+                     h=base.h if name == "video" else 288, n_kv=700, n_q=760, chunk=256, use_muon=muon,
+                     ns_steps=5 if muon else 0)
+    x = make_inputs(cfg, 91)
+    print(f"[gpu] graph capture {cfg.name} d={cfg.d} h={cfg.h} muon={muon}", flush=True)
+    sh = lambda a: a.reshape(cfg.B, cfg.H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    W0 = [to_dev(sh(x[w]), cfg, torch.float32) for w in ("W1", "W2", "W3")]
+    kw = dict(chunk=cfg.chunk, order=cfg.order, use_muon=bool(muon), ns_steps=cfg.ns_steps)
+    W = [w.clone() for w in W0]
+    o_ref = P.forward(q, k, v, eta, *W, **kw)
+    torch.cuda.synchronize()
+    W_ref = [w.clone() for w in W]
+    desc = P.binding.make_desc(cfg.B, cfg.H, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.chunk, cfg.order, muon,
+                               cfg.ns_steps, P.IO_BF16)
+    ws = torch.empty(P.workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    out = torch.empty_like(q)
+    Wg = [w.clone() for w in W0]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):   # warm the launch path outside the capture
+        P.forward(q, k, v, eta, *Wg, out=out, workspace=ws, **kw)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        P.forward(q, k, v, eta, *Wg, out=out, workspace=ws, **kw)
+    for rep in range(3):
+        for a, b in zip(Wg, W0):
+            a.copy_(b)
+        out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, o_ref), rep
+        assert all(torch.equal(a, b) for a, b in zip(Wg, W_ref)), rep
+        junk = torch.randn(1 << 20, device="cuda").sum()   # eager work between the replays
+        torch.cuda.synchronize()
+        del junk
+
+
 # ----------------------------------------------------------------------------- seeded shape sweep
 # Shapes drawn from a fixed seed: bf16 (d, h multiples of 32 up to 640) and
 # fp32 (multiples of 8 up to 160), 1-16 instances, 1-1200 key tokens, a query

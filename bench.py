@@ -53,6 +53,8 @@ def parse():
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the step replayed from a HIP graph captured once (host launch cost removed)")
     ap.add_argument("--library-gemms", action="store_true",
                     help="time the path's plain contractions as library GEMMs (torch.matmul), for context")
     ap.add_argument("--traffic-report", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"))
@@ -352,6 +354,10 @@ def main():
                                bool(cfg.lr3), P.FW_LINEAR if cfg.linear else P.FW_SWIGLU)
     ws = torch.empty(P.workspace_bytes(desc), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
+    launch_on = [stream]   # None while a step is captured into a HIP graph: torch's current stream
+
+    def launch_stream():
+        return launch_on[0].cuda_stream if launch_on[0] is not None else None
 
     io_step = None
     if cfg.layer_io:
@@ -363,8 +369,8 @@ def main():
         y = torch.empty(cfg.B, cfg.n_q, cfg.H, cfg.d, dtype=io, device=dev)
         io_step = {
             "prologue": lambda: P.prologue(qkv_raw, lr_raw, -4.6, n_kv=cfg.n_kv, out=(q, k, v, eta, None),
-                                           stream=stream.cuda_stream),
-            "rmsnorm": lambda: P.rmsnorm_out(out, rms_w, 1e-6, out=y, stream=stream.cuda_stream),
+                                           stream=launch_stream()),
+            "rmsnorm": lambda: P.rmsnorm_out(out, rms_w, 1e-6, out=y, stream=launch_stream()),
         }
         esz = 2 if cfg.io == "bf16" else 4
         R = 3 if cfg.lr3 else 1
@@ -388,25 +394,36 @@ def main():
     def path():
         if cfg.linear:
             P.forward_linear(q, k, v, eta, W[0], cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
-                             ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=stream.cuda_stream)
+                             ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=launch_stream())
         elif sched is not None:
             P.forward_schedule(q, k, v, eta, *W, sched, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
-                               chunk=cfg.chunk, out=out, workspace=ws, stream=stream.cuda_stream,
+                               chunk=cfg.chunk, out=out, workspace=ws, stream=launch_stream(),
                                **({"beta": beta, "M1": M[0], "M2": M[1], "M3": M[2]} if cfg.momentum else {}))
         elif cfg.momentum:
             P.forward_momentum(q, k, v, eta, beta, *W, *M, chunk=cfg.chunk, order=cfg.order,
                                use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps, out=out, workspace=ws,
-                               stream=stream.cuda_stream)
+                               stream=launch_stream())
         else:
             P.forward(q, k, v, eta, *W, chunk=cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
-                      ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=stream.cuda_stream)
+                      ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=launch_stream())
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    run = step
+    if args.graph:
+        # the whole step captured once into a HIP graph and replayed: the
+        # entry points launch kernels only, so the replay does the same work
+        graph = torch.cuda.CUDAGraph()
+        launch_on[0] = None
+        with torch.cuda.graph(graph):
+            step()
+        launch_on[0] = stream
+        torch.cuda.synchronize()
+        run = graph.replay
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        run()
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / max(args.steps, 1)
 
@@ -421,6 +438,7 @@ def main():
         "dtype": "bf16" if cfg.io == "bf16" else "fp32", "data": "synthetic",
         "config": {"workload": describe(cfg), "tokens_per_step": tokens, "flops_per_step": flops},
         "tokens_per_s": round(tokens / dt, 1),
+        "launch": "hip_graph" if args.graph else "eager",
         "pct_of_peak": round(100.0 * tflops / peak, 2),
     }
     if cfg.use_muon:   # the same time over the token FLOPs alone (Newton-Schulz FLOPs left out)

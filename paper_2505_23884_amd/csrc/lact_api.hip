@@ -412,9 +412,9 @@ int newton_schulz(Ctx& c) {
       f.cols = cols[g];
       f.nblocks = p.BH * f.group;
       f.steps = c.dsc->ns_steps;
-      f.ca = 3.4445f;
-      f.cb = -4.7750f;
-      f.cc = 2.0315f;
+      f.ca = kNsA;
+      f.cb = kNsB;
+      f.cc = kNsC;
       const double fl = (double)f.steps * f.nblocks * (4.0 * m * m * n + 2.0 * m * m * m);
       rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns_fused(f, c.s); });
       if (rc) return rc;
@@ -441,9 +441,9 @@ int newton_schulz(Ctx& c) {
     a.ystride = dh;
     a.astride = mm;
     a.m = m;
-    a.ca = 3.4445f;
-    a.cb = -4.7750f;
-    a.cc = 2.0315f;
+    a.ca = kNsA;
+    a.cb = kNsB;
+    a.cc = kNsC;
     a.nseg = nseg;
     for (int phase = 0; phase < 3; ++phase) {
       if (phase == 2 && fuse_last && t + 1 == c.dsc->ns_steps) {
@@ -460,7 +460,7 @@ int newton_schulz(Ctx& c) {
         f.ystride = dh;
         f.astride = mm;
         f.nblocks = (int)(p.BH * p.nmat * cdiv(m, ns_final_tile().rows));
-        f.ca = 3.4445f;
+        f.ca = kNsA;
         const double fl = 2.0 * p.BH * p.nmat * (double)m * m * m;
         rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns_final(f, c.s); });
         if (rc) return rc;

@@ -195,6 +195,9 @@ struct BetaArgs {
 // Whole Newton-Schulz iteration of small matrices, one workgroup per matrix:
 // Gram size m <= 128 and long side n <= 256 (fp16 operands).
 constexpr int kNsFusedM = 128, kNsFusedN = 256;
+// Quintic Newton-Schulz coefficients (a, b, c) of Muon (App. A, Details of Muon):
+// X <- a X + b (X X^T) X + c (X X^T)^2 X
+constexpr float kNsA = 3.4445f, kNsB = -4.7750f, kNsC = 2.0315f;
 struct NsFusedArgs {
   float* Y32;           // fp32 iterate, slot stride ystride: in = scaled gradient, out = NS result
   int spi;              // slots per instance

@@ -422,7 +422,10 @@ int newton_schulz(Ctx& c) {
     return LACT_OK;
   }
   const int64_t mm = (int64_t)m * m;
-  // 256 x 256 tiles for Gram matrices larger than 128, else 128 x 128
+  // Gram matrices larger than 128 (16-bit operands): the update product in
+  // 256 x 256 tiles; the Gram and polynomial products, which are symmetric,
+  // in 128 x 128 tiles of the upper triangle only (10 of 16 at m = 512), two
+  // workgroups per CU. Smaller matrices: 128 x 128 tiles throughout.
   const bool big = p.ns_fp16 && m > 128;
   // Square matrices (d == h) of side up to 512 with 16-bit operands: the last
   // step's update product and the weight update run as one launch
@@ -469,8 +472,11 @@ int newton_schulz(Ctx& c) {
       }
       a.total_blocks = 0;
       double fl = 0.0;
+      const bool tri = big && phase < 2;
+      const bool bigp = big && !tri;
       for (int g = 0; g < nseg; ++g) {
         NsSeg& sg = a.seg[g];
+        sg.tri = tri;
         sg.group = group_of(g);
         sg.slot_off[0] = slot_of(g);
         sg.slot_off[1] = 2;
@@ -491,13 +497,23 @@ int newton_schulz(Ctx& c) {
           sg.N = rows[g];
           sg.K = m;
         }
-        sg.tiles_m = (int)cdiv(sg.M, ns_tile(p.ns_fp16, big).rows);
-        sg.tiles_n = (int)cdiv(sg.N, ns_tile(p.ns_fp16, big).cols);
-        sg.nblocks = p.BH * sg.group * sg.tiles_m * sg.tiles_n;
+        const TileShape ts = ns_tile(p.ns_fp16, bigp);
+        sg.tiles_m = (int)cdiv(sg.M, ts.rows);
+        sg.tiles_n = (int)cdiv(sg.N, ts.cols);
+        sg.nblocks = p.BH * sg.group * (tri ? sg.tiles_m * (sg.tiles_m + 1) / 2 : sg.tiles_m * sg.tiles_n);
         a.total_blocks += sg.nblocks;
-        fl += 2.0 * p.BH * sg.group * (double)sg.M * sg.N * sg.K;
+        // FLOPs of the tiles computed (the triangle's: its off-diagonal tiles
+        // are written twice but computed once)
+        double area = (double)sg.M * sg.N;
+        if (tri) {
+          area = 0.0;
+          for (int ti = 0; ti < sg.tiles_m; ++ti)
+            for (int tj = ti; tj < sg.tiles_m; ++tj)
+              area += (double)std::min(ts.rows, sg.M - ti * ts.rows) * std::min(ts.cols, sg.N - tj * ts.cols);
+        }
+        fl += 2.0 * p.BH * sg.group * area * sg.K;
       }
-      rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns(a, p.ns_fp16, big, c.s); });
+      rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns(a, p.ns_fp16, bigp, c.s); });
       if (rc) return rc;
     }
   }

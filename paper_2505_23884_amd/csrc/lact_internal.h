@@ -122,6 +122,8 @@ struct NsSeg {
   int slot_off[2];      // j of each matrix of the group
   int M, N, K;          // output rows, output columns, contraction length
   int ldy;              // columns c of the stored Y
+  int tri;              // symmetric product: tiles of the upper triangle only
+                        // (square tiles); off-diagonal ones also write their mirror
 };
 
 struct NsArgs {

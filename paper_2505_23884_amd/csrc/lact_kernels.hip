@@ -1514,11 +1514,16 @@ __global__ __launch_bounds__(256) void k_scale_rows(const T* k, const float* eta
 // layout, each store instruction touched 32 rows 32 bytes at a time, and the
 // epilogue took longer than the product. 16-byte chunks are XOR-swizzled by
 // the staged row so that the column-wise writes and the row-wise reads are
-// both free of bank conflicts.
-template <typename T, class KK>
+// both free of bank conflicts. With `mirror` (an off-diagonal tile of a
+// symmetric product computed for the upper triangle only) the Gram and
+// polynomial tiles are also written untransposed, to rows i0 + r and columns
+// j0 + c: each lane gathers four consecutive staged rows of one tile row
+// (compiled in with MIRROR only: the 128 x 128 kinds).
+template <typename T, class KK, bool MIRROR>
 __device__ __forceinline__ void ns_epilogue_staged(const Acc<KK>& acc, uint8_t* smem, const NsArgs& args, int kind,
                                                    int64_t ld, int64_t i0, int64_t j0, int64_t mrows, int64_t ncols,
-                                                   void* Abw, void* A2w, float* Y32, void* Yout, void* Bbw) {
+                                                   void* Abw, void* A2w, float* Y32, void* Yout, void* Bbw,
+                                                   bool mirror) {
   constexpr int R = KK::ROWS_A;                  // tile rows = stored columns
   constexpr int SR = KK::WN * 32;                // staged stored rows per half
   constexpr int CPR = R / 4;                     // 16-byte chunks per staged row
@@ -1579,6 +1584,32 @@ __device__ __forceinline__ void ns_epilogue_staged(const Acc<KK>& acc, uint8_t* 
         if (Yout) st4<T>(Yout, gidx[i], y.x, y.y, y.z, y.w);   // none after the last step
       }
     }
+    if (MIRROR && mirror) {
+      // staged rows 4 s4 .. 4 s4 + 3 are tile columns c0 .. c0 + 3 (one 32-block)
+      constexpr int S4 = SR / 4;
+      constexpr int PERM = R * S4 / KK::THREADS;
+      static_assert((R * S4) % KK::THREADS == 0, "mirror shape");
+#pragma unroll
+      for (int i = 0; i < PERM; ++i) {
+        const int q = i * KK::THREADS + threadIdx.x;
+        const int r = q / S4, s0 = 4 * (q % S4);
+        const int c0 = (s0 / 32) * (KK::NI * 32) + half * 32 + (s0 & 31);
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int sr = s0 + e;
+          v[e] = st[sr * R + ((((r >> 2) ^ (sr & (CPR - 1)))) << 2) + (r & 3)];
+        }
+        if (r >= mrows || c0 >= ncols) continue;
+        const int64_t g = (i0 + r) * ld + j0 + c0;
+        if (gram) {
+          st4<T>(Abw, g, v[0], v[1], v[2], v[3]);
+          st4<T>(A2w, g, args.cc * v[0], args.cc * v[1], args.cc * v[2], args.cc * v[3]);   // off the diagonal
+        } else {
+          st4<T>(Bbw, g, v[0], v[1], v[2], v[3]);
+        }
+      }
+    }
     if (half == 0) lds_barrier();   // every wave has read the first half
   }
 }
@@ -1623,10 +1654,20 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
   const NsSeg& sg = first ? args.seg[0] : args.seg[1];
   if (!first) bid -= args.seg[0].nblocks;
   bid = xcd_remap(bid, sg.nblocks);
-  const int per = sg.tiles_m * sg.tiles_n;
+  const int per = sg.tri ? sg.tiles_m * (sg.tiles_m + 1) / 2 : sg.tiles_m * sg.tiles_n;
   const int q = bid / per;
   const int rr = bid - q * per;
-  const int64_t i0 = (int64_t)(rr / sg.tiles_n) * KK::ROWS_A, j0 = (int64_t)(rr % sg.tiles_n) * KK::ROWS_B;
+  int ti = rr / sg.tiles_n, tj = rr % sg.tiles_n;
+  if (sg.tri) {   // row ti of the upper triangle holds tiles_m - ti tiles
+    ti = 0;
+    int left = rr;
+    while (left >= sg.tiles_m - ti) {
+      left -= sg.tiles_m - ti;
+      ++ti;
+    }
+    tj = ti + left;
+  }
+  const int64_t i0 = (int64_t)ti * KK::ROWS_A, j0 = (int64_t)tj * KK::ROWS_B;
   const int64_t slot = (int64_t)(q / sg.group) * args.spi + sg.slot_off[q % sg.group];
   const int m = args.m, ldy = sg.ldy;
   const int64_t mrows = sg.M - i0, ncols = sg.N - j0;
@@ -1665,7 +1706,8 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
   const bool gram = kind == NS_GRAM_K || kind == NS_GRAM_MN;
   const int64_t ld = (gram || kind == NS_POLY) ? m : ldy;
   if constexpr (sizeof(T) == 2) {
-    ns_epilogue_staged<T, KK>(acc, smem, args, kind, ld, i0, j0, mrows, ncols, Abw, A2w, Y32, Yout, Bbw);
+    ns_epilogue_staged<T, KK, !BIG>(acc, smem, args, kind, ld, i0, j0, mrows, ncols, Abw, A2w, Y32, Yout, Bbw,
+                                    sg.tri && ti != tj && (gram || kind == NS_POLY));
     return;
   }
 #pragma unroll

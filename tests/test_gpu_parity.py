@@ -548,12 +548,25 @@ def test_muon_small_teacher_forced_and_two_chunks(order):
 
 
 def test_muon_large_gram_ragged_tiles():
-    # Gram size 256 > 128 takes the 256 x 256 Newton-Schulz tiles; h = 384 gives
-    # a ragged second tile; W1, W3 (384 x 256) iterate tall, W2 (256 x 384) wide
+    # Gram size 256 > 128: the update product takes 256 x 256 Newton-Schulz
+    # tiles (h = 384 gives a ragged second tile), the Gram and polynomial
+    # products the upper triangle of 128 x 128 tiles; W1, W3 (384 x 256)
+    # iterate tall, W2 (256 x 384) wide
     cfg = CONFIGS["lm32k_muon"].with_(name="muon_big", B=1, H=1, d=256, h=384, n_kv=512, n_q=512,
                                       chunk=256)
     x = make_inputs(cfg, 12)
     teacher_forced(cfg, x, [0])
+
+
+def test_muon_gram_triangle_three_tiles_wide_and_tall():
+    # Gram size 384: the Gram and polynomial products run over the upper
+    # triangle of a 3 x 3 grid of 128 x 128 tiles (three of the six tiles are
+    # off the diagonal and mirrored); W1, W3 (512 x 384) iterate tall, W2
+    # (384 x 512) wide, so both Gram orientations take the triangle
+    cfg = CONFIGS["lm32k_muon"].with_(name="muon_tri", B=1, H=2, d=384, h=512, n_kv=512, n_q=512,
+                                      chunk=256)
+    x = make_inputs(cfg, 15)
+    teacher_forced(cfg, x, [0, 1])
 
 
 def test_muon_small_gram_long_side_unfused():

@@ -122,8 +122,9 @@ struct NsSeg {
   int slot_off[2];      // j of each matrix of the group
   int M, N, K;          // output rows, output columns, contraction length
   int ldy;              // columns c of the stored Y
-  int tri;              // symmetric product: tiles of the upper triangle only
-                        // (square tiles); off-diagonal ones also write their mirror
+  int tri;              // symmetric product (16-bit operands, 128 x 128 tiles
+                        // only): tiles of the upper triangle, the off-diagonal
+                        // ones also writing their mirror
 };
 
 struct NsArgs {

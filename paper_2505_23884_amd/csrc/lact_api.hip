@@ -32,7 +32,7 @@ struct Plan {
   int nsplit;         // split-K ways of the gradient contraction
   int64_t split_len;  // tokens per split
   bool fused;         // gradient and weight update in one kind (BWD_GRAD_UPD)
-  bool narrow;        // narrow tile shapes of the second launch (16-bit, d <= 128)
+  bool narrow;        // narrow tile shapes of both launches (16-bit, d <= 128)
   bool muon;
   bool tile_sums;     // Muon without split: the gradient tiles leave the sums of squares
   int t13, t2;        // gradient tiles per matrix (W1 or W3; W2 or the linear W)
@@ -316,8 +316,8 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
     FwdArgs f{};
     FwdSeg& g = f.seg[0];
     g.kind = FWD_APPLY;
-    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_APPLY, p.bf16).rows);
-    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_APPLY, p.bf16).cols);
+    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_APPLY, p.bf16, p.narrow).rows);
+    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_APPLY, p.bf16, p.narrow).cols);
     g.nblocks = p.BH * g.tiles_m * g.tiles_n;
     g.rows = n;
     g.a0 = op(c.q + a * p.d * p.esz, p.d, c.dsc->n_q * p.d);
@@ -327,6 +327,7 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
     f.total_blocks = g.nblocks;
     f.d = p.d;
     f.h = p.h;
+    f.narrow = p.narrow;
     f.w1 = c.wop[0];
     f.w2 = c.wop[1];
     f.w3 = c.wop[2];
@@ -554,8 +555,8 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   {
     FwdSeg& g = f.seg[ns++];
     g.kind = FWD_UPDATE;
-    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_UPDATE, p.bf16).rows);
-    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_UPDATE, p.bf16).cols);
+    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_UPDATE, p.bf16, p.narrow).rows);
+    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_UPDATE, p.bf16, p.narrow).cols);
     g.nblocks = p.BH * g.tiles_m * g.tiles_n;
     g.rows = n;
     g.a0 = op(c.k + s0 * p.d * p.esz, p.d, c.dsc->n_kv * p.d);
@@ -571,8 +572,8 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   if (apply_too) {
     FwdSeg& g = f.seg[ns++];
     g.kind = FWD_APPLY;
-    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_APPLY, p.bf16).rows);
-    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_APPLY, p.bf16).cols);
+    g.tiles_m = (int)cdiv(p.h, fwd_tile(FWD_APPLY, p.bf16, p.narrow).rows);
+    g.tiles_n = (int)cdiv(n, fwd_tile(FWD_APPLY, p.bf16, p.narrow).cols);
     g.nblocks = p.BH * g.tiles_m * g.tiles_n;
     g.rows = n;
     g.a0 = op(c.q + s0 * p.d * p.esz, p.d, c.dsc->n_q * p.d);
@@ -583,6 +584,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   f.total_blocks = f.seg[0].nblocks + (ns > 1 ? f.seg[1].nblocks : 0);   // long tiles first
   f.d = p.d;
   f.h = p.h;
+  f.narrow = p.narrow;
   f.w1 = c.wop[0];
   f.w2 = c.wop[1];
   f.w3 = c.wop[2];

@@ -45,6 +45,7 @@ struct FwdArgs {
   int d, h;
   Operand w1, w3;       // h x d, kmajor (operand copies of the fast weight)
   Operand w2;           // d x h; the key forward reads it as an mn operand
+  bool narrow;          // 128 x 128 tiles, two workgroups per CU (16-bit, d <= 128)
 };
 
 // ---- second launch: apply GEMM-2 and/or the gradient contractions ---------
@@ -243,7 +244,7 @@ hipError_t launch_rmsnorm_out(RmsArgs a, bool io_bf16, hipStream_t s);
 struct TileShape {
   int rows, cols, threads;
 };
-TileShape fwd_tile(int kind, bool io_bf16);   // rows = hidden units, cols = tokens
+TileShape fwd_tile(int kind, bool io_bf16, bool narrow);   // rows = hidden units, cols = tokens
 TileShape bwd_tile(int kind, bool io_bf16, bool narrow);   // OUT: features x tokens; GRAD13:
                                                            // hidden x features; GRAD2: features x hidden
 TileShape ns_tile(bool fp16, bool big);       // tile-space rows x columns of the NS products

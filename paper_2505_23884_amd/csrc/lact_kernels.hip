@@ -175,6 +175,13 @@ LACT_KIND(KGradU16, 1, 1, 1, 3u, 2, 4, 2, 4, 4, true, 32, 0 * p, 0 * p);
 LACT_KIND(KOutN16, 1, 1, 1, 0u, 2, 4, 2, 4, 2, true, 64, 0 * p, 0 * p);
 LACT_KIND(KGrad13N16, 2, 1, 2, 7u, 4, 2, 2, 2, 4, true, 32, p, 0 * p);
 LACT_KIND(KGrad2N16, 1, 1, 1, 3u, 2, 4, 2, 2, 4, true, 32, 0 * p, 0 * p);
+// First launch for d <= 128 (16-bit): 4 waves of 64 x 64 (128 hidden x 128
+// tokens) and 32-K stages, so that a workgroup takes 64 KiB of LDS (its
+// output staging) and two workgroups share a CU: with K = d this short, a
+// tile's time is mostly the wait for its first stage and the epilogue, which
+// the other workgroup's loop overlaps.
+LACT_KIND(KApplyN16, 2, 1, 2, 0u, 2, 2, 2, 2, 2, true, 32, p, 0 * p);
+LACT_KIND(KDualN16, 1, 1, 1, 1u, 2, 2, 2, 2, 2, true, 32, 0 * p, 0 * p);
 // fp32 shapes: 4 waves of 64 x 64 (128 x 128 tiles), register path; the key
 // forward and its hidden backward share one loop (A = W1, W3, W2; B = K, V).
 LACT_KIND(KApply32, 2, 1, 2, 0u, 2, 2, 2, 2, 2, false, 32, p, 0 * p);
@@ -233,6 +240,20 @@ template <> struct Kinds<float> {
   using Out = KOut32;
   using Grad13 = KGrad13_32;
   using Grad2 = KGrad2_32;
+};
+
+// Kinds of the first launch: apply, key forward and its hidden backward.
+template <typename T, bool NARROW>
+struct FwdKinds {
+  using Apply = typename Kinds<T>::Apply;
+  using Update = typename Kinds<T>::Update;
+  using Dual = KDual16;
+};
+template <>
+struct FwdKinds<__bf16, true> {
+  using Apply = KApplyN16;
+  using Update = KApplyN16;
+  using Dual = KDualN16;
 };
 
 // Kinds of the second launch: the narrow shapes for 16-bit I/O with d <= 128.
@@ -952,13 +973,22 @@ __device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::
 // j, columns = tokens i): every lane holds four consecutive hidden units of
 // one token per register group, written as one packed store into the
 // token-major [tokens x h] output.
-template <typename T>
-__global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs args) {
-  using KA = typename Kinds<T>::Apply;
-  using KU = typename Kinds<T>::Update;
+template <typename T, bool NARROW>
+constexpr int fwd_smem() {
+  using FK = FwdKinds<T, NARROW>;
+  using KU = typename FK::Update;
+  return cmax(smem_bytes<T, typename FK::Apply>(),
+              cmax(smem_bytes<T, KU>(), sizeof(T) == 2 ? cmax(smem_bytes<T, typename FK::Dual>(),
+                                                              2 * KU::ROWS_A * KU::ROWS_B * 2)
+                                                       : 0));
+}
+
+template <typename T, bool NARROW>
+__device__ __forceinline__ void fwd_body(const FwdArgs& args, uint8_t* smem) {
+  using KA = typename FwdKinds<T, NARROW>::Apply;
+  using KU = typename FwdKinds<T, NARROW>::Update;
   static_assert(KA::THREADS == KU::THREADS, "one block size per launch");
-  __shared__ __attribute__((aligned(16)))
-  uint8_t smem[cmax(smem_bytes<T, KA>(), cmax(smem_bytes<T, KU>(), sizeof(T) == 2 ? smem_bytes<T, KDual16>() : 0))];
+  constexpr int kSmem = fwd_smem<T, NARROW>();
   constexpr int esz = sizeof(T);
   int bid = blockIdx.x;
   const bool first = bid < args.seg[0].nblocks;
@@ -982,7 +1012,7 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
     void* out = reinterpret_cast<uint8_t*>(sg.out0) + (inst * sg.out_inst) * esz;
     const int hrow0 = wave_m<KA>() * 32 * KA::MI + ((lane >> 5) << 2);
     if constexpr (sizeof(T) == 2) {
-      static_assert(KA::ROWS_A * KA::ROWS_B * 2 <= sizeof(smem), "staging fits");
+      static_assert(KA::ROWS_A * KA::ROWS_B * 2 <= kSmem, "staging fits");
 #pragma unroll
       for (int ni = 0; ni < KA::NI; ++ni)
 #pragma unroll
@@ -1031,7 +1061,7 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
     if constexpr (sizeof(T) == 2) {
       // Z1^T, Z3^T first, then D^T with the Z accumulators held: one
       // accumulator set per loop keeps the loops free of register spills.
-      using KD = KDual16;
+      using KD = typename FwdKinds<T, NARROW>::Dual;
       static_assert(KD::ROWS_A == KU::ROWS_A && KD::ROWS_B == KU::ROWS_B && KD::WM == KU::WM &&
                         KD::MI == KU::MI && KD::NI == KU::NI, "accumulator layouts match");
       Acc<KU> az;
@@ -1041,7 +1071,7 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
       constexpr int kSlot = KU::STAGE > KD::STAGE ? KU::STAGE : KD::STAGE;
       static_assert(2 * kSlot <= smem_bytes<T, KU>(), "chained ring fits");
       mainloop_chain<T, KU, KD, kSlot>(smem, opz, d, az, opd, d, ad);
-      static_assert(2 * KU::ROWS_A * KU::ROWS_B * 2 <= sizeof(smem), "staging fits");
+      static_assert(2 * KU::ROWS_A * KU::ROWS_B * 2 <= kSmem, "staging fits");
       update_epilogue_staged<KU>(az[0], az[1], ad[0], sg, inst, j0, i0, hrows, ntok, h, smem);
     } else {
       const View ops[5] = {w1, w3, w2, kk, vv};
@@ -1050,6 +1080,19 @@ __global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs 
       update_epilogue<T, KU>(acc[0], acc[1], acc[2], sg, inst, j0, i0, hrows, ntok, h);
     }
   }
+}
+
+template <typename T>
+__global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd(const FwdArgs args) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[fwd_smem<T, false>()];
+  fwd_body<T, false>(args, smem);
+}
+
+// d <= 128, 16-bit: two workgroups per CU (at most 256 VGPRs per wave).
+__global__ __launch_bounds__(KApplyN16::THREADS) __attribute__((amdgpu_waves_per_eu(2))) void k_fwd_narrow(
+    const FwdArgs args) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[fwd_smem<__bf16, true>()];
+  fwd_body<__bf16, true>(args, smem);
 }
 
 // The weight update of a GRAD_UPD tile from its accumulators P (= -g):
@@ -2076,7 +2119,8 @@ __global__ __launch_bounds__(256) void k_zero_rows(uint8_t* out, int64_t inst_by
 // ===========================================================================
 // Host-visible shapes and launchers
 
-TileShape fwd_tile(int kind, bool io_bf16) {
+TileShape fwd_tile(int kind, bool io_bf16, bool narrow) {
+  if (io_bf16 && narrow) return TileShape{KApplyN16::ROWS_A, KApplyN16::ROWS_B, KApplyN16::THREADS};
   if (io_bf16) return kind == FWD_APPLY ? TileShape{KApply16::ROWS_A, KApply16::ROWS_B, KApply16::THREADS}
                                         : TileShape{KApply16::ROWS_A, KApply16::ROWS_B, KApply16::THREADS};
   return kind == FWD_APPLY ? TileShape{KApply32::ROWS_A, KApply32::ROWS_B, KApply32::THREADS}
@@ -2164,7 +2208,8 @@ hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s) {
 
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;
-  if (io_bf16) k_fwd<__bf16><<<a.total_blocks, KApply16::THREADS, 0, s>>>(a);
+  if (io_bf16 && a.narrow) k_fwd_narrow<<<a.total_blocks, KApplyN16::THREADS, 0, s>>>(a);
+  else if (io_bf16) k_fwd<__bf16><<<a.total_blocks, KApply16::THREADS, 0, s>>>(a);
   else k_fwd<float><<<a.total_blocks, KApply32::THREADS, 0, s>>>(a);
   return hipGetLastError();
 }

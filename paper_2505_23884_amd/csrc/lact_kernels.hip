@@ -16,8 +16,9 @@
 //               same workgroup by the weight update of those rows, with or
 //               without momentum (no Muon, no split): the gradient never goes
 //               to memory
-// (the second launch also has narrow shapes of OUT, GRAD13 and GRAD2 for
-// d <= 128, so that the feature dimension fills the tile)
+// (for d <= 128 both launches have narrow shapes: OUT, GRAD13 and GRAD2 whose
+// feature dimension fills the tile, and k_fwd_narrow, whose 128 x 128 tiles
+// let two workgroups share a CU)
 //   NS_*        Newton-Schulz products (Muon, §3.2; App. A); k_ns_fused runs
 //               the whole iteration of a small matrix in one workgroup
 // plus the separate weight update with its row normalisation and momentum
@@ -32,7 +33,7 @@
 // go from HBM to LDS by raw-buffer DMA (buffer_load_dwordx4 ... lds) into a
 // ring of NSTAGE stages of BK K each. An operand is either K-contiguous in HBM
 // ("k": row-major [rows x K], kept as BK*2-byte rows in LDS, BK = 64 so that
-// every DMA fetches whole 128-byte lines) or row-contiguous ("mn": row-major
+// every DMA fetches whole 128-byte lines, except in k_fwd_narrow) or row-contiguous ("mn": row-major
 // [K x rows], the token-major layout; BK = 32 K rows in LDS, read with
 // ds_read_b64_tr_b16, which returns MFMA fragments of the transposed operand).
 // fp32 I/O runs on v_mfma_f32_32x32x2_f32 with a register-staged double

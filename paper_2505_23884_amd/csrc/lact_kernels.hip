@@ -177,12 +177,12 @@ LACT_KIND(KOutN16, 1, 1, 1, 0u, 2, 4, 2, 4, 2, true, 64, 0 * p, 0 * p);
 LACT_KIND(KGrad13N16, 2, 1, 2, 7u, 4, 2, 2, 2, 4, true, 32, p, 0 * p);
 LACT_KIND(KGrad2N16, 1, 1, 1, 3u, 2, 4, 2, 2, 4, true, 32, 0 * p, 0 * p);
 // First launch for d <= 128 (16-bit): 4 waves of 64 x 64 (128 hidden x 128
-// tokens) and 32-K stages, so that a workgroup takes 64 KiB of LDS (its
-// output staging) and two workgroups share a CU: with K = d this short, a
+// tokens) and three 32-K stages, so that a workgroup takes 72 KiB of LDS and
+// two workgroups share a CU: with K = d this short, a
 // tile's time is mostly the wait for its first stage and the epilogue, which
 // the other workgroup's loop overlaps.
-LACT_KIND(KApplyN16, 2, 1, 2, 0u, 2, 2, 2, 2, 2, true, 32, p, 0 * p);
-LACT_KIND(KDualN16, 1, 1, 1, 1u, 2, 2, 2, 2, 2, true, 32, 0 * p, 0 * p);
+LACT_KIND(KApplyN16, 2, 1, 2, 0u, 2, 2, 2, 2, 3, true, 32, p, 0 * p);
+LACT_KIND(KDualN16, 1, 1, 1, 1u, 2, 2, 2, 2, 3, true, 32, 0 * p, 0 * p);
 // fp32 shapes: 4 waves of 64 x 64 (128 x 128 tiles), register path; the key
 // forward and its hidden backward share one loop (A = W1, W3, W2; B = K, V).
 LACT_KIND(KApply32, 2, 1, 2, 0u, 2, 2, 2, 2, 2, false, 32, p, 0 * p);
@@ -773,12 +773,12 @@ __device__ __forceinline__ void mainloop(uint8_t* smem, const View (&ops)[K::NOP
   else mainloop_regs<K>(smem, ops, nk, acc);
 }
 
-// Two loops on one LDS ring of 2-stage slots of SLOT bytes: the first hands
+// Two loops on one LDS ring of NSTAGE slots of SLOT bytes: the first hands
 // its last free stage to the second (16-bit path).
 template <typename T, class K1, class K2, int SLOT>
 __device__ __forceinline__ void mainloop_chain(uint8_t* smem, const View (&ops1)[K1::NOPS], int64_t nk1, Acc<K1>& acc1,
                                                const View (&ops2)[K2::NOPS], int64_t nk2, Acc<K2>& acc2) {
-  static_assert(sizeof(T) == 2 && K1::NSTAGE == 2 && K2::NSTAGE == 2, "chained loops: 16-bit, two stages");
+  static_assert(sizeof(T) == 2 && K1::NSTAGE == K2::NSTAGE, "chained loops: 16-bit, one ring");
   zero_acc<K1>(acc1);
   zero_acc<K2>(acc2);
   ChainNext<K2, SLOT> nx(smem, ops2);
@@ -1070,7 +1070,7 @@ __device__ __forceinline__ void fwd_body(const FwdArgs& args, uint8_t* smem) {
       const View opz[3] = {w1, w3, kk};
       const View opd[2] = {w2, vv};
       constexpr int kSlot = KU::STAGE > KD::STAGE ? KU::STAGE : KD::STAGE;
-      static_assert(2 * kSlot <= smem_bytes<T, KU>(), "chained ring fits");
+      static_assert(KU::NSTAGE * kSlot <= kSmem, "chained ring fits");
       mainloop_chain<T, KU, KD, kSlot>(smem, opz, d, az, opd, d, ad);
       static_assert(2 * KU::ROWS_A * KU::ROWS_B * 2 <= kSmem, "staging fits");
       update_epilogue_staged<KU>(az[0], az[1], ad[0], sg, inst, j0, i0, hrows, ntok, h, smem);

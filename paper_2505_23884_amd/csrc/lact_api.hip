@@ -398,10 +398,13 @@ int newton_schulz(Ctx& c) {
   auto group_of = [&](int g) { return p.linear ? 1 : (g == 0 ? 2 : 1); };
   auto slot_of = [&](int g) { return p.linear ? 0 : (g == 0 ? 0 : 1); };
   if (p.ns_fp16 && m <= kNsFusedM && std::max(d, h) <= kNsFusedN) {
-    // small matrices: every step of one matrix in one workgroup
+    // small matrices: every step of one matrix in one workgroup, both
+    // groups (W1 and W3, W2) in one launch
     const int n = std::max(d, h);
+    NsFusedArgs fs[2]{};
+    double fl = 0.0;
     for (int g = 0; g < nseg; ++g) {
-      NsFusedArgs f{};
+      NsFusedArgs& f = fs[g];
       f.Y32 = pa.Y32;
       f.spi = p.nmat;
       f.Yb = c.ws + p.off_yb[0];
@@ -416,11 +419,11 @@ int newton_schulz(Ctx& c) {
       f.ca = kNsA;
       f.cb = kNsB;
       f.cc = kNsC;
-      const double fl = (double)f.steps * f.nblocks * (4.0 * m * m * n + 2.0 * m * m * m);
-      rc = timed(LACT_KCLASS_NS, fl, c.s, [&] { return launch_ns_fused(f, c.s); });
-      if (rc) return rc;
+      fl += (double)f.steps * f.nblocks * (4.0 * m * m * n + 2.0 * m * m * m);
     }
-    return LACT_OK;
+    return timed(LACT_KCLASS_NS, fl, c.s, [&] {
+      return nseg == 2 ? launch_ns_fused_pair(fs[0], fs[1], c.s) : launch_ns_fused(fs[0], c.s);
+    });
   }
   const int64_t mm = (int64_t)m * m;
   // Gram matrices larger than 128 (16-bit operands): the update product in

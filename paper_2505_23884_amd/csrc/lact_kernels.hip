@@ -19,8 +19,9 @@
 // (for d <= 128 both launches have narrow shapes: OUT, GRAD13 and GRAD2 whose
 // feature dimension fills the tile, and k_fwd_narrow, whose 128 x 128 tiles
 // let two workgroups share a CU)
-//   NS_*        Newton-Schulz products (Muon, §3.2; App. A); k_ns_fused runs
-//               the whole iteration of a small matrix in one workgroup
+//   NS_*        Newton-Schulz products (Muon, §3.2; App. A); k_ns_fused and
+//               k_ns_fused_pair run the whole iteration of a small matrix in
+//               one workgroup
 // plus the separate weight update with its row normalisation and momentum
 // (k_update, wherever the gradient and update kind does not apply),
 // the Newton-Schulz prologue (k_ns_prep, k_ns_scale), the momentum chunk
@@ -1847,17 +1848,19 @@ __device__ __forceinline__ void fs_put4(uint8_t* base, int row, int col, int pit
       h4{(_Float16)a, (_Float16)b, (_Float16)c, (_Float16)d};
 }
 
+// LDS of one fused Newton-Schulz workgroup: X (padded to 128 x 256 or
+// 256 x 128, fp16), A and B (128 x 128 fp16 each); the same for both
+// orientations.
+constexpr int kNsFusedX = kNsFusedM * kNsFusedN * 2, kNsFusedA = kNsFusedM * kNsFusedM * 2;
+
 template <bool TALL>
-__global__ __launch_bounds__(512) void k_ns_fused(const NsFusedArgs a) {
+__device__ __forceinline__ void ns_fused_body(const NsFusedArgs& a, int q, uint8_t* xs, uint8_t* as_, uint8_t* bs) {
   constexpr int M = kNsFusedM, N = kNsFusedN;
   constexpr int SR = TALL ? N : M, SC = TALL ? M : N;   // padded stored orientation
   constexpr int PX = SC * 2, PA = M * 2;                // LDS pitches (bytes)
-  __shared__ __attribute__((aligned(16))) uint8_t xs[SR * PX];
-  __shared__ __attribute__((aligned(16))) uint8_t as_[M * PA];
-  __shared__ __attribute__((aligned(16))) uint8_t bs[M * PA];
+  static_assert(SR * PX == kNsFusedX && M * PA == kNsFusedA, "LDS buffers");
   const uint32_t xb = lds_addr(xs), ab = lds_addr(as_), bb = lds_addr(bs);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, half = lane >> 5;
-  const int q = blockIdx.x;
   const int64_t slot = (int64_t)(q / a.group) * a.spi + a.slot_off[q % a.group];
   float* Y32 = a.Y32 + slot * a.ystride;
   const _Float16* Yb = reinterpret_cast<const _Float16*>(a.Yb) + slot * a.ystride;
@@ -2010,6 +2013,27 @@ __global__ __launch_bounds__(512) void k_ns_fused(const NsFusedArgs a) {
               make_float4(x32[mi][ni][4 * g], x32[mi][ni][4 * g + 1], x32[mi][ni][4 * g + 2], x32[mi][ni][4 * g + 3]);
       }
     }
+}
+
+template <bool TALL>
+__global__ __launch_bounds__(512) void k_ns_fused(const NsFusedArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t xs[kNsFusedX];
+  __shared__ __attribute__((aligned(16))) uint8_t as_[kNsFusedA];
+  __shared__ __attribute__((aligned(16))) uint8_t bs[kNsFusedA];
+  ns_fused_body<TALL>(a, blockIdx.x, xs, as_, bs);
+}
+
+// Both matrix groups of an instance set in one launch (W1 and W3, then W2, in
+// their own orientations): blocks below a0.nblocks take a0, the rest a1, so
+// that the matrices of both orientations fill the chip together.
+template <bool TALL0, bool TALL1>
+__global__ __launch_bounds__(512) void k_ns_fused_pair(const NsFusedArgs a0, const NsFusedArgs a1) {
+  __shared__ __attribute__((aligned(16))) uint8_t xs[kNsFusedX];
+  __shared__ __attribute__((aligned(16))) uint8_t as_[kNsFusedA];
+  __shared__ __attribute__((aligned(16))) uint8_t bs[kNsFusedA];
+  const int q = blockIdx.x;
+  if (q < a0.nblocks) ns_fused_body<TALL0>(a0, q, xs, as_, bs);
+  else ns_fused_body<TALL1>(a1, q - a0.nblocks, xs, as_, bs);
 }
 
 __device__ __forceinline__ float block_sum(float v, float* red) {
@@ -2172,6 +2196,16 @@ hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s) {
   if (a.nblocks <= 0 || a.steps <= 0) return hipSuccess;
   if (a.rows > a.cols) k_ns_fused<true><<<a.nblocks, 512, 0, s>>>(a);
   else k_ns_fused<false><<<a.nblocks, 512, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ns_fused_pair(const NsFusedArgs& a0, const NsFusedArgs& a1, hipStream_t s) {
+  if (a0.steps <= 0 || a0.nblocks + a1.nblocks <= 0) return hipSuccess;
+  const int64_t blocks = (int64_t)a0.nblocks + a1.nblocks;
+  // the two groups are transposes of each other's shape: at most one is tall
+  if (a0.rows > a0.cols) k_ns_fused_pair<true, false><<<(unsigned)blocks, 512, 0, s>>>(a0, a1);
+  else if (a1.rows > a1.cols) k_ns_fused_pair<false, true><<<(unsigned)blocks, 512, 0, s>>>(a0, a1);
+  else k_ns_fused_pair<false, false><<<(unsigned)blocks, 512, 0, s>>>(a0, a1);
   return hipGetLastError();
 }
 

@@ -177,9 +177,11 @@ Plan make_plan(const lact_desc* dsc) {
   // Without split the sums of squares that Newton-Schulz normalises by come
   // from the gradient tiles' epilogues (one entry per tile), and the scaling
   // reads the gradient directly: no separate pass over it (momentum keeps the
-  // pass, which also advances the state).
-  p.tile_sums = p.muon && p.nsplit == 1 && p.t13 <= p.ns_bps && p.t2 <= p.ns_bps;
+  // pass, which also advances the state). Small matrices (one fused
+  // Newton-Schulz workgroup each) take their norm in that workgroup instead.
   p.ns_fp16 = p.bf16;
+  const bool ns_small = p.ns_fp16 && p.m <= kNsFusedM && std::max(p.d, p.h) <= kNsFusedN;
+  p.tile_sums = p.muon && p.nsplit == 1 && p.t13 <= p.ns_bps && p.t2 <= p.ns_bps && !ns_small;
   p.ns_esz = p.ns_fp16 ? 2 : 4;
   if (p.muon) {
     const size_t slots = (size_t)p.BH * p.nmat, mm = (size_t)p.m * p.m;
@@ -378,26 +380,31 @@ int newton_schulz(Ctx& c) {
     pa.bbar_stride = kBetaBatch;
   }
   int rc = LACT_OK;
-  if (p.tile_sums && !c.beta) {
+  const int m = p.m, d = p.d, h = p.h;
+  // small matrices: the fused kernel normalises the gradient itself (after
+  // the momentum step of k_ns_prep, if any)
+  const bool fused = p.ns_fp16 && m <= kNsFusedM && std::max(d, h) <= kNsFusedN;
+  if (p.tile_sums && !c.beta && !fused) {
     pa.src = reinterpret_cast<const float*>(c.ws + p.off_step);
     pa.sum_n[0] = p.linear ? p.t2 : p.t13;
     pa.sum_n[1] = p.t2;
     pa.sum_n[2] = p.t13;
-  } else {
+  } else if (!fused || c.beta) {
     rc = timed(LACT_KCLASS_NS, 0.0, c.s, [&] { return launch_ns_prep(pa, c.s); });
     if (rc) return rc;
   }
-  rc = timed(LACT_KCLASS_NS, 0.0, c.s,
-             [&] { return launch_ns_scale(pa, c.ws + p.off_yb[0], p.ns_fp16, 1e-7f, c.s); });
-  if (rc) return rc;
-  const int m = p.m, d = p.d, h = p.h;
+  if (!fused) {
+    rc = timed(LACT_KCLASS_NS, 0.0, c.s,
+               [&] { return launch_ns_scale(pa, c.ws + p.off_yb[0], p.ns_fp16, 1e-7f, c.s); });
+    if (rc) return rc;
+  }
   // segment 0: W1 and W3 stored h x d; segment 1: W2 stored d x h
   // (linear: one segment, the d x d matrix)
   const int rows[2] = {h, d}, cols[2] = {d, h};
   const int nseg = p.linear ? 1 : 2;
   auto group_of = [&](int g) { return p.linear ? 1 : (g == 0 ? 2 : 1); };
   auto slot_of = [&](int g) { return p.linear ? 0 : (g == 0 ? 0 : 1); };
-  if (p.ns_fp16 && m <= kNsFusedM && std::max(d, h) <= kNsFusedN) {
+  if (fused) {
     // small matrices: every step of one matrix in one workgroup, both
     // groups (W1 and W3, W2) in one launch
     const int n = std::max(d, h);
@@ -419,6 +426,12 @@ int newton_schulz(Ctx& c) {
       f.ca = kNsA;
       f.cb = kNsB;
       f.cc = kNsC;
+      // the summed gradient: the split partials, or the momentum state's
+      // iterate that k_ns_prep left in Y32
+      f.src = c.beta ? pa.Y32 : pa.part;
+      f.nsplit = c.beta ? 1 : p.nsplit;
+      f.part_split = pa.part_split;
+      f.eps = 1e-7f;
       fl += (double)f.steps * f.nblocks * (4.0 * m * m * n + 2.0 * m * m * m);
     }
     return timed(LACT_KCLASS_NS, fl, c.s, [&] {

@@ -213,6 +213,13 @@ struct NsFusedArgs {
   int nblocks;          // instances * group
   int steps;
   float ca, cb, cc;     // quintic coefficients
+  // With src, the workgroup first forms X0 = G / (||G||_F + eps) itself, G the
+  // sum of nsplit fp32 partials part_split elements apart (same slot layout);
+  // without, Y32 and Yb already hold X0.
+  const float* src;
+  int nsplit;
+  int64_t part_split;
+  float eps;
 };
 
 // ---- the layer's prologue and output norm (lact_io.hip) ---------------------

@@ -1869,15 +1869,19 @@ __device__ __forceinline__ void ns_fused_body(const NsFusedArgs& a, int q, uint8
   // X (fp16) into LDS, zero padded
   for (int i = tid; i < SR * PX / 16; i += 512) *reinterpret_cast<u32x4_t*>(xs + i * 16) = u32x4_t{0u, 0u, 0u, 0u};
   __syncthreads();
-  for (int i = tid; i < sr * (sc / 8); i += 512) {
-    const int row = i / (sc / 8), ch = i % (sc / 8);
-    *reinterpret_cast<u32x4_t*>(xs + fs_off(row, ch, PX)) =
-        *reinterpret_cast<const u32x4_t*>(Yb + (int64_t)row * sc + ch * 8);
-  }
+  if (!a.src)
+    for (int i = tid; i < sr * (sc / 8); i += 512) {
+      const int row = i / (sc / 8), ch = i % (sc / 8);
+      *reinterpret_cast<u32x4_t*>(xs + fs_off(row, ch, PX)) =
+          *reinterpret_cast<const u32x4_t*>(Yb + (int64_t)row * sc + ch * 8);
+    }
   // X (fp32) into registers, in the tile layout of the update product: tile
-  // rows = stored columns (TR rows), tile columns = stored rows (TC)
+  // rows = stored columns (TR rows), tile columns = stored rows (TC); with
+  // src, the summed gradient
   constexpr int WM3 = TALL ? 2 : 4, WN3 = TALL ? 4 : 2;   // waves: 64 x 64 each
   const int r3 = (w / WN3) * 64, c3 = (w % WN3) * 64;
+  const float* xin = a.src ? a.src + slot * a.ystride : Y32;
+  const int nin = a.src ? a.nsplit : 1;
   f32x16_t x32[2][2];
 #pragma unroll
   for (int mi = 0; mi < 2; ++mi)
@@ -1888,13 +1892,52 @@ __device__ __forceinline__ void ns_fused_body(const NsFusedArgs& a, int q, uint8
       for (int g = 0; g < 4; ++g) {
         const int r = r3 + mi * 32 + 8 * g + 4 * half;
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (c < sr && r < sc) v = *reinterpret_cast<const float4*>(Y32 + (int64_t)c * sc + r);
+        if (c < sr && r < sc)
+          for (int sp = 0; sp < nin; ++sp) {
+            const float4 p = *reinterpret_cast<const float4*>(xin + sp * a.part_split + (int64_t)c * sc + r);
+            v = make_float4(v.x + p.x, v.y + p.y, v.z + p.z, v.w + p.w);
+          }
         x32[mi][ni][4 * g] = v.x;
         x32[mi][ni][4 * g + 1] = v.y;
         x32[mi][ni][4 * g + 2] = v.z;
         x32[mi][ni][4 * g + 3] = v.w;
       }
     }
+  if (a.src) {
+    // X0 = G / (||G||_F + eps): the whole matrix is in this workgroup's
+    // registers (padding is zero); the partial sums go through the start of
+    // the Gram buffer, which the first step overwrites only after a barrier
+    float ss = 0.f;
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) ss = fmaf(x32[mi][ni][e], x32[mi][ni][e], ss);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+    float* red = reinterpret_cast<float*>(as_);
+    if (lane == 0) red[w] = ss;
+    __syncthreads();
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t += red[i];
+    const float inv = 1.0f / (sqrtf(t) + a.eps);
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni) {
+        const int c = c3 + ni * 32 + (lane & 31);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int r = r3 + mi * 32 + 8 * g + 4 * half;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) x32[mi][ni][4 * g + e] *= inv;
+          fs_put4(xs, c, r, PX, x32[mi][ni][4 * g], x32[mi][ni][4 * g + 1], x32[mi][ni][4 * g + 2],
+                  x32[mi][ni][4 * g + 3]);
+        }
+      }
+  }
   __syncthreads();
 
   // Gram tile layout: waves 2 x 4 of 64 x 32
@@ -2193,14 +2236,14 @@ hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s) {
 }
 
 hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s) {
-  if (a.nblocks <= 0 || a.steps <= 0) return hipSuccess;
+  if (a.nblocks <= 0 || (a.steps <= 0 && !a.src)) return hipSuccess;
   if (a.rows > a.cols) k_ns_fused<true><<<a.nblocks, 512, 0, s>>>(a);
   else k_ns_fused<false><<<a.nblocks, 512, 0, s>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_ns_fused_pair(const NsFusedArgs& a0, const NsFusedArgs& a1, hipStream_t s) {
-  if (a0.steps <= 0 || a0.nblocks + a1.nblocks <= 0) return hipSuccess;
+  if ((a0.steps <= 0 && !a0.src) || a0.nblocks + a1.nblocks <= 0) return hipSuccess;
   const int64_t blocks = (int64_t)a0.nblocks + a1.nblocks;
   // the two groups are transposes of each other's shape: at most one is tall
   if (a0.rows > a0.cols) k_ns_fused_pair<true, false><<<(unsigned)blocks, 512, 0, s>>>(a0, a1);

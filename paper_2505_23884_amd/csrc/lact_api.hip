@@ -432,11 +432,19 @@ int newton_schulz(Ctx& c) {
       f.nsplit = c.beta ? 1 : p.nsplit;
       f.part_split = pa.part_split;
       f.eps = 1e-7f;
+      // and the weight update (no separate update launch follows)
+      for (int j = 0; j < p.nmat; ++j) {
+        f.W[j] = c.W[j];
+        f.Wb[j] = c.wb[c.wset][j];
+      }
       fl += (double)f.steps * f.nblocks * (4.0 * m * m * n + 2.0 * m * m * m);
     }
-    return timed(LACT_KCLASS_NS, fl, c.s, [&] {
+    rc = timed(LACT_KCLASS_NS, fl, c.s, [&] {
       return nseg == 2 ? launch_ns_fused_pair(fs[0], fs[1], c.s) : launch_ns_fused(fs[0], c.s);
     });
+    if (rc) return rc;
+    c.ns_updated = true;
+    return LACT_OK;
   }
   const int64_t mm = (int64_t)m * m;
   // Gram matrices larger than 128 (16-bit operands): the update product in

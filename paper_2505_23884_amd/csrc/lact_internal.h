@@ -220,6 +220,12 @@ struct NsFusedArgs {
   int nsplit;
   int64_t part_split;
   float eps;
+  // With W[0]: after the last step the workgroup applies the weight update to
+  // its matrix (U = W + X, W <- U ||W_row|| / ||U_row||, and the bf16 copy in
+  // Wb) instead of storing X to Y32. W, Wb: the fast weights, instance stride
+  // ystride (the slot layout without the matrix index).
+  float* W[3];
+  void* Wb[3];
 };
 
 // ---- the layer's prologue and output norm (lact_io.hip) ---------------------

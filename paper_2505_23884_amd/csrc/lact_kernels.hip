@@ -2043,6 +2043,75 @@ __device__ __forceinline__ void ns_fused_body(const NsFusedArgs& a, int q, uint8
       }
     lds_barrier();
   }
+  if (a.W[0]) {
+    // The weight update of this matrix with X as the step (§3.2 weight
+    // normalisation; Muon's update, App. A): a lane holds 32 columns of stored
+    // rows c (ni = 0, 1); row sums over the lane, its partner half (lane ^ 32)
+    // and the WM3 wave rows (through LDS, free after the last step's barrier)
+    const int j = a.slot_off[q % a.group];
+    const int64_t woff = (int64_t)(q / a.group) * a.ystride;
+    float* Wj = a.W[j] + woff;
+    __bf16* Wbj = reinterpret_cast<__bf16*>(a.Wb[j]) + woff;
+    float sw[2] = {0.f, 0.f}, su[2] = {0.f, 0.f};
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      const int c = c3 + ni * 32 + (lane & 31);
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int r = r3 + mi * 32 + 8 * g + 4 * half;
+          float4 wv = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (c < sr && r < sc) wv = *reinterpret_cast<const float4*>(Wj + (int64_t)c * sc + r);
+          const float wa[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float u = wa[e] + x32[mi][ni][4 * g + e];
+            x32[mi][ni][4 * g + e] = u;
+            sw[ni] = fmaf(wa[e], wa[e], sw[ni]);
+            su[ni] = fmaf(u, u, su[ni]);
+          }
+        }
+      sw[ni] += __shfl_xor(sw[ni], 32, 64);
+      su[ni] += __shfl_xor(su[ni], 32, 64);
+    }
+    float* red = reinterpret_cast<float*>(as_);   // [WM3][SR][2]
+    const int wr = w / WN3;
+    if (half == 0)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni) {
+        const int c = c3 + ni * 32 + (lane & 31);
+        red[(wr * SR + c) * 2] = sw[ni];
+        red[(wr * SR + c) * 2 + 1] = su[ni];
+      }
+    __syncthreads();
+    typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_t;
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      const int c = c3 + ni * 32 + (lane & 31);
+      float tw = 0.f, tu = 0.f;
+#pragma unroll
+      for (int k = 0; k < WM3; ++k) {
+        tw += red[(k * SR + c) * 2];
+        tu += red[(k * SR + c) * 2 + 1];
+      }
+      const float f = sqrtf(tw) / sqrtf(tu);
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int r = r3 + mi * 32 + 8 * g + 4 * half;
+          if (c < sr && r < sc) {
+            const float4 x = make_float4(x32[mi][ni][4 * g] * f, x32[mi][ni][4 * g + 1] * f,
+                                         x32[mi][ni][4 * g + 2] * f, x32[mi][ni][4 * g + 3] * f);
+            *reinterpret_cast<float4*>(Wj + (int64_t)c * sc + r) = x;
+            *reinterpret_cast<bf16x4_t*>(Wbj + (int64_t)c * sc + r) =
+                bf16x4_t{(__bf16)x.x, (__bf16)x.y, (__bf16)x.z, (__bf16)x.w};
+          }
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int mi = 0; mi < 2; ++mi)
 #pragma unroll

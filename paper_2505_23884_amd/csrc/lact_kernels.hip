@@ -23,7 +23,8 @@
 //               k_ns_fused_pair run the whole iteration of a small matrix in
 //               one workgroup
 // plus the separate weight update with its row normalisation and momentum
-// (k_update, wherever the gradient and update kind does not apply),
+// (k_update, wherever neither the gradient and update kind, k_ns_final nor
+// the fused small-matrix Newton-Schulz applies it),
 // the Newton-Schulz prologue (k_ns_prep, k_ns_scale), the momentum chunk
 // means (k_beta_mean), operand copies (k_prep), eta k (k_scale_rows) and the
 // zeroing of uncovered output rows (k_zero_rows).

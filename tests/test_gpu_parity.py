@@ -569,6 +569,17 @@ def test_muon_gram_triangle_three_tiles_wide_and_tall():
     teacher_forced(cfg, x, [0, 1])
 
 
+def test_muon_small_wide_then_tall_in_one_launch():
+    # d > h: W1, W3 (128 x 256) iterate wide and W2 (256 x 128) tall, the
+    # reverse of the video shape, in one fused launch that also normalises the
+    # gradient and applies the update
+    cfg = CONFIGS["video"].with_(name="muon_small_rev", B=1, H=2, d=256, h=128, n_kv=512, n_q=512,
+                                 chunk=256)
+    x = make_inputs(cfg, 16)
+    _, n_upd = update_launches(lambda: teacher_forced(cfg, x, [0, 1]))
+    assert n_upd == 0
+
+
 def test_muon_small_gram_long_side_unfused():
     # Gram size 96 <= 128 but the long side 384 > 256: the per-product
     # Newton-Schulz launches with 128 x 128 tiles (not the one-workgroup kernel)

@@ -412,9 +412,7 @@ int newton_schulz(Ctx& c) {
     double fl = 0.0;
     for (int g = 0; g < nseg; ++g) {
       NsFusedArgs& f = fs[g];
-      f.Y32 = pa.Y32;
       f.spi = p.nmat;
-      f.Yb = c.ws + p.off_yb[0];
       f.ystride = dh;
       f.group = group_of(g);
       f.slot_off[0] = slot_of(g);

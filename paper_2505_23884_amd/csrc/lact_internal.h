@@ -203,9 +203,15 @@ constexpr int kNsFusedM = 128, kNsFusedN = 256;
 // X <- a X + b (X X^T) X + c (X X^T)^2 X
 constexpr float kNsA = 3.4445f, kNsB = -4.7750f, kNsC = 2.0315f;
 struct NsFusedArgs {
-  float* Y32;           // fp32 iterate, slot stride ystride: in = scaled gradient, out = NS result
+  // X0 = G / (||G||_F + eps), G the sum of nsplit fp32 partials part_split
+  // elements apart (slot stride ystride); steps quintic iterations; then the
+  // weight update U = W + X, W <- U ||W_row|| / ||U_row|| with the bf16 copy
+  // (W, Wb: the fast weights, instance stride ystride)
+  const float* src;
+  int nsplit;
+  int64_t part_split;
+  float eps;
   int spi;              // slots per instance
-  const void* Yb;       // fp16 copy of the scaled gradient, same layout
   int64_t ystride;
   int group;            // matrices per instance in this launch (1 or 2)
   int slot_off[2];      // j of each matrix of the group
@@ -213,17 +219,6 @@ struct NsFusedArgs {
   int nblocks;          // instances * group
   int steps;
   float ca, cb, cc;     // quintic coefficients
-  // With src, the workgroup first forms X0 = G / (||G||_F + eps) itself, G the
-  // sum of nsplit fp32 partials part_split elements apart (same slot layout);
-  // without, Y32 and Yb already hold X0.
-  const float* src;
-  int nsplit;
-  int64_t part_split;
-  float eps;
-  // With W[0]: after the last step the workgroup applies the weight update to
-  // its matrix (U = W + X, W <- U ||W_row|| / ||U_row||, and the bf16 copy in
-  // Wb) instead of storing X to Y32. W, Wb: the fast weights, instance stride
-  // ystride (the slot layout without the matrix index).
   float* W[3];
   void* Wb[3];
 };

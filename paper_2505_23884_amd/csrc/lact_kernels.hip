@@ -1789,8 +1789,10 @@ __global__ __launch_bounds__((NsKinds<T, BIG>::K::THREADS)) void k_ns(const NsAr
 
 // ---------------------------------------------------------------------------
 // Whole Newton-Schulz iteration of one small matrix per workgroup (Gram size
-// m <= 128, long side n <= 256): the fp16 iterate X, Gram A and polynomial B
-// stay in LDS (64 + 32 + 32 KiB), the fp32 iterate in registers. Per step:
+// m <= 128, long side n <= 256), from the summed gradient to the updated
+// weights: X0 = G / (||G||_F + eps) is formed in registers, the fp16 iterate
+// X, Gram A and polynomial B stay in LDS (64 + 32 + 32 KiB), the fp32 iterate
+// in registers, and the weight update takes the result as its step. Per step:
 //   A = X X^T   (kept in fp32 registers, fp16 copy to LDS)
 //   B = b A + c A A
 //   X <- a X + B X
@@ -1863,26 +1865,17 @@ __device__ __forceinline__ void ns_fused_body(const NsFusedArgs& a, int q, uint8
   const uint32_t xb = lds_addr(xs), ab = lds_addr(as_), bb = lds_addr(bs);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, half = lane >> 5;
   const int64_t slot = (int64_t)(q / a.group) * a.spi + a.slot_off[q % a.group];
-  float* Y32 = a.Y32 + slot * a.ystride;
-  const _Float16* Yb = reinterpret_cast<const _Float16*>(a.Yb) + slot * a.ystride;
   const int sr = a.rows, sc = a.cols;                   // valid stored rows, columns
 
-  // X (fp16) into LDS, zero padded
+  // LDS copy of X zero padded (written below)
   for (int i = tid; i < SR * PX / 16; i += 512) *reinterpret_cast<u32x4_t*>(xs + i * 16) = u32x4_t{0u, 0u, 0u, 0u};
   __syncthreads();
-  if (!a.src)
-    for (int i = tid; i < sr * (sc / 8); i += 512) {
-      const int row = i / (sc / 8), ch = i % (sc / 8);
-      *reinterpret_cast<u32x4_t*>(xs + fs_off(row, ch, PX)) =
-          *reinterpret_cast<const u32x4_t*>(Yb + (int64_t)row * sc + ch * 8);
-    }
-  // X (fp32) into registers, in the tile layout of the update product: tile
-  // rows = stored columns (TR rows), tile columns = stored rows (TC); with
-  // src, the summed gradient
+  // The summed gradient into registers, in the tile layout of the update
+  // product: tile rows = stored columns (TR rows), tile columns = stored rows (TC)
   constexpr int WM3 = TALL ? 2 : 4, WN3 = TALL ? 4 : 2;   // waves: 64 x 64 each
   const int r3 = (w / WN3) * 64, c3 = (w % WN3) * 64;
-  const float* xin = a.src ? a.src + slot * a.ystride : Y32;
-  const int nin = a.src ? a.nsplit : 1;
+  const float* xin = a.src + slot * a.ystride;
+  const int nin = a.nsplit;
   f32x16_t x32[2][2];
 #pragma unroll
   for (int mi = 0; mi < 2; ++mi)
@@ -1904,7 +1897,7 @@ __device__ __forceinline__ void ns_fused_body(const NsFusedArgs& a, int q, uint8
         x32[mi][ni][4 * g + 3] = v.w;
       }
     }
-  if (a.src) {
+  {
     // X0 = G / (||G||_F + eps): the whole matrix is in this workgroup's
     // registers (padding is zero); the partial sums go through the start of
     // the Gram buffer, which the first step overwrites only after a barrier
@@ -2044,7 +2037,7 @@ __device__ __forceinline__ void ns_fused_body(const NsFusedArgs& a, int q, uint8
       }
     lds_barrier();
   }
-  if (a.W[0]) {
+  {
     // The weight update of this matrix with X as the step (§3.2 weight
     // normalisation; Muon's update, App. A): a lane holds 32 columns of stored
     // rows c (ni = 0, 1); row sums over the lane, its partner half (lane ^ 32)
@@ -2111,21 +2104,7 @@ __device__ __forceinline__ void ns_fused_body(const NsFusedArgs& a, int q, uint8
           }
         }
     }
-    return;
   }
-#pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      const int c = c3 + ni * 32 + (lane & 31);
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int r = r3 + mi * 32 + 8 * g + 4 * half;
-        if (c < sr && r < sc)
-          *reinterpret_cast<float4*>(Y32 + (int64_t)c * sc + r) =
-              make_float4(x32[mi][ni][4 * g], x32[mi][ni][4 * g + 1], x32[mi][ni][4 * g + 2], x32[mi][ni][4 * g + 3]);
-      }
-    }
 }
 
 template <bool TALL>
@@ -2306,14 +2285,14 @@ hipError_t launch_ns(const NsArgs& a, bool fp16, bool big, hipStream_t s) {
 }
 
 hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s) {
-  if (a.nblocks <= 0 || (a.steps <= 0 && !a.src)) return hipSuccess;
+  if (a.nblocks <= 0) return hipSuccess;
   if (a.rows > a.cols) k_ns_fused<true><<<a.nblocks, 512, 0, s>>>(a);
   else k_ns_fused<false><<<a.nblocks, 512, 0, s>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_ns_fused_pair(const NsFusedArgs& a0, const NsFusedArgs& a1, hipStream_t s) {
-  if ((a0.steps <= 0 && !a0.src) || a0.nblocks + a1.nblocks <= 0) return hipSuccess;
+  if (a0.nblocks + a1.nblocks <= 0) return hipSuccess;
   const int64_t blocks = (int64_t)a0.nblocks + a1.nblocks;
   // the two groups are transposes of each other's shape: at most one is tall
   if (a0.rows > a0.cols) k_ns_fused_pair<true, false><<<(unsigned)blocks, 512, 0, s>>>(a0, a1);

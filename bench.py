@@ -57,6 +57,10 @@ def parse():
                     help="time the step replayed from a HIP graph captured once (host launch cost removed)")
     ap.add_argument("--library-gemms", action="store_true",
                     help="time the path's plain contractions as library GEMMs (torch.matmul), for context")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the 1M-token NVS workload measured after the default one")
+    ap.add_argument("--device-inputs", action="store_true",
+                    help="draw the inputs on the device (plain uniform-chunk workloads)")
     ap.add_argument("--traffic-report", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"))
     return ap.parse_args()
 
@@ -264,14 +268,32 @@ def describe(cfg):
             f"chunk={cfg.chunk} {order}{muon}{mom}{lr3}, io {cfg.io}, fp32 state")
 
 
-def cpu_baseline(cfg, min_seconds):
+def cpu_model():
+    """The host CPU's model name and the CPUs this process may run on."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        ncpu = len(os.sched_getaffinity(0))
+    except AttributeError:
+        ncpu = os.cpu_count() or 1
+    return name, ncpu
+
+
+def _oracle_sample(cfg, min_seconds):
     """The fp64 oracle, as it is, on a bounded sample of the same workload:
     whole (b, h) instances (every chunk), one after another, until at least
-    `min_seconds` of host time have passed; timed on this host's cores. When
-    one instance is too large for that budget (NVS: 1M tokens in one chunk is
-    ~22 TFLOP), the sample is the first tokens of one instance with the same
-    d, h, order and options, chunked at the same size up to the sample length."""
-    from threadpoolctl import threadpool_info
+    `min_seconds` of host time have passed. When one instance is too large for
+    that budget (NVS: 1M tokens in one chunk is ~22 TFLOP), the sample is the
+    first tokens of one instance with the same d, h, order and options,
+    chunked at the same size up to the sample length.
+    Returns (FLOPs done, seconds, sample description, tokens done)."""
     from lact_synth import make_inputs
     from oracle import lact_oracle as O
 
@@ -304,50 +326,101 @@ def cpu_baseline(cfg, min_seconds):
                            order=scfg.order, use_muon=bool(scfg.use_muon), ns_steps=scfg.ns_steps)
         dt += time.perf_counter() - t0
         done += 1
-    fl = done * workload_flops(scfg, BH=1)
+    desc = (f"{done} of {scfg.BH} (b,h) instances, all {scfg.n_chunks} chunks each ({done * scfg.n_q} tokens), "
+            f"fp64 NumPy, {dt:.1f} s{note}")
+    return done * workload_flops(scfg, BH=1), dt, desc, done * scfg.n_q
+
+
+def cpu_baseline(cfg, min_seconds):
+    """The oracle timed on this host: once with every core the BLAS library
+    uses by default, once limited to one thread (a smaller time budget)."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    fl, dt, desc, toks = _oracle_sample(cfg, min_seconds)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    with threadpool_limits(limits=1):
+        fl1, dt1, desc1, toks1 = _oracle_sample(cfg, min_seconds / 2)
+    model, ncpu = cpu_model()
     return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of {scfg.BH} (b,h) instances, all {scfg.n_chunks} chunks each "
-                      f"({done * scfg.n_q} tokens), fp64 NumPy, {dt:.1f} s{note}",
-            "tokens_per_s": round(done * scfg.n_q / dt, 1)}
+            "sample": desc, "tokens_per_s": round(toks / dt, 1), "cpu_model": model, "host_cpus": ncpu,
+            "one_core": {"value": round(fl1 / dt1 / 1e12, 5), "unit": "TFLOP/s", "cores": 1, "sample": desc1,
+                         "tokens_per_s": round(toks1 / dt1, 1)}}
 
 
-def main():
-    args = parse()
-    if args.traffic_report:
-        traffic_report(args.config, *args.traffic_report)
-        return
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
-                          "n_gpus": args.gpus}))
-        sys.exit(2)
-    if args.copy_calibration:
-        copy_calibration()
-        return
+def device_inputs(cfg, dev, seed=0):
+    """Inputs of the recipe's distributions drawn on the device (a seeded torch
+    generator): q, k, v ~ N(0, 1) with unit rows, eta = 0.01 softplus(N(0, 1)),
+    W with N(0, 1/d) entries and unit rows. For workloads whose host draw
+    would cost tens of seconds and several GB of host memory (1M tokens)."""
     import torch
-
-    import paper_2505_23884_amd as P
-    from lact_synth import CONFIGS, make_inputs
-
-    cfg = CONFIGS[args.config]
-    if args.chunk:
-        if cfg.schedule or cfg.layer_io:
-            raise SystemExit("--chunk applies to the uniform-chunk workloads")
-        cfg = cfg.with_(name=f"{cfg.name}_c{args.chunk}", chunk=args.chunk)
-    if args.library_gemms:
-        library_gemms(cfg, max(args.steps, 5))
-        return
-    dev = torch.device("cuda:0")
-    x = make_inputs(cfg, 0)
+    gen = torch.Generator(device=dev).manual_seed(seed)
     io = torch.bfloat16 if cfg.io == "bf16" else torch.float32
-    sh = lambda a: a.reshape(cfg.B, cfg.H, *a.shape[1:])
-    q, k, v = (torch.from_numpy(sh(x[n])).to(dev, io) for n in ("q", "k", "v"))
-    eta = torch.from_numpy(sh(x["eta"])).to(dev, torch.float32)
-    W = [torch.from_numpy(sh(x[n])).to(dev, torch.float32) for n in ("W1", "W2", "W3")]
+
+    def tok(n):
+        x = torch.randn(cfg.B, cfg.H, n, cfg.d, generator=gen, device=dev)
+        return (x / x.norm(dim=-1, keepdim=True)).to(io)
+
+    def unit_rows(r, c):
+        w = torch.randn(cfg.H, r, c, generator=gen, device=dev) / cfg.d ** 0.5
+        w = w / w.norm(dim=-1, keepdim=True)
+        return w.unsqueeze(0).expand(cfg.B, -1, -1, -1).contiguous()
+
+    q, k, v = tok(cfg.n_q), tok(cfg.n_kv), tok(cfg.n_kv)
+    eta = 0.01 * torch.nn.functional.softplus(torch.randn(cfg.B, cfg.H, cfg.n_kv, generator=gen, device=dev))
+    return q, k, v, eta, [unit_rows(cfg.h, cfg.d), unit_rows(cfg.d, cfg.h), unit_rows(cfg.h, cfg.d)]
+
+
+def kernel_alg_bytes(cfg, kernel, launches_per_step):
+    """Algorithmic bytes per launch of the first (k_fwd) or second (k_bwd)
+    launch class: the path's inputs each reads and the outputs each writes,
+    at their own widths, with the materialised intermediates left out.
+    k_fwd reads q, k, v and eta once per step and the 16-bit weight copies
+    once per launch (3 d h for an update, 2 d h for an apply-only launch);
+    k_bwd reads k and v once and a weight copy once per launch, writes o once,
+    and, where it applies the weight update itself (256 < d, h <= 512 without
+    Muon), reads and writes the fp32 state and writes its copy per chunk.
+    None for other kernels and layouts."""
+    if cfg.schedule or cfg.linear or cfg.io != "bf16" or not launches_per_step:
+        return None
+    esz, dh, C = 2, cfg.d * cfg.h, cfg.chunk
+    nch = cfg.n_chunks
+    if kernel == "k_fwd":
+        upd = nch
+        applies = launches_per_step - upd
+        b = esz * cfg.d * (2 * cfg.n_kv + cfg.n_q) + 4 * cfg.n_kv + (3 * upd + 2 * applies) * dh * esz
+    elif kernel == "k_bwd":
+        fused = not cfg.use_muon and 256 < cfg.d <= 512 and 256 < cfg.h <= 512
+        b = esz * cfg.d * (2 * cfg.n_kv + cfg.n_q) + launches_per_step * dh * esz
+        if fused:
+            b += nch * 3 * dh * (4 + 4 + 2)
+    else:
+        return None
+    return cfg.BH * b / launches_per_step
+
+
+def measure(cfg, args, P, on_device=False):
+    """One workload: inputs resident in HBM, warmup, the timed steps, then the
+    per-launch timing pass (HIP events on the launch stream) for the roofline."""
+    import torch
+    from lact_synth import make_inputs
+
+    dev = torch.device("cuda:0")
+    io = torch.bfloat16 if cfg.io == "bf16" else torch.float32
+    if on_device:
+        q, k, v, eta, W = device_inputs(cfg, dev)
+        if cfg.momentum or cfg.schedule or cfg.linear or cfg.layer_io or cfg.lr3:
+            raise SystemExit("device-drawn inputs cover the plain uniform-chunk workloads")
+    else:
+        x = make_inputs(cfg, 0)
+        sh = lambda a: a.reshape(cfg.B, cfg.H, *a.shape[1:])
+        q, k, v = (torch.from_numpy(sh(x[n])).to(dev, io) for n in ("q", "k", "v"))
+        eta = torch.from_numpy(sh(x["eta"])).to(dev, torch.float32)
+        W = [torch.from_numpy(sh(x[n])).to(dev, torch.float32) for n in ("W1", "W2", "W3")]
+        if cfg.momentum:
+            beta = torch.from_numpy(sh(x["beta"])).to(dev, torch.float32)
+        del x
     if cfg.momentum:
-        beta = torch.from_numpy(sh(x["beta"])).to(dev, torch.float32)
         M = [torch.zeros_like(w) for w in W]
-    del x
     out = torch.empty_like(q)
     desc = P.binding.make_desc(cfg.B, cfg.H, cfg.d, cfg.h, cfg.n_kv, cfg.n_q, cfg.chunk, cfg.order,
                                cfg.use_muon, cfg.ns_steps, P.IO_BF16 if cfg.io == "bf16" else P.IO_FP32,
@@ -441,6 +514,8 @@ def main():
         "launch": "hip_graph" if args.graph else "eager",
         "pct_of_peak": round(100.0 * tflops / peak, 2),
     }
+    if on_device:
+        res["data"] = "synthetic, drawn on the device (seeded torch generator, the recipe's distributions)"
     if cfg.use_muon:   # the same time over the token FLOPs alone (Newton-Schulz FLOPs left out)
         res["value_without_muon_flops"] = round(workload_flops(cfg.with_(use_muon=0)) / dt / 1e12, 3)
 
@@ -463,10 +538,13 @@ def main():
         achieved = d["tflops"] or 0.0
         kname = DOMINANT_KERNEL.get(dom, dom)
         traffic = measured_traffic(cfg.name, kname)
+        alg = kernel_alg_bytes(cfg, kname, d["launches"] / max(args.steps, 1))
         res["roofline"] = {"bound": "mfma", "kernel": kname,
                            "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                            "frac": round(achieved / peak, 4), "traffic": traffic,
                            "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                           "alg_bytes_per_launch": round(alg) if alg else None,
+                           "traffic_over_alg": round(traffic / alg, 3) if (traffic and alg) else None,
                            "avg_launch_us": d["avg_us"],
                            "flops_per_launch": round(achieved * 1e12 * d["avg_us"] * 1e-6),
                            "per_class": per}
@@ -486,6 +564,46 @@ def main():
                 res["io_kernels"][name] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                                            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                                            "bytes_per_launch": io_bytes[name], "avg_launch_us": round(avg * 1e6, 3)}
+    return res
+
+
+# The second workload that the performance target names, measured in the same
+# process after the default one: NVS with a million context tokens.
+SECONDARY = "nvs1m"
+
+
+def main():
+    args = parse()
+    if args.traffic_report:
+        traffic_report(args.config, *args.traffic_report)
+        return
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    import torch
+
+    import paper_2505_23884_amd as P
+    from lact_synth import CONFIGS
+
+    cfg = CONFIGS[args.config]
+    if args.chunk:
+        if cfg.schedule or cfg.layer_io:
+            raise SystemExit("--chunk applies to the uniform-chunk workloads")
+        cfg = cfg.with_(name=f"{cfg.name}_c{args.chunk}", chunk=args.chunk)
+    if args.library_gemms:
+        library_gemms(cfg, max(args.steps, 5))
+        return
+    res = measure(cfg, args, P, on_device=args.device_inputs)
+    if not args.no_secondary and args.config == "lm32k" and not args.chunk:
+        torch.cuda.empty_cache()
+        sec = measure(CONFIGS[SECONDARY], args, P, on_device=True)
+        keep = ("value", "unit", "ms_per_step", "tokens_per_s", "pct_of_peak", "data", "config", "roofline")
+        res["secondary"] = {SECONDARY: {k: sec[k] for k in keep if k in sec}}
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(res), flush=True)

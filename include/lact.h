@@ -20,7 +20,7 @@
  *           with the final fast weights (the novel-view-synthesis layout:
  *           update on the input views, apply to the target views, §4).
  *
- * With the linear fast weight (lact_desc.fast_weight, §4.4) the same path
+ * With the linear fast weight (lact_desc.fast_weight, §5.4) the same path
  * runs for f_W(x) = W1 x with W1 in R^{d x d}: o = W1 q, g = -sum eta v k^T.
  *
  * Entry points: lact_forward (the path above), lact_forward_momentum (the
@@ -70,7 +70,7 @@ extern "C" {
 
 /* lact_desc.fast_weight */
 #define LACT_FW_SWIGLU 0        /* f_W(x) = W2 [SiLU(W1 x) o (W3 x)]                 */
-#define LACT_FW_LINEAR 1        /* f_W(x) = W1 x, W1 in R^{d x d} (§4.4): requires  */
+#define LACT_FW_LINEAR 1        /* f_W(x) = W1 x, W1 in R^{d x d} (§5.4): requires  */
                                 /* h == d and one rate per token; W2, W3 (and M2,  */
                                 /* M3) are unused and may be NULL                  */
 
@@ -171,7 +171,7 @@ int lact_forward_momentum(const lact_desc* desc,
 
 /*
  * General schedule: the fast-weight path over a caller-given list of segments
- * (the ttt_config loop of Alg. 1; §3.1 masks and the strided mask of §3.3
+ * (the ttt_config loop of Alg. 1; §3.1 masks and the strided mask of §4.3
  * that updates on clean video chunks only). Segments run in list order; each
  * is ONE update and/or apply over its token range [begin, end):
  *

@@ -21,7 +21,7 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
 * per-matrix rates one learning rate per token for each of W1, W2, W3 (the
                    lr of shape [b, l, 3] in the update of Alg. 1)
 * linear weight    f_W(x) = W x with W in R^{d x d}, the same loss and update
-                   rules (gradient -sum_i eta_i v_i k_i^T)          (§4.4 linear vs.
+                   rules (gradient -sum_i eta_i v_i k_i^T)          (§5.4 linear vs.
                    nonlinear fast weight; §3.1 loss eq.)
 * prologue         per token and head: q, k, v = SiLU of the projections,
                    q and k divided by their L2 norm, lr = softplus(raw + bias),
@@ -31,7 +31,7 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
 * schedule         a list of (mode, begin, end) segments, each one of
                    update-then-apply, apply-then-update, update-only or
                    apply-only on its token range (the ttt_config loop of Alg. 1;
-                   §3.1 masks, including the strided video mask of §3.3)
+                   §3.1 masks, including the strided video mask of §4.3)
 
 Math layout (one instance): W1, W3 in R^{h x d}, W2 in R^{d x h}; a "row" is
 the input dimension of the matrix (d for W1 and W3, h for W2). Tokens are rows
@@ -80,7 +80,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = [
-    "NS_COEFFS", "NS_EPS", "sigmoid", "silu", "swiglu_apply", "chunk_gradient",
+    "NS_COEFFS", "NS_EPS", "sigmoid", "silu", "silu_derivative", "swiglu_apply", "chunk_gradient",
     "newton_schulz", "weight_update", "update", "momentum_update", "lact_forward_instance",
     "lact_forward", "lact_forward_momentum", "SCHEDULE_MODES", "lact_forward_schedule_instance",
     "lact_forward_schedule", "softplus", "qkv_prologue", "rmsnorm_out", "linear_gradient",
@@ -120,15 +120,27 @@ def swiglu_apply(W1, W2, W3, X):
     return H @ W2.T           # W2 [ ... ], [n, d]
 
 
-def chunk_gradient(W1, W2, W3, K, V, eta, token_block: int = 65536):
-    """Gradient of sum_i eta_i * (-f_W(k_i)^T v_i) w.r.t. (W1, W2, W3).
+def silu_derivative(z: np.ndarray) -> np.ndarray:
+    """dSiLU/dz: with s = sigmoid(z), d(z s)/dz = s + z s (1 - s) (ds/dz = s (1 - s))."""
+    s = sigmoid(z)
+    return s + z * s * (1.0 - s)
 
-    §3.1 chunk-gradient and loss eqs.; the backward follows the update of
-    Alg. 1: forward on the keys, then the hidden gradient W2^T v_i pushed
-    through the gate product and the SiLU derivative
-    SiLU'(z) = s (1 + z (1 - s)), s = sigmoid(z).
-    eta is [n] (one rate) or [n, 3]: column j weights the gradient of
-    W_{j+1} only (per-matrix rates of Alg. 1, reading R9).
+
+def chunk_gradient(W1, W2, W3, K, V, eta, token_block: int = 65536):
+    """Gradient of sum_i eta_i * (-f_W(k_i)^T v_i) w.r.t. (W1, W2, W3)
+    (§3.1 chunk-gradient and loss eqs.), in closed form.
+
+    For one token, f_W(k)^T v = c^T (SiLU(z1) o z3) with z1 = W1 k, z3 = W3 k
+    and c = W2^T v (W2 only enters through c), so the product and chain rules
+    give
+        d/dW2 [f^T v] = v (SiLU(z1) o z3)^T
+        d/dW3 [f^T v] = (c o SiLU(z1)) k^T
+        d/dW1 [f^T v] = (c o z3 o SiLU'(z1)) k^T
+    and the loss carries -eta_i. Over a block of tokens stacked as rows
+    (K, V: [b, d]; Z1 = K W1^T, Z3 = K W3^T, C = V W2: [b, h]) each sum of
+    outer products is one matrix product. eta is [n] (one rate) or [n, 3]:
+    column j weights the gradient of W_{j+1} only (per-matrix rates of
+    Alg. 1, reading R9).
 
     Returns (g1 [h, d], g2 [d, h], g3 [h, d]) in float64.
     """
@@ -139,23 +151,14 @@ def chunk_gradient(W1, W2, W3, K, V, eta, token_block: int = 65536):
     n = K.shape[0]
     for s in range(0, n, token_block):   # reading R7
         e = min(n, s + token_block)
-        k = np.asarray(K[s:e], dtype=np.float64)
-        v = np.asarray(V[s:e], dtype=np.float64)
+        Kb = np.asarray(K[s:e], dtype=np.float64)
+        Vb = np.asarray(V[s:e], dtype=np.float64)
         lr = np.asarray(eta[s:e], dtype=np.float64)
-        lr1, lr2, lr3 = (lr[:, j:j + 1] for j in range(3)) if lr.ndim == 2 else (lr[:, None],) * 3
-        z1 = k @ W1.T                      # pre-activation of the gate, [b, h]
-        z3 = k @ W3.T                      # ungated hidden, [b, h]
-        sg = sigmoid(z1)
-        a = z1 * sg                        # SiLU(z1)
-        hid = a * z3                       # hidden state of f_W(k)
-        dhid = v @ W2                      # d(f^T v)/d hidden = W2^T v, [b, h]
-        dz3 = dhid * a                     # through the gate product, W3 branch
-        da = dhid * z3                     # through the gate product, W1 branch
-        dz1 = da * sg * (1.0 + z1 * (1.0 - sg))   # SiLU derivative
-        # L = -eta f^T v, so every gradient carries a minus sign.
-        g2 -= (v * lr2).T @ hid            # dL/dW2 = -sum eta v hid^T
-        g1 -= (dz1 * lr1).T @ k            # dL/dW1 = -sum eta dz1 k^T
-        g3 -= (dz3 * lr3).T @ k            # dL/dW3 = -sum eta dz3 k^T
+        r1, r2, r3 = (lr[:, j:j + 1] for j in range(3)) if lr.ndim == 2 else (lr[:, None],) * 3
+        Z1, Z3, C = Kb @ W1.T, Kb @ W3.T, Vb @ W2
+        g2 -= (r2 * Vb).T @ (silu(Z1) * Z3)
+        g3 -= (r3 * C * silu(Z1)).T @ Kb
+        g1 -= (r1 * C * Z3 * silu_derivative(Z1)).T @ Kb
     return g1, g2, g3
 
 
@@ -340,7 +343,7 @@ def rmsnorm_out(o, B: int, H: int, weight=None, eps: float = 1e-6):
 
 def linear_gradient(W, K, V, eta):
     """Gradient of sum_i eta_i * (-(W k_i)^T v_i) w.r.t. W for the linear fast
-    weight f_W(x) = W x (§4.4; §3.1 loss eq.): -sum_i eta_i v_i k_i^T, [d, d]."""
+    weight f_W(x) = W x (§5.4; §3.1 loss eq.): -sum_i eta_i v_i k_i^T, [d, d]."""
     K = np.asarray(K, dtype=np.float64)
     V = np.asarray(V, dtype=np.float64)
     lr = np.asarray(eta, dtype=np.float64)[:, None]

@@ -11,7 +11,7 @@
 //   BWD_OUT     O^T = W2 hidden^T                                  (apply, second matmul)
 //   BWD_GRAD13  P1 = (eta dz1)^T K,  P3 = (eta dz3)^T K             (gradient matmuls, -g1, -g3)
 //   BWD_GRAD2   P2 = V^T (eta hidden)                              (-g2; the linear
-//               fast weight's gradient V^T (eta K), §4.4, with OUT as its apply)
+//               fast weight's gradient V^T (eta K), §5.4, with OUT as its apply)
 //   BWD_GRAD_UPD  P1, P3, P2 of whole rows (256 < d, h <= 512) followed in the
 //               same workgroup by the weight update of those rows, with or
 //               without momentum (no Muon, no split): the gradient never goes

@@ -70,6 +70,15 @@ def test_sigmoid_silu_extremes():
     np.testing.assert_allclose(O.silu(z), F.silu(torch.as_tensor(z)).numpy(), rtol=1e-15, atol=1e-300)
 
 
+def test_silu_derivative_against_autograd():
+    # includes the saturated ends (derivative 0 and 1) and the minimum of SiLU
+    # near z = -1.2785 (derivative 0)
+    z = np.concatenate([np.linspace(-40.0, 40.0, 401), [-800.0, -1.2784645427610738, 800.0]])
+    tz = torch.as_tensor(z).requires_grad_(True)
+    F.silu(tz).sum().backward()
+    np.testing.assert_allclose(O.silu_derivative(z), tz.grad.numpy(), rtol=1e-13, atol=1e-15)
+
+
 # ----------------------------------------------------------------------------- gradient
 
 
@@ -604,7 +613,7 @@ def test_uncovered_rows_are_zero_and_later_applies_win():
 
 
 def _video_schedule(C, n_clean):
-    """Teacher forcing of §3.3: [X1_noise, X1, X2_noise, X2, ..., XN_noise];
+    """Teacher forcing of §4.3: [X1_noise, X1, X2_noise, X2, ..., XN_noise];
     noisy chunks are applied only, clean chunks update then apply."""
     sched, t = [], 0
     for i in range(n_clean + 1):
@@ -718,7 +727,7 @@ def test_output_rmsnorm_matches_library():
 
 
 # ----------------------------------------------------------------------------- linear fast weight
-# §4.4: f_W(x) = W x with the same dot-product loss and update rules.
+# §5.4: f_W(x) = W x with the same dot-product loss and update rules.
 
 
 def test_linear_gradient_matches_autograd():

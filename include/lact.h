@@ -40,7 +40,8 @@
  *    stream) and never synchronise the host, except when the environment
  *    variable LACT_SYNC=1 is set (debugging).
  *  - No entry point allocates memory: all scratch memory is the caller's
- *    `workspace` (lact_prologue and lact_rmsnorm_out need none).
+ *    `workspace` (lact_prologue and lact_rmsnorm_out need none), except for
+ *    lact_forward_noalloc, whose scratch is a fixed array of the library.
  *  - Arguments are validated before any HIP call, so every error below is
  *    reported without touching the GPU. Errors are negative return codes;
  *    nothing is thrown across the ABI. On an error no output is written.
@@ -63,6 +64,8 @@ extern "C" {
 #define LACT_EWORKSPACE (-3)    /* workspace NULL or smaller than required          */
 #define LACT_EUNSUPPORTED (-4)  /* shape outside the kernels' envelope (see below)  */
 #define LACT_EHIP (-5)          /* a HIP call failed; lact_last_hip_error() has it   */
+#define LACT_ESCRATCH (-6)      /* lact_forward_noalloc: the call needs more scratch */
+                                /* than LACT_NOALLOC_SCRATCH_BYTES                  */
 
 /* lact_desc.order */
 #define LACT_APPLY_THEN_UPDATE 0
@@ -134,6 +137,34 @@ int lact_forward(const lact_desc* desc,
                  void* o,
                  void* workspace, size_t workspace_bytes,
                  void* stream);
+
+/*
+ * lact_forward for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops and harnesses that forbid allocation):
+ * the same arguments, semantics and errors without the workspace. Its
+ * scratch memory is a fixed array of LACT_NOALLOC_SCRATCH_BYTES (128 MiB) in
+ * the library's device code, one copy per device, held from the library's
+ * load onto that device until the process ends; the call allocates nothing.
+ *
+ *  - LACT_ESCRATCH when lact_workspace_bytes(desc) exceeds that size
+ *    (checked with the other arguments, before any HIP call). A single LM
+ *    sequence (B = 1, H = 4, d = h = 512, chunk 2048) needs 74 MiB, 116 MiB
+ *    with Muon.
+ *  - The array is the one on the device of `stream` (the current device for
+ *    the null stream). The first call on a device looks its address up (a
+ *    host-side HIP query, no stream work); a caller that captures the call
+ *    in a graph makes one call outside the capture first.
+ *  - Every call on a device uses that device's one array and leaves its
+ *    contents behind (no call depends on them). Calls that can overlap on
+ *    one device (several streams or host threads) race on the array: the
+ *    caller serialises them.
+ */
+#define LACT_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int lact_forward_noalloc(const lact_desc* desc,
+                         const void* q, const void* k, const void* v, const float* eta,
+                         float* W1, float* W2, float* W3,
+                         void* o,
+                         void* stream);
 
 /*
  * The same path with a momentum test-time optimizer (App. A, implementing

@@ -12,7 +12,8 @@ IO_BF16, IO_FP32 = 0, 1
 KCLASS_NAMES = ("fwd", "bwd", "update", "ns", "prep", "io")
 
 _ERRORS = {0: "LACT_OK", -1: "LACT_EINVAL", -2: "LACT_EALIGN", -3: "LACT_EWORKSPACE",
-           -4: "LACT_EUNSUPPORTED", -5: "LACT_EHIP"}
+           -4: "LACT_EUNSUPPORTED", -5: "LACT_EHIP", -6: "LACT_ESCRATCH"}
+NOALLOC_SCRATCH_BYTES = 128 << 20   # LACT_NOALLOC_SCRATCH_BYTES
 
 
 class LactError(RuntimeError):
@@ -61,6 +62,8 @@ def load_library(path: str | None = None):
     L.lact_check_desc.restype = i32
     L.lact_forward.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.lact_forward.restype = i32
+    L.lact_forward_noalloc.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.lact_forward_noalloc.restype = i32
     L.lact_forward_momentum.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.lact_forward_momentum.restype = i32
     L.lact_forward_schedule.argtypes = [dp, ctypes.POINTER(LactSegment), i64] + [vp] * 13 + [sz, vp]
@@ -123,8 +126,9 @@ def _ptr(t):
 
 
 def _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps, out, workspace, stream,
-             fast_weight=FW_SWIGLU):
-    """Checks shapes and dtypes; returns (desc, out, workspace, stream handle)."""
+             fast_weight=FW_SWIGLU, need_workspace=True):
+    """Checks shapes and dtypes; returns (desc, out, workspace, stream handle)
+    (workspace None when need_workspace is False)."""
     import torch
     if q.dim() == 4:
         B, H = q.shape[0], q.shape[1]
@@ -157,9 +161,8 @@ def _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps, 
             or W2.shape[-2] != d or W2.shape[-1] != h or W1.shape[-1] != d):
         raise LactError(-1, "inconsistent tensor shapes")
     desc = make_desc(B, H, d, h, n_kv, n_q, chunk, order, use_muon, ns_steps, io, lr3, fast_weight)
-    nbytes = workspace_bytes(desc)
-    if workspace is None:
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    if need_workspace and workspace is None:
+        workspace = torch.empty(max(workspace_bytes(desc), 1), dtype=torch.uint8, device=q.device)
     if out is None:
         out = torch.empty_like(q)
     if stream is None:
@@ -182,6 +185,21 @@ def forward(q, k, v, eta, W1, W2, W3, chunk, order=APPLY_THEN_UPDATE, use_muon=F
                             _ptr(W2), _ptr(W3), _ptr(out), _ptr(workspace),
                             ctypes.c_size_t(workspace.numel() * workspace.element_size()),
                             ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return out
+
+
+def forward_noalloc(q, k, v, eta, W1, W2, W3, chunk, order=APPLY_THEN_UPDATE, use_muon=False, ns_steps=5,
+                    out=None, stream=None):
+    """forward() through lact_forward_noalloc: no workspace argument; the
+    library's fixed per-device scratch array serves as the workspace (calls
+    that may overlap on one device race on it). ``out`` is allocated here
+    when not given (pass it to allocate nothing)."""
+    desc, out, _, stream = _marshal(q, k, v, eta, W1, W2, W3, [], chunk, order, use_muon, ns_steps, out, None,
+                                    stream, need_workspace=False)
+    rc = lib().lact_forward_noalloc(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(W1),
+                                    _ptr(W2), _ptr(W3), _ptr(out), ctypes.c_void_p(stream))
     if rc:
         _raise(rc)
     return out

@@ -5,10 +5,17 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "lact.h"
 #include "lact_internal.h"
+
+// Scratch memory of lact_forward_noalloc (its workspace, for callers that
+// cannot allocate): one copy per device, loaded with the library's device
+// code and held until the process ends. In host code `scratch` is only the
+// symbol's stand-in; its device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[LACT_NOALLOC_SCRATCH_BYTES];
 
 namespace lact {
 namespace {
@@ -811,7 +818,7 @@ int update_chunk_linear(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
 // when there are key tokens).
 int setup(Ctx& c, const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
           const float* beta, float* W1, float* W2, float* W3, float* const M[3], void* o, void* workspace,
-          size_t workspace_bytes, void* stream) {
+          size_t workspace_bytes, void* stream, bool use_scratch = false) {
   int rc = check_desc(desc);
   if (rc) return rc;
   const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
@@ -828,8 +835,12 @@ int setup(Ctx& c, const lact_desc* desc, const void* q, const void* k, const voi
   c = Ctx{};
   c.dsc = desc;
   c.p = make_plan(desc);
-  if (!workspace || workspace_bytes < c.p.total) return LACT_EWORKSPACE;
-  if ((uintptr_t)workspace & (kAlign - 1)) return LACT_EALIGN;
+  if (use_scratch) {   // the fixed per-device array; its address is resolved by the caller
+    if (c.p.total > LACT_NOALLOC_SCRATCH_BYTES) return LACT_ESCRATCH;
+  } else {
+    if (!workspace || workspace_bytes < c.p.total) return LACT_EWORKSPACE;
+    if ((uintptr_t)workspace & (kAlign - 1)) return LACT_EALIGN;
+  }
   c.q = (const uint8_t*)q;
   c.k = (const uint8_t*)k;
   c.v = (const uint8_t*)v;
@@ -885,14 +896,57 @@ int beta_means(Ctx& c, int64_t t0, int64_t len, int64_t end, int nchunks) {
   return timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] { return launch_beta_mean(ba, c.s); });
 }
 
+// Device address of `scratch` on the device that stream `s` belongs to (the
+// current device for the null stream): looked up once per device, with that
+// device current, and kept for the life of the process.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch[kMaxDevices] = {};
+
+int scratch_for_stream(hipStream_t s, uint8_t** out) {
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return record_hip(e);
+  int dev = cur;
+  if (s) {
+    hipDevice_t sd = 0;
+    if ((e = hipStreamGetDevice(s, &sd)) != hipSuccess) return record_hip(e);
+    dev = (int)sd;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return LACT_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return record_hip(e);
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) {
+      const hipError_t back = hipSetDevice(cur);
+      if (e == hipSuccess) e = back;
+    }
+    if (e != hipSuccess) return record_hip(e);
+    if (!p || ((uintptr_t)p & (kAlign - 1))) {
+      snprintf(g_hip_err, sizeof g_hip_err, "scratch array at %p: not 256-byte aligned", p);
+      return LACT_EHIP;
+    }
+    g_scratch[dev] = reinterpret_cast<uint8_t*>(p);
+  }
+  *out = g_scratch[dev];
+  return LACT_OK;
+}
+
 // lact_forward and lact_forward_momentum: uniform chunks of desc->chunk tokens
-// in desc->order, then the apply-only tail.
+// in desc->order, then the apply-only tail. With use_scratch the workspace is
+// the device's scratch array (lact_forward_noalloc).
 int run_forward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
                 const float* beta, float* W1, float* W2, float* W3, float* const M[3], void* o,
-                void* workspace, size_t workspace_bytes, void* stream) {
+                void* workspace, size_t workspace_bytes, void* stream, bool use_scratch = false) {
   Ctx c;
-  int rc = setup(c, desc, q, k, v, eta, beta, W1, W2, W3, M, o, workspace, workspace_bytes, stream);
+  int rc = setup(c, desc, q, k, v, eta, beta, W1, W2, W3, M, o, workspace, workspace_bytes, stream, use_scratch);
   if (rc) return rc;
+  if (use_scratch) {
+    rc = scratch_for_stream(c.s, &c.ws);
+    if (rc) return rc;
+  }
   rc = prepare_weights(c);
   if (rc) return rc;
   const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk;
@@ -1009,6 +1063,11 @@ int lact_forward(const lact_desc* desc, const void* q, const void* k, const void
                  void* stream) {
   return run_forward(desc, q, k, v, eta, nullptr, W1, W2, W3, nullptr, o, workspace, workspace_bytes,
                      stream);
+}
+
+int lact_forward_noalloc(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                         float* W1, float* W2, float* W3, void* o, void* stream) {
+  return run_forward(desc, q, k, v, eta, nullptr, W1, W2, W3, nullptr, o, nullptr, 0, stream, true);
 }
 
 int lact_prologue(const lact_desc* desc, const void* qkv, const float* lr_raw, float lr_bias, const float* beta_raw,
@@ -1129,6 +1188,8 @@ const char* lact_strerror(int code) {
     case LACT_EWORKSPACE: return "workspace missing or too small";
     case LACT_EUNSUPPORTED: return "shape or option outside the kernels' envelope";
     case LACT_EHIP: return "HIP runtime error (see lact_last_hip_error)";
+    case LACT_ESCRATCH: return "the call needs more scratch memory than the fixed per-device array of "
+                               "lact_forward_noalloc holds (LACT_NOALLOC_SCRATCH_BYTES)";
     default: return "unknown error";
   }
 }

@@ -210,3 +210,29 @@ def test_timing_api_without_launches():
 def test_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(P.LactError):
         P.load_library(str(tmp_path / "missing.so"))
+
+
+def _fwd_noalloc(desc, q=0x1000, k=0x2000, v=0x3000, eta=0x4000, w1=0x5000, w2=0x6000, w3=0x7000, o=0x8000):
+    vp = ctypes.c_void_p
+    return P.lib().lact_forward_noalloc(ctypes.byref(desc), vp(q), vp(k), vp(v), vp(eta), vp(w1), vp(w2), vp(w3),
+                                        vp(o), vp(0))
+
+
+def test_noalloc_errors_before_any_hip_call():
+    # the binding's constant is the header's
+    m = re.search(r"#define LACT_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == P.binding.NOALLOC_SCRATCH_BYTES
+    d = make_desc(**GOOD)
+    assert _fwd_noalloc(d, q=0) == -1
+    assert _fwd_noalloc(d, w2=0) == -1
+    assert _fwd_noalloc(d, k=0x2008) == -2
+    assert _fwd_noalloc(make_desc(**dict(GOOD, d=12))) == -4
+    # a call that needs more than the fixed array: rejected before any HIP call
+    lm = dict(GOOD, B=4, H=4, d=512, h=512, n_kv=32768, n_q=32768, chunk=2048)
+    assert P.workspace_bytes(make_desc(**lm)) > P.binding.NOALLOC_SCRATCH_BYTES
+    assert _fwd_noalloc(make_desc(**lm)) == -6
+    assert _fwd_noalloc(make_desc(**lm), q=0) == -1       # argument errors come first
+    assert "scratch" in P.lib().lact_strerror(-6).decode()
+    # one LM sequence (B = 1, H = 4) fits, with Muon too
+    one = make_desc(**dict(lm, B=1, use_muon=True))
+    assert P.workspace_bytes(one) <= P.binding.NOALLOC_SCRATCH_BYTES

@@ -179,7 +179,9 @@ def _pmc(path, counter):
 
 def kernel_short_name(name):
     """k_fwd, k_bwd, ... from a mangled (…5k_fwdI…) or demangled (…::k_fwd<…) kernel name."""
-    for k in ("k_fwd", "k_bwd", "k_update", "k_prep", "k_ns_prep", "k_ns_scale", "k_ns"):
+    for k in ("k_fwd_narrow", "k_fwd", "k_bwd", "k_update", "k_prep", "k_scale_rows", "k_beta_mean", "k_zero_rows",
+              "k_ns_fused_pair", "k_ns_fused", "k_ns_final", "k_ns_prep", "k_ns_scale", "k_ns",
+              "k_prologue", "k_rmsnorm_out"):
         m = str(len(k)) + k
         if m + "I" in name or m + "E" in name or "::" + k + "<" in name or "::" + k + "(" in name:
             return k
@@ -187,8 +189,11 @@ def kernel_short_name(name):
 
 
 def traffic_report(cfg_name, fetch_csv, write_csv, cfetch_csv, cwrite_csv):
-    """HBM bytes per launch of every lact kernel: the counter's median per
-    dispatch, scaled by copy_bytes / (the same counter for the copy kernel)."""
+    """HBM bytes per launch of every lact kernel: the counter's mean per
+    dispatch (the same average over launches as the roofline's average launch
+    time; a kernel may serve launches of different sizes, such as the key
+    forward and the apply of the NVS workloads), scaled by
+    copy_bytes / (the same counter for the copy kernel)."""
     import statistics
     cf, cw = _pmc(cfetch_csv, "FETCH_SIZE"), _pmc(cwrite_csv, "WRITE_SIZE")
     copy_fetch = max(max(v) for v in cf.values())
@@ -201,8 +206,8 @@ def traffic_report(cfg_name, fetch_csv, write_csv, cfetch_csv, cwrite_csv):
         short = kernel_short_name(name)
         if short is None or name not in w:
             continue
-        fb = statistics.median(f[name]) * scale["fetch"]
-        wb = statistics.median(w[name]) * scale["write"]
+        fb = statistics.mean(f[name]) * scale["fetch"]
+        wb = statistics.mean(w[name]) * scale["write"]
         kernels[short] = {"fetch_bytes": round(fb), "write_bytes": round(wb), "traffic_bytes": round(fb + wb),
                           "dispatches": len(f[name])}
     rep = {"config": cfg_name, "kernels_source_sha256": source_hash(),

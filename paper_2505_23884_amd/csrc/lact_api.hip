@@ -40,6 +40,7 @@ struct Plan {
   int64_t split_len;  // tokens per split
   bool fused;         // gradient and weight update in one kind (BWD_GRAD_UPD)
   bool narrow;        // narrow tile shapes of both launches (16-bit, d <= 128)
+  bool ns_out;        // a chunk's output tiles run with its fused Newton-Schulz
   bool muon;
   bool tile_sums;     // Muon without split: the gradient tiles leave the sums of squares
   int t13, t2;        // gradient tiles per matrix (W1 or W3; W2 or the linear W)
@@ -97,6 +98,15 @@ Plan make_plan(const lact_desc* dsc) {
   p.nmat = p.linear ? 1 : 3;
   p.C = std::min<int64_t>(dsc->chunk, dsc->n_kv);
   p.narrow = p.bf16 && p.d <= 128;
+  // Small matrices with Muon (one fused Newton-Schulz workgroup each) and the
+  // narrow tile shapes: the output tiles of a chunk's apply run in the
+  // Newton-Schulz launch, on the CUs its one workgroup per matrix leaves idle,
+  // instead of beside the gradient tiles; the update writes the other set of
+  // operand copies. (Video: 4.39 -> 4.29 ms per step. The gradient tiles then
+  // have the second launch to themselves; three or four splits instead of two
+  // did not pay: the Newton-Schulz workgroups sum the partials.)
+  p.ns_out = p.narrow && dsc->use_muon && !p.linear && std::min(p.d, p.h) <= kNsFusedM &&
+             std::max(p.d, p.h) <= kNsFusedN;
   const int64_t tail = dsc->n_q - dsc->n_kv;
   // The applied-hidden buffer holds one chunk plus (bounded) tail rows so that
   // update-then-apply can apply its last chunk together with the tail.
@@ -161,7 +171,7 @@ Plan make_plan(const lact_desc* dsc) {
   }
   for (int m = 0; m < 3; ++m) {
     p.off_wb2[m] = o;
-    if (p.fused) o = align_up(o + (size_t)p.BH * dh * 2);
+    if (p.fused || p.ns_out) o = align_up(o + (size_t)p.BH * dh * 2);
   }
   // linear: no applied hidden (the apply is one product); one update buffer (eta k)
   p.off_hq = o;
@@ -282,6 +292,9 @@ struct Ctx {
   const float* beta;   // momentum: per-token factor [BH][n_kv], or nullptr
   float* M[3];         // momentum state (with beta)
   int64_t chunk_idx;   // index of the chunk being updated
+  BwdArgs out_pending{};   // with ns_out: the output tiles the next Newton-Schulz launch runs
+  double out_flops = 0.0;
+  bool has_out = false;
 };
 
 // Momentum factor of the current chunk for instance 0 (stride kBetaBatch).
@@ -366,6 +379,8 @@ int apply_rows(Ctx& c, int64_t s0, int64_t s1) {
   return LACT_OK;
 }
 
+void use_wset(Ctx& c, int set);
+
 // Muon (§3.2; App. A): Newton-Schulz on the three summed gradients of every
 // instance, in their stored orientation; leaves NS(P) in the fp32 iterate.
 int newton_schulz(Ctx& c) {
@@ -437,17 +452,27 @@ int newton_schulz(Ctx& c) {
       f.nsplit = c.beta ? 1 : p.nsplit;
       f.part_split = pa.part_split;
       f.eps = 1e-7f;
-      // and the weight update (no separate update launch follows)
+      // and the weight update (no separate update launch follows); with
+      // output tiles in the launch, the copies go to the other set
       for (int j = 0; j < p.nmat; ++j) {
         f.W[j] = c.W[j];
-        f.Wb[j] = c.wb[c.wset][j];
+        f.Wb[j] = c.wb[c.has_out ? c.wset ^ 1 : c.wset][j];
       }
       fl += (double)f.steps * f.nblocks * (4.0 * m * m * n + 2.0 * m * m * m);
     }
-    rc = timed(LACT_KCLASS_NS, fl, c.s, [&] {
-      return nseg == 2 ? launch_ns_fused_pair(fs[0], fs[1], c.s) : launch_ns_fused(fs[0], c.s);
-    });
-    if (rc) return rc;
+    if (c.has_out) {
+      if (nseg != 2) return LACT_EUNSUPPORTED;
+      c.has_out = false;
+      rc = timed(LACT_KCLASS_NS, fl + c.out_flops, c.s,
+                 [&] { return launch_ns_fused_pair_out(fs[0], fs[1], c.out_pending, c.s); });
+      if (rc) return rc;
+      use_wset(c, c.wset ^ 1);   // the next launches read the new copies
+    } else {
+      rc = timed(LACT_KCLASS_NS, fl, c.s, [&] {
+        return nseg == 2 ? launch_ns_fused_pair(fs[0], fs[1], c.s) : launch_ns_fused(fs[0], c.s);
+      });
+      if (rc) return rc;
+    }
     c.ns_updated = true;
     return LACT_OK;
   }
@@ -690,7 +715,11 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     set_tile_sums(c, g, 1);
   }
   if (apply_too) {
-    BwdSeg& o = b.seg[nb++];
+    // with ns_out the output tiles wait for the Newton-Schulz launch, which
+    // follows this one (finish_update) and still reads this copy set's W2
+    BwdArgs& ob = c.out_pending;
+    BwdSeg& o = p.ns_out ? ob.seg[0] : b.seg[nb++];
+    o = BwdSeg{};
     o.kind = BWD_OUT;
     o.tiles_m = (int)cdiv(p.d, bwd_tile(BWD_OUT, p.bf16, p.narrow).rows);
     o.tiles_n = (int)cdiv(n, bwd_tile(BWD_OUT, p.bf16, p.narrow).cols);
@@ -701,6 +730,15 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     o.b0 = c.wop[1];
     o.out = c.o + s0 * p.d * p.esz;
     o.out_inst = c.dsc->n_q * p.d;
+    if (p.ns_out) {
+      ob.nseg = 1;
+      ob.total_blocks = o.nblocks;
+      ob.d = p.d;
+      ob.h = p.h;
+      ob.narrow = p.narrow;
+      c.out_flops = 2.0 * p.BH * n * dh;
+      c.has_out = true;
+    }
   }
   b.nseg = nb;
   b.total_blocks = 0;
@@ -708,7 +746,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
   b.d = p.d;
   b.h = p.h;
   b.narrow = p.narrow;
-  const double bfl = (apply_too ? 2.0 : 0.0) * p.BH * n * dh + 6.0 * p.BH * n * dh;
+  const double bfl = (apply_too && !p.ns_out ? 2.0 : 0.0) * p.BH * n * dh + 6.0 * p.BH * n * dh;
   rc = timed(LACT_KCLASS_BWD, bfl, c.s, [&] { return launch_bwd(b, p.bf16, c.s); });
   if (rc) return rc;
   if (fused) {   // the update is done; the next launches read the new copies

@@ -277,6 +277,10 @@ hipError_t launch_ns_prep(const NsPrepArgs& a, hipStream_t s);
 hipError_t launch_ns_scale(const NsPrepArgs& a, void* Yb, bool fp16, float eps, hipStream_t s);
 hipError_t launch_ns_fused(const NsFusedArgs& a, hipStream_t s);
 hipError_t launch_ns_fused_pair(const NsFusedArgs& a0, const NsFusedArgs& a1, hipStream_t s);
+// The same with the output tiles of one chunk (out: one BWD_OUT segment, narrow
+// shapes) in the launch; the Newton-Schulz writes the copies of the other set.
+hipError_t launch_ns_fused_pair_out(const NsFusedArgs& a0, const NsFusedArgs& a1, const BwdArgs& out,
+                                    hipStream_t s);
 hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s);
 // Zero rows [r0, r1) of every instance of an output of `rows` rows of row_bytes
 // (a multiple of 16) each.

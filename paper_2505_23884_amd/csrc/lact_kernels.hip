@@ -1260,16 +1260,23 @@ __device__ __forceinline__ float2 tile_sumsq(const Acc<K>& acc, uint8_t* smem) {
 
 // Second launch: apply GEMM-2 and the gradient contractions (split over tokens).
 template <typename T, bool NARROW>
-__global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs args) {
+constexpr int bwd_smem() {
+  using KO = typename BwdKinds<T, NARROW>::Out;
+  using K13 = typename BwdKinds<T, NARROW>::Grad13;
+  using K2 = typename BwdKinds<T, NARROW>::Grad2;
+  return cmax(cmax(smem_bytes<T, KO>(), (sizeof(T) == 2 && !NARROW) ? smem_bytes<T, KGradU16>() : 0),
+              cmax(smem_bytes<T, K13>(), smem_bytes<T, K2>()));
+}
+
+// Block `blk` of the second launch (smem: bwd_smem bytes of LDS).
+template <typename T, bool NARROW>
+__device__ __forceinline__ void bwd_body(const BwdArgs& args, int blk, uint8_t* smem) {
   using KO = typename BwdKinds<T, NARROW>::Out;
   using K13 = typename BwdKinds<T, NARROW>::Grad13;
   using K2 = typename BwdKinds<T, NARROW>::Grad2;
   static_assert(KO::THREADS == K13::THREADS && KO::THREADS == K2::THREADS, "one block size per launch");
-  __shared__ __attribute__((aligned(16)))
-  uint8_t smem[cmax(cmax(smem_bytes<T, KO>(), (sizeof(T) == 2 && !NARROW) ? smem_bytes<T, KGradU16>() : 0),
-                    cmax(smem_bytes<T, K13>(), smem_bytes<T, K2>()))];
   constexpr int esz = sizeof(T);
-  int bid = blockIdx.x;
+  int bid = blk;
   int si = 0;
   if (bid >= args.seg[0].nblocks) {
     bid -= args.seg[0].nblocks;
@@ -1302,7 +1309,7 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
     const int64_t ob = inst * sg.out_inst;
     const int mrow0 = wave_m<KO>() * 32 * KO::MI + ((lane >> 5) << 2);
     if constexpr (sizeof(T) == 2) {
-      static_assert(KO::ROWS_A * KO::ROWS_B * 2 <= sizeof(smem), "staging fits");
+      static_assert(KO::ROWS_A * KO::ROWS_B * 2 <= bwd_smem<T, NARROW>(), "staging fits");
 #pragma unroll
       for (int ni = 0; ni < KO::NI; ++ni)
 #pragma unroll
@@ -1403,6 +1410,12 @@ __global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs ar
       if (threadIdx.x == 0) sg.sumsq[((int64_t)inst * sg.spi + sg.sumsq_j) * sg.sumsq_stride + rr] = t.x;
     }
   }
+}
+
+template <typename T, bool NARROW>
+__global__ __launch_bounds__(Kinds<T>::Out::THREADS) void k_bwd(const BwdArgs args) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[bwd_smem<T, NARROW>()];
+  bwd_body<T, NARROW>(args, blockIdx.x, smem);
 }
 
 // ===========================================================================
@@ -2128,6 +2141,26 @@ __global__ __launch_bounds__(512) void k_ns_fused_pair(const NsFusedArgs a0, con
   else ns_fused_body<TALL1>(a1, q - a0.nblocks, xs, as_, bs);
 }
 
+// The small-matrix Newton-Schulz of both groups together with the output
+// tiles of the same chunk's apply (o = W2 hidden, 16-bit narrow shapes): the
+// output reads the pre-update copy of W2 while the Newton-Schulz blocks write
+// the updated copies into the other copy set, so the two are independent and
+// the output tiles take the CUs that the one-workgroup-per-matrix
+// Newton-Schulz leaves idle. Blocks below a0.nblocks + a1.nblocks run the
+// Newton-Schulz, the rest the output tiles.
+template <bool TALL0, bool TALL1>
+__global__ __launch_bounds__(512) void k_ns_fused_pair_out(const NsFusedArgs a0, const NsFusedArgs a1,
+                                                           const BwdArgs out) {
+  static_assert(KOutN16::THREADS == 512, "one block size");
+  constexpr int kNs = kNsFusedX + 2 * kNsFusedA;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[cmax(kNs, bwd_smem<__bf16, true>())];
+  const int q = blockIdx.x;
+  if (q < a0.nblocks) ns_fused_body<TALL0>(a0, q, smem, smem + kNsFusedX, smem + kNsFusedX + kNsFusedA);
+  else if (q < a0.nblocks + a1.nblocks)
+    ns_fused_body<TALL1>(a1, q - a0.nblocks, smem, smem + kNsFusedX, smem + kNsFusedX + kNsFusedA);
+  else bwd_body<__bf16, true>(out, q - a0.nblocks - a1.nblocks, smem);
+}
+
 __device__ __forceinline__ float block_sum(float v, float* red) {
   v = wave_sum(v);
   const int w = threadIdx.x >> 6;
@@ -2298,6 +2331,17 @@ hipError_t launch_ns_fused_pair(const NsFusedArgs& a0, const NsFusedArgs& a1, hi
   if (a0.rows > a0.cols) k_ns_fused_pair<true, false><<<(unsigned)blocks, 512, 0, s>>>(a0, a1);
   else if (a1.rows > a1.cols) k_ns_fused_pair<false, true><<<(unsigned)blocks, 512, 0, s>>>(a0, a1);
   else k_ns_fused_pair<false, false><<<(unsigned)blocks, 512, 0, s>>>(a0, a1);
+  return hipGetLastError();
+}
+
+hipError_t launch_ns_fused_pair_out(const NsFusedArgs& a0, const NsFusedArgs& a1, const BwdArgs& out,
+                                    hipStream_t s) {
+  const int64_t blocks = (int64_t)a0.nblocks + a1.nblocks + out.total_blocks;
+  if (blocks <= 0) return hipSuccess;
+  if (!out.narrow || out.nseg != 1 || out.seg[0].kind != BWD_OUT) return hipErrorInvalidValue;
+  if (a0.rows > a0.cols) k_ns_fused_pair_out<true, false><<<(unsigned)blocks, 512, 0, s>>>(a0, a1, out);
+  else if (a1.rows > a1.cols) k_ns_fused_pair_out<false, true><<<(unsigned)blocks, 512, 0, s>>>(a0, a1, out);
+  else k_ns_fused_pair_out<false, false><<<(unsigned)blocks, 512, 0, s>>>(a0, a1, out);
   return hipGetLastError();
 }
 

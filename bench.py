@@ -180,7 +180,7 @@ def _pmc(path, counter):
 def kernel_short_name(name):
     """k_fwd, k_bwd, ... from a mangled (…5k_fwdI…) or demangled (…::k_fwd<…) kernel name."""
     for k in ("k_fwd_narrow", "k_fwd", "k_bwd", "k_update", "k_prep", "k_scale_rows", "k_beta_mean", "k_zero_rows",
-              "k_ns_fused_pair", "k_ns_fused", "k_ns_final", "k_ns_prep", "k_ns_scale", "k_ns",
+              "k_ns_fused_pair_out", "k_ns_fused_pair", "k_ns_fused", "k_ns_final", "k_ns_prep", "k_ns_scale", "k_ns",
               "k_prologue", "k_rmsnorm_out"):
         m = str(len(k)) + k
         if m + "I" in name or m + "E" in name or "::" + k + "<" in name or "::" + k + "(" in name:

@@ -684,6 +684,16 @@ def test_muon_gram_triangle_three_tiles_wide_and_tall():
     teacher_forced(cfg, x, [0, 1])
 
 
+def test_muon_small_odd_chunks_ragged_with_tail():
+    # the narrow small-matrix path (output tiles in the Newton-Schulz launch,
+    # operand copies alternating between two sets): an odd number of chunks,
+    # the last one ragged, then an apply-only tail read from the set the last
+    # update wrote, end to end against the oracle
+    cfg = CONFIGS["video"].with_(name="muon_odd_tail", B=1, H=2, d=128, h=256, n_kv=296, n_q=356, chunk=128)
+    x = make_inputs(cfg, 31)
+    check(cfg, x, run_gpu(cfg, x), run_oracle(cfg, x))
+
+
 def test_muon_small_wide_then_tall_in_one_launch():
     # d > h: W1, W3 (128 x 256) iterate wide and W2 (256 x 128) tall, the
     # reverse of the video shape, in one fused launch that also normalises the
@@ -868,6 +878,28 @@ def test_momentum_muon_teacher_forced(order):
     teacher_forced(cfg, x, [0, 1])
 
 
+def test_momentum_muon_small_single_call_is_the_chain():
+    # small matrices with Muon: the output tiles of each chunk run in the fused
+    # Newton-Schulz launch, which writes the operand copies into the other of
+    # two sets; one call over six chunks (the last ragged) against one call per
+    # chunk carrying (W, M), each starting again from the first set, bitwise;
+    # then the first two chunks against the oracle
+    cfg = CONFIGS["lm32k_muon_mom"].with_(name="mom_muon_chain", B=1, H=2, d=128, h=256, n_kv=680, n_q=680,
+                                          chunk=128)
+    x = make_inputs(cfg, 27)
+    og, Wg, Mg = run_gpu_momentum(cfg, x)
+    oc, Wc, Mc = chained_momentum_calls(cfg, x)
+    diff = {"o": int(np.count_nonzero(og != oc))}
+    diff.update({f"W{j + 1}": int(np.count_nonzero(Wg[j] != Wc[j])) for j in range(3)})
+    diff.update({f"M{j + 1}": int(np.count_nonzero(Mg[j] != Mc[j])) for j in range(3)})
+    print(f"[gpu] single call vs {cfg.n_chunks} chained calls: differing elements {diff}", flush=True)
+    assert all(v == 0 for v in diff.values()), diff
+    two = cfg.with_(n_kv=2 * cfg.chunk, n_q=2 * cfg.chunk)
+    x2 = {kk: (np.ascontiguousarray(vv[:, :two.n_kv]) if kk in ("q", "k", "v", "eta", "beta") else vv)
+          for kk, vv in x.items()}
+    check_momentum(two, x2, run_gpu_momentum(two, x2), run_oracle_momentum(two, x2))
+
+
 def test_momentum_muon_fp32_teacher_forced():
     cfg = CONFIGS["tiny_fp32"].with_(name="mom_muon_fp32", B=1, H=2, d=64, h=96, n_kv=512, n_q=512,
                                      chunk=128, use_muon=1, ns_steps=5, momentum=1)
@@ -903,7 +935,8 @@ def chained_momentum_calls(cfg, x):
     for s in range(0, cfg.n_kv, cfg.chunk):
         e = min(cfg.n_kv, s + cfg.chunk)
         o, _ = P.forward_momentum(cut(q, s, e), cut(k, s, e), cut(v, s, e), cut(eta, s, e), cut(beta, s, e), *W, *M,
-                                  chunk=cfg.chunk, order=cfg.order)
+                                  chunk=cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
+                                  ns_steps=cfg.ns_steps)
         outs.append(o)
     torch.cuda.synchronize()
     f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])

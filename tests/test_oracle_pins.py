@@ -786,3 +786,39 @@ def test_linear_layer_eta_zero_and_autograd_loop(muon):
 def test_linear_flops():
     assert O.linear_flops(2, 8, 10, 12, 3) == 2 * 2 * 64 * 22
     assert O.linear_flops(1, 4, 4, 4, 2, True, 5) == 2 * 16 * 8 + 2 * 5 * 6 * 64
+
+
+# ----------------------------------------------------------------------------- batched drivers
+
+
+def test_batched_drivers_stack_their_instances():
+    # every batched driver is its per-instance function over the selected
+    # instances, stacked in the selection's order (instances are independent)
+    rng = _rng(91)
+    BH, d, h, n, C = 3, 8, 12, 40, 16
+    q, k, v = (np.stack([_tokens(rng, n, d) for _ in range(BH)]) for _ in range(3))
+    eta = 0.05 * rng.random((BH, n))
+    beta = rng.random((BH, n))
+    W = [np.stack(ws) for ws in zip(*[_weights(rng, h, d) for _ in range(BH)])]
+    Wl = np.stack([rng.standard_normal((d, d)) for _ in range(BH)])
+    pick = [2, 0]
+    sched = [("apply_then_update", 0, 16), ("update_only", 16, 40), ("apply_only", 16, 40)]
+    one = lambda i: O.lact_forward_instance(q[i], k[i], v[i], eta[i], W[0][i], W[1][i], W[2][i], C, 0, True, 3)
+    got = O.lact_forward(q, k, v, eta, *W, chunk=C, order=0, use_muon=True, ns_steps=3, instances=pick)
+    for s, i in enumerate(pick):
+        o, Wi = one(i)
+        assert np.array_equal(got[0][s], o) and all(np.array_equal(got[1 + j][s], Wi[j]) for j in range(3))
+    got = O.lact_forward_momentum(q, k, v, eta, beta, *W, chunk=C, order=1, instances=pick)
+    for s, i in enumerate(pick):
+        o, Wi, Mi = O.lact_forward_instance(q[i], k[i], v[i], eta[i], W[0][i], W[1][i], W[2][i], C, 1,
+                                            beta=beta[i])
+        ref = (o, *Wi, *Mi)
+        assert all(np.array_equal(got[j][s], ref[j]) for j in range(7))
+    got = O.lact_forward_linear(q, k, v, eta, Wl, chunk=C, order=0, instances=pick)
+    for s, i in enumerate(pick):
+        o, Wi = O.lact_forward_linear_instance(q[i], k[i], v[i], eta[i], Wl[i], C, 0)
+        assert np.array_equal(got[0][s], o) and np.array_equal(got[1][s], Wi)
+    got = O.lact_forward_schedule(q, k, v, eta, *W, sched, instances=pick)
+    for s, i in enumerate(pick):
+        o, Wi = O.lact_forward_schedule_instance(q[i], k[i], v[i], eta[i], W[0][i], W[1][i], W[2][i], sched)
+        assert np.array_equal(got[0][s], o) and all(np.array_equal(got[1 + j][s], Wi[j]) for j in range(3))

@@ -28,6 +28,13 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
                    beta = sigmoid(raw); heads moved next to the batch  (Alg. 1, layer)
 * output norm      per-head RMSNorm of o, heads moved back next to the
                    channels                                          (Alg. 1, layer)
+* backward (linear) the reverse of the linear fast weight's chunk loop: from the
+                   cotangents of o (and of the final W) to those of q, k, v,
+                   eta and the initial W, through the apply (o = W q), the
+                   chunk gradient and the norm-preserving update of every
+                   chunk (§3.1 loss and update; §5.4; reverse mode written out
+                   by hand: the chunk gradient -sum eta v k^T does not depend
+                   on W, so no second derivative enters)
 * schedule         a list of (mode, begin, end) segments, each one of
                    update-then-apply, apply-then-update, update-only or
                    apply-only on its token range (the ttt_config loop of Alg. 1;
@@ -85,6 +92,7 @@ __all__ = [
     "lact_forward", "lact_forward_momentum", "SCHEDULE_MODES", "lact_forward_schedule_instance",
     "lact_forward_schedule", "softplus", "qkv_prologue", "rmsnorm_out", "linear_gradient",
     "lact_forward_linear_instance", "lact_forward_linear", "linear_flops", "layer_flops",
+    "weight_update_vjp", "lact_backward_linear_instance", "lact_backward_linear",
 ]
 
 # Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
@@ -382,6 +390,78 @@ def lact_forward_linear_instance(q, k, v, eta, W, chunk: int, order: int, use_mu
     if n_q > n_kv:
         o[n_kv:] = apply(W, q[n_kv:])
     return (o, W, M) if mom else (o, W)
+
+
+def weight_update_vjp(W, step, dWn):
+    """Reverse of weight_update (W' = (n / u) U with U = W - step, n and u the
+    row norms of W and U): from the cotangent dWn of W', the cotangents of W
+    and of step. Per row, with a = dWn . U:
+        dU    = (n / u) dWn - (n a / u^3) U
+        dW    = dU + (a / (u n)) W        (W enters through U and through n)
+        dstep = -dU
+    """
+    W = np.asarray(W, dtype=np.float64)
+    U = W - np.asarray(step, dtype=np.float64)
+    dWn = np.asarray(dWn, dtype=np.float64)
+    n = np.sqrt(np.sum(W * W, axis=1, keepdims=True))
+    u = np.sqrt(np.sum(U * U, axis=1, keepdims=True))
+    a = np.sum(dWn * U, axis=1, keepdims=True)
+    dU = (n / u) * dWn - (n * a / u ** 3) * U
+    return dU + (a / (u * n)) * W, -dU
+
+
+def lact_backward_linear_instance(q, k, v, eta, W0, do, chunk: int, order: int, dW_final=None):
+    """Reverse of lact_forward_linear_instance (no Muon, no momentum): given the
+    cotangent ``do`` [n_q, d] of the outputs and optionally ``dW_final`` of the
+    returned fast weight, the cotangents (dq, dk, dv, deta, dW0) of the inputs.
+
+    The forward chunk loop is replayed to recover the fast weight entering
+    every chunk; the chunks are then reversed. With o_t = W q_t the apply
+    gives dW += do^T q and dq = do W; the chunk gradient g = -sum_t eta_t v_t
+    k_t^T, with dg its cotangent (weight_update_vjp), gives
+        dv_t = -eta_t dg k_t,  dk_t = -eta_t dg^T v_t,  deta_t = -v_t^T dg k_t.
+    Apply-then-update applies the weights entering the chunk, update-then-apply
+    those leaving it; the tail is applied with the final weights.
+    """
+    q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
+    eta = np.asarray(eta, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    n_q, n_kv = q.shape[0], k.shape[0]
+    Ws = [np.asarray(W0, dtype=np.float64).copy()]
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        Ws.append(weight_update(Ws[-1], linear_gradient(Ws[-1], k[s:e], v[s:e], eta[s:e])))
+    dW = np.zeros_like(Ws[0]) if dW_final is None else np.asarray(dW_final, dtype=np.float64).copy()
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    deta = np.zeros(n_kv)
+    if n_q > n_kv:
+        dW += do[n_kv:].T @ q[n_kv:]
+        dq[n_kv:] = do[n_kv:] @ Ws[-1]
+    starts = list(range(0, n_kv, chunk))
+    for c in reversed(range(len(starts))):
+        s, e = starts[c], min(n_kv, starts[c] + chunk)
+        if order == 1:                      # applied with the weights leaving the chunk
+            dW += do[s:e].T @ q[s:e]
+            dq[s:e] = do[s:e] @ Ws[c + 1]
+        g = linear_gradient(Ws[c], k[s:e], v[s:e], eta[s:e])
+        dW, dg = weight_update_vjp(Ws[c], g, dW)
+        kg = k[s:e] @ dg.T                  # rows dg k_t
+        dv[s:e] = -eta[s:e, None] * kg
+        dk[s:e] = -eta[s:e, None] * (v[s:e] @ dg)
+        deta[s:e] = -np.sum(v[s:e] * kg, axis=1)
+        if order == 0:                      # applied with the weights entering the chunk
+            dW += do[s:e].T @ q[s:e]
+            dq[s:e] = do[s:e] @ Ws[c]
+    return dq, dk, dv, deta, dW
+
+
+def lact_backward_linear(q, k, v, eta, W0, do, chunk: int, order: int, dW_final=None, instances=None):
+    """Batched driver of lact_backward_linear_instance: (dq, dk, dv, deta, dW0)
+    stacked over the selected instances."""
+    idx = range(q.shape[0]) if instances is None else instances
+    res = [lact_backward_linear_instance(q[i], k[i], v[i], eta[i], W0[i], do[i], chunk, order,
+                                         None if dW_final is None else dW_final[i]) for i in idx]
+    return tuple(np.stack(col) for col in zip(*res))
 
 
 def lact_forward_linear(q, k, v, eta, W, chunk: int, order: int, use_muon: bool = False,

@@ -822,3 +822,87 @@ def test_batched_drivers_stack_their_instances():
     for s, i in enumerate(pick):
         o, Wi = O.lact_forward_schedule_instance(q[i], k[i], v[i], eta[i], W[0][i], W[1][i], W[2][i], sched)
         assert np.array_equal(got[0][s], o) and all(np.array_equal(got[1 + j][s], Wi[j]) for j in range(3))
+
+
+# ----------------------------------------------------------------------------- backward (linear fast weight)
+
+
+def _torch_linear_layer(q, k, v, eta, W, chunk, order):
+    """The linear fast weight's chunk loop from library ops (torch autograd
+    sees every step): o_t = W q_t, W <- rownorm-preserving (W - g) with
+    g = -sum_t eta_t v_t k_t^T."""
+    n_q, n_kv = q.shape[0], k.shape[0]
+    outs = []
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        if order == 0:
+            outs.append(q[s:e] @ W.T)
+        g = -(v[s:e] * eta[s:e, None]).T @ k[s:e]
+        U = W - g
+        W = U * (torch.linalg.vector_norm(W, dim=1, keepdim=True) / torch.linalg.vector_norm(U, dim=1, keepdim=True))
+        if order == 1:
+            outs.append(q[s:e] @ W.T)
+    if n_q > n_kv:
+        outs.append(q[n_kv:] @ W.T)
+    return torch.cat(outs), W
+
+
+def test_weight_update_vjp_matches_autograd():
+    rng = _rng(101)
+    W, step, dWn = (rng.standard_normal((6, 5)) for _ in range(3))
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    Wt, St = t(W), t(step)
+    U = Wt - St
+    Wn = U * (torch.linalg.vector_norm(Wt, dim=1, keepdim=True) / torch.linalg.vector_norm(U, dim=1, keepdim=True))
+    (Wn * torch.tensor(dWn)).sum().backward()
+    dW, dstep = O.weight_update_vjp(W, step, dWn)
+    assert np.allclose(dW, Wt.grad.numpy(), rtol=1e-11, atol=1e-12)
+    assert np.allclose(dstep, St.grad.numpy(), rtol=1e-11, atol=1e-12)
+
+
+@pytest.mark.parametrize("order,final", [(0, False), (1, False), (0, True), (1, True)])
+def test_linear_backward_matches_autograd(order, final):
+    # several chunks, the last one ragged, and an apply-only tail
+    rng = _rng(102 + order + 2 * final)
+    d, n_kv, n_q, C = 6, 23, 29, 7
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.05 + 0.2 * rng.random(n_kv)
+    W0 = rng.standard_normal((d, d))
+    do = rng.standard_normal((n_q, d))
+    dWf = rng.standard_normal((d, d)) if final else None
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    qt, kt, vt, et, Wt = t(q), t(k), t(v), t(eta), t(W0)
+    o, Wfin = _torch_linear_layer(qt, kt, vt, et, Wt, C, order)
+    loss = (o * torch.tensor(do)).sum() + ((Wfin * torch.tensor(dWf)).sum() if final else 0.0)
+    loss.backward()
+    got = O.lact_backward_linear_instance(q, k, v, eta, W0, do, C, order, dWf)
+    for name, g, ref in zip(("dq", "dk", "dv", "deta", "dW0"), got, (qt, kt, vt, et, Wt)):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-9, atol=1e-11), name
+    # the forward the backward replays is the oracle's own forward
+    o_ref, W_ref = O.lact_forward_linear_instance(q, k, v, eta, W0, C, order)
+    assert np.allclose(o.detach().numpy(), o_ref, rtol=1e-12, atol=1e-13)
+    assert np.allclose(Wfin.detach().numpy(), W_ref, rtol=1e-12, atol=1e-13)
+
+
+def test_linear_backward_finite_differences():
+    # central differences of the NumPy forward oracle on a scalar read-out
+    rng = _rng(107)
+    d, n_kv, n_q, C = 4, 9, 11, 4
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.3 * rng.random(n_kv)
+    W0 = rng.standard_normal((d, d))
+    do, dWf = rng.standard_normal((n_q, d)), rng.standard_normal((d, d))
+    for order in (0, 1):
+        def readout(q_, k_, v_, eta_, W_):
+            o, W = O.lact_forward_linear_instance(q_, k_, v_, eta_, W_, C, order)
+            return float(np.sum(o * do) + np.sum(W * dWf))
+        grads = O.lact_backward_linear_instance(q, k, v, eta, W0, do, C, order, dWf)
+        args = [q, k, v, eta, W0]
+        for which, idx in ((0, (3, 1)), (0, (10, 2)), (1, (2, 0)), (1, (8, 3)), (2, (5, 1)), (3, (6,)), (4, (1, 2))):
+            h = 1e-6
+            plus = [a.copy() for a in args]
+            minus = [a.copy() for a in args]
+            plus[which][idx] += h
+            minus[which][idx] -= h
+            fd = (readout(*plus) - readout(*minus)) / (2 * h)
+            assert abs(fd - grads[which][idx]) <= 1e-6 * max(1.0, abs(fd)), (order, which, idx, fd, grads[which][idx])

@@ -25,7 +25,8 @@
  *
  * Entry points: lact_forward (the path above), lact_forward_momentum (the
  * momentum test-time optimizer, App. A), lact_forward_schedule (a caller-given
- * list of update/apply segments, Alg. 1), lact_prologue and lact_rmsnorm_out
+ * list of update/apply segments, Alg. 1), lact_backward_linear (the reverse of
+ * the linear fast weight's chunk loop), lact_prologue and lact_rmsnorm_out
  * (the layer's steps on either side of the path, Alg. 1); per-matrix learning
  * rates through lact_desc.eta_per_matrix.
  *
@@ -245,6 +246,52 @@ int lact_forward_schedule(const lact_desc* desc,
                           void* stream);
 
 /*
+ * Backward of lact_forward for the linear fast weight (§5.4: f_W(x) = W x,
+ * W in R^{d x d}; chunk loss and gradient of §3.1, g = -sum eta_i v_i k_i^T;
+ * per-row norm-preserving update of §3.2 and Alg. 1). Given the cotangent dO
+ * of the outputs o (and optionally that of the final fast weights), it
+ * returns the cotangents of every input: the reverse of the chunk loop,
+ * with the fast weights of every chunk boundary recomputed from W0 and kept
+ * in the workspace. Per chunk c (W_c before its update, W_{c+1} after):
+ *
+ *   U = W_c - g,  n, u = row norms of W_c, U,  a = <dW_{c+1}, U> per row
+ *   dU = (n / u) dW_{c+1} - (n a / u^3) U,   dW_c = dU + (a / (u n)) W_c
+ *   dv_i = eta_i dU k_i,  dk_i = eta_i dU^T v_i,  deta_i = v_i^T dU k_i
+ *
+ * and the chunk's apply o_i = W q_i adds dO_i q_i^T to the cotangent of the
+ * weight it used (W_c with apply-then-update, W_{c+1} with
+ * update-then-apply; the tail [n_kv, n_q) uses the final weight) and
+ * gives dq_i = W^T dO_i.
+ *
+ * Requires desc->fast_weight == LACT_FW_LINEAR and use_muon == 0 (else
+ * LACT_EUNSUPPORTED); other fields as lact_forward.
+ *
+ *   q, k, v, eta        the forward's inputs (as lact_forward)              in
+ *   W0       [B*H, d, d]   fp32, the fast weight BEFORE the forward           in
+ *   dout     [B*H, n_q, d] io_dtype, cotangent of o                           in
+ *   dW_final [B*H, d, d]   fp32, cotangent of the final fast weight, or NULL
+ *                          (zero)                                             in
+ *   dq       [B*H, n_q, d] io_dtype                                           out
+ *   dk, dv   [B*H, n_kv, d] io_dtype                                          out
+ *   deta     [B*H, n_kv]   fp32                                               out
+ *   dW0      [B*H, d, d]   fp32, cotangent of W0                              out
+ *   workspace   >= lact_backward_workspace_bytes(desc), 256-byte aligned
+ *
+ * Every element of the outputs is written. Pointers are device pointers,
+ * 16-byte aligned (eta and deta: 4); outputs must not alias inputs, each
+ * other or the workspace. Errors as lact_forward (validated before any HIP
+ * call). A zero row norm of W or U gives non-finite values, as in the
+ * forward.
+ */
+size_t lact_backward_workspace_bytes(const lact_desc* desc, int* err);
+int lact_backward_linear(const lact_desc* desc,
+                         const void* q, const void* k, const void* v, const float* eta,
+                         const float* W0, const void* dout, const float* dW_final,
+                         void* dq, void* dk, void* dv, float* deta, float* dW0,
+                         void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/*
  * The layer's steps on either side of the path (Alg. 1, layer), each one pass
  * over HBM. Only B, H, d, n_q, n_kv, io_dtype and eta_per_matrix of `desc`
  * are used (the descriptor must still be valid).
@@ -291,6 +338,9 @@ int lact_rmsnorm_out(const lact_desc* desc, const void* o, const float* weight, 
 #define LACT_KCLASS_PREP 4     /* initial fp32 -> bf16 operand copies; schedule   */
                                /* output rows zeroed                              */
 #define LACT_KCLASS_IO 5       /* lact_prologue and lact_rmsnorm_out              */
+                               /* (lact_backward_linear: its contractions count   */
+                               /* as BWD, its row and token steps as UPDATE, its  */
+                               /* transposed copies as PREP)                      */
 #define LACT_KCLASS_COUNT 6
 int lact_timing_enable(int enable);
 int lact_timing_reset(void);

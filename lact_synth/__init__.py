@@ -27,13 +27,19 @@ Recipe (one (seed, config) -> one set of host arrays):
   float32, from an eighth sub-stream (the factor is the sigmoid of a linear
   projection of the token, App. A; a unit-variance logit stands in for the
   projection), so the other seven draws are the same with or without it.
+
+Cotangents for the backward of the linear fast weight (``make_cotangents``),
+from their own two sub-streams of ``SeedSequence([seed, 1])``: dO ~ N(0, 1/d)
+per element in the shape of q (rounded to bfloat16 for bf16 workloads) and
+the cotangent of the final fast weight ~ N(0, 1/d) per element, float32.
 """
 from __future__ import annotations
 
 import dataclasses
 import numpy as np
 
-__all__ = ["LactConfig", "CONFIGS", "make_inputs", "make_schedule", "round_to_bf16", "bf16_bits"]
+__all__ = ["LactConfig", "CONFIGS", "make_inputs", "make_cotangents", "make_schedule", "round_to_bf16",
+           "bf16_bits"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -168,3 +174,17 @@ def make_inputs(cfg: LactConfig, seed: int = 0, heads: list | None = None):
         zb = rb.standard_normal((n, cfg.n_kv), dtype=np.float32).astype(np.float64)
         out["beta"] = (1.0 / (1.0 + np.exp(-zb))).astype(np.float32)
     return out
+
+
+def make_cotangents(cfg: LactConfig, seed: int = 0, heads: list | None = None):
+    """Seeded cotangents of the linear fast weight's outputs: dict with
+    ``do`` [n, n_q, d] (the I/O precision's values, float32 arrays) and
+    ``dW`` [n, d, d] float32, n = the number of kept instances."""
+    rd, rw = (np.random.default_rng(s) for s in np.random.SeedSequence([seed, 1]).spawn(2))
+    n = cfg.BH if heads is None else len(heads)
+    std = 1.0 / np.sqrt(cfg.d)
+    do = rd.standard_normal((n, cfg.n_q, cfg.d), dtype=np.float32) * np.float32(std)
+    if cfg.io == "bf16":
+        do = round_to_bf16(do)
+    dW = rw.standard_normal((n, cfg.d, cfg.d), dtype=np.float32) * np.float32(std)
+    return dict(do=do, dW=dW)

@@ -68,6 +68,10 @@ def load_library(path: str | None = None):
     L.lact_forward_momentum.restype = i32
     L.lact_forward_schedule.argtypes = [dp, ctypes.POINTER(LactSegment), i64] + [vp] * 13 + [sz, vp]
     L.lact_forward_schedule.restype = i32
+    L.lact_backward_workspace_bytes.argtypes = [dp, ctypes.POINTER(i32)]
+    L.lact_backward_workspace_bytes.restype = sz
+    L.lact_backward_linear.argtypes = [dp] + [vp] * 12 + [vp, sz, vp]
+    L.lact_backward_linear.restype = i32
     f32 = ctypes.c_float
     L.lact_prologue.argtypes = [dp, vp, vp, f32, vp, vp, vp, vp, vp, vp, vp]
     L.lact_prologue.restype = i32
@@ -267,6 +271,46 @@ def forward_linear(q, k, v, eta, W, chunk, order=APPLY_THEN_UPDATE, use_muon=Fal
     if rc:
         _raise(rc)
     return (out, M) if beta is not None else out
+
+
+def backward_workspace_bytes(desc: LactDesc) -> int:
+    err = ctypes.c_int(0)
+    n = lib().lact_backward_workspace_bytes(ctypes.byref(desc), ctypes.byref(err))
+    if err.value:
+        _raise(err.value)
+    return int(n)
+
+
+def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, workspace=None,
+                    stream=None):
+    """Backward of forward_linear (lact_backward_linear): the cotangents of q,
+    k, v, eta and of the initial fast weight W0 [.., d, d] (fp32, not written)
+    given dout (q's shape and dtype) and, optionally, the cotangent of the
+    final fast weight. Returns (dq, dk, dv, deta, dW0)."""
+    import torch
+    if W0.shape[-1] != W0.shape[-2]:
+        raise LactError(-1, "the linear fast weight is square, [.., d, d]")
+    extra = [(dout, "dout")] + ([(dW_final, "dW_final")] if dW_final is not None else [])
+    if dout.shape != q.shape or dout.dtype != q.dtype:
+        raise LactError(-1, "dout must have q's shape and dtype")
+    if dW_final is not None and (dW_final.shape != W0.shape or dW_final.dtype != torch.float32):
+        raise LactError(-1, "dW_final must have W0's shape, fp32")
+    desc, dq, _, stream = _marshal(q, k, v, eta, W0, W0, W0, extra[1:], chunk, order, False, 0, None, None,
+                                   stream, FW_LINEAR, need_workspace=False)
+    if not dout.is_cuda or not dout.is_contiguous():
+        raise LactError(-1, "dout must be a contiguous device tensor")
+    if workspace is None:
+        workspace = torch.empty(max(backward_workspace_bytes(desc), 1), dtype=torch.uint8, device=q.device)
+    dk, dv = torch.empty_like(k), torch.empty_like(v)
+    deta = torch.empty_like(eta)
+    dW0 = torch.empty_like(W0)
+    rc = lib().lact_backward_linear(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(W0), _ptr(dout),
+                                    _ptr(dW_final), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(deta), _ptr(dW0),
+                                    _ptr(workspace), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                                    ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return dq, dk, dv, deta, dW0
 
 
 def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_steps=5, beta=None,

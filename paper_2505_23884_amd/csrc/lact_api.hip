@@ -1080,6 +1080,231 @@ int run_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, 
   return LACT_OK;
 }
 
+// ---------------------------------------------------------------- backward
+// Reverse of the linear fast weight's chunk loop (§5.4 with the §3.1 chunk
+// gradient and the per-row norm-preserving update of §3.2): the fast weights
+// of every chunk boundary are recomputed with the forward's own update and
+// kept; the reverse walks the chunks from the last, carrying the cotangent of
+// the fast weight in dW0. Workspace: the forward's, then W_1 .. W_nch, the
+// split partials of the apply's contribution dO^T Q, and the operand copies
+// of the update's cotangent (row-major and transposed) and of a transposed
+// fast weight.
+struct BwdLayout {
+  Plan p;
+  int64_t nch;         // chunks of the forward
+  int64_t tail_len;    // tokens per piece of the apply-only tail
+  int64_t tail_split;  // tokens per split of a tail piece (at most p.nsplit splits)
+  size_t off_traj, off_apart, off_ub, off_ut, off_wt, total;
+};
+
+int bwd_layout(const lact_desc* dsc, BwdLayout* L) {
+  int rc = check_desc(dsc);
+  if (rc) return rc;
+  if (dsc->fast_weight != LACT_FW_LINEAR || dsc->use_muon) return LACT_EUNSUPPORTED;
+  L->p = make_plan(dsc);
+  const Plan& p = L->p;
+  const double dd = (double)p.d * p.d;
+  L->nch = dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0;
+  // the trajectory holds every chunk's weights: bound it before sizing
+  if ((double)L->nch * p.BH * dd * 4.0 + (double)p.total > 4.0e18) return LACT_EUNSUPPORTED;
+  L->tail_len = std::max<int64_t>(p.C, 8192);
+  L->tail_split = std::max<int64_t>(32, cdiv(cdiv(L->tail_len, p.nsplit), 32) * 32);
+  const size_t w4 = (size_t)p.BH * p.d * p.d * 4, wio = (size_t)p.BH * p.d * p.d * p.esz;
+  size_t o = p.total;
+  L->off_traj = o;
+  o = align_up(o + (size_t)L->nch * w4);
+  L->off_apart = o;
+  o = align_up(o + (size_t)p.nsplit * w4);
+  L->off_ub = o;
+  o = align_up(o + wio);
+  L->off_ut = o;
+  o = align_up(o + wio);
+  L->off_wt = o;
+  o = align_up(o + wio);
+  L->total = o;
+  return LACT_OK;
+}
+
+// One GRAD2 segment: out[m][j] = sum over rows [0, n) of a[., m] b[., j], in
+// splits of split_len tokens (fp32 partials, BH d^2 floats between splits).
+void lin_grad_seg(BwdSeg& g, const Plan& p, Operand a, Operand b, float* out, int64_t n, int64_t split_len) {
+  const TileShape t = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
+  g.kind = BWD_GRAD2;
+  g.tiles_m = (int)cdiv(p.d, t.rows);
+  g.tiles_n = (int)cdiv(p.d, t.cols);
+  g.nsplit = (int)std::max<int64_t>(1, cdiv(n, split_len));
+  g.nblocks = p.BH * g.tiles_m * g.tiles_n * g.nsplit;
+  g.rows = n;
+  g.split_len = split_len;
+  g.a0 = a;
+  g.b0 = b;
+  g.out = out;
+  g.out_inst = (int64_t)p.d * p.d;
+  g.out_split = (int64_t)p.BH * p.d * p.d;
+  g.out_off = 0;
+}
+
+// One OUT segment: out[t][m] = sum_e a[t][e] b[m][e] for rows t in [0, n)
+// (rows of out d apart, instances out_inst apart).
+void lin_out_seg(BwdSeg& o, const Plan& p, Operand a, Operand b, void* out, int64_t out_inst, int64_t n) {
+  const TileShape t = bwd_tile(BWD_OUT, p.bf16, p.narrow);
+  o.kind = BWD_OUT;
+  o.tiles_m = (int)cdiv(p.d, t.rows);
+  o.tiles_n = (int)cdiv(n, t.cols);
+  o.nsplit = 1;
+  o.nblocks = p.BH * o.tiles_m * o.tiles_n;
+  o.rows = n;
+  o.a0 = a;
+  o.b0 = b;
+  o.out = out;
+  o.out_inst = out_inst;
+}
+
+int lin_launch(Ctx& c, BwdArgs& b, int nseg, double flops) {
+  b.nseg = nseg;
+  b.total_blocks = 0;
+  for (int i = 0; i < nseg; ++i) b.total_blocks += b.seg[i].nblocks;
+  b.d = c.p.d;
+  b.h = c.p.d;
+  b.narrow = c.p.narrow;
+  return timed(LACT_KCLASS_BWD, flops, c.s, [&] { return launch_bwd(b, c.p.bf16, c.s); });
+}
+
+int run_backward_linear(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                        const float* W0, const void* dout, const float* dWf, void* dq, void* dk, void* dv,
+                        float* deta, float* dW0, void* workspace, size_t workspace_bytes, void* stream) {
+  BwdLayout L;
+  int rc = bwd_layout(desc, &L);
+  if (rc) return rc;
+  const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
+  if (!W0 || !dW0) return LACT_EINVAL;
+  if (any_q && (!q || !dout || !dq)) return LACT_EINVAL;
+  if (any_kv && (!k || !v || !eta || !dk || !dv || !deta)) return LACT_EINVAL;
+  if (misaligned(W0) || misaligned(dW0) || (dWf && misaligned(dWf))) return LACT_EALIGN;
+  if (any_q && (misaligned(q) || misaligned(dout) || misaligned(dq))) return LACT_EALIGN;
+  if (any_kv && (misaligned(k) || misaligned(v) || misaligned(dk) || misaligned(dv))) return LACT_EALIGN;
+  if (any_kv && (((uintptr_t)eta & 3) || ((uintptr_t)deta & 3))) return LACT_EALIGN;
+  if (!workspace || workspace_bytes < L.total) return LACT_EWORKSPACE;
+  Ctx c;
+  // the forward's context over the same inputs; W1 is pointed at each
+  // trajectory slot before its update, so W0 itself is never written
+  rc = setup(c, desc, q, k, v, eta, nullptr, const_cast<float*>(W0), nullptr, nullptr, nullptr, dq, workspace,
+             workspace_bytes, stream);
+  if (rc) return rc;
+  const Plan& p = c.p;
+  if (p.bf16) {   // the update also writes operand copies (not read here)
+    for (int m = 0; m < 3; ++m) {
+      c.wb[0][m] = c.ws + p.off_wb[m];
+      c.wb[1][m] = c.ws + p.off_wb2[m];
+    }
+    use_wset(c, 0);
+  }
+  const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk, d = p.d, BH = p.BH;
+  const int64_t dd = d * d, esz = p.esz;
+  const size_t w4 = (size_t)BH * dd * 4;
+  auto traj = [&](int64_t i) -> float* {
+    return i == 0 ? const_cast<float*>(W0) : reinterpret_cast<float*>(c.ws + L.off_traj + (size_t)(i - 1) * w4);
+  };
+  // forward: the weights after every chunk
+  for (int64_t ci = 0; ci < L.nch; ++ci) {
+    const int64_t s0 = ci * C, s1 = std::min(n_kv, s0 + C);
+    rc = timed(LACT_KCLASS_PREP, 0.0, c.s,
+               [&] { return hipMemcpyAsync(traj(ci + 1), traj(ci), w4, hipMemcpyDeviceToDevice, c.s); });
+    if (rc) return rc;
+    c.W[0] = traj(ci + 1);
+    c.chunk_idx = ci;
+    rc = update_chunk_linear(c, s0, s1, false);
+    if (rc) return rc;
+  }
+  float* G = dW0;
+  float* apart = reinterpret_cast<float*>(c.ws + L.off_apart);
+  float* part = reinterpret_cast<float*>(c.ws + p.off_step);
+  uint8_t* ub = c.ws + L.off_ub;
+  uint8_t* ut = c.ws + L.off_ut;
+  uint8_t* wt = c.ws + L.off_wt;
+  const int64_t psplit = BH * dd;
+  const uint8_t* qb = (const uint8_t*)q;
+  const uint8_t* kb = (const uint8_t*)k;
+  const uint8_t* vb = (const uint8_t*)v;
+  const uint8_t* ob = (const uint8_t*)dout;
+  int64_t wt_of = -1;   // trajectory index whose transposed copy wt holds
+  auto make_wt = [&](int64_t i) -> int {
+    if (wt_of == i) return LACT_OK;
+    wt_of = i;
+    return timed(LACT_KCLASS_PREP, 0.0, c.s,
+                 [&] { return launch_transpose_cvt(traj(i), wt, p.BH, p.d, p.bf16, c.s); });
+  };
+  const Operand wt_op = op(wt, d, dd);
+  // tail [n_kv, n_q): applied with the final weight; its dO^T Q joins the
+  // cotangent of that weight (dW_final, or zero)
+  bool first = true;
+  if (any_q && n_q > n_kv) {
+    rc = make_wt(L.nch);
+    if (rc) return rc;
+    for (int64_t a = n_kv; a < n_q; a += L.tail_len) {
+      const int64_t n = std::min(L.tail_len, n_q - a);
+      BwdArgs b{};
+      lin_grad_seg(b.seg[0], p, op(ob + a * d * esz, d, n_q * d), op(qb + a * d * esz, d, n_q * d), apart, n,
+                   L.tail_split);
+      lin_out_seg(b.seg[1], p, op(ob + a * d * esz, d, n_q * d), wt_op, (uint8_t*)dq + a * d * esz, n_q * d, n);
+      rc = lin_launch(c, b, 2, 4.0 * BH * n * dd);
+      if (rc) return rc;
+      const int mode = first ? (dWf ? 1 : 0) : 2;
+      const int ns = b.seg[0].nsplit;
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s,
+                 [&] { return launch_sum_parts(G, dWf, mode, apart, ns, psplit, BH * dd, c.s); });
+      if (rc) return rc;
+      first = false;
+    }
+  }
+  if (first) {
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s,
+               [&] { return launch_sum_parts(G, dWf, dWf ? 1 : 0, nullptr, 0, psplit, BH * dd, c.s); });
+    if (rc) return rc;
+  }
+  const bool then_apply = desc->order == LACT_UPDATE_THEN_APPLY;
+  const uint8_t* ek = c.ws + p.off_upd[0];   // eta k of the chunk, [BH][C][d]
+  for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
+    const int64_t s0 = ci * C, s1 = std::min(n_kv, s0 + C), n = s1 - s0;
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] {
+      return launch_scale_rows(kb + s0 * d * esz, eta + s0, c.ws + p.off_upd[0], p.BH, n, p.d, n_kv * d, n_kv,
+                               p.C * d, p.bf16, c.s);
+    });
+    if (rc) return rc;
+    // the chunk's apply used W_{c+1} (update-then-apply) or W_c
+    rc = make_wt(then_apply ? ci + 1 : ci);
+    if (rc) return rc;
+    const Operand vo = op(vb + s0 * d * esz, d, n_kv * d), eko = op(ek, d, p.C * d);
+    const Operand doo = op(ob + s0 * d * esz, d, n_q * d), qo = op(qb + s0 * d * esz, d, n_q * d);
+    {
+      BwdArgs b{};
+      lin_grad_seg(b.seg[0], p, vo, eko, part, n, p.split_len);    // P = sum eta v k^T (= -g)
+      lin_grad_seg(b.seg[1], p, doo, qo, apart, n, p.split_len);   // dO^T Q
+      lin_out_seg(b.seg[2], p, doo, wt_op, (uint8_t*)dq + s0 * d * esz, n_q * d, n);   // dq = dO W
+      rc = lin_launch(c, b, 3, 6.0 * BH * n * dd);
+      if (rc) return rc;
+    }
+    const int ns = (int)std::max<int64_t>(1, cdiv(n, p.split_len));
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] {
+      return launch_lin_vjp(traj(ci), part, apart, ns, psplit, then_apply, G, ub, ut, p.BH, p.d, p.bf16, c.s);
+    });
+    if (rc) return rc;
+    {
+      BwdArgs b{};
+      lin_out_seg(b.seg[0], p, eko, op(ub, d, dd), (uint8_t*)dv + s0 * d * esz, n_kv * d, n);   // dv = eta k Uh^T
+      lin_out_seg(b.seg[1], p, vo, op(ut, d, dd), (uint8_t*)dk + s0 * d * esz, n_kv * d, n);    // Z = v Uh
+      rc = lin_launch(c, b, 2, 4.0 * BH * n * dd);
+      if (rc) return rc;
+    }
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] {
+      return launch_lin_tokens(kb + s0 * d * esz, eta + s0, (uint8_t*)dk + s0 * d * esz, deta + s0, p.BH, n, p.d,
+                               n_kv * d, n_kv * d, n_kv, p.bf16, c.s);
+    });
+    if (rc) return rc;
+  }
+  return LACT_OK;
+}
+
 }  // namespace
 }  // namespace lact
 
@@ -1101,6 +1326,20 @@ int lact_forward(const lact_desc* desc, const void* q, const void* k, const void
                  void* stream) {
   return run_forward(desc, q, k, v, eta, nullptr, W1, W2, W3, nullptr, o, workspace, workspace_bytes,
                      stream);
+}
+
+size_t lact_backward_workspace_bytes(const lact_desc* desc, int* err) {
+  BwdLayout L;
+  const int rc = bwd_layout(desc, &L);
+  if (err) *err = rc;
+  return rc ? 0 : L.total;
+}
+
+int lact_backward_linear(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                         const float* W0, const void* dout, const float* dW_final, void* dq, void* dk, void* dv,
+                         float* deta, float* dW0, void* workspace, size_t workspace_bytes, void* stream) {
+  return run_backward_linear(desc, q, k, v, eta, W0, dout, dW_final, dq, dk, dv, deta, dW0, workspace,
+                             workspace_bytes, stream);
 }
 
 int lact_forward_noalloc(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,

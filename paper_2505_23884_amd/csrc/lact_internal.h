@@ -284,6 +284,14 @@ hipError_t launch_ns_fused_pair_out(const NsFusedArgs& a0, const NsFusedArgs& a1
 hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s);
 // Zero rows [r0, r1) of every instance of an output of `rows` rows of row_bytes
 // (a multiple of 16) each.
+// Reverse of the linear fast weight's chunk loop (see lact_kernels.hip).
+hipError_t launch_lin_vjp(const float* W, const float* P, const float* A, int nsplit, int64_t psplit, bool a_first,
+                          float* G, void* Ub, void* UT, int BH, int d, bool io_bf16, hipStream_t s);
+hipError_t launch_transpose_cvt(const float* W, void* WT, int BH, int d, bool io_bf16, hipStream_t s);
+hipError_t launch_lin_tokens(const void* K, const float* eta, void* dk, float* deta, int BH, int64_t n, int d,
+                             int64_t k_inst, int64_t z_inst, int64_t eta_inst, bool io_bf16, hipStream_t s);
+hipError_t launch_sum_parts(float* G, const float* init, int mode, const float* P, int nsplit, int64_t psplit,
+                            int64_t n, hipStream_t s);
 hipError_t launch_zero_rows(void* out, int BH, int64_t row_bytes, int64_t rows, int64_t r0, int64_t r1,
                             hipStream_t s);
 constexpr int kNsBlockElems = 4096;

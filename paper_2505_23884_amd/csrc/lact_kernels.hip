@@ -2253,6 +2253,154 @@ __global__ __launch_bounds__(256) void k_beta_mean(const BetaArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Reverse of the linear fast weight's chunk loop (§5.4 with the §3.1 loss and
+// norm-preserving update): the contractions run on the OUT and GRAD2 kinds;
+// these kernels are the row-wise and token-wise steps between them.
+
+// Reverse of W' = (n / u) U, U = W + P (P = sum of the split partials of
+// sum_t eta_t v_t k_t^T, the negated chunk gradient): one wave per row of the
+// d x d matrix. From the cotangent G of W' (in place), with a = G . U per row:
+//   Uh = (n / u) G - (n a / u^3) U,   G <- Uh + (a / (u n)) W,
+// and Uh (the cotangent of U, i.e. minus that of the gradient) in the
+// operand type, row-major into Ub and transposed into UT. The apply's own
+// contribution (the nsplit partials A, same split stride as P) joins G
+// before the reverse when a_first (the chunk was applied with W'), after it
+// otherwise (applied with W). A zero row norm gives the same non-finite
+// values as the forward's division.
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void k_lin_vjp(const float* W, const float* P, const float* A, int nsplit,
+                                                 int64_t psplit, int a_first, float* G, T* Ub, T* UT, int BH, int d) {
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (wave >= BH * d) return;
+  const int inst = wave / d, r = wave - inst * d;
+  const int64_t dd = (int64_t)d * d, off = inst * dd + (int64_t)r * d;
+  const int nv = d >> 2;
+  const float4* w4 = reinterpret_cast<const float4*>(W + off);
+  const float4* p4 = reinterpret_cast<const float4*>(P + off);
+  const float4* a4 = reinterpret_cast<const float4*>(A + off);
+  float4* g4 = reinterpret_cast<float4*>(G + off);
+  const int64_t ps = psplit >> 2;
+  float4 w[NV], u[NV], g[NV], ap[NV];
+  float sw = 0.f, su = 0.f, sa = 0.f;
+#pragma unroll
+  for (int t = 0; t < NV; ++t) {
+    const int i = lane + 64 * t;
+    const bool in = i < nv;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    w[t] = in ? w4[i] : z;
+    g[t] = in ? g4[i] : z;
+    float4 acc = w[t], aa = z;
+    for (int sp = 0; sp < nsplit && in; ++sp) {
+      const float4 q = p4[sp * ps + i];
+      acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
+      const float4 e = a4[sp * ps + i];
+      aa.x += e.x; aa.y += e.y; aa.z += e.z; aa.w += e.w;
+    }
+    u[t] = acc;
+    if (a_first) {
+      g[t].x += aa.x; g[t].y += aa.y; g[t].z += aa.z; g[t].w += aa.w;
+      aa = z;
+    }
+    ap[t] = aa;
+    sw += w[t].x * w[t].x + w[t].y * w[t].y + w[t].z * w[t].z + w[t].w * w[t].w;
+    su += u[t].x * u[t].x + u[t].y * u[t].y + u[t].z * u[t].z + u[t].w * u[t].w;
+    sa += g[t].x * u[t].x + g[t].y * u[t].y + g[t].z * u[t].z + g[t].w * u[t].w;
+  }
+  sw = wave_sum(sw);
+  su = wave_sum(su);
+  sa = wave_sum(sa);
+  const float n = sqrtf(sw), uu = sqrtf(su);
+  const float c1 = n / uu, c2 = n * sa / (uu * uu * uu), c3 = sa / (uu * n);
+#pragma unroll
+  for (int t = 0; t < NV; ++t) {
+    const int i = lane + 64 * t;
+    if (i >= nv) continue;
+    const float4 uh = make_float4(c1 * g[t].x - c2 * u[t].x, c1 * g[t].y - c2 * u[t].y, c1 * g[t].z - c2 * u[t].z,
+                                  c1 * g[t].w - c2 * u[t].w);
+    g4[i] = make_float4(uh.x + c3 * w[t].x + ap[t].x, uh.y + c3 * w[t].y + ap[t].y, uh.z + c3 * w[t].z + ap[t].z,
+                        uh.w + c3 * w[t].w + ap[t].w);
+    st4<T>(Ub, off + 4 * i, uh.x, uh.y, uh.z, uh.w);
+    const int64_t col = inst * dd + (int64_t)(4 * i) * d + r;   // UT[e][r] for e = 4i .. 4i+3
+    UT[col] = (T)uh.x;
+    UT[col + d] = (T)uh.y;
+    UT[col + 2 * d] = (T)uh.z;
+    UT[col + 3 * d] = (T)uh.w;
+  }
+}
+
+// Transposed operand copy: WT[i][e][f] = W[i][f][e] (fp32 -> operand type),
+// 32 x 32 tiles through LDS so that both sides move whole rows; one block per
+// (instance, tile) in a flat grid.
+template <typename T>
+__global__ __launch_bounds__(256) void k_transpose_cvt(const float* W, T* WT, int d, int tiles) {
+  __shared__ float tile[32][33];
+  const int64_t dd = (int64_t)d * d;
+  const int64_t per = (int64_t)tiles * tiles;
+  const int64_t inst = blockIdx.x / per;
+  const int rest = (int)(blockIdx.x - inst * per);
+  const float* src = W + inst * dd;
+  T* dst = WT + inst * dd;
+  const int r0 = (rest / tiles) * 32, c0 = (rest % tiles) * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int k = ty; k < 32; k += 8) {
+    const int r = r0 + k, c = c0 + tx;
+    tile[k][tx] = (r < d && c < d) ? src[(int64_t)r * d + c] : 0.0f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int r = c0 + k, c = r0 + tx;   // output row = input column
+    if (r < d && c < d) dst[(int64_t)r * d + c] = (T)tile[tx][k];
+  }
+}
+
+// Token step of the reverse, one wave per key token t of a chunk (grid
+// stride over BH x n tokens). On entry dk holds Z = V Uh (rows t); with it
+// dk_t = eta_t Z_t and deta_t = k_t . Z_t (= v_t^T Uh k_t).
+template <typename T>
+__global__ __launch_bounds__(256) void k_lin_tokens(const T* K, const float* eta, T* dk, float* deta, int BH,
+                                                    int64_t n, int d, int64_t k_inst, int64_t z_inst,
+                                                    int64_t eta_inst) {
+  const int lane = threadIdx.x & 63;
+  const int64_t total = (int64_t)BH * n;
+  for (int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wave < total; wave += (int64_t)gridDim.x * 4) {
+    const int64_t inst = wave / n, t = wave - inst * n;
+    const int64_t ko = inst * k_inst + t * d, zo = inst * z_inst + t * d;
+    const float e = eta[inst * eta_inst + t];
+    float dot = 0.0f;
+    for (int c = 4 * lane; c < d; c += 256) {
+      float z[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        z[q] = (float)dk[zo + c + q];
+        dot += (float)K[ko + c + q] * z[q];
+      }
+      st4<T>(dk, zo + c, e * z[0], e * z[1], e * z[2], e * z[3]);
+    }
+    dot = wave_sum(dot);
+    if (lane == 0) deta[inst * eta_inst + t] = dot;
+  }
+}
+
+// G = base + sum of nsplit partials (stride psplit floats) over n floats (a
+// multiple of 4); base is zero (mode 0), init (mode 1) or G itself (mode 2).
+__global__ __launch_bounds__(256) void k_sum_parts(float* G, const float* init, int mode, const float* P, int nsplit,
+                                                   int64_t psplit, int64_t n) {
+  const int64_t n4 = n >> 2, ps = psplit >> 2;
+  float4* g4 = reinterpret_cast<float4*>(G);
+  const float4* i4 = reinterpret_cast<const float4*>(init);
+  const float4* p4 = reinterpret_cast<const float4*>(P);
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    float4 a = mode == 0 ? make_float4(0.f, 0.f, 0.f, 0.f) : (mode == 1 ? i4[i] : g4[i]);
+    for (int sp = 0; sp < nsplit; ++sp) {
+      const float4 q = p4[sp * ps + i];
+      a.x += q.x; a.y += q.y; a.z += q.z; a.w += q.w;
+    }
+    g4[i] = a;
+  }
+}
+
 // Rows [r0, r1) of every instance of a row-major [BH, n, d] output set to zero
 // (tokens that no apply segment of a schedule covers): nvec 16-byte vectors
 // per instance, grid-stride over all instances.
@@ -2438,6 +2586,66 @@ hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d
   if (blocks <= 0) return hipSuccess;
   k_prep<<<(unsigned)blocks, 256, 0, s>>>(W[0], W[1], W[2], reinterpret_cast<__bf16*>(Wb[0]),
                                          reinterpret_cast<__bf16*>(Wb[1]), reinterpret_cast<__bf16*>(Wb[2]), n4);
+  return hipGetLastError();
+}
+
+// Reverse of the linear fast weight's chunk loop: the steps between the
+// OUT / GRAD2 contractions (io_bf16 selects bf16 operand copies, else fp32).
+hipError_t launch_lin_vjp(const float* W, const float* P, const float* A, int nsplit, int64_t psplit, bool a_first,
+                          float* G, void* Ub, void* UT, int BH, int d, bool io_bf16, hipStream_t s) {
+  const int64_t rows = (int64_t)BH * d;
+  if (rows <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((rows + 3) / 4);
+  const int per_lane = (d / 4 + 63) / 64;
+  auto go = [&](auto tag, auto nvc) {
+    using T = decltype(tag);
+    constexpr int NV = decltype(nvc)::value;
+    k_lin_vjp<T, NV><<<blocks, 256, 0, s>>>(W, P, A, nsplit, psplit, a_first ? 1 : 0, G, reinterpret_cast<T*>(Ub),
+                                            reinterpret_cast<T*>(UT), BH, d);
+  };
+  auto pick = [&](auto tag) {
+    if (per_lane <= 1) go(tag, std::integral_constant<int, 1>{});
+    else if (per_lane <= 2) go(tag, std::integral_constant<int, 2>{});
+    else if (per_lane <= 4) go(tag, std::integral_constant<int, 4>{});
+    else if (per_lane <= 8) go(tag, std::integral_constant<int, 8>{});
+    else go(tag, std::integral_constant<int, 16>{});
+  };
+  if (io_bf16) pick(__bf16{});
+  else pick(float{});
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_cvt(const float* W, void* WT, int BH, int d, bool io_bf16, hipStream_t s) {
+  if (BH <= 0 || d <= 0) return hipSuccess;
+  const int tiles = (d + 31) / 32;
+  // the descriptor check keeps B*H*ceil(d/128)^2 under 2^24, so this stays under 2^28
+  const unsigned blocks = (unsigned)((int64_t)BH * tiles * tiles);
+  if (io_bf16) k_transpose_cvt<__bf16><<<blocks, 256, 0, s>>>(W, reinterpret_cast<__bf16*>(WT), d, tiles);
+  else k_transpose_cvt<float><<<blocks, 256, 0, s>>>(W, reinterpret_cast<float*>(WT), d, tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_lin_tokens(const void* K, const float* eta, void* dk, float* deta, int BH, int64_t n, int d,
+                             int64_t k_inst, int64_t z_inst, int64_t eta_inst, bool io_bf16, hipStream_t s) {
+  const int64_t rows = (int64_t)BH * n;
+  if (rows <= 0) return hipSuccess;
+  const int64_t need = (rows + 3) / 4;
+  const unsigned blocks = (unsigned)(need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20));
+  if (io_bf16)
+    k_lin_tokens<__bf16><<<blocks, 256, 0, s>>>(reinterpret_cast<const __bf16*>(K), eta, reinterpret_cast<__bf16*>(dk),
+                                                deta, BH, n, d, k_inst, z_inst, eta_inst);
+  else
+    k_lin_tokens<float><<<blocks, 256, 0, s>>>(reinterpret_cast<const float*>(K), eta, reinterpret_cast<float*>(dk),
+                                               deta, BH, n, d, k_inst, z_inst, eta_inst);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_parts(float* G, const float* init, int mode, const float* P, int nsplit, int64_t psplit,
+                            int64_t n, hipStream_t s) {
+  const int64_t need = (n / 4 + 255) / 256;
+  if (need <= 0) return hipSuccess;
+  const int64_t blocks = need < 4096 ? need : 4096;
+  k_sum_parts<<<(unsigned)blocks, 256, 0, s>>>(G, init, mode, P, nsplit, psplit, n);
   return hipGetLastError();
 }
 

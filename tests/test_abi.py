@@ -236,3 +236,43 @@ def test_noalloc_errors_before_any_hip_call():
     # one LM sequence (B = 1, H = 4) fits, with Muon too
     one = make_desc(**dict(lm, B=1, use_muon=True))
     assert P.workspace_bytes(one) <= P.binding.NOALLOC_SCRATCH_BYTES
+
+
+def _bwd(desc, nbytes=None, **kw):
+    a = dict(q=0x1000, k=0x2000, v=0x3000, eta=0x4000, w0=0x5000, do=0x6000, dwf=0, dq=0x7000, dk=0x8000,
+             dv=0x9000, deta=0xA000, dw0=0xB000, ws=0x10000)
+    a.update(kw)
+    if nbytes is None:
+        err = ctypes.c_int(0)
+        nbytes = P.lib().lact_backward_workspace_bytes(ctypes.byref(desc), ctypes.byref(err))
+    vp = ctypes.c_void_p
+    return P.lib().lact_backward_linear(ctypes.byref(desc), *(vp(a[n]) for n in (
+        "q", "k", "v", "eta", "w0", "do", "dwf", "dq", "dk", "dv", "deta", "dw0", "ws")), ctypes.c_size_t(nbytes), vp(0))
+
+
+def test_backward_errors_before_any_hip_call():
+    lin = dict(GOOD, h=64, fast_weight=1)
+    d = make_desc(**lin)
+    assert P.binding.backward_workspace_bytes(d) > P.workspace_bytes(d)
+    # the linear fast weight without Muon only
+    for bad in (dict(GOOD), dict(lin, use_muon=True)):
+        err = ctypes.c_int(0)
+        assert P.lib().lact_backward_workspace_bytes(ctypes.byref(make_desc(**bad)), ctypes.byref(err)) == 0
+        assert err.value == -4
+        assert _bwd(make_desc(**bad), nbytes=1 << 30) == -4
+    assert _bwd(make_desc(**dict(lin, d=12, h=12)), nbytes=1 << 30) == -4
+    assert _bwd(d, q=0) == -1
+    assert _bwd(d, do=0) == -1
+    assert _bwd(d, dw0=0) == -1
+    assert _bwd(d, deta=0) == -1
+    assert _bwd(d, w0=0x5008) == -2
+    assert _bwd(d, dwf=0x5008) == -2       # dW_final, when given, is aligned too
+    assert _bwd(d, deta=0xA002) == -2
+    assert _bwd(d, ws=0) == -3
+    assert _bwd(d, nbytes=P.binding.backward_workspace_bytes(d) - 1) == -3
+    # no key tokens: k, v, eta and their cotangents may be NULL (reaches the workspace check)
+    nk = make_desc(**dict(lin, n_kv=0))
+    assert _bwd(nk, k=0, v=0, eta=0, dk=0, dv=0, deta=0, ws=0) == -3
+    # the workspace keeps the weights of every chunk boundary: it grows with the chunk count
+    more = make_desc(**dict(lin, chunk=128))
+    assert P.binding.backward_workspace_bytes(more) > P.binding.backward_workspace_bytes(d)

@@ -16,7 +16,7 @@ import pytest
 import torch
 
 import paper_2505_23884_amd as P
-from lact_synth import CONFIGS, make_inputs
+from lact_synth import CONFIGS, make_cotangents, make_inputs
 from oracle import lact_oracle as O
 
 pytestmark = pytest.mark.gpu
@@ -1300,6 +1300,113 @@ def test_linear_eta_zero_is_a_plain_product():
     o, W = run_gpu_linear(cfg, x)
     assert np.array_equal(W, x["W1"])
     assert rel(o, np.einsum("bnd,bed->bne", x["q"].astype(np.float64), x["W1"].astype(np.float64))) <= TOL["bf16"]
+
+
+# ----------------------------------------------------------------------------- linear backward
+# lact_backward_linear: the reverse of the linear fast weight's chunk loop
+# against the oracle's reverse (pinned to autograd and finite differences).
+
+
+def run_gpu_linear_bwd(cfg, x, ct, with_dW=True):
+    print(f"[gpu] linear backward {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} n_kv={cfg.n_kv} n_q={cfg.n_q} "
+          f"C={cfg.chunk} order={cfg.order} io={cfg.io} dW_final={with_dW}", flush=True)
+    n = len(x["q"])
+    B, H = (cfg.B, cfg.H) if n == cfg.BH else (n, 1)
+    sh = lambda a: a.reshape(B, H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    W0 = to_dev(sh(x["W1"]), cfg, torch.float32)
+    do = to_dev(sh(ct["do"]), cfg)
+    dWf = to_dev(sh(ct["dW"]), cfg, torch.float32) if with_dW else None
+    W_in = W0.clone()
+    r = P.backward_linear(q, k, v, eta, W0, do, cfg.chunk, order=cfg.order, dW_final=dWf)
+    torch.cuda.synchronize()
+    assert torch.equal(W0, W_in)   # W0 is read only
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    return tuple(f(t) for t in r)
+
+
+def check_linear_bwd(cfg, x, ct, got, with_dW=True, instances=None):
+    idx = slice(None) if instances is None else list(instances)
+    sel = lambda a: a if instances is None else a[list(instances)]
+    ref = O.lact_backward_linear(sel(x["q"]), sel(x["k"]), sel(x["v"]), sel(x["eta"]), sel(x["W1"]), sel(ct["do"]),
+                                 cfg.chunk, cfg.order, dW_final=sel(ct["dW"]) if with_dW else None)
+    errs, blocks = {}, {}
+    for name, g, r in zip(("dq", "dk", "dv", "deta", "dW0"), got, ref):
+        g = g[idx]
+        if g.size == 0:
+            continue
+        errs[name] = rel(g, r)
+        if name == "deta":
+            # deta_t = k_t . Z_t (Z = V dU) is a dot product that can cancel:
+            # per token its error is bounded by |k_t| |Z_t| times the operands'
+            # rounding, not by |deta_t| (|Z_t| = |dk_t| / eta_t from the oracle)
+            zn = np.linalg.norm(ref[1], axis=-1) / sel(x["eta"]).astype(np.float64)
+            kn = np.linalg.norm(sel(x["k"]).astype(np.float64), axis=-1)
+            errs["deta/(|k||Z|)"] = float(np.max(np.abs(g - ref[3]) / (kn * zn)))
+            continue
+        blocks[name] = worst_block(g, r, W_BLOCK if name == "dW0" else O_BLOCK)
+    assert_errs(errs, TOL[cfg.io], blocks)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_linear_backward_bf16_ragged(order):
+    # three chunks (the last partial) and a tail, several 128-tiles per matrix
+    cfg = CONFIGS["lm32k"].with_(name="linear_bwd", B=1, H=2, d=256, h=256, n_kv=700, n_q=760, chunk=256,
+                                 order=order, linear=1)
+    x, ct = make_inputs(cfg, 61), make_cotangents(cfg, 61)
+    check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct))
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_linear_backward_fp32_small(order):
+    # fp32 I/O, dims that are not a multiple of the tile, no final cotangent
+    cfg = CONFIGS["tiny_fp32"].with_(name="linear_bwd_fp32", B=2, H=1, d=40, h=40, n_kv=300, n_q=333, chunk=100,
+                                     order=order, linear=1)
+    x, ct = make_inputs(cfg, 62), make_cotangents(cfg, 62)
+    check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct, with_dW=False), with_dW=False)
+
+
+def test_linear_backward_narrow_tiles_without_tail():
+    # d = 128 (the narrow bf16 tiles), n_q == n_kv, one chunk of a single token at the end
+    cfg = CONFIGS["lm32k"].with_(name="linear_bwd_narrow", B=2, H=2, d=128, h=128, n_kv=513, n_q=513, chunk=128,
+                                 order=0, linear=1)
+    x, ct = make_inputs(cfg, 63), make_cotangents(cfg, 63)
+    check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct))
+
+
+def test_linear_backward_apply_only():
+    # no key tokens: dq = dO W0^T-side product, dW0 = dW_final + dO^T Q over a
+    # tail of several pieces (pieces of 8192 tokens)
+    cfg = CONFIGS["lm32k"].with_(name="linear_bwd_apply_only", B=1, H=1, d=64, h=64, n_kv=0, n_q=20000, chunk=256,
+                                 order=1, linear=1)
+    x, ct = make_inputs(cfg, 64), make_cotangents(cfg, 64)
+    check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct))
+
+
+def test_linear_backward_lm_shape_sampled_instances():
+    # one LM sequence with the linear fast weight (4 heads, d = 512, 16 chunks of 2048)
+    cfg = CONFIGS["lm32k"].with_(name="linear_bwd_lm32k_b1", B=1, linear=1)
+    x, ct = make_inputs(cfg, 65), make_cotangents(cfg, 65)
+    got = run_gpu_linear_bwd(cfg, x, ct)
+    check_linear_bwd(cfg, x, ct, got, instances=[0, 3])
+
+
+def test_linear_backward_nvs_shape_reduced_context():
+    # d = 768, one update-then-apply chunk of 8192 tokens plus 2048 target tokens
+    cfg = CONFIGS["nvs256k_linear"].with_(name="nvs8k_linear_bwd", n_kv=8192, n_q=8192 + 2048, chunk=8192)
+    x, ct = make_inputs(cfg, 66), make_cotangents(cfg, 66)
+    check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct))
+
+
+def test_linear_backward_repeats_bitwise():
+    cfg = CONFIGS["lm32k"].with_(name="linear_bwd_repeat", B=1, H=2, d=256, h=256, n_kv=600, n_q=640, chunk=256,
+                                 order=1, linear=1)
+    x, ct = make_inputs(cfg, 67), make_cotangents(cfg, 67)
+    a = run_gpu_linear_bwd(cfg, x, ct)
+    b = run_gpu_linear_bwd(cfg, x, ct)
+    for u, w in zip(a, b):
+        assert np.array_equal(u, w)
 
 
 # ----------------------------------------------------------------------------- envelope limits

@@ -1,7 +1,7 @@
 """The seeded input generator: shapes, determinism, bf16 exactness, unit norms."""
 import numpy as np
 
-from lact_synth import CONFIGS, bf16_bits, make_inputs, round_to_bf16
+from lact_synth import CONFIGS, bf16_bits, make_cotangents, make_inputs, round_to_bf16
 
 
 def test_bf16_rounding_is_rne():
@@ -53,3 +53,15 @@ def test_momentum_factor_draw():
     assert np.all((a["beta"] > 0) & (a["beta"] < 1)) and abs(a["beta"].mean() - 0.5) < 0.02
     for key in b:                       # the other draws do not move
         assert np.array_equal(a[key], b[key])
+
+
+def test_cotangent_draw():
+    cfg = CONFIGS["lm32k"].with_(name="ct", B=1, H=2, d=64, h=64, n_kv=100, n_q=130, chunk=64, linear=1)
+    a, b = make_cotangents(cfg, 5), make_cotangents(cfg, 5)
+    assert a["do"].shape == (2, 130, 64) and a["dW"].shape == (2, 64, 64)
+    assert np.array_equal(a["do"], b["do"]) and np.array_equal(a["dW"], b["dW"])
+    assert np.array_equal(round_to_bf16(a["do"]), a["do"])
+    assert not np.array_equal(make_cotangents(cfg, 6)["do"], a["do"])
+    # the forward's inputs do not move when cotangents are drawn
+    assert np.array_equal(make_inputs(cfg, 5)["q"], make_inputs(cfg, 5)["q"])
+    assert abs(float(np.std(a["do"])) * 8.0 - 1.0) < 0.05

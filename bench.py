@@ -32,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "LaCT layer fwd TFLOP/s + tokens/s at 32K ctx; % of bf16 MFMA peak"
+METRIC_BWD = "LaCT linear fast-weight backward TFLOP/s + tokens/s; % of bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
@@ -61,6 +62,8 @@ def parse():
                     help="skip the 1M-token NVS workload measured after the default one")
     ap.add_argument("--device-inputs", action="store_true",
                     help="draw the inputs on the device (plain uniform-chunk workloads)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the linear fast weight's backward (lact_backward_linear) on a linear workload")
     ap.add_argument("--traffic-report", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"))
     return ap.parse_args()
 
@@ -258,6 +261,16 @@ def workload_flops(cfg, BH=None):
     return BH * (12.0 * dh * cfg.n_kv + 6.0 * dh * cfg.n_q + cfg.n_chunks * ns)
 
 
+def backward_flops(cfg, BH=None):
+    """Algorithmic FLOPs of the linear fast weight's backward: the replayed
+    chunk gradients (2 d^2 per key token), the key-side cotangents dv = eta dU k
+    and dk = eta dU^T v (4 d^2 per key token) and the apply's dW += dO^T Q and
+    dq = W^T dO (4 d^2 per query token). The second evaluation of the chunk
+    gradient in the reverse is not counted."""
+    BH = cfg.BH if BH is None else BH
+    return BH * float(cfg.d) * cfg.d * (6.0 * cfg.n_kv + 4.0 * cfg.n_q)
+
+
 def describe(cfg):
     order = "apply-then-update" if cfg.order == 0 else "update-then-apply"
     muon = f", Muon {cfg.ns_steps} NS steps" if cfg.use_muon else ""
@@ -291,18 +304,20 @@ def cpu_model():
     return name, ncpu
 
 
-def _oracle_sample(cfg, min_seconds):
+def _oracle_sample(cfg, min_seconds, backward=False):
     """The fp64 oracle, as it is, on a bounded sample of the same workload:
     whole (b, h) instances (every chunk), one after another, until at least
     `min_seconds` of host time have passed. When one instance is too large for
     that budget (NVS: 1M tokens in one chunk is ~22 TFLOP), the sample is the
     first tokens of one instance with the same d, h, order and options,
     chunked at the same size up to the sample length.
+    With backward, the oracle's reverse of the linear fast weight's chunk loop.
     Returns (FLOPs done, seconds, sample description, tokens done)."""
-    from lact_synth import make_inputs
+    from lact_synth import make_cotangents, make_inputs
     from oracle import lact_oracle as O
 
-    one = workload_flops(cfg, BH=1)
+    flops_of = backward_flops if backward else workload_flops
+    one = flops_of(cfg, BH=1)
     scfg, note = cfg, ""
     if one > 4e12:   # roughly 30 s or more of fp64 NumPy for one instance
         n = 16384
@@ -313,8 +328,12 @@ def _oracle_sample(cfg, min_seconds):
     done, dt = 0, 0.0
     while done < scfg.BH and dt < min_seconds:
         x = make_inputs(scfg, 0, heads=[done])
+        ct = make_cotangents(scfg, 0, heads=[done]) if backward else None
         t0 = time.perf_counter()
-        if scfg.linear:
+        if backward:
+            O.lact_backward_linear_instance(x["q"][0], x["k"][0], x["v"][0], x["eta"][0], x["W1"][0], ct["do"][0],
+                                            scfg.chunk, scfg.order)
+        elif scfg.linear:
             O.lact_forward_linear(x["q"], x["k"], x["v"], x["eta"], x["W1"], scfg.chunk, scfg.order,
                                   bool(scfg.use_muon), scfg.ns_steps)
         elif scfg.schedule:
@@ -333,18 +352,18 @@ def _oracle_sample(cfg, min_seconds):
         done += 1
     desc = (f"{done} of {scfg.BH} (b,h) instances, all {scfg.n_chunks} chunks each ({done * scfg.n_q} tokens), "
             f"fp64 NumPy, {dt:.1f} s{note}")
-    return done * workload_flops(scfg, BH=1), dt, desc, done * scfg.n_q
+    return done * flops_of(scfg, BH=1), dt, desc, done * scfg.n_q
 
 
-def cpu_baseline(cfg, min_seconds):
+def cpu_baseline(cfg, min_seconds, backward=False):
     """The oracle timed on this host: once with every core the BLAS library
     uses by default, once limited to one thread (a smaller time budget)."""
     from threadpoolctl import threadpool_info, threadpool_limits
 
-    fl, dt, desc, toks = _oracle_sample(cfg, min_seconds)
+    fl, dt, desc, toks = _oracle_sample(cfg, min_seconds, backward)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     with threadpool_limits(limits=1):
-        fl1, dt1, desc1, toks1 = _oracle_sample(cfg, min_seconds / 2)
+        fl1, dt1, desc1, toks1 = _oracle_sample(cfg, min_seconds / 2, backward)
     model, ncpu = cpu_model()
     return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": desc, "tokens_per_s": round(toks / dt, 1), "cpu_model": model, "host_cpus": ncpu,
@@ -469,8 +488,23 @@ def measure(cfg, args, P, on_device=False):
         if io_step is not None:
             io_step["rmsnorm"]()
 
+    if args.backward:
+        from lact_synth import make_cotangents
+        if not cfg.linear or cfg.use_muon or cfg.momentum or on_device:
+            raise SystemExit("--backward runs the linear fast weight without Muon or momentum, host-drawn inputs")
+        ct = make_cotangents(cfg, 0)
+        dout = torch.from_numpy(ct["do"].reshape(cfg.B, cfg.H, cfg.n_q, cfg.d)).to(dev, io)
+        del ct
+        grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v), torch.empty_like(eta),
+                 torch.empty_like(W[0]))
+        bdesc = desc
+        ws = torch.empty(P.backward_workspace_bytes(bdesc), dtype=torch.uint8, device=dev)
+
     def path():
-        if cfg.linear:
+        if args.backward:
+            P.backward_linear(q, k, v, eta, W[0], dout, cfg.chunk, order=cfg.order, out=grads, workspace=ws,
+                              stream=launch_stream())
+        elif cfg.linear:
             P.forward_linear(q, k, v, eta, W[0], cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
                              ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=launch_stream())
         elif sched is not None:
@@ -505,16 +539,17 @@ def measure(cfg, args, P, on_device=False):
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / max(args.steps, 1)
 
-    flops = workload_flops(cfg)
+    flops = backward_flops(cfg) if args.backward else workload_flops(cfg)
     tflops = flops / dt / 1e12
     tokens = cfg.B * cfg.n_q
     peak = PEAK_BF16_TFLOPS if cfg.io == "bf16" else PEAK_FP32_MFMA_TFLOPS
     res = {
-        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "metric": METRIC_BWD if args.backward else METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if cfg.io == "bf16" else "fp32", "data": "synthetic",
-        "config": {"workload": describe(cfg), "tokens_per_step": tokens, "flops_per_step": flops},
+        "config": {"workload": describe(cfg) + (", backward (lact_backward_linear)" if args.backward else ""),
+                   "tokens_per_step": tokens, "flops_per_step": flops},
         "tokens_per_s": round(tokens / dt, 1),
         "launch": "hip_graph" if args.graph else "eager",
         "pct_of_peak": round(100.0 * tflops / peak, 2),
@@ -599,6 +634,8 @@ def main():
         if cfg.schedule or cfg.layer_io:
             raise SystemExit("--chunk applies to the uniform-chunk workloads")
         cfg = cfg.with_(name=f"{cfg.name}_c{args.chunk}", chunk=args.chunk)
+    if args.backward and not args.no_secondary:
+        args.no_secondary = True   # the backward line stands alone
     if args.library_gemms:
         library_gemms(cfg, max(args.steps, 5))
         return
@@ -610,7 +647,7 @@ def main():
         res["secondary"] = {SECONDARY: {k: sec[k] for k in keep if k in sec}}
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, args.backward)
     print(json.dumps(res), flush=True)
 
 

@@ -281,12 +281,13 @@ def backward_workspace_bytes(desc: LactDesc) -> int:
     return int(n)
 
 
-def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, workspace=None,
-                    stream=None):
+def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, out=None,
+                    workspace=None, stream=None):
     """Backward of forward_linear (lact_backward_linear): the cotangents of q,
     k, v, eta and of the initial fast weight W0 [.., d, d] (fp32, not written)
     given dout (q's shape and dtype) and, optionally, the cotangent of the
-    final fast weight. Returns (dq, dk, dv, deta, dW0)."""
+    final fast weight. Returns (dq, dk, dv, deta, dW0), written into ``out``
+    (a tuple of five tensors of those shapes) when it is given."""
     import torch
     if W0.shape[-1] != W0.shape[-2]:
         raise LactError(-1, "the linear fast weight is square, [.., d, d]")
@@ -295,15 +296,21 @@ def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_f
         raise LactError(-1, "dout must have q's shape and dtype")
     if dW_final is not None and (dW_final.shape != W0.shape or dW_final.dtype != torch.float32):
         raise LactError(-1, "dW_final must have W0's shape, fp32")
-    desc, dq, _, stream = _marshal(q, k, v, eta, W0, W0, W0, extra[1:], chunk, order, False, 0, None, None,
-                                   stream, FW_LINEAR, need_workspace=False)
+    desc, dq, _, stream = _marshal(q, k, v, eta, W0, W0, W0, extra[1:], chunk, order, False, 0,
+                                   None if out is None else out[0], None, stream, FW_LINEAR, need_workspace=False)
     if not dout.is_cuda or not dout.is_contiguous():
         raise LactError(-1, "dout must be a contiguous device tensor")
     if workspace is None:
         workspace = torch.empty(max(backward_workspace_bytes(desc), 1), dtype=torch.uint8, device=q.device)
-    dk, dv = torch.empty_like(k), torch.empty_like(v)
-    deta = torch.empty_like(eta)
-    dW0 = torch.empty_like(W0)
+    if out is None:
+        dk, dv = torch.empty_like(k), torch.empty_like(v)
+        deta = torch.empty_like(eta)
+        dW0 = torch.empty_like(W0)
+    else:
+        _, dk, dv, deta, dW0 = out
+        for t, ref, name in ((dq, q, "dq"), (dk, k, "dk"), (dv, v, "dv"), (deta, eta, "deta"), (dW0, W0, "dW0")):
+            if t.shape != ref.shape or t.dtype != ref.dtype or not t.is_cuda or not t.is_contiguous():
+                raise LactError(-1, f"{name} must be a contiguous device tensor shaped like its input")
     rc = lib().lact_backward_linear(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(W0), _ptr(dout),
                                     _ptr(dW_final), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(deta), _ptr(dW0),
                                     _ptr(workspace), ctypes.c_size_t(workspace.numel() * workspace.element_size()),

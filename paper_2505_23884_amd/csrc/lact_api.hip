@@ -1082,19 +1082,27 @@ int run_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, 
 
 // ---------------------------------------------------------------- backward
 // Reverse of the linear fast weight's chunk loop (§5.4 with the §3.1 chunk
-// gradient and the per-row norm-preserving update of §3.2): the fast weights
-// of every chunk boundary are recomputed with the forward's own update and
-// kept; the reverse walks the chunks from the last, carrying the cotangent of
-// the fast weight in dW0. Workspace: the forward's, then W_1 .. W_nch, the
-// split partials of the apply's contribution dO^T Q, and the operand copies
-// of the update's cotangent (row-major and transposed) and of a transposed
-// fast weight.
+// gradient and the per-row norm-preserving update of §3.2). The linear
+// gradient does not depend on the fast weight, so the negated gradients
+// P_c = sum_{t in c} eta_t v_t k_t^T of all chunks come from one
+// contraction (its token splits are the chunks), beside the apply's
+// contributions A_c = dO_c^T Q_c; the weights W_1 .. W_nch at the chunk
+// boundaries follow from one row-wise update per chunk, and their
+// transposed operand copies from one launch. The reverse then walks the
+// chunks from the last, carrying the cotangent of the fast weight in dW0:
+// per chunk the row-wise reverse of the update, one launch of three
+// products (dv before its rate, dk and dq) and a token step.
+// Workspace: eta k of every key token, P and A of every chunk, the
+// trajectory, the transposed copies, the partials of the tail's dO^T Q and
+// the two operand copies of the update's cotangent.
 struct BwdLayout {
   Plan p;
-  int64_t nch;         // chunks of the forward
-  int64_t tail_len;    // tokens per piece of the apply-only tail
-  int64_t tail_split;  // tokens per split of a tail piece (at most p.nsplit splits)
-  size_t off_traj, off_apart, off_ub, off_ut, off_wt, total;
+  int64_t nch;          // chunks of the forward
+  bool batched;         // chunk = whole 32-token steps: one split per chunk
+  int64_t group;        // chunks per launch of the batched contractions
+  int64_t tail_len;     // tokens per piece of the apply-only tail
+  int64_t tail_split;   // tokens per split of a tail piece (at most p.nsplit splits)
+  size_t off_ek, off_P, off_A, off_traj, off_wt, off_tail, off_ub, off_ut, total;
 };
 
 int bwd_layout(const lact_desc* dsc, BwdLayout* L) {
@@ -1105,28 +1113,39 @@ int bwd_layout(const lact_desc* dsc, BwdLayout* L) {
   const Plan& p = L->p;
   const double dd = (double)p.d * p.d;
   L->nch = dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0;
-  // the trajectory holds every chunk's weights: bound it before sizing
-  if ((double)L->nch * p.BH * dd * 4.0 + (double)p.total > 4.0e18) return LACT_EUNSUPPORTED;
+  // per chunk: P, A and W (fp32) and a transposed copy; per key token eta k
+  const double need = (double)L->nch * p.BH * dd * (12.0 + p.esz) + (double)p.BH * dsc->n_kv * p.d * p.esz;
+  if (need > 4.0e18) return LACT_EUNSUPPORTED;
+  L->batched = dsc->chunk % 32 == 0;
+  const TileShape g2 = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
+  const int64_t tiles = (int64_t)p.BH * cdiv(p.d, g2.rows) * cdiv(p.d, g2.cols);
+  L->group = std::max<int64_t>(1, ((int64_t)1 << 29) / tiles);   // two segments stay under 2^30 blocks
   L->tail_len = std::max<int64_t>(p.C, 8192);
   L->tail_split = std::max<int64_t>(32, cdiv(cdiv(L->tail_len, p.nsplit), 32) * 32);
   const size_t w4 = (size_t)p.BH * p.d * p.d * 4, wio = (size_t)p.BH * p.d * p.d * p.esz;
-  size_t o = p.total;
+  size_t o = 0;
+  L->off_ek = o;
+  o = align_up(o + (size_t)p.BH * dsc->n_kv * p.d * p.esz);
+  L->off_P = o;
+  o = align_up(o + (size_t)L->nch * w4);
+  L->off_A = o;
+  o = align_up(o + (size_t)L->nch * w4);
   L->off_traj = o;
   o = align_up(o + (size_t)L->nch * w4);
-  L->off_apart = o;
-  o = align_up(o + (size_t)p.nsplit * w4);
+  L->off_wt = o;
+  o = align_up(o + (size_t)(L->nch + 1) * wio);
+  L->off_tail = o;
+  o = align_up(o + (dsc->n_q > dsc->n_kv ? (size_t)p.nsplit * w4 : 0));
   L->off_ub = o;
   o = align_up(o + wio);
   L->off_ut = o;
   o = align_up(o + wio);
-  L->off_wt = o;
-  o = align_up(o + wio);
-  L->total = o;
+  L->total = std::max<size_t>(o, kAlign);
   return LACT_OK;
 }
 
 // One GRAD2 segment: out[m][j] = sum over rows [0, n) of a[., m] b[., j], in
-// splits of split_len tokens (fp32 partials, BH d^2 floats between splits).
+// splits of split_len tokens (fp32, BH d^2 floats between splits).
 void lin_grad_seg(BwdSeg& g, const Plan& p, Operand a, Operand b, float* out, int64_t n, int64_t split_len) {
   const TileShape t = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
   g.kind = BWD_GRAD2;
@@ -1160,14 +1179,14 @@ void lin_out_seg(BwdSeg& o, const Plan& p, Operand a, Operand b, void* out, int6
   o.out_inst = out_inst;
 }
 
-int lin_launch(Ctx& c, BwdArgs& b, int nseg, double flops) {
+int lin_launch(const Plan& p, hipStream_t s, BwdArgs& b, int nseg, double flops) {
   b.nseg = nseg;
   b.total_blocks = 0;
   for (int i = 0; i < nseg; ++i) b.total_blocks += b.seg[i].nblocks;
-  b.d = c.p.d;
-  b.h = c.p.d;
-  b.narrow = c.p.narrow;
-  return timed(LACT_KCLASS_BWD, flops, c.s, [&] { return launch_bwd(b, c.p.bf16, c.s); });
+  b.d = p.d;
+  b.h = p.d;
+  b.narrow = p.narrow;
+  return timed(LACT_KCLASS_BWD, flops, s, [&] { return launch_bwd(b, p.bf16, s); });
 }
 
 int run_backward_linear(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
@@ -1185,120 +1204,136 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
   if (any_kv && (misaligned(k) || misaligned(v) || misaligned(dk) || misaligned(dv))) return LACT_EALIGN;
   if (any_kv && (((uintptr_t)eta & 3) || ((uintptr_t)deta & 3))) return LACT_EALIGN;
   if (!workspace || workspace_bytes < L.total) return LACT_EWORKSPACE;
-  Ctx c;
-  // the forward's context over the same inputs; W1 is pointed at each
-  // trajectory slot before its update, so W0 itself is never written
-  rc = setup(c, desc, q, k, v, eta, nullptr, const_cast<float*>(W0), nullptr, nullptr, nullptr, dq, workspace,
-             workspace_bytes, stream);
-  if (rc) return rc;
-  const Plan& p = c.p;
-  if (p.bf16) {   // the update also writes operand copies (not read here)
-    for (int m = 0; m < 3; ++m) {
-      c.wb[0][m] = c.ws + p.off_wb[m];
-      c.wb[1][m] = c.ws + p.off_wb2[m];
-    }
-    use_wset(c, 0);
-  }
+  if ((uintptr_t)workspace & (kAlign - 1)) return LACT_EALIGN;
+  const Plan& p = L.p;
+  const hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
   const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk, d = p.d, BH = p.BH;
-  const int64_t dd = d * d, esz = p.esz;
+  const int64_t dd = d * d, esz = p.esz, wio = BH * dd * esz;
   const size_t w4 = (size_t)BH * dd * 4;
-  auto traj = [&](int64_t i) -> float* {
-    return i == 0 ? const_cast<float*>(W0) : reinterpret_cast<float*>(c.ws + L.off_traj + (size_t)(i - 1) * w4);
-  };
-  // forward: the weights after every chunk
-  for (int64_t ci = 0; ci < L.nch; ++ci) {
-    const int64_t s0 = ci * C, s1 = std::min(n_kv, s0 + C);
-    rc = timed(LACT_KCLASS_PREP, 0.0, c.s,
-               [&] { return hipMemcpyAsync(traj(ci + 1), traj(ci), w4, hipMemcpyDeviceToDevice, c.s); });
-    if (rc) return rc;
-    c.W[0] = traj(ci + 1);
-    c.chunk_idx = ci;
-    rc = update_chunk_linear(c, s0, s1, false);
-    if (rc) return rc;
-  }
-  float* G = dW0;
-  float* apart = reinterpret_cast<float*>(c.ws + L.off_apart);
-  float* part = reinterpret_cast<float*>(c.ws + p.off_step);
-  uint8_t* ub = c.ws + L.off_ub;
-  uint8_t* ut = c.ws + L.off_ut;
-  uint8_t* wt = c.ws + L.off_wt;
   const int64_t psplit = BH * dd;
   const uint8_t* qb = (const uint8_t*)q;
   const uint8_t* kb = (const uint8_t*)k;
   const uint8_t* vb = (const uint8_t*)v;
   const uint8_t* ob = (const uint8_t*)dout;
-  int64_t wt_of = -1;   // trajectory index whose transposed copy wt holds
-  auto make_wt = [&](int64_t i) -> int {
-    if (wt_of == i) return LACT_OK;
-    wt_of = i;
-    return timed(LACT_KCLASS_PREP, 0.0, c.s,
-                 [&] { return launch_transpose_cvt(traj(i), wt, p.BH, p.d, p.bf16, c.s); });
+  uint8_t* ek = ws + L.off_ek;
+  float* Pall = reinterpret_cast<float*>(ws + L.off_P);
+  float* Aall = reinterpret_cast<float*>(ws + L.off_A);
+  auto traj = [&](int64_t i) -> float* {
+    return i == 0 ? const_cast<float*>(W0) : reinterpret_cast<float*>(ws + L.off_traj + (size_t)(i - 1) * w4);
   };
-  const Operand wt_op = op(wt, d, dd);
+  auto wt = [&](int64_t i) -> uint8_t* { return ws + L.off_wt + (size_t)i * wio; };
+  // eta k of every key token, then P_c and A_c of every chunk
+  if (any_kv) {
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+      return launch_scale_rows(kb, eta, ek, p.BH, n_kv, p.d, n_kv * d, n_kv, n_kv * d, p.bf16, s);
+    });
+    if (rc) return rc;
+  }
+  if (L.batched) {
+    for (int64_t c0 = 0; c0 < L.nch; c0 += L.group) {
+      const int64_t t0 = c0 * C, t1 = std::min(n_kv, (c0 + L.group) * C), n = t1 - t0;
+      BwdArgs b{};
+      lin_grad_seg(b.seg[0], p, op(vb + t0 * d * esz, d, n_kv * d), op(ek + t0 * d * esz, d, n_kv * d),
+                   Pall + c0 * psplit, n, C);
+      lin_grad_seg(b.seg[1], p, op(ob + t0 * d * esz, d, n_q * d), op(qb + t0 * d * esz, d, n_q * d),
+                   Aall + c0 * psplit, n, C);
+      rc = lin_launch(p, s, b, 2, 4.0 * BH * n * dd);
+      if (rc) return rc;
+    }
+  } else {
+    for (int64_t ci = 0; ci < L.nch; ++ci) {
+      const int64_t t0 = ci * C, n = std::min(n_kv, t0 + C) - t0, one = cdiv(n, 32) * 32;
+      BwdArgs b{};
+      lin_grad_seg(b.seg[0], p, op(vb + t0 * d * esz, d, n_kv * d), op(ek + t0 * d * esz, d, n_kv * d),
+                   Pall + ci * psplit, n, one);
+      lin_grad_seg(b.seg[1], p, op(ob + t0 * d * esz, d, n_q * d), op(qb + t0 * d * esz, d, n_q * d),
+                   Aall + ci * psplit, n, one);
+      rc = lin_launch(p, s, b, 2, 4.0 * BH * n * dd);
+      if (rc) return rc;
+    }
+  }
+  // W_{c+1} = rows of W_c + P_c rescaled to W_c's row norms
+  for (int64_t ci = 0; ci < L.nch; ++ci) {
+    UpdArgs u{};
+    u.W[0] = traj(ci + 1);
+    u.Wsrc[0] = traj(ci);
+    u.step = Pall + ci * psplit;
+    u.nsplit = 1;
+    u.step_split = 0;
+    u.nmat = 1;
+    u.BH = p.BH;
+    u.d = p.d;
+    u.h = p.d;
+    u.rows_total = p.BH * p.d;
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_update(u, false, s); });
+    if (rc) return rc;
+  }
+  // transposed operand copies of W_0 .. W_nch (W_1 .. W_nch are contiguous)
+  rc = timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_transpose_cvt(W0, wt(0), p.BH, p.d, p.bf16, s); });
+  if (rc) return rc;
+  {
+    const int64_t t = cdiv(d, 32), per = std::max<int64_t>(1, ((int64_t)1 << 30) / (BH * t * t));
+    for (int64_t c0 = 1; c0 <= L.nch; c0 += per) {   // whole sets of BH matrices, under 2^30 blocks
+      const int64_t m = std::min(per, L.nch + 1 - c0);
+      rc = timed(LACT_KCLASS_PREP, 0.0, s,
+                 [&] { return launch_transpose_cvt(traj(c0), wt(c0), (int)(m * BH), p.d, p.bf16, s); });
+      if (rc) return rc;
+    }
+  }
+  float* G = dW0;
   // tail [n_kv, n_q): applied with the final weight; its dO^T Q joins the
   // cotangent of that weight (dW_final, or zero)
   bool first = true;
   if (any_q && n_q > n_kv) {
-    rc = make_wt(L.nch);
-    if (rc) return rc;
+    float* tpart = reinterpret_cast<float*>(ws + L.off_tail);
     for (int64_t a = n_kv; a < n_q; a += L.tail_len) {
       const int64_t n = std::min(L.tail_len, n_q - a);
       BwdArgs b{};
-      lin_grad_seg(b.seg[0], p, op(ob + a * d * esz, d, n_q * d), op(qb + a * d * esz, d, n_q * d), apart, n,
+      lin_grad_seg(b.seg[0], p, op(ob + a * d * esz, d, n_q * d), op(qb + a * d * esz, d, n_q * d), tpart, n,
                    L.tail_split);
-      lin_out_seg(b.seg[1], p, op(ob + a * d * esz, d, n_q * d), wt_op, (uint8_t*)dq + a * d * esz, n_q * d, n);
-      rc = lin_launch(c, b, 2, 4.0 * BH * n * dd);
+      lin_out_seg(b.seg[1], p, op(ob + a * d * esz, d, n_q * d), op(wt(L.nch), d, dd), (uint8_t*)dq + a * d * esz,
+                  n_q * d, n);
+      rc = lin_launch(p, s, b, 2, 4.0 * BH * n * dd);
       if (rc) return rc;
       const int mode = first ? (dWf ? 1 : 0) : 2;
       const int ns = b.seg[0].nsplit;
-      rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s,
-                 [&] { return launch_sum_parts(G, dWf, mode, apart, ns, psplit, BH * dd, c.s); });
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
+                 [&] { return launch_sum_parts(G, dWf, mode, tpart, ns, psplit, BH * dd, s); });
       if (rc) return rc;
       first = false;
     }
   }
   if (first) {
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s,
-               [&] { return launch_sum_parts(G, dWf, dWf ? 1 : 0, nullptr, 0, psplit, BH * dd, c.s); });
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
+               [&] { return launch_sum_parts(G, dWf, dWf ? 1 : 0, nullptr, 0, psplit, BH * dd, s); });
     if (rc) return rc;
   }
   const bool then_apply = desc->order == LACT_UPDATE_THEN_APPLY;
-  const uint8_t* ek = c.ws + p.off_upd[0];   // eta k of the chunk, [BH][C][d]
+  uint8_t* ub = ws + L.off_ub;
+  uint8_t* ut = ws + L.off_ut;
   for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
-    const int64_t s0 = ci * C, s1 = std::min(n_kv, s0 + C), n = s1 - s0;
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] {
-      return launch_scale_rows(kb + s0 * d * esz, eta + s0, c.ws + p.off_upd[0], p.BH, n, p.d, n_kv * d, n_kv,
-                               p.C * d, p.bf16, c.s);
+    const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+      return launch_lin_vjp(traj(ci), Pall + ci * psplit, Aall + ci * psplit, 1, psplit, then_apply, G, ub, ut,
+                            p.BH, p.d, p.bf16, s);
     });
     if (rc) return rc;
-    // the chunk's apply used W_{c+1} (update-then-apply) or W_c
-    rc = make_wt(then_apply ? ci + 1 : ci);
+    BwdArgs b{};
+    lin_out_seg(b.seg[0], p, op(kb + s0 * d * esz, d, n_kv * d), op(ub, d, dd), (uint8_t*)dv + s0 * d * esz,
+                n_kv * d, n);   // Y = K Uh^T
+    lin_out_seg(b.seg[1], p, op(vb + s0 * d * esz, d, n_kv * d), op(ut, d, dd), (uint8_t*)dk + s0 * d * esz,
+                n_kv * d, n);   // dk = eta (V Uh)
+    b.seg[1].row_scale = eta + s0;
+    b.seg[1].scale_inst = n_kv;
+    // dq = dO W with the weight the chunk was applied with
+    lin_out_seg(b.seg[2], p, op(ob + s0 * d * esz, d, n_q * d), op(wt(then_apply ? ci + 1 : ci), d, dd),
+                (uint8_t*)dq + s0 * d * esz, n_q * d, n);
+    rc = lin_launch(p, s, b, 3, 6.0 * BH * n * dd);
     if (rc) return rc;
-    const Operand vo = op(vb + s0 * d * esz, d, n_kv * d), eko = op(ek, d, p.C * d);
-    const Operand doo = op(ob + s0 * d * esz, d, n_q * d), qo = op(qb + s0 * d * esz, d, n_q * d);
-    {
-      BwdArgs b{};
-      lin_grad_seg(b.seg[0], p, vo, eko, part, n, p.split_len);    // P = sum eta v k^T (= -g)
-      lin_grad_seg(b.seg[1], p, doo, qo, apart, n, p.split_len);   // dO^T Q
-      lin_out_seg(b.seg[2], p, doo, wt_op, (uint8_t*)dq + s0 * d * esz, n_q * d, n);   // dq = dO W
-      rc = lin_launch(c, b, 3, 6.0 * BH * n * dd);
-      if (rc) return rc;
-    }
-    const int ns = (int)std::max<int64_t>(1, cdiv(n, p.split_len));
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] {
-      return launch_lin_vjp(traj(ci), part, apart, ns, psplit, then_apply, G, ub, ut, p.BH, p.d, p.bf16, c.s);
-    });
-    if (rc) return rc;
-    {
-      BwdArgs b{};
-      lin_out_seg(b.seg[0], p, eko, op(ub, d, dd), (uint8_t*)dv + s0 * d * esz, n_kv * d, n);   // dv = eta k Uh^T
-      lin_out_seg(b.seg[1], p, vo, op(ut, d, dd), (uint8_t*)dk + s0 * d * esz, n_kv * d, n);    // Z = v Uh
-      rc = lin_launch(c, b, 2, 4.0 * BH * n * dd);
-      if (rc) return rc;
-    }
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, c.s, [&] {
-      return launch_lin_tokens(kb + s0 * d * esz, eta + s0, (uint8_t*)dk + s0 * d * esz, deta + s0, p.BH, n, p.d,
-                               n_kv * d, n_kv * d, n_kv, p.bf16, c.s);
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+      return launch_lin_tokens(vb + s0 * d * esz, eta + s0, (uint8_t*)dv + s0 * d * esz, deta + s0, p.BH, n, p.d,
+                               n_kv * d, n_kv, p.bf16, s);
     });
     if (rc) return rc;
   }

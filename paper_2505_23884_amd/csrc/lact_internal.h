@@ -63,6 +63,8 @@ struct BwdSeg {
   int64_t out_inst;     // elements between instances
   int64_t out_split;    // GRAD: elements between splits
   int64_t out_off;      // GRAD2: offset of its matrix in an instance's partials
+  const float* row_scale;  // OUT (or nullptr): token t's row is scaled by row_scale[inst * scale_inst + t]
+  int64_t scale_inst;
   // GRAD_UPD (16-bit I/O, whole rows per tile, no split): the gradients of
   // W1 (a0 = eta dz1, b0 = K), W3 (a1 = eta dz3, b0) and W2 (a2 = V,
   // b1 = eta hidden) and the weight update in one pass; tiles_m counts the
@@ -91,6 +93,7 @@ struct BwdArgs {
 // ---- weight update ----------------------------------------------------------
 struct UpdArgs {
   float* W[3];          // fp32 state W1 [h x d], W2 [d x h], W3 [h x d]
+  const float* Wsrc[3]; // where the state before the update is read (nullptr: W itself, in place)
   void* Wb[3];          // operand copies (bf16 mode) or nullptr
   const float* step;    // summed (or split) step, layout [split][inst][3][d*h]
   int nsplit;
@@ -288,8 +291,8 @@ hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s);
 hipError_t launch_lin_vjp(const float* W, const float* P, const float* A, int nsplit, int64_t psplit, bool a_first,
                           float* G, void* Ub, void* UT, int BH, int d, bool io_bf16, hipStream_t s);
 hipError_t launch_transpose_cvt(const float* W, void* WT, int BH, int d, bool io_bf16, hipStream_t s);
-hipError_t launch_lin_tokens(const void* K, const float* eta, void* dk, float* deta, int BH, int64_t n, int d,
-                             int64_t k_inst, int64_t z_inst, int64_t eta_inst, bool io_bf16, hipStream_t s);
+hipError_t launch_lin_tokens(const void* V, const float* eta, void* dv, float* deta, int BH, int64_t n, int d,
+                             int64_t tok_inst, int64_t eta_inst, bool io_bf16, hipStream_t s);
 hipError_t launch_sum_parts(float* G, const float* init, int mode, const float* P, int nsplit, int64_t psplit,
                             int64_t n, hipStream_t s);
 hipError_t launch_zero_rows(void* out, int BH, int64_t row_bytes, int64_t rows, int64_t r0, int64_t r1,

@@ -1308,6 +1308,17 @@ __device__ __forceinline__ void bwd_body(const BwdArgs& args, int blk, uint8_t* 
     mainloop<T, KO>(smem, ops, h, acc);
     const int64_t ob = inst * sg.out_inst;
     const int mrow0 = wave_m<KO>() * 32 * KO::MI + ((lane >> 5) << 2);
+    if (sg.row_scale) {   // per-token factor of the output rows
+#pragma unroll
+      for (int ni = 0; ni < KO::NI; ++ni) {
+        const int tok = acc_col<KO>(ni);
+        const float sc = tok < ntok ? sg.row_scale[inst * sg.scale_inst + t0 + tok] : 0.0f;
+#pragma unroll
+        for (int mi = 0; mi < KO::MI; ++mi)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[0][mi][ni][r] *= sc;
+      }
+    }
     if constexpr (sizeof(T) == 2) {
       static_assert(KO::ROWS_A * KO::ROWS_B * 2 <= bwd_smem<T, NARROW>(), "staging fits");
 #pragma unroll
@@ -1456,6 +1467,7 @@ __global__ __launch_bounds__(256) void k_update(const UpdArgs a) {
   const int64_t dh = (int64_t)a.d * a.h;
   const int64_t off = inst * dh + (int64_t)r * L;
   float4* W = reinterpret_cast<float4*>(a.W[mat] + off);
+  const float4* Wi = reinterpret_cast<const float4*>((a.Wsrc[mat] ? a.Wsrc[mat] : a.W[mat]) + off);
   const float4* P = reinterpret_cast<const float4*>(a.step + inst * a.nmat * dh + mat * dh + (int64_t)r * L);
   const int64_t ps = a.step_split >> 2;
   float4* Mv = a.M[0] ? reinterpret_cast<float4*>(a.M[mat] + off) : nullptr;
@@ -1463,7 +1475,7 @@ __global__ __launch_bounds__(256) void k_update(const UpdArgs a) {
 #pragma unroll
   for (int t = 0; t < NV; ++t) {
     const int i = lane + 64 * t;
-    w[t] = W[i < nv ? i : 0];
+    w[t] = Wi[i < nv ? i : 0];
     u[t] = P[i < nv ? i : 0];
     if (Mv) m[t] = Mv[i < nv ? i : 0];
   }
@@ -2258,9 +2270,18 @@ __global__ __launch_bounds__(256) void k_beta_mean(const BetaArgs a) {
 // norm-preserving update): the contractions run on the OUT and GRAD2 kinds;
 // these kernels are the row-wise and token-wise steps between them.
 
+// Rows of the d x d matrix per workgroup of k_lin_vjp: the rows' cotangent in
+// the operand type is staged in LDS (up to 64 KB) to leave as whole
+// segments of the transposed copy.
+template <typename T, int NV>
+constexpr int vjp_rows() {
+  return cmax(4, 65536 / (256 * NV * (int)sizeof(T)) > 32 ? 32 : 65536 / (256 * NV * (int)sizeof(T)));
+}
+
 // Reverse of W' = (n / u) U, U = W + P (P = sum of the split partials of
-// sum_t eta_t v_t k_t^T, the negated chunk gradient): one wave per row of the
-// d x d matrix. From the cotangent G of W' (in place), with a = G . U per row:
+// sum_t eta_t v_t k_t^T, the negated chunk gradient), vjp_rows() rows of
+// one instance per workgroup, one wave per row at a time. From the
+// cotangent G of W' (in place), with a = G . U per row:
 //   Uh = (n / u) G - (n a / u^3) U,   G <- Uh + (a / (u n)) W,
 // and Uh (the cotangent of U, i.e. minus that of the gradient) in the
 // operand type, row-major into Ub and transposed into UT. The apply's own
@@ -2268,65 +2289,100 @@ __global__ __launch_bounds__(256) void k_beta_mean(const BetaArgs a) {
 // before the reverse when a_first (the chunk was applied with W'), after it
 // otherwise (applied with W). A zero row norm gives the same non-finite
 // values as the forward's division.
+template <int NV>
+constexpr int vjp_waves() { return NV <= 4 ? 16 : 4; }   // rows of up to 1024 floats: 16 waves in flight
+
 template <typename T, int NV>
-__global__ __launch_bounds__(256) void k_lin_vjp(const float* W, const float* P, const float* A, int nsplit,
-                                                 int64_t psplit, int a_first, float* G, T* Ub, T* UT, int BH, int d) {
-  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (wave >= BH * d) return;
-  const int inst = wave / d, r = wave - inst * d;
-  const int64_t dd = (int64_t)d * d, off = inst * dd + (int64_t)r * d;
+__global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_lin_vjp(const float* W, const float* P, const float* A,
+                                                                  int nsplit, int64_t psplit, int a_first, float* G,
+                                                                  T* Ub, T* UT, int d) {
+  constexpr int R = vjp_rows<T, NV>();
+  constexpr int NW = vjp_waves<NV>();
+  constexpr int LD = 256 * NV + 4 / (int)sizeof(T);   // one 4-byte word of padding per staged row
+  __shared__ __attribute__((aligned(16))) T tile[R * LD];
+  const int per = (d + R - 1) / R;
+  const int inst = blockIdx.x / per;
+  const int r0 = (blockIdx.x - inst * per) * R;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t dd = (int64_t)d * d;
   const int nv = d >> 2;
-  const float4* w4 = reinterpret_cast<const float4*>(W + off);
-  const float4* p4 = reinterpret_cast<const float4*>(P + off);
-  const float4* a4 = reinterpret_cast<const float4*>(A + off);
-  float4* g4 = reinterpret_cast<float4*>(G + off);
   const int64_t ps = psplit >> 2;
-  float4 w[NV], u[NV], g[NV], ap[NV];
-  float sw = 0.f, su = 0.f, sa = 0.f;
-#pragma unroll
-  for (int t = 0; t < NV; ++t) {
-    const int i = lane + 64 * t;
-    const bool in = i < nv;
+  for (int rr = w; rr < R; rr += NW) {
+    const int r = r0 + rr;
+    if (r >= d) break;
+    const int64_t off = inst * dd + (int64_t)r * d;
+    const float4* w4 = reinterpret_cast<const float4*>(W + off);
+    const float4* p4 = reinterpret_cast<const float4*>(P + off);
+    const float4* a4 = reinterpret_cast<const float4*>(A + off);
+    float4* g4 = reinterpret_cast<float4*>(G + off);
+    float4 wv[NV], u[NV], g[NV], ap[NV];
     const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-    w[t] = in ? w4[i] : z;
-    g[t] = in ? g4[i] : z;
-    float4 acc = w[t], aa = z;
-    for (int sp = 0; sp < nsplit && in; ++sp) {
-      const float4 q = p4[sp * ps + i];
-      acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
-      const float4 e = a4[sp * ps + i];
-      aa.x += e.x; aa.y += e.y; aa.z += e.z; aa.w += e.w;
-    }
-    u[t] = acc;
-    if (a_first) {
-      g[t].x += aa.x; g[t].y += aa.y; g[t].z += aa.z; g[t].w += aa.w;
-      aa = z;
-    }
-    ap[t] = aa;
-    sw += w[t].x * w[t].x + w[t].y * w[t].y + w[t].z * w[t].z + w[t].w * w[t].w;
-    su += u[t].x * u[t].x + u[t].y * u[t].y + u[t].z * u[t].z + u[t].w * u[t].w;
-    sa += g[t].x * u[t].x + g[t].y * u[t].y + g[t].z * u[t].z + g[t].w * u[t].w;
-  }
-  sw = wave_sum(sw);
-  su = wave_sum(su);
-  sa = wave_sum(sa);
-  const float n = sqrtf(sw), uu = sqrtf(su);
-  const float c1 = n / uu, c2 = n * sa / (uu * uu * uu), c3 = sa / (uu * n);
 #pragma unroll
-  for (int t = 0; t < NV; ++t) {
-    const int i = lane + 64 * t;
-    if (i >= nv) continue;
-    const float4 uh = make_float4(c1 * g[t].x - c2 * u[t].x, c1 * g[t].y - c2 * u[t].y, c1 * g[t].z - c2 * u[t].z,
-                                  c1 * g[t].w - c2 * u[t].w);
-    g4[i] = make_float4(uh.x + c3 * w[t].x + ap[t].x, uh.y + c3 * w[t].y + ap[t].y, uh.z + c3 * w[t].z + ap[t].z,
-                        uh.w + c3 * w[t].w + ap[t].w);
-    st4<T>(Ub, off + 4 * i, uh.x, uh.y, uh.z, uh.w);
-    const int64_t col = inst * dd + (int64_t)(4 * i) * d + r;   // UT[e][r] for e = 4i .. 4i+3
-    UT[col] = (T)uh.x;
-    UT[col + d] = (T)uh.y;
-    UT[col + 2 * d] = (T)uh.z;
-    UT[col + 3 * d] = (T)uh.w;
+    for (int t = 0; t < NV; ++t) {
+      const int i = lane + 64 * t, ic = i < nv ? i : 0;   // lanes past the row load element 0, then drop it
+      wv[t] = w4[ic];
+      g[t] = g4[ic];
+      if (i >= nv) wv[t] = g[t] = z;
+      u[t] = wv[t];
+      ap[t] = z;
+    }
+    for (int sp = 0; sp < nsplit; ++sp) {
+#pragma unroll
+      for (int t = 0; t < NV; ++t) {
+        const int i = lane + 64 * t;
+        if (i < nv) {
+          const float4 q = p4[sp * ps + i], e = a4[sp * ps + i];
+          u[t].x += q.x; u[t].y += q.y; u[t].z += q.z; u[t].w += q.w;
+          ap[t].x += e.x; ap[t].y += e.y; ap[t].z += e.z; ap[t].w += e.w;
+        }
+      }
+    }
+    float sw = 0.f, su = 0.f, sa = 0.f;
+#pragma unroll
+    for (int t = 0; t < NV; ++t) {
+      if (a_first) {
+        g[t].x += ap[t].x; g[t].y += ap[t].y; g[t].z += ap[t].z; g[t].w += ap[t].w;
+        ap[t] = z;
+      }
+      sw += wv[t].x * wv[t].x + wv[t].y * wv[t].y + wv[t].z * wv[t].z + wv[t].w * wv[t].w;
+      su += u[t].x * u[t].x + u[t].y * u[t].y + u[t].z * u[t].z + u[t].w * u[t].w;
+      sa += g[t].x * u[t].x + g[t].y * u[t].y + g[t].z * u[t].z + g[t].w * u[t].w;
+    }
+    sw = wave_sum(sw);
+    su = wave_sum(su);
+    sa = wave_sum(sa);
+    const float n = sqrtf(sw), uu = sqrtf(su);
+    const float c1 = n / uu, c2 = n * sa / (uu * uu * uu), c3 = sa / (uu * n);
+#pragma unroll
+    for (int t = 0; t < NV; ++t) {
+      const int i = lane + 64 * t;
+      if (i >= nv) continue;
+      const float4 uh = make_float4(c1 * g[t].x - c2 * u[t].x, c1 * g[t].y - c2 * u[t].y,
+                                    c1 * g[t].z - c2 * u[t].z, c1 * g[t].w - c2 * u[t].w);
+      g4[i] = make_float4(uh.x + c3 * wv[t].x + ap[t].x, uh.y + c3 * wv[t].y + ap[t].y,
+                          uh.z + c3 * wv[t].z + ap[t].z, uh.w + c3 * wv[t].w + ap[t].w);
+      st4<T>(Ub, off + 4 * i, uh.x, uh.y, uh.z, uh.w);
+      T* row = tile + rr * LD + 4 * i;
+      row[0] = (T)uh.x;
+      row[1] = (T)uh.y;
+      row[2] = (T)uh.z;
+      row[3] = (T)uh.w;
+    }
+  }
+  __syncthreads();
+  // UT[e][r0 .. r0 + R): four consecutive rows of the block per store
+  constexpr int Q = R / 4;
+  const int rows = d - r0 < R ? d - r0 : R;
+  for (int pi = threadIdx.x; pi < d * Q; pi += 64 * NW) {
+    const int e = pi / Q, j = 4 * (pi - (pi / Q) * Q);
+    if (j >= rows) continue;
+    const int64_t o = inst * dd + (int64_t)e * d + r0 + j;
+    if (j + 4 <= rows) {
+      st4<T>(UT, o, (float)tile[j * LD + e], (float)tile[(j + 1) * LD + e], (float)tile[(j + 2) * LD + e],
+             (float)tile[(j + 3) * LD + e]);
+    } else {
+      for (int q = 0; j + q < rows; ++q) UT[o + q] = tile[(j + q) * LD + e];
+    }
   }
 }
 
@@ -2356,27 +2412,26 @@ __global__ __launch_bounds__(256) void k_transpose_cvt(const float* W, T* WT, in
 }
 
 // Token step of the reverse, one wave per key token t of a chunk (grid
-// stride over BH x n tokens). On entry dk holds Z = V Uh (rows t); with it
-// dk_t = eta_t Z_t and deta_t = k_t . Z_t (= v_t^T Uh k_t).
+// stride over BH x n tokens). On entry dv holds Y = K Uh^T (rows t); it
+// leaves as dv_t = eta_t Y_t, with deta_t = v_t . Y_t (= v_t^T Uh k_t).
 template <typename T>
-__global__ __launch_bounds__(256) void k_lin_tokens(const T* K, const float* eta, T* dk, float* deta, int BH,
-                                                    int64_t n, int d, int64_t k_inst, int64_t z_inst,
-                                                    int64_t eta_inst) {
+__global__ __launch_bounds__(256) void k_lin_tokens(const T* V, const float* eta, T* dv, float* deta, int BH,
+                                                    int64_t n, int d, int64_t tok_inst, int64_t eta_inst) {
   const int lane = threadIdx.x & 63;
   const int64_t total = (int64_t)BH * n;
   for (int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wave < total; wave += (int64_t)gridDim.x * 4) {
     const int64_t inst = wave / n, t = wave - inst * n;
-    const int64_t ko = inst * k_inst + t * d, zo = inst * z_inst + t * d;
+    const int64_t o = inst * tok_inst + t * d;
     const float e = eta[inst * eta_inst + t];
     float dot = 0.0f;
     for (int c = 4 * lane; c < d; c += 256) {
-      float z[4];
+      float y[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        z[q] = (float)dk[zo + c + q];
-        dot += (float)K[ko + c + q] * z[q];
+        y[q] = (float)dv[o + c + q];
+        dot += (float)V[o + c + q] * y[q];
       }
-      st4<T>(dk, zo + c, e * z[0], e * z[1], e * z[2], e * z[3]);
+      st4<T>(dv, o + c, e * y[0], e * y[1], e * y[2], e * y[3]);
     }
     dot = wave_sum(dot);
     if (lane == 0) deta[inst * eta_inst + t] = dot;
@@ -2593,15 +2648,15 @@ hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d
 // OUT / GRAD2 contractions (io_bf16 selects bf16 operand copies, else fp32).
 hipError_t launch_lin_vjp(const float* W, const float* P, const float* A, int nsplit, int64_t psplit, bool a_first,
                           float* G, void* Ub, void* UT, int BH, int d, bool io_bf16, hipStream_t s) {
-  const int64_t rows = (int64_t)BH * d;
-  if (rows <= 0) return hipSuccess;
-  const unsigned blocks = (unsigned)((rows + 3) / 4);
+  if ((int64_t)BH * d <= 0) return hipSuccess;
   const int per_lane = (d / 4 + 63) / 64;
   auto go = [&](auto tag, auto nvc) {
     using T = decltype(tag);
     constexpr int NV = decltype(nvc)::value;
-    k_lin_vjp<T, NV><<<blocks, 256, 0, s>>>(W, P, A, nsplit, psplit, a_first ? 1 : 0, G, reinterpret_cast<T*>(Ub),
-                                            reinterpret_cast<T*>(UT), BH, d);
+    constexpr int R = vjp_rows<T, NV>();
+    const unsigned blocks = (unsigned)((int64_t)BH * ((d + R - 1) / R));   // <= 2^20 * 1024
+    k_lin_vjp<T, NV><<<blocks, 64 * vjp_waves<NV>(), 0, s>>>(W, P, A, nsplit, psplit, a_first ? 1 : 0, G,
+                                                             reinterpret_cast<T*>(Ub), reinterpret_cast<T*>(UT), d);
   };
   auto pick = [&](auto tag) {
     if (per_lane <= 1) go(tag, std::integral_constant<int, 1>{});
@@ -2618,25 +2673,25 @@ hipError_t launch_lin_vjp(const float* W, const float* P, const float* A, int ns
 hipError_t launch_transpose_cvt(const float* W, void* WT, int BH, int d, bool io_bf16, hipStream_t s) {
   if (BH <= 0 || d <= 0) return hipSuccess;
   const int tiles = (d + 31) / 32;
-  // the descriptor check keeps B*H*ceil(d/128)^2 under 2^24, so this stays under 2^28
+  // callers keep BH * ceil(d / 32)^2 under 2^31 (one set of weights: under 2^28 by the descriptor check)
   const unsigned blocks = (unsigned)((int64_t)BH * tiles * tiles);
   if (io_bf16) k_transpose_cvt<__bf16><<<blocks, 256, 0, s>>>(W, reinterpret_cast<__bf16*>(WT), d, tiles);
   else k_transpose_cvt<float><<<blocks, 256, 0, s>>>(W, reinterpret_cast<float*>(WT), d, tiles);
   return hipGetLastError();
 }
 
-hipError_t launch_lin_tokens(const void* K, const float* eta, void* dk, float* deta, int BH, int64_t n, int d,
-                             int64_t k_inst, int64_t z_inst, int64_t eta_inst, bool io_bf16, hipStream_t s) {
+hipError_t launch_lin_tokens(const void* V, const float* eta, void* dv, float* deta, int BH, int64_t n, int d,
+                             int64_t tok_inst, int64_t eta_inst, bool io_bf16, hipStream_t s) {
   const int64_t rows = (int64_t)BH * n;
   if (rows <= 0) return hipSuccess;
   const int64_t need = (rows + 3) / 4;
   const unsigned blocks = (unsigned)(need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20));
   if (io_bf16)
-    k_lin_tokens<__bf16><<<blocks, 256, 0, s>>>(reinterpret_cast<const __bf16*>(K), eta, reinterpret_cast<__bf16*>(dk),
-                                                deta, BH, n, d, k_inst, z_inst, eta_inst);
+    k_lin_tokens<__bf16><<<blocks, 256, 0, s>>>(reinterpret_cast<const __bf16*>(V), eta, reinterpret_cast<__bf16*>(dv),
+                                                deta, BH, n, d, tok_inst, eta_inst);
   else
-    k_lin_tokens<float><<<blocks, 256, 0, s>>>(reinterpret_cast<const float*>(K), eta, reinterpret_cast<float*>(dk),
-                                               deta, BH, n, d, k_inst, z_inst, eta_inst);
+    k_lin_tokens<float><<<blocks, 256, 0, s>>>(reinterpret_cast<const float*>(V), eta, reinterpret_cast<float*>(dv),
+                                               deta, BH, n, d, tok_inst, eta_inst);
   return hipGetLastError();
 }
 

@@ -184,7 +184,7 @@ def kernel_short_name(name):
     """k_fwd, k_bwd, ... from a mangled (…5k_fwdI…) or demangled (…::k_fwd<…) kernel name."""
     for k in ("k_fwd_narrow", "k_fwd", "k_bwd", "k_update", "k_prep", "k_scale_rows", "k_beta_mean", "k_zero_rows",
               "k_ns_fused_pair_out", "k_ns_fused_pair", "k_ns_fused", "k_ns_final", "k_ns_prep", "k_ns_scale", "k_ns",
-              "k_prologue", "k_rmsnorm_out"):
+              "k_prologue", "k_rmsnorm_out", "k_lin_vjp", "k_lin_tokens", "k_transpose_cvt", "k_sum_parts"):
         m = str(len(k)) + k
         if m + "I" in name or m + "E" in name or "::" + k + "<" in name or "::" + k + "(" in name:
             return k
@@ -608,8 +608,10 @@ def measure(cfg, args, P, on_device=False):
 
 
 # The second workload that the performance target names, measured in the same
-# process after the default one: NVS with a million context tokens.
+# process after the default one: NVS with a million context tokens; then the
+# backward of the linear fast weight at the LM shape.
 SECONDARY = "nvs1m"
+SECONDARY_BWD = "lm32k_linear"
 
 
 def main():
@@ -645,6 +647,12 @@ def main():
         sec = measure(CONFIGS[SECONDARY], args, P, on_device=True)
         keep = ("value", "unit", "ms_per_step", "tokens_per_s", "pct_of_peak", "data", "config", "roofline")
         res["secondary"] = {SECONDARY: {k: sec[k] for k in keep if k in sec}}
+        torch.cuda.empty_cache()
+        # the backward of the linear fast weight at the LM shape (its own metric)
+        bargs = argparse.Namespace(**{**vars(args), "backward": True})
+        bwd = measure(CONFIGS[SECONDARY_BWD], bargs, P)
+        res["secondary"][SECONDARY_BWD + "_backward"] = {"metric": bwd["metric"],
+                                                          **{k: bwd[k] for k in keep if k in bwd}}
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, args.backward)

@@ -35,6 +35,11 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
                    chunk (§3.1 loss and update; §5.4; reverse mode written out
                    by hand: the chunk gradient -sum eta v k^T does not depend
                    on W, so no second derivative enters)
+* backward (SwiGLU) the reverse of the SwiGLU fast weight's chunk loop, the same
+                   cotangents in and out (W0 = (W1, W2, W3)); the chunk
+                   gradient depends on W, so its reverse carries the second
+                   derivative of SiLU (reverse mode written out by hand,
+                   step by step against the forward's closed form)
 * schedule         a list of (mode, begin, end) segments, each one of
                    update-then-apply, apply-then-update, update-only or
                    apply-only on its token range (the ttt_config loop of Alg. 1;
@@ -93,6 +98,8 @@ __all__ = [
     "lact_forward_schedule", "softplus", "qkv_prologue", "rmsnorm_out", "linear_gradient",
     "lact_forward_linear_instance", "lact_forward_linear", "linear_flops", "layer_flops",
     "weight_update_vjp", "lact_backward_linear_instance", "lact_backward_linear",
+    "silu_second_derivative", "swiglu_apply_vjp", "chunk_gradient_vjp", "lact_backward_instance",
+    "lact_backward",
 ]
 
 # Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
@@ -461,6 +468,150 @@ def lact_backward_linear(q, k, v, eta, W0, do, chunk: int, order: int, dW_final=
     idx = range(q.shape[0]) if instances is None else instances
     res = [lact_backward_linear_instance(q[i], k[i], v[i], eta[i], W0[i], do[i], chunk, order,
                                          None if dW_final is None else dW_final[i]) for i in idx]
+    return tuple(np.stack(col) for col in zip(*res))
+
+
+def silu_second_derivative(z: np.ndarray) -> np.ndarray:
+    """d^2 SiLU / dz^2: differentiating s + z s (1 - s) once more with
+    ds/dz = s (1 - s) gives s (1 - s) (2 + z (1 - 2 s))."""
+    s = sigmoid(z)
+    return s * (1.0 - s) * (2.0 + z * (1.0 - 2.0 * s))
+
+
+def swiglu_apply_vjp(W1, W2, W3, X, dO):
+    """Reverse of swiglu_apply: from the cotangent dO [n, d] of O = f_W(X),
+    the cotangents (dX [n, d], dW1 [h, d], dW2 [d, h], dW3 [h, d]).
+
+    With Z1 = X W1^T, Z3 = X W3^T, H = SiLU(Z1) o Z3 and O = H W2^T:
+    dW2 = dO^T H, dH = dO W2, dZ3 = dH o SiLU(Z1), dZ1 = dH o Z3 o SiLU'(Z1),
+    dW1 = dZ1^T X, dW3 = dZ3^T X, dX = dZ1 W1 + dZ3 W3.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    dO = np.asarray(dO, dtype=np.float64)
+    Z1, Z3 = X @ W1.T, X @ W3.T
+    H = silu(Z1) * Z3
+    dH = dO @ W2
+    dZ3 = dH * silu(Z1)
+    dZ1 = dH * Z3 * silu_derivative(Z1)
+    return dZ1 @ W1 + dZ3 @ W3, dZ1.T @ X, dO.T @ H, dZ3.T @ X
+
+
+def chunk_gradient_vjp(W1, W2, W3, K, V, eta, G1, G2, G3):
+    """Reverse of chunk_gradient (one rate per token): from the cotangents
+    (G1, G2, G3) of the gradients (g1, g2, g3), the cotangents
+    (dW1, dW2, dW3, dK, dV, deta) of its inputs.
+
+    The forward in the notation of chunk_gradient, with rates e = eta:
+        Z1 = K W1^T, Z3 = K W3^T, C = V W2, S = SiLU(Z1), S1 = SiLU'(Z1)
+        A  = S o Z3,  R3 = e C o S,  R1 = e C o Z3 o S1
+        g2 = -(e V)^T A,  g3 = -R3^T K,  g1 = -R1^T K
+    and its reverse, one step at a time from the last:
+        dA  = -e (V G2),  dV = -e (A G2^T),  deta = -rowsum(V o (A G2^T))
+        dR3 = -K G3^T,    dK = -R3 G3
+        dR1 = -K G1^T,    dK -= R1 G1
+        R3:  dC = e dR3 o S,  dS = e dR3 o C,  deta += rowsum(dR3 o C o S)
+        R1:  dC += e dR1 o Z3 o S1,  dZ3 = e dR1 o C o S1,
+             dS1 = e dR1 o C o Z3,   deta += rowsum(dR1 o C o Z3 o S1)
+        A:   dS += dA o Z3,  dZ3 += dA o S
+        S, S1 (both of Z1):  dZ1 = dS o S1 + dS1 o SiLU''(Z1)
+        C = V W2:   dV += dC W2^T,  dW2 = V^T dC
+        Z1, Z3:     dK += dZ1 W1 + dZ3 W3,  dW1 = dZ1^T K,  dW3 = dZ3^T K
+    """
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    e = np.asarray(eta, dtype=np.float64)[:, None]
+    G1, G2, G3 = (np.asarray(g, dtype=np.float64) for g in (G1, G2, G3))
+    Z1, Z3, C = K @ W1.T, K @ W3.T, V @ W2
+    S, S1 = silu(Z1), silu_derivative(Z1)
+    A = S * Z3
+    R3, R1 = e * C * S, e * C * Z3 * S1
+    AG2 = A @ G2.T
+    dA = -e * (V @ G2)
+    dV = -e * AG2
+    deta = -np.sum(V * AG2, axis=1)
+    dR3 = -K @ G3.T
+    dR1 = -K @ G1.T
+    dK = -R3 @ G3 - R1 @ G1
+    dC = e * dR3 * S + e * dR1 * Z3 * S1
+    dS = e * dR3 * C + dA * Z3
+    dZ3 = e * dR1 * C * S1 + dA * S
+    dS1 = e * dR1 * C * Z3
+    deta = deta + np.sum(dR3 * C * S, axis=1) + np.sum(dR1 * C * Z3 * S1, axis=1)
+    dZ1 = dS * S1 + dS1 * silu_second_derivative(Z1)
+    dV = dV + dC @ W2.T
+    dK = dK + dZ1 @ W1 + dZ3 @ W3
+    return dZ1.T @ K, V.T @ dC, dZ3.T @ K, dK, dV, deta
+
+
+def lact_backward_instance(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final=None):
+    """Reverse of lact_forward_instance for the SwiGLU fast weight (no Muon,
+    no momentum, one rate per token): given the cotangent ``do`` [n_q, d] of
+    the outputs and optionally ``dW_final`` = (dW1, dW2, dW3) of the returned
+    fast weights, the cotangents (dq, dk, dv, deta, (dW1, dW2, dW3)) of the
+    inputs, the last three those of the initial fast weights.
+
+    The chunk loop is replayed to recover the fast weights entering every
+    chunk; the chunks are then reversed. A chunk's update W' = (n / u)(W - g)
+    per matrix goes back through weight_update_vjp (the cotangent of g is
+    minus that of U) and then through chunk_gradient_vjp (g depends on W, k,
+    v and eta); its apply goes back through swiglu_apply_vjp with the weights
+    it used (entering the chunk with apply-then-update, leaving it with
+    update-then-apply; the tail uses the final weights).
+    """
+    q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
+    eta = np.asarray(eta, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    n_q, n_kv = q.shape[0], k.shape[0]
+    Ws = [tuple(np.asarray(w, dtype=np.float64).copy() for w in (W1, W2, W3))]
+    gs = []
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        g = chunk_gradient(*Ws[-1], k[s:e], v[s:e], eta[s:e])
+        gs.append(g)
+        Ws.append(tuple(weight_update(w, gj) for w, gj in zip(Ws[-1], g)))
+    dW = [np.zeros_like(w) for w in Ws[0]] if dW_final is None else [
+        np.asarray(w, dtype=np.float64).copy() for w in dW_final]
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    deta = np.zeros(n_kv)
+
+    def apply_back(W, s, e):
+        dx, a1, a2, a3 = swiglu_apply_vjp(*W, q[s:e], do[s:e])
+        dq[s:e] = dx
+        for j, a in enumerate((a1, a2, a3)):
+            dW[j] += a
+
+    if n_q > n_kv:
+        apply_back(Ws[-1], n_kv, n_q)
+    starts = list(range(0, n_kv, chunk))
+    for c in reversed(range(len(starts))):
+        s, e = starts[c], min(n_kv, starts[c] + chunk)
+        if order == 1:                      # applied with the weights leaving the chunk
+            apply_back(Ws[c + 1], s, e)
+        dg = []
+        for j in range(3):
+            dW[j], dgj = weight_update_vjp(Ws[c][j], gs[c][j], dW[j])
+            dg.append(dgj)
+        b1, b2, b3, dkc, dvc, detac = chunk_gradient_vjp(*Ws[c], k[s:e], v[s:e], eta[s:e], *dg)
+        dW[0] += b1
+        dW[1] += b2
+        dW[2] += b3
+        dk[s:e], dv[s:e], deta[s:e] = dkc, dvc, detac
+        if order == 0:                      # applied with the weights entering the chunk
+            apply_back(Ws[c], s, e)
+    return dq, dk, dv, deta, tuple(dW)
+
+
+def lact_backward(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final=None, instances=None):
+    """Batched driver of lact_backward_instance: (dq, dk, dv, deta, dW1, dW2,
+    dW3) stacked over the selected instances; dW_final is None or a triple
+    of [BH, ...] arrays."""
+    idx = range(q.shape[0]) if instances is None else instances
+    res = []
+    for i in idx:
+        dq, dk, dv, deta, dW = lact_backward_instance(
+            q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], do[i], chunk, order,
+            None if dW_final is None else tuple(w[i] for w in dW_final))
+        res.append((dq, dk, dv, deta, *dW))
     return tuple(np.stack(col) for col in zip(*res))
 
 

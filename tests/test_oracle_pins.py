@@ -906,3 +906,170 @@ def test_linear_backward_finite_differences():
             minus[which][idx] -= h
             fd = (readout(*plus) - readout(*minus)) / (2 * h)
             assert abs(fd - grads[which][idx]) <= 1e-6 * max(1.0, abs(fd)), (order, which, idx, fd, grads[which][idx])
+
+
+# ----------------------------------------------------------------------------- SwiGLU backward
+
+
+def _torch_swiglu_t(W1, W2, W3, X):
+    """Library SwiGLU MLP on tensors (autograd sees it): F.linear + F.silu."""
+    return F.linear(F.silu(F.linear(X, W1)) * F.linear(X, W3), W2)
+
+
+def test_silu_second_derivative_matches_autograd():
+    z = torch.linspace(-30.0, 30.0, 241, requires_grad=True)
+    (g,) = torch.autograd.grad(F.silu(z).sum(), z, create_graph=True)
+    (gg,) = torch.autograd.grad(g.sum(), z)
+    assert np.allclose(O.silu_second_derivative(z.detach().numpy()), gg.numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_swiglu_apply_vjp_matches_autograd():
+    rng = _rng(111)
+    h, d, n = 7, 5, 9
+    W1, W2, W3 = _weights(rng, h, d)
+    X, dO = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    W1t, W2t, W3t, Xt = t(W1), t(W2), t(W3), t(X)
+    (_torch_swiglu_t(W1t, W2t, W3t, Xt) * torch.tensor(dO)).sum().backward()
+    got = O.swiglu_apply_vjp(W1, W2, W3, X, dO)
+    for g, ref in zip(got, (Xt, W1t, W2t, W3t)):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def _torch_chunk_gradient(W1, W2, W3, K, V, eta):
+    """The chunk gradient by torch autograd of the chunk loss, kept in the
+    graph (create_graph) so that it can be differentiated again."""
+    loss = -(eta[:, None] * _torch_swiglu_t(W1, W2, W3, K) * V).sum()
+    return torch.autograd.grad(loss, (W1, W2, W3), create_graph=True)
+
+
+def test_chunk_gradient_vjp_matches_double_backward():
+    rng = _rng(112)
+    h, d, n = 6, 4, 11
+    W1, W2, W3 = _weights(rng, h, d)
+    K, V = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    eta = 0.1 + rng.random(n)
+    G = (rng.standard_normal((h, d)), rng.standard_normal((d, h)), rng.standard_normal((h, d)))
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    ins = [t(a) for a in (W1, W2, W3, K, V, eta)]
+    g = _torch_chunk_gradient(*ins)
+    # the oracle's forward closed form is the autograd gradient
+    for a, b in zip(g, O.chunk_gradient(W1, W2, W3, K, V, eta)):
+        assert np.allclose(a.detach().numpy(), b, rtol=1e-11, atol=1e-12)
+    sum(((gj * torch.tensor(Gj)).sum() for gj, Gj in zip(g, G))).backward()
+    got = O.chunk_gradient_vjp(W1, W2, W3, K, V, eta, *G)
+    for name, a, ref in zip(("dW1", "dW2", "dW3", "dK", "dV", "deta"), got, ins):
+        assert np.allclose(a, ref.grad.numpy(), rtol=1e-10, atol=1e-12), name
+
+
+def _torch_swiglu_layer(q, k, v, eta, W, chunk, order):
+    """The SwiGLU fast weight's chunk loop in torch: the chunk gradient by
+    autograd (create_graph), the row-norm-preserving update, both orders and
+    an apply-only tail; autograd sees every step."""
+    n_q, n_kv = q.shape[0], k.shape[0]
+    outs = []
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        if order == 0:
+            outs.append(_torch_swiglu_t(*W, q[s:e]))
+        g = _torch_chunk_gradient(*W, k[s:e], v[s:e], eta[s:e])
+        new = []
+        for w, gj in zip(W, g):
+            U = w - gj
+            new.append(U * (torch.linalg.vector_norm(w, dim=1, keepdim=True)
+                            / torch.linalg.vector_norm(U, dim=1, keepdim=True)))
+        W = tuple(new)
+        if order == 1:
+            outs.append(_torch_swiglu_t(*W, q[s:e]))
+    if n_q > n_kv:
+        outs.append(_torch_swiglu_t(*W, q[n_kv:]))
+    return torch.cat(outs), W
+
+
+@pytest.mark.parametrize("order,final", [(0, False), (1, False), (0, True), (1, True)])
+def test_swiglu_backward_matches_autograd(order, final):
+    # several chunks, the last one ragged, an apply-only tail, non-square h x d
+    rng = _rng(113 + order + 2 * final)
+    d, h, n_kv, n_q, C = 5, 7, 17, 21, 6
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random(n_kv)
+    W0 = _weights(rng, h, d, unit=True)
+    do = rng.standard_normal((n_q, d))
+    dWf = tuple(rng.standard_normal(w.shape) for w in W0) if final else None
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    qt, kt, vt, et = t(q), t(k), t(v), t(eta)
+    Wt = tuple(t(w) for w in W0)
+    o, Wfin = _torch_swiglu_layer(qt, kt, vt, et, Wt, C, order)
+    loss = (o * torch.tensor(do)).sum()
+    if final:
+        loss = loss + sum((w * torch.tensor(x)).sum() for w, x in zip(Wfin, dWf))
+    loss.backward()
+    dq, dk, dv, deta, dW = O.lact_backward_instance(q, k, v, eta, *W0, do, C, order, dWf)
+    for name, g, ref in zip(("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3"), (dq, dk, dv, deta, *dW),
+                            (qt, kt, vt, et, *Wt)):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-9, atol=1e-11), name
+    # the forward the backward replays is the oracle's own forward
+    o_ref, W_ref = O.lact_forward_instance(q, k, v, eta, *W0, C, order)
+    assert np.allclose(o.detach().numpy(), o_ref, rtol=1e-12, atol=1e-13)
+    for a, b in zip(Wfin, W_ref):
+        assert np.allclose(a.detach().numpy(), b, rtol=1e-12, atol=1e-13)
+
+
+def test_swiglu_backward_finite_differences():
+    # central differences of the NumPy forward oracle on a scalar read-out
+    rng = _rng(118)
+    d, h, n_kv, n_q, C = 4, 6, 9, 11, 4
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.3 * rng.random(n_kv)
+    W0 = _weights(rng, h, d, unit=True)
+    do = rng.standard_normal((n_q, d))
+    dWf = tuple(rng.standard_normal(w.shape) for w in W0)
+    for order in (0, 1):
+        def readout(q_, k_, v_, eta_, W1_, W2_, W3_):
+            o, W = O.lact_forward_instance(q_, k_, v_, eta_, W1_, W2_, W3_, C, order)
+            return float(np.sum(o * do) + sum(np.sum(a * b) for a, b in zip(W, dWf)))
+        dq, dk, dv, deta, dW = O.lact_backward_instance(q, k, v, eta, *W0, do, C, order, dWf)
+        grads = (dq, dk, dv, deta, *dW)
+        args = [q, k, v, eta, *W0]
+        for which, idx in ((0, (3, 1)), (0, (10, 2)), (1, (2, 0)), (1, (8, 3)), (2, (5, 1)), (3, (6,)),
+                           (4, (1, 2)), (5, (3, 4)), (6, (5, 0))):
+            eps = 1e-6
+            plus = [a.copy() for a in args]
+            minus = [a.copy() for a in args]
+            plus[which][idx] += eps
+            minus[which][idx] -= eps
+            fd = (readout(*plus) - readout(*minus)) / (2 * eps)
+            assert abs(fd - grads[which][idx]) <= 2e-6 * max(1.0, abs(fd)), (order, which, idx, fd, grads[which][idx])
+
+
+def test_swiglu_backward_at_eta_zero_is_the_apply_chain():
+    # eta = 0: the gradient is zero for every W, so each update is the
+    # identity map and passes the weights' cotangent through unchanged; k and
+    # v get none, and dW0 is the apply's reverse over all tokens at once
+    rng = _rng(119)
+    d, h, n, C = 4, 6, 10, 4
+    q, k, v = _tokens(rng, n, d), _tokens(rng, n, d), _tokens(rng, n, d)
+    W0 = _weights(rng, h, d, unit=True)
+    do = rng.standard_normal((n, d))
+    for order in (0, 1):
+        dq, dk, dv, deta, dW = O.lact_backward_instance(q, k, v, np.zeros(n), *W0, do, C, order)
+        dx, a1, a2, a3 = O.swiglu_apply_vjp(*W0, q, do)
+        assert np.allclose(dq, dx, rtol=1e-12, atol=1e-13)
+        assert np.array_equal(dk, np.zeros_like(dk)) and np.array_equal(dv, np.zeros_like(dv))
+        for g, a in zip(dW, (a1, a2, a3)):
+            assert np.allclose(g, a, rtol=1e-11, atol=1e-12)
+
+
+def test_swiglu_backward_batched_driver_stacks_instances():
+    rng = _rng(120)
+    BH, d, h, n, C = 3, 4, 6, 9, 4
+    q, k, v = (np.stack([_tokens(rng, n, d) for _ in range(BH)]) for _ in range(3))
+    eta = 0.1 + 0.3 * rng.random((BH, n))
+    Ws = [_weights(rng, h, d, unit=True) for _ in range(BH)]
+    W1, W2, W3 = (np.stack([w[j] for w in Ws]) for j in range(3))
+    do = rng.standard_normal((BH, n, d))
+    got = O.lact_backward(q, k, v, eta, W1, W2, W3, do, C, 1, instances=[2, 0])
+    for pos, i in enumerate((2, 0)):
+        dq, dk, dv, deta, dW = O.lact_backward_instance(q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], do[i], C, 1)
+        for a, b in zip(got, (dq, dk, dv, deta, *dW)):
+            assert np.array_equal(a[pos], b)

@@ -25,8 +25,9 @@
  *
  * Entry points: lact_forward (the path above), lact_forward_momentum (the
  * momentum test-time optimizer, App. A), lact_forward_schedule (a caller-given
- * list of update/apply segments, Alg. 1), lact_backward_linear (the reverse of
- * the linear fast weight's chunk loop), lact_prologue and lact_rmsnorm_out
+ * list of update/apply segments, Alg. 1), lact_backward and
+ * lact_backward_linear (the reverse of the chunk loop, SwiGLU and linear
+ * fast weight), lact_prologue and lact_rmsnorm_out
  * (the layer's steps on either side of the path, Alg. 1); per-matrix learning
  * rates through lact_desc.eta_per_matrix.
  *
@@ -264,7 +265,9 @@ int lact_forward_schedule(const lact_desc* desc,
  * gives dq_i = W^T dO_i.
  *
  * Requires desc->fast_weight == LACT_FW_LINEAR and use_muon == 0 (else
- * LACT_EUNSUPPORTED); other fields as lact_forward.
+ * LACT_EUNSUPPORTED); other fields as lact_forward. The workspace size
+ * (lact_backward_workspace_bytes) covers both backward entry points: it
+ * follows desc->fast_weight.
  *
  *   q, k, v, eta        the forward's inputs (as lact_forward)              in
  *   W0       [B*H, d, d]   fp32, the fast weight BEFORE the forward           in
@@ -290,6 +293,50 @@ int lact_backward_linear(const lact_desc* desc,
                          void* dq, void* dk, void* dv, float* deta, float* dW0,
                          void* workspace, size_t workspace_bytes,
                          void* stream);
+
+/*
+ * Backward of lact_forward for the SwiGLU fast weight (§3.1 loss, chunk
+ * gradient and SwiGLU eqs.; §3.2 per-row norm-preserving update; Alg. 1),
+ * without Muon or momentum and with one rate per token (else
+ * LACT_EUNSUPPORTED). Given the cotangent dO of the outputs and optionally
+ * those of the final fast weights, the cotangents of every input: the
+ * reverse of the chunk loop, with the weights and negated gradients of every
+ * chunk recomputed by the forward's own launches and kept in the workspace.
+ * A chunk's update W' = (n / u)(W - g) goes back through the row rescaling
+ * (as in lact_backward_linear) and then through the chunk gradient g, which
+ * depends on W1, W2, W3, k, v and eta (its reverse carries SiLU's second
+ * derivative); the apply o = W2 [SiLU(W1 q) o (W3 q)] goes back with the
+ * weights it used (entering the chunk with apply-then-update, leaving it
+ * with update-then-apply; the tail with the final weights).
+ *
+ *   q, k, v, eta          the forward's inputs (as lact_forward)                in
+ *   W1, W2, W3            fp32 fast weights BEFORE the forward (not written)     in
+ *   dout   [B*H, n_q, d]  io_dtype, cotangent of o                               in
+ *   dW1_final, dW2_final, dW3_final  fp32 cotangents of the final fast weights,
+ *                         each may be NULL (zero)                                in
+ *   dq     [B*H, n_q, d]  io_dtype                                               out
+ *   dk, dv [B*H, n_kv, d] io_dtype                                               out
+ *   deta   [B*H, n_kv]    fp32                                                   out
+ *   dW1, dW2, dW3         fp32, shapes of W1, W2, W3: cotangents of the initial
+ *                         fast weights                                           out
+ *   workspace   >= lact_backward_workspace_bytes(desc), 256-byte aligned (it
+ *               holds every chunk's weights and gradient partials, about
+ *               (3 + 3 * splits) * B*H * d*h * 4 bytes per chunk, plus buffers
+ *               of a chunk's tokens)
+ *
+ * Every element of the outputs is written. Pointers are device pointers,
+ * 16-byte aligned (eta and deta: 4); outputs must not alias inputs, each
+ * other or the workspace. Errors as lact_forward, validated before any HIP
+ * call.
+ */
+int lact_backward(const lact_desc* desc,
+                  const void* q, const void* k, const void* v, const float* eta,
+                  const float* W1, const float* W2, const float* W3, const void* dout,
+                  const float* dW1_final, const float* dW2_final, const float* dW3_final,
+                  void* dq, void* dk, void* dv, float* deta,
+                  float* dW1, float* dW2, float* dW3,
+                  void* workspace, size_t workspace_bytes,
+                  void* stream);
 
 /*
  * The layer's steps on either side of the path (Alg. 1, layer), each one pass

@@ -28,10 +28,11 @@ Recipe (one (seed, config) -> one set of host arrays):
   projection of the token, App. A; a unit-variance logit stands in for the
   projection), so the other seven draws are the same with or without it.
 
-Cotangents for the backward of the linear fast weight (``make_cotangents``),
-from their own two sub-streams of ``SeedSequence([seed, 1])``: dO ~ N(0, 1/d)
-per element in the shape of q (rounded to bfloat16 for bf16 workloads) and
-the cotangent of the final fast weight ~ N(0, 1/d) per element, float32.
+Cotangents for the backward (``make_cotangents``), from their own two
+sub-streams of ``SeedSequence([seed, 1])``: dO ~ N(0, 1/d) per element in the
+shape of q (rounded to bfloat16 for bf16 workloads) and the cotangents of the
+final fast weights ~ N(0, 1/d) per element, float32 (one d x d matrix for the
+linear fast weight, else W1, W2, W3 in that order from the second stream).
 """
 from __future__ import annotations
 
@@ -179,14 +180,21 @@ def make_inputs(cfg: LactConfig, seed: int = 0, heads: list | None = None):
 
 
 def make_cotangents(cfg: LactConfig, seed: int = 0, heads: list | None = None):
-    """Seeded cotangents of the linear fast weight's outputs: dict with
-    ``do`` [n, n_q, d] (the I/O precision's values, float32 arrays) and
-    ``dW`` [n, d, d] float32, n = the number of kept instances."""
+    """Seeded cotangents of the layer's outputs: dict with ``do`` [n, n_q, d]
+    (the I/O precision's values, float32 arrays) and the final fast weights'
+    cotangents, float32: ``dW`` [n, d, d] for the linear fast weight, else
+    ``dW1``, ``dW3`` [n, h, d] and ``dW2`` [n, d, h] (drawn in that order);
+    n = the number of kept instances."""
     rd, rw = (np.random.default_rng(s) for s in np.random.SeedSequence([seed, 1]).spawn(2))
     n = cfg.BH if heads is None else len(heads)
     std = 1.0 / np.sqrt(cfg.d)
     do = rd.standard_normal((n, cfg.n_q, cfg.d), dtype=np.float32) * np.float32(std)
     if cfg.io == "bf16":
         do = round_to_bf16(do)
-    dW = rw.standard_normal((n, cfg.d, cfg.d), dtype=np.float32) * np.float32(std)
-    return dict(do=do, dW=dW)
+    if cfg.linear:
+        dW = rw.standard_normal((n, cfg.d, cfg.d), dtype=np.float32) * np.float32(std)
+        return dict(do=do, dW=dW)
+    dW1 = rw.standard_normal((n, cfg.h, cfg.d), dtype=np.float32) * np.float32(std)
+    dW2 = rw.standard_normal((n, cfg.d, cfg.h), dtype=np.float32) * np.float32(std)
+    dW3 = rw.standard_normal((n, cfg.h, cfg.d), dtype=np.float32) * np.float32(std)
+    return dict(do=do, dW1=dW1, dW2=dW2, dW3=dW3)

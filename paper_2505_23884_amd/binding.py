@@ -72,6 +72,8 @@ def load_library(path: str | None = None):
     L.lact_backward_workspace_bytes.restype = sz
     L.lact_backward_linear.argtypes = [dp] + [vp] * 12 + [vp, sz, vp]
     L.lact_backward_linear.restype = i32
+    L.lact_backward.argtypes = [dp] + [vp] * 19 + [sz, vp]
+    L.lact_backward.restype = i32
     f32 = ctypes.c_float
     L.lact_prologue.argtypes = [dp, vp, vp, f32, vp, vp, vp, vp, vp, vp, vp]
     L.lact_prologue.restype = i32
@@ -318,6 +320,45 @@ def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_f
     if rc:
         _raise(rc)
     return dq, dk, dv, deta, dW0
+
+
+def backward(q, k, v, eta, W1, W2, W3, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, out=None,
+             workspace=None, stream=None):
+    """Backward of forward() for the SwiGLU fast weight (lact_backward), no
+    Muon or momentum: the cotangents of q, k, v, eta and of the initial fast
+    weights W1, W2, W3 (fp32, not written) given dout (q's shape and dtype)
+    and, optionally, dW_final = (dW1, dW2, dW3) of the final fast weights (any
+    of them None). Returns (dq, dk, dv, deta, dW1, dW2, dW3), written into
+    ``out`` (a tuple of seven tensors of those shapes) when it is given."""
+    import torch
+    dWf = tuple(dW_final) if dW_final is not None else (None, None, None)
+    extra = [(t, name) for t, name in zip(dWf, ("dW1_final", "dW2_final", "dW3_final")) if t is not None]
+    if dout.shape != q.shape or dout.dtype != q.dtype:
+        raise LactError(-1, "dout must have q's shape and dtype")
+    for t, ref in zip(dWf, (W1, W2, W3)):
+        if t is not None and (t.shape != ref.shape or t.dtype != torch.float32):
+            raise LactError(-1, "dW_final tensors must have the fast weights' shapes, fp32")
+    desc, dq, _, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, False, 0,
+                                   None if out is None else out[0], None, stream, FW_SWIGLU, need_workspace=False)
+    if not dout.is_cuda or not dout.is_contiguous():
+        raise LactError(-1, "dout must be a contiguous device tensor")
+    if workspace is None:
+        workspace = torch.empty(max(backward_workspace_bytes(desc), 1), dtype=torch.uint8, device=q.device)
+    if out is None:
+        res = (dq, torch.empty_like(k), torch.empty_like(v), torch.empty_like(eta), torch.empty_like(W1),
+               torch.empty_like(W2), torch.empty_like(W3))
+    else:
+        res = tuple(out)
+        for t, ref, name in zip(res, (q, k, v, eta, W1, W2, W3), ("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3")):
+            if t.shape != ref.shape or t.dtype != ref.dtype or not t.is_cuda or not t.is_contiguous():
+                raise LactError(-1, f"{name} must be a contiguous device tensor shaped like its input")
+    rc = lib().lact_backward(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(W1), _ptr(W2), _ptr(W3),
+                             _ptr(dout), _ptr(dWf[0]), _ptr(dWf[1]), _ptr(dWf[2]), *(_ptr(t) for t in res),
+                             _ptr(workspace), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                             ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return res
 
 
 def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_steps=5, beta=None,

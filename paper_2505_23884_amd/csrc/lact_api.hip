@@ -86,7 +86,7 @@ int check_desc(const lact_desc* d) {
   return LACT_OK;
 }
 
-Plan make_plan(const lact_desc* dsc) {
+Plan make_plan(const lact_desc* dsc, bool allow_fused = true) {
   Plan p{};
   p.BH = dsc->B * dsc->H;
   p.d = dsc->d;
@@ -132,8 +132,8 @@ Plan make_plan(const lact_desc* dsc) {
   // apply tiles share the launch (apply-then-update, or more than one chunk)
   // and take the CUs the row tiles leave.
   const int upd_cols = grad_upd_tile().cols;
-  const bool upd_shape = p.bf16 && !p.linear && !dsc->use_muon && p.d > 256 && p.h > 256 && p.d <= upd_cols &&
-                         p.h <= upd_cols;
+  const bool upd_shape = allow_fused && p.bf16 && !p.linear && !dsc->use_muon && p.d > 256 && p.h > 256 &&
+                         p.d <= upd_cols && p.h <= upd_cols;
   const bool apply_alongside = dsc->order == LACT_APPLY_THEN_UPDATE || dsc->n_kv > p.C;
   int64_t ns;
   if (upd_shape && tiles >= 128 && (p.C < 8192 || apply_alongside)) {
@@ -295,6 +295,7 @@ struct Ctx {
   BwdArgs out_pending{};   // with ns_out: the output tiles the next Newton-Schulz launch runs
   double out_flops = 0.0;
   bool has_out = false;
+  const float* Wsrc[3] = {};   // where the update reads the state (nullptr: W, in place)
 };
 
 // Momentum factor of the current chunk for instance 0 (stride kBetaBatch).
@@ -765,6 +766,7 @@ int finish_update(Ctx& c) {
   UpdArgs u{};
   for (int m = 0; m < p.nmat; ++m) {
     u.W[m] = c.W[m];
+    u.Wsrc[m] = c.Wsrc[m];
     u.Wb[m] = p.bf16 ? c.wb[c.wset][m] : nullptr;
   }
   u.nmat = p.nmat;
@@ -1270,14 +1272,16 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     if (rc) return rc;
   }
   // transposed operand copies of W_0 .. W_nch (W_1 .. W_nch are contiguous)
-  rc = timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_transpose_cvt(W0, wt(0), p.BH, p.d, p.bf16, s); });
+  rc = timed(LACT_KCLASS_PREP, 0.0, s,
+             [&] { return launch_copy_w(W0, dd, wt(0), d, dd, p.BH, p.d, p.d, true, p.bf16, s); });
   if (rc) return rc;
   {
     const int64_t t = cdiv(d, 32), per = std::max<int64_t>(1, ((int64_t)1 << 30) / (BH * t * t));
     for (int64_t c0 = 1; c0 <= L.nch; c0 += per) {   // whole sets of BH matrices, under 2^30 blocks
       const int64_t m = std::min(per, L.nch + 1 - c0);
-      rc = timed(LACT_KCLASS_PREP, 0.0, s,
-                 [&] { return launch_transpose_cvt(traj(c0), wt(c0), (int)(m * BH), p.d, p.bf16, s); });
+      rc = timed(LACT_KCLASS_PREP, 0.0, s, [&] {
+        return launch_copy_w(traj(c0), dd, wt(c0), d, dd, (int)(m * BH), p.d, p.d, true, p.bf16, s);
+      });
       if (rc) return rc;
     }
   }
@@ -1297,16 +1301,16 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
       rc = lin_launch(p, s, b, 2, 4.0 * BH * n * dd);
       if (rc) return rc;
       const int mode = first ? (dWf ? 1 : 0) : 2;
-      const int ns = b.seg[0].nsplit;
+      const PartSet ps{tpart, b.seg[0].nsplit, psplit, dd};
       rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
-                 [&] { return launch_sum_parts(G, dWf, mode, tpart, ns, psplit, BH * dd, s); });
+                 [&] { return launch_accum(G, dd, dWf, dd, mode, ps, PartSet{}, p.BH, dd, s); });
       if (rc) return rc;
       first = false;
     }
   }
   if (first) {
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
-               [&] { return launch_sum_parts(G, dWf, dWf ? 1 : 0, nullptr, 0, psplit, BH * dd, s); });
+               [&] { return launch_accum(G, dd, dWf, dd, dWf ? 1 : 0, PartSet{}, PartSet{}, p.BH, dd, s); });
     if (rc) return rc;
   }
   const bool then_apply = desc->order == LACT_UPDATE_THEN_APPLY;
@@ -1314,10 +1318,25 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
   uint8_t* ut = ws + L.off_ut;
   for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
     const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
-      return launch_lin_vjp(traj(ci), Pall + ci * psplit, Aall + ci * psplit, 1, psplit, then_apply, G, ub, ut,
-                            p.BH, p.d, p.bf16, s);
-    });
+    VjpArgs va{};
+    va.W = traj(ci);
+    va.w_inst = dd;
+    va.P = PartSet{Pall + ci * psplit, 1, psplit, dd};
+    const PartSet ac{Aall + ci * psplit, 1, psplit, dd};
+    if (then_apply) va.pre[0] = ac;   // applied with the weights leaving the chunk
+    else va.post = ac;
+    va.G = G;
+    va.g_inst = dd;
+    va.Ub = ub;
+    va.ub_ld = d;
+    va.ub_inst = dd;
+    va.UT = ut;
+    va.ut_ld = d;
+    va.ut_inst = dd;
+    va.BH = p.BH;
+    va.R = p.d;
+    va.L = p.d;
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(va, p.bf16, s); });
     if (rc) return rc;
     BwdArgs b{};
     lin_out_seg(b.seg[0], p, op(kb + s0 * d * esz, d, n_kv * d), op(ub, d, dd), (uint8_t*)dv + s0 * d * esz,
@@ -1336,6 +1355,402 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
                                n_kv * d, n_kv, p.bf16, s);
     });
     if (rc) return rc;
+  }
+  return LACT_OK;
+}
+
+// Reverse of the SwiGLU fast weight's chunk loop (§3.1 loss and chunk
+// gradient, §3.2 per-row norm-preserving update; Alg. 1), no Muon or
+// momentum, one rate per token. The forward's own update launches replay
+// the chunk loop (unfused, so that every chunk's negated gradient P_c stays
+// in a slot of its own, and reading W_c from the trajectory while writing
+// W_{c+1}). The reverse then walks the chunks from the last, carrying the
+// cotangent of (W1, W2, W3) in dW1, dW2, dW3. Per chunk: the row-wise reverse
+// of the update (three matrices), six [n x h] products (Z1 = K W1^T,
+// Z3 = K W3^T, C = V W2 and the same three with the update's cotangent), the
+// per-token step with SiLU's first and second derivatives, dk (one product
+// over 4h) and dv (over 2h), the weight cotangents of the gradient's own
+// dependence on W (GRAD13 + GRAD2), and the apply's reverse (three [n x h]
+// products, a per-token step, dq over 2h, its weight cotangents). The
+// contractions are the OUT and GRAD kinds with operands laid out so that
+// each sum runs over one contiguous row ([R3 | R1 | dZ1 | dZ3] against
+// [U3^T | U1^T | W1^T | W3^T], [eta A | dC] against [U2 | W2]).
+struct SwBwdLayout {
+  Plan p;               // the forward's plan without the fused gradient-and-update kind
+  int64_t nch;          // chunks of the forward
+  int64_t T;            // token rows of the chunk buffers (a chunk, or a piece of the tail)
+  int64_t tail_split;   // tokens per split of a tail piece (at most p.nsplit splits)
+  size_t slotP;         // bytes of one chunk's gradient partials
+  size_t off_P, off_traj, off_z[6], off_pk, off_pv, off_u[3], off_a[3], off_bk, off_bv, off_bq, off_ur[3],
+      off_apart, off_bpart, total;
+};
+
+int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L) {
+  int rc = check_desc(dsc);
+  if (rc) return rc;
+  if (dsc->fast_weight != LACT_FW_SWIGLU || dsc->use_muon || dsc->eta_per_matrix) return LACT_EUNSUPPORTED;
+  L->p = make_plan(dsc, false);
+  const Plan& p = L->p;
+  const double dh = (double)p.d * p.h;
+  L->nch = dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0;
+  const int64_t tail = dsc->n_q - dsc->n_kv;
+  L->T = std::max<int64_t>(1, std::max<int64_t>(p.C, std::min<int64_t>(tail, 4096)));
+  const double need = (double)L->nch * p.BH * dh * 12.0 * (p.nsplit + 1) + (double)p.BH * L->T * p.h * p.esz * 12.0;
+  if (need > 4.0e18) return LACT_EUNSUPPORTED;
+  L->tail_split = std::max<int64_t>(32, cdiv(cdiv(L->T, p.nsplit), 32) * 32);
+  const size_t w4 = (size_t)p.BH * p.d * p.h * 4, wio = (size_t)p.BH * p.d * p.h * p.esz;
+  const size_t rows = (size_t)p.BH * L->T * p.h * p.esz;   // one [T x h] buffer
+  L->slotP = (size_t)p.nsplit * 3 * w4;
+  // the forward's own layout first (at least what its validation asks for)
+  size_t o = align_up(std::max(p.total, make_plan(dsc).total));
+  L->off_P = o;
+  o = align_up(o + (size_t)L->nch * L->slotP);
+  L->off_traj = o;
+  o = align_up(o + (size_t)L->nch * 3 * w4);
+  for (int i = 0; i < 6; ++i) {
+    L->off_z[i] = o;
+    o = align_up(o + rows);
+  }
+  L->off_pk = o;
+  o = align_up(o + 4 * rows);
+  L->off_pv = o;
+  o = align_up(o + 2 * rows);
+  for (int i = 0; i < 3; ++i) {   // W1, W3 row-major and W2^T of the update's weights, then the apply's
+    L->off_u[i] = o;
+    o = align_up(o + wio);
+  }
+  for (int i = 0; i < 3; ++i) {
+    L->off_a[i] = o;
+    o = align_up(o + wio);
+  }
+  L->off_bk = o;   // [d x 4h]: U3^T | U1^T | W1^T | W3^T
+  o = align_up(o + 4 * wio);
+  L->off_bv = o;   // [d x 2h]: U2 | W2
+  o = align_up(o + 2 * wio);
+  L->off_bq = o;   // [d x 2h]: W1^T | W3^T of the apply's weights
+  o = align_up(o + 2 * wio);
+  for (int i = 0; i < 3; ++i) {   // U1, U3 row-major and U2^T
+    L->off_ur[i] = o;
+    o = align_up(o + wio);
+  }
+  L->off_apart = o;
+  o = align_up(o + (size_t)p.nsplit * 3 * w4);
+  L->off_bpart = o;
+  o = align_up(o + (size_t)p.nsplit * 3 * w4);
+  L->total = o;
+  return LACT_OK;
+}
+
+int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                        const float* const W0[3], const void* dout, const float* const dWf[3], void* dq, void* dk,
+                        void* dv, float* deta, float* const dW[3], void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  SwBwdLayout L;
+  int rc = sw_bwd_layout(desc, &L);
+  if (rc) return rc;
+  const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
+  for (int m = 0; m < 3; ++m) {
+    if (!W0[m] || !dW[m]) return LACT_EINVAL;
+    if (misaligned(W0[m]) || misaligned(dW[m]) || (dWf[m] && misaligned(dWf[m]))) return LACT_EALIGN;
+  }
+  if (any_q && (!q || !dout || !dq)) return LACT_EINVAL;
+  if (any_kv && (!k || !v || !eta || !dk || !dv || !deta)) return LACT_EINVAL;
+  if (any_q && (misaligned(q) || misaligned(dout) || misaligned(dq))) return LACT_EALIGN;
+  if (any_kv && (misaligned(k) || misaligned(v) || misaligned(dk) || misaligned(dv))) return LACT_EALIGN;
+  if (any_kv && (((uintptr_t)eta & 3) || ((uintptr_t)deta & 3))) return LACT_EALIGN;
+  if (!workspace || workspace_bytes < L.total) return LACT_EWORKSPACE;
+  if ((uintptr_t)workspace & (kAlign - 1)) return LACT_EALIGN;
+  Ctx c;
+  // the forward's context; its updates read W_c and write W_{c+1} in the
+  // trajectory, never W0
+  rc = setup(c, desc, q, k, v, eta, nullptr, const_cast<float*>(W0[0]), const_cast<float*>(W0[1]),
+             const_cast<float*>(W0[2]), nullptr, dq, workspace, workspace_bytes, stream);
+  if (rc) return rc;
+  c.p = L.p;
+  const Plan& p = c.p;
+  const hipStream_t s = c.s;
+  uint8_t* ws = c.ws;
+  const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk, d = p.d, h = p.h, BH = p.BH;
+  const int64_t dh = d * h, esz = p.esz;
+  const size_t w4 = (size_t)BH * dh * 4;
+  const int64_t psplit = BH * 3 * dh;   // floats between splits of a partial set
+  auto traj = [&](int64_t i, int m) -> float* {
+    return i == 0 ? const_cast<float*>(W0[m])
+                  : reinterpret_cast<float*>(ws + L.off_traj + ((size_t)(i - 1) * 3 + m) * w4);
+  };
+  rc = prepare_weights(c);
+  if (rc) return rc;
+  for (int64_t ci = 0; ci < L.nch; ++ci) {
+    const int64_t s0 = ci * C, s1 = std::min(n_kv, s0 + C);
+    for (int m = 0; m < 3; ++m) {
+      c.W[m] = traj(ci + 1, m);
+      c.Wsrc[m] = traj(ci, m);
+    }
+    if (!p.bf16) {   // fp32: the contractions read the state itself
+      c.wop[0] = op(traj(ci, 0), d, dh);
+      c.wop[1] = op(traj(ci, 1), h, dh);
+      c.wop[2] = op(traj(ci, 2), d, dh);
+    }
+    c.p.off_step = L.off_P + (size_t)ci * L.slotP;
+    c.chunk_idx = ci;
+    rc = update_chunk(c, s0, s1, false);
+    if (rc) return rc;
+  }
+  c.p.off_step = L.p.off_step;
+  const uint8_t* qb = (const uint8_t*)q;
+  const uint8_t* kb = (const uint8_t*)k;
+  const uint8_t* vb = (const uint8_t*)v;
+  const uint8_t* ob = (const uint8_t*)dout;
+  uint8_t* zb[6];
+  for (int i = 0; i < 6; ++i) zb[i] = ws + L.off_z[i];
+  uint8_t* pk = ws + L.off_pk;
+  uint8_t* pv = ws + L.off_pv;
+  uint8_t* bk = ws + L.off_bk;
+  uint8_t* bv = ws + L.off_bv;
+  uint8_t* bq = ws + L.off_bq;
+  float* apart = reinterpret_cast<float*>(ws + L.off_apart);
+  float* bpart = reinterpret_cast<float*>(ws + L.off_bpart);
+  const int64_t T = L.T;
+  // one launch of up to three OUT segments, out[t][m] = sum_e a[t][e] b[m][e]
+  // over K columns, rows of out `rows_out` wide
+  struct Out {
+    Operand a, b;
+    void* out;
+    int64_t out_inst;
+  };
+  auto outs = [&](const Out* o, int nseg, int64_t n, int rows_out, int K) -> int {
+    BwdArgs b{};
+    const TileShape t = bwd_tile(BWD_OUT, p.bf16, p.narrow);
+    for (int i = 0; i < nseg; ++i) {
+      BwdSeg& g = b.seg[i];
+      g.kind = BWD_OUT;
+      g.tiles_m = (int)cdiv(rows_out, t.rows);
+      g.tiles_n = (int)cdiv(n, t.cols);
+      g.nsplit = 1;
+      g.nblocks = p.BH * g.tiles_m * g.tiles_n;
+      g.rows = n;
+      g.a0 = o[i].a;
+      g.b0 = o[i].b;
+      g.out = o[i].out;
+      g.out_inst = o[i].out_inst;
+    }
+    b.nseg = nseg;
+    b.total_blocks = 0;
+    for (int i = 0; i < nseg; ++i) b.total_blocks += b.seg[i].nblocks;
+    b.d = rows_out;
+    b.h = K;
+    b.narrow = p.narrow;
+    return timed(LACT_KCLASS_BWD, 2.0 * nseg * BH * n * rows_out * K, s, [&] { return launch_bwd(b, p.bf16, s); });
+  };
+  // weight cotangents over rows [0, n): W1 += a1^T b, W3 += a3^T b (GRAD13)
+  // and W2 += a2^T b2 (GRAD2), as split partials into `out`; returns the split count
+  auto grads = [&](Operand a1, Operand a3, Operand b13, Operand a2, Operand b2, float* out, int64_t n,
+                   int64_t split_len, int* nsplit) -> int {
+    const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16, p.narrow), g2 = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
+    const int ns = (int)std::max<int64_t>(1, cdiv(n, split_len));
+    BwdArgs b{};
+    BwdSeg& x = b.seg[0];
+    x.kind = BWD_GRAD13;
+    x.tiles_m = (int)cdiv(h, g13.rows);
+    x.tiles_n = (int)cdiv(d, g13.cols);
+    x.nsplit = ns;
+    x.nblocks = p.BH * x.tiles_m * x.tiles_n * ns;
+    x.rows = n;
+    x.split_len = split_len;
+    x.a0 = a1;
+    x.a1 = a3;
+    x.b0 = b13;
+    x.out = out;
+    x.out_inst = 3 * dh;
+    x.out_split = psplit;
+    BwdSeg& y = b.seg[1];
+    y.kind = BWD_GRAD2;
+    y.tiles_m = (int)cdiv(d, g2.rows);
+    y.tiles_n = (int)cdiv(h, g2.cols);
+    y.nsplit = ns;
+    y.nblocks = p.BH * y.tiles_m * y.tiles_n * ns;
+    y.rows = n;
+    y.split_len = split_len;
+    y.a0 = a2;
+    y.b0 = b2;
+    y.out = out;
+    y.out_inst = 3 * dh;
+    y.out_split = psplit;
+    y.out_off = dh;
+    b.nseg = 2;
+    b.total_blocks = x.nblocks + y.nblocks;
+    b.d = p.d;
+    b.h = p.h;
+    b.narrow = p.narrow;
+    *nsplit = ns;
+    return timed(LACT_KCLASS_BWD, 6.0 * BH * n * dh, s, [&] { return launch_bwd(b, p.bf16, s); });
+  };
+  auto copy = [&](const float* W, int R, int Lc, void* dst, int64_t ld, int64_t dst_inst, bool trans) -> int {
+    return timed(LACT_KCLASS_PREP, 0.0, s, [&] {
+      return launch_copy_w(W, (int64_t)R * Lc, dst, ld, dst_inst, p.BH, R, Lc, trans, p.bf16, s);
+    });
+  };
+  // operand copies of weights (W1, W2, W3) for the [n x h] products (W1, W3
+  // row-major, W2^T) into set `u`, and W1^T, W3^T into `bt` (ld bt_ld)
+  auto weight_copies = [&](const float* W1, const float* W2, const float* W3, const size_t* u, uint8_t* bt,
+                           int64_t bt_ld) -> int {
+    int r = copy(W1, (int)h, (int)d, ws + u[0], d, dh, false);
+    if (!r) r = copy(W3, (int)h, (int)d, ws + u[1], d, dh, false);
+    if (!r) r = copy(W2, (int)d, (int)h, ws + u[2], d, dh, true);
+    if (!r) r = copy(W1, (int)h, (int)d, bt, bt_ld, d * bt_ld, true);
+    if (!r) r = copy(W3, (int)h, (int)d, bt + h * esz, bt_ld, d * bt_ld, true);
+    return r;
+  };
+  const int64_t zi = T * h;   // elements between instances of a [T x h] buffer
+  int a_ns = 0, b_ns = 0;
+  // the apply's reverse on query rows [a, a + n) with the weights whose
+  // copies are in `u` (row-major W1, W3 and W2^T) and `bt` (W1^T | W3^T, ld bt_ld)
+  auto apply_back = [&](int64_t a, int64_t n, const size_t* u, const uint8_t* bt, int64_t bt_ld,
+                        int64_t split_len) -> int {
+    const Operand qo = op(qb + a * d * esz, d, n_q * d), doo = op(ob + a * d * esz, d, n_q * d);
+    const Out h3[3] = {{qo, op(ws + u[0], d, dh), zb[0], zi},
+                       {qo, op(ws + u[1], d, dh), zb[1], zi},
+                       {doo, op(ws + u[2], d, dh), zb[2], zi}};
+    int r = outs(h3, 3, n, (int)h, (int)d);
+    if (r) return r;
+    r = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+      return launch_swiglu_apply_rows(zb[0], zb[1], zb[2], zi, pk, T * 2 * h, pv, zi, p.BH, n, (int)h, p.bf16, s);
+    });
+    if (r) return r;
+    const Out dqo{op(pk, 2 * h, T * 2 * h), op(bt, bt_ld, d * bt_ld), (uint8_t*)dq + a * d * esz, n_q * d};
+    r = outs(&dqo, 1, n, (int)d, (int)(2 * h));
+    if (r) return r;
+    return grads(op(pk, 2 * h, T * 2 * h), op(pk + h * esz, 2 * h, T * 2 * h), qo, doo, op(pv, h, zi), apart, n,
+                 split_len, &a_ns);
+  };
+  auto pset = [&](float* base, int ns, int m) -> PartSet { return PartSet{base + m * dh, ns, psplit, 3 * dh}; };
+  // tail [n_kv, n_q): applied with the final weights, on top of dW_final (or zero)
+  bool first = true;
+  if (any_q && n_q > n_kv) {
+    rc = weight_copies(traj(L.nch, 0), traj(L.nch, 1), traj(L.nch, 2), L.off_a, bq, 2 * h);
+    if (rc) return rc;
+    for (int64_t a = n_kv; a < n_q; a += T) {
+      const int64_t n = std::min(T, n_q - a);
+      rc = apply_back(a, n, L.off_a, bq, 2 * h, L.tail_split);
+      if (rc) return rc;
+      for (int m = 0; m < 3; ++m) {
+        const int64_t RL = dh;
+        const int mode = first ? (dWf[m] ? 1 : 0) : 2;
+        const PartSet ps = pset(apart, a_ns, m);
+        rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
+                   [&] { return launch_accum(dW[m], RL, dWf[m], RL, mode, ps, PartSet{}, p.BH, RL, s); });
+        if (rc) return rc;
+      }
+      first = false;
+    }
+  }
+  if (first) {
+    for (int m = 0; m < 3; ++m) {
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+        return launch_accum(dW[m], dh, dWf[m], dh, dWf[m] ? 1 : 0, PartSet{}, PartSet{}, p.BH, dh, s);
+      });
+      if (rc) return rc;
+    }
+  }
+  const bool then_apply = desc->order == LACT_UPDATE_THEN_APPLY;
+  bool a_pending = false, b_pending = false;   // partials that the next reverse adds first
+  uint8_t* ur[3] = {ws + L.off_ur[0], ws + L.off_ur[1], ws + L.off_ur[2]};
+  for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
+    const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
+    if (then_apply) {   // applied with the weights leaving the chunk
+      rc = weight_copies(traj(ci + 1, 0), traj(ci + 1, 1), traj(ci + 1, 2), L.off_a, bq, 2 * h);
+      if (!rc) rc = apply_back(s0, n, L.off_a, bq, 2 * h, p.split_len);
+      if (rc) return rc;
+      a_pending = true;
+    }
+    // the update's reverse, matrix by matrix: W1, W3 ([h x d]) and W2 ([d x h])
+    for (int m = 0; m < 3; ++m) {
+      VjpArgs va{};
+      const bool w2 = m == 1;
+      va.W = traj(ci, m);
+      va.w_inst = dh;
+      va.P = pset(reinterpret_cast<float*>(ws + L.off_P + (size_t)ci * L.slotP), p.nsplit, m);
+      if (b_pending) va.pre[0] = pset(bpart, b_ns, m);
+      if (a_pending) va.pre[1] = pset(apart, a_ns, m);
+      va.G = dW[m];
+      va.g_inst = dh;
+      if (w2) {   // U2 row-major into [U2 | W2], U2^T for V U2
+        va.Ub = bv;
+        va.ub_ld = 2 * h;
+        va.ub_inst = d * 2 * h;
+        va.UT = ur[2];
+        va.ut_ld = d;
+        va.ut_inst = dh;
+      } else {    // U1, U3 row-major for K U^T; transposed into [U3^T | U1^T | ...]
+        va.Ub = ur[m == 0 ? 0 : 1];
+        va.ub_ld = d;
+        va.ub_inst = dh;
+        va.UT = bk + (m == 0 ? h : 0) * esz;
+        va.ut_ld = 4 * h;
+        va.ut_inst = d * 4 * h;
+      }
+      va.BH = p.BH;
+      va.R = (int)(w2 ? d : h);
+      va.L = (int)(w2 ? h : d);
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(va, p.bf16, s); });
+      if (rc) return rc;
+    }
+    a_pending = b_pending = false;
+    rc = weight_copies(traj(ci, 0), traj(ci, 1), traj(ci, 2), L.off_u, bk + 2 * h * esz, 4 * h);
+    if (!rc) rc = copy(traj(ci, 1), (int)d, (int)h, bv + h * esz, 2 * h, d * 2 * h, false);   // W2 into [U2 | W2]
+    if (rc) return rc;
+    const Operand ko = op(kb + s0 * d * esz, d, n_kv * d), vo = op(vb + s0 * d * esz, d, n_kv * d);
+    const Out f3[3] = {{ko, op(ws + L.off_u[0], d, dh), zb[0], zi},
+                       {ko, op(ws + L.off_u[1], d, dh), zb[1], zi},
+                       {vo, op(ws + L.off_u[2], d, dh), zb[2], zi}};
+    rc = outs(f3, 3, n, (int)h, (int)d);
+    if (rc) return rc;
+    const Out x3[3] = {{ko, op(ur[0], d, dh), zb[3], zi}, {ko, op(ur[1], d, dh), zb[4], zi}, {vo, op(ur[2], d, dh), zb[5], zi}};
+    rc = outs(x3, 3, n, (int)h, (int)d);
+    if (rc) return rc;
+    SwigluRowsArgs ra{};
+    ra.Z1 = zb[0];
+    ra.Z3 = zb[1];
+    ra.C = zb[2];
+    ra.X1 = zb[3];
+    ra.X3 = zb[4];
+    ra.Y2 = zb[5];
+    ra.in_inst = zi;
+    ra.eta = eta + s0;
+    ra.eta_inst = n_kv;
+    ra.Pk = pk;
+    ra.pk_inst = T * 4 * h;
+    ra.Pv = pv;
+    ra.pv_inst = T * 2 * h;
+    ra.deta = deta + s0;
+    ra.BH = p.BH;
+    ra.n = n;
+    ra.h = (int)h;
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_swiglu_rows(ra, p.bf16, s); });
+    if (rc) return rc;
+    const Out dko{op(pk, 4 * h, T * 4 * h), op(bk, 4 * h, d * 4 * h), (uint8_t*)dk + s0 * d * esz, n_kv * d};
+    rc = outs(&dko, 1, n, (int)d, (int)(4 * h));
+    if (rc) return rc;
+    const Out dvo{op(pv, 2 * h, T * 2 * h), op(bv, 2 * h, d * 2 * h), (uint8_t*)dv + s0 * d * esz, n_kv * d};
+    rc = outs(&dvo, 1, n, (int)d, (int)(2 * h));
+    if (rc) return rc;
+    rc = grads(op(pk + 2 * h * esz, 4 * h, T * 4 * h), op(pk + 3 * h * esz, 4 * h, T * 4 * h), ko, vo,
+               op(pv + h * esz, 2 * h, T * 2 * h), bpart, n, p.split_len, &b_ns);
+    if (rc) return rc;
+    b_pending = true;
+    if (!then_apply) {   // applied with the weights entering the chunk (copies made above)
+      rc = apply_back(s0, n, L.off_u, bk + 2 * h * esz, 4 * h, p.split_len);
+      if (rc) return rc;
+      a_pending = true;
+    }
+  }
+  if (a_pending || b_pending) {
+    for (int m = 0; m < 3; ++m) {
+      const PartSet s0 = b_pending ? pset(bpart, b_ns, m) : PartSet{};
+      const PartSet s1 = a_pending ? pset(apart, a_ns, m) : PartSet{};
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_accum(dW[m], dh, nullptr, 0, 2, s0, s1, p.BH, dh, s); });
+      if (rc) return rc;
+    }
   }
   return LACT_OK;
 }
@@ -1364,10 +1779,30 @@ int lact_forward(const lact_desc* desc, const void* q, const void* k, const void
 }
 
 size_t lact_backward_workspace_bytes(const lact_desc* desc, int* err) {
-  BwdLayout L;
-  const int rc = bwd_layout(desc, &L);
+  int rc = check_desc(desc);
+  size_t total = 0;
+  if (!rc && desc->fast_weight == LACT_FW_LINEAR) {
+    BwdLayout L;
+    rc = bwd_layout(desc, &L);
+    total = L.total;
+  } else if (!rc) {
+    SwBwdLayout L;
+    rc = sw_bwd_layout(desc, &L);
+    total = L.total;
+  }
   if (err) *err = rc;
-  return rc ? 0 : L.total;
+  return rc ? 0 : total;
+}
+
+int lact_backward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                  const float* W1, const float* W2, const float* W3, const void* dout, const float* dW1_final,
+                  const float* dW2_final, const float* dW3_final, void* dq, void* dk, void* dv, float* deta,
+                  float* dW1, float* dW2, float* dW3, void* workspace, size_t workspace_bytes, void* stream) {
+  const float* W0[3] = {W1, W2, W3};
+  const float* dWf[3] = {dW1_final, dW2_final, dW3_final};
+  float* const dW[3] = {dW1, dW2, dW3};
+  return run_backward_swiglu(desc, q, k, v, eta, W0, dout, dWf, dq, dk, dv, deta, dW, workspace, workspace_bytes,
+                             stream);
 }
 
 int lact_backward_linear(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,

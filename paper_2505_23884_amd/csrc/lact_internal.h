@@ -287,14 +287,61 @@ hipError_t launch_ns_fused_pair_out(const NsFusedArgs& a0, const NsFusedArgs& a1
 hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s);
 // Zero rows [r0, r1) of every instance of an output of `rows` rows of row_bytes
 // (a multiple of 16) each.
-// Reverse of the linear fast weight's chunk loop (see lact_kernels.hip).
-hipError_t launch_lin_vjp(const float* W, const float* P, const float* A, int nsplit, int64_t psplit, bool a_first,
-                          float* G, void* Ub, void* UT, int BH, int d, bool io_bf16, hipStream_t s);
-hipError_t launch_transpose_cvt(const float* W, void* WT, int BH, int d, bool io_bf16, hipStream_t s);
+// ---- backward: the steps between the OUT / GRAD contractions --------------
+// A set of fp32 split partials of a [R x L] matrix: element (inst, r, c) of
+// split s at p[s * split + inst * inst + r * L + c], summed over s < n
+// (p == nullptr or n == 0: no set).
+struct PartSet {
+  const float* p;
+  int n;
+  int64_t split, inst;
+};
+
+// Reverse of W' = (n / u) U, U = W + sum P, per row of a [R x L] matrix.
+struct VjpArgs {
+  const float* W; int64_t w_inst;     // weights entering the chunk
+  PartSet P;                          // U = W + sum P (the negated chunk gradient)
+  PartSet pre[2];                     // added to the cotangent before the reverse
+  PartSet post;                       // added after it
+  float* G; int64_t g_inst;           // cotangent of W' in, of W out (in place)
+  void* Ub; int64_t ub_ld, ub_inst;   // cotangent of U in the operand type, row-major (or nullptr)
+  void* UT; int64_t ut_ld, ut_inst;   // the same, transposed (or nullptr)
+  int BH, R, L;
+};
+
+hipError_t launch_vjp(const VjpArgs& a, bool io_bf16, hipStream_t s);
+// dst = W (trans = false: dst[r * ld + c]) or W^T (dst[c * ld + r]) in the
+// operand type, from fp32 [R x L] matrices w_inst apart (dst_inst apart).
+hipError_t launch_copy_w(const float* W, int64_t w_inst, void* dst, int64_t ld, int64_t dst_inst, int BH, int R, int L,
+                         bool trans, bool io_bf16, hipStream_t s);
+// G = base + sum of the sets over BH instances of RL floats each (RL a
+// multiple of 4); base: 0 (mode 0), init (mode 1) or G itself (mode 2).
+hipError_t launch_accum(float* G, int64_t g_inst, const float* init, int64_t i_inst, int mode, PartSet s0, PartSet s1,
+                        int BH, int64_t RL, hipStream_t s);
+// Linear fast weight, per key token of a chunk: dv = eta Y (Y in dv on
+// entry), deta = v . Y.
 hipError_t launch_lin_tokens(const void* V, const float* eta, void* dv, float* deta, int BH, int64_t n, int d,
                              int64_t tok_inst, int64_t eta_inst, bool io_bf16, hipStream_t s);
-hipError_t launch_sum_parts(float* G, const float* init, int mode, const float* P, int nsplit, int64_t psplit,
-                            int64_t n, hipStream_t s);
+
+// SwiGLU fast weight, per key token of a chunk (rows of h): from Z1 = K W1^T,
+// Z3 = K W3^T, C = V W2, X1 = K U1^T, X3 = K U3^T, Y2 = V U2 (U: the update's
+// cotangent) and eta, the operands Pk = [R3 | R1 | dZ1 | dZ3] and
+// Pv = [eta A | dC] of the next contractions and deta.
+struct SwigluRowsArgs {
+  const void* Z1; const void* Z3; const void* C; const void* X1; const void* X3; const void* Y2;
+  int64_t in_inst;                    // elements between instances of the six [n x h] inputs
+  const float* eta; int64_t eta_inst;
+  void* Pk; int64_t pk_inst;          // [n x 4h]
+  void* Pv; int64_t pv_inst;          // [n x 2h]
+  float* deta;
+  int BH; int64_t n; int h;
+};
+hipError_t launch_swiglu_rows(const SwigluRowsArgs& a, bool io_bf16, hipStream_t s);
+// SwiGLU apply, per query token: from Zq1 = Q W1^T, Zq3 = Q W3^T, Dh = dO W2,
+// Pq = [dZq1 | dZq3] ([n x 2h]) and Hq = SiLU(Zq1) o Zq3 ([n x h]).
+hipError_t launch_swiglu_apply_rows(const void* Z1, const void* Z3, const void* Dh, int64_t in_inst, void* Pq,
+                                    int64_t pq_inst, void* Hq, int64_t hq_inst, int BH, int64_t n, int h, bool io_bf16,
+                                    hipStream_t s);
 hipError_t launch_zero_rows(void* out, int BH, int64_t row_bytes, int64_t rows, int64_t r0, int64_t r1,
                             hipStream_t s);
 constexpr int kNsBlockElems = 4096;

@@ -2270,51 +2270,57 @@ __global__ __launch_bounds__(256) void k_beta_mean(const BetaArgs a) {
 // norm-preserving update): the contractions run on the OUT and GRAD2 kinds;
 // these kernels are the row-wise and token-wise steps between them.
 
-// Rows of the d x d matrix per workgroup of k_lin_vjp: the rows' cotangent in
-// the operand type is staged in LDS (up to 64 KB) to leave as whole
-// segments of the transposed copy.
+// Rows of a matrix per workgroup of k_vjp: the rows' cotangent in the operand
+// type is staged in LDS (up to 64 KB) to leave as whole segments of the
+// transposed copy.
 template <typename T, int NV>
 constexpr int vjp_rows() {
   return cmax(4, 65536 / (256 * NV * (int)sizeof(T)) > 32 ? 32 : 65536 / (256 * NV * (int)sizeof(T)));
 }
 
-// Reverse of W' = (n / u) U, U = W + P (P = sum of the split partials of
-// sum_t eta_t v_t k_t^T, the negated chunk gradient), vjp_rows() rows of
-// one instance per workgroup, one wave per row at a time. From the
-// cotangent G of W' (in place), with a = G . U per row:
-//   Uh = (n / u) G - (n a / u^3) U,   G <- Uh + (a / (u n)) W,
-// and Uh (the cotangent of U, i.e. minus that of the gradient) in the
-// operand type, row-major into Ub and transposed into UT. The apply's own
-// contribution (the nsplit partials A, same split stride as P) joins G
-// before the reverse when a_first (the chunk was applied with W'), after it
-// otherwise (applied with W). A zero row norm gives the same non-finite
-// values as the forward's division.
 template <int NV>
 constexpr int vjp_waves() { return NV <= 4 ? 16 : 4; }   // rows of up to 1024 floats: 16 waves in flight
 
+// acc += the split partials of set s at element 4 i of row offset roff
+// (lanes past the row pass i = 0 and drop the result).
+__device__ __forceinline__ void add_set(const PartSet& s, int64_t inst, int64_t roff, int i, float4& acc) {
+  if (!s.p) return;
+  const float4* p = reinterpret_cast<const float4*>(s.p + inst * s.inst + roff);
+  const int64_t ss = s.split >> 2;
+  for (int k = 0; k < s.n; ++k) {
+    const float4 q = p[k * ss + i];
+    acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
+  }
+}
+
+// Reverse of W' = (n / u) U, U = W + P (P the negated chunk gradient, as
+// split partials), vjp_rows() rows of one instance per workgroup, one wave
+// per row at a time. From the cotangent G of W' (in place; the pre sets
+// join it first), with a = G . U per row:
+//   Uh = (n / u) G - (n a / u^3) U,   G <- Uh + (a / (u n)) W  (+ the post set),
+// and Uh (the cotangent of U, i.e. minus that of the gradient) in the
+// operand type, row-major into Ub and transposed into UT. A zero row norm
+// gives the same non-finite values as the forward's division.
 template <typename T, int NV>
-__global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_lin_vjp(const float* W, const float* P, const float* A,
-                                                                  int nsplit, int64_t psplit, int a_first, float* G,
-                                                                  T* Ub, T* UT, int d) {
-  constexpr int R = vjp_rows<T, NV>();
+__global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_vjp(const VjpArgs a) {
+  constexpr int RR = vjp_rows<T, NV>();
   constexpr int NW = vjp_waves<NV>();
   constexpr int LD = 256 * NV + 4 / (int)sizeof(T);   // one 4-byte word of padding per staged row
-  __shared__ __attribute__((aligned(16))) T tile[R * LD];
-  const int per = (d + R - 1) / R;
-  const int inst = blockIdx.x / per;
-  const int r0 = (blockIdx.x - inst * per) * R;
+  __shared__ __attribute__((aligned(16))) T tile[RR * LD];
+  const int L = a.L;
+  const int per = (a.R + RR - 1) / RR;
+  const int64_t inst = blockIdx.x / per;
+  const int r0 = (int)(blockIdx.x - inst * per) * RR;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t dd = (int64_t)d * d;
-  const int nv = d >> 2;
-  const int64_t ps = psplit >> 2;
-  for (int rr = w; rr < R; rr += NW) {
+  const int nv = L >> 2;
+  T* Ub = reinterpret_cast<T*>(a.Ub);
+  T* UT = reinterpret_cast<T*>(a.UT);
+  for (int rr = w; rr < RR; rr += NW) {
     const int r = r0 + rr;
-    if (r >= d) break;
-    const int64_t off = inst * dd + (int64_t)r * d;
-    const float4* w4 = reinterpret_cast<const float4*>(W + off);
-    const float4* p4 = reinterpret_cast<const float4*>(P + off);
-    const float4* a4 = reinterpret_cast<const float4*>(A + off);
-    float4* g4 = reinterpret_cast<float4*>(G + off);
+    if (r >= a.R) break;
+    const int64_t roff = (int64_t)r * L;
+    const float4* w4 = reinterpret_cast<const float4*>(a.W + inst * a.w_inst + roff);
+    float4* g4 = reinterpret_cast<float4*>(a.G + inst * a.g_inst + roff);
     float4 wv[NV], u[NV], g[NV], ap[NV];
     const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
@@ -2322,28 +2328,17 @@ __global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_lin_vjp(const float* W
       const int i = lane + 64 * t, ic = i < nv ? i : 0;   // lanes past the row load element 0, then drop it
       wv[t] = w4[ic];
       g[t] = g4[ic];
-      if (i >= nv) wv[t] = g[t] = z;
       u[t] = wv[t];
       ap[t] = z;
-    }
-    for (int sp = 0; sp < nsplit; ++sp) {
-#pragma unroll
-      for (int t = 0; t < NV; ++t) {
-        const int i = lane + 64 * t;
-        if (i < nv) {
-          const float4 q = p4[sp * ps + i], e = a4[sp * ps + i];
-          u[t].x += q.x; u[t].y += q.y; u[t].z += q.z; u[t].w += q.w;
-          ap[t].x += e.x; ap[t].y += e.y; ap[t].z += e.z; ap[t].w += e.w;
-        }
-      }
+      add_set(a.P, inst, roff, ic, u[t]);
+      add_set(a.pre[0], inst, roff, ic, g[t]);
+      add_set(a.pre[1], inst, roff, ic, g[t]);
+      add_set(a.post, inst, roff, ic, ap[t]);
+      if (i >= nv) wv[t] = u[t] = g[t] = z;
     }
     float sw = 0.f, su = 0.f, sa = 0.f;
 #pragma unroll
     for (int t = 0; t < NV; ++t) {
-      if (a_first) {
-        g[t].x += ap[t].x; g[t].y += ap[t].y; g[t].z += ap[t].z; g[t].w += ap[t].w;
-        ap[t] = z;
-      }
       sw += wv[t].x * wv[t].x + wv[t].y * wv[t].y + wv[t].z * wv[t].z + wv[t].w * wv[t].w;
       su += u[t].x * u[t].x + u[t].y * u[t].y + u[t].z * u[t].z + u[t].w * u[t].w;
       sa += g[t].x * u[t].x + g[t].y * u[t].y + g[t].z * u[t].z + g[t].w * u[t].w;
@@ -2361,7 +2356,7 @@ __global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_lin_vjp(const float* W
                                     c1 * g[t].z - c2 * u[t].z, c1 * g[t].w - c2 * u[t].w);
       g4[i] = make_float4(uh.x + c3 * wv[t].x + ap[t].x, uh.y + c3 * wv[t].y + ap[t].y,
                           uh.z + c3 * wv[t].z + ap[t].z, uh.w + c3 * wv[t].w + ap[t].w);
-      st4<T>(Ub, off + 4 * i, uh.x, uh.y, uh.z, uh.w);
+      if (Ub) st4<T>(Ub, inst * a.ub_inst + (int64_t)r * a.ub_ld + 4 * i, uh.x, uh.y, uh.z, uh.w);
       T* row = tile + rr * LD + 4 * i;
       row[0] = (T)uh.x;
       row[1] = (T)uh.y;
@@ -2369,51 +2364,75 @@ __global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_lin_vjp(const float* W
       row[3] = (T)uh.w;
     }
   }
+  if (!UT) return;   // uniform over the launch
   __syncthreads();
-  // UT[e][r0 .. r0 + R): four consecutive rows of the block per store
-  constexpr int Q = R / 4;
-  const int rows = d - r0 < R ? d - r0 : R;
-  for (int pi = threadIdx.x; pi < d * Q; pi += 64 * NW) {
-    const int e = pi / Q, j = 4 * (pi - (pi / Q) * Q);
+  // UT[c][r0 .. r0 + RR): four consecutive rows of the block per store
+  constexpr int Q = RR / 4;
+  const int rows = a.R - r0 < RR ? a.R - r0 : RR;
+  for (int pi = threadIdx.x; pi < L * Q; pi += 64 * NW) {
+    const int c = pi / Q, j = 4 * (pi - (pi / Q) * Q);
     if (j >= rows) continue;
-    const int64_t o = inst * dd + (int64_t)e * d + r0 + j;
-    if (j + 4 <= rows) {
-      st4<T>(UT, o, (float)tile[j * LD + e], (float)tile[(j + 1) * LD + e], (float)tile[(j + 2) * LD + e],
-             (float)tile[(j + 3) * LD + e]);
+    const int64_t o = inst * a.ut_inst + (int64_t)c * a.ut_ld + r0 + j;
+    if (j + 4 <= rows && ((o & 3) == 0)) {
+      st4<T>(UT, o, (float)tile[j * LD + c], (float)tile[(j + 1) * LD + c], (float)tile[(j + 2) * LD + c],
+             (float)tile[(j + 3) * LD + c]);
     } else {
-      for (int q = 0; j + q < rows; ++q) UT[o + q] = tile[(j + q) * LD + e];
+      for (int q = 0; q < 4 && j + q < rows; ++q) UT[o + q] = tile[(j + q) * LD + c];
     }
   }
 }
 
-// Transposed operand copy: WT[i][e][f] = W[i][f][e] (fp32 -> operand type),
-// 32 x 32 tiles through LDS so that both sides move whole rows; one block per
-// (instance, tile) in a flat grid.
-template <typename T>
-__global__ __launch_bounds__(256) void k_transpose_cvt(const float* W, T* WT, int d, int tiles) {
+// Operand copy of fp32 [R x L] matrices, transposed or not: 32 x 32 tiles
+// through LDS so that both sides move whole rows; one block per (instance,
+// tile) in a flat grid.
+template <typename T, bool TRANS>
+__global__ __launch_bounds__(256) void k_copy_w(const float* W, int64_t w_inst, T* dst, int64_t ld, int64_t d_inst,
+                                                int R, int L, int tr, int tl) {
   __shared__ float tile[32][33];
-  const int64_t dd = (int64_t)d * d;
-  const int64_t per = (int64_t)tiles * tiles;
+  const int64_t per = (int64_t)tr * tl;
   const int64_t inst = blockIdx.x / per;
   const int rest = (int)(blockIdx.x - inst * per);
-  const float* src = W + inst * dd;
-  T* dst = WT + inst * dd;
-  const int r0 = (rest / tiles) * 32, c0 = (rest % tiles) * 32;
+  const float* src = W + inst * w_inst;
+  T* out = dst + inst * d_inst;
+  const int r0 = (rest / tl) * 32, c0 = (rest % tl) * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
   for (int k = ty; k < 32; k += 8) {
     const int r = r0 + k, c = c0 + tx;
-    tile[k][tx] = (r < d && c < d) ? src[(int64_t)r * d + c] : 0.0f;
+    tile[k][tx] = (r < R && c < L) ? src[(int64_t)r * L + c] : 0.0f;
+  }
+  if constexpr (!TRANS) {
+    for (int k = ty; k < 32; k += 8) {
+      const int r = r0 + k, c = c0 + tx;
+      if (r < R && c < L) out[(int64_t)r * ld + c] = (T)tile[k][tx];
+    }
+    return;
   }
   __syncthreads();
   for (int k = ty; k < 32; k += 8) {
-    const int r = c0 + k, c = r0 + tx;   // output row = input column
-    if (r < d && c < d) dst[(int64_t)r * d + c] = (T)tile[tx][k];
+    const int c = c0 + k, r = r0 + tx;   // output row = input column
+    if (r < R && c < L) out[(int64_t)c * ld + r] = (T)tile[tx][k];
   }
 }
 
-// Token step of the reverse, one wave per key token t of a chunk (grid
-// stride over BH x n tokens). On entry dv holds Y = K Uh^T (rows t); it
-// leaves as dv_t = eta_t Y_t, with deta_t = v_t . Y_t (= v_t^T Uh k_t).
+// G = base + the sets, grid stride over BH x RL / 4 float4s.
+__global__ __launch_bounds__(256) void k_accum(float* G, int64_t g_inst, const float* init, int64_t i_inst, int mode,
+                                               const PartSet s0, const PartSet s1, int BH, int64_t RL) {
+  const int64_t per = RL >> 2, total = (int64_t)BH * per;
+  for (int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x; x < total; x += (int64_t)gridDim.x * 256) {
+    const int64_t inst = x / per;
+    const int i = (int)(x - inst * per);
+    float4* g = reinterpret_cast<float4*>(G + inst * g_inst) + i;
+    float4 acc = mode == 0 ? make_float4(0.f, 0.f, 0.f, 0.f)
+                           : (mode == 1 ? reinterpret_cast<const float4*>(init + inst * i_inst)[i] : *g);
+    add_set(s0, inst, 0, i, acc);
+    add_set(s1, inst, 0, i, acc);
+    *g = acc;
+  }
+}
+
+// Linear fast weight, one wave per key token t of a chunk (grid stride over
+// BH x n tokens). On entry dv holds Y = K Uh^T (rows t); it leaves as
+// dv_t = eta_t Y_t, with deta_t = v_t . Y_t (= v_t^T Uh k_t).
 template <typename T>
 __global__ __launch_bounds__(256) void k_lin_tokens(const T* V, const float* eta, T* dv, float* deta, int BH,
                                                     int64_t n, int d, int64_t tok_inst, int64_t eta_inst) {
@@ -2438,21 +2457,98 @@ __global__ __launch_bounds__(256) void k_lin_tokens(const T* V, const float* eta
   }
 }
 
-// G = base + sum of nsplit partials (stride psplit floats) over n floats (a
-// multiple of 4); base is zero (mode 0), init (mode 1) or G itself (mode 2).
-__global__ __launch_bounds__(256) void k_sum_parts(float* G, const float* init, int mode, const float* P, int nsplit,
-                                                   int64_t psplit, int64_t n) {
-  const int64_t n4 = n >> 2, ps = psplit >> 2;
-  float4* g4 = reinterpret_cast<float4*>(G);
-  const float4* i4 = reinterpret_cast<const float4*>(init);
-  const float4* p4 = reinterpret_cast<const float4*>(P);
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
-    float4 a = mode == 0 ? make_float4(0.f, 0.f, 0.f, 0.f) : (mode == 1 ? i4[i] : g4[i]);
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float4 q = p4[sp * ps + i];
-      a.x += q.x; a.y += q.y; a.z += q.z; a.w += q.w;
+template <typename T>
+__device__ __forceinline__ void ld4(const void* base, int64_t idx, float* v) {
+  const T* p = reinterpret_cast<const T*>(base) + idx;
+  if constexpr (sizeof(T) == 2) {
+    typedef __attribute__((ext_vector_type(4))) T t4;
+    const t4 x = *reinterpret_cast<const t4*>(p);
+    v[0] = (float)x[0]; v[1] = (float)x[1]; v[2] = (float)x[2]; v[3] = (float)x[3];
+  } else {
+    const float4 x = *reinterpret_cast<const float4*>(p);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  }
+}
+
+// SwiGLU chunk-gradient reverse, one wave per key token (grid stride). With
+// S = SiLU(Z1), S1 = SiLU'(Z1), S2 = SiLU''(Z1), A = S Z3 and the token's rate e:
+//   dA  = e Y2,  dC = e (X3 S + X1 Z3 S1),  dZ3 = e X1 C S1 + dA S,
+//   dZ1 = (e X3 C + dA Z3) S1 + e X1 C Z3 S2,  R3 = e C S,  R1 = e C Z3 S1,
+//   deta = sum over the hidden units of A Y2 + X3 C S + X1 C Z3 S1.
+template <typename T>
+__global__ __launch_bounds__(256) void k_swiglu_rows(const SwigluRowsArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int h = a.h;
+  const int64_t total = (int64_t)a.BH * a.n;
+  for (int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wave < total; wave += (int64_t)gridDim.x * 4) {
+    const int64_t inst = wave / a.n, t = wave - inst * a.n;
+    const int64_t io = inst * a.in_inst + t * h;
+    const int64_t ko = inst * a.pk_inst + t * 4 * h, vo = inst * a.pv_inst + t * 2 * h;
+    const float e = a.eta[inst * a.eta_inst + t];
+    float dsum = 0.0f;
+    for (int j = 4 * lane; j < h; j += 256) {
+      float z1[4], z3[4], c[4], x1[4], x3[4], y2[4];
+      ld4<T>(a.Z1, io + j, z1);
+      ld4<T>(a.Z3, io + j, z3);
+      ld4<T>(a.C, io + j, c);
+      ld4<T>(a.X1, io + j, x1);
+      ld4<T>(a.X3, io + j, x3);
+      ld4<T>(a.Y2, io + j, y2);
+      float r3[4], r1[4], dz1[4], dz3[4], ea[4], dc[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float sg = sigmoidf_fast(z1[q]);
+        const float S = z1[q] * sg, S1 = sg + z1[q] * sg * (1.0f - sg);
+        const float S2 = sg * (1.0f - sg) * (2.0f + z1[q] * (1.0f - 2.0f * sg));
+        const float A = S * z3[q], dA = e * y2[q];
+        dc[q] = e * (x3[q] * S + x1[q] * z3[q] * S1);
+        dz3[q] = e * x1[q] * c[q] * S1 + dA * S;
+        dz1[q] = (e * x3[q] * c[q] + dA * z3[q]) * S1 + e * x1[q] * c[q] * z3[q] * S2;
+        r3[q] = e * c[q] * S;
+        r1[q] = e * c[q] * z3[q] * S1;
+        ea[q] = e * A;
+        dsum += A * y2[q] + x3[q] * c[q] * S + x1[q] * c[q] * z3[q] * S1;
+      }
+      st4<T>(a.Pk, ko + j, r3[0], r3[1], r3[2], r3[3]);
+      st4<T>(a.Pk, ko + h + j, r1[0], r1[1], r1[2], r1[3]);
+      st4<T>(a.Pk, ko + 2 * h + j, dz1[0], dz1[1], dz1[2], dz1[3]);
+      st4<T>(a.Pk, ko + 3 * h + j, dz3[0], dz3[1], dz3[2], dz3[3]);
+      st4<T>(a.Pv, vo + j, ea[0], ea[1], ea[2], ea[3]);
+      st4<T>(a.Pv, vo + h + j, dc[0], dc[1], dc[2], dc[3]);
     }
-    g4[i] = a;
+    dsum = wave_sum(dsum);
+    if (lane == 0) a.deta[inst * a.eta_inst + t] = dsum;
+  }
+}
+
+// SwiGLU apply reverse, one wave per query token (grid stride):
+// Hq = SiLU(Zq1) Zq3, dZq3 = Dh SiLU(Zq1), dZq1 = Dh Zq3 SiLU'(Zq1).
+template <typename T>
+__global__ __launch_bounds__(256) void k_swiglu_apply_rows(const T* Z1, const T* Z3, const T* Dh, int64_t in_inst, T* Pq,
+                                                           int64_t pq_inst, T* Hq, int64_t hq_inst, int BH, int64_t n,
+                                                           int h) {
+  const int lane = threadIdx.x & 63;
+  const int64_t total = (int64_t)BH * n;
+  for (int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wave < total; wave += (int64_t)gridDim.x * 4) {
+    const int64_t inst = wave / n, t = wave - inst * n;
+    const int64_t io = inst * in_inst + t * h, po = inst * pq_inst + t * 2 * h, ho = inst * hq_inst + t * h;
+    for (int j = 4 * lane; j < h; j += 256) {
+      float z1[4], z3[4], dh[4], d1[4], d3[4], hq[4];
+      ld4<T>(Z1, io + j, z1);
+      ld4<T>(Z3, io + j, z3);
+      ld4<T>(Dh, io + j, dh);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float sg = sigmoidf_fast(z1[q]);
+        const float S = z1[q] * sg, S1 = sg + z1[q] * sg * (1.0f - sg);
+        hq[q] = S * z3[q];
+        d3[q] = dh[q] * S;
+        d1[q] = dh[q] * z3[q] * S1;
+      }
+      st4<T>(Pq, po + j, d1[0], d1[1], d1[2], d1[3]);
+      st4<T>(Pq, po + h + j, d3[0], d3[1], d3[2], d3[3]);
+      st4<T>(Hq, ho + j, hq[0], hq[1], hq[2], hq[3]);
+    }
   }
 }
 
@@ -2644,19 +2740,17 @@ hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d
   return hipGetLastError();
 }
 
-// Reverse of the linear fast weight's chunk loop: the steps between the
-// OUT / GRAD2 contractions (io_bf16 selects bf16 operand copies, else fp32).
-hipError_t launch_lin_vjp(const float* W, const float* P, const float* A, int nsplit, int64_t psplit, bool a_first,
-                          float* G, void* Ub, void* UT, int BH, int d, bool io_bf16, hipStream_t s) {
-  if ((int64_t)BH * d <= 0) return hipSuccess;
-  const int per_lane = (d / 4 + 63) / 64;
+// Backward steps between the OUT / GRAD contractions (io_bf16 selects bf16
+// operand copies, else fp32).
+hipError_t launch_vjp(const VjpArgs& a, bool io_bf16, hipStream_t s) {
+  if ((int64_t)a.BH * a.R <= 0) return hipSuccess;
+  const int per_lane = (a.L / 4 + 63) / 64;
   auto go = [&](auto tag, auto nvc) {
     using T = decltype(tag);
     constexpr int NV = decltype(nvc)::value;
-    constexpr int R = vjp_rows<T, NV>();
-    const unsigned blocks = (unsigned)((int64_t)BH * ((d + R - 1) / R));   // <= 2^20 * 1024
-    k_lin_vjp<T, NV><<<blocks, 64 * vjp_waves<NV>(), 0, s>>>(W, P, A, nsplit, psplit, a_first ? 1 : 0, G,
-                                                             reinterpret_cast<T*>(Ub), reinterpret_cast<T*>(UT), d);
+    constexpr int RR = vjp_rows<T, NV>();
+    const unsigned blocks = (unsigned)((int64_t)a.BH * ((a.R + RR - 1) / RR));   // <= 2^20 * 1024
+    k_vjp<T, NV><<<blocks, 64 * vjp_waves<NV>(), 0, s>>>(a);
   };
   auto pick = [&](auto tag) {
     if (per_lane <= 1) go(tag, std::integral_constant<int, 1>{});
@@ -2670,13 +2764,30 @@ hipError_t launch_lin_vjp(const float* W, const float* P, const float* A, int ns
   return hipGetLastError();
 }
 
-hipError_t launch_transpose_cvt(const float* W, void* WT, int BH, int d, bool io_bf16, hipStream_t s) {
-  if (BH <= 0 || d <= 0) return hipSuccess;
-  const int tiles = (d + 31) / 32;
-  // callers keep BH * ceil(d / 32)^2 under 2^31 (one set of weights: under 2^28 by the descriptor check)
-  const unsigned blocks = (unsigned)((int64_t)BH * tiles * tiles);
-  if (io_bf16) k_transpose_cvt<__bf16><<<blocks, 256, 0, s>>>(W, reinterpret_cast<__bf16*>(WT), d, tiles);
-  else k_transpose_cvt<float><<<blocks, 256, 0, s>>>(W, reinterpret_cast<float*>(WT), d, tiles);
+hipError_t launch_copy_w(const float* W, int64_t w_inst, void* dst, int64_t ld, int64_t dst_inst, int BH, int R, int L,
+                         bool trans, bool io_bf16, hipStream_t s) {
+  if (BH <= 0 || R <= 0 || L <= 0) return hipSuccess;
+  const int tr = (R + 31) / 32, tl = (L + 31) / 32;
+  // callers keep BH * tiles under 2^31 (one set of weights: under 2^28 by the descriptor check)
+  const unsigned blocks = (unsigned)((int64_t)BH * tr * tl);
+  if (io_bf16) {
+    __bf16* o = reinterpret_cast<__bf16*>(dst);
+    if (trans) k_copy_w<__bf16, true><<<blocks, 256, 0, s>>>(W, w_inst, o, ld, dst_inst, R, L, tr, tl);
+    else k_copy_w<__bf16, false><<<blocks, 256, 0, s>>>(W, w_inst, o, ld, dst_inst, R, L, tr, tl);
+  } else {
+    float* o = reinterpret_cast<float*>(dst);
+    if (trans) k_copy_w<float, true><<<blocks, 256, 0, s>>>(W, w_inst, o, ld, dst_inst, R, L, tr, tl);
+    else k_copy_w<float, false><<<blocks, 256, 0, s>>>(W, w_inst, o, ld, dst_inst, R, L, tr, tl);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_accum(float* G, int64_t g_inst, const float* init, int64_t i_inst, int mode, PartSet s0, PartSet s1,
+                        int BH, int64_t RL, hipStream_t s) {
+  const int64_t need = ((int64_t)BH * (RL / 4) + 255) / 256;
+  if (need <= 0) return hipSuccess;
+  const int64_t blocks = need < 4096 ? need : 4096;
+  k_accum<<<(unsigned)blocks, 256, 0, s>>>(G, g_inst, init, i_inst, mode, s0, s1, BH, RL);
   return hipGetLastError();
 }
 
@@ -2695,12 +2806,31 @@ hipError_t launch_lin_tokens(const void* V, const float* eta, void* dv, float* d
   return hipGetLastError();
 }
 
-hipError_t launch_sum_parts(float* G, const float* init, int mode, const float* P, int nsplit, int64_t psplit,
-                            int64_t n, hipStream_t s) {
-  const int64_t need = (n / 4 + 255) / 256;
-  if (need <= 0) return hipSuccess;
-  const int64_t blocks = need < 4096 ? need : 4096;
-  k_sum_parts<<<(unsigned)blocks, 256, 0, s>>>(G, init, mode, P, nsplit, psplit, n);
+hipError_t launch_swiglu_rows(const SwigluRowsArgs& a, bool io_bf16, hipStream_t s) {
+  const int64_t rows = (int64_t)a.BH * a.n;
+  if (rows <= 0) return hipSuccess;
+  const int64_t need = (rows + 3) / 4;
+  const unsigned blocks = (unsigned)(need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20));
+  if (io_bf16) k_swiglu_rows<__bf16><<<blocks, 256, 0, s>>>(a);
+  else k_swiglu_rows<float><<<blocks, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_apply_rows(const void* Z1, const void* Z3, const void* Dh, int64_t in_inst, void* Pq,
+                                    int64_t pq_inst, void* Hq, int64_t hq_inst, int BH, int64_t n, int h, bool io_bf16,
+                                    hipStream_t s) {
+  const int64_t rows = (int64_t)BH * n;
+  if (rows <= 0) return hipSuccess;
+  const int64_t need = (rows + 3) / 4;
+  const unsigned blocks = (unsigned)(need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20));
+  auto go = [&](auto tag) {
+    using T = decltype(tag);
+    k_swiglu_apply_rows<T><<<blocks, 256, 0, s>>>(reinterpret_cast<const T*>(Z1), reinterpret_cast<const T*>(Z3),
+                                                  reinterpret_cast<const T*>(Dh), in_inst, reinterpret_cast<T*>(Pq),
+                                                  pq_inst, reinterpret_cast<T*>(Hq), hq_inst, BH, n, h);
+  };
+  if (io_bf16) go(__bf16{});
+  else go(float{});
   return hipGetLastError();
 }
 

@@ -254,11 +254,12 @@ def test_backward_errors_before_any_hip_call():
     lin = dict(GOOD, h=64, fast_weight=1)
     d = make_desc(**lin)
     assert P.binding.backward_workspace_bytes(d) > P.workspace_bytes(d)
-    # the linear fast weight without Muon only
-    for bad in (dict(GOOD), dict(lin, use_muon=True)):
+    # the linear entry point: the linear fast weight without Muon only
+    for bad in (dict(lin, use_muon=True),):
         err = ctypes.c_int(0)
         assert P.lib().lact_backward_workspace_bytes(ctypes.byref(make_desc(**bad)), ctypes.byref(err)) == 0
         assert err.value == -4
+    for bad in (dict(GOOD), dict(lin, use_muon=True)):
         assert _bwd(make_desc(**bad), nbytes=1 << 30) == -4
     assert _bwd(make_desc(**dict(lin, d=12, h=12)), nbytes=1 << 30) == -4
     assert _bwd(d, q=0) == -1
@@ -276,3 +277,45 @@ def test_backward_errors_before_any_hip_call():
     # the workspace keeps the weights of every chunk boundary: it grows with the chunk count
     more = make_desc(**dict(lin, chunk=128))
     assert P.binding.backward_workspace_bytes(more) > P.binding.backward_workspace_bytes(d)
+
+
+def _bwd_sw(desc, nbytes=None, **kw):
+    a = dict(q=0x1000, k=0x2000, v=0x3000, eta=0x4000, w1=0x5000, w2=0x6000, w3=0x7000, do=0x8000, f1=0, f2=0, f3=0,
+             dq=0x9000, dk=0xA000, dv=0xB000, deta=0xC000, d1=0xD000, d2=0xE000, d3=0xF000, ws=0x100000)
+    a.update(kw)
+    if nbytes is None:
+        err = ctypes.c_int(0)
+        nbytes = P.lib().lact_backward_workspace_bytes(ctypes.byref(desc), ctypes.byref(err))
+    vp = ctypes.c_void_p
+    return P.lib().lact_backward(ctypes.byref(desc), *(vp(a[n]) for n in (
+        "q", "k", "v", "eta", "w1", "w2", "w3", "do", "f1", "f2", "f3", "dq", "dk", "dv", "deta", "d1", "d2", "d3",
+        "ws")), ctypes.c_size_t(nbytes), vp(0))
+
+
+def test_swiglu_backward_errors_before_any_hip_call():
+    d = make_desc(**GOOD)
+    # one workspace query for both fast weights; the SwiGLU backward keeps
+    # every chunk's weights and gradient partials, so it grows with the chunk count
+    assert P.binding.backward_workspace_bytes(d) > P.workspace_bytes(d)
+    assert P.binding.backward_workspace_bytes(make_desc(**dict(GOOD, chunk=128))) > P.binding.backward_workspace_bytes(d)
+    # no Muon, no per-matrix rates, not the linear fast weight
+    for bad in (dict(GOOD, use_muon=True), dict(GOOD, eta_per_matrix=1), dict(GOOD, h=64, fast_weight=1)):
+        assert _bwd_sw(make_desc(**bad), nbytes=1 << 30) == -4
+    for bad in (dict(GOOD, use_muon=True), dict(GOOD, eta_per_matrix=1)):
+        err = ctypes.c_int(0)
+        assert P.lib().lact_backward_workspace_bytes(ctypes.byref(make_desc(**bad)), ctypes.byref(err)) == 0
+        assert err.value == -4
+    assert _bwd_sw(make_desc(**dict(GOOD, d=12)), nbytes=1 << 30) == -4
+    assert _bwd_sw(d, q=0) == -1
+    assert _bwd_sw(d, do=0) == -1
+    assert _bwd_sw(d, w2=0) == -1
+    assert _bwd_sw(d, d3=0) == -1
+    assert _bwd_sw(d, deta=0) == -1
+    assert _bwd_sw(d, w1=0x5008) == -2
+    assert _bwd_sw(d, f2=0x5008) == -2     # a final-weight cotangent, when given, is aligned too
+    assert _bwd_sw(d, deta=0xC002) == -2
+    assert _bwd_sw(d, ws=0) == -3
+    assert _bwd_sw(d, ws=0x100010) == -2   # 256-byte workspace alignment
+    assert _bwd_sw(d, nbytes=P.binding.backward_workspace_bytes(d) - 1) == -3
+    nk = make_desc(**dict(GOOD, n_kv=0))
+    assert _bwd_sw(nk, k=0, v=0, eta=0, dk=0, dv=0, deta=0, ws=0) == -3

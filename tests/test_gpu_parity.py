@@ -1409,6 +1409,126 @@ def test_linear_backward_repeats_bitwise():
         assert np.array_equal(u, w)
 
 
+# ----------------------------------------------------------------------------- SwiGLU backward
+# lact_backward: the reverse of the SwiGLU fast weight's chunk loop against
+# the oracle's reverse (pinned to torch double backward, autograd of an
+# independent chunk loop and finite differences).
+
+
+def run_gpu_swiglu_bwd(cfg, x, ct, with_dW=True):
+    print(f"[gpu] swiglu backward {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} n_kv={cfg.n_kv} n_q={cfg.n_q} "
+          f"C={cfg.chunk} order={cfg.order} io={cfg.io} dW_final={with_dW}", flush=True)
+    n = len(x["q"])
+    B, H = (cfg.B, cfg.H) if n == cfg.BH else (n, 1)
+    sh = lambda a: a.reshape(B, H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    W = [to_dev(sh(x[w]), cfg, torch.float32) for w in ("W1", "W2", "W3")]
+    do = to_dev(sh(ct["do"]), cfg)
+    dWf = tuple(to_dev(sh(ct[w]), cfg, torch.float32) for w in ("dW1", "dW2", "dW3")) if with_dW else None
+    W_in = [w.clone() for w in W]
+    r = P.backward(q, k, v, eta, *W, do, cfg.chunk, order=cfg.order, dW_final=dWf)
+    torch.cuda.synchronize()
+    for a, b in zip(W, W_in):
+        assert torch.equal(a, b)   # the initial weights are read only
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    return tuple(f(t) for t in r)
+
+
+def worst_window(got, ref, rows):
+    """Worst rel-L2 over windows of `rows` rows of every instance of [inst, n]
+    arrays, the last window ending at the last row (no window shorter than
+    `rows` unless the instance is)."""
+    worst, where = 0.0, ""
+    for i in range(got.shape[0]):
+        n = got.shape[1]
+        starts = list(range(0, max(n - rows, 0) + 1, rows))
+        if starts[-1] + rows < n:
+            starts.append(n - rows)
+        for a in starts:
+            e = rel(got[i, a:a + rows], ref[i, a:a + rows])
+            if np.isnan(e) or e > worst:
+                worst, where = e, f"instance {i} rows [{a}, {min(a + rows, n)})"
+    return worst, where
+
+
+def check_swiglu_bwd(cfg, x, ct, got, with_dW=True, instances=None):
+    idx = slice(None) if instances is None else list(instances)
+    sel = lambda a: a if instances is None else a[list(instances)]
+    ref = O.lact_backward(sel(x["q"]), sel(x["k"]), sel(x["v"]), sel(x["eta"]), sel(x["W1"]), sel(x["W2"]),
+                          sel(x["W3"]), sel(ct["do"]), cfg.chunk, cfg.order,
+                          dW_final=tuple(sel(ct[w]) for w in ("dW1", "dW2", "dW3")) if with_dW else None)
+    errs, blocks = {}, {}
+    for name, g, r in zip(("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3"), got, ref):
+        g = g[idx]
+        if g.size == 0:
+            continue
+        errs[name] = rel(g, r)
+        if name == "deta":   # a per-token sum over h with cancellations: windows of 256 tokens
+            blocks[name] = worst_window(g, r, O_BLOCK)
+        else:
+            blocks[name] = worst_block(g, r, W_BLOCK if name.startswith("dW") else O_BLOCK)
+    assert_errs(errs, TOL[cfg.io], blocks)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_backward_bf16_ragged(order):
+    # three chunks (the last partial) and a tail; d, h of several 128-tiles, h != d
+    cfg = CONFIGS["lm32k"].with_(name="swiglu_bwd", B=1, H=2, d=256, h=384, n_kv=700, n_q=760, chunk=256,
+                                 order=order)
+    x, ct = make_inputs(cfg, 71), make_cotangents(cfg, 71)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct))
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_backward_fp32_small(order):
+    # fp32 I/O, dims and a chunk that are not multiples of the tiles or of 32, no final cotangent
+    cfg = CONFIGS["tiny_fp32"].with_(name="swiglu_bwd_fp32", B=2, H=1, d=40, h=56, n_kv=300, n_q=333, chunk=100,
+                                     order=order)
+    x, ct = make_inputs(cfg, 72), make_cotangents(cfg, 72)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct, with_dW=False), with_dW=False)
+
+
+def test_swiglu_backward_narrow_tiles_without_tail():
+    # d = 128 (the narrow bf16 tiles), the video head shape, n_q == n_kv, a last chunk of one token
+    cfg = CONFIGS["video"].with_(name="swiglu_bwd_narrow", B=1, H=3, n_kv=513, n_q=513, chunk=128, use_muon=0)
+    x, ct = make_inputs(cfg, 73), make_cotangents(cfg, 73)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct))
+
+
+def test_swiglu_backward_apply_only():
+    # no key tokens: the apply's reverse over a tail of two pieces (4096 tokens each)
+    cfg = CONFIGS["lm32k"].with_(name="swiglu_bwd_apply_only", B=1, H=1, d=64, h=96, n_kv=0, n_q=5000, chunk=256,
+                                 order=1)
+    x, ct = make_inputs(cfg, 74), make_cotangents(cfg, 74)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct))
+
+
+def test_swiglu_backward_lm_shape_sampled_instance():
+    # one LM sequence (4 heads, d = h = 512, 16 chunks of 2048), one instance checked
+    cfg = CONFIGS["lm32k"].with_(name="swiglu_bwd_lm32k_b1", B=1)
+    x, ct = make_inputs(cfg, 75), make_cotangents(cfg, 75)
+    got = run_gpu_swiglu_bwd(cfg, x, ct)
+    check_swiglu_bwd(cfg, x, ct, got, instances=[2])
+
+
+def test_swiglu_backward_nvs_shape_reduced_context():
+    # d = 768, h = 1536 (dk contracts over 4h = 6144): one update-then-apply chunk of 8192 tokens plus 2048 targets
+    cfg = CONFIGS["nvs256k"].with_(name="nvs8k_swiglu_bwd", n_kv=8192, n_q=8192 + 2048, chunk=8192)
+    x, ct = make_inputs(cfg, 76), make_cotangents(cfg, 76)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct))
+
+
+def test_swiglu_backward_repeats_bitwise():
+    cfg = CONFIGS["lm32k"].with_(name="swiglu_bwd_repeat", B=1, H=2, d=128, h=256, n_kv=600, n_q=640, chunk=256,
+                                 order=0)
+    x, ct = make_inputs(cfg, 77), make_cotangents(cfg, 77)
+    a = run_gpu_swiglu_bwd(cfg, x, ct)
+    b = run_gpu_swiglu_bwd(cfg, x, ct)
+    for u, w in zip(a, b):
+        assert np.array_equal(u, w)
+
+
 # ----------------------------------------------------------------------------- envelope limits
 # The largest head and hidden dims (4096), very many instances, the most
 # Newton-Schulz steps, and a chunk longer than the sequence.

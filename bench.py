@@ -32,7 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "LaCT layer fwd TFLOP/s + tokens/s at 32K ctx; % of bf16 MFMA peak"
-METRIC_BWD = "LaCT linear fast-weight backward TFLOP/s + tokens/s; % of bf16 MFMA peak"
+METRIC_BWD = "LaCT fast-weight backward TFLOP/s + tokens/s; % of bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
@@ -63,7 +63,7 @@ def parse():
     ap.add_argument("--device-inputs", action="store_true",
                     help="draw the inputs on the device (plain uniform-chunk workloads)")
     ap.add_argument("--backward", action="store_true",
-                    help="time the linear fast weight's backward (lact_backward_linear) on a linear workload")
+                    help="time the backward (lact_backward, or lact_backward_linear on a linear workload)")
     ap.add_argument("--traffic-report", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"))
     return ap.parse_args()
 
@@ -262,13 +262,20 @@ def workload_flops(cfg, BH=None):
 
 
 def backward_flops(cfg, BH=None):
-    """Algorithmic FLOPs of the linear fast weight's backward: the replayed
-    chunk gradients (2 d^2 per key token), the key-side cotangents dv = eta dU k
-    and dk = eta dU^T v (4 d^2 per key token) and the apply's dW += dO^T Q and
-    dq = W^T dO (4 d^2 per query token). The second evaluation of the chunk
-    gradient in the reverse is not counted."""
+    """Algorithmic FLOPs of the backward (2 per multiply-add of each product).
+    Linear fast weight: the replayed chunk gradients (2 d^2 per key token),
+    dv = eta dU k and dk = eta dU^T v (4 d^2 per key token), the apply's
+    dW += dO^T Q and dq = W^T dO (4 d^2 per query token). SwiGLU: the replayed
+    update (key forward and gradient, 12 d h per key token), the update's
+    reverse (K U1^T, K U3^T, V U2, dk over 4h, dv over 2h and the three weight
+    cotangents: 24 d h per key token) and the apply's (Q W1^T, Q W3^T, dO W2,
+    dq over 2h and three weight cotangents: 16 d h per query token). Products
+    that the implementation evaluates a second time instead of keeping them
+    (K W1^T, K W3^T, V W2 in the reverse) are not counted."""
     BH = cfg.BH if BH is None else BH
-    return BH * float(cfg.d) * cfg.d * (6.0 * cfg.n_kv + 4.0 * cfg.n_q)
+    if cfg.linear:
+        return BH * float(cfg.d) * cfg.d * (6.0 * cfg.n_kv + 4.0 * cfg.n_q)
+    return BH * float(cfg.d) * cfg.h * (36.0 * cfg.n_kv + 16.0 * cfg.n_q)
 
 
 def describe(cfg):
@@ -311,7 +318,7 @@ def _oracle_sample(cfg, min_seconds, backward=False):
     that budget (NVS: 1M tokens in one chunk is ~22 TFLOP), the sample is the
     first tokens of one instance with the same d, h, order and options,
     chunked at the same size up to the sample length.
-    With backward, the oracle's reverse of the linear fast weight's chunk loop.
+    With backward, the oracle's reverse of the chunk loop.
     Returns (FLOPs done, seconds, sample description, tokens done)."""
     from lact_synth import make_cotangents, make_inputs
     from oracle import lact_oracle as O
@@ -330,9 +337,12 @@ def _oracle_sample(cfg, min_seconds, backward=False):
         x = make_inputs(scfg, 0, heads=[done])
         ct = make_cotangents(scfg, 0, heads=[done]) if backward else None
         t0 = time.perf_counter()
-        if backward:
+        if backward and scfg.linear:
             O.lact_backward_linear_instance(x["q"][0], x["k"][0], x["v"][0], x["eta"][0], x["W1"][0], ct["do"][0],
                                             scfg.chunk, scfg.order)
+        elif backward:
+            O.lact_backward_instance(x["q"][0], x["k"][0], x["v"][0], x["eta"][0], x["W1"][0], x["W2"][0],
+                                     x["W3"][0], ct["do"][0], scfg.chunk, scfg.order)
         elif scfg.linear:
             O.lact_forward_linear(x["q"], x["k"], x["v"], x["eta"], x["W1"], scfg.chunk, scfg.order,
                                   bool(scfg.use_muon), scfg.ns_steps)
@@ -490,20 +500,23 @@ def measure(cfg, args, P, on_device=False):
 
     if args.backward:
         from lact_synth import make_cotangents
-        if not cfg.linear or cfg.use_muon or cfg.momentum or on_device:
-            raise SystemExit("--backward runs the linear fast weight without Muon or momentum, host-drawn inputs")
+        if cfg.use_muon or cfg.momentum or cfg.lr3 or cfg.schedule or cfg.layer_io or on_device:
+            raise SystemExit("--backward runs without Muon, momentum, per-matrix rates or a schedule, host-drawn inputs")
         ct = make_cotangents(cfg, 0)
         dout = torch.from_numpy(ct["do"].reshape(cfg.B, cfg.H, cfg.n_q, cfg.d)).to(dev, io)
         del ct
         grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v), torch.empty_like(eta),
-                 torch.empty_like(W[0]))
+                 *(torch.empty_like(w) for w in (W[:1] if cfg.linear else W)))
         bdesc = desc
         ws = torch.empty(P.backward_workspace_bytes(bdesc), dtype=torch.uint8, device=dev)
 
     def path():
-        if args.backward:
+        if args.backward and cfg.linear:
             P.backward_linear(q, k, v, eta, W[0], dout, cfg.chunk, order=cfg.order, out=grads, workspace=ws,
                               stream=launch_stream())
+        elif args.backward:
+            P.backward(q, k, v, eta, *W, dout, cfg.chunk, order=cfg.order, out=grads, workspace=ws,
+                       stream=launch_stream())
         elif cfg.linear:
             P.forward_linear(q, k, v, eta, W[0], cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
                              ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=launch_stream())
@@ -548,7 +561,8 @@ def measure(cfg, args, P, on_device=False):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if cfg.io == "bf16" else "fp32", "data": "synthetic",
-        "config": {"workload": describe(cfg) + (", backward (lact_backward_linear)" if args.backward else ""),
+        "config": {"workload": describe(cfg) + ((", backward (lact_backward_linear)" if cfg.linear else
+                                                 ", backward (lact_backward)") if args.backward else ""),
                    "tokens_per_step": tokens, "flops_per_step": flops},
         "tokens_per_s": round(tokens / dt, 1),
         "launch": "hip_graph" if args.graph else "eager",
@@ -609,9 +623,9 @@ def measure(cfg, args, P, on_device=False):
 
 # The second workload that the performance target names, measured in the same
 # process after the default one: NVS with a million context tokens; then the
-# backward of the linear fast weight at the LM shape.
+# backward at the LM shape, with the SwiGLU and with the linear fast weight.
 SECONDARY = "nvs1m"
-SECONDARY_BWD = "lm32k_linear"
+SECONDARY_BWD = ("lm32k", "lm32k_linear")
 
 
 def main():
@@ -648,12 +662,12 @@ def main():
         keep = ("value", "unit", "ms_per_step", "tokens_per_s", "pct_of_peak", "data", "config", "roofline")
         res["secondary"] = {SECONDARY: {k: sec[k] for k in keep if k in sec}}
         torch.cuda.empty_cache()
-        # the backward of the linear fast weight at the LM shape (its own metric)
+        # the backward at the LM shape, SwiGLU and linear fast weight (its own metric)
         bargs = argparse.Namespace(**{**vars(args), "backward": True})
-        bwd = measure(CONFIGS[SECONDARY_BWD], bargs, P)
-        res["secondary"][SECONDARY_BWD + "_backward"] = {"metric": bwd["metric"],
-                                                          **{k: bwd[k] for k in keep if k in bwd}}
-        torch.cuda.empty_cache()
+        for name in SECONDARY_BWD:
+            bwd = measure(CONFIGS[name], bargs, P)
+            res["secondary"][name + "_backward"] = {"metric": bwd["metric"], **{k: bwd[k] for k in keep if k in bwd}}
+            torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, args.backward)
     print(json.dumps(res), flush=True)

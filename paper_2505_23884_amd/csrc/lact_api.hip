@@ -1272,16 +1272,17 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     if (rc) return rc;
   }
   // transposed operand copies of W_0 .. W_nch (W_1 .. W_nch are contiguous)
-  rc = timed(LACT_KCLASS_PREP, 0.0, s,
-             [&] { return launch_copy_w(W0, dd, wt(0), d, dd, p.BH, p.d, p.d, true, p.bf16, s); });
+  {
+    const CopySeg cs{W0, dd, wt(0), d, dd, p.d, p.d, 1};
+    rc = timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_copies(&cs, 1, p.BH, p.bf16, s); });
+  }
   if (rc) return rc;
   {
     const int64_t t = cdiv(d, 32), per = std::max<int64_t>(1, ((int64_t)1 << 30) / (BH * t * t));
     for (int64_t c0 = 1; c0 <= L.nch; c0 += per) {   // whole sets of BH matrices, under 2^30 blocks
       const int64_t m = std::min(per, L.nch + 1 - c0);
-      rc = timed(LACT_KCLASS_PREP, 0.0, s, [&] {
-        return launch_copy_w(traj(c0), dd, wt(c0), d, dd, (int)(m * BH), p.d, p.d, true, p.bf16, s);
-      });
+      const CopySeg cs{traj(c0), dd, wt(c0), d, dd, p.d, p.d, 1};
+      rc = timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_copies(&cs, 1, (int)(m * BH), p.bf16, s); });
       if (rc) return rc;
     }
   }
@@ -1336,7 +1337,7 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     va.BH = p.BH;
     va.R = p.d;
     va.L = p.d;
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(va, p.bf16, s); });
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(&va, 1, p.bf16, s); });
     if (rc) return rc;
     BwdArgs b{};
     lin_out_seg(b.seg[0], p, op(kb + s0 * d * esz, d, n_kv * d), op(ub, d, dd), (uint8_t*)dv + s0 * d * esz,
@@ -1366,23 +1367,24 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
 // in a slot of its own, and reading W_c from the trajectory while writing
 // W_{c+1}). The reverse then walks the chunks from the last, carrying the
 // cotangent of (W1, W2, W3) in dW1, dW2, dW3. Per chunk: the row-wise reverse
-// of the update (three matrices), six [n x h] products (Z1 = K W1^T,
-// Z3 = K W3^T, C = V W2 and the same three with the update's cotangent), the
-// per-token step with SiLU's first and second derivatives, dk (one product
-// over 4h) and dv (over 2h), the weight cotangents of the gradient's own
-// dependence on W (GRAD13 + GRAD2), and the apply's reverse (three [n x h]
-// products, a per-token step, dq over 2h, its weight cotangents). The
-// contractions are the OUT and GRAD kinds with operands laid out so that
-// each sum runs over one contiguous row ([R3 | R1 | dZ1 | dZ3] against
-// [U3^T | U1^T | W1^T | W3^T], [eta A | dC] against [U2 | W2]).
+// of the update (three matrices, one launch), the operand copies of the
+// chunk's weights (one launch), nine [n x h] products in three launches
+// (Z1 = K W1^T, Z3 = K W3^T, C = V W2; the same with the update's cotangent;
+// the apply's Q W1^T, Q W3^T, dO W2), the per-token steps with SiLU's first
+// and second derivatives, one launch for dk (a sum over 4h), dv and dq (over
+// 2h), and the weight cotangents of the gradient's own dependence on W and
+// of the apply (GRAD13 + GRAD2, two launches). The contractions are the OUT
+// and GRAD kinds with operands laid out so that each sum runs over one
+// contiguous row ([R3 | R1 | dZ1 | dZ3] against [U3^T | U1^T | W1^T | W3^T],
+// [eta A | dC] against [U2 | W2], [dZq1 | dZq3] against [W1^T | W3^T]).
 struct SwBwdLayout {
   Plan p;               // the forward's plan without the fused gradient-and-update kind
   int64_t nch;          // chunks of the forward
   int64_t T;            // token rows of the chunk buffers (a chunk, or a piece of the tail)
   int64_t tail_split;   // tokens per split of a tail piece (at most p.nsplit splits)
   size_t slotP;         // bytes of one chunk's gradient partials
-  size_t off_P, off_traj, off_z[6], off_pk, off_pv, off_u[3], off_a[3], off_bk, off_bv, off_bq, off_ur[3],
-      off_apart, off_bpart, total;
+  size_t off_P, off_traj, off_z[6], off_pk, off_pv, off_pq, off_hq, off_u[3], off_a[3], off_bk, off_bv, off_bq,
+      off_ur[3], off_apart, off_bpart, total;
 };
 
 int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L) {
@@ -1395,7 +1397,7 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L) {
   L->nch = dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0;
   const int64_t tail = dsc->n_q - dsc->n_kv;
   L->T = std::max<int64_t>(1, std::max<int64_t>(p.C, std::min<int64_t>(tail, 4096)));
-  const double need = (double)L->nch * p.BH * dh * 12.0 * (p.nsplit + 1) + (double)p.BH * L->T * p.h * p.esz * 12.0;
+  const double need = (double)L->nch * p.BH * dh * 12.0 * (p.nsplit + 1) + (double)p.BH * L->T * p.h * p.esz * 15.0;
   if (need > 4.0e18) return LACT_EUNSUPPORTED;
   L->tail_split = std::max<int64_t>(32, cdiv(cdiv(L->T, p.nsplit), 32) * 32);
   const size_t w4 = (size_t)p.BH * p.d * p.h * 4, wio = (size_t)p.BH * p.d * p.h * p.esz;
@@ -1403,40 +1405,26 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L) {
   L->slotP = (size_t)p.nsplit * 3 * w4;
   // the forward's own layout first (at least what its validation asks for)
   size_t o = align_up(std::max(p.total, make_plan(dsc).total));
-  L->off_P = o;
-  o = align_up(o + (size_t)L->nch * L->slotP);
-  L->off_traj = o;
-  o = align_up(o + (size_t)L->nch * 3 * w4);
-  for (int i = 0; i < 6; ++i) {
-    L->off_z[i] = o;
-    o = align_up(o + rows);
-  }
-  L->off_pk = o;
-  o = align_up(o + 4 * rows);
-  L->off_pv = o;
-  o = align_up(o + 2 * rows);
-  for (int i = 0; i < 3; ++i) {   // W1, W3 row-major and W2^T of the update's weights, then the apply's
-    L->off_u[i] = o;
-    o = align_up(o + wio);
-  }
-  for (int i = 0; i < 3; ++i) {
-    L->off_a[i] = o;
-    o = align_up(o + wio);
-  }
-  L->off_bk = o;   // [d x 4h]: U3^T | U1^T | W1^T | W3^T
-  o = align_up(o + 4 * wio);
-  L->off_bv = o;   // [d x 2h]: U2 | W2
-  o = align_up(o + 2 * wio);
-  L->off_bq = o;   // [d x 2h]: W1^T | W3^T of the apply's weights
-  o = align_up(o + 2 * wio);
-  for (int i = 0; i < 3; ++i) {   // U1, U3 row-major and U2^T
-    L->off_ur[i] = o;
-    o = align_up(o + wio);
-  }
-  L->off_apart = o;
-  o = align_up(o + (size_t)p.nsplit * 3 * w4);
-  L->off_bpart = o;
-  o = align_up(o + (size_t)p.nsplit * 3 * w4);
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  L->off_P = take((size_t)L->nch * L->slotP);
+  L->off_traj = take((size_t)L->nch * 3 * w4);
+  for (int i = 0; i < 6; ++i) L->off_z[i] = take(rows);
+  L->off_pk = take(4 * rows);   // [T x 4h]: R3 | R1 | dZ1 | dZ3
+  L->off_pv = take(2 * rows);   // [T x 2h]: eta A | dC
+  L->off_pq = take(2 * rows);   // [T x 2h]: dZq1 | dZq3
+  L->off_hq = take(rows);       // [T x h]: the apply's hidden
+  for (int i = 0; i < 3; ++i) L->off_u[i] = take(wio);   // W1, W3 row-major and W2^T of the update's weights
+  for (int i = 0; i < 3; ++i) L->off_a[i] = take(wio);   // the same of the apply's weights
+  L->off_bk = take(4 * wio);    // [d x 4h]: U3^T | U1^T | W1^T | W3^T
+  L->off_bv = take(2 * wio);    // [d x 2h]: U2 | W2
+  L->off_bq = take(2 * wio);    // [d x 2h]: W1^T | W3^T of the apply's weights
+  for (int i = 0; i < 3; ++i) L->off_ur[i] = take(wio);   // U1, U3 row-major and U2^T
+  L->off_apart = take((size_t)p.nsplit * 3 * w4);
+  L->off_bpart = take((size_t)p.nsplit * 3 * w4);
   L->total = o;
   return LACT_OK;
 }
@@ -1505,22 +1493,28 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
   for (int i = 0; i < 6; ++i) zb[i] = ws + L.off_z[i];
   uint8_t* pk = ws + L.off_pk;
   uint8_t* pv = ws + L.off_pv;
+  uint8_t* pq = ws + L.off_pq;
+  uint8_t* hq = ws + L.off_hq;
   uint8_t* bk = ws + L.off_bk;
   uint8_t* bv = ws + L.off_bv;
   uint8_t* bq = ws + L.off_bq;
+  uint8_t* ur[3] = {ws + L.off_ur[0], ws + L.off_ur[1], ws + L.off_ur[2]};
   float* apart = reinterpret_cast<float*>(ws + L.off_apart);
   float* bpart = reinterpret_cast<float*>(ws + L.off_bpart);
   const int64_t T = L.T;
+  const int64_t zi = T * h;   // elements between instances of a [T x h] buffer
   // one launch of up to three OUT segments, out[t][m] = sum_e a[t][e] b[m][e]
-  // over K columns, rows of out `rows_out` wide
+  // over K columns (per segment), rows of out `rows_out` wide
   struct Out {
     Operand a, b;
     void* out;
     int64_t out_inst;
+    int64_t K;
   };
-  auto outs = [&](const Out* o, int nseg, int64_t n, int rows_out, int K) -> int {
+  auto outs = [&](const Out* o, int nseg, int64_t n, int rows_out) -> int {
     BwdArgs b{};
     const TileShape t = bwd_tile(BWD_OUT, p.bf16, p.narrow);
+    double fl = 0.0;
     for (int i = 0; i < nseg; ++i) {
       BwdSeg& g = b.seg[i];
       g.kind = BWD_OUT;
@@ -1533,17 +1527,19 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       g.b0 = o[i].b;
       g.out = o[i].out;
       g.out_inst = o[i].out_inst;
+      g.klen = o[i].K;
+      fl += 2.0 * BH * n * rows_out * o[i].K;
     }
     b.nseg = nseg;
     b.total_blocks = 0;
     for (int i = 0; i < nseg; ++i) b.total_blocks += b.seg[i].nblocks;
     b.d = rows_out;
-    b.h = K;
+    b.h = (int)o[0].K;
     b.narrow = p.narrow;
-    return timed(LACT_KCLASS_BWD, 2.0 * nseg * BH * n * rows_out * K, s, [&] { return launch_bwd(b, p.bf16, s); });
+    return timed(LACT_KCLASS_BWD, fl, s, [&] { return launch_bwd(b, p.bf16, s); });
   };
   // weight cotangents over rows [0, n): W1 += a1^T b, W3 += a3^T b (GRAD13)
-  // and W2 += a2^T b2 (GRAD2), as split partials into `out`; returns the split count
+  // and W2 += a2^T b2 (GRAD2), as split partials into `out`
   auto grads = [&](Operand a1, Operand a3, Operand b13, Operand a2, Operand b2, float* out, int64_t n,
                    int64_t split_len, int* nsplit) -> int {
     const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16, p.narrow), g2 = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
@@ -1585,60 +1581,59 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     *nsplit = ns;
     return timed(LACT_KCLASS_BWD, 6.0 * BH * n * dh, s, [&] { return launch_bwd(b, p.bf16, s); });
   };
-  auto copy = [&](const float* W, int R, int Lc, void* dst, int64_t ld, int64_t dst_inst, bool trans) -> int {
-    return timed(LACT_KCLASS_PREP, 0.0, s, [&] {
-      return launch_copy_w(W, (int64_t)R * Lc, dst, ld, dst_inst, p.BH, R, Lc, trans, p.bf16, s);
-    });
+  // operand copies of weights (W1, W2, W3): W1, W3 row-major and W2^T into
+  // `u`, W1^T | W3^T into `bt` (ld bt_ld), and W2 into `b2` (ld 2h) if given
+  auto weight_copies = [&](int64_t i, const size_t* u, uint8_t* bt, int64_t bt_ld, uint8_t* b2) -> int {
+    const float* W1 = traj(i, 0);
+    const float* W2 = traj(i, 1);
+    const float* W3 = traj(i, 2);
+    const CopySeg cs[6] = {{W1, dh, ws + u[0], d, dh, (int)h, (int)d, 0},
+                           {W3, dh, ws + u[1], d, dh, (int)h, (int)d, 0},
+                           {W2, dh, ws + u[2], d, dh, (int)d, (int)h, 1},
+                           {W1, dh, bt, bt_ld, d * bt_ld, (int)h, (int)d, 1},
+                           {W3, dh, bt + h * esz, bt_ld, d * bt_ld, (int)h, (int)d, 1},
+                           {W2, dh, b2, 2 * h, d * 2 * h, (int)d, (int)h, 0}};
+    return timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_copies(cs, b2 ? 6 : 5, p.BH, p.bf16, s); });
   };
-  // operand copies of weights (W1, W2, W3) for the [n x h] products (W1, W3
-  // row-major, W2^T) into set `u`, and W1^T, W3^T into `bt` (ld bt_ld)
-  auto weight_copies = [&](const float* W1, const float* W2, const float* W3, const size_t* u, uint8_t* bt,
-                           int64_t bt_ld) -> int {
-    int r = copy(W1, (int)h, (int)d, ws + u[0], d, dh, false);
-    if (!r) r = copy(W3, (int)h, (int)d, ws + u[1], d, dh, false);
-    if (!r) r = copy(W2, (int)d, (int)h, ws + u[2], d, dh, true);
-    if (!r) r = copy(W1, (int)h, (int)d, bt, bt_ld, d * bt_ld, true);
-    if (!r) r = copy(W3, (int)h, (int)d, bt + h * esz, bt_ld, d * bt_ld, true);
-    return r;
-  };
-  const int64_t zi = T * h;   // elements between instances of a [T x h] buffer
   int a_ns = 0, b_ns = 0;
-  // the apply's reverse on query rows [a, a + n) with the weights whose
-  // copies are in `u` (row-major W1, W3 and W2^T) and `bt` (W1^T | W3^T, ld bt_ld)
-  auto apply_back = [&](int64_t a, int64_t n, const size_t* u, const uint8_t* bt, int64_t bt_ld,
-                        int64_t split_len) -> int {
+  // the apply's reverse on query rows [a, a + n) up to its weight cotangents
+  // (into apart) with the weights whose copies are in `u`; dq is left to
+  // the caller's OUT launch (Pq against the transposed weights)
+  auto apply_back = [&](int64_t a, int64_t n, const size_t* u, int64_t split_len) -> int {
     const Operand qo = op(qb + a * d * esz, d, n_q * d), doo = op(ob + a * d * esz, d, n_q * d);
-    const Out h3[3] = {{qo, op(ws + u[0], d, dh), zb[0], zi},
-                       {qo, op(ws + u[1], d, dh), zb[1], zi},
-                       {doo, op(ws + u[2], d, dh), zb[2], zi}};
-    int r = outs(h3, 3, n, (int)h, (int)d);
+    const Out h3[3] = {{qo, op(ws + u[0], d, dh), zb[0], zi, d},
+                       {qo, op(ws + u[1], d, dh), zb[1], zi, d},
+                       {doo, op(ws + u[2], d, dh), zb[2], zi, d}};
+    int r = outs(h3, 3, n, (int)h);
     if (r) return r;
     r = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
-      return launch_swiglu_apply_rows(zb[0], zb[1], zb[2], zi, pk, T * 2 * h, pv, zi, p.BH, n, (int)h, p.bf16, s);
+      return launch_swiglu_apply_rows(zb[0], zb[1], zb[2], zi, pq, T * 2 * h, hq, zi, p.BH, n, (int)h, p.bf16, s);
     });
     if (r) return r;
-    const Out dqo{op(pk, 2 * h, T * 2 * h), op(bt, bt_ld, d * bt_ld), (uint8_t*)dq + a * d * esz, n_q * d};
-    r = outs(&dqo, 1, n, (int)d, (int)(2 * h));
-    if (r) return r;
-    return grads(op(pk, 2 * h, T * 2 * h), op(pk + h * esz, 2 * h, T * 2 * h), qo, doo, op(pv, h, zi), apart, n,
+    return grads(op(pq, 2 * h, T * 2 * h), op(pq + h * esz, 2 * h, T * 2 * h), qo, doo, op(hq, h, zi), apart, n,
                  split_len, &a_ns);
+  };
+  auto dq_out = [&](int64_t a, const uint8_t* bt, int64_t bt_ld) -> Out {
+    return Out{op(pq, 2 * h, T * 2 * h), op(bt, bt_ld, d * bt_ld), (uint8_t*)dq + a * d * esz, n_q * d, 2 * h};
   };
   auto pset = [&](float* base, int ns, int m) -> PartSet { return PartSet{base + m * dh, ns, psplit, 3 * dh}; };
   // tail [n_kv, n_q): applied with the final weights, on top of dW_final (or zero)
   bool first = true;
   if (any_q && n_q > n_kv) {
-    rc = weight_copies(traj(L.nch, 0), traj(L.nch, 1), traj(L.nch, 2), L.off_a, bq, 2 * h);
+    rc = weight_copies(L.nch, L.off_a, bq, 2 * h, nullptr);
     if (rc) return rc;
     for (int64_t a = n_kv; a < n_q; a += T) {
       const int64_t n = std::min(T, n_q - a);
-      rc = apply_back(a, n, L.off_a, bq, 2 * h, L.tail_split);
+      rc = apply_back(a, n, L.off_a, L.tail_split);
+      if (rc) return rc;
+      const Out o = dq_out(a, bq, 2 * h);
+      rc = outs(&o, 1, n, (int)d);
       if (rc) return rc;
       for (int m = 0; m < 3; ++m) {
-        const int64_t RL = dh;
         const int mode = first ? (dWf[m] ? 1 : 0) : 2;
         const PartSet ps = pset(apart, a_ns, m);
         rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
-                   [&] { return launch_accum(dW[m], RL, dWf[m], RL, mode, ps, PartSet{}, p.BH, RL, s); });
+                   [&] { return launch_accum(dW[m], dh, dWf[m], dh, mode, ps, PartSet{}, p.BH, dh, s); });
         if (rc) return rc;
       }
       first = false;
@@ -1654,59 +1649,60 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
   }
   const bool then_apply = desc->order == LACT_UPDATE_THEN_APPLY;
   bool a_pending = false, b_pending = false;   // partials that the next reverse adds first
-  uint8_t* ur[3] = {ws + L.off_ur[0], ws + L.off_ur[1], ws + L.off_ur[2]};
   for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
     const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
-    if (then_apply) {   // applied with the weights leaving the chunk
-      rc = weight_copies(traj(ci + 1, 0), traj(ci + 1, 1), traj(ci + 1, 2), L.off_a, bq, 2 * h);
-      if (!rc) rc = apply_back(s0, n, L.off_a, bq, 2 * h, p.split_len);
+    if (then_apply) {   // applied with the weights leaving the chunk: its cotangent joins first
+      rc = weight_copies(ci + 1, L.off_a, bq, 2 * h, nullptr);
+      if (!rc) rc = apply_back(s0, n, L.off_a, p.split_len);
       if (rc) return rc;
       a_pending = true;
     }
-    // the update's reverse, matrix by matrix: W1, W3 ([h x d]) and W2 ([d x h])
+    // the update's reverse: W1, W3 ([h x d]) and W2 ([d x h]) in one launch
+    VjpArgs va[3] = {};
     for (int m = 0; m < 3; ++m) {
-      VjpArgs va{};
+      VjpArgs& x = va[m];
       const bool w2 = m == 1;
-      va.W = traj(ci, m);
-      va.w_inst = dh;
-      va.P = pset(reinterpret_cast<float*>(ws + L.off_P + (size_t)ci * L.slotP), p.nsplit, m);
-      if (b_pending) va.pre[0] = pset(bpart, b_ns, m);
-      if (a_pending) va.pre[1] = pset(apart, a_ns, m);
-      va.G = dW[m];
-      va.g_inst = dh;
+      x.W = traj(ci, m);
+      x.w_inst = dh;
+      x.P = pset(reinterpret_cast<float*>(ws + L.off_P + (size_t)ci * L.slotP), p.nsplit, m);
+      if (b_pending) x.pre[0] = pset(bpart, b_ns, m);
+      if (a_pending) x.pre[1] = pset(apart, a_ns, m);
+      x.G = dW[m];
+      x.g_inst = dh;
       if (w2) {   // U2 row-major into [U2 | W2], U2^T for V U2
-        va.Ub = bv;
-        va.ub_ld = 2 * h;
-        va.ub_inst = d * 2 * h;
-        va.UT = ur[2];
-        va.ut_ld = d;
-        va.ut_inst = dh;
+        x.Ub = bv;
+        x.ub_ld = 2 * h;
+        x.ub_inst = d * 2 * h;
+        x.UT = ur[2];
+        x.ut_ld = d;
+        x.ut_inst = dh;
       } else {    // U1, U3 row-major for K U^T; transposed into [U3^T | U1^T | ...]
-        va.Ub = ur[m == 0 ? 0 : 1];
-        va.ub_ld = d;
-        va.ub_inst = dh;
-        va.UT = bk + (m == 0 ? h : 0) * esz;
-        va.ut_ld = 4 * h;
-        va.ut_inst = d * 4 * h;
+        x.Ub = ur[m == 0 ? 0 : 1];
+        x.ub_ld = d;
+        x.ub_inst = dh;
+        x.UT = bk + (m == 0 ? h : 0) * esz;
+        x.ut_ld = 4 * h;
+        x.ut_inst = d * 4 * h;
       }
-      va.BH = p.BH;
-      va.R = (int)(w2 ? d : h);
-      va.L = (int)(w2 ? h : d);
-      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(va, p.bf16, s); });
-      if (rc) return rc;
+      x.BH = p.BH;
+      x.R = (int)(w2 ? d : h);
+      x.L = (int)(w2 ? h : d);
     }
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(va, 3, p.bf16, s); });
+    if (rc) return rc;
     a_pending = b_pending = false;
-    rc = weight_copies(traj(ci, 0), traj(ci, 1), traj(ci, 2), L.off_u, bk + 2 * h * esz, 4 * h);
-    if (!rc) rc = copy(traj(ci, 1), (int)d, (int)h, bv + h * esz, 2 * h, d * 2 * h, false);   // W2 into [U2 | W2]
+    rc = weight_copies(ci, L.off_u, bk + 2 * h * esz, 4 * h, bv + h * esz);
     if (rc) return rc;
     const Operand ko = op(kb + s0 * d * esz, d, n_kv * d), vo = op(vb + s0 * d * esz, d, n_kv * d);
-    const Out f3[3] = {{ko, op(ws + L.off_u[0], d, dh), zb[0], zi},
-                       {ko, op(ws + L.off_u[1], d, dh), zb[1], zi},
-                       {vo, op(ws + L.off_u[2], d, dh), zb[2], zi}};
-    rc = outs(f3, 3, n, (int)h, (int)d);
+    const Out f3[3] = {{ko, op(ws + L.off_u[0], d, dh), zb[0], zi, d},
+                       {ko, op(ws + L.off_u[1], d, dh), zb[1], zi, d},
+                       {vo, op(ws + L.off_u[2], d, dh), zb[2], zi, d}};
+    rc = outs(f3, 3, n, (int)h);
     if (rc) return rc;
-    const Out x3[3] = {{ko, op(ur[0], d, dh), zb[3], zi}, {ko, op(ur[1], d, dh), zb[4], zi}, {vo, op(ur[2], d, dh), zb[5], zi}};
-    rc = outs(x3, 3, n, (int)h, (int)d);
+    const Out x3[3] = {{ko, op(ur[0], d, dh), zb[3], zi, d},
+                       {ko, op(ur[1], d, dh), zb[4], zi, d},
+                       {vo, op(ur[2], d, dh), zb[5], zi, d}};
+    rc = outs(x3, 3, n, (int)h);
     if (rc) return rc;
     SwigluRowsArgs ra{};
     ra.Z1 = zb[0];
@@ -1728,21 +1724,22 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     ra.h = (int)h;
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_swiglu_rows(ra, p.bf16, s); });
     if (rc) return rc;
-    const Out dko{op(pk, 4 * h, T * 4 * h), op(bk, 4 * h, d * 4 * h), (uint8_t*)dk + s0 * d * esz, n_kv * d};
-    rc = outs(&dko, 1, n, (int)d, (int)(4 * h));
-    if (rc) return rc;
-    const Out dvo{op(pv, 2 * h, T * 2 * h), op(bv, 2 * h, d * 2 * h), (uint8_t*)dv + s0 * d * esz, n_kv * d};
-    rc = outs(&dvo, 1, n, (int)d, (int)(2 * h));
+    if (!then_apply) {   // applied with the weights entering the chunk (their copies are in place)
+      rc = apply_back(s0, n, L.off_u, p.split_len);
+      if (rc) return rc;
+    }
+    // dk (a sum over 4h), dv and dq (over 2h) in one launch
+    const Out kvq[3] = {
+        {op(pk, 4 * h, T * 4 * h), op(bk, 4 * h, d * 4 * h), (uint8_t*)dk + s0 * d * esz, n_kv * d, 4 * h},
+        {op(pv, 2 * h, T * 2 * h), op(bv, 2 * h, d * 2 * h), (uint8_t*)dv + s0 * d * esz, n_kv * d, 2 * h},
+        then_apply ? dq_out(s0, bq, 2 * h) : dq_out(s0, bk + 2 * h * esz, 4 * h)};
+    rc = outs(kvq, 3, n, (int)d);
     if (rc) return rc;
     rc = grads(op(pk + 2 * h * esz, 4 * h, T * 4 * h), op(pk + 3 * h * esz, 4 * h, T * 4 * h), ko, vo,
                op(pv + h * esz, 2 * h, T * 2 * h), bpart, n, p.split_len, &b_ns);
     if (rc) return rc;
     b_pending = true;
-    if (!then_apply) {   // applied with the weights entering the chunk (copies made above)
-      rc = apply_back(s0, n, L.off_u, bk + 2 * h * esz, 4 * h, p.split_len);
-      if (rc) return rc;
-      a_pending = true;
-    }
+    a_pending = !then_apply;   // the entering weights' apply joins before the previous chunk's reverse
   }
   if (a_pending || b_pending) {
     for (int m = 0; m < 3; ++m) {

@@ -65,6 +65,7 @@ struct BwdSeg {
   int64_t out_off;      // GRAD2: offset of its matrix in an instance's partials
   const float* row_scale;  // OUT (or nullptr): token t's row is scaled by row_scale[inst * scale_inst + t]
   int64_t scale_inst;
+  int64_t klen;         // OUT: contraction length (0: the launch's h)
   // GRAD_UPD (16-bit I/O, whole rows per tile, no split): the gradients of
   // W1 (a0 = eta dz1, b0 = K), W3 (a1 = eta dz3, b0) and W2 (a2 = V,
   // b1 = eta hidden) and the weight update in one pass; tiles_m counts the
@@ -309,11 +310,18 @@ struct VjpArgs {
   int BH, R, L;
 };
 
-hipError_t launch_vjp(const VjpArgs& a, bool io_bf16, hipStream_t s);
-// dst = W (trans = false: dst[r * ld + c]) or W^T (dst[c * ld + r]) in the
-// operand type, from fp32 [R x L] matrices w_inst apart (dst_inst apart).
-hipError_t launch_copy_w(const float* W, int64_t w_inst, void* dst, int64_t ld, int64_t dst_inst, int BH, int R, int L,
-                         bool trans, bool io_bf16, hipStream_t s);
+// Up to three matrices' reverses in one launch (rows of the longest up to 4096).
+hipError_t launch_vjp(const VjpArgs* a, int n, bool io_bf16, hipStream_t s);
+// Operand copies of fp32 [R x L] matrices (w_inst apart): dst = W
+// (dst[r * ld + c]) or W^T (dst[c * ld + r]) in the operand type, dst_inst
+// apart; up to kMaxCopies in one launch.
+struct CopySeg {
+  const float* W; int64_t w_inst;
+  void* dst; int64_t ld, dst_inst;
+  int R, L, trans;
+};
+constexpr int kMaxCopies = 8;
+hipError_t launch_copies(const CopySeg* c, int n, int BH, bool io_bf16, hipStream_t s);
 // G = base + sum of the sets over BH instances of RL floats each (RL a
 // multiple of 4); base: 0 (mode 0), init (mode 1) or G itself (mode 2).
 hipError_t launch_accum(float* G, int64_t g_inst, const float* init, int64_t i_inst, int mode, PartSet s0, PartSet s1,

@@ -1303,9 +1303,10 @@ __device__ __forceinline__ void bwd_body(const BwdArgs& args, int blk, uint8_t* 
     const int64_t m0 = (int64_t)(rr % sg.tiles_m) * KO::ROWS_A;   // feature tile (fastest)
     const int64_t t0 = (int64_t)(rr / sg.tiles_m) * KO::ROWS_B;   // token tile
     const int64_t mrows = d - m0, ntok = sg.rows - t0;
-    const View ops[2] = {view_k(sg.b0, inst, m0, 0, mrows, h, esz), view_k(sg.a0, inst, t0, 0, ntok, h, esz)};
+    const int64_t kk = sg.klen ? sg.klen : h;   // contraction length of this segment
+    const View ops[2] = {view_k(sg.b0, inst, m0, 0, mrows, kk, esz), view_k(sg.a0, inst, t0, 0, ntok, kk, esz)};
     Acc<KO> acc;
-    mainloop<T, KO>(smem, ops, h, acc);
+    mainloop<T, KO>(smem, ops, kk, acc);
     const int64_t ob = inst * sg.out_inst;
     const int mrow0 = wave_m<KO>() * 32 * KO::MI + ((lane >> 5) << 2);
     if (sg.row_scale) {   // per-token factor of the output rows
@@ -2302,15 +2303,14 @@ __device__ __forceinline__ void add_set(const PartSet& s, int64_t inst, int64_t 
 // operand type, row-major into Ub and transposed into UT. A zero row norm
 // gives the same non-finite values as the forward's division.
 template <typename T, int NV>
-__global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_vjp(const VjpArgs a) {
+__device__ __forceinline__ void vjp_body(const VjpArgs& a, int blk, T* tile) {
   constexpr int RR = vjp_rows<T, NV>();
   constexpr int NW = vjp_waves<NV>();
   constexpr int LD = 256 * NV + 4 / (int)sizeof(T);   // one 4-byte word of padding per staged row
-  __shared__ __attribute__((aligned(16))) T tile[RR * LD];
   const int L = a.L;
   const int per = (a.R + RR - 1) / RR;
-  const int64_t inst = blockIdx.x / per;
-  const int r0 = (int)(blockIdx.x - inst * per) * RR;
+  const int64_t inst = blk / per;
+  const int r0 = (int)(blk - inst * per) * RR;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nv = L >> 2;
   T* Ub = reinterpret_cast<T*>(a.Ub);
@@ -2382,35 +2382,57 @@ __global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_vjp(const VjpArgs a) {
   }
 }
 
-// Operand copy of fp32 [R x L] matrices, transposed or not: 32 x 32 tiles
-// through LDS so that both sides move whole rows; one block per (instance,
-// tile) in a flat grid.
-template <typename T, bool TRANS>
-__global__ __launch_bounds__(256) void k_copy_w(const float* W, int64_t w_inst, T* dst, int64_t ld, int64_t d_inst,
-                                                int R, int L, int tr, int tl) {
+// Up to three matrices' reverses, blocks n0 of the first, n1 of the second,
+// then the third's.
+template <typename T, int NV>
+__global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_vjp(const VjpArgs a0, const VjpArgs a1, const VjpArgs a2,
+                                                              int n0, int n1) {
+  __shared__ __attribute__((aligned(16))) T tile[vjp_rows<T, NV>() * (256 * NV + 4 / (int)sizeof(T))];
+  const int b = blockIdx.x;
+  if (b < n0) vjp_body<T, NV>(a0, b, tile);
+  else if (b < n0 + n1) vjp_body<T, NV>(a1, b - n0, tile);
+  else vjp_body<T, NV>(a2, b - n0 - n1, tile);
+}
+
+// Operand copies of fp32 [R x L] matrices, transposed or not: 32 x 32 tiles
+// through LDS so that both sides move whole rows; one block per (segment,
+// instance, tile) in a flat grid (segments in order).
+struct CopyArgs {
+  CopySeg seg[kMaxCopies];
+  int first[kMaxCopies + 1];   // first block of each segment
+  int n, BH;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_copies(const CopyArgs a) {
   __shared__ float tile[32][33];
+  int si = 0;
+  while (si + 1 < a.n && (int)blockIdx.x >= a.first[si + 1]) ++si;
+  const CopySeg& g = a.seg[si];
+  const int tr = (g.R + 31) / 32, tl = (g.L + 31) / 32;
+  const int64_t b = blockIdx.x - a.first[si];
   const int64_t per = (int64_t)tr * tl;
-  const int64_t inst = blockIdx.x / per;
-  const int rest = (int)(blockIdx.x - inst * per);
-  const float* src = W + inst * w_inst;
-  T* out = dst + inst * d_inst;
+  const int64_t inst = b / per;
+  const int rest = (int)(b - inst * per);
+  const float* src = g.W + inst * g.w_inst;
+  T* out = reinterpret_cast<T*>(g.dst) + inst * g.dst_inst;
   const int r0 = (rest / tl) * 32, c0 = (rest % tl) * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
   for (int k = ty; k < 32; k += 8) {
     const int r = r0 + k, c = c0 + tx;
-    tile[k][tx] = (r < R && c < L) ? src[(int64_t)r * L + c] : 0.0f;
+    tile[k][tx] = (r < g.R && c < g.L) ? src[(int64_t)r * g.L + c] : 0.0f;
   }
-  if constexpr (!TRANS) {
+  if (!g.trans) {   // uniform over the block
     for (int k = ty; k < 32; k += 8) {
       const int r = r0 + k, c = c0 + tx;
-      if (r < R && c < L) out[(int64_t)r * ld + c] = (T)tile[k][tx];
+      if (r < g.R && c < g.L) out[(int64_t)r * g.ld + c] = (T)tile[k][tx];
     }
     return;
   }
   __syncthreads();
   for (int k = ty; k < 32; k += 8) {
     const int c = c0 + k, r = r0 + tx;   // output row = input column
-    if (r < R && c < L) out[(int64_t)c * ld + r] = (T)tile[tx][k];
+    if (r < g.R && c < g.L) out[(int64_t)c * g.ld + r] = (T)tile[tx][k];
   }
 }
 
@@ -2742,15 +2764,22 @@ hipError_t launch_prep(const float* const W[3], void* const Wb[3], int BH, int d
 
 // Backward steps between the OUT / GRAD contractions (io_bf16 selects bf16
 // operand copies, else fp32).
-hipError_t launch_vjp(const VjpArgs& a, bool io_bf16, hipStream_t s) {
-  if ((int64_t)a.BH * a.R <= 0) return hipSuccess;
-  const int per_lane = (a.L / 4 + 63) / 64;
+hipError_t launch_vjp(const VjpArgs* a, int n, bool io_bf16, hipStream_t s) {
+  if (n < 1 || n > 3) return hipErrorInvalidValue;
+  int Lmax = 0;
+  for (int i = 0; i < n; ++i) Lmax = a[i].L > Lmax ? a[i].L : Lmax;
+  const int per_lane = (Lmax / 4 + 63) / 64;
+  const VjpArgs none{};
   auto go = [&](auto tag, auto nvc) {
     using T = decltype(tag);
     constexpr int NV = decltype(nvc)::value;
     constexpr int RR = vjp_rows<T, NV>();
-    const unsigned blocks = (unsigned)((int64_t)a.BH * ((a.R + RR - 1) / RR));   // <= 2^20 * 1024
-    k_vjp<T, NV><<<blocks, 64 * vjp_waves<NV>(), 0, s>>>(a);
+    int nb[3] = {0, 0, 0};
+    for (int i = 0; i < n; ++i) nb[i] = a[i].BH * ((a[i].R + RR - 1) / RR);   // <= 2^20 * 1024 each
+    const int64_t blocks = (int64_t)nb[0] + nb[1] + nb[2];
+    if (blocks <= 0) return;
+    k_vjp<T, NV><<<(unsigned)blocks, 64 * vjp_waves<NV>(), 0, s>>>(a[0], n > 1 ? a[1] : none, n > 2 ? a[2] : none,
+                                                                   nb[0], nb[1]);
   };
   auto pick = [&](auto tag) {
     if (per_lane <= 1) go(tag, std::integral_constant<int, 1>{});
@@ -2764,21 +2793,23 @@ hipError_t launch_vjp(const VjpArgs& a, bool io_bf16, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_copy_w(const float* W, int64_t w_inst, void* dst, int64_t ld, int64_t dst_inst, int BH, int R, int L,
-                         bool trans, bool io_bf16, hipStream_t s) {
-  if (BH <= 0 || R <= 0 || L <= 0) return hipSuccess;
-  const int tr = (R + 31) / 32, tl = (L + 31) / 32;
-  // callers keep BH * tiles under 2^31 (one set of weights: under 2^28 by the descriptor check)
-  const unsigned blocks = (unsigned)((int64_t)BH * tr * tl);
-  if (io_bf16) {
-    __bf16* o = reinterpret_cast<__bf16*>(dst);
-    if (trans) k_copy_w<__bf16, true><<<blocks, 256, 0, s>>>(W, w_inst, o, ld, dst_inst, R, L, tr, tl);
-    else k_copy_w<__bf16, false><<<blocks, 256, 0, s>>>(W, w_inst, o, ld, dst_inst, R, L, tr, tl);
-  } else {
-    float* o = reinterpret_cast<float*>(dst);
-    if (trans) k_copy_w<float, true><<<blocks, 256, 0, s>>>(W, w_inst, o, ld, dst_inst, R, L, tr, tl);
-    else k_copy_w<float, false><<<blocks, 256, 0, s>>>(W, w_inst, o, ld, dst_inst, R, L, tr, tl);
+hipError_t launch_copies(const CopySeg* c, int n, int BH, bool io_bf16, hipStream_t s) {
+  if (n < 0 || n > kMaxCopies) return hipErrorInvalidValue;
+  CopyArgs a{};
+  a.n = n;
+  a.BH = BH;
+  int64_t total = 0;
+  for (int i = 0; i < n; ++i) {
+    a.seg[i] = c[i];
+    a.first[i] = (int)total;
+    total += (int64_t)BH * ((c[i].R + 31) / 32) * ((c[i].L + 31) / 32);
   }
+  // callers keep the sum under 2^31 (one set of weights: under 2^28 each by the descriptor check)
+  if (total <= 0) return hipSuccess;
+  if (total >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  a.first[n] = (int)total;
+  if (io_bf16) k_copies<__bf16><<<(unsigned)total, 256, 0, s>>>(a);
+  else k_copies<float><<<(unsigned)total, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 

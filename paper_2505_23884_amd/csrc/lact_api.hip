@@ -1273,7 +1273,7 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
   }
   // transposed operand copies of W_0 .. W_nch (W_1 .. W_nch are contiguous)
   {
-    const CopySeg cs{W0, dd, wt(0), d, dd, p.d, p.d, 1};
+    const CopySeg cs{W0, dd, p.d, p.d, nullptr, 0, 0, wt(0), d, dd};
     rc = timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_copies(&cs, 1, p.BH, p.bf16, s); });
   }
   if (rc) return rc;
@@ -1281,7 +1281,7 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     const int64_t t = cdiv(d, 32), per = std::max<int64_t>(1, ((int64_t)1 << 30) / (BH * t * t));
     for (int64_t c0 = 1; c0 <= L.nch; c0 += per) {   // whole sets of BH matrices, under 2^30 blocks
       const int64_t m = std::min(per, L.nch + 1 - c0);
-      const CopySeg cs{traj(c0), dd, wt(c0), d, dd, p.d, p.d, 1};
+      const CopySeg cs{traj(c0), dd, p.d, p.d, nullptr, 0, 0, wt(c0), d, dd};
       rc = timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_copies(&cs, 1, (int)(m * BH), p.bf16, s); });
       if (rc) return rc;
     }
@@ -1587,13 +1587,11 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     const float* W1 = traj(i, 0);
     const float* W2 = traj(i, 1);
     const float* W3 = traj(i, 2);
-    const CopySeg cs[6] = {{W1, dh, ws + u[0], d, dh, (int)h, (int)d, 0},
-                           {W3, dh, ws + u[1], d, dh, (int)h, (int)d, 0},
-                           {W2, dh, ws + u[2], d, dh, (int)d, (int)h, 1},
-                           {W1, dh, bt, bt_ld, d * bt_ld, (int)h, (int)d, 1},
-                           {W3, dh, bt + h * esz, bt_ld, d * bt_ld, (int)h, (int)d, 1},
-                           {W2, dh, b2, 2 * h, d * 2 * h, (int)d, (int)h, 0}};
-    return timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_copies(cs, b2 ? 6 : 5, p.BH, p.bf16, s); });
+    // each matrix read once, both of its copies written from the same tile
+    const CopySeg cs[3] = {{W1, dh, (int)h, (int)d, ws + u[0], d, dh, bt, bt_ld, d * bt_ld},
+                           {W3, dh, (int)h, (int)d, ws + u[1], d, dh, bt + h * esz, bt_ld, d * bt_ld},
+                           {W2, dh, (int)d, (int)h, b2, 2 * h, d * 2 * h, ws + u[2], d, dh}};
+    return timed(LACT_KCLASS_PREP, 0.0, s, [&] { return launch_copies(cs, 3, p.BH, p.bf16, s); });
   };
   int a_ns = 0, b_ns = 0;
   // the apply's reverse on query rows [a, a + n) up to its weight cotangents

@@ -312,13 +312,15 @@ struct VjpArgs {
 
 // Up to three matrices' reverses in one launch (rows of the longest up to 4096).
 hipError_t launch_vjp(const VjpArgs* a, int n, bool io_bf16, hipStream_t s);
-// Operand copies of fp32 [R x L] matrices (w_inst apart): dst = W
-// (dst[r * ld + c]) or W^T (dst[c * ld + r]) in the operand type, dst_inst
-// apart; up to kMaxCopies in one launch.
+// Operand copies of fp32 [R x L] matrices (w_inst apart) in the operand
+// type: dst = W (dst[r * ld + c], dst_inst apart) and/or dstT = W^T
+// (dstT[c * ldT + r], dstT_inst apart), either one may be nullptr; up to
+// kMaxCopies matrices in one launch.
 struct CopySeg {
   const float* W; int64_t w_inst;
+  int R, L;
   void* dst; int64_t ld, dst_inst;
-  int R, L, trans;
+  void* dstT; int64_t ldT, dstT_inst;
 };
 constexpr int kMaxCopies = 8;
 hipError_t launch_copies(const CopySeg* c, int n, int BH, bool io_bf16, hipStream_t s);

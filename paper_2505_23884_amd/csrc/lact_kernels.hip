@@ -2394,45 +2394,71 @@ __global__ __launch_bounds__(64 * vjp_waves<NV>()) void k_vjp(const VjpArgs a0, 
   else vjp_body<T, NV>(a2, b - n0 - n1, tile);
 }
 
-// Operand copies of fp32 [R x L] matrices, transposed or not: 32 x 32 tiles
-// through LDS so that both sides move whole rows; one block per (segment,
-// instance, tile) in a flat grid (segments in order).
+// Operand copies of fp32 [R x L] matrices, row-major and/or transposed: one
+// 64 x 64 tile per block (segments in order, then instances, then tiles),
+// read once as float4 rows into LDS and written as runs of four elements
+// along the rows of each copy.
 struct CopyArgs {
   CopySeg seg[kMaxCopies];
   int first[kMaxCopies + 1];   // first block of each segment
-  int n, BH;
+  int n;
 };
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_copies(const CopyArgs a) {
-  __shared__ float tile[32][33];
+  __shared__ float tile[64][65];
   int si = 0;
   while (si + 1 < a.n && (int)blockIdx.x >= a.first[si + 1]) ++si;
   const CopySeg& g = a.seg[si];
-  const int tr = (g.R + 31) / 32, tl = (g.L + 31) / 32;
+  const int tr = (g.R + 63) / 64, tl = (g.L + 63) / 64;
   const int64_t b = blockIdx.x - a.first[si];
   const int64_t per = (int64_t)tr * tl;
   const int64_t inst = b / per;
   const int rest = (int)(b - inst * per);
+  const int r0 = (rest / tl) * 64, c0 = (rest % tl) * 64;
   const float* src = g.W + inst * g.w_inst;
-  T* out = reinterpret_cast<T*>(g.dst) + inst * g.dst_inst;
-  const int r0 = (rest / tl) * 32, c0 = (rest % tl) * 32;
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  for (int k = ty; k < 32; k += 8) {
-    const int r = r0 + k, c = c0 + tx;
-    tile[k][tx] = (r < g.R && c < g.L) ? src[(int64_t)r * g.L + c] : 0.0f;
-  }
-  if (!g.trans) {   // uniform over the block
-    for (int k = ty; k < 32; k += 8) {
-      const int r = r0 + k, c = c0 + tx;
-      if (r < g.R && c < g.L) out[(int64_t)r * g.ld + c] = (T)tile[k][tx];
+  const int t = threadIdx.x, q = (t & 15) * 4;
+  for (int k = t >> 4; k < 64; k += 16) {   // row k of the tile, columns q .. q + 3
+    const int r = r0 + k, c = c0 + q;
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < g.R && c + 3 < g.L) {
+      x = *reinterpret_cast<const float4*>(src + (int64_t)r * g.L + c);
+    } else if (r < g.R) {
+      float e[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < 4 && c + j < g.L; ++j) e[j] = src[(int64_t)r * g.L + c + j];
+      x = make_float4(e[0], e[1], e[2], e[3]);
     }
-    return;
+    tile[k][q] = x.x;
+    tile[k][q + 1] = x.y;
+    tile[k][q + 2] = x.z;
+    tile[k][q + 3] = x.w;
   }
   __syncthreads();
-  for (int k = ty; k < 32; k += 8) {
-    const int c = c0 + k, r = r0 + tx;   // output row = input column
-    if (r < g.R && c < g.L) out[(int64_t)c * g.ld + r] = (T)tile[tx][k];
+  if (g.dst) {   // uniform over the block
+    T* out = reinterpret_cast<T*>(g.dst) + inst * g.dst_inst;
+    for (int k = t >> 4; k < 64; k += 16) {
+      const int r = r0 + k, c = c0 + q;
+      if (r >= g.R) continue;
+      const int64_t o = (int64_t)r * g.ld + c;
+      if (c + 3 < g.L && (o & 3) == 0) {
+        st4<T>(out, o, tile[k][q], tile[k][q + 1], tile[k][q + 2], tile[k][q + 3]);
+      } else {
+        for (int j = 0; j < 4 && c + j < g.L; ++j) out[o + j] = (T)tile[k][q + j];
+      }
+    }
+  }
+  if (g.dstT) {
+    T* out = reinterpret_cast<T*>(g.dstT) + inst * g.dstT_inst;
+    for (int k = t >> 4; k < 64; k += 16) {   // output row = input column c0 + k, elements r0 + q .. + 3
+      const int c = c0 + k, r = r0 + q;
+      if (c >= g.L) continue;
+      const int64_t o = (int64_t)c * g.ldT + r;
+      if (r + 3 < g.R && (o & 3) == 0) {
+        st4<T>(out, o, tile[q][k], tile[q + 1][k], tile[q + 2][k], tile[q + 3][k]);
+      } else {
+        for (int j = 0; j < 4 && r + j < g.R; ++j) out[o + j] = (T)tile[q + j][k];
+      }
+    }
   }
 }
 
@@ -2797,12 +2823,11 @@ hipError_t launch_copies(const CopySeg* c, int n, int BH, bool io_bf16, hipStrea
   if (n < 0 || n > kMaxCopies) return hipErrorInvalidValue;
   CopyArgs a{};
   a.n = n;
-  a.BH = BH;
   int64_t total = 0;
   for (int i = 0; i < n; ++i) {
     a.seg[i] = c[i];
     a.first[i] = (int)total;
-    total += (int64_t)BH * ((c[i].R + 31) / 32) * ((c[i].L + 31) / 32);
+    total += (int64_t)BH * ((c[i].R + 63) / 64) * ((c[i].L + 63) / 64);
   }
   // callers keep the sum under 2^31 (one set of weights: under 2^28 each by the descriptor check)
   if (total <= 0) return hipSuccess;

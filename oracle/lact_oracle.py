@@ -39,7 +39,9 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
                    cotangents in and out (W0 = (W1, W2, W3)); the chunk
                    gradient depends on W, so its reverse carries the second
                    derivative of SiLU (reverse mode written out by hand,
-                   step by step against the forward's closed form)
+                   step by step against the forward's closed form); with
+                   Muon, the reverse of every Newton-Schulz step between
+                   the gradient and the update (both fast weights)
 * schedule         a list of (mode, begin, end) segments, each one of
                    update-then-apply, apply-then-update, update-only or
                    apply-only on its token range (the ttt_config loop of Alg. 1;
@@ -99,7 +101,7 @@ __all__ = [
     "lact_forward_linear_instance", "lact_forward_linear", "linear_flops", "layer_flops",
     "weight_update_vjp", "lact_backward_linear_instance", "lact_backward_linear",
     "silu_second_derivative", "swiglu_apply_vjp", "chunk_gradient_vjp", "lact_backward_instance",
-    "lact_backward",
+    "lact_backward", "newton_schulz_vjp",
 ]
 
 # Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
@@ -417,8 +419,42 @@ def weight_update_vjp(W, step, dWn):
     return dU + (a / (u * n)) * W, -dU
 
 
-def lact_backward_linear_instance(q, k, v, eta, W0, do, chunk: int, order: int, dW_final=None):
-    """Reverse of lact_forward_linear_instance (no Muon, no momentum): given the
+def newton_schulz_vjp(G, dX, steps: int = NS_STEPS_DEFAULT, coeffs=NS_COEFFS, eps: float = NS_EPS):
+    """Reverse of newton_schulz: from the cotangent dX of its result, the
+    cotangent of G. The iterates are replayed in the wide orientation; one
+    step X' = a X + B X with B = b A + c A A and A = X X^T (A and B
+    symmetric) goes back as
+        dB = dX' X^T,  dA = b dB + c (dB A + A dB),
+        dX = a dX' + B dX' + (dA + dA^T) X,
+    and the scaling X_0 = G / (s + eps), s = ||G||_F, as
+        dG = dX_0 / (s + eps) - <dX_0, G> G / ((s + eps)^2 s).
+    """
+    a, b, c = coeffs
+    G = np.asarray(G, dtype=np.float64)
+    dX = np.asarray(dX, dtype=np.float64)
+    transposed = G.shape[0] > G.shape[1]
+    if transposed:
+        G, dX = G.T, dX.T
+    s = np.linalg.norm(G)
+    X = G / (s + eps)
+    Xs = []
+    for _ in range(steps):
+        Xs.append(X)
+        A = X @ X.T
+        X = a * X + (b * A + c * (A @ A)) @ X
+    for X in reversed(Xs):
+        A = X @ X.T
+        Bm = b * A + c * (A @ A)
+        dB = dX @ X.T
+        dA = b * dB + c * (dB @ A + A @ dB)
+        dX = a * dX + Bm.T @ dX + (dA + dA.T) @ X
+    dG = dX / (s + eps) - (np.sum(dX * G) / ((s + eps) ** 2 * s)) * G
+    return dG.T if transposed else dG
+
+
+def lact_backward_linear_instance(q, k, v, eta, W0, do, chunk: int, order: int, dW_final=None,
+                                  use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT):
+    """Reverse of lact_forward_linear_instance (no momentum; Muon optional): given the
     cotangent ``do`` [n_q, d] of the outputs and optionally ``dW_final`` of the
     returned fast weight, the cotangents (dq, dk, dv, deta, dW0) of the inputs.
 
@@ -428,16 +464,19 @@ def lact_backward_linear_instance(q, k, v, eta, W0, do, chunk: int, order: int, 
     k_t^T, with dg its cotangent (weight_update_vjp), gives
         dv_t = -eta_t dg k_t,  dk_t = -eta_t dg^T v_t,  deta_t = -v_t^T dg k_t.
     Apply-then-update applies the weights entering the chunk, update-then-apply
-    those leaving it; the tail is applied with the final weights.
+    those leaving it; the tail is applied with the final weights. With Muon
+    the update's step is newton_schulz(g) and its cotangent goes back through
+    newton_schulz_vjp before it reaches g.
     """
     q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
     eta = np.asarray(eta, dtype=np.float64)
     do = np.asarray(do, dtype=np.float64)
     n_q, n_kv = q.shape[0], k.shape[0]
+    step_of = (lambda g: newton_schulz(g, ns_steps)) if use_muon else (lambda g: g)
     Ws = [np.asarray(W0, dtype=np.float64).copy()]
     for s in range(0, n_kv, chunk):
         e = min(n_kv, s + chunk)
-        Ws.append(weight_update(Ws[-1], linear_gradient(Ws[-1], k[s:e], v[s:e], eta[s:e])))
+        Ws.append(weight_update(Ws[-1], step_of(linear_gradient(Ws[-1], k[s:e], v[s:e], eta[s:e]))))
     dW = np.zeros_like(Ws[0]) if dW_final is None else np.asarray(dW_final, dtype=np.float64).copy()
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
     deta = np.zeros(n_kv)
@@ -451,7 +490,9 @@ def lact_backward_linear_instance(q, k, v, eta, W0, do, chunk: int, order: int, 
             dW += do[s:e].T @ q[s:e]
             dq[s:e] = do[s:e] @ Ws[c + 1]
         g = linear_gradient(Ws[c], k[s:e], v[s:e], eta[s:e])
-        dW, dg = weight_update_vjp(Ws[c], g, dW)
+        dW, dg = weight_update_vjp(Ws[c], step_of(g), dW)
+        if use_muon:
+            dg = newton_schulz_vjp(g, dg, ns_steps)
         kg = k[s:e] @ dg.T                  # rows dg k_t
         dv[s:e] = -eta[s:e, None] * kg
         dk[s:e] = -eta[s:e, None] * (v[s:e] @ dg)
@@ -462,12 +503,14 @@ def lact_backward_linear_instance(q, k, v, eta, W0, do, chunk: int, order: int, 
     return dq, dk, dv, deta, dW
 
 
-def lact_backward_linear(q, k, v, eta, W0, do, chunk: int, order: int, dW_final=None, instances=None):
+def lact_backward_linear(q, k, v, eta, W0, do, chunk: int, order: int, dW_final=None, instances=None,
+                         use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT):
     """Batched driver of lact_backward_linear_instance: (dq, dk, dv, deta, dW0)
     stacked over the selected instances."""
     idx = range(q.shape[0]) if instances is None else instances
     res = [lact_backward_linear_instance(q[i], k[i], v[i], eta[i], W0[i], do[i], chunk, order,
-                                         None if dW_final is None else dW_final[i]) for i in idx]
+                                         None if dW_final is None else dW_final[i], use_muon, ns_steps)
+           for i in idx]
     return tuple(np.stack(col) for col in zip(*res))
 
 
@@ -543,9 +586,10 @@ def chunk_gradient_vjp(W1, W2, W3, K, V, eta, G1, G2, G3):
     return dZ1.T @ K, V.T @ dC, dZ3.T @ K, dK, dV, deta
 
 
-def lact_backward_instance(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final=None):
-    """Reverse of lact_forward_instance for the SwiGLU fast weight (no Muon,
-    no momentum, one rate per token): given the cotangent ``do`` [n_q, d] of
+def lact_backward_instance(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final=None,
+                           use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT):
+    """Reverse of lact_forward_instance for the SwiGLU fast weight (Muon
+    optional, no momentum, one rate per token): given the cotangent ``do`` [n_q, d] of
     the outputs and optionally ``dW_final`` = (dW1, dW2, dW3) of the returned
     fast weights, the cotangents (dq, dk, dv, deta, (dW1, dW2, dW3)) of the
     inputs, the last three those of the initial fast weights.
@@ -556,19 +600,22 @@ def lact_backward_instance(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int,
     minus that of U) and then through chunk_gradient_vjp (g depends on W, k,
     v and eta); its apply goes back through swiglu_apply_vjp with the weights
     it used (entering the chunk with apply-then-update, leaving it with
-    update-then-apply; the tail uses the final weights).
+    update-then-apply; the tail uses the final weights). With Muon the
+    update's steps are newton_schulz(g_j), and their cotangents go back
+    through newton_schulz_vjp before they reach the gradients.
     """
     q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
     eta = np.asarray(eta, dtype=np.float64)
     do = np.asarray(do, dtype=np.float64)
     n_q, n_kv = q.shape[0], k.shape[0]
+    step_of = (lambda g: newton_schulz(g, ns_steps)) if use_muon else (lambda g: g)
     Ws = [tuple(np.asarray(w, dtype=np.float64).copy() for w in (W1, W2, W3))]
     gs = []
     for s in range(0, n_kv, chunk):
         e = min(n_kv, s + chunk)
         g = chunk_gradient(*Ws[-1], k[s:e], v[s:e], eta[s:e])
         gs.append(g)
-        Ws.append(tuple(weight_update(w, gj) for w, gj in zip(Ws[-1], g)))
+        Ws.append(tuple(weight_update(w, step_of(gj)) for w, gj in zip(Ws[-1], g)))
     dW = [np.zeros_like(w) for w in Ws[0]] if dW_final is None else [
         np.asarray(w, dtype=np.float64).copy() for w in dW_final]
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
@@ -589,8 +636,8 @@ def lact_backward_instance(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int,
             apply_back(Ws[c + 1], s, e)
         dg = []
         for j in range(3):
-            dW[j], dgj = weight_update_vjp(Ws[c][j], gs[c][j], dW[j])
-            dg.append(dgj)
+            dW[j], dgj = weight_update_vjp(Ws[c][j], step_of(gs[c][j]), dW[j])
+            dg.append(newton_schulz_vjp(gs[c][j], dgj, ns_steps) if use_muon else dgj)
         b1, b2, b3, dkc, dvc, detac = chunk_gradient_vjp(*Ws[c], k[s:e], v[s:e], eta[s:e], *dg)
         dW[0] += b1
         dW[1] += b2
@@ -601,7 +648,8 @@ def lact_backward_instance(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int,
     return dq, dk, dv, deta, tuple(dW)
 
 
-def lact_backward(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final=None, instances=None):
+def lact_backward(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final=None, instances=None,
+                  use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT):
     """Batched driver of lact_backward_instance: (dq, dk, dv, deta, dW1, dW2,
     dW3) stacked over the selected instances; dW_final is None or a triple
     of [BH, ...] arrays."""
@@ -610,7 +658,7 @@ def lact_backward(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final
     for i in idx:
         dq, dk, dv, deta, dW = lact_backward_instance(
             q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], do[i], chunk, order,
-            None if dW_final is None else tuple(w[i] for w in dW_final))
+            None if dW_final is None else tuple(w[i] for w in dW_final), use_muon, ns_steps)
         res.append((dq, dk, dv, deta, *dW))
     return tuple(np.stack(col) for col in zip(*res))
 

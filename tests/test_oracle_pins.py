@@ -1073,3 +1073,115 @@ def test_swiglu_backward_batched_driver_stacks_instances():
         dq, dk, dv, deta, dW = O.lact_backward_instance(q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], do[i], C, 1)
         for a, b in zip(got, (dq, dk, dv, deta, *dW)):
             assert np.array_equal(a[pos], b)
+
+
+# ----------------------------------------------------------------------------- Muon backward
+
+
+def _torch_newton_schulz(G, steps=5):
+    """Muon's quintic iteration in torch (wide orientation, G / (||G|| + 1e-7))."""
+    a, b, c = 3.4445, -4.7750, 2.0315
+    tall = G.shape[0] > G.shape[1]
+    X = G.T if tall else G
+    X = X / (torch.linalg.matrix_norm(X) + 1e-7)
+    for _ in range(steps):
+        A = X @ X.T
+        X = a * X + (b * A + c * A @ A) @ X
+    return X.T if tall else X
+
+
+@pytest.mark.parametrize("shape", [(6, 9), (9, 6), (7, 7)])
+def test_newton_schulz_vjp_matches_autograd(shape):
+    rng = _rng(121 + shape[0])
+    G, dX = rng.standard_normal(shape), rng.standard_normal(shape)
+    Gt = torch.tensor(G, requires_grad=True)
+    (_torch_newton_schulz(Gt) * torch.tensor(dX)).sum().backward()
+    assert np.allclose(O.newton_schulz(G), _torch_newton_schulz(torch.tensor(G)).numpy(), rtol=1e-12, atol=1e-13)
+    assert np.allclose(O.newton_schulz_vjp(G, dX), Gt.grad.numpy(), rtol=1e-9, atol=1e-11)
+
+
+def test_newton_schulz_vjp_finite_differences():
+    rng = _rng(124)
+    G, dX = rng.standard_normal((5, 8)), rng.standard_normal((5, 8))
+    got = O.newton_schulz_vjp(G, dX)
+    for idx in ((0, 0), (2, 5), (4, 7), (3, 1)):
+        eps = 1e-6
+        P, M = G.copy(), G.copy()
+        P[idx] += eps
+        M[idx] -= eps
+        fd = (np.sum(O.newton_schulz(P) * dX) - np.sum(O.newton_schulz(M) * dX)) / (2 * eps)
+        assert abs(fd - got[idx]) <= 1e-6 * max(1.0, abs(fd))
+
+
+def _torch_swiglu_layer_muon(q, k, v, eta, W, chunk, order):
+    n_q, n_kv = q.shape[0], k.shape[0]
+    outs = []
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        if order == 0:
+            outs.append(_torch_swiglu_t(*W, q[s:e]))
+        g = _torch_chunk_gradient(*W, k[s:e], v[s:e], eta[s:e])
+        new = []
+        for w, gj in zip(W, g):
+            U = w - _torch_newton_schulz(gj)
+            new.append(U * (torch.linalg.vector_norm(w, dim=1, keepdim=True)
+                            / torch.linalg.vector_norm(U, dim=1, keepdim=True)))
+        W = tuple(new)
+        if order == 1:
+            outs.append(_torch_swiglu_t(*W, q[s:e]))
+    if n_q > n_kv:
+        outs.append(_torch_swiglu_t(*W, q[n_kv:]))
+    return torch.cat(outs), W
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_muon_backward_matches_autograd(order):
+    # three chunks (the last ragged), a tail, h != d (W1, W3 tall, W2 wide)
+    rng = _rng(125 + order)
+    d, h, n_kv, n_q, C = 5, 7, 15, 19, 6
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random(n_kv)
+    W0 = _weights(rng, h, d, unit=True)
+    do = rng.standard_normal((n_q, d))
+    dWf = tuple(rng.standard_normal(w.shape) for w in W0)
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    qt, kt, vt, et = t(q), t(k), t(v), t(eta)
+    Wt = tuple(t(w) for w in W0)
+    o, Wfin = _torch_swiglu_layer_muon(qt, kt, vt, et, Wt, C, order)
+    loss = (o * torch.tensor(do)).sum() + sum((w * torch.tensor(x)).sum() for w, x in zip(Wfin, dWf))
+    loss.backward()
+    dq, dk, dv, deta, dW = O.lact_backward_instance(q, k, v, eta, *W0, do, C, order, dWf, use_muon=True)
+    for name, g, ref in zip(("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3"), (dq, dk, dv, deta, *dW),
+                            (qt, kt, vt, et, *Wt)):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-8, atol=1e-10), name
+    o_ref, W_ref = O.lact_forward_instance(q, k, v, eta, *W0, C, order, use_muon=True)
+    assert np.allclose(o.detach().numpy(), o_ref, rtol=1e-11, atol=1e-12)
+
+
+def test_linear_muon_backward_matches_autograd():
+    rng = _rng(127)
+    d, n_kv, n_q, C = 6, 17, 20, 6
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random(n_kv)
+    W0 = rng.standard_normal((d, d))
+    do, dWf = rng.standard_normal((n_q, d)), rng.standard_normal((d, d))
+    for order in (0, 1):
+        t = lambda a: torch.tensor(a, requires_grad=True)
+        qt, kt, vt, et, Wt = t(q), t(k), t(v), t(eta), t(W0)
+        W = Wt
+        outs = []
+        for s in range(0, n_kv, C):
+            e = min(n_kv, s + C)
+            if order == 0:
+                outs.append(qt[s:e] @ W.T)
+            g = -(vt[s:e] * et[s:e, None]).T @ kt[s:e]
+            U = W - _torch_newton_schulz(g)
+            W = U * (torch.linalg.vector_norm(W, dim=1, keepdim=True) / torch.linalg.vector_norm(U, dim=1, keepdim=True))
+            if order == 1:
+                outs.append(qt[s:e] @ W.T)
+        outs.append(qt[n_kv:] @ W.T)
+        loss = (torch.cat(outs) * torch.tensor(do)).sum() + (W * torch.tensor(dWf)).sum()
+        loss.backward()
+        got = O.lact_backward_linear_instance(q, k, v, eta, W0, do, C, order, dWf, use_muon=True)
+        for name, g, ref in zip(("dq", "dk", "dv", "deta", "dW0"), got, (qt, kt, vt, et, Wt)):
+            assert np.allclose(g, ref.grad.numpy(), rtol=1e-8, atol=1e-10), (order, name)

@@ -272,11 +272,18 @@ def backward_flops(cfg, BH=None):
     cotangents: 24 d h per key token) and the apply's (Q W1^T, Q W3^T, dO W2,
     dq over 2h and three weight cotangents: 16 d h per query token). Products
     that the implementation evaluates a second time instead of keeping them
-    (K W1^T, K W3^T, V W2 in the reverse) are not counted."""
+    (K W1^T, K W3^T, V W2 in the reverse) are not counted. With Muon, per
+    chunk and matrix: the replayed iteration (App. A: 4 m^2 n + 2 m^3 per
+    step, m <= n its sides) and its reverse (dX' X^T, B dX', M X and S A:
+    6 m^2 n + 2 m^3 per step); the second replay that the reverse makes to
+    recover the iterates is not counted."""
     BH = cfg.BH if BH is None else BH
+    nmat = 1 if cfg.linear else 3
+    m, n = float(min(cfg.d, cfg.h)), float(max(cfg.d, cfg.h))
+    ns = cfg.n_chunks * nmat * cfg.ns_steps * (10.0 * m * m * n + 4.0 * m ** 3) if cfg.use_muon else 0.0
     if cfg.linear:
-        return BH * float(cfg.d) * cfg.d * (6.0 * cfg.n_kv + 4.0 * cfg.n_q)
-    return BH * float(cfg.d) * cfg.h * (36.0 * cfg.n_kv + 16.0 * cfg.n_q)
+        return BH * (float(cfg.d) * cfg.d * (6.0 * cfg.n_kv + 4.0 * cfg.n_q) + ns)
+    return BH * (float(cfg.d) * cfg.h * (36.0 * cfg.n_kv + 16.0 * cfg.n_q) + ns)
 
 
 def describe(cfg):
@@ -340,10 +347,12 @@ def _oracle_sample(cfg, min_seconds, backward=False):
         t0 = time.perf_counter()
         if backward and scfg.linear:
             O.lact_backward_linear_instance(x["q"][0], x["k"][0], x["v"][0], x["eta"][0], x["W1"][0], ct["do"][0],
-                                            scfg.chunk, scfg.order)
+                                            scfg.chunk, scfg.order, use_muon=bool(scfg.use_muon),
+                                            ns_steps=scfg.ns_steps)
         elif backward:
             O.lact_backward_instance(x["q"][0], x["k"][0], x["v"][0], x["eta"][0], x["W1"][0], x["W2"][0],
-                                     x["W3"][0], ct["do"][0], scfg.chunk, scfg.order)
+                                     x["W3"][0], ct["do"][0], scfg.chunk, scfg.order, use_muon=bool(scfg.use_muon),
+                                     ns_steps=scfg.ns_steps)
         elif scfg.linear:
             O.lact_forward_linear(x["q"], x["k"], x["v"], x["eta"], x["W1"], scfg.chunk, scfg.order,
                                   bool(scfg.use_muon), scfg.ns_steps)
@@ -501,8 +510,9 @@ def measure(cfg, args, P, on_device=False):
 
     if args.backward:
         from lact_synth import make_cotangents
-        if cfg.use_muon or cfg.momentum or cfg.lr3 or cfg.schedule or cfg.layer_io or on_device:
-            raise SystemExit("--backward runs without Muon, momentum, per-matrix rates or a schedule, host-drawn inputs")
+        if cfg.momentum or cfg.lr3 or cfg.schedule or cfg.layer_io or on_device or (cfg.use_muon and cfg.io != "bf16"):
+            raise SystemExit("--backward runs without momentum, per-matrix rates or a schedule (Muon with bf16 I/O), "
+                             "host-drawn inputs")
         ct = make_cotangents(cfg, 0)
         dout = torch.from_numpy(ct["do"].reshape(cfg.B, cfg.H, cfg.n_q, cfg.d)).to(dev, io)
         del ct
@@ -513,11 +523,11 @@ def measure(cfg, args, P, on_device=False):
 
     def path():
         if args.backward and cfg.linear:
-            P.backward_linear(q, k, v, eta, W[0], dout, cfg.chunk, order=cfg.order, out=grads, workspace=ws,
-                              stream=launch_stream())
+            P.backward_linear(q, k, v, eta, W[0], dout, cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
+                              ns_steps=cfg.ns_steps, out=grads, workspace=ws, stream=launch_stream())
         elif args.backward:
-            P.backward(q, k, v, eta, *W, dout, cfg.chunk, order=cfg.order, out=grads, workspace=ws,
-                       stream=launch_stream())
+            P.backward(q, k, v, eta, *W, dout, cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
+                       ns_steps=cfg.ns_steps, out=grads, workspace=ws, stream=launch_stream())
         elif cfg.linear:
             P.forward_linear(q, k, v, eta, W[0], cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
                              ns_steps=cfg.ns_steps, out=out, workspace=ws, stream=launch_stream())
@@ -624,9 +634,9 @@ def measure(cfg, args, P, on_device=False):
 
 # The second workload that the performance target names, measured in the same
 # process after the default one: NVS with a million context tokens; then the
-# backward at the LM shape, with the SwiGLU and with the linear fast weight.
+# backward at the LM shape: SwiGLU without and with Muon, and the linear fast weight.
 SECONDARY = "nvs1m"
-SECONDARY_BWD = ("lm32k", "lm32k_linear")
+SECONDARY_BWD = ("lm32k", "lm32k_muon", "lm32k_linear")
 
 
 def main():

@@ -264,8 +264,10 @@ int lact_forward_schedule(const lact_desc* desc,
  * update-then-apply; the tail [n_kv, n_q) uses the final weight) and
  * gives dq_i = W^T dO_i.
  *
- * Requires desc->fast_weight == LACT_FW_LINEAR and use_muon == 0 (else
- * LACT_EUNSUPPORTED); other fields as lact_forward. The workspace size
+ * Requires desc->fast_weight == LACT_FW_LINEAR (else LACT_EUNSUPPORTED);
+ * with use_muon the update's step Muon(g) goes back through the reverse of
+ * every Newton-Schulz step (fp16 operands, fp32 iterates; bf16 I/O only,
+ * else LACT_EUNSUPPORTED); other fields as lact_forward. The workspace size
  * (lact_backward_workspace_bytes) covers both backward entry points: it
  * follows desc->fast_weight.
  *
@@ -297,8 +299,8 @@ int lact_backward_linear(const lact_desc* desc,
 /*
  * Backward of lact_forward for the SwiGLU fast weight (§3.1 loss, chunk
  * gradient and SwiGLU eqs.; §3.2 per-row norm-preserving update; Alg. 1),
- * without Muon or momentum and with one rate per token (else
- * LACT_EUNSUPPORTED). Given the cotangent dO of the outputs and optionally
+ * with or without Muon (App. A; with Muon bf16 I/O only) and with one rate
+ * per token (else LACT_EUNSUPPORTED); momentum is not differentiated. Given the cotangent dO of the outputs and optionally
  * those of the final fast weights, the cotangents of every input: the
  * reverse of the chunk loop, with the weights and negated gradients of every
  * chunk recomputed by the forward's own launches and kept in the workspace.
@@ -307,7 +309,12 @@ int lact_backward_linear(const lact_desc* desc,
  * depends on W1, W2, W3, k, v and eta (its reverse carries SiLU's second
  * derivative); the apply o = W2 [SiLU(W1 q) o (W3 q)] goes back with the
  * weights it used (entering the chunk with apply-then-update, leaving it
- * with update-then-apply; the tail with the final weights).
+ * with update-then-apply; the tail with the final weights). With Muon the
+ * steps Muon(g_j) go back through every Newton-Schulz step (the iteration is
+ * replayed per chunk; fp16 operands, fp32 iterates). Newton-Schulz
+ * multiplies the null space of a rank-deficient gradient (a chunk shorter
+ * than min(d, h)) by 3.4445 per step, and its reverse amplifies rounding
+ * there by the same factor.
  *
  *   q, k, v, eta          the forward's inputs (as lact_forward)                in
  *   W1, W2, W3            fp32 fast weights BEFORE the forward (not written)     in

@@ -283,8 +283,8 @@ def backward_workspace_bytes(desc: LactDesc) -> int:
     return int(n)
 
 
-def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, out=None,
-                    workspace=None, stream=None):
+def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, use_muon=False,
+                    ns_steps=5, out=None, workspace=None, stream=None):
     """Backward of forward_linear (lact_backward_linear): the cotangents of q,
     k, v, eta and of the initial fast weight W0 [.., d, d] (fp32, not written)
     given dout (q's shape and dtype) and, optionally, the cotangent of the
@@ -298,7 +298,7 @@ def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_f
         raise LactError(-1, "dout must have q's shape and dtype")
     if dW_final is not None and (dW_final.shape != W0.shape or dW_final.dtype != torch.float32):
         raise LactError(-1, "dW_final must have W0's shape, fp32")
-    desc, dq, _, stream = _marshal(q, k, v, eta, W0, W0, W0, extra[1:], chunk, order, False, 0,
+    desc, dq, _, stream = _marshal(q, k, v, eta, W0, W0, W0, extra[1:], chunk, order, use_muon, ns_steps,
                                    None if out is None else out[0], None, stream, FW_LINEAR, need_workspace=False)
     if not dout.is_cuda or not dout.is_contiguous():
         raise LactError(-1, "dout must be a contiguous device tensor")
@@ -322,10 +322,10 @@ def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_f
     return dq, dk, dv, deta, dW0
 
 
-def backward(q, k, v, eta, W1, W2, W3, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, out=None,
-             workspace=None, stream=None):
-    """Backward of forward() for the SwiGLU fast weight (lact_backward), no
-    Muon or momentum: the cotangents of q, k, v, eta and of the initial fast
+def backward(q, k, v, eta, W1, W2, W3, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, use_muon=False,
+             ns_steps=5, out=None, workspace=None, stream=None):
+    """Backward of forward() for the SwiGLU fast weight (lact_backward), with
+    or without Muon (bf16 I/O for Muon), no momentum: the cotangents of q, k, v, eta and of the initial fast
     weights W1, W2, W3 (fp32, not written) given dout (q's shape and dtype)
     and, optionally, dW_final = (dW1, dW2, dW3) of the final fast weights (any
     of them None). Returns (dq, dk, dv, deta, dW1, dW2, dW3), written into
@@ -338,7 +338,7 @@ def backward(q, k, v, eta, W1, W2, W3, dout, chunk, order=APPLY_THEN_UPDATE, dW_
     for t, ref in zip(dWf, (W1, W2, W3)):
         if t is not None and (t.shape != ref.shape or t.dtype != torch.float32):
             raise LactError(-1, "dW_final tensors must have the fast weights' shapes, fp32")
-    desc, dq, _, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, False, 0,
+    desc, dq, _, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps,
                                    None if out is None else out[0], None, stream, FW_SWIGLU, need_workspace=False)
     if not dout.is_cuda or not dout.is_contiguous():
         raise LactError(-1, "dout must be a contiguous device tensor")

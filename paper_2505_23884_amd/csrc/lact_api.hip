@@ -418,7 +418,7 @@ int newton_schulz(Ctx& c) {
   }
   if (!fused) {
     rc = timed(LACT_KCLASS_NS, 0.0, c.s,
-               [&] { return launch_ns_scale(pa, c.ws + p.off_yb[0], p.ns_fp16, 1e-7f, c.s); });
+               [&] { return launch_ns_scale(pa, c.ws + p.off_yb[0], p.ns_fp16, kNsEps, c.s); });
     if (rc) return rc;
   }
   // segment 0: W1 and W3 stored h x d; segment 1: W2 stored d x h
@@ -452,7 +452,7 @@ int newton_schulz(Ctx& c) {
       f.src = c.beta ? pa.Y32 : pa.part;
       f.nsplit = c.beta ? 1 : p.nsplit;
       f.part_split = pa.part_split;
-      f.eps = 1e-7f;
+      f.eps = kNsEps;
       // and the weight update (no separate update launch follows); with
       // output tiles in the launch, the copies go to the other set
       for (int j = 0; j < p.nmat; ++j) {
@@ -1082,6 +1082,244 @@ int run_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, 
   return LACT_OK;
 }
 
+// ---------------------------------------------------------------- backward of Newton-Schulz
+// Muon's step of a chunk (App. A, Details of Muon; §3.2) and its reverse, on
+// slots s = inst * nmat + j of wide [m x n] fp32 matrices (a stored matrix
+// with more rows than columns is transposed into its slot). The reverse
+// replays the iteration from the chunk's gradient, keeping the fp16 operand
+// copies of every iterate X_k, of A_k = X_k X_k^T and of B_k = b A_k + c A_k^2,
+// and then goes back one step at a time:
+//   dB = dX' X^T,  S = dB + dB^T,  M = b S + c (S A + (S A)^T)  (= dA + dA^T),
+//   dX = a dX' + B dX' + M X,
+// and through the scaling X_0 = G / (||G|| + eps). Products: the k_bwd kinds
+// with fp16 operands (OUT for sums along rows, GRAD2 for sums down columns,
+// fp32 partials), fp32 iterates.
+struct NsBwdLayout {
+  int S, m, n;
+  size_t g, x32, p1, p2, x16, a16, b16, t16, q16, s16, m16, db16, nrm, dot, pstep, ustep, ug, total;
+};
+
+size_t ns_bwd_layout(const Plan& p, int steps, size_t o, NsBwdLayout* N) {
+  N->S = p.BH * p.nmat;
+  N->m = std::min(p.d, p.h);
+  N->n = std::max(p.d, p.h);
+  const size_t mn = (size_t)N->m * N->n, mm = (size_t)N->m * N->m, S = N->S;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  N->g = take(S * mn * 4);
+  N->x32 = take(S * mn * 4);
+  N->p1 = take(S * mn * 4);
+  N->p2 = take(S * mn * 4);
+  N->x16 = take((size_t)std::max(steps, 1) * S * mn * 2);
+  N->a16 = take((size_t)std::max(steps, 1) * S * mm * 2);
+  N->b16 = take((size_t)std::max(steps, 1) * S * mm * 2);
+  N->t16 = take(S * mn * 2);
+  N->q16 = take(S * mm * 2);
+  N->s16 = take(S * mm * 2);
+  N->m16 = take(S * mm * 2);
+  N->db16 = take(S * mm * 2);
+  N->nrm = take(S * 4);
+  N->dot = take(S * 4);
+  N->pstep = take(S * mn * 4);   // stored layouts [inst][nmat][d h]
+  N->ustep = take(S * mn * 4);
+  N->ug = take(S * mn * 4);
+  N->total = o;
+  return o;
+}
+
+struct NsBwd {
+  const Plan& p;
+  const NsBwdLayout& N;
+  uint8_t* ws;
+  hipStream_t s;
+  int steps;
+  int R[3], L[3];   // stored shape of matrix j
+  template <class T>
+  T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+  int64_t mn() const { return (int64_t)N.m * N.n; }
+  int64_t mm() const { return (int64_t)N.m * N.m; }
+  bool tall(int j) const { return R[j] > L[j]; }
+
+  // stored [inst][nmat][R x L] (nsum splits `split` apart, times sign) <-> wide slots
+  int gather(const float* src, int nsum, int64_t split, float sign, float* wide) const {
+    CopySeg cs[3] = {};
+    const int64_t dh = (int64_t)p.d * p.h;
+    for (int j = 0; j < p.nmat; ++j) {
+      CopySeg& c = cs[j];
+      c.W = src + j * dh;
+      c.w_inst = p.nmat * dh;
+      c.R = R[j];
+      c.L = L[j];
+      c.nsum = nsum;
+      c.split = split;
+      c.sign = sign;
+      if (tall(j)) {
+        c.dstT = wide + j * mn();
+        c.ldT = R[j];
+        c.dstT_inst = p.nmat * mn();
+      } else {
+        c.dst = wide + j * mn();
+        c.ld = L[j];
+        c.dst_inst = p.nmat * mn();
+      }
+    }
+    return timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_copies_f32(cs, p.nmat, p.BH, s); });
+  }
+  int scatter(const float* wide, float sign, float* dst) const {
+    CopySeg cs[3] = {};
+    const int64_t dh = (int64_t)p.d * p.h;
+    for (int j = 0; j < p.nmat; ++j) {
+      CopySeg& c = cs[j];
+      c.W = wide + j * mn();
+      c.w_inst = p.nmat * mn();
+      c.R = N.m;
+      c.L = N.n;
+      c.sign = sign;
+      if (tall(j)) {   // the stored matrix is the slot's transpose
+        c.dstT = dst + j * dh;
+        c.ldT = L[j];
+        c.dstT_inst = p.nmat * dh;
+      } else {
+        c.dst = dst + j * dh;
+        c.ld = L[j];
+        c.dst_inst = p.nmat * dh;
+      }
+    }
+    return timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_copies_f32(cs, p.nmat, p.BH, s); });
+  }
+  // out[i][j] = sum_e a[i][e] b[j][e] over K per slot (rows of a: `rows`, of b: rows_out)
+  int out(const _Float16* a, int64_t a_ld, int64_t a_inst, const _Float16* b, int64_t b_ld, int64_t b_inst,
+          _Float16* o, int rows, int rows_out, int K) const {
+    BwdArgs x{};
+    const TileShape t = bwd_tile(BWD_OUT, true, false);
+    BwdSeg& g = x.seg[0];
+    g.kind = BWD_OUT;
+    g.tiles_m = (int)cdiv(rows_out, t.rows);
+    g.tiles_n = (int)cdiv(rows, t.cols);
+    g.nsplit = 1;
+    g.nblocks = N.S * g.tiles_m * g.tiles_n;
+    g.rows = rows;
+    g.a0 = op(a, a_ld, a_inst);
+    g.b0 = op(b, b_ld, b_inst);
+    g.out = o;
+    g.out_inst = (int64_t)rows * rows_out;
+    g.klen = K;
+    x.nseg = 1;
+    x.total_blocks = g.nblocks;
+    x.d = rows_out;
+    x.h = K;
+    x.narrow = 0;
+    return timed(LACT_KCLASS_NS, 2.0 * N.S * rows * rows_out * K, s, [&] { return launch_bwd_f16(x, s); });
+  }
+  // out = a^T b per slot: a [m x m] (rows i), b [m x n] (rows i), fp32 [m x n]; up to two at once
+  int grad2(const _Float16* const* a, const _Float16* const* b, float* const* o, int nseg) const {
+    BwdArgs x{};
+    const TileShape t = bwd_tile(BWD_GRAD2, true, false);
+    for (int i = 0; i < nseg; ++i) {
+      BwdSeg& g = x.seg[i];
+      g.kind = BWD_GRAD2;
+      g.tiles_m = (int)cdiv(N.m, t.rows);
+      g.tiles_n = (int)cdiv(N.n, t.cols);
+      g.nsplit = 1;
+      g.nblocks = N.S * g.tiles_m * g.tiles_n;
+      g.rows = N.m;
+      g.split_len = cdiv(N.m, 32) * 32;
+      g.a0 = op(a[i], N.m, mm());
+      g.b0 = op(b[i], N.n, mn());
+      g.out = o[i];
+      g.out_inst = mn();
+      g.out_split = N.S * mn();
+      g.out_off = 0;
+    }
+    x.nseg = nseg;
+    x.total_blocks = 0;
+    for (int i = 0; i < nseg; ++i) x.total_blocks += x.seg[i].nblocks;
+    x.d = N.m;
+    x.h = N.n;
+    x.narrow = 0;
+    return timed(LACT_KCLASS_NS, 2.0 * nseg * N.S * mm() * N.n, s, [&] { return launch_bwd_f16(x, s); });
+  }
+  int lin(int mode, const float* x, const float* y, const float* p1, const float* p2, const float* sc,
+          const float* sc2, float a, float* o32, _Float16* o16) const {
+    NsLinArgs l{};
+    l.mode = mode;
+    l.x = x;
+    l.y = y;
+    l.p1 = p1;
+    l.p2 = p2;
+    l.sc = sc;
+    l.sc2 = sc2;
+    l.a = a;
+    l.eps = (float)kNsEps;
+    l.out32 = o32;
+    l.out16 = o16;
+    l.S = N.S;
+    l.len = mn();
+    return timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_ns_lin(l, s); });
+  }
+  _Float16* X16(int k) const { return at<_Float16>(N.x16) + (size_t)k * N.S * mn(); }
+  _Float16* A16(int k) const { return at<_Float16>(N.a16) + (size_t)k * N.S * mm(); }
+  _Float16* B16(int k) const { return at<_Float16>(N.b16) + (size_t)k * N.S * mm(); }
+
+  // The step -Muon(g) of the gradient whose negated split partials are
+  // P (stored layout), into pstep (stored layout, one split).
+  int forward(const float* P, int nsplit, int64_t split) const {
+    float* G = at<float>(N.g);
+    float* X = at<float>(N.x32);
+    int rc = gather(P, nsplit, split, -1.0f, G);
+    if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_slot_dot(G, G, N.S, mn(), at<float>(N.nrm), s); });
+    if (!rc) rc = lin(0, G, nullptr, nullptr, nullptr, at<float>(N.nrm), nullptr, 0.f, X, steps > 0 ? X16(0) : nullptr);
+    for (int k = 0; k < steps && !rc; ++k) {
+      rc = out(X16(k), N.n, mn(), X16(k), N.n, mn(), A16(k), N.m, N.m, N.n);   // A = X X^T
+      if (!rc) rc = out(A16(k), N.m, mm(), A16(k), N.m, mm(), at<_Float16>(N.q16), N.m, N.m, N.m);   // A A
+      if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] {   // B = b A + c A A (symmetrised)
+        return launch_sym(A16(k), (float)kNsB, at<_Float16>(N.q16), 0.5f * (float)kNsC, B16(k), N.S, N.m, s);
+      });
+      const _Float16* a2[1] = {B16(k)};
+      const _Float16* b2[1] = {X16(k)};
+      float* o2[1] = {at<float>(N.p1)};
+      if (!rc) rc = grad2(a2, b2, o2, 1);   // B X
+      if (!rc) rc = lin(1, X, nullptr, at<float>(N.p1), nullptr, nullptr, nullptr, (float)kNsA, X,
+                        k + 1 < steps ? X16(k + 1) : nullptr);
+    }
+    if (!rc) rc = scatter(X, -1.0f, at<float>(N.pstep));
+    return rc;
+  }
+  // From the update's cotangent of U = W - step (ustep, stored layout), the
+  // gradient's cotangent negated (-dg, stored layout) into ug.
+  int reverse() const {
+    float* G = at<float>(N.g);
+    float* X = at<float>(N.x32);
+    _Float16* T = at<_Float16>(N.t16);
+    int rc = gather(at<float>(N.ustep), 1, 0, -1.0f, X);   // d step = -dU
+    if (!rc) rc = lin(1, X, nullptr, nullptr, nullptr, nullptr, nullptr, 1.0f, nullptr, T);
+    for (int k = steps - 1; k >= 0 && !rc; --k) {
+      rc = out(T, N.n, mn(), X16(k), N.n, mn(), at<_Float16>(N.db16), N.m, N.m, N.n);   // dB = dX' X^T
+      if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] {
+        return launch_sym(nullptr, 0.f, at<_Float16>(N.db16), 1.0f, at<_Float16>(N.s16), N.S, N.m, s);
+      });
+      if (!rc) rc = out(at<_Float16>(N.s16), N.m, mm(), A16(k), N.m, mm(), at<_Float16>(N.q16), N.m, N.m, N.m);
+      if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] {   // M = b S + c (S A + (S A)^T)
+        return launch_sym(at<_Float16>(N.s16), (float)kNsB, at<_Float16>(N.q16), (float)kNsC, at<_Float16>(N.m16),
+                          N.S, N.m, s);
+      });
+      const _Float16* a2[2] = {B16(k), at<_Float16>(N.m16)};
+      const _Float16* b2[2] = {T, X16(k)};
+      float* o2[2] = {at<float>(N.p1), at<float>(N.p2)};
+      if (!rc) rc = grad2(a2, b2, o2, 2);   // B dX', M X
+      if (!rc) rc = lin(1, X, nullptr, at<float>(N.p1), at<float>(N.p2), nullptr, nullptr, (float)kNsA, X,
+                        k > 0 ? T : nullptr);
+    }
+    if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_slot_dot(X, G, N.S, mn(), at<float>(N.dot), s); });
+    if (!rc) rc = lin(2, X, G, nullptr, nullptr, at<float>(N.nrm), at<float>(N.dot), 0.f, X, nullptr);
+    if (!rc) rc = scatter(X, -1.0f, at<float>(N.ug));
+    return rc;
+  }
+};
+
 // ---------------------------------------------------------------- backward
 // Reverse of the linear fast weight's chunk loop (§5.4 with the §3.1 chunk
 // gradient and the per-row norm-preserving update of §3.2). The linear
@@ -1099,6 +1337,7 @@ int run_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, 
 // the two operand copies of the update's cotangent.
 struct BwdLayout {
   Plan p;
+  NsBwdLayout ns;       // with Muon: the Newton-Schulz reverse's buffers
   int64_t nch;          // chunks of the forward
   bool batched;         // chunk = whole 32-token steps: one split per chunk
   int64_t group;        // chunks per launch of the batched contractions
@@ -1110,7 +1349,8 @@ struct BwdLayout {
 int bwd_layout(const lact_desc* dsc, BwdLayout* L) {
   int rc = check_desc(dsc);
   if (rc) return rc;
-  if (dsc->fast_weight != LACT_FW_LINEAR || dsc->use_muon) return LACT_EUNSUPPORTED;
+  if (dsc->fast_weight != LACT_FW_LINEAR) return LACT_EUNSUPPORTED;
+  if (dsc->use_muon && dsc->io_dtype != LACT_IO_BF16) return LACT_EUNSUPPORTED;   // fp16 Newton-Schulz reverse
   L->p = make_plan(dsc);
   const Plan& p = L->p;
   const double dd = (double)p.d * p.d;
@@ -1142,6 +1382,7 @@ int bwd_layout(const lact_desc* dsc, BwdLayout* L) {
   o = align_up(o + wio);
   L->off_ut = o;
   o = align_up(o + wio);
+  if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns);
   L->total = std::max<size_t>(o, kAlign);
   return LACT_OK;
 }
@@ -1255,12 +1496,19 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
       if (rc) return rc;
     }
   }
-  // W_{c+1} = rows of W_c + P_c rescaled to W_c's row norms
+  // W_{c+1} = rows of W_c + P_c (or, with Muon, W_c - Muon(g_c)) rescaled to
+  // W_c's row norms
   for (int64_t ci = 0; ci < L.nch; ++ci) {
     UpdArgs u{};
     u.W[0] = traj(ci + 1);
     u.Wsrc[0] = traj(ci);
     u.step = Pall + ci * psplit;
+    if (p.muon) {
+      const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}};
+      rc = nb.forward(Pall + ci * psplit, 1, psplit);
+      if (rc) return rc;
+      u.step = nb.at<float>(L.ns.pstep);
+    }
     u.nsplit = 1;
     u.step_split = 0;
     u.nmat = 1;
@@ -1319,10 +1567,15 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
   uint8_t* ut = ws + L.off_ut;
   for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
     const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
+    const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}};
+    if (p.muon) {   // the step is Muon(g): replay the iteration into its negation
+      rc = nb.forward(Pall + ci * psplit, 1, psplit);
+      if (rc) return rc;
+    }
     VjpArgs va{};
     va.W = traj(ci);
     va.w_inst = dd;
-    va.P = PartSet{Pall + ci * psplit, 1, psplit, dd};
+    va.P = p.muon ? PartSet{nb.at<float>(L.ns.pstep), 1, psplit, dd} : PartSet{Pall + ci * psplit, 1, psplit, dd};
     const PartSet ac{Aall + ci * psplit, 1, psplit, dd};
     if (then_apply) va.pre[0] = ac;   // applied with the weights leaving the chunk
     else va.post = ac;
@@ -1337,8 +1590,20 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     va.BH = p.BH;
     va.R = p.d;
     va.L = p.d;
+    if (p.muon) {   // the update's cotangent in fp32 for the Newton-Schulz reverse
+      va.Ub = va.UT = nullptr;
+      va.U32 = nb.at<float>(L.ns.ustep);
+      va.u32_inst = dd;
+    }
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(&va, 1, p.bf16, s); });
     if (rc) return rc;
+    if (p.muon) {   // the gradient's cotangent (negated) in the operand layouts
+      rc = nb.reverse();
+      if (rc) return rc;
+      const CopySeg cs{nb.at<float>(L.ns.ug), dd, p.d, p.d, ub, d, dd, ut, d, dd};
+      rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_copies(&cs, 1, p.BH, p.bf16, s); });
+      if (rc) return rc;
+    }
     BwdArgs b{};
     lin_out_seg(b.seg[0], p, op(kb + s0 * d * esz, d, n_kv * d), op(ub, d, dd), (uint8_t*)dv + s0 * d * esz,
                 n_kv * d, n);   // Y = K Uh^T
@@ -1379,6 +1644,7 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
 // [eta A | dC] against [U2 | W2], [dZq1 | dZq3] against [W1^T | W3^T]).
 struct SwBwdLayout {
   Plan p;               // the forward's plan without the fused gradient-and-update kind
+  NsBwdLayout ns;       // with Muon: the Newton-Schulz reverse's buffers
   int64_t nch;          // chunks of the forward
   int64_t T;            // token rows of the chunk buffers (a chunk, or a piece of the tail)
   int64_t tail_split;   // tokens per split of a tail piece (at most p.nsplit splits)
@@ -1390,7 +1656,8 @@ struct SwBwdLayout {
 int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L) {
   int rc = check_desc(dsc);
   if (rc) return rc;
-  if (dsc->fast_weight != LACT_FW_SWIGLU || dsc->use_muon || dsc->eta_per_matrix) return LACT_EUNSUPPORTED;
+  if (dsc->fast_weight != LACT_FW_SWIGLU || dsc->eta_per_matrix) return LACT_EUNSUPPORTED;
+  if (dsc->use_muon && dsc->io_dtype != LACT_IO_BF16) return LACT_EUNSUPPORTED;   // fp16 Newton-Schulz reverse
   L->p = make_plan(dsc, false);
   const Plan& p = L->p;
   const double dh = (double)p.d * p.h;
@@ -1425,6 +1692,7 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L) {
   for (int i = 0; i < 3; ++i) L->off_ur[i] = take(wio);   // U1, U3 row-major and U2^T
   L->off_apart = take((size_t)p.nsplit * 3 * w4);
   L->off_bpart = take((size_t)p.nsplit * 3 * w4);
+  if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns);
   L->total = o;
   return LACT_OK;
 }
@@ -1473,6 +1741,12 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     for (int m = 0; m < 3; ++m) {
       c.W[m] = traj(ci + 1, m);
       c.Wsrc[m] = traj(ci, m);
+      if (p.muon) {   // Muon's fused last steps update W in place: start from a copy
+        c.Wsrc[m] = nullptr;
+        rc = timed(LACT_KCLASS_PREP, 0.0, c.s,
+                   [&] { return hipMemcpyAsync(traj(ci + 1, m), traj(ci, m), w4, hipMemcpyDeviceToDevice, c.s); });
+        if (rc) return rc;
+      }
     }
     if (!p.bf16) {   // fp32: the contractions read the state itself
       c.wop[0] = op(traj(ci, 0), d, dh);
@@ -1656,13 +1930,19 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       a_pending = true;
     }
     // the update's reverse: W1, W3 ([h x d]) and W2 ([d x h]) in one launch
+    const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {(int)h, (int)d, (int)h}, {(int)d, (int)h, (int)d}};
+    float* gslot = reinterpret_cast<float*>(ws + L.off_P + (size_t)ci * L.slotP);
+    if (p.muon) {   // the steps are Muon(g_j): replay the iteration into their negation
+      rc = nb.forward(gslot, p.nsplit, psplit);
+      if (rc) return rc;
+    }
     VjpArgs va[3] = {};
     for (int m = 0; m < 3; ++m) {
       VjpArgs& x = va[m];
       const bool w2 = m == 1;
       x.W = traj(ci, m);
       x.w_inst = dh;
-      x.P = pset(reinterpret_cast<float*>(ws + L.off_P + (size_t)ci * L.slotP), p.nsplit, m);
+      x.P = p.muon ? pset(nb.at<float>(L.ns.pstep), 1, m) : pset(gslot, p.nsplit, m);
       if (b_pending) x.pre[0] = pset(bpart, b_ns, m);
       if (a_pending) x.pre[1] = pset(apart, a_ns, m);
       x.G = dW[m];
@@ -1685,9 +1965,24 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       x.BH = p.BH;
       x.R = (int)(w2 ? d : h);
       x.L = (int)(w2 ? h : d);
+      if (p.muon) {   // the update's cotangent in fp32 for the Newton-Schulz reverse
+        x.Ub = x.UT = nullptr;
+        x.U32 = nb.at<float>(L.ns.ustep) + m * dh;
+        x.u32_inst = 3 * dh;
+      }
     }
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(va, 3, p.bf16, s); });
     if (rc) return rc;
+    if (p.muon) {   // the gradients' cotangents (negated) into the operand layouts
+      rc = nb.reverse();
+      if (rc) return rc;
+      const float* ug = nb.at<float>(L.ns.ug);
+      const CopySeg cs[3] = {{ug, 3 * dh, (int)h, (int)d, ur[0], d, dh, bk + h * esz, 4 * h, d * 4 * h},
+                             {ug + 2 * dh, 3 * dh, (int)h, (int)d, ur[1], d, dh, bk, 4 * h, d * 4 * h},
+                             {ug + dh, 3 * dh, (int)d, (int)h, bv, 2 * h, d * 2 * h, ur[2], d, dh}};
+      rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_copies(cs, 3, p.BH, p.bf16, s); });
+      if (rc) return rc;
+    }
     a_pending = b_pending = false;
     rc = weight_copies(ci, L.off_u, bk + 2 * h * esz, 4 * h, bv + h * esz);
     if (rc) return rc;

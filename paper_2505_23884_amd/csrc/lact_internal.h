@@ -206,6 +206,8 @@ constexpr int kNsFusedM = 128, kNsFusedN = 256;
 // Quintic Newton-Schulz coefficients (a, b, c) of Muon (App. A, Details of Muon):
 // X <- a X + b (X X^T) X + c (X X^T)^2 X
 constexpr float kNsA = 3.4445f, kNsB = -4.7750f, kNsC = 2.0315f;
+// Muon divides the gradient by ||G||_F + kNsEps, so a zero gradient gives a zero step.
+constexpr float kNsEps = 1e-7f;
 struct NsFusedArgs {
   // X0 = G / (||G||_F + eps), G the sum of nsplit fp32 partials part_split
   // elements apart (slot stride ystride); steps quintic iterations; then the
@@ -307,6 +309,7 @@ struct VjpArgs {
   float* G; int64_t g_inst;           // cotangent of W' in, of W out (in place)
   void* Ub; int64_t ub_ld, ub_inst;   // cotangent of U in the operand type, row-major (or nullptr)
   void* UT; int64_t ut_ld, ut_inst;   // the same, transposed (or nullptr)
+  float* U32; int64_t u32_inst;       // the same in fp32, row-major with rows of L (or nullptr)
   int BH, R, L;
 };
 
@@ -321,9 +324,37 @@ struct CopySeg {
   int R, L;
   void* dst; int64_t ld, dst_inst;
   void* dstT; int64_t ldT, dstT_inst;
+  int nsum;                 // source splits summed (0 or 1: one)
+  int64_t split;            // floats between source splits
+  float sign;               // factor of the sum (0: 1)
 };
 constexpr int kMaxCopies = 8;
 hipError_t launch_copies(const CopySeg* c, int n, int BH, bool io_bf16, hipStream_t s);
+// The same with fp32 copies.
+hipError_t launch_copies_f32(const CopySeg* c, int n, int BH, hipStream_t s);
+
+// ---- reverse of Newton-Schulz (slots of wide [m x n] fp32 matrices) --------
+// The k_bwd kinds with fp16 operands (fp16 OUT results, fp32 GRAD partials).
+hipError_t launch_bwd_f16(const BwdArgs& a, hipStream_t s);
+// out[s] = sum over len elements of x[s] * y[s] (slot s), one workgroup per slot.
+hipError_t launch_slot_dot(const float* x, const float* y, int S, int64_t len, float* out, hipStream_t s);
+// Elementwise over S slots of len floats (x, y, p1, p2 fp32; sc, sc2 per slot):
+//   mode 0: out = x / (sqrt(sc) + eps)
+//   mode 1: out = a x + p1 (+ p2 when given)
+//   mode 2: out = x / (sqrt(sc) + eps) - sc2 / ((sqrt(sc) + eps)^2 sqrt(sc)) y
+// into out32 and/or its fp16 copy out16.
+struct NsLinArgs {
+  int mode;
+  const float* x; const float* y; const float* p1; const float* p2;
+  const float* sc; const float* sc2;
+  float a, eps;
+  float* out32; _Float16* out16;
+  int S; int64_t len;
+};
+hipError_t launch_ns_lin(const NsLinArgs& a, hipStream_t s);
+// out = alpha X + beta (Y + Y^T) per slot of fp16 [m x m] matrices (X may be nullptr).
+hipError_t launch_sym(const _Float16* X, float alpha, const _Float16* Y, float beta, _Float16* out, int S, int m,
+                      hipStream_t s);
 // G = base + sum of the sets over BH instances of RL floats each (RL a
 // multiple of 4); base: 0 (mode 0), init (mode 1) or G itself (mode 2).
 hipError_t launch_accum(float* G, int64_t g_inst, const float* init, int64_t i_inst, int mode, PartSet s0, PartSet s1,

@@ -237,6 +237,13 @@ template <> struct Kinds<__bf16> {
   using Grad13 = KGrad13_16;
   using Grad2 = KGrad2_16;
 };
+template <> struct Kinds<_Float16> {   // the backward of Newton-Schulz: fp16 operands
+  using Apply = KApply16;
+  using Update = KApply16;
+  using Out = KOut16;
+  using Grad13 = KGrad13_16;
+  using Grad2 = KGrad2_16;
+};
 template <> struct Kinds<float> {
   using Apply = KApply32;
   using Update = KUpdate32;
@@ -839,17 +846,17 @@ __device__ __forceinline__ void lds_barrier() {
 // chunks of a row are XOR-rotated by the token's low 4 bits, so that the 32
 // tokens of one accumulator write and the 16 chunks of one row read spread
 // over all banks.
-template <int R>
+template <int R, typename E = __bf16>
 __device__ __forceinline__ void stage_put(uint8_t* buf, int tok, int row, float a, float b, float c, float d) {
-  typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_t;
+  typedef __attribute__((ext_vector_type(4))) E e4_t;
   const int off = tok * (2 * R) + ((((row >> 3) ^ (tok & 15))) << 4) + (((row >> 2) & 1) << 3);
-  *reinterpret_cast<bf16x4_t*>(buf + off) = bf16x4_t{(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+  *reinterpret_cast<e4_t*>(buf + off) = e4_t{(E)a, (E)b, (E)c, (E)d};
 }
 
 // Copy the staged tile to out (element (token 0, row 0) of the tile, ld
 // elements between tokens): tokens < ntok, rows < nrow (a multiple of 8).
-template <int R, int C, int THREADS>
-__device__ __forceinline__ void stage_flush(const uint8_t* buf, __bf16* out, int64_t ld, int64_t ntok, int64_t nrow) {
+template <int R, int C, int THREADS, typename E = __bf16>
+__device__ __forceinline__ void stage_flush(const uint8_t* buf, E* out, int64_t ld, int64_t ntok, int64_t nrow) {
   constexpr int CPR = R / 8, TOTAL = C * CPR;
   static_assert(CPR >= 16 && TOTAL % THREADS == 0, "staging shape");
 #pragma unroll
@@ -1329,11 +1336,11 @@ __device__ __forceinline__ void bwd_body(const BwdArgs& args, int blk, uint8_t* 
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const f32x16_t& a = acc[0][mi][ni];
-            stage_put<KO::ROWS_A>(smem, acc_col<KO>(ni), mrow0 + mi * 32 + 8 * g, a[4 * g], a[4 * g + 1],
+            stage_put<KO::ROWS_A, T>(smem, acc_col<KO>(ni), mrow0 + mi * 32 + 8 * g, a[4 * g], a[4 * g + 1],
                                   a[4 * g + 2], a[4 * g + 3]);
           }
       lds_barrier();
-      stage_flush<KO::ROWS_A, KO::ROWS_B, KO::THREADS>(smem, reinterpret_cast<__bf16*>(sg.out) + ob + t0 * d + m0, d,
+      stage_flush<KO::ROWS_A, KO::ROWS_B, KO::THREADS, T>(smem, reinterpret_cast<T*>(sg.out) + ob + t0 * d + m0, d,
                                                          ntok, mrows);
       return;
     }
@@ -1354,7 +1361,7 @@ __device__ __forceinline__ void bwd_body(const BwdArgs& args, int blk, uint8_t* 
     return;
   }
 
-  if constexpr (sizeof(T) == 2 && !NARROW) {
+  if constexpr (sizeof(T) == 2 && !NARROW && !__is_same(T, _Float16)) {
     if (sg.kind == BWD_GRAD_UPD) {
       grad_update_tile<T>(sg, inst, rr, d, h, smem);
       return;
@@ -2357,6 +2364,7 @@ __device__ __forceinline__ void vjp_body(const VjpArgs& a, int blk, T* tile) {
       g4[i] = make_float4(uh.x + c3 * wv[t].x + ap[t].x, uh.y + c3 * wv[t].y + ap[t].y,
                           uh.z + c3 * wv[t].z + ap[t].z, uh.w + c3 * wv[t].w + ap[t].w);
       if (Ub) st4<T>(Ub, inst * a.ub_inst + (int64_t)r * a.ub_ld + 4 * i, uh.x, uh.y, uh.z, uh.w);
+      if (a.U32) reinterpret_cast<float4*>(a.U32 + inst * a.u32_inst + roff)[i] = uh;
       T* row = tile + rr * LD + 4 * i;
       row[0] = (T)uh.x;
       row[1] = (T)uh.y;
@@ -2418,16 +2426,23 @@ __global__ __launch_bounds__(256) void k_copies(const CopyArgs a) {
   const int r0 = (rest / tl) * 64, c0 = (rest % tl) * 64;
   const float* src = g.W + inst * g.w_inst;
   const int t = threadIdx.x, q = (t & 15) * 4;
+  const int nsum = g.nsum > 1 ? g.nsum : 1;
+  const float sign = g.sign != 0.0f ? g.sign : 1.0f;
   for (int k = t >> 4; k < 64; k += 16) {   // row k of the tile, columns q .. q + 3
     const int r = r0 + k, c = c0 + q;
     float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < g.R && c + 3 < g.L) {
-      x = *reinterpret_cast<const float4*>(src + (int64_t)r * g.L + c);
-    } else if (r < g.R) {
+    for (int sp = 0; sp < nsum; ++sp) {
+      const float* sr = src + sp * g.split;
       float e[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int j = 0; j < 4 && c + j < g.L; ++j) e[j] = src[(int64_t)r * g.L + c + j];
-      x = make_float4(e[0], e[1], e[2], e[3]);
+      if (r < g.R && c + 3 < g.L) {
+        const float4 v = *reinterpret_cast<const float4*>(sr + (int64_t)r * g.L + c);
+        e[0] = v.x; e[1] = v.y; e[2] = v.z; e[3] = v.w;
+      } else if (r < g.R) {
+        for (int j = 0; j < 4 && c + j < g.L; ++j) e[j] = sr[(int64_t)r * g.L + c + j];
+      }
+      x.x += e[0]; x.y += e[1]; x.z += e[2]; x.w += e[3];
     }
+    x.x *= sign; x.y *= sign; x.z *= sign; x.w *= sign;
     tile[k][q] = x.x;
     tile[k][q + 1] = x.y;
     tile[k][q + 2] = x.z;
@@ -2459,6 +2474,80 @@ __global__ __launch_bounds__(256) void k_copies(const CopyArgs a) {
         for (int j = 0; j < 4 && r + j < g.R; ++j) out[o + j] = (T)tile[q + j][k];
       }
     }
+  }
+}
+
+// Sum over one slot of x * y, one workgroup per slot (a fixed reduction
+// order, so repeated calls agree bit for bit).
+__global__ __launch_bounds__(256) void k_slot_dot(const float* x, const float* y, int64_t len, float* out) {
+  __shared__ float red[4];
+  const float4* x4 = reinterpret_cast<const float4*>(x + blockIdx.x * len);
+  const float4* y4 = reinterpret_cast<const float4*>(y + blockIdx.x * len);
+  float acc = 0.0f;
+  for (int64_t i = threadIdx.x; i < (len >> 2); i += 256) {
+    const float4 a = x4[i], b = y4[i];
+    acc += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+  }
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) out[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// Elementwise steps of the Newton-Schulz reverse (see NsLinArgs), grid stride.
+__global__ __launch_bounds__(256) void k_ns_lin(const NsLinArgs a) {
+  const int64_t n4 = a.len >> 2, total = (int64_t)a.S * n4;
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < total; q += (int64_t)gridDim.x * 256) {
+    const int64_t slot = q / n4;
+    const float4 x = reinterpret_cast<const float4*>(a.x)[q];
+    float4 r;
+    if (a.mode == 0) {
+      const float f = 1.0f / (sqrtf(a.sc[slot]) + a.eps);
+      r = make_float4(x.x * f, x.y * f, x.z * f, x.w * f);
+    } else if (a.mode == 1) {
+      r = make_float4(a.a * x.x, a.a * x.y, a.a * x.z, a.a * x.w);
+      if (a.p1) {
+        const float4 p = reinterpret_cast<const float4*>(a.p1)[q];
+        r.x += p.x; r.y += p.y; r.z += p.z; r.w += p.w;
+      }
+      if (a.p2) {
+        const float4 p = reinterpret_cast<const float4*>(a.p2)[q];
+        r.x += p.x; r.y += p.y; r.z += p.z; r.w += p.w;
+      }
+    } else {
+      const float nrm = sqrtf(a.sc[slot]), se = nrm + a.eps;
+      const float f = 1.0f / se, gf = a.sc2[slot] / (se * se * nrm);
+      const float4 y = reinterpret_cast<const float4*>(a.y)[q];
+      r = make_float4(x.x * f - gf * y.x, x.y * f - gf * y.y, x.z * f - gf * y.z, x.w * f - gf * y.w);
+    }
+    if (a.out32) reinterpret_cast<float4*>(a.out32)[q] = r;
+    if (a.out16) st4<_Float16>(a.out16, 4 * q, r.x, r.y, r.z, r.w);
+  }
+}
+
+// out = alpha X + beta (Y + Y^T) per slot of fp16 [m x m] matrices: one
+// 32 x 32 output tile per block, Y's mirror tile through LDS.
+__global__ __launch_bounds__(256) void k_sym(const _Float16* X, float alpha, const _Float16* Y, float beta,
+                                             _Float16* out, int m, int tiles) {
+  __shared__ float mir[32][33];
+  const int per = tiles * tiles;
+  const int64_t slot = blockIdx.x / per;
+  const int rest = blockIdx.x - (int)slot * per;
+  const int r0 = (rest / tiles) * 32, c0 = (rest % tiles) * 32;
+  const int64_t base = slot * (int64_t)m * m;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int k = ty; k < 32; k += 8) {   // mirror tile: Y[c0 + k][r0 + tx]
+    const int r = c0 + k, c = r0 + tx;
+    mir[k][tx] = (r < m && c < m) ? (float)Y[base + (int64_t)r * m + c] : 0.0f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int r = r0 + k, c = c0 + tx;
+    if (r >= m || c >= m) continue;
+    const int64_t o = base + (int64_t)r * m + c;
+    float v = beta * ((float)Y[o] + mir[tx][k]);
+    if (X) v += alpha * (float)X[o];
+    out[o] = (_Float16)v;
   }
 }
 
@@ -2835,6 +2924,52 @@ hipError_t launch_copies(const CopySeg* c, int n, int BH, bool io_bf16, hipStrea
   a.first[n] = (int)total;
   if (io_bf16) k_copies<__bf16><<<(unsigned)total, 256, 0, s>>>(a);
   else k_copies<float><<<(unsigned)total, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_copies_f32(const CopySeg* c, int n, int BH, hipStream_t s) {
+  if (n < 0 || n > kMaxCopies) return hipErrorInvalidValue;
+  CopyArgs a{};
+  a.n = n;
+  int64_t total = 0;
+  for (int i = 0; i < n; ++i) {
+    a.seg[i] = c[i];
+    a.first[i] = (int)total;
+    total += (int64_t)BH * ((c[i].R + 63) / 64) * ((c[i].L + 63) / 64);
+  }
+  if (total <= 0) return hipSuccess;
+  if (total >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  a.first[n] = (int)total;
+  k_copies<float><<<(unsigned)total, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_f16(const BwdArgs& a, hipStream_t s) {
+  if (a.total_blocks <= 0) return hipSuccess;
+  k_bwd<_Float16, false><<<a.total_blocks, KOut16::THREADS, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_slot_dot(const float* x, const float* y, int S, int64_t len, float* out, hipStream_t s) {
+  if (S <= 0) return hipSuccess;
+  k_slot_dot<<<(unsigned)S, 256, 0, s>>>(x, y, len, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_ns_lin(const NsLinArgs& a, hipStream_t s) {
+  const int64_t need = ((int64_t)a.S * (a.len / 4) + 255) / 256;
+  if (need <= 0) return hipSuccess;
+  const int64_t blocks = need < 8192 ? need : 8192;
+  k_ns_lin<<<(unsigned)blocks, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_sym(const _Float16* X, float alpha, const _Float16* Y, float beta, _Float16* out, int S, int m,
+                      hipStream_t s) {
+  const int tiles = (m + 31) / 32;
+  const int64_t blocks = (int64_t)S * tiles * tiles;
+  if (blocks <= 0) return hipSuccess;
+  k_sym<<<(unsigned)blocks, 256, 0, s>>>(X, alpha, Y, beta, out, m, tiles);
   return hipGetLastError();
 }
 

@@ -254,13 +254,15 @@ def test_backward_errors_before_any_hip_call():
     lin = dict(GOOD, h=64, fast_weight=1)
     d = make_desc(**lin)
     assert P.binding.backward_workspace_bytes(d) > P.workspace_bytes(d)
-    # the linear entry point: the linear fast weight without Muon only
-    for bad in (dict(lin, use_muon=True),):
-        err = ctypes.c_int(0)
-        assert P.lib().lact_backward_workspace_bytes(ctypes.byref(make_desc(**bad)), ctypes.byref(err)) == 0
-        assert err.value == -4
-    for bad in (dict(GOOD), dict(lin, use_muon=True)):
+    # the linear entry point: the linear fast weight only; Muon with bf16 I/O only
+    muon_fp32 = dict(lin, use_muon=True, io_dtype=1)
+    err = ctypes.c_int(0)
+    assert P.lib().lact_backward_workspace_bytes(ctypes.byref(make_desc(**muon_fp32)), ctypes.byref(err)) == 0
+    assert err.value == -4
+    for bad in (dict(GOOD), muon_fp32):
         assert _bwd(make_desc(**bad), nbytes=1 << 30) == -4
+    # Muon keeps the Newton-Schulz iterates of a chunk: a larger workspace
+    assert P.binding.backward_workspace_bytes(make_desc(**dict(lin, use_muon=True))) > P.binding.backward_workspace_bytes(d)
     assert _bwd(make_desc(**dict(lin, d=12, h=12)), nbytes=1 << 30) == -4
     assert _bwd(d, q=0) == -1
     assert _bwd(d, do=0) == -1
@@ -298,10 +300,12 @@ def test_swiglu_backward_errors_before_any_hip_call():
     # every chunk's weights and gradient partials, so it grows with the chunk count
     assert P.binding.backward_workspace_bytes(d) > P.workspace_bytes(d)
     assert P.binding.backward_workspace_bytes(make_desc(**dict(GOOD, chunk=128))) > P.binding.backward_workspace_bytes(d)
-    # no Muon, no per-matrix rates, not the linear fast weight
-    for bad in (dict(GOOD, use_muon=True), dict(GOOD, eta_per_matrix=1), dict(GOOD, h=64, fast_weight=1)):
+    # no per-matrix rates, not the linear fast weight, Muon with bf16 I/O only
+    muon_fp32 = dict(GOOD, use_muon=True, io_dtype=1, d=64, h=64)
+    for bad in (muon_fp32, dict(GOOD, eta_per_matrix=1), dict(GOOD, h=64, fast_weight=1)):
         assert _bwd_sw(make_desc(**bad), nbytes=1 << 30) == -4
-    for bad in (dict(GOOD, use_muon=True), dict(GOOD, eta_per_matrix=1)):
+    assert P.binding.backward_workspace_bytes(make_desc(**dict(GOOD, use_muon=True))) > P.binding.backward_workspace_bytes(d)
+    for bad in (muon_fp32, dict(GOOD, eta_per_matrix=1)):
         err = ctypes.c_int(0)
         assert P.lib().lact_backward_workspace_bytes(ctypes.byref(make_desc(**bad)), ctypes.byref(err)) == 0
         assert err.value == -4

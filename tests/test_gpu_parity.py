@@ -1319,7 +1319,8 @@ def run_gpu_linear_bwd(cfg, x, ct, with_dW=True):
     do = to_dev(sh(ct["do"]), cfg)
     dWf = to_dev(sh(ct["dW"]), cfg, torch.float32) if with_dW else None
     W_in = W0.clone()
-    r = P.backward_linear(q, k, v, eta, W0, do, cfg.chunk, order=cfg.order, dW_final=dWf)
+    r = P.backward_linear(q, k, v, eta, W0, do, cfg.chunk, order=cfg.order, dW_final=dWf,
+                          use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps)
     torch.cuda.synchronize()
     assert torch.equal(W0, W_in)   # W0 is read only
     f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
@@ -1329,8 +1330,12 @@ def run_gpu_linear_bwd(cfg, x, ct, with_dW=True):
 def check_linear_bwd(cfg, x, ct, got, with_dW=True, instances=None):
     idx = slice(None) if instances is None else list(instances)
     sel = lambda a: a if instances is None else a[list(instances)]
-    ref = O.lact_backward_linear(sel(x["q"]), sel(x["k"]), sel(x["v"]), sel(x["eta"]), sel(x["W1"]), sel(ct["do"]),
-                                 cfg.chunk, cfg.order, dW_final=sel(ct["dW"]) if with_dW else None)
+
+    def ref_fn(xx):
+        return O.lact_backward_linear(sel(xx["q"]), sel(xx["k"]), sel(xx["v"]), sel(xx["eta"]), sel(xx["W1"]),
+                                      sel(ct["do"]), cfg.chunk, cfg.order, dW_final=sel(ct["dW"]) if with_dW else None,
+                                      use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps)
+    ref = ref_fn(x)
     errs, blocks = {}, {}
     for name, g, r in zip(("dq", "dk", "dv", "deta", "dW0"), got, ref):
         g = g[idx]
@@ -1346,7 +1351,14 @@ def check_linear_bwd(cfg, x, ct, got, with_dW=True, instances=None):
             errs["deta/(|k||Z|)"] = float(np.max(np.abs(g - ref[3]) / (kn * zn)))
             continue
         blocks[name] = worst_block(g, r, W_BLOCK if name == "dW0" else O_BLOCK)
-    assert_errs(errs, TOL[cfg.io], blocks)
+    if not cfg.use_muon:
+        assert_errs(errs, TOL[cfg.io], blocks)
+        return
+    names = ("dq", "dk", "dv", "deta", "dW0")
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io])
+    wb, bb = dict(zip(names, whole)), dict(zip(names, block))
+    wb["deta/(|k||Z|)"] = max(TOL[cfg.io], wb["deta"])
+    assert_bars(errs, blocks, wb, bb)
 
 
 @pytest.mark.parametrize("order", [0, 1])
@@ -1427,7 +1439,8 @@ def run_gpu_swiglu_bwd(cfg, x, ct, with_dW=True):
     do = to_dev(sh(ct["do"]), cfg)
     dWf = tuple(to_dev(sh(ct[w]), cfg, torch.float32) for w in ("dW1", "dW2", "dW3")) if with_dW else None
     W_in = [w.clone() for w in W]
-    r = P.backward(q, k, v, eta, *W, do, cfg.chunk, order=cfg.order, dW_final=dWf)
+    r = P.backward(q, k, v, eta, *W, do, cfg.chunk, order=cfg.order, dW_final=dWf, use_muon=bool(cfg.use_muon),
+                   ns_steps=cfg.ns_steps)
     torch.cuda.synchronize()
     for a, b in zip(W, W_in):
         assert torch.equal(a, b)   # the initial weights are read only
@@ -1452,14 +1465,51 @@ def worst_window(got, ref, rows):
     return worst, where
 
 
+def ulp_neighbour(x, seed):
+    """The bf16 token tensors q, k, v of `x` moved by at most one bf16 ulp
+    (a relative 2^-8 jitter, rounded back to bf16): another rounding of the
+    same data, equally valid as bf16 input."""
+    from lact_synth import round_to_bf16
+    rng = np.random.default_rng(seed)
+    j = lambda a: round_to_bf16((a * (1.0 + 2.0 ** -8 * rng.uniform(-1.0, 1.0, a.shape))).astype(np.float32))
+    return dict(x, q=j(x["q"]), k=j(x["k"]), v=j(x["v"]))
+
+
+def muon_bars(ref_fn, x, ref, tol):
+    """Bars of the Muon backward: Newton-Schulz amplifies small singular
+    directions of the chunk gradient (a factor up to a^5 ~ 480), so its
+    reverse is ill-conditioned in the gradient. The oracle's own results for
+    two bf16 roundings of the same inputs (ulp_neighbour) differ by spread_j
+    per output; the bar is max(tol, spread_j) over the tensor and
+    max(tol, 1.5 spread_j) over a block."""
+    alt = ref_fn(ulp_neighbour(x, 2505))
+    spread = [rel(a, b) for a, b in zip(alt, ref)]
+    print("[gpu] oracle spread under one-ulp input changes", [f"{v:.2e}" for v in spread], flush=True)
+    return [max(tol, v) for v in spread], [max(tol, 1.5 * v) for v in spread]
+
+
+def assert_bars(errs, blocks, whole, block):
+    print("[gpu] rel-L2", {kk: f"{vv:.2e}" for kk, vv in errs.items()}, flush=True)
+    print("[gpu] worst block", {kk: f"{vv[0]:.2e} at {vv[1]}" for kk, vv in blocks.items()}, flush=True)
+    for kk, vv in errs.items():
+        assert vv <= whole[kk], (kk, vv, whole[kk])
+    for kk, (vv, where) in blocks.items():
+        assert vv <= block[kk], (kk, vv, where, block[kk])
+
+
 def check_swiglu_bwd(cfg, x, ct, got, with_dW=True, instances=None):
     idx = slice(None) if instances is None else list(instances)
     sel = lambda a: a if instances is None else a[list(instances)]
-    ref = O.lact_backward(sel(x["q"]), sel(x["k"]), sel(x["v"]), sel(x["eta"]), sel(x["W1"]), sel(x["W2"]),
-                          sel(x["W3"]), sel(ct["do"]), cfg.chunk, cfg.order,
-                          dW_final=tuple(sel(ct[w]) for w in ("dW1", "dW2", "dW3")) if with_dW else None)
+
+    def ref_fn(xx):
+        return O.lact_backward(sel(xx["q"]), sel(xx["k"]), sel(xx["v"]), sel(xx["eta"]), sel(xx["W1"]),
+                               sel(xx["W2"]), sel(xx["W3"]), sel(ct["do"]), cfg.chunk, cfg.order,
+                               dW_final=tuple(sel(ct[w]) for w in ("dW1", "dW2", "dW3")) if with_dW else None,
+                               use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps)
+    ref = ref_fn(x)
+    names = ("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3")
     errs, blocks = {}, {}
-    for name, g, r in zip(("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3"), got, ref):
+    for name, g, r in zip(names, got, ref):
         g = g[idx]
         if g.size == 0:
             continue
@@ -1468,7 +1518,11 @@ def check_swiglu_bwd(cfg, x, ct, got, with_dW=True, instances=None):
             blocks[name] = worst_window(g, r, O_BLOCK)
         else:
             blocks[name] = worst_block(g, r, W_BLOCK if name.startswith("dW") else O_BLOCK)
-    assert_errs(errs, TOL[cfg.io], blocks)
+    if not cfg.use_muon:
+        assert_errs(errs, TOL[cfg.io], blocks)
+        return
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io])
+    assert_bars(errs, blocks, dict(zip(names, whole)), dict(zip(names, block)))
 
 
 @pytest.mark.parametrize("order", [0, 1])
@@ -1527,6 +1581,40 @@ def test_swiglu_backward_repeats_bitwise():
     b = run_gpu_swiglu_bwd(cfg, x, ct)
     for u, w in zip(a, b):
         assert np.array_equal(u, w)
+
+
+# ----------------------------------------------------------------------------- Muon backward
+# The backward through Muon's Newton-Schulz steps (fp16 operands, fp32
+# iterates), two chunks end to end (the Muon recurrence amplifies rounding
+# from chunk to chunk; the forward's parity protocol does the same).
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_muon_backward_small_matrices(order):
+    # d = 128, h = 256: W1, W3 taller than wide (their gradients transposed
+    # into the Newton-Schulz slots), the forward's one-workgroup Newton-Schulz
+    cfg = CONFIGS["video"].with_(name="swiglu_muon_bwd", B=1, H=2, n_kv=400, n_q=440, chunk=256, order=order)
+    x, ct = make_inputs(cfg, 81), make_cotangents(cfg, 81)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct))
+
+
+def test_swiglu_muon_backward_lm_shape_two_chunks():
+    # d = h = 512 (the LM's Gram size), two chunks of 2048
+    cfg = CONFIGS["lm32k_muon"].with_(name="swiglu_muon_bwd_lm", B=1, H=2, n_kv=4096, n_q=4096)
+    x, ct = make_inputs(cfg, 82), make_cotangents(cfg, 82)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct))
+
+
+@pytest.mark.parametrize("d", [128, 512])
+def test_linear_muon_backward_two_chunks(d):
+    # chunks of at least d tokens (a full-rank chunk gradient, as in every
+    # workload of the paper): with fewer, Newton-Schulz multiplies the
+    # gradient's null space by a^5 ~ 480 and the reverse amplifies rounding there
+    C = max(256, d)
+    cfg = CONFIGS["lm32k_muon"].with_(name="linear_muon_bwd", B=1, H=2, d=d, h=d, n_kv=2 * C, n_q=2 * C + 48, chunk=C,
+                                      order=1, linear=1)
+    x, ct = make_inputs(cfg, 83), make_cotangents(cfg, 83)
+    check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct))
 
 
 # ----------------------------------------------------------------------------- envelope limits

@@ -1185,3 +1185,21 @@ def test_linear_muon_backward_matches_autograd():
         got = O.lact_backward_linear_instance(q, k, v, eta, W0, do, C, order, dWf, use_muon=True)
         for name, g, ref in zip(("dq", "dk", "dv", "deta", "dW0"), got, (qt, kt, vt, et, Wt)):
             assert np.allclose(g, ref.grad.numpy(), rtol=1e-8, atol=1e-10), (order, name)
+
+
+def test_newton_schulz_vjp_amplifies_the_null_space_by_a_per_step():
+    # G = s u w^T (rank one): a cotangent y z^T with y orthogonal to u and z
+    # orthogonal to w leaves A = X X^T unchanged and is annihilated by B, so
+    # each step multiplies it by a; through five steps and the scaling the
+    # reverse returns a^5 y z^T / (s + eps) (the amplification that makes the
+    # reverse ill-conditioned when a chunk gradient is rank-deficient)
+    rng = _rng(128)
+    m, n, s = 4, 6, 0.37
+    u = rng.standard_normal(m); u /= np.linalg.norm(u)
+    w = rng.standard_normal(n); w /= np.linalg.norm(w)
+    y = rng.standard_normal(m); y -= (y @ u) * u
+    z = rng.standard_normal(n); z -= (z @ w) * w
+    G, dX = s * np.outer(u, w), np.outer(y, z)
+    a = O.NS_COEFFS[0]
+    assert np.allclose(O.newton_schulz_vjp(G, dX, 5), a ** 5 * dX / (s + O.NS_EPS), rtol=1e-10, atol=1e-12)
+    assert np.allclose(O.newton_schulz_vjp(G, dX, 2), a ** 2 * dX / (s + O.NS_EPS), rtol=1e-10, atol=1e-12)

@@ -41,7 +41,10 @@ It follows "Test-Time Training Done Right" (LaCT) step by step, per
                    derivative of SiLU (reverse mode written out by hand,
                    step by step against the forward's closed form); with
                    Muon, the reverse of every Newton-Schulz step between
-                   the gradient and the update (both fast weights)
+                   the gradient and the update (both fast weights); with
+                   momentum, the state's cotangent carried from chunk to
+                   chunk and the factor's cotangent spread over the chunk's
+                   tokens
 * schedule         a list of (mode, begin, end) segments, each one of
                    update-then-apply, apply-then-update, update-only or
                    apply-only on its token range (the ttt_config loop of Alg. 1;
@@ -101,7 +104,7 @@ __all__ = [
     "lact_forward_linear_instance", "lact_forward_linear", "linear_flops", "layer_flops",
     "weight_update_vjp", "lact_backward_linear_instance", "lact_backward_linear",
     "silu_second_derivative", "swiglu_apply_vjp", "chunk_gradient_vjp", "lact_backward_instance",
-    "lact_backward", "newton_schulz_vjp",
+    "lact_backward", "newton_schulz_vjp", "lact_backward_momentum_instance", "lact_backward_momentum",
 ]
 
 # Newton-Schulz quintic coefficients and iteration count (App. A, Details of Muon).
@@ -661,6 +664,105 @@ def lact_backward(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final
             None if dW_final is None else tuple(w[i] for w in dW_final), use_muon, ns_steps)
         res.append((dq, dk, dv, deta, *dW))
     return tuple(np.stack(col) for col in zip(*res))
+
+
+def lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, chunk: int, order: int, dW_final=None,
+                                    dM_final=None, use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT):
+    """Reverse of the chunk loop with the momentum optimizer (momentum_update;
+    App. A), SwiGLU (W0, M0 triples) or linear (W0, M0 single [d, d] arrays)
+    fast weight, Muon optional. Per chunk c with M' = bbar_c M + g_c and
+    W' = weight_update(W, step(M')), step = Muon or the identity:
+        dM'   = (cotangent carried from M') + step^T(d step)
+        g_c's cotangent = dM';  carried to M: bbar_c dM'
+        d bbar_c = <dM', M>, shared equally by the chunk's tokens (bbar is
+        their mean of beta).
+    Returns (dq, dk, dv, deta, dbeta, dW0, dM0), dW0 and dM0 triples for
+    SwiGLU, single arrays for the linear fast weight.
+    """
+    linear = not isinstance(W0, (tuple, list))
+    q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
+    eta = np.asarray(eta, dtype=np.float64)
+    beta = np.asarray(beta, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    tup = (lambda a: (a,)) if linear else (lambda a: tuple(a))
+    W = tuple(np.asarray(w, dtype=np.float64).copy() for w in tup(W0))
+    M = tuple(np.asarray(m, dtype=np.float64).copy() for m in tup(M0))
+    n_q, n_kv = q.shape[0], k.shape[0]
+    step_of = (lambda g: newton_schulz(g, ns_steps)) if use_muon else (lambda g: g)
+    grad = (lambda Wc, s, e: (linear_gradient(Wc[0], k[s:e], v[s:e], eta[s:e]),)) if linear else \
+        (lambda Wc, s, e: chunk_gradient(*Wc, k[s:e], v[s:e], eta[s:e]))
+    apply_vjp = (lambda Wc, X, dO: (dO @ Wc[0], dO.T @ X)) if linear else \
+        (lambda Wc, X, dO: (lambda r: (r[0], r[1], r[2], r[3]))(swiglu_apply_vjp(*Wc, X, dO)))
+    Ws, Ms, bbars = [W], [M], []
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        g = grad(Ws[-1], s, e)
+        bbar = float(np.mean(beta[s:e]))
+        Mn = tuple(bbar * m + gj for m, gj in zip(Ms[-1], g))
+        Ws.append(tuple(weight_update(w, step_of(m)) for w, m in zip(Ws[-1], Mn)))
+        Ms.append(Mn)
+        bbars.append(bbar)
+    nm = len(W)
+    dW = [np.zeros_like(w) for w in W] if dW_final is None else [
+        np.asarray(x, dtype=np.float64).copy() for x in tup(dW_final)]
+    dM = [np.zeros_like(m) for m in M] if dM_final is None else [
+        np.asarray(x, dtype=np.float64).copy() for x in tup(dM_final)]
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    deta, dbeta = np.zeros(n_kv), np.zeros(n_kv)
+
+    def apply_back(Wc, s, e):
+        r = apply_vjp(Wc, q[s:e], do[s:e])
+        dq[s:e] = r[0]
+        for j in range(nm):
+            dW[j] += r[1 + j]
+
+    if n_q > n_kv:
+        apply_back(Ws[-1], n_kv, n_q)
+    starts = list(range(0, n_kv, chunk))
+    for c in reversed(range(len(starts))):
+        s, e = starts[c], min(n_kv, starts[c] + chunk)
+        if order == 1:
+            apply_back(Ws[c + 1], s, e)
+        dMt = []
+        for j in range(nm):
+            dW[j], dst = weight_update_vjp(Ws[c][j], step_of(Ms[c + 1][j]), dW[j])
+            dMt.append(dM[j] + (newton_schulz_vjp(Ms[c + 1][j], dst, ns_steps) if use_muon else dst))
+        if linear:
+            kg = k[s:e] @ dMt[0].T
+            dv[s:e] = -eta[s:e, None] * kg
+            dk[s:e] = -eta[s:e, None] * (v[s:e] @ dMt[0])
+            deta[s:e] = -np.sum(v[s:e] * kg, axis=1)
+        else:
+            b1, b2, b3, dk[s:e], dv[s:e], deta[s:e] = chunk_gradient_vjp(*Ws[c], k[s:e], v[s:e], eta[s:e], *dMt)
+            for j, b in enumerate((b1, b2, b3)):
+                dW[j] += b
+        dbeta[s:e] = sum(float(np.sum(a * m)) for a, m in zip(dMt, Ms[c])) / (e - s)
+        dM = [bbars[c] * a for a in dMt]
+        if order == 0:
+            apply_back(Ws[c], s, e)
+    out = (lambda t: t[0]) if linear else tuple
+    return dq, dk, dv, deta, dbeta, out(dW), out(dM)
+
+
+def lact_backward_momentum(q, k, v, eta, beta, W0, M0, do, chunk: int, order: int, dW_final=None, dM_final=None,
+                           use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT, instances=None):
+    """Batched driver of lact_backward_momentum_instance: W0, M0 (and the
+    final cotangents) are triples of [BH, ...] arrays (SwiGLU) or single
+    [BH, d, d] arrays (linear); returns (dq, dk, dv, deta, dbeta) stacked and
+    dW0, dM0 stacked the same way."""
+    linear = not isinstance(W0, (tuple, list))
+    idx = range(q.shape[0]) if instances is None else instances
+    pick = (lambda a, i: a[i]) if linear else (lambda a, i: tuple(x[i] for x in a))
+    res = [lact_backward_momentum_instance(q[i], k[i], v[i], eta[i], beta[i], pick(W0, i), pick(M0, i), do[i], chunk,
+                                           order, None if dW_final is None else pick(dW_final, i),
+                                           None if dM_final is None else pick(dM_final, i), use_muon, ns_steps)
+           for i in idx]
+    cols = list(zip(*res))
+    head = tuple(np.stack(c) for c in cols[:5])
+    if linear:
+        return head + (np.stack(cols[5]), np.stack(cols[6]))
+    return head + (tuple(np.stack([r[j] for r in cols[5]]) for j in range(3)),
+                   tuple(np.stack([r[j] for r in cols[6]]) for j in range(3)))
 
 
 def lact_forward_linear(q, k, v, eta, W, chunk: int, order: int, use_muon: bool = False,

@@ -1203,3 +1203,110 @@ def test_newton_schulz_vjp_amplifies_the_null_space_by_a_per_step():
     a = O.NS_COEFFS[0]
     assert np.allclose(O.newton_schulz_vjp(G, dX, 5), a ** 5 * dX / (s + O.NS_EPS), rtol=1e-10, atol=1e-12)
     assert np.allclose(O.newton_schulz_vjp(G, dX, 2), a ** 2 * dX / (s + O.NS_EPS), rtol=1e-10, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------- momentum backward
+
+
+def _torch_momentum_layer(q, k, v, eta, beta, W, M, chunk, order, muon, linear):
+    """The chunk loop with the momentum optimizer in torch (chunk gradient by
+    autograd, bbar the chunk's mean of beta), SwiGLU or linear."""
+    n_q, n_kv = q.shape[0], k.shape[0]
+    f = (lambda W_, X: X @ W_[0].T) if linear else (lambda W_, X: _torch_swiglu_t(*W_, X))
+    outs = []
+    for s in range(0, n_kv, chunk):
+        e = min(n_kv, s + chunk)
+        if order == 0:
+            outs.append(f(W, q[s:e]))
+        if linear:
+            g = (-(v[s:e] * eta[s:e, None]).T @ k[s:e],)
+        else:
+            g = _torch_chunk_gradient(*W, k[s:e], v[s:e], eta[s:e])
+        bbar = beta[s:e].mean()
+        M = tuple(bbar * m + gj for m, gj in zip(M, g))
+        new = []
+        for w, m in zip(W, M):
+            U = w - (_torch_newton_schulz(m) if muon else m)
+            new.append(U * (torch.linalg.vector_norm(w, dim=1, keepdim=True)
+                            / torch.linalg.vector_norm(U, dim=1, keepdim=True)))
+        W = tuple(new)
+        if order == 1:
+            outs.append(f(W, q[s:e]))
+    if n_q > n_kv:
+        outs.append(f(W, q[n_kv:]))
+    return torch.cat(outs), W, M
+
+
+@pytest.mark.parametrize("linear,muon,order", [(False, False, 0), (False, True, 1), (True, False, 1), (True, True, 0)])
+def test_momentum_backward_matches_autograd(linear, muon, order):
+    rng = _rng(131 + 2 * linear + muon)
+    d, h, n_kv, n_q, C = 5, (5 if linear else 7), 15, 19, 6
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random(n_kv)
+    beta = rng.random(n_kv)
+    if linear:
+        W0 = (rng.standard_normal((d, d)),)
+        M0 = (0.1 * rng.standard_normal((d, d)),)
+    else:
+        W0 = _weights(rng, h, d, unit=True)
+        M0 = tuple(0.1 * rng.standard_normal(w.shape) for w in W0)
+    do = rng.standard_normal((n_q, d))
+    dWf = tuple(rng.standard_normal(w.shape) for w in W0)
+    dMf = tuple(rng.standard_normal(w.shape) for w in W0)
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    qt, kt, vt, et, bt = t(q), t(k), t(v), t(eta), t(beta)
+    Wt, Mt = tuple(t(w) for w in W0), tuple(t(m) for m in M0)
+    o, Wfin, Mfin = _torch_momentum_layer(qt, kt, vt, et, bt, Wt, Mt, C, order, muon, linear)
+    loss = (o * torch.tensor(do)).sum() + sum((w * torch.tensor(x)).sum() for w, x in zip(Wfin, dWf)) \
+        + sum((m * torch.tensor(x)).sum() for m, x in zip(Mfin, dMf))
+    loss.backward()
+    one = (lambda a: a[0]) if linear else (lambda a: a)
+    r = O.lact_backward_momentum_instance(q, k, v, eta, beta, one(W0), one(M0), do, C, order, one(dWf), one(dMf),
+                                          use_muon=muon)
+    for name, g, ref in zip(("dq", "dk", "dv", "deta", "dbeta"), r[:5], (qt, kt, vt, et, bt)):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-8, atol=1e-10), name
+    dW, dM = ((r[5],), (r[6],)) if linear else (r[5], r[6])
+    for a, ref in zip(dW, Wt):
+        assert np.allclose(a, ref.grad.numpy(), rtol=1e-8, atol=1e-10)
+    for a, ref in zip(dM, Mt):
+        assert np.allclose(a, ref.grad.numpy(), rtol=1e-8, atol=1e-10)
+
+
+def test_momentum_backward_at_beta_zero_is_the_plain_backward():
+    # beta = 0 and M0 = 0: every chunk's state is its own gradient, so the
+    # reverse is the plain one (dbeta is not zero: the factor still matters)
+    rng = _rng(135)
+    d, h, n, C = 4, 6, 13, 5
+    q, k, v = _tokens(rng, n, d), _tokens(rng, n, d), _tokens(rng, n, d)
+    eta = 0.1 + 0.3 * rng.random(n)
+    W0 = _weights(rng, h, d, unit=True)
+    M0 = tuple(np.zeros_like(w) for w in W0)
+    do = rng.standard_normal((n, d))
+    for muon in (False, True):
+        r = O.lact_backward_momentum_instance(q, k, v, eta, np.zeros(n), W0, M0, do, C, 1, use_muon=muon)
+        dq, dk, dv, deta, dW = O.lact_backward_instance(q, k, v, eta, *W0, do, C, 1, use_muon=muon)
+        for a, b in zip(r[:4] + tuple(r[5]), (dq, dk, dv, deta) + tuple(dW)):
+            assert np.allclose(a, b, rtol=1e-11, atol=1e-12)
+
+
+def test_momentum_backward_batched_driver_stacks_instances():
+    rng = _rng(136)
+    BH, d, h, n, C = 3, 4, 6, 9, 4
+    q, k, v = (np.stack([_tokens(rng, n, d) for _ in range(BH)]) for _ in range(3))
+    eta, beta = 0.1 + 0.3 * rng.random((BH, n)), rng.random((BH, n))
+    Ws = [_weights(rng, h, d, unit=True) for _ in range(BH)]
+    W = tuple(np.stack([w[j] for w in Ws]) for j in range(3))
+    M = tuple(0.1 * rng.standard_normal(w.shape) for w in W)
+    do = rng.standard_normal((BH, n, d))
+    got = O.lact_backward_momentum(q, k, v, eta, beta, W, M, do, C, 0, instances=[2, 0])
+    for pos, i in enumerate((2, 0)):
+        r = O.lact_backward_momentum_instance(q[i], k[i], v[i], eta[i], beta[i], tuple(w[i] for w in W),
+                                              tuple(m[i] for m in M), do[i], C, 0)
+        for a, b in zip(got[:5], r[:5]):
+            assert np.array_equal(a[pos], b)
+        for a, b in zip(got[5] + got[6], r[5] + r[6]):
+            assert np.array_equal(a[pos], b)
+    lin = O.lact_backward_momentum(q, k, v, eta, beta, W[0][:, :d, :], M[0][:, :d, :], do, C, 1, instances=[1])
+    r = O.lact_backward_momentum_instance(q[1], k[1], v[1], eta[1], beta[1], W[0][1, :d, :], M[0][1, :d, :], do[1], C, 1)
+    for a, b in zip(lin, r):
+        assert np.array_equal(a[0], b)

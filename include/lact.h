@@ -25,9 +25,10 @@
  *
  * Entry points: lact_forward (the path above), lact_forward_momentum (the
  * momentum test-time optimizer, App. A), lact_forward_schedule (a caller-given
- * list of update/apply segments, Alg. 1), lact_backward and
- * lact_backward_linear (the reverse of the chunk loop, SwiGLU and linear
- * fast weight), lact_prologue and lact_rmsnorm_out
+ * list of update/apply segments, Alg. 1), lact_backward,
+ * lact_backward_linear and lact_backward_momentum (the reverse of the chunk
+ * loop: SwiGLU and linear fast weight, and the momentum optimizer),
+ * lact_prologue and lact_rmsnorm_out
  * (the layer's steps on either side of the path, Alg. 1); per-matrix learning
  * rates through lact_desc.eta_per_matrix.
  *
@@ -300,7 +301,8 @@ int lact_backward_linear(const lact_desc* desc,
  * Backward of lact_forward for the SwiGLU fast weight (§3.1 loss, chunk
  * gradient and SwiGLU eqs.; §3.2 per-row norm-preserving update; Alg. 1),
  * with or without Muon (App. A; with Muon bf16 I/O only) and with one rate
- * per token (else LACT_EUNSUPPORTED); momentum is not differentiated. Given the cotangent dO of the outputs and optionally
+ * per token (else LACT_EUNSUPPORTED); momentum: lact_backward_momentum. Given
+ * the cotangent dO of the outputs and optionally
  * those of the final fast weights, the cotangents of every input: the
  * reverse of the chunk loop, with the weights and negated gradients of every
  * chunk recomputed by the forward's own launches and kept in the workspace.
@@ -344,6 +346,54 @@ int lact_backward(const lact_desc* desc,
                   float* dW1, float* dW2, float* dW3,
                   void* workspace, size_t workspace_bytes,
                   void* stream);
+
+/*
+ * Backward of lact_forward_momentum (§3.2 momentum optimizer, App. A;
+ * SwiGLU or linear fast weight, with or without Muon; with Muon bf16 I/O
+ * only). Chunk c advances the state as M' = bbar_c M + g_c, bbar_c the mean
+ * of beta over the chunk's tokens, and updates W' = (n / u)(W - step(M')),
+ * step the identity or Muon. Going back, the cotangent of M' is what later
+ * chunks carry back to it plus what reaches it through the step; it is the
+ * cotangent of the chunk gradient g_c (whose reverse is that of
+ * lact_backward / lact_backward_linear), bbar_c times it is carried on to M,
+ * and its inner product with M is the cotangent of bbar_c, shared equally by
+ * the chunk's tokens (dbeta). The forward's launches replay the chunk loop
+ * and keep the weights and states of every chunk in the workspace.
+ *
+ *   q, k, v, eta, beta    the forward's inputs (as lact_forward_momentum)       in
+ *   W1, W2, W3            fp32 fast weights BEFORE the forward (not written)     in
+ *   M1, M2, M3            fp32 momentum BEFORE the forward (not written)         in
+ *   dout   [B*H, n_q, d]  io_dtype, cotangent of o                               in
+ *   dW1_final .. dW3_final, dM1_final .. dM3_final  fp32 cotangents of the final
+ *                         fast weights and momentum, each may be NULL (zero)     in
+ *   dq, dk, dv, deta      as lact_backward                                       out
+ *   dbeta  [B*H, n_kv]    fp32, cotangent of beta                                out
+ *   dW1 .. dW3, dM1 .. dM3  fp32, cotangents of the initial weights and state    out
+ *   workspace   >= lact_backward_momentum_workspace_bytes(desc), 256-byte
+ *               aligned (lact_backward's, plus every chunk's state and the
+ *               chunk means of beta)
+ *
+ * With the linear fast weight only W1, M1, dW1_final, dM1_final, dW1 and dM1
+ * are used (the others are ignored). Pointers are device pointers, 16-byte
+ * aligned (eta, beta, deta, dbeta: 4); outputs must not alias inputs, each
+ * other or the workspace. Every element of the outputs is written. Errors as
+ * lact_backward; a NULL M, dM or (with n_kv > 0) beta or dbeta is
+ * LACT_EINVAL.
+ */
+size_t lact_backward_momentum_workspace_bytes(const lact_desc* desc, int* err);
+int lact_backward_momentum(const lact_desc* desc,
+                           const void* q, const void* k, const void* v, const float* eta,
+                           const float* beta,
+                           const float* W1, const float* W2, const float* W3,
+                           const float* M1, const float* M2, const float* M3,
+                           const void* dout,
+                           const float* dW1_final, const float* dW2_final, const float* dW3_final,
+                           const float* dM1_final, const float* dM2_final, const float* dM3_final,
+                           void* dq, void* dk, void* dv, float* deta, float* dbeta,
+                           float* dW1, float* dW2, float* dW3,
+                           float* dM1, float* dM2, float* dM3,
+                           void* workspace, size_t workspace_bytes,
+                           void* stream);
 
 /*
  * The layer's steps on either side of the path (Alg. 1, layer), each one pass

@@ -185,7 +185,7 @@ def make_cotangents(cfg: LactConfig, seed: int = 0, heads: list | None = None):
     cotangents, float32: ``dW`` [n, d, d] for the linear fast weight, else
     ``dW1``, ``dW3`` [n, h, d] and ``dW2`` [n, d, h] (drawn in that order);
     n = the number of kept instances."""
-    rd, rw = (np.random.default_rng(s) for s in np.random.SeedSequence([seed, 1]).spawn(2))
+    rd, rw, rm = (np.random.default_rng(s) for s in np.random.SeedSequence([seed, 1]).spawn(3))
     n = cfg.BH if heads is None else len(heads)
     std = 1.0 / np.sqrt(cfg.d)
     do = rd.standard_normal((n, cfg.n_q, cfg.d), dtype=np.float32) * np.float32(std)
@@ -193,8 +193,30 @@ def make_cotangents(cfg: LactConfig, seed: int = 0, heads: list | None = None):
         do = round_to_bf16(do)
     if cfg.linear:
         dW = rw.standard_normal((n, cfg.d, cfg.d), dtype=np.float32) * np.float32(std)
-        return dict(do=do, dW=dW)
+        out = dict(do=do, dW=dW)
+        if cfg.momentum:   # the final momentum's cotangent, dM [n, d, d]
+            out["dM"] = rm.standard_normal((n, cfg.d, cfg.d), dtype=np.float32) * np.float32(std)
+        return out
     dW1 = rw.standard_normal((n, cfg.h, cfg.d), dtype=np.float32) * np.float32(std)
     dW2 = rw.standard_normal((n, cfg.d, cfg.h), dtype=np.float32) * np.float32(std)
     dW3 = rw.standard_normal((n, cfg.h, cfg.d), dtype=np.float32) * np.float32(std)
-    return dict(do=do, dW1=dW1, dW2=dW2, dW3=dW3)
+    out = dict(do=do, dW1=dW1, dW2=dW2, dW3=dW3)
+    if cfg.momentum:   # the final momentum's cotangents dM1, dM2, dM3 (shapes of the weights)
+        for name, shape in (("dM1", (n, cfg.h, cfg.d)), ("dM2", (n, cfg.d, cfg.h)), ("dM3", (n, cfg.h, cfg.d))):
+            out[name] = rm.standard_normal(shape, dtype=np.float32) * np.float32(std)
+    return out
+
+
+def make_momentum_state(cfg: LactConfig, seed: int = 0, heads: list | None = None):
+    """A seeded momentum state to start from, float32: ``M`` [n, d, d] for the
+    linear fast weight, else ``M1``, ``M3`` [n, h, d] and ``M2`` [n, d, h].
+    Entries are N(0, 1) times 1e-3 / sqrt(d): a few chunk gradients' worth at
+    the rates of make_inputs (a chunk gradient's entries are ~1e-3 of the
+    weights' own, which are ~1 / sqrt(d))."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 2]))
+    n = cfg.BH if heads is None else len(heads)
+    sc = np.float32(1e-3 / np.sqrt(cfg.d))
+    if cfg.linear:
+        return dict(M=rng.standard_normal((n, cfg.d, cfg.d), dtype=np.float32) * sc)
+    return {name: rng.standard_normal(shape, dtype=np.float32) * sc
+            for name, shape in (("M1", (n, cfg.h, cfg.d)), ("M2", (n, cfg.d, cfg.h)), ("M3", (n, cfg.h, cfg.d)))}

@@ -667,7 +667,8 @@ def lact_backward(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final
 
 
 def lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, chunk: int, order: int, dW_final=None,
-                                    dM_final=None, use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT):
+                                    dM_final=None, use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT,
+                                    dbeta_scale: bool = False):
     """Reverse of the chunk loop with the momentum optimizer (momentum_update;
     App. A), SwiGLU (W0, M0 triples) or linear (W0, M0 single [d, d] arrays)
     fast weight, Muon optional. Per chunk c with M' = bbar_c M + g_c and
@@ -677,7 +678,10 @@ def lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, chunk: int, 
         d bbar_c = <dM', M>, shared equally by the chunk's tokens (bbar is
         their mean of beta).
     Returns (dq, dk, dv, deta, dbeta, dW0, dM0), dW0 and dM0 triples for
-    SwiGLU, single arrays for the linear fast weight.
+    SwiGLU, single arrays for the linear fast weight; with dbeta_scale also,
+    per token, |dM'| |M| / (chunk length) of its chunk (norms over the
+    matrices together): by Cauchy-Schwarz the largest |dbeta| that vectors
+    of those norms give, the scale of dbeta's rounding error.
     """
     linear = not isinstance(W0, (tuple, list))
     q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
@@ -708,7 +712,7 @@ def lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, chunk: int, 
     dM = [np.zeros_like(m) for m in M] if dM_final is None else [
         np.asarray(x, dtype=np.float64).copy() for x in tup(dM_final)]
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
-    deta, dbeta = np.zeros(n_kv), np.zeros(n_kv)
+    deta, dbeta, bscale = np.zeros(n_kv), np.zeros(n_kv), np.zeros(n_kv)
 
     def apply_back(Wc, s, e):
         r = apply_vjp(Wc, q[s:e], do[s:e])
@@ -737,32 +741,39 @@ def lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, chunk: int, 
             for j, b in enumerate((b1, b2, b3)):
                 dW[j] += b
         dbeta[s:e] = sum(float(np.sum(a * m)) for a, m in zip(dMt, Ms[c])) / (e - s)
+        bscale[s:e] = np.sqrt(sum(float(np.sum(a * a)) for a in dMt) *
+                              sum(float(np.sum(m * m)) for m in Ms[c])) / (e - s)
         dM = [bbars[c] * a for a in dMt]
         if order == 0:
             apply_back(Ws[c], s, e)
     out = (lambda t: t[0]) if linear else tuple
-    return dq, dk, dv, deta, dbeta, out(dW), out(dM)
+    res = (dq, dk, dv, deta, dbeta, out(dW), out(dM))
+    return res + (bscale,) if dbeta_scale else res
 
 
 def lact_backward_momentum(q, k, v, eta, beta, W0, M0, do, chunk: int, order: int, dW_final=None, dM_final=None,
-                           use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT, instances=None):
+                           use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT, instances=None,
+                           dbeta_scale: bool = False):
     """Batched driver of lact_backward_momentum_instance: W0, M0 (and the
     final cotangents) are triples of [BH, ...] arrays (SwiGLU) or single
     [BH, d, d] arrays (linear); returns (dq, dk, dv, deta, dbeta) stacked and
-    dW0, dM0 stacked the same way."""
+    dW0, dM0 stacked the same way (and the stacked dbeta scales with
+    dbeta_scale)."""
     linear = not isinstance(W0, (tuple, list))
     idx = range(q.shape[0]) if instances is None else instances
     pick = (lambda a, i: a[i]) if linear else (lambda a, i: tuple(x[i] for x in a))
     res = [lact_backward_momentum_instance(q[i], k[i], v[i], eta[i], beta[i], pick(W0, i), pick(M0, i), do[i], chunk,
                                            order, None if dW_final is None else pick(dW_final, i),
-                                           None if dM_final is None else pick(dM_final, i), use_muon, ns_steps)
+                                           None if dM_final is None else pick(dM_final, i), use_muon, ns_steps,
+                                           dbeta_scale)
            for i in idx]
     cols = list(zip(*res))
     head = tuple(np.stack(c) for c in cols[:5])
+    tail = (np.stack(cols[7]),) if dbeta_scale else ()
     if linear:
-        return head + (np.stack(cols[5]), np.stack(cols[6]))
+        return head + (np.stack(cols[5]), np.stack(cols[6])) + tail
     return head + (tuple(np.stack([r[j] for r in cols[5]]) for j in range(3)),
-                   tuple(np.stack([r[j] for r in cols[6]]) for j in range(3)))
+                   tuple(np.stack([r[j] for r in cols[6]]) for j in range(3))) + tail
 
 
 def lact_forward_linear(q, k, v, eta, W, chunk: int, order: int, use_muon: bool = False,

@@ -74,6 +74,10 @@ def load_library(path: str | None = None):
     L.lact_backward_linear.restype = i32
     L.lact_backward.argtypes = [dp] + [vp] * 19 + [sz, vp]
     L.lact_backward.restype = i32
+    L.lact_backward_momentum_workspace_bytes.argtypes = [dp, ctypes.POINTER(i32)]
+    L.lact_backward_momentum_workspace_bytes.restype = sz
+    L.lact_backward_momentum.argtypes = [dp] + [vp] * 30 + [sz, vp]
+    L.lact_backward_momentum.restype = i32
     f32 = ctypes.c_float
     L.lact_prologue.argtypes = [dp, vp, vp, f32, vp, vp, vp, vp, vp, vp, vp]
     L.lact_prologue.restype = i32
@@ -359,6 +363,78 @@ def backward(q, k, v, eta, W1, W2, W3, dout, chunk, order=APPLY_THEN_UPDATE, dW_
     if rc:
         _raise(rc)
     return res
+
+
+def backward_momentum_workspace_bytes(desc: LactDesc) -> int:
+    err = ctypes.c_int(0)
+    n = lib().lact_backward_momentum_workspace_bytes(ctypes.byref(desc), ctypes.byref(err))
+    if err.value:
+        _raise(err.value)
+    return int(n)
+
+
+def backward_momentum(q, k, v, eta, beta, W0, M0, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None,
+                      dM_final=None, use_muon=False, ns_steps=5, out=None, workspace=None, stream=None):
+    """Backward of the momentum optimizer's path (lact_backward_momentum).
+
+    W0, M0: the fast weights and momentum before the forward (fp32, not
+    written): triples (W1, W2, W3), (M1, M2, M3) for SwiGLU, single [.., d, d]
+    tensors for the linear fast weight; dW_final, dM_final the same (any of
+    them None: zero). Returns (dq, dk, dv, deta, dbeta, dW0, dM0) with dW0,
+    dM0 shaped like W0, M0; written into ``out`` (that tuple) when given."""
+    import torch
+    linear = not isinstance(W0, (tuple, list))
+    Ws = (W0,) if linear else tuple(W0)
+    Ms = (M0,) if linear else tuple(M0)
+    nm = len(Ws)
+    if nm not in (1, 3) or len(Ms) != nm:
+        raise LactError(-1, "W0 and M0: three tensors (SwiGLU) or one (linear)")
+    if linear and W0.shape[-1] != W0.shape[-2]:
+        raise LactError(-1, "the linear fast weight is square, [.., d, d]")
+    dWf = (None,) * nm if dW_final is None else ((dW_final,) if linear else tuple(dW_final))
+    dMf = (None,) * nm if dM_final is None else ((dM_final,) if linear else tuple(dM_final))
+    if len(dWf) != nm or len(dMf) != nm:
+        raise LactError(-1, "dW_final and dM_final must match W0")
+    for t, ref in zip(Ms + dWf + dMf, Ws * 3):
+        if t is not None and (t.shape != ref.shape or t.dtype != torch.float32):
+            raise LactError(-1, "momentum and final cotangents must have the fast weights' shapes, fp32")
+    if dout.shape != q.shape or dout.dtype != q.dtype:
+        raise LactError(-1, "dout must have q's shape and dtype")
+    if beta.numel() != k.numel() // k.shape[-1] or beta.dtype != torch.float32:
+        raise LactError(-1, "beta must be [.., n_kv] fp32")
+    extra = [(beta, "beta")] + [(t, "M") for t in Ms] + [(t, "d_final") for t in dWf + dMf if t is not None]
+    W1, W2, W3 = (Ws[0],) * 3 if linear else Ws
+    desc, dq, _, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk, order, use_muon, ns_steps,
+                                   None if out is None else out[0], None, stream,
+                                   FW_LINEAR if linear else FW_SWIGLU, need_workspace=False)
+    if not dout.is_cuda or not dout.is_contiguous():
+        raise LactError(-1, "dout must be a contiguous device tensor")
+    if workspace is None:
+        workspace = torch.empty(max(backward_momentum_workspace_bytes(desc), 1), dtype=torch.uint8, device=q.device)
+    if out is None:
+        dW = tuple(torch.empty_like(w) for w in Ws)
+        dM = tuple(torch.empty_like(m) for m in Ms)
+        head = (dq, torch.empty_like(k), torch.empty_like(v), torch.empty_like(eta), torch.empty_like(beta))
+    else:
+        head = tuple(out[:5])
+        dW = (out[5],) if linear else tuple(out[5])
+        dM = (out[6],) if linear else tuple(out[6])
+        refs = (q, k, v, eta, beta) + Ws + Ms
+        for t, ref in zip(head + dW + dM, refs):
+            if t.shape != ref.shape or t.dtype != ref.dtype or not t.is_cuda or not t.is_contiguous():
+                raise LactError(-1, "outputs must be contiguous device tensors shaped like their inputs")
+    pad = (lambda xs: tuple(xs) + (None,) * (3 - len(xs)))
+    args = ([_ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(beta)] + [_ptr(t) for t in pad(Ws)] +
+            [_ptr(t) for t in pad(Ms)] + [_ptr(dout)] + [_ptr(t) for t in pad(dWf)] + [_ptr(t) for t in pad(dMf)] +
+            [_ptr(t) for t in head[:4]] + [_ptr(head[4])] + [_ptr(t) for t in pad(dW)] + [_ptr(t) for t in pad(dM)])
+    rc = lib().lact_backward_momentum(ctypes.byref(desc), *args, _ptr(workspace),
+                                      ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                                      ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    if linear:
+        return head + (dW[0], dM[0])
+    return head + (dW, dM)
 
 
 def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_steps=5, beta=None,

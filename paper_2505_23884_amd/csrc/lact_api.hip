@@ -1168,6 +1168,28 @@ struct NsBwd {
     }
     return timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_copies_f32(cs, p.nmat, p.BH, s); });
   }
+  // the same from per-matrix slabs ([BH][R x L] each)
+  int gather_slabs(const float* const src[3], float sign, float* wide) const {
+    CopySeg cs[3] = {};
+    for (int j = 0; j < p.nmat; ++j) {
+      CopySeg& c = cs[j];
+      c.W = src[j];
+      c.w_inst = (int64_t)R[j] * L[j];
+      c.R = R[j];
+      c.L = L[j];
+      c.sign = sign;
+      if (tall(j)) {
+        c.dstT = wide + j * mn();
+        c.ldT = R[j];
+        c.dstT_inst = p.nmat * mn();
+      } else {
+        c.dst = wide + j * mn();
+        c.ld = L[j];
+        c.dst_inst = p.nmat * mn();
+      }
+    }
+    return timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_copies_f32(cs, p.nmat, p.BH, s); });
+  }
   int scatter(const float* wide, float sign, float* dst) const {
     CopySeg cs[3] = {};
     const int64_t dh = (int64_t)p.d * p.h;
@@ -1265,11 +1287,12 @@ struct NsBwd {
   _Float16* B16(int k) const { return at<_Float16>(N.b16) + (size_t)k * N.S * mm(); }
 
   // The step -Muon(g) of the gradient whose negated split partials are
-  // P (stored layout), into pstep (stored layout, one split).
-  int forward(const float* P, int nsplit, int64_t split) const {
+  // P (stored layout), into pstep (stored layout, one split); with slabs,
+  // of the momentum state in per-matrix slabs instead.
+  int forward(const float* P, int nsplit, int64_t split, const float* const* slabs = nullptr) const {
     float* G = at<float>(N.g);
     float* X = at<float>(N.x32);
-    int rc = gather(P, nsplit, split, -1.0f, G);
+    int rc = slabs ? gather_slabs(slabs, 1.0f, G) : gather(P, nsplit, split, -1.0f, G);
     if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_slot_dot(G, G, N.S, mn(), at<float>(N.nrm), s); });
     if (!rc) rc = lin(0, G, nullptr, nullptr, nullptr, at<float>(N.nrm), nullptr, 0.f, X, steps > 0 ? X16(0) : nullptr);
     for (int k = 0; k < steps && !rc; ++k) {
@@ -1344,9 +1367,13 @@ struct BwdLayout {
   int64_t tail_len;     // tokens per piece of the apply-only tail
   int64_t tail_split;   // tokens per split of a tail piece (at most p.nsplit splits)
   size_t off_ek, off_P, off_A, off_traj, off_wt, off_tail, off_ub, off_ut, total;
+  bool mom;             // momentum: the state's trajectory, chunk means, buffers of its reverse
+  size_t off_mtraj, off_bbar_all, off_mu, off_mpart;
 };
 
-int bwd_layout(const lact_desc* dsc, BwdLayout* L) {
+constexpr int kMomBlocks = 64;   // workgroups per instance of the momentum reverse
+
+int bwd_layout(const lact_desc* dsc, BwdLayout* L, bool mom = false) {
   int rc = check_desc(dsc);
   if (rc) return rc;
   if (dsc->fast_weight != LACT_FW_LINEAR) return LACT_EUNSUPPORTED;
@@ -1383,6 +1410,17 @@ int bwd_layout(const lact_desc* dsc, BwdLayout* L) {
   L->off_ut = o;
   o = align_up(o + wio);
   if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns);
+  L->mom = mom;
+  if (mom) {
+    L->off_mtraj = o;
+    o = align_up(o + (size_t)L->nch * w4);
+    L->off_bbar_all = o;
+    o = align_up(o + (size_t)p.BH * std::max<int64_t>(L->nch, 1) * 4);
+    L->off_mu = o;
+    o = align_up(o + w4);
+    L->off_mpart = o;
+    o = align_up(o + (size_t)p.BH * kMomBlocks * 4);
+  }
   L->total = std::max<size_t>(o, kAlign);
   return LACT_OK;
 }
@@ -1432,13 +1470,24 @@ int lin_launch(const Plan& p, hipStream_t s, BwdArgs& b, int nseg, double flops)
   return timed(LACT_KCLASS_BWD, flops, s, [&] { return launch_bwd(b, p.bf16, s); });
 }
 
+// With M0 != nullptr: the momentum optimizer (beta the per-token factors,
+// dMf the final state's cotangent or nullptr, dbeta and dM0 the outputs).
 int run_backward_linear(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
                         const float* W0, const void* dout, const float* dWf, void* dq, void* dk, void* dv,
-                        float* deta, float* dW0, void* workspace, size_t workspace_bytes, void* stream) {
+                        float* deta, float* dW0, void* workspace, size_t workspace_bytes, void* stream,
+                        const float* beta = nullptr, const float* M0 = nullptr, const float* dMf = nullptr,
+                        float* dbeta = nullptr, float* dM0 = nullptr) {
+  const bool mom = M0 != nullptr;
   BwdLayout L;
-  int rc = bwd_layout(desc, &L);
+  int rc = bwd_layout(desc, &L, mom);
   if (rc) return rc;
   const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
+  if (mom) {
+    if (!dM0) return LACT_EINVAL;
+    if (any_kv && (!beta || !dbeta)) return LACT_EINVAL;
+    if (misaligned(M0) || misaligned(dM0) || (dMf && misaligned(dMf))) return LACT_EALIGN;
+    if (any_kv && (((uintptr_t)beta & 3) || ((uintptr_t)dbeta & 3))) return LACT_EALIGN;
+  }
   if (!W0 || !dW0) return LACT_EINVAL;
   if (any_q && (!q || !dout || !dq)) return LACT_EINVAL;
   if (any_kv && (!k || !v || !eta || !dk || !dv || !deta)) return LACT_EINVAL;
@@ -1466,6 +1515,25 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     return i == 0 ? const_cast<float*>(W0) : reinterpret_cast<float*>(ws + L.off_traj + (size_t)(i - 1) * w4);
   };
   auto wt = [&](int64_t i) -> uint8_t* { return ws + L.off_wt + (size_t)i * wio; };
+  auto mtraj = [&](int64_t i) -> float* {   // momentum state entering chunk i
+    return i == 0 ? const_cast<float*>(M0) : reinterpret_cast<float*>(ws + L.off_mtraj + (size_t)(i - 1) * w4);
+  };
+  float* bbar_all = mom ? reinterpret_cast<float*>(ws + L.off_bbar_all) : nullptr;
+  float* mu = mom ? reinterpret_cast<float*>(ws + L.off_mu) : nullptr;
+  if (mom && L.nch > 0) {   // every chunk's mean of beta, [BH][nch]
+    BetaArgs ba{};
+    ba.beta = beta;
+    ba.n_kv = n_kv;
+    ba.chunk = C;
+    ba.t0 = 0;
+    ba.end = n_kv;
+    ba.nchunks = (int)L.nch;
+    ba.BH = p.BH;
+    ba.bbar = bbar_all;
+    ba.stride = (int)L.nch;
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_beta_mean(ba, s); });
+    if (rc) return rc;
+  }
   // eta k of every key token, then P_c and A_c of every chunk
   if (any_kv) {
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
@@ -1497,15 +1565,32 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     }
   }
   // W_{c+1} = rows of W_c + P_c (or, with Muon, W_c - Muon(g_c)) rescaled to
-  // W_c's row norms
+  // W_c's row norms; with momentum the step is M_{c+1} = bbar_c M_c + g_c
+  // (or Muon of it)
   for (int64_t ci = 0; ci < L.nch; ++ci) {
     UpdArgs u{};
     u.W[0] = traj(ci + 1);
     u.Wsrc[0] = traj(ci);
     u.step = Pall + ci * psplit;
+    if (mom && !p.muon) {   // the update advances the state in place, in its trajectory slot
+      rc = timed(LACT_KCLASS_PREP, 0.0, s,
+                 [&] { return hipMemcpyAsync(mtraj(ci + 1), mtraj(ci), w4, hipMemcpyDeviceToDevice, s); });
+      if (rc) return rc;
+      u.M[0] = mtraj(ci + 1);
+      u.bbar = bbar_all + ci;
+      u.bbar_stride = (int)L.nch;
+    }
     if (p.muon) {
       const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}};
-      rc = nb.forward(Pall + ci * psplit, 1, psplit);
+      const float* slab[3] = {mtraj(ci + 1), nullptr, nullptr};
+      if (mom) {
+        rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+          return launch_mom_adv(mtraj(ci), bbar_all + ci, L.nch, PartSet{Pall + ci * psplit, 1, psplit, dd},
+                                mtraj(ci + 1), p.BH, dd, s);
+        });
+        if (rc) return rc;
+      }
+      rc = nb.forward(Pall + ci * psplit, 1, psplit, mom ? slab : nullptr);
       if (rc) return rc;
       u.step = nb.at<float>(L.ns.pstep);
     }
@@ -1562,20 +1647,27 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
                [&] { return launch_accum(G, dd, dWf, dd, dWf ? 1 : 0, PartSet{}, PartSet{}, p.BH, dd, s); });
     if (rc) return rc;
   }
+  if (mom) {   // the final state's cotangent, or zero
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
+               [&] { return launch_accum(dM0, dd, dMf, dd, dMf ? 1 : 0, PartSet{}, PartSet{}, p.BH, dd, s); });
+    if (rc) return rc;
+  }
   const bool then_apply = desc->order == LACT_UPDATE_THEN_APPLY;
   uint8_t* ub = ws + L.off_ub;
   uint8_t* ut = ws + L.off_ut;
   for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
     const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
     const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}};
-    if (p.muon) {   // the step is Muon(g): replay the iteration into its negation
-      rc = nb.forward(Pall + ci * psplit, 1, psplit);
+    const float* slab[3] = {mom ? mtraj(ci + 1) : nullptr, nullptr, nullptr};
+    if (p.muon) {   // the step is Muon(g), or Muon(M_{c+1}): replay the iteration into its negation
+      rc = nb.forward(Pall + ci * psplit, 1, psplit, mom ? slab : nullptr);
       if (rc) return rc;
     }
     VjpArgs va{};
     va.W = traj(ci);
     va.w_inst = dd;
-    va.P = p.muon ? PartSet{nb.at<float>(L.ns.pstep), 1, psplit, dd} : PartSet{Pall + ci * psplit, 1, psplit, dd};
+    va.P = p.muon ? PartSet{nb.at<float>(L.ns.pstep), 1, psplit, dd}
+                  : (mom ? PartSet{mtraj(ci + 1), 1, 0, dd, -1.0f} : PartSet{Pall + ci * psplit, 1, psplit, dd});
     const PartSet ac{Aall + ci * psplit, 1, psplit, dd};
     if (then_apply) va.pre[0] = ac;   // applied with the weights leaving the chunk
     else va.post = ac;
@@ -1590,17 +1682,38 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     va.BH = p.BH;
     va.R = p.d;
     va.L = p.d;
-    if (p.muon) {   // the update's cotangent in fp32 for the Newton-Schulz reverse
+    if (p.muon || mom) {   // the update's cotangent in fp32 (Newton-Schulz or momentum reverse next)
       va.Ub = va.UT = nullptr;
-      va.U32 = nb.at<float>(L.ns.ustep);
+      va.U32 = p.muon ? nb.at<float>(L.ns.ustep) : mu;
       va.u32_inst = dd;
     }
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(&va, 1, p.bf16, s); });
     if (rc) return rc;
-    if (p.muon) {   // the gradient's cotangent (negated) in the operand layouts
+    if (p.muon) {
       rc = nb.reverse();
       if (rc) return rc;
-      const CopySeg cs{nb.at<float>(L.ns.ug), dd, p.d, p.d, ub, d, dd, ut, d, dd};
+    }
+    const float* ug = p.muon ? nb.at<float>(L.ns.ug) : mu;
+    if (mom) {   // dM' = carried - (step's share); the gradient's cotangent; carry bbar dM'; dbeta
+      MomBwdArgs ma{};
+      ma.U = const_cast<float*>(ug);
+      ma.R[0] = dM0;
+      ma.M[0] = mtraj(ci);
+      ma.bbar = bbar_all + ci;
+      ma.bbar_inst = L.nch;
+      ma.part = reinterpret_cast<float*>(ws + L.off_mpart);
+      ma.BH = p.BH;
+      ma.nmat = 1;
+      ma.nblk = kMomBlocks;
+      ma.dh = dd;
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_mom_bwd(ma, s); });
+      if (!rc) rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+        return launch_mom_dbeta(ma.part, kMomBlocks, p.BH, dbeta + s0, n_kv, n, s);
+      });
+      if (rc) return rc;
+    }
+    if (p.muon || mom) {   // the gradient's cotangent (negated) in the operand layouts
+      const CopySeg cs{ug, dd, p.d, p.d, ub, d, dd, ut, d, dd};
       rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_copies(&cs, 1, p.BH, p.bf16, s); });
       if (rc) return rc;
     }
@@ -1645,6 +1758,8 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
 struct SwBwdLayout {
   Plan p;               // the forward's plan without the fused gradient-and-update kind
   NsBwdLayout ns;       // with Muon: the Newton-Schulz reverse's buffers
+  bool mom;             // momentum: the state's trajectory, chunk means, buffers of its reverse
+  size_t off_mtraj, off_bbar_all, off_mu, off_mpart;
   int64_t nch;          // chunks of the forward
   int64_t T;            // token rows of the chunk buffers (a chunk, or a piece of the tail)
   int64_t tail_split;   // tokens per split of a tail piece (at most p.nsplit splits)
@@ -1653,7 +1768,7 @@ struct SwBwdLayout {
       off_ur[3], off_apart, off_bpart, total;
 };
 
-int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L) {
+int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false) {
   int rc = check_desc(dsc);
   if (rc) return rc;
   if (dsc->fast_weight != LACT_FW_SWIGLU || dsc->eta_per_matrix) return LACT_EUNSUPPORTED;
@@ -1693,18 +1808,37 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L) {
   L->off_apart = take((size_t)p.nsplit * 3 * w4);
   L->off_bpart = take((size_t)p.nsplit * 3 * w4);
   if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns);
+  L->mom = mom;
+  if (mom) {
+    L->off_mtraj = take((size_t)L->nch * 3 * w4);
+    L->off_bbar_all = take((size_t)p.BH * std::max<int64_t>(L->nch, 1) * 4);
+    L->off_mu = take(3 * w4);
+    L->off_mpart = take((size_t)p.BH * kMomBlocks * 4);
+  }
   L->total = o;
   return LACT_OK;
 }
 
+// With beta != nullptr: the momentum optimizer (M0 the initial state, dMf
+// the final state's cotangents or nullptr, dbeta and dM the outputs).
 int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
                         const float* const W0[3], const void* dout, const float* const dWf[3], void* dq, void* dk,
                         void* dv, float* deta, float* const dW[3], void* workspace, size_t workspace_bytes,
-                        void* stream) {
+                        void* stream, const float* beta = nullptr, const float* const* M0 = nullptr,
+                        const float* const* dMf = nullptr, float* dbeta = nullptr, float* const* dMo = nullptr) {
+  const bool mom = M0 != nullptr;
   SwBwdLayout L;
-  int rc = sw_bwd_layout(desc, &L);
+  int rc = sw_bwd_layout(desc, &L, mom);
   if (rc) return rc;
   const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
+  if (mom) {
+    for (int m = 0; m < 3; ++m) {
+      if (!M0[m] || !dMo[m]) return LACT_EINVAL;
+      if (misaligned(M0[m]) || misaligned(dMo[m]) || (dMf[m] && misaligned(dMf[m]))) return LACT_EALIGN;
+    }
+    if (any_kv && (!beta || !dbeta)) return LACT_EINVAL;
+    if (any_kv && (((uintptr_t)beta & 3) || ((uintptr_t)dbeta & 3))) return LACT_EALIGN;
+  }
   for (int m = 0; m < 3; ++m) {
     if (!W0[m] || !dW[m]) return LACT_EINVAL;
     if (misaligned(W0[m]) || misaligned(dW[m]) || (dWf[m] && misaligned(dWf[m]))) return LACT_EALIGN;
@@ -1719,8 +1853,10 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
   Ctx c;
   // the forward's context; its updates read W_c and write W_{c+1} in the
   // trajectory, never W0
-  rc = setup(c, desc, q, k, v, eta, nullptr, const_cast<float*>(W0[0]), const_cast<float*>(W0[1]),
-             const_cast<float*>(W0[2]), nullptr, dq, workspace, workspace_bytes, stream);
+  float* const Mseed[3] = {mom ? const_cast<float*>(M0[0]) : nullptr, mom ? const_cast<float*>(M0[1]) : nullptr,
+                           mom ? const_cast<float*>(M0[2]) : nullptr};
+  rc = setup(c, desc, q, k, v, eta, mom ? beta : nullptr, const_cast<float*>(W0[0]), const_cast<float*>(W0[1]),
+             const_cast<float*>(W0[2]), mom ? Mseed : nullptr, dq, workspace, workspace_bytes, stream);
   if (rc) return rc;
   c.p = L.p;
   const Plan& p = c.p;
@@ -1734,10 +1870,27 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     return i == 0 ? const_cast<float*>(W0[m])
                   : reinterpret_cast<float*>(ws + L.off_traj + ((size_t)(i - 1) * 3 + m) * w4);
   };
+  auto mtraj = [&](int64_t i, int m) -> float* {   // momentum state entering chunk i
+    return i == 0 ? const_cast<float*>(M0[m])
+                  : reinterpret_cast<float*>(ws + L.off_mtraj + ((size_t)(i - 1) * 3 + m) * w4);
+  };
   rc = prepare_weights(c);
   if (rc) return rc;
   for (int64_t ci = 0; ci < L.nch; ++ci) {
     const int64_t s0 = ci * C, s1 = std::min(n_kv, s0 + C);
+    if (mom) {   // the state advances in place in its trajectory slot
+      if (ci % kBetaBatch == 0) {
+        c.chunk_idx = ci;
+        rc = beta_means(c, s0, C, n_kv, (int)std::min<int64_t>(kBetaBatch, L.nch - ci));
+        if (rc) return rc;
+      }
+      for (int m = 0; m < 3; ++m) {
+        rc = timed(LACT_KCLASS_PREP, 0.0, c.s,
+                   [&] { return hipMemcpyAsync(mtraj(ci + 1, m), mtraj(ci, m), w4, hipMemcpyDeviceToDevice, c.s); });
+        if (rc) return rc;
+        c.M[m] = mtraj(ci + 1, m);
+      }
+    }
     for (int m = 0; m < 3; ++m) {
       c.W[m] = traj(ci + 1, m);
       c.Wsrc[m] = traj(ci, m);
@@ -1759,6 +1912,29 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     if (rc) return rc;
   }
   c.p.off_step = L.p.off_step;
+  float* bbar_all = mom ? reinterpret_cast<float*>(ws + L.off_bbar_all) : nullptr;
+  if (mom && L.nch > 0) {   // every chunk's mean of beta, [BH][nch]
+    BetaArgs ba{};
+    ba.beta = beta;
+    ba.n_kv = n_kv;
+    ba.chunk = C;
+    ba.t0 = 0;
+    ba.end = n_kv;
+    ba.nchunks = (int)L.nch;
+    ba.BH = p.BH;
+    ba.bbar = bbar_all;
+    ba.stride = (int)L.nch;
+    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_beta_mean(ba, s); });
+    if (rc) return rc;
+  }
+  if (mom) {   // the final state's cotangent, or zero
+    for (int m = 0; m < 3; ++m) {
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+        return launch_accum(dMo[m], dh, dMf[m], dh, dMf[m] ? 1 : 0, PartSet{}, PartSet{}, p.BH, dh, s);
+      });
+      if (rc) return rc;
+    }
+  }
   const uint8_t* qb = (const uint8_t*)q;
   const uint8_t* kb = (const uint8_t*)k;
   const uint8_t* vb = (const uint8_t*)v;
@@ -1932,8 +2108,10 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     // the update's reverse: W1, W3 ([h x d]) and W2 ([d x h]) in one launch
     const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {(int)h, (int)d, (int)h}, {(int)d, (int)h, (int)d}};
     float* gslot = reinterpret_cast<float*>(ws + L.off_P + (size_t)ci * L.slotP);
-    if (p.muon) {   // the steps are Muon(g_j): replay the iteration into their negation
-      rc = nb.forward(gslot, p.nsplit, psplit);
+    const float* mnext[3] = {mom ? mtraj(ci + 1, 0) : nullptr, mom ? mtraj(ci + 1, 1) : nullptr,
+                             mom ? mtraj(ci + 1, 2) : nullptr};
+    if (p.muon) {   // the steps are Muon(g_j), or Muon(M_j) with momentum: replay the iteration
+      rc = nb.forward(gslot, p.nsplit, psplit, mom ? mnext : nullptr);
       if (rc) return rc;
     }
     VjpArgs va[3] = {};
@@ -1942,7 +2120,8 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       const bool w2 = m == 1;
       x.W = traj(ci, m);
       x.w_inst = dh;
-      x.P = p.muon ? pset(nb.at<float>(L.ns.pstep), 1, m) : pset(gslot, p.nsplit, m);
+      x.P = p.muon ? pset(nb.at<float>(L.ns.pstep), 1, m)
+                   : (mom ? PartSet{mnext[m], 1, 0, dh, -1.0f} : pset(gslot, p.nsplit, m));
       if (b_pending) x.pre[0] = pset(bpart, b_ns, m);
       if (a_pending) x.pre[1] = pset(apart, a_ns, m);
       x.G = dW[m];
@@ -1965,18 +2144,40 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       x.BH = p.BH;
       x.R = (int)(w2 ? d : h);
       x.L = (int)(w2 ? h : d);
-      if (p.muon) {   // the update's cotangent in fp32 for the Newton-Schulz reverse
+      if (p.muon || mom) {   // the update's cotangent in fp32 (Newton-Schulz or momentum reverse next)
         x.Ub = x.UT = nullptr;
-        x.U32 = nb.at<float>(L.ns.ustep) + m * dh;
+        x.U32 = (p.muon ? nb.at<float>(L.ns.ustep) : reinterpret_cast<float*>(ws + L.off_mu)) + m * dh;
         x.u32_inst = 3 * dh;
       }
     }
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_vjp(va, 3, p.bf16, s); });
     if (rc) return rc;
-    if (p.muon) {   // the gradients' cotangents (negated) into the operand layouts
+    if (p.muon) {
       rc = nb.reverse();
       if (rc) return rc;
-      const float* ug = nb.at<float>(L.ns.ug);
+    }
+    if (mom) {   // dM' = carried - (step's share); the gradient's cotangent; carry bbar dM'; dbeta
+      MomBwdArgs ma{};
+      ma.U = p.muon ? nb.at<float>(L.ns.ug) : reinterpret_cast<float*>(ws + L.off_mu);
+      for (int m = 0; m < 3; ++m) {
+        ma.R[m] = dMo[m];
+        ma.M[m] = mtraj(ci, m);
+      }
+      ma.bbar = bbar_all + ci;
+      ma.bbar_inst = L.nch;
+      ma.part = reinterpret_cast<float*>(ws + L.off_mpart);
+      ma.BH = p.BH;
+      ma.nmat = 3;
+      ma.nblk = kMomBlocks;
+      ma.dh = dh;
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_mom_bwd(ma, s); });
+      if (!rc) rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+        return launch_mom_dbeta(ma.part, kMomBlocks, p.BH, dbeta + s0, n_kv, n, s);
+      });
+      if (rc) return rc;
+    }
+    if (p.muon || mom) {   // the gradients' cotangents (negated) into the operand layouts
+      const float* ug = p.muon ? nb.at<float>(L.ns.ug) : reinterpret_cast<float*>(ws + L.off_mu);
       const CopySeg cs[3] = {{ug, 3 * dh, (int)h, (int)d, ur[0], d, dh, bk + h * esz, 4 * h, d * 4 * h},
                              {ug + 2 * dh, 3 * dh, (int)h, (int)d, ur[1], d, dh, bk, 4 * h, d * 4 * h},
                              {ug + dh, 3 * dh, (int)d, (int)h, bv, 2 * h, d * 2 * h, ur[2], d, dh}};
@@ -2082,6 +2283,45 @@ size_t lact_backward_workspace_bytes(const lact_desc* desc, int* err) {
   }
   if (err) *err = rc;
   return rc ? 0 : total;
+}
+
+size_t lact_backward_momentum_workspace_bytes(const lact_desc* desc, int* err) {
+  int rc = check_desc(desc);
+  size_t total = 0;
+  if (!rc && desc->fast_weight == LACT_FW_LINEAR) {
+    BwdLayout L;
+    rc = bwd_layout(desc, &L, true);
+    total = L.total;
+  } else if (!rc) {
+    SwBwdLayout L;
+    rc = sw_bwd_layout(desc, &L, true);
+    total = L.total;
+  }
+  if (err) *err = rc;
+  return rc ? 0 : total;
+}
+
+int lact_backward_momentum(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
+                           const float* beta, const float* W1, const float* W2, const float* W3, const float* M1,
+                           const float* M2, const float* M3, const void* dout, const float* dW1_final,
+                           const float* dW2_final, const float* dW3_final, const float* dM1_final,
+                           const float* dM2_final, const float* dM3_final, void* dq, void* dk, void* dv,
+                           float* deta, float* dbeta, float* dW1, float* dW2, float* dW3, float* dM1, float* dM2,
+                           float* dM3, void* workspace, size_t workspace_bytes, void* stream) {
+  const int rc = check_desc(desc);
+  if (rc) return rc;
+  if (!M1 || !dM1) return LACT_EINVAL;   // the entry point's state and its cotangent
+  if (desc->fast_weight == LACT_FW_LINEAR)
+    return run_backward_linear(desc, q, k, v, eta, W1, dout, dW1_final, dq, dk, dv, deta, dW1, workspace,
+                               workspace_bytes, stream, beta, M1, dM1_final, dbeta, dM1);
+  const float* W0[3] = {W1, W2, W3};
+  const float* dWf[3] = {dW1_final, dW2_final, dW3_final};
+  float* const dW[3] = {dW1, dW2, dW3};
+  const float* M0[3] = {M1, M2, M3};
+  const float* dMf[3] = {dM1_final, dM2_final, dM3_final};
+  float* const dMo[3] = {dM1, dM2, dM3};
+  return run_backward_swiglu(desc, q, k, v, eta, W0, dout, dWf, dq, dk, dv, deta, dW, workspace, workspace_bytes,
+                             stream, beta, M0, dMf, dbeta, dMo);
 }
 
 int lact_backward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,

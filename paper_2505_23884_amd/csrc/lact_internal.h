@@ -194,7 +194,7 @@ struct BetaArgs {
   const float* beta;    // [BH][n_kv]
   int64_t n_kv, chunk;
   int64_t t0, end;      // first token of chunk 0; bound of the last chunk
-  int nchunks;          // <= kBetaBatch
+  int nchunks;          // the forward's batches: <= kBetaBatch; the backward: every chunk
   int BH;
   float* bbar;
   int stride;
@@ -298,6 +298,7 @@ struct PartSet {
   const float* p;
   int n;
   int64_t split, inst;
+  float sign;   // factor of the sum (0: 1)
 };
 
 // Reverse of W' = (n / u) U, U = W + sum P, per row of a [R x L] matrix.
@@ -359,6 +360,26 @@ hipError_t launch_sym(const _Float16* X, float alpha, const _Float16* Y, float b
 // multiple of 4); base: 0 (mode 0), init (mode 1) or G itself (mode 2).
 hipError_t launch_accum(float* G, int64_t g_inst, const float* init, int64_t i_inst, int mode, PartSet s0, PartSet s1,
                         int BH, int64_t RL, hipStream_t s);
+// Momentum reverse of one chunk (M' = bbar M + g): U holds minus the
+// cotangent that reaches M' through the update's step ([inst][nmat][dh]); R
+// (per matrix [BH][dh]) the cotangent carried from later chunks. With
+// dM' = R - U: U <- -dM' (the gradient's cotangent, negated), R <- bbar dM',
+// and part[inst * nblk + b] the block's share of <dM', M> (M per matrix).
+struct MomBwdArgs {
+  float* U;
+  float* R[3];
+  const float* M[3];
+  const float* bbar; int64_t bbar_inst;
+  float* part;
+  int BH, nmat, nblk;
+  int64_t dh;
+};
+hipError_t launch_mom_bwd(const MomBwdArgs& a, hipStream_t s);
+// dbeta[inst * n_kv + t] = (sum of the instance's nblk partials) / n for t < n.
+hipError_t launch_mom_dbeta(const float* part, int nblk, int BH, float* dbeta, int64_t n_kv, int64_t n, hipStream_t s);
+// M'[inst] = bbar[inst * bbar_inst] M[inst] - (sum of the nsplit partials P), dh floats per instance.
+hipError_t launch_mom_adv(const float* M, const float* bbar, int64_t bbar_inst, PartSet P, float* Mout, int BH,
+                          int64_t dh, hipStream_t s);
 // Linear fast weight, per key token of a chunk: dv = eta Y (Y in dv on
 // entry), deta = v . Y.
 hipError_t launch_lin_tokens(const void* V, const float* eta, void* dv, float* deta, int BH, int64_t n, int d,

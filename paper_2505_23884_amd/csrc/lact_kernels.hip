@@ -2295,9 +2295,10 @@ __device__ __forceinline__ void add_set(const PartSet& s, int64_t inst, int64_t 
   if (!s.p) return;
   const float4* p = reinterpret_cast<const float4*>(s.p + inst * s.inst + roff);
   const int64_t ss = s.split >> 2;
+  const float f = s.sign != 0.0f ? s.sign : 1.0f;
   for (int k = 0; k < s.n; ++k) {
     const float4 q = p[k * ss + i];
-    acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
+    acc.x += f * q.x; acc.y += f * q.y; acc.z += f * q.z; acc.w += f * q.w;
   }
 }
 
@@ -2474,6 +2475,62 @@ __global__ __launch_bounds__(256) void k_copies(const CopyArgs a) {
         for (int j = 0; j < 4 && r + j < g.R; ++j) out[o + j] = (T)tile[q + j][k];
       }
     }
+  }
+}
+
+// Momentum reverse of one chunk (see MomBwdArgs): each block a fixed range
+// of one instance's nmat * dh floats, its share of <dM', M> in a fixed order.
+__global__ __launch_bounds__(256) void k_mom_bwd(const MomBwdArgs a) {
+  __shared__ float red[4];
+  const int inst = blockIdx.x / a.nblk, b = blockIdx.x - inst * a.nblk;
+  const int64_t n4 = a.nmat * a.dh / 4, per = (n4 + a.nblk - 1) / a.nblk;
+  const int64_t e0 = b * per, e1 = e0 + per < n4 ? e0 + per : n4;
+  const float bb = a.bbar[inst * a.bbar_inst];
+  float dot = 0.0f;
+  for (int64_t e = e0 + threadIdx.x; e < e1; e += 256) {
+    const int j = (int)((4 * e) / a.dh);
+    const int64_t off = inst * a.dh + 4 * e - j * a.dh;
+    float4* u = reinterpret_cast<float4*>(a.U + inst * a.nmat * a.dh) + e;
+    float4* r = reinterpret_cast<float4*>(a.R[j] + off);
+    const float4 m = *reinterpret_cast<const float4*>(a.M[j] + off);
+    const float4 uu = *u, rr = *r;
+    const float4 t = make_float4(rr.x - uu.x, rr.y - uu.y, rr.z - uu.z, rr.w - uu.w);   // dM'
+    dot += t.x * m.x + t.y * m.y + t.z * m.z + t.w * m.w;
+    *u = make_float4(-t.x, -t.y, -t.z, -t.w);
+    *r = make_float4(bb * t.x, bb * t.y, bb * t.z, bb * t.w);
+  }
+  dot = wave_sum(dot);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = dot;
+  __syncthreads();
+  if (threadIdx.x == 0) a.part[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// dbeta of a chunk's tokens: one block per instance, the partials summed in order.
+__global__ __launch_bounds__(256) void k_mom_dbeta(const float* part, int nblk, float* dbeta, int64_t n_kv,
+                                                   int64_t n) {
+  __shared__ float tot;
+  if (threadIdx.x == 0) {
+    float s = 0.0f;
+    for (int b = 0; b < nblk; ++b) s += part[(int64_t)blockIdx.x * nblk + b];
+    tot = s / (float)n;
+  }
+  __syncthreads();
+  for (int64_t t = threadIdx.x; t < n; t += 256) dbeta[(int64_t)blockIdx.x * n_kv + t] = tot;
+}
+
+// M' = bbar M - sum P per instance (grid stride over float4s).
+__global__ __launch_bounds__(256) void k_mom_adv(const float* M, const float* bbar, int64_t bbar_inst, const PartSet P,
+                                                 float* Mout, int BH, int64_t dh) {
+  const int64_t n4 = dh >> 2, total = (int64_t)BH * n4;
+  for (int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x; x < total; x += (int64_t)gridDim.x * 256) {
+    const int64_t inst = x / n4;
+    const int i = (int)(x - inst * n4);
+    const float bb = bbar[inst * bbar_inst];
+    const float4 m = reinterpret_cast<const float4*>(M + inst * dh)[i];
+    float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
+    add_set(P, inst, 0, i, g);
+    reinterpret_cast<float4*>(Mout + inst * dh)[i] = make_float4(bb * m.x - g.x, bb * m.y - g.y, bb * m.z - g.z,
+                                                                 bb * m.w - g.w);
   }
 }
 
@@ -2809,6 +2866,7 @@ hipError_t launch_zero_rows(void* out, int BH, int64_t row_bytes, int64_t rows, 
 hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.BH * a.nchunks;
   if (blocks <= 0) return hipSuccess;
+  if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   k_beta_mean<<<(unsigned)blocks, 256, 0, s>>>(a);
   return hipGetLastError();
 }
@@ -2941,6 +2999,28 @@ hipError_t launch_copies_f32(const CopySeg* c, int n, int BH, hipStream_t s) {
   if (total >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   a.first[n] = (int)total;
   k_copies<float><<<(unsigned)total, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mom_bwd(const MomBwdArgs& a, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.BH * a.nblk;
+  if (blocks <= 0) return hipSuccess;
+  k_mom_bwd<<<(unsigned)blocks, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mom_dbeta(const float* part, int nblk, int BH, float* dbeta, int64_t n_kv, int64_t n, hipStream_t s) {
+  if (BH <= 0 || n <= 0) return hipSuccess;
+  k_mom_dbeta<<<(unsigned)BH, 256, 0, s>>>(part, nblk, dbeta, n_kv, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_mom_adv(const float* M, const float* bbar, int64_t bbar_inst, PartSet P, float* Mout, int BH,
+                          int64_t dh, hipStream_t s) {
+  const int64_t need = ((int64_t)BH * (dh / 4) + 255) / 256;
+  if (need <= 0) return hipSuccess;
+  const int64_t blocks = need < 8192 ? need : 8192;
+  k_mom_adv<<<(unsigned)blocks, 256, 0, s>>>(M, bbar, bbar_inst, P, Mout, BH, dh);
   return hipGetLastError();
 }
 

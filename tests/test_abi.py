@@ -323,3 +323,51 @@ def test_swiglu_backward_errors_before_any_hip_call():
     assert _bwd_sw(d, nbytes=P.binding.backward_workspace_bytes(d) - 1) == -3
     nk = make_desc(**dict(GOOD, n_kv=0))
     assert _bwd_sw(nk, k=0, v=0, eta=0, dk=0, dv=0, deta=0, ws=0) == -3
+
+
+def _bwd_mom(desc, nbytes=None, **kw):
+    names = ("q", "k", "v", "eta", "beta", "w1", "w2", "w3", "m1", "m2", "m3", "do", "f1", "f2", "f3", "g1", "g2",
+             "g3", "dq", "dk", "dv", "deta", "dbeta", "d1", "d2", "d3", "e1", "e2", "e3", "ws")
+    a = {n: 0x1000 * (i + 1) for i, n in enumerate(names)}
+    for n in ("f1", "f2", "f3", "g1", "g2", "g3"):
+        a[n] = 0
+    a["ws"] = 0x100000
+    a.update(kw)
+    if nbytes is None:
+        err = ctypes.c_int(0)
+        nbytes = P.lib().lact_backward_momentum_workspace_bytes(ctypes.byref(desc), ctypes.byref(err))
+    vp = ctypes.c_void_p
+    return P.lib().lact_backward_momentum(ctypes.byref(desc), *(vp(a[n]) for n in names), ctypes.c_size_t(nbytes),
+                                          vp(0))
+
+
+@pytest.mark.parametrize("fw", [0, 1])
+def test_momentum_backward_errors_before_any_hip_call(fw):
+    base = dict(GOOD, h=64, fast_weight=1) if fw else dict(GOOD)
+    d = make_desc(**base)
+    nb = P.binding.backward_momentum_workspace_bytes(d)
+    # the plain backward's workspace plus every chunk's state
+    assert nb > P.binding.backward_workspace_bytes(d)
+    assert P.binding.backward_momentum_workspace_bytes(make_desc(**dict(base, chunk=128))) > nb
+    muon_fp32 = dict(base, use_muon=True, io_dtype=1, d=64, h=64)
+    err = ctypes.c_int(0)
+    assert P.lib().lact_backward_momentum_workspace_bytes(ctypes.byref(make_desc(**muon_fp32)), ctypes.byref(err)) == 0
+    assert err.value == -4
+    assert _bwd_mom(make_desc(**muon_fp32), nbytes=1 << 30) == -4
+    assert _bwd_mom(d, m1=0) == -1
+    assert _bwd_mom(d, e1=0) == -1
+    assert _bwd_mom(d, beta=0) == -1
+    assert _bwd_mom(d, dbeta=0) == -1
+    assert _bwd_mom(d, m1=0x9008) == -2
+    assert _bwd_mom(d, g1=0x9008) == -2    # a final-state cotangent, when given, is aligned too
+    assert _bwd_mom(d, dbeta=0x17002) == -2
+    assert _bwd_mom(d, ws=0) == -3
+    assert _bwd_mom(d, nbytes=nb - 1) == -3
+    if fw == 0:
+        assert _bwd_mom(d, m3=0) == -1
+        assert _bwd_mom(d, e2=0) == -1
+    else:   # the linear fast weight ignores the second and third matrices
+        assert _bwd_mom(d, m2=0, m3=0, e2=0, e3=0, w2=0, w3=0, d2=0, d3=0, ws=0) == -3
+    # no key tokens: beta and dbeta may be NULL as well
+    nk = make_desc(**dict(base, n_kv=0))
+    assert _bwd_mom(nk, k=0, v=0, eta=0, beta=0, dk=0, dv=0, deta=0, dbeta=0, ws=0) == -3

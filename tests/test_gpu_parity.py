@@ -16,7 +16,7 @@ import pytest
 import torch
 
 import paper_2505_23884_amd as P
-from lact_synth import CONFIGS, make_cotangents, make_inputs
+from lact_synth import CONFIGS, make_cotangents, make_inputs, make_momentum_state
 from oracle import lact_oracle as O
 
 pytestmark = pytest.mark.gpu
@@ -1615,6 +1615,172 @@ def test_linear_muon_backward_two_chunks(d):
                                       order=1, linear=1)
     x, ct = make_inputs(cfg, 83), make_cotangents(cfg, 83)
     check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct))
+
+
+# ----------------------------------------------------------------------------- momentum backward
+# lact_backward_momentum: the reverse of the chunk loop with the momentum
+# optimizer (M' = bbar M + g, the step M' or Muon(M')) against the oracle's
+# reverse (pinned to torch autograd of an independent chunk loop and to the
+# beta = 0 reduction), from a nonzero initial state with cotangents of the
+# final weights and state.
+
+
+def run_gpu_mom_bwd(cfg, x, ct, st, with_final=True):
+    print(f"[gpu] momentum backward {cfg.name} linear={cfg.linear} B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} "
+          f"n_kv={cfg.n_kv} n_q={cfg.n_q} C={cfg.chunk} order={cfg.order} io={cfg.io} muon={cfg.use_muon} "
+          f"final={with_final}", flush=True)
+    n = len(x["q"])
+    B, H = (cfg.B, cfg.H) if n == cfg.BH else (n, 1)
+    sh = lambda a: a.reshape(B, H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta, beta = (to_dev(sh(x[a]), cfg, torch.float32) for a in ("eta", "beta"))
+    dev = lambda names, src: tuple(to_dev(sh(src[w]), cfg, torch.float32) for w in names)
+    if cfg.linear:
+        W, M = dev(("W1",), x)[0], dev(("M",), st)[0]
+        dWf, dMf = (dev(("dW",), ct)[0], dev(("dM",), ct)[0]) if with_final else (None, None)
+        keep = [W, M]
+    else:
+        W, M = dev(("W1", "W2", "W3"), x), dev(("M1", "M2", "M3"), st)
+        dWf, dMf = (dev(("dW1", "dW2", "dW3"), ct), dev(("dM1", "dM2", "dM3"), ct)) if with_final else (None, None)
+        keep = list(W) + list(M)
+    before = [t.clone() for t in keep]
+    do = to_dev(sh(ct["do"]), cfg)
+    r = P.backward_momentum(q, k, v, eta, beta, W, M, do, cfg.chunk, order=cfg.order, dW_final=dWf,
+                            dM_final=dMf, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps)
+    torch.cuda.synchronize()
+    for a, b in zip(keep, before):
+        assert torch.equal(a, b)   # the initial weights and state are read only
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    head = tuple(f(t) for t in r[:5])
+    if cfg.linear:
+        return head + ((f(r[5]),), (f(r[6]),))
+    return head + (tuple(f(t) for t in r[5]), tuple(f(t) for t in r[6]))
+
+
+def check_mom_bwd(cfg, x, ct, st, got, with_final=True, instances=None):
+    idx = slice(None) if instances is None else list(instances)
+    sel = lambda a: a if instances is None else a[list(instances)]
+    wn = ("W1",) if cfg.linear else ("W1", "W2", "W3")
+    mn = ("M",) if cfg.linear else ("M1", "M2", "M3")
+    dwn = ("dW",) if cfg.linear else ("dW1", "dW2", "dW3")
+    dmn = ("dM",) if cfg.linear else ("dM1", "dM2", "dM3")
+    pack = (lambda t: t[0]) if cfg.linear else tuple
+
+    def ref_fn(xx):
+        r = O.lact_backward_momentum(sel(xx["q"]), sel(xx["k"]), sel(xx["v"]), sel(xx["eta"]), sel(xx["beta"]),
+                                     pack([sel(xx[w]) for w in wn]), pack([sel(st[m]) for m in mn]), sel(ct["do"]),
+                                     cfg.chunk, cfg.order,
+                                     dW_final=pack([sel(ct[w]) for w in dwn]) if with_final else None,
+                                     dM_final=pack([sel(ct[m]) for m in dmn]) if with_final else None,
+                                     use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps, dbeta_scale=True)
+        fl = (lambda t: [t]) if cfg.linear else list
+        return list(r[:5]) + fl(r[5]) + fl(r[6]) + [r[7]]
+    ref = ref_fn(x)
+    names = ["dq", "dk", "dv", "deta", "dbeta"] + ["d" + w for w in wn] + ["d" + m for m in mn]
+    flat = list(got[:5]) + list(got[5]) + list(got[6])
+    errs, blocks = {}, {}
+    for name, g, r in zip(names, flat, ref):
+        g = g[idx]
+        if g.size == 0:
+            continue
+        errs[name] = rel(g, r)
+        if name in ("deta", "dbeta"):   # per-token sums with cancellations: windows of 256 tokens
+            blocks[name] = worst_window(g, r, O_BLOCK)
+        else:
+            blocks[name] = worst_block(g, r, W_BLOCK if name.startswith(("dW", "dM")) else O_BLOCK)
+    if flat[4][idx].size:
+        # dbeta_c = <dM'_c, M_c> / n_c is an inner product that can cancel: its
+        # rounding error scales with |dM'_c| |M_c| / n_c (the oracle's scale)
+        errs["dbeta/scale"] = float(np.max(np.abs(flat[4][idx] - ref[4]) / ref[-1]))
+    if not cfg.use_muon:
+        assert_errs(errs, TOL[cfg.io], blocks)
+        return
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io])
+    wb, bb = dict(zip(names, whole)), dict(zip(names, block))
+    # with Muon, dbeta's per-chunk values are held to the scaled bound, with
+    # the bar of dM' (that of the state's cotangents); the few per-chunk
+    # values make its rel-L2 and its spread too noisy to compare
+    wb["dbeta/scale"] = max(wb[n] for n in names[-len(mn):])
+    wb["dbeta"], bb["dbeta"] = float("inf"), float("inf")
+    assert_bars(errs, blocks, wb, bb)
+
+
+def mom_case(base, seed, **kw):
+    cfg = CONFIGS[base].with_(momentum=1, **kw)
+    return cfg, make_inputs(cfg, seed), make_cotangents(cfg, seed), make_momentum_state(cfg, seed)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_momentum_backward_bf16_ragged(order):
+    # three chunks (the last partial) and a tail; d, h of several 128-tiles, h != d
+    cfg, x, ct, st = mom_case("lm32k_mom", 91, name="swiglu_mom_bwd", B=1, H=2, d=256, h=384, n_kv=700, n_q=760,
+                              chunk=256, order=order)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_momentum_backward_fp32_small(order):
+    # fp32 I/O, dims and a chunk that are not multiples of the tiles or of 32, no final cotangents
+    cfg, x, ct, st = mom_case("tiny_fp32", 92, name="swiglu_mom_bwd_fp32", B=2, H=1, d=40, h=56, n_kv=300, n_q=333,
+                              chunk=100, order=order)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st, with_final=False), with_final=False)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_linear_momentum_backward_bf16_ragged(order):
+    cfg, x, ct, st = mom_case("lm32k_linear", 93, name="linear_mom_bwd", B=1, H=2, d=256, h=256, n_kv=700,
+                              n_q=760, chunk=256, order=order)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
+
+
+def test_linear_momentum_backward_fp32_small():
+    cfg, x, ct, st = mom_case("tiny_fp32", 94, name="linear_mom_bwd_fp32", B=2, H=1, d=40, h=40, n_kv=300,
+                              n_q=333, chunk=100, order=0, linear=1)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st, with_final=False), with_final=False)
+
+
+def test_momentum_backward_beta_zero():
+    # bbar = 0: no cotangent reaches the initial state (dM0 = 0 exactly), and
+    # the rest is the plain backward's (the state then is the chunk gradient)
+    cfg, x, ct, st = mom_case("lm32k_mom", 95, name="swiglu_mom_bwd_beta0", B=1, H=2, d=128, h=256, n_kv=600,
+                              n_q=640, chunk=256)
+    x["beta"][:] = 0.0
+    got = run_gpu_mom_bwd(cfg, x, ct, st, with_final=False)
+    for m in got[6]:
+        assert not np.any(m)
+    plain = run_gpu_swiglu_bwd(cfg, x, ct, with_dW=False)
+    errs = {name: rel(a, b) for name, a, b in zip(("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3"),
+                                                   got[:4] + tuple(got[5]), plain)}
+    print("[gpu] beta = 0 vs the plain backward", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for kk, vv in errs.items():
+        assert vv <= 1e-5, (kk, vv)
+    check_mom_bwd(cfg, x, ct, st, got, with_final=False)
+
+
+def test_swiglu_momentum_backward_lm_shape_sampled_instance():
+    # one LM sequence (4 heads, d = h = 512, 16 chunks of 2048), one instance checked
+    cfg, x, ct, st = mom_case("lm32k_mom", 96, name="swiglu_mom_bwd_lm32k_b1", B=1)
+    got = run_gpu_mom_bwd(cfg, x, ct, st)
+    check_mom_bwd(cfg, x, ct, st, got, instances=[1])
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_muon_momentum_backward_small_matrices(order):
+    cfg, x, ct, st = mom_case("video", 97, name="swiglu_muon_mom_bwd", B=1, H=2, n_kv=400, n_q=440, chunk=256,
+                              order=order)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
+
+
+def test_swiglu_muon_momentum_backward_lm_shape_two_chunks():
+    cfg, x, ct, st = mom_case("lm32k_muon_mom", 98, name="swiglu_muon_mom_bwd_lm", B=1, H=2, n_kv=4096, n_q=4096)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
+
+
+def test_linear_muon_momentum_backward_two_chunks():
+    # chunks of d tokens: full-rank chunk gradients (see the plain Muon case)
+    cfg, x, ct, st = mom_case("lm32k_muon_mom", 99, name="linear_muon_mom_bwd", B=1, H=2, d=256, h=256, n_kv=512,
+                              n_q=560, chunk=256, order=1, linear=1)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
 
 
 # ----------------------------------------------------------------------------- envelope limits

@@ -1310,3 +1310,32 @@ def test_momentum_backward_batched_driver_stacks_instances():
     r = O.lact_backward_momentum_instance(q[1], k[1], v[1], eta[1], beta[1], W[0][1, :d, :], M[0][1, :d, :], do[1], C, 1)
     for a, b in zip(lin, r):
         assert np.array_equal(a[0], b)
+
+
+def test_momentum_backward_dbeta_scale():
+    # one chunk, no cotangent of o or of the final weights: dM' is the final
+    # state's cotangent; with dM_final = M0 the inner product <dM', M0> meets
+    # its Cauchy-Schwarz bound, so dbeta equals the scale ||M0||^2 / n
+    rng = _rng(137)
+    d, h, n = 4, 6, 7
+    q, k, v = _tokens(rng, n, d), _tokens(rng, n, d), _tokens(rng, n, d)
+    eta, beta = 0.1 + 0.3 * rng.random(n), rng.random(n)
+    W0 = _weights(rng, h, d, unit=True)
+    M0 = tuple(0.1 * rng.standard_normal(w.shape) for w in W0)
+    r = O.lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, np.zeros((n, d)), n, 0, dM_final=M0,
+                                          dbeta_scale=True)
+    m2 = sum(float(np.sum(m * m)) for m in M0)
+    assert np.allclose(r[4], m2 / n, rtol=1e-13)
+    assert np.allclose(r[7], m2 / n, rtol=1e-13)
+    # in general |dbeta| stays within the scale, over chunks, orders and Muon
+    for order, muon in ((0, False), (1, True)):
+        do = rng.standard_normal((n, d))
+        dMf = tuple(rng.standard_normal(w.shape) for w in W0)
+        r = O.lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, 3, order, dM_final=dMf, use_muon=muon,
+                                              dbeta_scale=True)
+        plain = O.lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, 3, order, dM_final=dMf,
+                                                  use_muon=muon)
+        assert len(r) == 8 and len(plain) == 7
+        assert np.all(np.abs(r[4]) <= r[7] * (1 + 1e-12)) and np.all(r[7] > 0)
+        for a, b in zip(r[:5], plain[:5]):
+            assert np.array_equal(a, b)

@@ -63,7 +63,7 @@ def parse():
     ap.add_argument("--device-inputs", action="store_true",
                     help="draw the inputs on the device (plain uniform-chunk workloads)")
     ap.add_argument("--backward", action="store_true",
-                    help="time the backward (lact_backward, or lact_backward_linear on a linear workload)")
+                    help="time the backward (lact_backward; lact_backward_linear on a linear workload, lact_backward_momentum with momentum)")
     ap.add_argument("--traffic-report", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"))
     return ap.parse_args()
 
@@ -185,7 +185,7 @@ def kernel_short_name(name):
     for k in ("k_fwd_narrow", "k_fwd", "k_bwd", "k_update", "k_prep", "k_scale_rows", "k_beta_mean", "k_zero_rows",
               "k_ns_fused_pair_out", "k_ns_fused_pair", "k_ns_fused", "k_ns_final", "k_ns_prep", "k_ns_scale", "k_ns",
               "k_prologue", "k_rmsnorm_out", "k_vjp", "k_lin_tokens", "k_copies", "k_accum", "k_swiglu_apply_rows",
-              "k_swiglu_rows"):
+              "k_swiglu_rows", "k_mom_bwd", "k_mom_dbeta", "k_mom_adv", "k_slot_dot", "k_ns_lin", "k_sym"):
         m = str(len(k)) + k
         if m + "I" in name or m + "E" in name or "::" + k + "<" in name or "::" + k + "(" in name:
             return k
@@ -276,7 +276,8 @@ def backward_flops(cfg, BH=None):
     chunk and matrix: the replayed iteration (App. A: 4 m^2 n + 2 m^3 per
     step, m <= n its sides) and its reverse (dX' X^T, B dX', M X and S A:
     6 m^2 n + 2 m^3 per step); the second replay that the reverse makes to
-    recover the iterates is not counted."""
+    recover the iterates is not counted. Momentum adds elementwise passes
+    over the state only (no products)."""
     BH = cfg.BH if BH is None else BH
     nmat = 1 if cfg.linear else 3
     m, n = float(min(cfg.d, cfg.h)), float(max(cfg.d, cfg.h))
@@ -344,8 +345,17 @@ def _oracle_sample(cfg, min_seconds, backward=False):
     while done < scfg.BH and dt < min_seconds:
         x = make_inputs(scfg, 0, heads=[done])
         ct = make_cotangents(scfg, 0, heads=[done]) if backward else None
+        if backward and scfg.momentum:
+            from lact_synth import make_momentum_state
+            st = make_momentum_state(scfg, 0, heads=[done])
+            W0 = x["W1"][0] if scfg.linear else tuple(x[w][0] for w in ("W1", "W2", "W3"))
+            M0 = st["M"][0] if scfg.linear else tuple(st[m][0] for m in ("M1", "M2", "M3"))
         t0 = time.perf_counter()
-        if backward and scfg.linear:
+        if backward and scfg.momentum:
+            O.lact_backward_momentum_instance(x["q"][0], x["k"][0], x["v"][0], x["eta"][0], x["beta"][0], W0, M0,
+                                              ct["do"][0], scfg.chunk, scfg.order, use_muon=bool(scfg.use_muon),
+                                              ns_steps=scfg.ns_steps)
+        elif backward and scfg.linear:
             O.lact_backward_linear_instance(x["q"][0], x["k"][0], x["v"][0], x["eta"][0], x["W1"][0], ct["do"][0],
                                             scfg.chunk, scfg.order, use_muon=bool(scfg.use_muon),
                                             ns_steps=scfg.ns_steps)
@@ -510,19 +520,33 @@ def measure(cfg, args, P, on_device=False):
 
     if args.backward:
         from lact_synth import make_cotangents
-        if cfg.momentum or cfg.lr3 or cfg.schedule or cfg.layer_io or on_device or (cfg.use_muon and cfg.io != "bf16"):
-            raise SystemExit("--backward runs without momentum, per-matrix rates or a schedule (Muon with bf16 I/O), "
+        if cfg.lr3 or cfg.schedule or cfg.layer_io or on_device or (cfg.use_muon and cfg.io != "bf16"):
+            raise SystemExit("--backward runs without per-matrix rates or a schedule (Muon with bf16 I/O), "
                              "host-drawn inputs")
         ct = make_cotangents(cfg, 0)
         dout = torch.from_numpy(ct["do"].reshape(cfg.B, cfg.H, cfg.n_q, cfg.d)).to(dev, io)
         del ct
+        Wb = W[:1] if cfg.linear else W
         grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v), torch.empty_like(eta),
-                 *(torch.empty_like(w) for w in (W[:1] if cfg.linear else W)))
-        bdesc = desc
-        ws = torch.empty(P.backward_workspace_bytes(bdesc), dtype=torch.uint8, device=dev)
+                 *(torch.empty_like(w) for w in Wb))
+        if cfg.momentum:   # from a seeded nonzero state; the factor's and the state's cotangents too
+            from lact_synth import make_momentum_state
+            st = make_momentum_state(cfg, 0)
+            M = [torch.from_numpy(st[m].reshape(cfg.B, cfg.H, *st[m].shape[1:])).to(dev, torch.float32)
+                 for m in (("M",) if cfg.linear else ("M1", "M2", "M3"))]
+            del st
+            pick = (lambda t: t[0]) if cfg.linear else tuple
+            grads = grads[:4] + (torch.empty_like(beta), pick(grads[4:]), pick([torch.empty_like(m) for m in M]))
+            ws = torch.empty(P.backward_momentum_workspace_bytes(desc), dtype=torch.uint8, device=dev)
+        else:
+            ws = torch.empty(P.backward_workspace_bytes(desc), dtype=torch.uint8, device=dev)
 
     def path():
-        if args.backward and cfg.linear:
+        if args.backward and cfg.momentum:
+            P.backward_momentum(q, k, v, eta, beta, Wb[0] if cfg.linear else tuple(Wb), M[0] if cfg.linear else tuple(M),
+                                dout, cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
+                                out=grads, workspace=ws, stream=launch_stream())
+        elif args.backward and cfg.linear:
             P.backward_linear(q, k, v, eta, W[0], dout, cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon),
                               ns_steps=cfg.ns_steps, out=grads, workspace=ws, stream=launch_stream())
         elif args.backward:
@@ -572,7 +596,8 @@ def measure(cfg, args, P, on_device=False):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if cfg.io == "bf16" else "fp32", "data": "synthetic",
-        "config": {"workload": describe(cfg) + ((", backward (lact_backward_linear)" if cfg.linear else
+        "config": {"workload": describe(cfg) + ((", backward (lact_backward_momentum)" if cfg.momentum else
+                                                 ", backward (lact_backward_linear)" if cfg.linear else
                                                  ", backward (lact_backward)") if args.backward else ""),
                    "tokens_per_step": tokens, "flops_per_step": flops},
         "tokens_per_s": round(tokens / dt, 1),
@@ -634,9 +659,9 @@ def measure(cfg, args, P, on_device=False):
 
 # The second workload that the performance target names, measured in the same
 # process after the default one: NVS with a million context tokens; then the
-# backward at the LM shape: SwiGLU without and with Muon, and the linear fast weight.
+# backward at the LM shape: SwiGLU without and with Muon, the linear fast weight, and SwiGLU with momentum.
 SECONDARY = "nvs1m"
-SECONDARY_BWD = ("lm32k", "lm32k_muon", "lm32k_linear")
+SECONDARY_BWD = ("lm32k", "lm32k_muon", "lm32k_linear", "lm32k_mom")
 
 
 def main():

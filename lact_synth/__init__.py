@@ -92,6 +92,8 @@ CONFIGS = {
     "lm32k_lr3": LactConfig("lm32k_lr3", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", lr3=1),
     # linear fast weight at the LM shape (the workload of its backward)
     "lm32k_linear": LactConfig("lm32k_linear", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", linear=1),
+    "lm32k_linear_mom": LactConfig("lm32k_linear_mom", 4, 4, 512, 512, 32768, 32768, 2048, 0, 0, 0, "bf16", 1,
+                                   linear=1),
     # video teacher forcing: 18 clean chunks of 3120 tokens interleaved with 19
     # noisy ones, [X1n, X1, ..., X18, X19n] (115440 tokens in all)
     "video_tf": LactConfig("video_tf", 1, 40, 128, 256, 37 * 3120, 37 * 3120, 3120, 0, 1, 5, "bf16",

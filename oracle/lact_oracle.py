@@ -543,46 +543,53 @@ def swiglu_apply_vjp(W1, W2, W3, X, dO):
 
 
 def chunk_gradient_vjp(W1, W2, W3, K, V, eta, G1, G2, G3):
-    """Reverse of chunk_gradient (one rate per token): from the cotangents
-    (G1, G2, G3) of the gradients (g1, g2, g3), the cotangents
-    (dW1, dW2, dW3, dK, dV, deta) of its inputs.
+    """Reverse of chunk_gradient: from the cotangents (G1, G2, G3) of the
+    gradients (g1, g2, g3), the cotangents (dW1, dW2, dW3, dK, dV, deta) of
+    its inputs; eta (and deta) [n] for one rate per token or [n, 3] for
+    per-matrix rates (column j that of W_{j+1}).
 
-    The forward in the notation of chunk_gradient, with rates e = eta:
+    The forward in the notation of chunk_gradient, with rates e1, e2, e3 of
+    W1, W2, W3 (all equal to eta with one rate):
         Z1 = K W1^T, Z3 = K W3^T, C = V W2, S = SiLU(Z1), S1 = SiLU'(Z1)
-        A  = S o Z3,  R3 = e C o S,  R1 = e C o Z3 o S1
-        g2 = -(e V)^T A,  g3 = -R3^T K,  g1 = -R1^T K
+        A  = S o Z3,  R3 = e3 C o S,  R1 = e1 C o Z3 o S1
+        g2 = -(e2 V)^T A,  g3 = -R3^T K,  g1 = -R1^T K
     and its reverse, one step at a time from the last:
-        dA  = -e (V G2),  dV = -e (A G2^T),  deta = -rowsum(V o (A G2^T))
-        dR3 = -K G3^T,    dK = -R3 G3
-        dR1 = -K G1^T,    dK -= R1 G1
-        R3:  dC = e dR3 o S,  dS = e dR3 o C,  deta += rowsum(dR3 o C o S)
-        R1:  dC += e dR1 o Z3 o S1,  dZ3 = e dR1 o C o S1,
-             dS1 = e dR1 o C o Z3,   deta += rowsum(dR1 o C o Z3 o S1)
+        dA  = -e2 (V G2),  dV = -e2 (A G2^T),  de2 = -rowsum(V o (A G2^T))
+        dR3 = -K G3^T,     dK = -R3 G3
+        dR1 = -K G1^T,     dK -= R1 G1
+        R3:  dC = e3 dR3 o S,  dS = e3 dR3 o C,  de3 = rowsum(dR3 o C o S)
+        R1:  dC += e1 dR1 o Z3 o S1,  dZ3 = e1 dR1 o C o S1,
+             dS1 = e1 dR1 o C o Z3,   de1 = rowsum(dR1 o C o Z3 o S1)
         A:   dS += dA o Z3,  dZ3 += dA o S
         S, S1 (both of Z1):  dZ1 = dS o S1 + dS1 o SiLU''(Z1)
         C = V W2:   dV += dC W2^T,  dW2 = V^T dC
         Z1, Z3:     dK += dZ1 W1 + dZ3 W3,  dW1 = dZ1^T K,  dW3 = dZ3^T K
+    With one rate, deta = de1 + de2 + de3.
     """
     K = np.asarray(K, dtype=np.float64)
     V = np.asarray(V, dtype=np.float64)
-    e = np.asarray(eta, dtype=np.float64)[:, None]
+    eta = np.asarray(eta, dtype=np.float64)
+    per_matrix = eta.ndim == 2
+    e1, e2, e3 = (eta[:, j:j + 1] for j in range(3)) if per_matrix else (eta[:, None],) * 3
     G1, G2, G3 = (np.asarray(g, dtype=np.float64) for g in (G1, G2, G3))
     Z1, Z3, C = K @ W1.T, K @ W3.T, V @ W2
     S, S1 = silu(Z1), silu_derivative(Z1)
     A = S * Z3
-    R3, R1 = e * C * S, e * C * Z3 * S1
+    R3, R1 = e3 * C * S, e1 * C * Z3 * S1
     AG2 = A @ G2.T
-    dA = -e * (V @ G2)
-    dV = -e * AG2
-    deta = -np.sum(V * AG2, axis=1)
+    dA = -e2 * (V @ G2)
+    dV = -e2 * AG2
+    de2 = -np.sum(V * AG2, axis=1)
     dR3 = -K @ G3.T
     dR1 = -K @ G1.T
     dK = -R3 @ G3 - R1 @ G1
-    dC = e * dR3 * S + e * dR1 * Z3 * S1
-    dS = e * dR3 * C + dA * Z3
-    dZ3 = e * dR1 * C * S1 + dA * S
-    dS1 = e * dR1 * C * Z3
-    deta = deta + np.sum(dR3 * C * S, axis=1) + np.sum(dR1 * C * Z3 * S1, axis=1)
+    dC = e3 * dR3 * S + e1 * dR1 * Z3 * S1
+    dS = e3 * dR3 * C + dA * Z3
+    dZ3 = e1 * dR1 * C * S1 + dA * S
+    dS1 = e1 * dR1 * C * Z3
+    de3 = np.sum(dR3 * C * S, axis=1)
+    de1 = np.sum(dR1 * C * Z3 * S1, axis=1)
+    deta = np.stack([de1, de2, de3], axis=1) if per_matrix else de2 + de3 + de1
     dZ1 = dS * S1 + dS1 * silu_second_derivative(Z1)
     dV = dV + dC @ W2.T
     dK = dK + dZ1 @ W1 + dZ3 @ W3
@@ -592,7 +599,8 @@ def chunk_gradient_vjp(W1, W2, W3, K, V, eta, G1, G2, G3):
 def lact_backward_instance(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int, dW_final=None,
                            use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT):
     """Reverse of lact_forward_instance for the SwiGLU fast weight (Muon
-    optional, no momentum, one rate per token): given the cotangent ``do`` [n_q, d] of
+    optional, no momentum; eta [n_kv] or per-matrix [n_kv, 3], deta shaped
+    like it): given the cotangent ``do`` [n_q, d] of
     the outputs and optionally ``dW_final`` = (dW1, dW2, dW3) of the returned
     fast weights, the cotangents (dq, dk, dv, deta, (dW1, dW2, dW3)) of the
     inputs, the last three those of the initial fast weights.
@@ -622,7 +630,7 @@ def lact_backward_instance(q, k, v, eta, W1, W2, W3, do, chunk: int, order: int,
     dW = [np.zeros_like(w) for w in Ws[0]] if dW_final is None else [
         np.asarray(w, dtype=np.float64).copy() for w in dW_final]
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
-    deta = np.zeros(n_kv)
+    deta = np.zeros(eta.shape)
 
     def apply_back(W, s, e):
         dx, a1, a2, a3 = swiglu_apply_vjp(*W, q[s:e], do[s:e])
@@ -712,7 +720,7 @@ def lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, chunk: int, 
     dM = [np.zeros_like(m) for m in M] if dM_final is None else [
         np.asarray(x, dtype=np.float64).copy() for x in tup(dM_final)]
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
-    deta, dbeta, bscale = np.zeros(n_kv), np.zeros(n_kv), np.zeros(n_kv)
+    deta, dbeta, bscale = np.zeros(eta.shape), np.zeros(n_kv), np.zeros(n_kv)
 
     def apply_back(Wc, s, e):
         r = apply_vjp(Wc, q[s:e], do[s:e])

@@ -938,8 +938,14 @@ def test_swiglu_apply_vjp_matches_autograd():
 
 def _torch_chunk_gradient(W1, W2, W3, K, V, eta):
     """The chunk gradient by torch autograd of the chunk loss, kept in the
-    graph (create_graph) so that it can be differentiated again."""
-    loss = -(eta[:, None] * _torch_swiglu_t(W1, W2, W3, K) * V).sum()
+    graph (create_graph) so that it can be differentiated again. With
+    per-matrix rates (eta [n, 3]) the gradient of W_j is that of the loss
+    weighted by column j."""
+    f = _torch_swiglu_t(W1, W2, W3, K)
+    if eta.dim() == 2:
+        return tuple(torch.autograd.grad(-(eta[:, j:j + 1] * f * V).sum(), W, create_graph=True)[0]
+                     for j, W in enumerate((W1, W2, W3)))
+    loss = -(eta[:, None] * f * V).sum()
     return torch.autograd.grad(loss, (W1, W2, W3), create_graph=True)
 
 
@@ -1339,3 +1345,84 @@ def test_momentum_backward_dbeta_scale():
         assert np.all(np.abs(r[4]) <= r[7] * (1 + 1e-12)) and np.all(r[7] > 0)
         for a, b in zip(r[:5], plain[:5]):
             assert np.array_equal(a, b)
+
+
+# ----------------------------------------------------------------------------- per-matrix rates, backward
+
+
+def test_chunk_gradient_vjp_per_matrix_rates_matches_double_backward():
+    rng = _rng(140)
+    h, d, n = 6, 4, 11
+    W1, W2, W3 = _weights(rng, h, d)
+    K, V = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    eta = 0.1 + rng.random((n, 3))
+    G = (rng.standard_normal((h, d)), rng.standard_normal((d, h)), rng.standard_normal((h, d)))
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    ins = [t(a) for a in (W1, W2, W3, K, V, eta)]
+    g = _torch_chunk_gradient(*ins)
+    for a, b in zip(g, O.chunk_gradient(W1, W2, W3, K, V, eta)):
+        assert np.allclose(a.detach().numpy(), b, rtol=1e-11, atol=1e-12)
+    sum(((gj * torch.tensor(Gj)).sum() for gj, Gj in zip(g, G))).backward()
+    got = O.chunk_gradient_vjp(W1, W2, W3, K, V, eta, *G)
+    assert got[5].shape == (n, 3)
+    for name, a, ref in zip(("dW1", "dW2", "dW3", "dK", "dV", "deta"), got, ins):
+        assert np.allclose(a, ref.grad.numpy(), rtol=1e-10, atol=1e-12), name
+
+
+def test_chunk_gradient_vjp_equal_rate_columns_reduce_to_one_rate():
+    # three equal columns: every cotangent but deta is the one-rate result,
+    # and deta's columns sum to the one-rate deta
+    rng = _rng(141)
+    h, d, n = 7, 5, 9
+    W = _weights(rng, h, d)
+    K, V = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    eta = 0.1 + rng.random(n)
+    G = (rng.standard_normal((h, d)), rng.standard_normal((d, h)), rng.standard_normal((h, d)))
+    one = O.chunk_gradient_vjp(*W, K, V, eta, *G)
+    three = O.chunk_gradient_vjp(*W, K, V, np.repeat(eta[:, None], 3, axis=1), *G)
+    for a, b in zip(one[:5], three[:5]):
+        assert np.allclose(a, b, rtol=1e-13, atol=1e-15)
+    assert np.allclose(three[5].sum(axis=1), one[5], rtol=1e-12, atol=1e-14)
+    # a rate that is zero for one matrix: that matrix's gradient, and its
+    # cotangents through it, vanish (W2: no dV through e2 A, no e2 column)
+    eta3 = np.repeat(eta[:, None], 3, axis=1)
+    eta3[:, 1] = 0.0
+    G2only = (np.zeros((h, d)), G[1], np.zeros((h, d)))
+    r = O.chunk_gradient_vjp(*W, K, V, eta3, *G2only)
+    assert np.allclose(r[0], 0) and np.allclose(r[2], 0) and np.allclose(r[1], 0) and np.allclose(r[3], 0)
+    assert np.allclose(r[5][:, 0], 0) and np.allclose(r[5][:, 2], 0)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_backward_per_matrix_rates_matches_autograd(order):
+    rng = _rng(142 + order)
+    d, h, n_kv, n_q, C = 5, 7, 17, 21, 6
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random((n_kv, 3))
+    W0 = _weights(rng, h, d, unit=True)
+    do = rng.standard_normal((n_q, d))
+    dWf = tuple(rng.standard_normal(w.shape) for w in W0)
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    qt, kt, vt, et = t(q), t(k), t(v), t(eta)
+    Wt = tuple(t(w) for w in W0)
+    o, Wfin = _torch_swiglu_layer(qt, kt, vt, et, Wt, C, order)
+    loss = (o * torch.tensor(do)).sum() + sum((w * torch.tensor(x)).sum() for w, x in zip(Wfin, dWf))
+    loss.backward()
+    dq, dk, dv, deta, dW = O.lact_backward_instance(q, k, v, eta, *W0, do, C, order, dWf)
+    assert deta.shape == (n_kv, 3)
+    for name, g, ref in zip(("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3"), (dq, dk, dv, deta, *dW),
+                            (qt, kt, vt, et, *Wt)):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-9, atol=1e-11), name
+    # with Muon and with momentum too (the same per-matrix chunk gradient)
+    beta = rng.random(n_kv)
+    M0 = tuple(0.05 * rng.standard_normal(w.shape) for w in W0)
+    bt, Mt = t(beta), tuple(t(m) for m in M0)
+    qt, kt, vt, et = t(q), t(k), t(v), t(eta)
+    Wt = tuple(t(w) for w in W0)
+    o, Wfin, Mfin = _torch_momentum_layer(qt, kt, vt, et, bt, Wt, Mt, C, order, True, False)
+    ((o * torch.tensor(do)).sum() + sum((w * torch.tensor(x)).sum() for w, x in zip(Wfin, dWf))).backward()
+    r = O.lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, C, order, dWf, use_muon=True)
+    for name, g, ref in zip(("dq", "dk", "dv", "deta", "dbeta"), r[:5], (qt, kt, vt, et, bt)):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-8, atol=1e-10), name
+    for a, ref in zip(r[5] + r[6], Wt + Mt):
+        assert np.allclose(a, ref.grad.numpy(), rtol=1e-8, atol=1e-10)

@@ -520,8 +520,8 @@ def measure(cfg, args, P, on_device=False):
 
     if args.backward:
         from lact_synth import make_cotangents
-        if cfg.lr3 or cfg.schedule or cfg.layer_io or on_device or (cfg.use_muon and cfg.io != "bf16"):
-            raise SystemExit("--backward runs without per-matrix rates or a schedule (Muon with bf16 I/O), "
+        if cfg.schedule or cfg.layer_io or on_device or (cfg.use_muon and cfg.io != "bf16"):
+            raise SystemExit("--backward runs without a schedule or the layer's prologue (Muon with bf16 I/O), "
                              "host-drawn inputs")
         ct = make_cotangents(cfg, 0)
         dout = torch.from_numpy(ct["do"].reshape(cfg.B, cfg.H, cfg.n_q, cfg.d)).to(dev, io)

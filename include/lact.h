@@ -300,9 +300,10 @@ int lact_backward_linear(const lact_desc* desc,
 /*
  * Backward of lact_forward for the SwiGLU fast weight (§3.1 loss, chunk
  * gradient and SwiGLU eqs.; §3.2 per-row norm-preserving update; Alg. 1),
- * with or without Muon (App. A; with Muon bf16 I/O only) and with one rate
- * per token (else LACT_EUNSUPPORTED); momentum: lact_backward_momentum. Given
- * the cotangent dO of the outputs and optionally
+ * with or without Muon (App. A; with Muon bf16 I/O only), with one rate per
+ * token or per-matrix rates (eta_per_matrix: each matrix's gradient weighted
+ * by its own column, deta with one column per matrix); momentum:
+ * lact_backward_momentum. Given the cotangent dO of the outputs and optionally
  * those of the final fast weights, the cotangents of every input: the
  * reverse of the chunk loop, with the weights and negated gradients of every
  * chunk recomputed by the forward's own launches and kept in the workspace.
@@ -325,7 +326,7 @@ int lact_backward_linear(const lact_desc* desc,
  *                         each may be NULL (zero)                                in
  *   dq     [B*H, n_q, d]  io_dtype                                               out
  *   dk, dv [B*H, n_kv, d] io_dtype                                               out
- *   deta   [B*H, n_kv]    fp32                                                   out
+ *   deta   [B*H, n_kv]    fp32 ([B*H, n_kv, 3] with eta_per_matrix)             out
  *   dW1, dW2, dW3         fp32, shapes of W1, W2, W3: cotangents of the initial
  *                         fast weights                                           out
  *   workspace   >= lact_backward_workspace_bytes(desc), 256-byte aligned (it

@@ -1739,8 +1739,9 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
 }
 
 // Reverse of the SwiGLU fast weight's chunk loop (§3.1 loss and chunk
-// gradient, §3.2 per-row norm-preserving update; Alg. 1), no Muon or
-// momentum, one rate per token. The forward's own update launches replay
+// gradient, §3.2 per-row norm-preserving update; Alg. 1), one rate per token
+// or one per matrix (Alg. 1's three rates), with Muon (NsBwd) and the
+// momentum optimizer (App. A) optional. The forward's own update launches replay
 // the chunk loop (unfused, so that every chunk's negated gradient P_c stays
 // in a slot of its own, and reading W_c from the trajectory while writing
 // W_{c+1}). The reverse then walks the chunks from the last, carrying the
@@ -1771,7 +1772,7 @@ struct SwBwdLayout {
 int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false) {
   int rc = check_desc(dsc);
   if (rc) return rc;
-  if (dsc->fast_weight != LACT_FW_SWIGLU || dsc->eta_per_matrix) return LACT_EUNSUPPORTED;
+  if (dsc->fast_weight != LACT_FW_SWIGLU) return LACT_EUNSUPPORTED;
   if (dsc->use_muon && dsc->io_dtype != LACT_IO_BF16) return LACT_EUNSUPPORTED;   // fp16 Newton-Schulz reverse
   L->p = make_plan(dsc, false);
   const Plan& p = L->p;
@@ -2206,13 +2207,14 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     ra.X3 = zb[4];
     ra.Y2 = zb[5];
     ra.in_inst = zi;
-    ra.eta = eta + s0;
+    ra.eta = eta + s0 * p.es;
     ra.eta_inst = n_kv;
+    ra.eta_cols = p.es;
     ra.Pk = pk;
     ra.pk_inst = T * 4 * h;
     ra.Pv = pv;
     ra.pv_inst = T * 2 * h;
-    ra.deta = deta + s0;
+    ra.deta = deta + s0 * p.es;
     ra.BH = p.BH;
     ra.n = n;
     ra.h = (int)h;

@@ -392,7 +392,8 @@ hipError_t launch_lin_tokens(const void* V, const float* eta, void* dv, float* d
 struct SwigluRowsArgs {
   const void* Z1; const void* Z3; const void* C; const void* X1; const void* X3; const void* Y2;
   int64_t in_inst;                    // elements between instances of the six [n x h] inputs
-  const float* eta; int64_t eta_inst;
+  const float* eta; int64_t eta_inst;  // tokens between instances; eta_cols rates per token (1, or 3 per matrix)
+  int eta_cols;                       // deta has the same layout
   void* Pk; int64_t pk_inst;          // [n x 4h]
   void* Pv; int64_t pv_inst;          // [n x 2h]
   float* deta;

@@ -2665,21 +2665,26 @@ __device__ __forceinline__ void ld4(const void* base, int64_t idx, float* v) {
 }
 
 // SwiGLU chunk-gradient reverse, one wave per key token (grid stride). With
-// S = SiLU(Z1), S1 = SiLU'(Z1), S2 = SiLU''(Z1), A = S Z3 and the token's rate e:
-//   dA  = e Y2,  dC = e (X3 S + X1 Z3 S1),  dZ3 = e X1 C S1 + dA S,
-//   dZ1 = (e X3 C + dA Z3) S1 + e X1 C Z3 S2,  R3 = e C S,  R1 = e C Z3 S1,
-//   deta = sum over the hidden units of A Y2 + X3 C S + X1 C Z3 S1.
+// S = SiLU(Z1), S1 = SiLU'(Z1), S2 = SiLU''(Z1), A = S Z3 and the token's
+// rates e1, e2, e3 of W1, W2, W3 (one rate: all three the same):
+//   dA  = e2 Y2,  dC = e3 X3 S + e1 X1 Z3 S1,  dZ3 = e1 X1 C S1 + dA S,
+//   dZ1 = (e3 X3 C + dA Z3) S1 + e1 X1 C Z3 S2,  R3 = e3 C S,  R1 = e1 C Z3 S1,
+//   and, summed over the hidden units, de1 = X1 C Z3 S1, de2 = A Y2,
+//   de3 = X3 C S (one rate: deta = their sum).
 template <typename T>
 __global__ __launch_bounds__(256) void k_swiglu_rows(const SwigluRowsArgs a) {
   const int lane = threadIdx.x & 63;
   const int h = a.h;
+  const bool per_matrix = a.eta_cols == 3;
   const int64_t total = (int64_t)a.BH * a.n;
   for (int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wave < total; wave += (int64_t)gridDim.x * 4) {
     const int64_t inst = wave / a.n, t = wave - inst * a.n;
     const int64_t io = inst * a.in_inst + t * h;
     const int64_t ko = inst * a.pk_inst + t * 4 * h, vo = inst * a.pv_inst + t * 2 * h;
-    const float e = a.eta[inst * a.eta_inst + t];
-    float dsum = 0.0f;
+    const int64_t eo = (inst * a.eta_inst + t) * a.eta_cols;
+    const float e1 = a.eta[eo];
+    const float e2 = per_matrix ? a.eta[eo + 1] : e1, e3 = per_matrix ? a.eta[eo + 2] : e1;
+    float d1 = 0.0f, d2 = 0.0f, d3 = 0.0f;
     for (int j = 4 * lane; j < h; j += 256) {
       float z1[4], z3[4], c[4], x1[4], x3[4], y2[4];
       ld4<T>(a.Z1, io + j, z1);
@@ -2694,14 +2699,17 @@ __global__ __launch_bounds__(256) void k_swiglu_rows(const SwigluRowsArgs a) {
         const float sg = sigmoidf_fast(z1[q]);
         const float S = z1[q] * sg, S1 = sg + z1[q] * sg * (1.0f - sg);
         const float S2 = sg * (1.0f - sg) * (2.0f + z1[q] * (1.0f - 2.0f * sg));
-        const float A = S * z3[q], dA = e * y2[q];
-        dc[q] = e * (x3[q] * S + x1[q] * z3[q] * S1);
-        dz3[q] = e * x1[q] * c[q] * S1 + dA * S;
-        dz1[q] = (e * x3[q] * c[q] + dA * z3[q]) * S1 + e * x1[q] * c[q] * z3[q] * S2;
-        r3[q] = e * c[q] * S;
-        r1[q] = e * c[q] * z3[q] * S1;
-        ea[q] = e * A;
-        dsum += A * y2[q] + x3[q] * c[q] * S + x1[q] * c[q] * z3[q] * S1;
+        const float A = S * z3[q], dA = e2 * y2[q];
+        const float t1 = x1[q] * c[q] * z3[q] * S1, t3 = x3[q] * c[q] * S;
+        dc[q] = e3 * x3[q] * S + e1 * x1[q] * z3[q] * S1;
+        dz3[q] = e1 * x1[q] * c[q] * S1 + dA * S;
+        dz1[q] = (e3 * x3[q] * c[q] + dA * z3[q]) * S1 + e1 * x1[q] * c[q] * z3[q] * S2;
+        r3[q] = e3 * c[q] * S;
+        r1[q] = e1 * c[q] * z3[q] * S1;
+        ea[q] = e2 * A;
+        d1 += t1;
+        d2 += A * y2[q];
+        d3 += t3;
       }
       st4<T>(a.Pk, ko + j, r3[0], r3[1], r3[2], r3[3]);
       st4<T>(a.Pk, ko + h + j, r1[0], r1[1], r1[2], r1[3]);
@@ -2710,8 +2718,19 @@ __global__ __launch_bounds__(256) void k_swiglu_rows(const SwigluRowsArgs a) {
       st4<T>(a.Pv, vo + j, ea[0], ea[1], ea[2], ea[3]);
       st4<T>(a.Pv, vo + h + j, dc[0], dc[1], dc[2], dc[3]);
     }
-    dsum = wave_sum(dsum);
-    if (lane == 0) a.deta[inst * a.eta_inst + t] = dsum;
+    if (per_matrix) {
+      d1 = wave_sum(d1);
+      d2 = wave_sum(d2);
+      d3 = wave_sum(d3);
+      if (lane == 0) {
+        a.deta[eo] = d1;
+        a.deta[eo + 1] = d2;
+        a.deta[eo + 2] = d3;
+      }
+    } else {
+      const float dsum = wave_sum(d2 + d3 + d1);
+      if (lane == 0) a.deta[eo] = dsum;
+    }
   }
 }
 

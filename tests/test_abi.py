@@ -300,15 +300,18 @@ def test_swiglu_backward_errors_before_any_hip_call():
     # every chunk's weights and gradient partials, so it grows with the chunk count
     assert P.binding.backward_workspace_bytes(d) > P.workspace_bytes(d)
     assert P.binding.backward_workspace_bytes(make_desc(**dict(GOOD, chunk=128))) > P.binding.backward_workspace_bytes(d)
-    # no per-matrix rates, not the linear fast weight, Muon with bf16 I/O only
+    # not the linear fast weight, Muon with bf16 I/O only; per-matrix rates accepted
     muon_fp32 = dict(GOOD, use_muon=True, io_dtype=1, d=64, h=64)
-    for bad in (muon_fp32, dict(GOOD, eta_per_matrix=1), dict(GOOD, h=64, fast_weight=1)):
+    for bad in (muon_fp32, dict(GOOD, h=64, fast_weight=1)):
         assert _bwd_sw(make_desc(**bad), nbytes=1 << 30) == -4
     assert P.binding.backward_workspace_bytes(make_desc(**dict(GOOD, use_muon=True))) > P.binding.backward_workspace_bytes(d)
-    for bad in (muon_fp32, dict(GOOD, eta_per_matrix=1)):
-        err = ctypes.c_int(0)
-        assert P.lib().lact_backward_workspace_bytes(ctypes.byref(make_desc(**bad)), ctypes.byref(err)) == 0
-        assert err.value == -4
+    err = ctypes.c_int(0)
+    assert P.lib().lact_backward_workspace_bytes(ctypes.byref(make_desc(**muon_fp32)), ctypes.byref(err)) == 0
+    assert err.value == -4
+    lr3 = make_desc(**dict(GOOD, eta_per_matrix=1))
+    assert P.binding.backward_workspace_bytes(lr3) > 0
+    assert _bwd_sw(lr3, deta=0) == -1
+    assert _bwd_sw(lr3, ws=0) == -3
     assert _bwd_sw(make_desc(**dict(GOOD, d=12)), nbytes=1 << 30) == -4
     assert _bwd_sw(d, q=0) == -1
     assert _bwd_sw(d, do=0) == -1

@@ -1783,6 +1783,51 @@ def test_linear_muon_momentum_backward_two_chunks():
     check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
 
 
+# ----------------------------------------------------------------------------- per-matrix rates, backward
+# Alg. 1's three rates per token (eta [.., n_kv, 3], deta the same): each
+# matrix's gradient weighted by its own column.
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_backward_per_matrix_rates_bf16_ragged(order):
+    cfg = CONFIGS["lm32k_lr3"].with_(name="swiglu_bwd_lr3", B=1, H=2, d=256, h=384, n_kv=700, n_q=760, chunk=256,
+                                     order=order)
+    x, ct = make_inputs(cfg, 101), make_cotangents(cfg, 101)
+    assert x["eta"].shape[-1] == 3
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct))
+
+
+def test_swiglu_backward_per_matrix_rates_fp32_small():
+    cfg = CONFIGS["tiny_fp32"].with_(name="swiglu_bwd_lr3_fp32", B=2, H=1, d=40, h=56, n_kv=300, n_q=333, chunk=100,
+                                     order=1, lr3=1)
+    x, ct = make_inputs(cfg, 102), make_cotangents(cfg, 102)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct, with_dW=False), with_dW=False)
+
+
+def test_swiglu_backward_equal_rate_columns_match_one_rate():
+    # the three columns equal to the one-rate eta: the same cotangents, and
+    # deta's columns sum to the one-rate deta
+    cfg = CONFIGS["lm32k"].with_(name="swiglu_bwd_lr3_equal", B=1, H=2, d=128, h=256, n_kv=600, n_q=640, chunk=256)
+    x, ct = make_inputs(cfg, 103), make_cotangents(cfg, 103)
+    one = run_gpu_swiglu_bwd(cfg, x, ct)
+    x3 = dict(x, eta=np.ascontiguousarray(np.repeat(x["eta"][..., None], 3, axis=-1)))
+    three = run_gpu_swiglu_bwd(cfg.with_(lr3=1), x3, ct)
+    errs = {name: rel(a, b) for name, a, b in zip(("dq", "dk", "dv", "dW1", "dW2", "dW3"),
+                                                   one[:3] + one[4:], three[:3] + three[4:])}
+    errs["deta"] = rel(three[3].sum(axis=-1), one[3])
+    print("[gpu] three equal rates vs one", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for kk, vv in errs.items():
+        assert vv <= 1e-5, (kk, vv)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_momentum_muon_backward_per_matrix_rates(order):
+    # the LM training layer's options together: per-matrix rates, momentum and Muon
+    cfg, x, ct, st = mom_case("lm32k_muon_mom", 104, name="swiglu_lr3_mom_muon_bwd", B=1, H=2, d=128, h=256,
+                              n_kv=512, n_q=560, chunk=256, order=order, lr3=1)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
+
+
 # ----------------------------------------------------------------------------- envelope limits
 # The largest head and hidden dims (4096), very many instances, the most
 # Newton-Schulz steps, and a chunk longer than the sequence.

@@ -867,6 +867,106 @@ def lact_forward_schedule(q, k, v, eta, W1, W2, W3, schedule, use_muon: bool = F
     return tuple(np.stack(col) for col in zip(*res))
 
 
+def lact_backward_schedule_instance(q, k, v, eta, W1, W2, W3, do, schedule, dW_final=None,
+                                    use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT, beta=None, M=None,
+                                    dM_final=None):
+    """Reverse of lact_forward_schedule_instance (the ttt_config loop of
+    Alg. 1; reading R10): the cotangents of q, k, v, eta (and beta with
+    momentum) and of the initial fast weights (and state) given ``do`` and,
+    optionally, those of the final weights (and state).
+
+    The schedule's events (an apply or an update over its segment's tokens,
+    in the segment's order) are replayed to recover the weights (and state)
+    that each event used, then reversed: an apply goes back through
+    swiglu_apply_vjp with its weights; an update through weight_update_vjp,
+    Muon and the momentum recurrence as in lact_backward_momentum_instance,
+    then chunk_gradient_vjp over its tokens. An output row written by more
+    than one apply keeps the last value, so only the last apply of a row
+    receives that row's cotangent; key rows used by more than one update
+    collect every update's share.
+    Returns (dq, dk, dv, deta, (dW1, dW2, dW3)) or, with beta,
+    (dq, dk, dv, deta, dbeta, (dW1, dW2, dW3), (dM1, dM2, dM3)).
+    """
+    q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
+    eta = np.asarray(eta, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    mom = beta is not None
+    step_of = (lambda g: newton_schulz(g, ns_steps)) if use_muon else (lambda g: g)
+    W = tuple(np.asarray(w, dtype=np.float64).copy() for w in (W1, W2, W3))
+    Mc = tuple(np.zeros_like(w) for w in W) if M is None else tuple(np.asarray(m, dtype=np.float64).copy()
+                                                                    for m in M)
+    parts = {"update_then_apply": ("update", "apply"), "apply_then_update": ("apply", "update"),
+             "update_only": ("update",), "apply_only": ("apply",)}
+    Ws, Ms, steps, bbars, events = [W], [Mc], [], [], []
+    for mode, b, e in schedule:
+        mode = SCHEDULE_MODES[mode] if not isinstance(mode, str) else mode
+        for kind in parts[mode]:
+            events.append((kind, b, e, len(Ws) - 1))
+            if kind == "update":
+                g = chunk_gradient(*Ws[-1], k[b:e], v[b:e], eta[b:e])
+                if mom:
+                    bbar = float(np.mean(np.asarray(beta, dtype=np.float64)[b:e]))
+                    src = tuple(bbar * m + gj for m, gj in zip(Ms[-1], g))
+                    Ms.append(src)
+                    bbars.append(bbar)
+                else:
+                    src = g
+                steps.append(src)
+                Ws.append(tuple(weight_update(w, step_of(x)) for w, x in zip(Ws[-1], src)))
+    dW = [np.zeros_like(w) for w in W] if dW_final is None else [
+        np.asarray(x, dtype=np.float64).copy() for x in dW_final]
+    dM = [np.zeros_like(w) for w in W] if dM_final is None else [
+        np.asarray(x, dtype=np.float64).copy() for x in dM_final]
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    deta, dbeta = np.zeros(eta.shape), np.zeros(k.shape[0])
+    claimed = np.zeros(q.shape[0], dtype=bool)
+    for kind, b, e, wi in reversed(events):
+        if kind == "apply":
+            dO = np.where(claimed[b:e, None], 0.0, do[b:e])
+            claimed[b:e] = True
+            dx, a1, a2, a3 = swiglu_apply_vjp(*Ws[wi], q[b:e], dO)
+            dq[b:e] += dx
+            for j, a in enumerate((a1, a2, a3)):
+                dW[j] += a
+            continue
+        dg = []
+        for j in range(3):
+            dW[j], dst = weight_update_vjp(Ws[wi][j], step_of(steps[wi][j]), dW[j])
+            dg.append(newton_schulz_vjp(steps[wi][j], dst, ns_steps) if use_muon else dst)
+        if mom:
+            dg = [a + x for a, x in zip(dM, dg)]
+        b1, b2, b3, dkc, dvc, detac = chunk_gradient_vjp(*Ws[wi], k[b:e], v[b:e], eta[b:e], *dg)
+        for j, x in enumerate((b1, b2, b3)):
+            dW[j] += x
+        dk[b:e] += dkc
+        dv[b:e] += dvc
+        deta[b:e] += detac
+        if mom:
+            dbeta[b:e] += sum(float(np.sum(a * m)) for a, m in zip(dg, Ms[wi])) / (e - b)
+            dM = [bbars[wi] * a for a in dg]
+    if mom:
+        return dq, dk, dv, deta, dbeta, tuple(dW), tuple(dM)
+    return dq, dk, dv, deta, tuple(dW)
+
+
+def lact_backward_schedule(q, k, v, eta, W1, W2, W3, do, schedule, dW_final=None, use_muon: bool = False,
+                           ns_steps: int = NS_STEPS_DEFAULT, beta=None, M=None, dM_final=None, instances=None):
+    """Batched driver of lact_backward_schedule_instance (one schedule for
+    every instance): (dq, dk, dv, deta, dW1, dW2, dW3) stacked, and with beta
+    (dq, dk, dv, deta, dbeta, dW1, dW2, dW3, dM1, dM2, dM3); W, M and the
+    final cotangents are triples of [BH, ...] arrays (or None)."""
+    idx = range(q.shape[0]) if instances is None else instances
+    pick = lambda t, i: None if t is None else tuple(x[i] for x in t)
+    res = []
+    for i in idx:
+        r = lact_backward_schedule_instance(q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], do[i], schedule,
+                                            pick(dW_final, i), use_muon, ns_steps,
+                                            None if beta is None else beta[i], pick(M, i), pick(dM_final, i))
+        flat = r[:4] + tuple(r[4]) if beta is None else r[:5] + tuple(r[5]) + tuple(r[6])
+        res.append(flat)
+    return tuple(np.stack(col) for col in zip(*res))
+
+
 def layer_flops(BH: int, d: int, h: int, n_kv: int, n_q: int, n_chunks: int,
                 use_muon: bool = False, ns_steps: int = NS_STEPS_DEFAULT) -> float:
     """Algorithmic FLOPs of the path (App. A, FLOPs calculation).

@@ -1426,3 +1426,125 @@ def test_swiglu_backward_per_matrix_rates_matches_autograd(order):
         assert np.allclose(g, ref.grad.numpy(), rtol=1e-8, atol=1e-10), name
     for a, ref in zip(r[5] + r[6], Wt + Mt):
         assert np.allclose(a, ref.grad.numpy(), rtol=1e-8, atol=1e-10)
+
+
+# ----------------------------------------------------------------------------- backward of a general schedule
+
+
+def _torch_schedule_layer(q, k, v, eta, W, schedule, beta=None, M=None, muon=False):
+    """The schedule's segments in torch (autograd sees every step): an apply
+    overwrites its rows of o (rows applied twice keep the later value), an
+    update takes the chunk gradient by autograd, the momentum recurrence with
+    the segment's mean of beta, Muon, and the row-norm-preserving update."""
+    o = torch.zeros(q.shape, dtype=q.dtype)
+    parts = {"update_then_apply": ("update", "apply"), "apply_then_update": ("apply", "update"),
+             "update_only": ("update",), "apply_only": ("apply",)}
+    for mode, b, e in schedule:
+        for kind in parts[mode]:
+            if kind == "apply":
+                rows = torch.zeros(q.shape[0], 1, dtype=q.dtype)
+                rows[b:e] = 1.0
+                full = torch.zeros(q.shape, dtype=q.dtype)
+                full = torch.cat([full[:b], _torch_swiglu_t(*W, q[b:e]), full[e:]])
+                o = o * (1 - rows) + full
+                continue
+            g = _torch_chunk_gradient(*W, k[b:e], v[b:e], eta[b:e])
+            if beta is not None:
+                M = tuple(beta[b:e].mean() * m + gj for m, gj in zip(M, g))
+                g = M
+            new = []
+            for w, x in zip(W, g):
+                U = w - (_torch_newton_schulz(x) if muon else x)
+                new.append(U * (torch.linalg.vector_norm(w, dim=1, keepdim=True)
+                                / torch.linalg.vector_norm(U, dim=1, keepdim=True)))
+            W = tuple(new)
+    return o, W, M
+
+
+@pytest.mark.parametrize("mom,muon", [(False, False), (True, False), (True, True)])
+def test_schedule_backward_matches_autograd(mom, muon):
+    # every mode, an apply-only stretch between updates, rows applied twice
+    # (the later apply keeps them), key rows updated twice, an unapplied row
+    # range and unused key rows
+    rng = _rng(150 + 2 * mom + muon)
+    d, h, n_kv, n_q = 4, 6, 20, 26
+    schedule = [("apply_then_update", 0, 5), ("apply_only", 5, 9), ("update_then_apply", 5, 9),
+                ("update_only", 9, 14), ("apply_then_update", 3, 8), ("apply_only", 14, 20), ("apply_only", 22, 26)]
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random(n_kv)
+    beta = rng.random(n_kv) if mom else None
+    W0 = _weights(rng, h, d, unit=True)
+    M0 = tuple(0.05 * rng.standard_normal(w.shape) for w in W0) if mom else None
+    do = rng.standard_normal((n_q, d))
+    dWf = tuple(rng.standard_normal(w.shape) for w in W0)
+    dMf = tuple(rng.standard_normal(w.shape) for w in W0) if mom else None
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    qt, kt, vt, et = t(q), t(k), t(v), t(eta)
+    Wt = tuple(t(w) for w in W0)
+    bt = t(beta) if mom else None
+    Mt = tuple(t(m) for m in M0) if mom else None
+    o, Wfin, Mfin = _torch_schedule_layer(qt, kt, vt, et, Wt, schedule, bt, Mt, muon)
+    loss = (o * torch.tensor(do)).sum() + sum((w * torch.tensor(x)).sum() for w, x in zip(Wfin, dWf))
+    if mom:
+        loss = loss + sum((m * torch.tensor(x)).sum() for m, x in zip(Mfin, dMf))
+    loss.backward()
+    r = O.lact_backward_schedule_instance(q, k, v, eta, *W0, do, schedule, dWf, use_muon=muon, beta=beta, M=M0,
+                                          dM_final=dMf)
+    refs = (qt, kt, vt, et) + ((bt,) if mom else ())
+    for name, g, ref in zip(("dq", "dk", "dv", "deta", "dbeta"), r, refs):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-8, atol=1e-10), name
+    dW = r[5] if mom else r[4]
+    for a, ref in zip(dW, Wt):
+        assert np.allclose(a, ref.grad.numpy(), rtol=1e-8, atol=1e-10)
+    if mom:
+        for a, ref in zip(r[6], Mt):
+            assert np.allclose(a, ref.grad.numpy(), rtol=1e-8, atol=1e-10)
+    # rows no apply covers get no cotangent, nor key rows no update uses
+    assert not np.any(r[0][20:22]) and not np.any(r[1][14:]) and not np.any(r[3][14:])
+    # the forward the backward replays is the oracle's own forward
+    fw = O.lact_forward_schedule_instance(q, k, v, eta, *W0, schedule, use_muon=muon, beta=beta, M=M0)
+    assert np.allclose(o.detach().numpy(), fw[0], rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("order,muon", [(0, False), (1, False), (0, True)])
+def test_schedule_backward_of_uniform_chunks_is_the_chunk_loop_backward(order, muon):
+    rng = _rng(155 + order + 2 * muon)
+    d, h, n_kv, n_q, C = 4, 6, 13, 17, 5
+    mode = "apply_then_update" if order == 0 else "update_then_apply"
+    schedule = [(mode, s, min(n_kv, s + C)) for s in range(0, n_kv, C)] + [("apply_only", n_kv, n_q)]
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random((n_kv, 3))
+    W0 = _weights(rng, h, d, unit=True)
+    do = rng.standard_normal((n_q, d))
+    dWf = tuple(rng.standard_normal(w.shape) for w in W0)
+    got = O.lact_backward_schedule_instance(q, k, v, eta, *W0, do, schedule, dWf, use_muon=muon)
+    ref = O.lact_backward_instance(q, k, v, eta, *W0, do, C, order, dWf, use_muon=muon)
+    for a, b in zip(got[:4] + got[4], ref[:4] + ref[4]):
+        assert np.allclose(a, b, rtol=1e-13, atol=1e-15)
+    beta = rng.random(n_kv)
+    M0 = tuple(0.05 * rng.standard_normal(w.shape) for w in W0)
+    dMf = tuple(rng.standard_normal(w.shape) for w in W0)
+    got = O.lact_backward_schedule_instance(q, k, v, eta, *W0, do, schedule, dWf, use_muon=muon, beta=beta, M=M0,
+                                            dM_final=dMf)
+    ref = O.lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, C, order, dWf, dMf, use_muon=muon)
+    for a, b in zip(got[:5] + got[5] + got[6], ref[:5] + ref[5] + ref[6]):
+        assert np.allclose(a, b, rtol=1e-13, atol=1e-15)
+
+
+def test_schedule_backward_batched_driver_stacks_instances():
+    rng = _rng(160)
+    BH, d, h, n = 3, 4, 6, 12
+    schedule = [("apply_only", 0, 4), ("update_then_apply", 4, 8), ("apply_only", 8, 12)]
+    q, k, v = (np.stack([_tokens(rng, n, d) for _ in range(BH)]) for _ in range(3))
+    eta, beta = 0.1 + 0.3 * rng.random((BH, n)), rng.random((BH, n))
+    Ws = [_weights(rng, h, d, unit=True) for _ in range(BH)]
+    W = tuple(np.stack([w[j] for w in Ws]) for j in range(3))
+    M = tuple(0.1 * rng.standard_normal(w.shape) for w in W)
+    do = rng.standard_normal((BH, n, d))
+    got = O.lact_backward_schedule(q, k, v, eta, *W, do, schedule, beta=beta, M=M, instances=[2, 0])
+    assert len(got) == 11
+    for pos, i in enumerate((2, 0)):
+        r = O.lact_backward_schedule_instance(q[i], k[i], v[i], eta[i], *(w[i] for w in W), do[i], schedule,
+                                              beta=beta[i], M=tuple(m[i] for m in M))
+        for a, b in zip(got, r[:5] + r[5] + r[6]):
+            assert np.array_equal(a[pos], b)

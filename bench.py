@@ -277,11 +277,23 @@ def backward_flops(cfg, BH=None):
     step, m <= n its sides) and its reverse (dX' X^T, B dX', M X and S A:
     6 m^2 n + 2 m^3 per step); the second replay that the reverse makes to
     recover the iterates is not counted. Momentum adds elementwise passes
-    over the state only (no products)."""
+    over the state only (no products). A schedule counts its update
+    segments' key tokens and its apply segments' query tokens."""
     BH = cfg.BH if BH is None else BH
     nmat = 1 if cfg.linear else 3
     m, n = float(min(cfg.d, cfg.h)), float(max(cfg.d, cfg.h))
-    ns = cfg.n_chunks * nmat * cfg.ns_steps * (10.0 * m * m * n + 4.0 * m ** 3) if cfg.use_muon else 0.0
+    ns1 = nmat * cfg.ns_steps * (10.0 * m * m * n + 4.0 * m ** 3) if cfg.use_muon else 0.0
+    ns = cfg.n_chunks * ns1
+    if cfg.schedule:
+        from lact_synth import make_schedule
+        dh = float(cfg.d) * cfg.h
+        f = 0.0
+        for mode, b, e in make_schedule(cfg):
+            if mode != "apply_only":
+                f += 36.0 * dh * (e - b) + ns1
+            if mode != "update_only":
+                f += 16.0 * dh * (e - b)
+        return BH * f
     if cfg.linear:
         return BH * (float(cfg.d) * cfg.d * (6.0 * cfg.n_kv + 4.0 * cfg.n_q) + ns)
     return BH * (float(cfg.d) * cfg.h * (36.0 * cfg.n_kv + 16.0 * cfg.n_q) + ns)
@@ -520,16 +532,19 @@ def measure(cfg, args, P, on_device=False):
 
     if args.backward:
         from lact_synth import make_cotangents
-        if cfg.schedule or cfg.layer_io or on_device or (cfg.use_muon and cfg.io != "bf16"):
-            raise SystemExit("--backward runs without a schedule or the layer's prologue (Muon with bf16 I/O), "
-                             "host-drawn inputs")
+        if cfg.layer_io or on_device or (cfg.use_muon and cfg.io != "bf16"):
+            raise SystemExit("--backward runs without the layer's prologue (Muon with bf16 I/O), host-drawn inputs")
         ct = make_cotangents(cfg, 0)
         dout = torch.from_numpy(ct["do"].reshape(cfg.B, cfg.H, cfg.n_q, cfg.d)).to(dev, io)
         del ct
         Wb = W[:1] if cfg.linear else W
         grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v), torch.empty_like(eta),
                  *(torch.empty_like(w) for w in Wb))
-        if cfg.momentum:   # from a seeded nonzero state; the factor's and the state's cotangents too
+        if sched is not None:   # lact_backward_schedule (no momentum here)
+            if cfg.momentum:
+                raise SystemExit("--backward of a scheduled workload runs without momentum")
+            ws = torch.empty(P.binding.backward_schedule_workspace_bytes(desc, sched), dtype=torch.uint8, device=dev)
+        elif cfg.momentum:   # from a seeded nonzero state; the factor's and the state's cotangents too
             from lact_synth import make_momentum_state
             st = make_momentum_state(cfg, 0)
             M = [torch.from_numpy(st[m].reshape(cfg.B, cfg.H, *st[m].shape[1:])).to(dev, torch.float32)
@@ -542,7 +557,11 @@ def measure(cfg, args, P, on_device=False):
             ws = torch.empty(P.backward_workspace_bytes(desc), dtype=torch.uint8, device=dev)
 
     def path():
-        if args.backward and cfg.momentum:
+        if args.backward and sched is not None:
+            P.backward_schedule(q, k, v, eta, *W, dout, sched, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
+                                chunk=cfg.chunk, workspace=ws, stream=launch_stream(),
+                                out=grads[:4] + (tuple(grads[4:]),))
+        elif args.backward and cfg.momentum:
             P.backward_momentum(q, k, v, eta, beta, Wb[0] if cfg.linear else tuple(Wb), M[0] if cfg.linear else tuple(M),
                                 dout, cfg.chunk, order=cfg.order, use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps,
                                 out=grads, workspace=ws, stream=launch_stream())
@@ -596,7 +615,8 @@ def measure(cfg, args, P, on_device=False):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if cfg.io == "bf16" else "fp32", "data": "synthetic",
-        "config": {"workload": describe(cfg) + ((", backward (lact_backward_momentum)" if cfg.momentum else
+        "config": {"workload": describe(cfg) + ((", backward (lact_backward_schedule)" if cfg.schedule else
+                                                 ", backward (lact_backward_momentum)" if cfg.momentum else
                                                  ", backward (lact_backward_linear)" if cfg.linear else
                                                  ", backward (lact_backward)") if args.backward else ""),
                    "tokens_per_step": tokens, "flops_per_step": flops},

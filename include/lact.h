@@ -26,8 +26,9 @@
  * Entry points: lact_forward (the path above), lact_forward_momentum (the
  * momentum test-time optimizer, App. A), lact_forward_schedule (a caller-given
  * list of update/apply segments, Alg. 1), lact_backward,
- * lact_backward_linear and lact_backward_momentum (the reverse of the chunk
- * loop: SwiGLU and linear fast weight, and the momentum optimizer),
+ * lact_backward_linear, lact_backward_momentum and lact_backward_schedule
+ * (the reverse of the chunk loop: SwiGLU and linear fast weight, the
+ * momentum optimizer, a general schedule),
  * lact_prologue and lact_rmsnorm_out
  * (the layer's steps on either side of the path, Alg. 1); per-matrix learning
  * rates through lact_desc.eta_per_matrix.
@@ -383,6 +384,45 @@ int lact_backward(const lact_desc* desc,
  */
 size_t lact_backward_momentum_workspace_bytes(const lact_desc* desc, int* err);
 int lact_backward_momentum(const lact_desc* desc,
+                           const void* q, const void* k, const void* v, const float* eta,
+                           const float* beta,
+                           const float* W1, const float* W2, const float* W3,
+                           const float* M1, const float* M2, const float* M3,
+                           const void* dout,
+                           const float* dW1_final, const float* dW2_final, const float* dW3_final,
+                           const float* dM1_final, const float* dM2_final, const float* dM3_final,
+                           void* dq, void* dk, void* dv, float* deta, float* dbeta,
+                           float* dW1, float* dW2, float* dW3,
+                           float* dM1, float* dM2, float* dM3,
+                           void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
+ * Backward of lact_forward_schedule (the ttt_config loop of Alg. 1: update,
+ * apply, update-then-apply and apply-then-update segments, such as the
+ * strided mask of teacher-forced video of §4.3), SwiGLU fast weight, with or
+ * without Muon (bf16 I/O) and, with M1 != NULL, the momentum optimizer (as
+ * lact_backward_momentum, each update segment's own mean of beta; with
+ * M1 == NULL beta, M2, M3, their final cotangents, dbeta and dM are
+ * ignored). The segments' events are replayed by the forward's launches and
+ * reversed: an apply goes back with the weights it used, an update as in
+ * lact_backward. The apply segments must not overlap each other, nor the
+ * update segments (else LACT_EUNSUPPORTED): each row's cotangent is written
+ * once. Rows of dq that no apply covers, and rows of dk, dv, deta (dbeta)
+ * that no update uses, are written as zeros.
+ *
+ *   segs, nseg            as lact_forward_schedule (a HOST array)              in
+ *   other arguments       as lact_backward_momentum (per-matrix rates allowed)
+ *   workspace   >= lact_backward_schedule_workspace_bytes(desc, segs, nseg,
+ *               M1 != NULL), 256-byte aligned (it grows with the number of
+ *               update segments)
+ *
+ * Errors as lact_backward_momentum; an invalid segment is LACT_EINVAL, the
+ * linear fast weight LACT_EUNSUPPORTED.
+ */
+size_t lact_backward_schedule_workspace_bytes(const lact_desc* desc, const lact_segment* segs, int64_t nseg,
+                                              int momentum, int* err);
+int lact_backward_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg,
                            const void* q, const void* k, const void* v, const float* eta,
                            const float* beta,
                            const float* W1, const float* W2, const float* W3,

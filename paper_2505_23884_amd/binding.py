@@ -78,6 +78,11 @@ def load_library(path: str | None = None):
     L.lact_backward_momentum_workspace_bytes.restype = sz
     L.lact_backward_momentum.argtypes = [dp] + [vp] * 30 + [sz, vp]
     L.lact_backward_momentum.restype = i32
+    L.lact_backward_schedule_workspace_bytes.argtypes = [dp, ctypes.POINTER(LactSegment), i64, i32,
+                                                         ctypes.POINTER(i32)]
+    L.lact_backward_schedule_workspace_bytes.restype = sz
+    L.lact_backward_schedule.argtypes = [dp, ctypes.POINTER(LactSegment), i64] + [vp] * 30 + [sz, vp]
+    L.lact_backward_schedule.restype = i32
     f32 = ctypes.c_float
     L.lact_prologue.argtypes = [dp, vp, vp, f32, vp, vp, vp, vp, vp, vp, vp]
     L.lact_prologue.restype = i32
@@ -446,13 +451,7 @@ def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_s
     allocated when omitted). Returns o, or (o, (M1, M2, M3)) with beta.
     """
     import torch
-    segs = (LactSegment * max(len(schedule), 1))()
-    longest = 1
-    for i, (mode, b, e) in enumerate(schedule):
-        m = SEG_MODES[mode] if isinstance(mode, str) else int(mode)
-        segs[i] = LactSegment(m, 0, int(b), int(e))
-        if m != SEG_APPLY_ONLY:
-            longest = max(longest, int(e) - int(b))
+    segs, longest = _segments(schedule)
     extra = []
     if beta is not None:
         if M1 is None and M2 is None and M3 is None:
@@ -471,6 +470,84 @@ def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_s
     if rc:
         _raise(rc)
     return (out, M) if beta is not None else out
+
+
+def _segments(schedule):
+    """ctypes segments of a (mode, begin, end) sequence, and the longest update."""
+    segs = (LactSegment * max(len(schedule), 1))()
+    longest = 1
+    for i, (mode, b, e) in enumerate(schedule):
+        m = SEG_MODES[mode] if isinstance(mode, str) else int(mode)
+        segs[i] = LactSegment(m, 0, int(b), int(e))
+        if m != SEG_APPLY_ONLY:
+            longest = max(longest, int(e) - int(b))
+    return segs, longest
+
+
+def backward_schedule_workspace_bytes(desc: LactDesc, schedule, momentum=False) -> int:
+    segs, _ = _segments(schedule)
+    err = ctypes.c_int(0)
+    n = lib().lact_backward_schedule_workspace_bytes(ctypes.byref(desc), segs, ctypes.c_int64(len(schedule)),
+                                                     int(bool(momentum)), ctypes.byref(err))
+    if err.value:
+        _raise(err.value)
+    return int(n)
+
+
+def backward_schedule(q, k, v, eta, W1, W2, W3, dout, schedule, *, dW_final=None, use_muon=False, ns_steps=5,
+                      beta=None, M=None, dM_final=None, chunk=None, out=None, workspace=None, stream=None):
+    """Backward of forward_schedule (lact_backward_schedule), SwiGLU fast
+    weight: the cotangents of q, k, v, eta and of the initial W1, W2, W3 (not
+    written) given dout and, optionally, dW_final = (dW1, dW2, dW3). With
+    ``beta`` the momentum optimizer (M = (M1, M2, M3) the initial state, zeros
+    when omitted; dM_final its final cotangents). Returns (dq, dk, dv, deta,
+    (dW1, dW2, dW3)) or, with beta, (dq, dk, dv, deta, dbeta, (dW1, dW2, dW3),
+    (dM1, dM2, dM3)); written into ``out`` (that tuple) when given."""
+    import torch
+    segs, longest = _segments(schedule)
+    W = (W1, W2, W3)
+    mom = beta is not None
+    if mom and M is None:
+        M = tuple(torch.zeros_like(w) for w in W)
+    dWf = (None,) * 3 if dW_final is None else tuple(dW_final)
+    dMf = (None,) * 3 if (dM_final is None or not mom) else tuple(dM_final)
+    for t, ref in zip(dWf + dMf + (tuple(M) if mom else ()), W * 3):
+        if t is not None and (t.shape != ref.shape or t.dtype != torch.float32):
+            raise LactError(-1, "momentum and final cotangents must have the fast weights' shapes, fp32")
+    if dout.shape != q.shape or dout.dtype != q.dtype:
+        raise LactError(-1, "dout must have q's shape and dtype")
+    extra = [(t, "d_final") for t in dWf + dMf if t is not None]
+    if mom:
+        extra += [(beta, "beta")] + [(m, "M") for m in M]
+    desc, dq, _, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk or longest, 0, use_muon, ns_steps,
+                                   None if out is None else out[0], None, stream, FW_SWIGLU, need_workspace=False)
+    if not dout.is_cuda or not dout.is_contiguous():
+        raise LactError(-1, "dout must be a contiguous device tensor")
+    if workspace is None:
+        nb = backward_schedule_workspace_bytes(desc, schedule, mom)
+        workspace = torch.empty(max(nb, 1), dtype=torch.uint8, device=q.device)
+    if out is None:
+        head = (dq, torch.empty_like(k), torch.empty_like(v), torch.empty_like(eta))
+        dW = tuple(torch.empty_like(w) for w in W)
+        dbeta = torch.empty_like(beta) if mom else None
+        dM = tuple(torch.empty_like(w) for w in W) if mom else (None,) * 3
+    else:
+        head = tuple(out[:4])
+        dbeta = out[4] if mom else None
+        dW = tuple(out[5] if mom else out[4])
+        dM = tuple(out[6]) if mom else (None,) * 3
+    Ms = tuple(M) if mom else (None,) * 3
+    args = ([_ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(beta)] + [_ptr(w) for w in W] + [_ptr(m) for m in Ms] +
+            [_ptr(dout)] + [_ptr(t) for t in dWf] + [_ptr(t) for t in dMf] + [_ptr(t) for t in head] +
+            [_ptr(dbeta)] + [_ptr(t) for t in dW] + [_ptr(t) for t in dM])
+    rc = lib().lact_backward_schedule(ctypes.byref(desc), segs, ctypes.c_int64(len(schedule)), *args, _ptr(workspace),
+                                      ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                                      ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    if mom:
+        return head + (dbeta, dW, dM)
+    return head + (dW,)
 
 
 def prologue(qkv, lr_raw, lr_bias, beta_raw=None, n_kv=None, out=None, stream=None):

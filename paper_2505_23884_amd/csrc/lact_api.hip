@@ -1761,15 +1761,18 @@ struct SwBwdLayout {
   NsBwdLayout ns;       // with Muon: the Newton-Schulz reverse's buffers
   bool mom;             // momentum: the state's trajectory, chunk means, buffers of its reverse
   size_t off_mtraj, off_bbar_all, off_mu, off_mpart;
-  int64_t nch;          // chunks of the forward
-  int64_t T;            // token rows of the chunk buffers (a chunk, or a piece of the tail)
+  int64_t nch;          // updates of the forward (its chunks, or the schedule's update segments)
+  int64_t T;            // token rows of the chunk buffers (a chunk, or a piece of an apply-only stretch)
   int64_t tail_split;   // tokens per split of a tail piece (at most p.nsplit splits)
   size_t slotP;         // bytes of one chunk's gradient partials
   size_t off_P, off_traj, off_z[6], off_pk, off_pv, off_pq, off_hq, off_u[3], off_a[3], off_bk, off_bv, off_bq,
       off_ur[3], off_apart, off_bpart, total;
 };
 
-int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false) {
+// nupd: the schedule's updates (negative: lact_forward's chunks);
+// apply_len: its longest apply-only segment (negative: the tail n_q - n_kv).
+int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false, int64_t nupd = -1,
+                  int64_t apply_len = -1) {
   int rc = check_desc(dsc);
   if (rc) return rc;
   if (dsc->fast_weight != LACT_FW_SWIGLU) return LACT_EUNSUPPORTED;
@@ -1777,8 +1780,8 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false) {
   L->p = make_plan(dsc, false);
   const Plan& p = L->p;
   const double dh = (double)p.d * p.h;
-  L->nch = dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0;
-  const int64_t tail = dsc->n_q - dsc->n_kv;
+  L->nch = nupd >= 0 ? nupd : (dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0);
+  const int64_t tail = apply_len >= 0 ? apply_len : dsc->n_q - dsc->n_kv;
   L->T = std::max<int64_t>(1, std::max<int64_t>(p.C, std::min<int64_t>(tail, 4096)));
   const double need = (double)L->nch * p.BH * dh * 12.0 * (p.nsplit + 1) + (double)p.BH * L->T * p.h * p.esz * 15.0;
   if (need > 4.0e18) return LACT_EUNSUPPORTED;
@@ -1820,16 +1823,95 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false) {
   return LACT_OK;
 }
 
+// One segment of the backward's schedule: a LACT_SEG_* mode over tokens
+// [b, e), the index of its update among the schedule's updates (upd) and
+// the number of updates before it (the weights an apply before its update,
+// or an apply-only segment, uses: W_before).
+struct BSeg {
+  int mode;
+  int64_t b, e;
+  int64_t before;
+};
+
+// The uniform schedule of lact_forward (chunks of desc->chunk, then the
+// apply-only tail), or the caller's segments checked for the backward: the
+// update ranges must not overlap each other, nor the apply ranges (the
+// reverse writes the cotangents of a token's rows once).
+int backward_segments(const lact_desc* desc, const lact_segment* segs, int64_t nseg, std::vector<BSeg>* out,
+                      int64_t* nupd, int64_t* longest_apply) {
+  out->clear();
+  *nupd = 0;
+  *longest_apply = 0;
+  if (nseg < 0) {
+    const int mode = desc->order == LACT_UPDATE_THEN_APPLY ? LACT_SEG_UPDATE_THEN_APPLY : LACT_SEG_APPLY_THEN_UPDATE;
+    for (int64_t s0 = 0; s0 < desc->n_kv; s0 += desc->chunk)
+      out->push_back(BSeg{mode, s0, std::min(desc->n_kv, s0 + desc->chunk), (*nupd)++});
+    if (desc->n_q > desc->n_kv) {
+      out->push_back(BSeg{LACT_SEG_APPLY_ONLY, desc->n_kv, desc->n_q, *nupd});
+      *longest_apply = desc->n_q - desc->n_kv;
+    }
+    return LACT_OK;
+  }
+  int rc = check_segments(desc, segs, nseg);
+  if (rc) return rc;
+  std::vector<std::pair<int64_t, int64_t>> ur, ar;
+  for (int64_t i = 0; i < nseg; ++i) {
+    const lact_segment& g = segs[i];
+    out->push_back(BSeg{g.mode, g.begin, g.end, *nupd});
+    if (is_update(g.mode)) {
+      ur.emplace_back(g.begin, g.end);
+      ++*nupd;
+    }
+    if (is_apply(g.mode)) ar.emplace_back(g.begin, g.end);
+    if (g.mode == LACT_SEG_APPLY_ONLY) *longest_apply = std::max(*longest_apply, g.end - g.begin);
+  }
+  for (auto* r : {&ur, &ar}) {
+    std::sort(r->begin(), r->end());
+    for (size_t i = 1; i < r->size(); ++i)
+      if ((*r)[i].first < (*r)[i - 1].second) return LACT_EUNSUPPORTED;
+  }
+  return LACT_OK;
+}
+
+// Zeroes rows [r0, r1) of every instance of a per-token fp32 array of `cols`
+// values per row ([BH][rows][cols]).
+int zero_f32_rows(float* x, int BH, int64_t rows, int cols, int64_t r0, int64_t r1, hipStream_t s) {
+  if (r1 <= r0) return LACT_OK;
+  return timed(LACT_KCLASS_PREP, 0.0, s,
+               [&] { return launch_zero_f32(x, BH, rows * cols, r0 * cols, (r1 - r0) * cols, s); });
+}
+
+// Rows of [0, n) that no range of `r` covers, as [b, e) pairs.
+std::vector<std::pair<int64_t, int64_t>> uncovered(std::vector<std::pair<int64_t, int64_t>> r, int64_t n) {
+  std::sort(r.begin(), r.end());
+  std::vector<std::pair<int64_t, int64_t>> gaps;
+  int64_t at = 0;
+  for (const auto& x : r) {
+    if (x.first > at) gaps.emplace_back(at, x.first);
+    at = std::max(at, x.second);
+  }
+  if (n > at) gaps.emplace_back(at, n);
+  return gaps;
+}
+
 // With beta != nullptr: the momentum optimizer (M0 the initial state, dMf
-// the final state's cotangents or nullptr, dbeta and dM the outputs).
+// the final state's cotangents or nullptr, dbeta and dM the outputs). With
+// nsched >= 0: the caller's schedule `sched` (else lact_forward's chunks).
 int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,
                         const float* const W0[3], const void* dout, const float* const dWf[3], void* dq, void* dk,
                         void* dv, float* deta, float* const dW[3], void* workspace, size_t workspace_bytes,
                         void* stream, const float* beta = nullptr, const float* const* M0 = nullptr,
-                        const float* const* dMf = nullptr, float* dbeta = nullptr, float* const* dMo = nullptr) {
+                        const float* const* dMf = nullptr, float* dbeta = nullptr, float* const* dMo = nullptr,
+                        const lact_segment* sched = nullptr, int64_t nsched = -1) {
   const bool mom = M0 != nullptr;
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  std::vector<BSeg> segs;
+  int64_t nupd = 0, longest_apply = 0;
+  rc = backward_segments(desc, sched, nsched, &segs, &nupd, &longest_apply);
+  if (rc) return rc;
   SwBwdLayout L;
-  int rc = sw_bwd_layout(desc, &L, mom);
+  rc = sw_bwd_layout(desc, &L, mom, nupd, longest_apply);
   if (rc) return rc;
   const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
   if (mom) {
@@ -1852,7 +1934,7 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
   if (!workspace || workspace_bytes < L.total) return LACT_EWORKSPACE;
   if ((uintptr_t)workspace & (kAlign - 1)) return LACT_EALIGN;
   Ctx c;
-  // the forward's context; its updates read W_c and write W_{c+1} in the
+  // the forward's context; its updates read W_u and write W_{u+1} in the
   // trajectory, never W0
   float* const Mseed[3] = {mom ? const_cast<float*>(M0[0]) : nullptr, mom ? const_cast<float*>(M0[1]) : nullptr,
                            mom ? const_cast<float*>(M0[2]) : nullptr};
@@ -1863,71 +1945,91 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
   const Plan& p = c.p;
   const hipStream_t s = c.s;
   uint8_t* ws = c.ws;
-  const int64_t n_kv = desc->n_kv, n_q = desc->n_q, C = desc->chunk, d = p.d, h = p.h, BH = p.BH;
+  const int64_t n_kv = desc->n_kv, n_q = desc->n_q, d = p.d, h = p.h, BH = p.BH;
   const int64_t dh = d * h, esz = p.esz;
   const size_t w4 = (size_t)BH * dh * 4;
   const int64_t psplit = BH * 3 * dh;   // floats between splits of a partial set
-  auto traj = [&](int64_t i, int m) -> float* {
+  auto traj = [&](int64_t i, int m) -> float* {   // weights entering update i (i = nupd: the final ones)
     return i == 0 ? const_cast<float*>(W0[m])
                   : reinterpret_cast<float*>(ws + L.off_traj + ((size_t)(i - 1) * 3 + m) * w4);
   };
-  auto mtraj = [&](int64_t i, int m) -> float* {   // momentum state entering chunk i
+  auto mtraj = [&](int64_t i, int m) -> float* {   // momentum state entering update i
     return i == 0 ? const_cast<float*>(M0[m])
                   : reinterpret_cast<float*>(ws + L.off_mtraj + ((size_t)(i - 1) * 3 + m) * w4);
   };
+  // rows of the cotangents that no apply (dq) or no update (dk, dv, deta, dbeta) reaches
+  if (nsched >= 0) {
+    std::vector<std::pair<int64_t, int64_t>> ur, ar;
+    for (const BSeg& g : segs) {
+      if (is_update(g.mode)) ur.emplace_back(g.b, g.e);
+      if (is_apply(g.mode)) ar.emplace_back(g.b, g.e);
+    }
+    for (const auto& gap : uncovered(ar, n_q)) {
+      rc = timed(LACT_KCLASS_PREP, 0.0, s,
+                 [&] { return launch_zero_rows(dq, p.BH, d * esz, n_q, gap.first, gap.second, s); });
+      if (rc) return rc;
+    }
+    for (const auto& gap : uncovered(ur, n_kv)) {
+      rc = timed(LACT_KCLASS_PREP, 0.0, s,
+                 [&] { return launch_zero_rows(dk, p.BH, d * esz, n_kv, gap.first, gap.second, s); });
+      if (!rc) rc = timed(LACT_KCLASS_PREP, 0.0, s,
+                          [&] { return launch_zero_rows(dv, p.BH, d * esz, n_kv, gap.first, gap.second, s); });
+      if (!rc) rc = zero_f32_rows(deta, p.BH, n_kv, p.es, gap.first, gap.second, s);
+      if (!rc && mom) rc = zero_f32_rows(dbeta, p.BH, n_kv, 1, gap.first, gap.second, s);
+      if (rc) return rc;
+    }
+  }
+  // replay: every update's weights (and state) in the trajectory, its
+  // negated gradient partials in a slot of its own
   rc = prepare_weights(c);
   if (rc) return rc;
-  for (int64_t ci = 0; ci < L.nch; ++ci) {
-    const int64_t s0 = ci * C, s1 = std::min(n_kv, s0 + C);
-    if (mom) {   // the state advances in place in its trajectory slot
-      if (ci % kBetaBatch == 0) {
-        c.chunk_idx = ci;
-        rc = beta_means(c, s0, C, n_kv, (int)std::min<int64_t>(kBetaBatch, L.nch - ci));
-        if (rc) return rc;
-      }
+  float* bbar_all = mom ? reinterpret_cast<float*>(ws + L.off_bbar_all) : nullptr;
+  for (const BSeg& g : segs) {
+    if (!is_update(g.mode)) continue;
+    const int64_t u = g.before;
+    if (mom) {   // the update's mean of beta (the replay's slot and [BH][nupd]); the state advances in its slot
+      c.chunk_idx = 0;
+      rc = beta_means(c, g.b, g.e - g.b, g.e, 1);
+      if (rc) return rc;
+      BetaArgs ba{};
+      ba.beta = beta;
+      ba.n_kv = n_kv;
+      ba.chunk = g.e - g.b;
+      ba.t0 = g.b;
+      ba.end = g.e;
+      ba.nchunks = 1;
+      ba.BH = p.BH;
+      ba.bbar = bbar_all + u;
+      ba.stride = (int)nupd;
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_beta_mean(ba, s); });
+      if (rc) return rc;
       for (int m = 0; m < 3; ++m) {
         rc = timed(LACT_KCLASS_PREP, 0.0, c.s,
-                   [&] { return hipMemcpyAsync(mtraj(ci + 1, m), mtraj(ci, m), w4, hipMemcpyDeviceToDevice, c.s); });
+                   [&] { return hipMemcpyAsync(mtraj(u + 1, m), mtraj(u, m), w4, hipMemcpyDeviceToDevice, c.s); });
         if (rc) return rc;
-        c.M[m] = mtraj(ci + 1, m);
+        c.M[m] = mtraj(u + 1, m);
       }
     }
     for (int m = 0; m < 3; ++m) {
-      c.W[m] = traj(ci + 1, m);
-      c.Wsrc[m] = traj(ci, m);
+      c.W[m] = traj(u + 1, m);
+      c.Wsrc[m] = traj(u, m);
       if (p.muon) {   // Muon's fused last steps update W in place: start from a copy
         c.Wsrc[m] = nullptr;
         rc = timed(LACT_KCLASS_PREP, 0.0, c.s,
-                   [&] { return hipMemcpyAsync(traj(ci + 1, m), traj(ci, m), w4, hipMemcpyDeviceToDevice, c.s); });
+                   [&] { return hipMemcpyAsync(traj(u + 1, m), traj(u, m), w4, hipMemcpyDeviceToDevice, c.s); });
         if (rc) return rc;
       }
     }
     if (!p.bf16) {   // fp32: the contractions read the state itself
-      c.wop[0] = op(traj(ci, 0), d, dh);
-      c.wop[1] = op(traj(ci, 1), h, dh);
-      c.wop[2] = op(traj(ci, 2), d, dh);
+      c.wop[0] = op(traj(u, 0), d, dh);
+      c.wop[1] = op(traj(u, 1), h, dh);
+      c.wop[2] = op(traj(u, 2), d, dh);
     }
-    c.p.off_step = L.off_P + (size_t)ci * L.slotP;
-    c.chunk_idx = ci;
-    rc = update_chunk(c, s0, s1, false);
+    c.p.off_step = L.off_P + (size_t)u * L.slotP;
+    rc = update_chunk(c, g.b, g.e, false);
     if (rc) return rc;
   }
   c.p.off_step = L.p.off_step;
-  float* bbar_all = mom ? reinterpret_cast<float*>(ws + L.off_bbar_all) : nullptr;
-  if (mom && L.nch > 0) {   // every chunk's mean of beta, [BH][nch]
-    BetaArgs ba{};
-    ba.beta = beta;
-    ba.n_kv = n_kv;
-    ba.chunk = C;
-    ba.t0 = 0;
-    ba.end = n_kv;
-    ba.nchunks = (int)L.nch;
-    ba.BH = p.BH;
-    ba.bbar = bbar_all;
-    ba.stride = (int)L.nch;
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_beta_mean(ba, s); });
-    if (rc) return rc;
-  }
   if (mom) {   // the final state's cotangent, or zero
     for (int m = 0; m < 3; ++m) {
       rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
@@ -2066,51 +2168,74 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     return Out{op(pq, 2 * h, T * 2 * h), op(bt, bt_ld, d * bt_ld), (uint8_t*)dq + a * d * esz, n_q * d, 2 * h};
   };
   auto pset = [&](float* base, int ns, int m) -> PartSet { return PartSet{base + m * dh, ns, psplit, 3 * dh}; };
-  // tail [n_kv, n_q): applied with the final weights, on top of dW_final (or zero)
+  // The running cotangent of the current weights lives in dW; `first` while
+  // it still has to start from dW_final (or zero). The partials of the
+  // gradient's own dependence on W (bpart) and of an apply (apart) stay
+  // pending until the next update's reverse adds them, or a flush does.
   bool first = true;
-  if (any_q && n_q > n_kv) {
-    rc = weight_copies(L.nch, L.off_a, bq, 2 * h, nullptr);
-    if (rc) return rc;
-    for (int64_t a = n_kv; a < n_q; a += T) {
-      const int64_t n = std::min(T, n_q - a);
-      rc = apply_back(a, n, L.off_a, L.tail_split);
-      if (rc) return rc;
-      const Out o = dq_out(a, bq, 2 * h);
-      rc = outs(&o, 1, n, (int)d);
-      if (rc) return rc;
-      for (int m = 0; m < 3; ++m) {
-        const int mode = first ? (dWf[m] ? 1 : 0) : 2;
-        const PartSet ps = pset(apart, a_ns, m);
-        rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
-                   [&] { return launch_accum(dW[m], dh, dWf[m], dh, mode, ps, PartSet{}, p.BH, dh, s); });
+  bool a_pending = false, b_pending = false;
+  auto flush = [&]() -> int {
+    if (!first && !a_pending && !b_pending) return LACT_OK;
+    for (int m = 0; m < 3; ++m) {
+      const PartSet s0 = b_pending ? pset(bpart, b_ns, m) : PartSet{};
+      const PartSet s1 = a_pending ? pset(apart, a_ns, m) : PartSet{};
+      const int mode = first ? (dWf[m] ? 1 : 0) : 2;
+      const int r = timed(LACT_KCLASS_UPDATE, 0.0, s,
+                          [&] { return launch_accum(dW[m], dh, dWf[m], dh, mode, s0, s1, p.BH, dh, s); });
+      if (r) return r;
+    }
+    first = a_pending = b_pending = false;
+    return LACT_OK;
+  };
+  for (auto it = segs.rbegin(); it != segs.rend(); ++it) {
+    const BSeg& g = *it;
+    const int64_t s0 = g.b, n = g.e - g.b;
+    if (g.mode == LACT_SEG_APPLY_ONLY) {   // in pieces of up to T rows, with the weights of that time
+      if (a_pending) {
+        rc = flush();
         if (rc) return rc;
       }
-      first = false;
-    }
-  }
-  if (first) {
-    for (int m = 0; m < 3; ++m) {
-      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
-        return launch_accum(dW[m], dh, dWf[m], dh, dWf[m] ? 1 : 0, PartSet{}, PartSet{}, p.BH, dh, s);
-      });
+      rc = weight_copies(g.before, L.off_a, bq, 2 * h, nullptr);
       if (rc) return rc;
+      for (int64_t a = g.b; a < g.e; a += T) {
+        const int64_t na = std::min(T, g.e - a);
+        rc = apply_back(a, na, L.off_a, L.tail_split);
+        if (rc) return rc;
+        const Out o = dq_out(a, bq, 2 * h);
+        rc = outs(&o, 1, na, (int)d);
+        if (rc) return rc;
+        a_pending = true;
+        rc = flush();
+        if (rc) return rc;
+      }
+      continue;
     }
-  }
-  const bool then_apply = desc->order == LACT_UPDATE_THEN_APPLY;
-  bool a_pending = false, b_pending = false;   // partials that the next reverse adds first
-  for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
-    const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
-    if (then_apply) {   // applied with the weights leaving the chunk: its cotangent joins first
-      rc = weight_copies(ci + 1, L.off_a, bq, 2 * h, nullptr);
+    const int64_t u = g.before;
+    const bool then_apply = g.mode == LACT_SEG_UPDATE_THEN_APPLY;
+    const bool applies = g.mode != LACT_SEG_UPDATE_ONLY;
+    if (then_apply) {   // applied with the weights leaving the update: its cotangent joins first
+      if (a_pending) {
+        rc = flush();
+        if (rc) return rc;
+      }
+      rc = weight_copies(u + 1, L.off_a, bq, 2 * h, nullptr);
       if (!rc) rc = apply_back(s0, n, L.off_a, p.split_len);
       if (rc) return rc;
       a_pending = true;
     }
+    if (first) {   // the update's reverse reads the running cotangent
+      const bool ap = a_pending, bp = b_pending;
+      a_pending = b_pending = false;
+      rc = flush();
+      if (rc) return rc;
+      a_pending = ap;
+      b_pending = bp;
+    }
     // the update's reverse: W1, W3 ([h x d]) and W2 ([d x h]) in one launch
     const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {(int)h, (int)d, (int)h}, {(int)d, (int)h, (int)d}};
-    float* gslot = reinterpret_cast<float*>(ws + L.off_P + (size_t)ci * L.slotP);
-    const float* mnext[3] = {mom ? mtraj(ci + 1, 0) : nullptr, mom ? mtraj(ci + 1, 1) : nullptr,
-                             mom ? mtraj(ci + 1, 2) : nullptr};
+    float* gslot = reinterpret_cast<float*>(ws + L.off_P + (size_t)u * L.slotP);
+    const float* mnext[3] = {mom ? mtraj(u + 1, 0) : nullptr, mom ? mtraj(u + 1, 1) : nullptr,
+                             mom ? mtraj(u + 1, 2) : nullptr};
     if (p.muon) {   // the steps are Muon(g_j), or Muon(M_j) with momentum: replay the iteration
       rc = nb.forward(gslot, p.nsplit, psplit, mom ? mnext : nullptr);
       if (rc) return rc;
@@ -2119,7 +2244,7 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     for (int m = 0; m < 3; ++m) {
       VjpArgs& x = va[m];
       const bool w2 = m == 1;
-      x.W = traj(ci, m);
+      x.W = traj(u, m);
       x.w_inst = dh;
       x.P = p.muon ? pset(nb.at<float>(L.ns.pstep), 1, m)
                    : (mom ? PartSet{mnext[m], 1, 0, dh, -1.0f} : pset(gslot, p.nsplit, m));
@@ -2162,10 +2287,10 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       ma.U = p.muon ? nb.at<float>(L.ns.ug) : reinterpret_cast<float*>(ws + L.off_mu);
       for (int m = 0; m < 3; ++m) {
         ma.R[m] = dMo[m];
-        ma.M[m] = mtraj(ci, m);
+        ma.M[m] = mtraj(u, m);
       }
-      ma.bbar = bbar_all + ci;
-      ma.bbar_inst = L.nch;
+      ma.bbar = bbar_all + u;
+      ma.bbar_inst = nupd;
       ma.part = reinterpret_cast<float*>(ws + L.off_mpart);
       ma.BH = p.BH;
       ma.nmat = 3;
@@ -2186,7 +2311,7 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       if (rc) return rc;
     }
     a_pending = b_pending = false;
-    rc = weight_copies(ci, L.off_u, bk + 2 * h * esz, 4 * h, bv + h * esz);
+    rc = weight_copies(u, L.off_u, bk + 2 * h * esz, 4 * h, bv + h * esz);
     if (rc) return rc;
     const Operand ko = op(kb + s0 * d * esz, d, n_kv * d), vo = op(vb + s0 * d * esz, d, n_kv * d);
     const Out f3[3] = {{ko, op(ws + L.off_u[0], d, dh), zb[0], zi, d},
@@ -2220,7 +2345,7 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     ra.h = (int)h;
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_swiglu_rows(ra, p.bf16, s); });
     if (rc) return rc;
-    if (!then_apply) {   // applied with the weights entering the chunk (their copies are in place)
+    if (applies && !then_apply) {   // applied with the weights entering the update (their copies are in place)
       rc = apply_back(s0, n, L.off_u, p.split_len);
       if (rc) return rc;
     }
@@ -2229,23 +2354,15 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
         {op(pk, 4 * h, T * 4 * h), op(bk, 4 * h, d * 4 * h), (uint8_t*)dk + s0 * d * esz, n_kv * d, 4 * h},
         {op(pv, 2 * h, T * 2 * h), op(bv, 2 * h, d * 2 * h), (uint8_t*)dv + s0 * d * esz, n_kv * d, 2 * h},
         then_apply ? dq_out(s0, bq, 2 * h) : dq_out(s0, bk + 2 * h * esz, 4 * h)};
-    rc = outs(kvq, 3, n, (int)d);
+    rc = outs(kvq, applies ? 3 : 2, n, (int)d);
     if (rc) return rc;
     rc = grads(op(pk + 2 * h * esz, 4 * h, T * 4 * h), op(pk + 3 * h * esz, 4 * h, T * 4 * h), ko, vo,
                op(pv + h * esz, 2 * h, T * 2 * h), bpart, n, p.split_len, &b_ns);
     if (rc) return rc;
     b_pending = true;
-    a_pending = !then_apply;   // the entering weights' apply joins before the previous chunk's reverse
+    a_pending = applies && !then_apply;   // the entering weights' apply joins before the previous update's reverse
   }
-  if (a_pending || b_pending) {
-    for (int m = 0; m < 3; ++m) {
-      const PartSet s0 = b_pending ? pset(bpart, b_ns, m) : PartSet{};
-      const PartSet s1 = a_pending ? pset(apart, a_ns, m) : PartSet{};
-      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_accum(dW[m], dh, nullptr, 0, 2, s0, s1, p.BH, dh, s); });
-      if (rc) return rc;
-    }
-  }
-  return LACT_OK;
+  return flush();
 }
 
 }  // namespace
@@ -2324,6 +2441,43 @@ int lact_backward_momentum(const lact_desc* desc, const void* q, const void* k, 
   float* const dMo[3] = {dM1, dM2, dM3};
   return run_backward_swiglu(desc, q, k, v, eta, W0, dout, dWf, dq, dk, dv, deta, dW, workspace, workspace_bytes,
                              stream, beta, M0, dMf, dbeta, dMo);
+}
+
+size_t lact_backward_schedule_workspace_bytes(const lact_desc* desc, const lact_segment* segs, int64_t nseg,
+                                              int momentum, int* err) {
+  int rc = check_desc(desc);
+  std::vector<BSeg> bs;
+  int64_t nupd = 0, longest = 0;
+  if (!rc && desc->fast_weight != LACT_FW_SWIGLU) rc = LACT_EUNSUPPORTED;
+  if (!rc) rc = backward_segments(desc, segs, nseg, &bs, &nupd, &longest);
+  SwBwdLayout L;
+  if (!rc) rc = sw_bwd_layout(desc, &L, momentum != 0, nupd, longest);
+  if (err) *err = rc;
+  return rc ? 0 : L.total;
+}
+
+int lact_backward_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, const void* q,
+                           const void* k, const void* v, const float* eta, const float* beta, const float* W1,
+                           const float* W2, const float* W3, const float* M1, const float* M2, const float* M3,
+                           const void* dout, const float* dW1_final, const float* dW2_final, const float* dW3_final,
+                           const float* dM1_final, const float* dM2_final, const float* dM3_final, void* dq,
+                           void* dk, void* dv, float* deta, float* dbeta, float* dW1, float* dW2, float* dW3,
+                           float* dM1, float* dM2, float* dM3, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  const int rc = check_desc(desc);
+  if (rc) return rc;
+  if (desc->fast_weight != LACT_FW_SWIGLU) return LACT_EUNSUPPORTED;
+  if (nseg < 0 || (nseg > 0 && !segs)) return LACT_EINVAL;
+  const float* W0[3] = {W1, W2, W3};
+  const float* dWf[3] = {dW1_final, dW2_final, dW3_final};
+  float* const dW[3] = {dW1, dW2, dW3};
+  const float* M0[3] = {M1, M2, M3};
+  const float* dMf[3] = {dM1_final, dM2_final, dM3_final};
+  float* const dMo[3] = {dM1, dM2, dM3};
+  const bool mom = M1 != nullptr;
+  return run_backward_swiglu(desc, q, k, v, eta, W0, dout, dWf, dq, dk, dv, deta, dW, workspace, workspace_bytes,
+                             stream, mom ? beta : nullptr, mom ? M0 : nullptr, mom ? dMf : nullptr,
+                             mom ? dbeta : nullptr, mom ? dMo : nullptr, segs, nseg);
 }
 
 int lact_backward(const lact_desc* desc, const void* q, const void* k, const void* v, const float* eta,

@@ -407,6 +407,8 @@ hipError_t launch_swiglu_apply_rows(const void* Z1, const void* Z3, const void* 
                                     hipStream_t s);
 hipError_t launch_zero_rows(void* out, int BH, int64_t row_bytes, int64_t rows, int64_t r0, int64_t r1,
                             hipStream_t s);
+// x[i * inst + off + j] = 0 for j in [0, count), instances i in [0, BH).
+hipError_t launch_zero_f32(float* x, int BH, int64_t inst, int64_t off, int64_t count, hipStream_t s);
 constexpr int kNsBlockElems = 4096;
 
 }  // namespace lact

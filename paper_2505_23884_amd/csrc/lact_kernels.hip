@@ -2765,6 +2765,14 @@ __global__ __launch_bounds__(256) void k_swiglu_apply_rows(const T* Z1, const T*
   }
 }
 
+// x[i * inst + off + j] = 0 for j < count, every instance i (grid stride).
+__global__ __launch_bounds__(256) void k_zero_f32(float* x, int64_t inst, int64_t off, int64_t count, int64_t total) {
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
+    const int64_t i = t / count;
+    x[i * inst + off + (t - i * count)] = 0.0f;
+  }
+}
+
 // Rows [r0, r1) of every instance of a row-major [BH, n, d] output set to zero
 // (tokens that no apply segment of a schedule covers): nvec 16-byte vectors
 // per instance, grid-stride over all instances.
@@ -2879,6 +2887,14 @@ hipError_t launch_zero_rows(void* out, int BH, int64_t row_bytes, int64_t rows, 
   const int64_t need = (total + 255) / 256, blocks = need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20);
   k_zero_rows<<<(unsigned)blocks, 256, 0, s>>>(reinterpret_cast<uint8_t*>(out), rows * row_bytes, r0 * row_bytes,
                                                nvec, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_f32(float* x, int BH, int64_t inst, int64_t off, int64_t count, hipStream_t s) {
+  const int64_t total = (int64_t)BH * count;
+  if (total <= 0) return hipSuccess;
+  const int64_t need = (total + 255) / 256, blocks = need < ((int64_t)1 << 20) ? need : ((int64_t)1 << 20);
+  k_zero_f32<<<(unsigned)blocks, 256, 0, s>>>(x, inst, off, count, total);
   return hipGetLastError();
 }
 

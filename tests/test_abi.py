@@ -374,3 +374,55 @@ def test_momentum_backward_errors_before_any_hip_call(fw):
     # no key tokens: beta and dbeta may be NULL as well
     nk = make_desc(**dict(base, n_kv=0))
     assert _bwd_mom(nk, k=0, v=0, eta=0, beta=0, dk=0, dv=0, deta=0, dbeta=0, ws=0) == -3
+
+
+def _bwd_sched(desc, segs, nbytes=None, mom=False, **kw):
+    names = ("q", "k", "v", "eta", "beta", "w1", "w2", "w3", "m1", "m2", "m3", "do", "f1", "f2", "f3", "g1", "g2",
+             "g3", "dq", "dk", "dv", "deta", "dbeta", "d1", "d2", "d3", "e1", "e2", "e3", "ws")
+    a = {n: 0x1000 * (i + 1) for i, n in enumerate(names)}
+    for n in ("f1", "f2", "f3", "g1", "g2", "g3"):
+        a[n] = 0
+    if not mom:
+        for n in ("beta", "m1", "m2", "m3", "dbeta", "e1", "e2", "e3"):
+            a[n] = 0
+    a["ws"] = 0x100000
+    a.update(kw)
+    arr = (P.binding.LactSegment * max(len(segs), 1))()
+    for i, (m, b, e) in enumerate(segs):
+        arr[i] = P.binding.LactSegment(m, 0, b, e)
+    if nbytes is None:
+        err = ctypes.c_int(0)
+        nbytes = P.lib().lact_backward_schedule_workspace_bytes(ctypes.byref(desc), arr, len(segs), int(mom),
+                                                                ctypes.byref(err))
+    vp = ctypes.c_void_p
+    return P.lib().lact_backward_schedule(ctypes.byref(desc), arr, len(segs), *(vp(a[n]) for n in names),
+                                          ctypes.c_size_t(nbytes), vp(0))
+
+
+def test_schedule_backward_errors_before_any_hip_call():
+    d = make_desc(**dict(GOOD, n_kv=1000, n_q=1100, chunk=256))
+    segs = [(3, 0, 256), (1, 256, 512), (2, 512, 700), (0, 700, 956), (3, 956, 1100)]
+    err = ctypes.c_int(0)
+    arr = (P.binding.LactSegment * len(segs))(*(P.binding.LactSegment(m, 0, b, e) for m, b, e in segs))
+    nb = P.lib().lact_backward_schedule_workspace_bytes(ctypes.byref(d), arr, len(segs), 0, ctypes.byref(err))
+    assert err.value == 0 and nb > 0
+    # three updates: less than the uniform schedule's four chunks; momentum adds the state's trajectory
+    assert nb < P.binding.backward_workspace_bytes(d)
+    nbm = P.lib().lact_backward_schedule_workspace_bytes(ctypes.byref(d), arr, len(segs), 1, ctypes.byref(err))
+    assert nbm > nb
+    assert _bwd_sched(d, segs, ws=0) == -3
+    assert _bwd_sched(d, segs, nbytes=nb - 1) == -3
+    assert _bwd_sched(d, segs, mom=True, ws=0) == -3
+    assert _bwd_sched(d, segs, mom=True, dbeta=0) == -1
+    assert _bwd_sched(d, segs, mom=True, m2=0) == -1
+    assert _bwd_sched(d, segs, dq=0) == -1
+    assert _bwd_sched(d, [(2, 0, 300)]) == -1          # an update longer than the chunk
+    assert _bwd_sched(d, [(4, 0, 10)]) == -1           # an unknown mode
+    assert _bwd_sched(d, [(3, 0, 1200)]) == -1         # an apply past n_q
+    # overlapping applies, or overlapping updates: not differentiated
+    assert _bwd_sched(d, [(3, 0, 100), (3, 50, 150)]) == -4
+    assert _bwd_sched(d, [(2, 0, 100), (2, 50, 150)]) == -4
+    # the linear fast weight has no schedule backward
+    assert _bwd_sched(make_desc(**dict(GOOD, h=64, fast_weight=1)), segs) == -4
+    # an empty schedule reaches the workspace check
+    assert _bwd_sched(d, [], ws=0) == -3

@@ -1828,6 +1828,121 @@ def test_swiglu_momentum_muon_backward_per_matrix_rates(order):
     check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
 
 
+# ----------------------------------------------------------------------------- schedule backward
+# lact_backward_schedule: the reverse of a caller-given segment list against
+# the oracle's (pinned to torch autograd of a schedule loop and to the chunk
+# loop's backward for uniform chunks).
+
+
+def run_gpu_sched_bwd(cfg, x, ct, schedule, st=None, with_final=True):
+    print(f"[gpu] schedule backward {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} h={cfg.h} n_kv={cfg.n_kv} "
+          f"n_q={cfg.n_q} segments={len(schedule)} io={cfg.io} muon={cfg.use_muon} momentum={st is not None}",
+          flush=True)
+    n = len(x["q"])
+    B, H = (cfg.B, cfg.H) if n == cfg.BH else (n, 1)
+    sh = lambda a: a.reshape(B, H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    dev = lambda names, src: tuple(to_dev(sh(src[w]), cfg, torch.float32) for w in names)
+    W = dev(("W1", "W2", "W3"), x)
+    dWf = dev(("dW1", "dW2", "dW3"), ct) if with_final else None
+    kw = {}
+    if st is not None:
+        kw = dict(beta=to_dev(sh(x["beta"]), cfg, torch.float32), M=dev(("M1", "M2", "M3"), st),
+                  dM_final=dev(("dM1", "dM2", "dM3"), ct) if with_final else None)
+    do = to_dev(sh(ct["do"]), cfg)
+    r = P.backward_schedule(q, k, v, eta, *W, do, schedule, dW_final=dWf, use_muon=bool(cfg.use_muon),
+                            ns_steps=cfg.ns_steps, chunk=cfg.chunk, **kw)
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    nh = 5 if st is not None else 4
+    out = tuple(f(t) for t in r[:nh]) + tuple(f(t) for t in r[nh])
+    if st is not None:
+        out += tuple(f(t) for t in r[6])
+    return out
+
+
+def check_sched_bwd(cfg, x, ct, schedule, got, st=None, with_final=True):
+    def ref_fn(xx):
+        kw = {}
+        if st is not None:
+            kw = dict(beta=xx["beta"], M=tuple(st[m] for m in ("M1", "M2", "M3")),
+                      dM_final=tuple(ct[m] for m in ("dM1", "dM2", "dM3")) if with_final else None)
+        return O.lact_backward_schedule(xx["q"], xx["k"], xx["v"], xx["eta"], xx["W1"], xx["W2"], xx["W3"],
+                                        ct["do"], schedule,
+                                        dW_final=tuple(ct[w] for w in ("dW1", "dW2", "dW3")) if with_final else None,
+                                        use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps, **kw)
+    ref = ref_fn(x)
+    names = ["dq", "dk", "dv", "deta"] + (["dbeta"] if st is not None else []) + ["dW1", "dW2", "dW3"] + \
+        (["dM1", "dM2", "dM3"] if st is not None else [])
+    errs, blocks = {}, {}
+    for name, g, r in zip(names, got, ref):
+        # rows that the schedule leaves without a cotangent are exact zeros on both sides
+        zero = ~np.any(r.reshape(r.shape[0], r.shape[1], -1) != 0, axis=-1) if name in ("dq", "dk", "dv") else None
+        if zero is not None:
+            assert not np.any(g[zero]), name
+        errs[name] = rel(g, r)
+        if name in ("deta", "dbeta"):
+            blocks[name] = worst_window(g, r, O_BLOCK)
+        else:
+            blocks[name] = worst_block(g, r, W_BLOCK if name.startswith(("dW", "dM")) else O_BLOCK)
+    if not cfg.use_muon:
+        assert_errs(errs, TOL[cfg.io], blocks)
+        return
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io])
+    wb, bb = dict(zip(names, whole)), dict(zip(names, block))
+    if st is not None:   # as in the momentum backward's Muon tests: few per-update values
+        wb["dbeta"], bb["dbeta"] = float("inf"), float("inf")
+    assert_bars(errs, blocks, wb, bb)
+
+
+def mixed_schedule(C):
+    """Every mode, an apply-only stretch between updates, output rows no apply
+    covers (zeros) and key rows no update uses."""
+    return [("apply_then_update", 0, C), ("apply_only", C, 2 * C), ("update_then_apply", 2 * C, 3 * C - 40),
+            ("update_only", 3 * C - 40, 4 * C - 40), ("apply_only", 3 * C - 40, 4 * C - 40),
+            ("apply_then_update", 4 * C, 5 * C - 7), ("apply_only", 5 * C + 20, 6 * C + 33)]
+
+
+def test_schedule_backward_mixed_bf16():
+    C = 128
+    cfg = CONFIGS["lm32k"].with_(name="sched_bwd_mixed", B=1, H=2, d=128, h=256, n_kv=6 * C, n_q=6 * C + 40,
+                                 chunk=C)
+    x, ct = make_inputs(cfg, 111), make_cotangents(cfg, 111)
+    sched = mixed_schedule(C)
+    check_sched_bwd(cfg, x, ct, sched, run_gpu_sched_bwd(cfg, x, ct, sched))
+
+
+def test_schedule_backward_mixed_momentum_fp32_per_matrix_rates():
+    C = 64
+    cfg = CONFIGS["tiny_fp32"].with_(name="sched_bwd_mom_fp32", B=2, H=1, d=40, h=56, n_kv=6 * C, n_q=6 * C + 40,
+                                     chunk=C, lr3=1, momentum=1)
+    x, ct, st = make_inputs(cfg, 112), make_cotangents(cfg, 112), make_momentum_state(cfg, 112)
+    sched = mixed_schedule(C)
+    check_sched_bwd(cfg, x, ct, sched, run_gpu_sched_bwd(cfg, x, ct, sched, st), st)
+
+
+def test_schedule_backward_video_teacher_forcing_muon():
+    # the strided mask: noisy chunks applied only, clean ones update then
+    # apply (5 chunks of 256 tokens: 2 updates), video head shape, Muon
+    cfg = CONFIGS["video_tf"].with_(name="sched_bwd_video_tf", H=2, n_kv=5 * 256, n_q=5 * 256, chunk=256)
+    from lact_synth import make_schedule
+    sched = make_schedule(cfg)
+    x, ct = make_inputs(cfg, 113), make_cotangents(cfg, 113)
+    check_sched_bwd(cfg, x, ct, sched, run_gpu_sched_bwd(cfg, x, ct, sched))
+
+
+def test_schedule_backward_of_uniform_chunks_is_lact_backward_bitwise():
+    cfg = CONFIGS["lm32k"].with_(name="sched_bwd_uniform", B=1, H=2, d=128, h=256, n_kv=600, n_q=640, chunk=256,
+                                 order=1)
+    x, ct = make_inputs(cfg, 114), make_cotangents(cfg, 114)
+    sched = [("update_then_apply", s, min(600, s + 256)) for s in range(0, 600, 256)] + [("apply_only", 600, 640)]
+    a = run_gpu_sched_bwd(cfg, x, ct, sched)
+    b = run_gpu_swiglu_bwd(cfg, x, ct)
+    for name, u, w in zip(("dq", "dk", "dv", "deta", "dW1", "dW2", "dW3"), a, b):
+        assert np.array_equal(u, w), name
+
+
 # ----------------------------------------------------------------------------- envelope limits
 # The largest head and hidden dims (4096), very many instances, the most
 # Newton-Schulz steps, and a chunk longer than the sequence.

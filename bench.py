@@ -185,7 +185,7 @@ def kernel_short_name(name):
     for k in ("k_fwd_narrow", "k_fwd", "k_bwd", "k_update", "k_prep", "k_scale_rows", "k_beta_mean", "k_zero_rows",
               "k_ns_fused_pair_out", "k_ns_fused_pair", "k_ns_fused", "k_ns_final", "k_ns_prep", "k_ns_scale", "k_ns",
               "k_prologue", "k_rmsnorm_out", "k_vjp", "k_lin_tokens", "k_copies", "k_accum", "k_swiglu_apply_rows",
-              "k_swiglu_rows", "k_mom_bwd", "k_mom_dbeta", "k_mom_adv", "k_slot_dot", "k_ns_lin", "k_sym"):
+              "k_swiglu_rows", "k_mom_bwd", "k_mom_dbeta", "k_mom_adv", "k_slot_dot_part", "k_slot_dot_sum", "k_ns_lin", "k_sym"):
         m = str(len(k)) + k
         if m + "I" in name or m + "E" in name or "::" + k + "<" in name or "::" + k + "(" in name:
             return k
@@ -275,8 +275,9 @@ def backward_flops(cfg, BH=None):
     (K W1^T, K W3^T, V W2 in the reverse) are not counted. With Muon, per
     chunk and matrix: the replayed iteration (App. A: 4 m^2 n + 2 m^3 per
     step, m <= n its sides) and its reverse (dX' X^T, B dX', M X and S A:
-    6 m^2 n + 2 m^3 per step); the second replay that the reverse makes to
-    recover the iterates is not counted. Momentum adds elementwise passes
+    6 m^2 n + 2 m^3 per step). The iteration runs once, in the replay, with
+    its iterates kept (where they fit; else it is replayed per chunk in the
+    reverse, which is not counted). Momentum adds elementwise passes
     over the state only (no products). A schedule counts its update
     segments' key tokens and its apply segments' query tokens."""
     BH = cfg.BH if BH is None else BH

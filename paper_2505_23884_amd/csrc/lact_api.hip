@@ -295,6 +295,7 @@ struct Ctx {
   BwdArgs out_pending{};   // with ns_out: the output tiles the next Newton-Schulz launch runs
   double out_flops = 0.0;
   bool has_out = false;
+  bool grad_only = false;   // update_chunk stops after the gradient partials (the backward's own update follows)
   const float* Wsrc[3] = {};   // where the update reads the state (nullptr: W, in place)
 };
 
@@ -754,6 +755,7 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     use_wset(c, c.wset ^ 1);
     return LACT_OK;
   }
+  if (c.grad_only) return LACT_OK;
   return finish_update(c);
 }
 
@@ -1096,14 +1098,22 @@ int run_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, 
 // fp32 partials), fp32 iterates.
 struct NsBwdLayout {
   int S, m, n;
-  size_t g, x32, p1, p2, x16, a16, b16, t16, q16, s16, m16, db16, nrm, dot, pstep, ustep, ug, total;
+  int64_t iters;   // slices of the iterates and steps: 1 (replayed per chunk) or one per chunk (kept)
+  size_t g, x32, p1, p2, x16, a16, b16, t16, q16, s16, m16, db16, nrm, dot, dotp, pstep, ustep, ug, total;
 };
 
-size_t ns_bwd_layout(const Plan& p, int steps, size_t o, NsBwdLayout* N) {
+// Chunks whose Newton-Schulz iterates and steps the backward keeps (each
+// chunk's iteration then runs once, in the replay), within this many bytes.
+constexpr double kKeepIterBytes = 24.0 * (1 << 30);
+
+size_t ns_bwd_layout(const Plan& p, int steps, size_t o, NsBwdLayout* N, int64_t nch = 1) {
   N->S = p.BH * p.nmat;
   N->m = std::min(p.d, p.h);
   N->n = std::max(p.d, p.h);
   const size_t mn = (size_t)N->m * N->n, mm = (size_t)N->m * N->m, S = N->S;
+  const double per = ((double)std::max(steps, 1) * S * (mn + 2 * mm) * 2.0 + (double)S * mn * 4.0);
+  N->iters = nch > 1 && per * nch <= kKeepIterBytes ? nch : 1;
+  const size_t it = (size_t)N->iters;
   auto take = [&](size_t bytes) {
     const size_t at = o;
     o = align_up(o + bytes);
@@ -1113,9 +1123,9 @@ size_t ns_bwd_layout(const Plan& p, int steps, size_t o, NsBwdLayout* N) {
   N->x32 = take(S * mn * 4);
   N->p1 = take(S * mn * 4);
   N->p2 = take(S * mn * 4);
-  N->x16 = take((size_t)std::max(steps, 1) * S * mn * 2);
-  N->a16 = take((size_t)std::max(steps, 1) * S * mm * 2);
-  N->b16 = take((size_t)std::max(steps, 1) * S * mm * 2);
+  N->x16 = take(it * std::max(steps, 1) * S * mn * 2);
+  N->a16 = take(it * std::max(steps, 1) * S * mm * 2);
+  N->b16 = take(it * std::max(steps, 1) * S * mm * 2);
   N->t16 = take(S * mn * 2);
   N->q16 = take(S * mm * 2);
   N->s16 = take(S * mm * 2);
@@ -1123,7 +1133,8 @@ size_t ns_bwd_layout(const Plan& p, int steps, size_t o, NsBwdLayout* N) {
   N->db16 = take(S * mm * 2);
   N->nrm = take(S * 4);
   N->dot = take(S * 4);
-  N->pstep = take(S * mn * 4);   // stored layouts [inst][nmat][d h]
+  N->dotp = take(S * 32 * 4);   // the dot products' per-workgroup partials
+  N->pstep = take(it * S * mn * 4);   // stored layouts [inst][nmat][d h]
   N->ustep = take(S * mn * 4);
   N->ug = take(S * mn * 4);
   N->total = o;
@@ -1137,6 +1148,7 @@ struct NsBwd {
   hipStream_t s;
   int steps;
   int R[3], L[3];   // stored shape of matrix j
+  int64_t ci = 0;   // the chunk whose slice of kept iterates is used (with one slice: always slice 0)
   template <class T>
   T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
   int64_t mn() const { return (int64_t)N.m * N.n; }
@@ -1282,10 +1294,23 @@ struct NsBwd {
     l.len = mn();
     return timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_ns_lin(l, s); });
   }
-  _Float16* X16(int k) const { return at<_Float16>(N.x16) + (size_t)k * N.S * mn(); }
-  _Float16* A16(int k) const { return at<_Float16>(N.a16) + (size_t)k * N.S * mm(); }
-  _Float16* B16(int k) const { return at<_Float16>(N.b16) + (size_t)k * N.S * mm(); }
+  size_t sk(int k) const { return (size_t)(ci % N.iters) * steps + k; }   // step k of this chunk's slice
+  _Float16* X16(int k) const { return at<_Float16>(N.x16) + sk(k) * N.S * mn(); }
+  _Float16* A16(int k) const { return at<_Float16>(N.a16) + sk(k) * N.S * mm(); }
+  _Float16* B16(int k) const { return at<_Float16>(N.b16) + sk(k) * N.S * mm(); }
+  float* pst() const { return at<float>(N.pstep) + (size_t)(ci % N.iters) * N.S * mn(); }   // the step, negated
+  bool kept() const { return N.iters > 1; }
 
+  // What the reverse needs besides the kept iterates: the iteration's input
+  // G (from P or the slabs, as forward) and its squared norm.
+  int prepare(const float* P, int nsplit, int64_t split, const float* const* slabs = nullptr) const {
+    float* G = at<float>(N.g);
+    int rc = slabs ? gather_slabs(slabs, 1.0f, G) : gather(P, nsplit, split, -1.0f, G);
+    if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] {
+      return launch_slot_dot(G, G, N.S, mn(), at<float>(N.nrm), at<float>(N.dotp), s);
+    });
+    return rc;
+  }
   // The step -Muon(g) of the gradient whose negated split partials are
   // P (stored layout), into pstep (stored layout, one split); with slabs,
   // of the momentum state in per-matrix slabs instead.
@@ -1293,7 +1318,7 @@ struct NsBwd {
     float* G = at<float>(N.g);
     float* X = at<float>(N.x32);
     int rc = slabs ? gather_slabs(slabs, 1.0f, G) : gather(P, nsplit, split, -1.0f, G);
-    if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_slot_dot(G, G, N.S, mn(), at<float>(N.nrm), s); });
+    if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_slot_dot(G, G, N.S, mn(), at<float>(N.nrm), at<float>(N.dotp), s); });
     if (!rc) rc = lin(0, G, nullptr, nullptr, nullptr, at<float>(N.nrm), nullptr, 0.f, X, steps > 0 ? X16(0) : nullptr);
     for (int k = 0; k < steps && !rc; ++k) {
       rc = out(X16(k), N.n, mn(), X16(k), N.n, mn(), A16(k), N.m, N.m, N.n);   // A = X X^T
@@ -1308,7 +1333,7 @@ struct NsBwd {
       if (!rc) rc = lin(1, X, nullptr, at<float>(N.p1), nullptr, nullptr, nullptr, (float)kNsA, X,
                         k + 1 < steps ? X16(k + 1) : nullptr);
     }
-    if (!rc) rc = scatter(X, -1.0f, at<float>(N.pstep));
+    if (!rc) rc = scatter(X, -1.0f, pst());
     return rc;
   }
   // From the update's cotangent of U = W - step (ustep, stored layout), the
@@ -1336,7 +1361,7 @@ struct NsBwd {
       if (!rc) rc = lin(1, X, nullptr, at<float>(N.p1), at<float>(N.p2), nullptr, nullptr, (float)kNsA, X,
                         k > 0 ? T : nullptr);
     }
-    if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_slot_dot(X, G, N.S, mn(), at<float>(N.dot), s); });
+    if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_slot_dot(X, G, N.S, mn(), at<float>(N.dot), at<float>(N.dotp), s); });
     if (!rc) rc = lin(2, X, G, nullptr, nullptr, at<float>(N.nrm), at<float>(N.dot), 0.f, X, nullptr);
     if (!rc) rc = scatter(X, -1.0f, at<float>(N.ug));
     return rc;
@@ -1409,7 +1434,7 @@ int bwd_layout(const lact_desc* dsc, BwdLayout* L, bool mom = false) {
   o = align_up(o + wio);
   L->off_ut = o;
   o = align_up(o + wio);
-  if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns);
+  if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns, L->nch);
   L->mom = mom;
   if (mom) {
     L->off_mtraj = o;
@@ -1580,8 +1605,8 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
       u.bbar = bbar_all + ci;
       u.bbar_stride = (int)L.nch;
     }
-    if (p.muon) {
-      const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}};
+    if (p.muon) {   // the iterates go to this chunk's slice when they are kept
+      const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}, ci};
       const float* slab[3] = {mtraj(ci + 1), nullptr, nullptr};
       if (mom) {
         rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
@@ -1592,7 +1617,7 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
       }
       rc = nb.forward(Pall + ci * psplit, 1, psplit, mom ? slab : nullptr);
       if (rc) return rc;
-      u.step = nb.at<float>(L.ns.pstep);
+      u.step = nb.pst();
     }
     u.nsplit = 1;
     u.step_split = 0;
@@ -1657,16 +1682,17 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
   uint8_t* ut = ws + L.off_ut;
   for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
     const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
-    const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}};
+    const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}, ci};
     const float* slab[3] = {mom ? mtraj(ci + 1) : nullptr, nullptr, nullptr};
-    if (p.muon) {   // the step is Muon(g), or Muon(M_{c+1}): replay the iteration into its negation
-      rc = nb.forward(Pall + ci * psplit, 1, psplit, mom ? slab : nullptr);
+    if (p.muon) {   // the step is Muon(g), or Muon(M_{c+1}): its kept iterates, else replay the iteration
+      rc = nb.kept() ? nb.prepare(Pall + ci * psplit, 1, psplit, mom ? slab : nullptr)
+                     : nb.forward(Pall + ci * psplit, 1, psplit, mom ? slab : nullptr);
       if (rc) return rc;
     }
     VjpArgs va{};
     va.W = traj(ci);
     va.w_inst = dd;
-    va.P = p.muon ? PartSet{nb.at<float>(L.ns.pstep), 1, psplit, dd}
+    va.P = p.muon ? PartSet{nb.pst(), 1, psplit, dd}
                   : (mom ? PartSet{mtraj(ci + 1), 1, 0, dd, -1.0f} : PartSet{Pall + ci * psplit, 1, psplit, dd});
     const PartSet ac{Aall + ci * psplit, 1, psplit, dd};
     if (then_apply) va.pre[0] = ac;   // applied with the weights leaving the chunk
@@ -1811,7 +1837,7 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false, int64_
   for (int i = 0; i < 3; ++i) L->off_ur[i] = take(wio);   // U1, U3 row-major and U2^T
   L->off_apart = take((size_t)p.nsplit * 3 * w4);
   L->off_bpart = take((size_t)p.nsplit * 3 * w4);
-  if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns);
+  if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns, L->nch);
   L->mom = mom;
   if (mom) {
     L->off_mtraj = take((size_t)L->nch * 3 * w4);
@@ -2010,10 +2036,11 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
         c.M[m] = mtraj(u + 1, m);
       }
     }
+    const bool keep = p.muon && L.ns.iters > 1;   // the iteration runs here, once, its iterates kept
     for (int m = 0; m < 3; ++m) {
       c.W[m] = traj(u + 1, m);
       c.Wsrc[m] = traj(u, m);
-      if (p.muon) {   // Muon's fused last steps update W in place: start from a copy
+      if (p.muon && !keep) {   // Muon's fused last steps update W in place: start from a copy
         c.Wsrc[m] = nullptr;
         rc = timed(LACT_KCLASS_PREP, 0.0, c.s,
                    [&] { return hipMemcpyAsync(traj(u + 1, m), traj(u, m), w4, hipMemcpyDeviceToDevice, c.s); });
@@ -2026,8 +2053,43 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       c.wop[2] = op(traj(u, 2), d, dh);
     }
     c.p.off_step = L.off_P + (size_t)u * L.slotP;
+    c.grad_only = keep;
     rc = update_chunk(c, g.b, g.e, false);
+    c.grad_only = false;
     if (rc) return rc;
+    if (keep) {
+      float* gslot = reinterpret_cast<float*>(ws + c.p.off_step);
+      const float* mnext[3] = {mom ? mtraj(u + 1, 0) : nullptr, mom ? mtraj(u + 1, 1) : nullptr,
+                               mom ? mtraj(u + 1, 2) : nullptr};
+      if (mom) {   // M_{u+1} = bbar M_u + g (the copy above is overwritten)
+        for (int m = 0; m < 3; ++m) {
+          rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
+            return launch_mom_adv(mtraj(u, m), bbar_all + u, nupd,
+                                  PartSet{gslot + m * dh, p.nsplit, psplit, 3 * dh}, mtraj(u + 1, m), p.BH, dh, s);
+          });
+          if (rc) return rc;
+        }
+      }
+      const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {(int)h, (int)d, (int)h}, {(int)d, (int)h, (int)d}, u};
+      rc = nb.forward(gslot, p.nsplit, psplit, mom ? mnext : nullptr);
+      if (rc) return rc;
+      UpdArgs ua{};
+      for (int m = 0; m < 3; ++m) {
+        ua.W[m] = traj(u + 1, m);
+        ua.Wsrc[m] = traj(u, m);
+        ua.Wb[m] = c.wb[c.wset][m];
+      }
+      ua.step = nb.pst();
+      ua.nsplit = 1;
+      ua.step_split = 0;
+      ua.BH = p.BH;
+      ua.d = p.d;
+      ua.h = p.h;
+      ua.nmat = 3;
+      ua.rows_total = p.BH * (2 * p.h + p.d);
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_update(ua, p.bf16, s); });
+      if (rc) return rc;
+    }
   }
   c.p.off_step = L.p.off_step;
   if (mom) {   // the final state's cotangent, or zero
@@ -2232,12 +2294,13 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       b_pending = bp;
     }
     // the update's reverse: W1, W3 ([h x d]) and W2 ([d x h]) in one launch
-    const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {(int)h, (int)d, (int)h}, {(int)d, (int)h, (int)d}};
+    const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {(int)h, (int)d, (int)h}, {(int)d, (int)h, (int)d}, u};
     float* gslot = reinterpret_cast<float*>(ws + L.off_P + (size_t)u * L.slotP);
     const float* mnext[3] = {mom ? mtraj(u + 1, 0) : nullptr, mom ? mtraj(u + 1, 1) : nullptr,
                              mom ? mtraj(u + 1, 2) : nullptr};
-    if (p.muon) {   // the steps are Muon(g_j), or Muon(M_j) with momentum: replay the iteration
-      rc = nb.forward(gslot, p.nsplit, psplit, mom ? mnext : nullptr);
+    if (p.muon) {   // the steps are Muon(g_j), or Muon(M_j) with momentum: kept iterates, else a replay
+      rc = nb.kept() ? nb.prepare(gslot, p.nsplit, psplit, mom ? mnext : nullptr)
+                     : nb.forward(gslot, p.nsplit, psplit, mom ? mnext : nullptr);
       if (rc) return rc;
     }
     VjpArgs va[3] = {};
@@ -2246,7 +2309,7 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       const bool w2 = m == 1;
       x.W = traj(u, m);
       x.w_inst = dh;
-      x.P = p.muon ? pset(nb.at<float>(L.ns.pstep), 1, m)
+      x.P = p.muon ? pset(nb.pst(), 1, m)
                    : (mom ? PartSet{mnext[m], 1, 0, dh, -1.0f} : pset(gslot, p.nsplit, m));
       if (b_pending) x.pre[0] = pset(bpart, b_ns, m);
       if (a_pending) x.pre[1] = pset(apart, a_ns, m);

@@ -337,8 +337,10 @@ hipError_t launch_copies_f32(const CopySeg* c, int n, int BH, hipStream_t s);
 // ---- reverse of Newton-Schulz (slots of wide [m x n] fp32 matrices) --------
 // The k_bwd kinds with fp16 operands (fp16 OUT results, fp32 GRAD partials).
 hipError_t launch_bwd_f16(const BwdArgs& a, hipStream_t s);
-// out[s] = sum over len elements of x[s] * y[s] (slot s), one workgroup per slot.
-hipError_t launch_slot_dot(const float* x, const float* y, int S, int64_t len, float* out, hipStream_t s);
+// out[s] = sum over len elements of x[s] * y[s] (slot s), in a fixed order
+// (32 workgroups per slot, then their partials in order).
+hipError_t launch_slot_dot(const float* x, const float* y, int S, int64_t len, float* out, float* part,
+                           hipStream_t s);   // part: S * 32 floats of scratch
 // Elementwise over S slots of len floats (x, y, p1, p2 fp32; sc, sc2 per slot):
 //   mode 0: out = x / (sqrt(sc) + eps)
 //   mode 1: out = a x + p1 (+ p2 when given)

@@ -2536,19 +2536,35 @@ __global__ __launch_bounds__(256) void k_mom_adv(const float* M, const float* bb
 
 // Sum over one slot of x * y, one workgroup per slot (a fixed reduction
 // order, so repeated calls agree bit for bit).
-__global__ __launch_bounds__(256) void k_slot_dot(const float* x, const float* y, int64_t len, float* out) {
+// Sum over one slot of x * y in two passes of fixed order: kDotBlocks
+// workgroups per slot each sum a contiguous range of float4s into part,
+// then one wave per slot adds the slot's partials in order.
+constexpr int kDotBlocks = 32;
+__global__ __launch_bounds__(256) void k_slot_dot_part(const float* x, const float* y, int64_t len, float* part) {
   __shared__ float red[4];
-  const float4* x4 = reinterpret_cast<const float4*>(x + blockIdx.x * len);
-  const float4* y4 = reinterpret_cast<const float4*>(y + blockIdx.x * len);
+  const int64_t slot = blockIdx.x / kDotBlocks;
+  const int b = (int)(blockIdx.x - slot * kDotBlocks);
+  const int64_t n4 = len >> 2, per = (n4 + kDotBlocks - 1) / kDotBlocks;
+  const int64_t i0 = b * per, i1 = i0 + per < n4 ? i0 + per : n4;
+  const float4* x4 = reinterpret_cast<const float4*>(x + slot * len);
+  const float4* y4 = reinterpret_cast<const float4*>(y + slot * len);
   float acc = 0.0f;
-  for (int64_t i = threadIdx.x; i < (len >> 2); i += 256) {
-    const float4 a = x4[i], b = y4[i];
-    acc += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+  for (int64_t i = i0 + threadIdx.x; i < i1; i += 256) {
+    const float4 a = x4[i], c = y4[i];
+    acc += a.x * c.x + a.y * c.y + a.z * c.z + a.w * c.w;
   }
   acc = wave_sum(acc);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
   __syncthreads();
-  if (threadIdx.x == 0) out[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+  if (threadIdx.x == 0) part[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ __launch_bounds__(64) void k_slot_dot_sum(const float* part, float* out) {
+  if (threadIdx.x == 0) {
+    float t = 0.0f;
+    for (int b = 0; b < kDotBlocks; ++b) t += part[(int64_t)blockIdx.x * kDotBlocks + b];
+    out[blockIdx.x] = t;
+  }
 }
 
 // Elementwise steps of the Newton-Schulz reverse (see NsLinArgs), grid stride.
@@ -2584,27 +2600,42 @@ __global__ __launch_bounds__(256) void k_ns_lin(const NsLinArgs a) {
 
 // out = alpha X + beta (Y + Y^T) per slot of fp16 [m x m] matrices: one
 // 32 x 32 output tile per block, Y's mirror tile through LDS.
+// 64 x 64 tiles, each row segment moved as 16-byte vectors of 8 halves (m is
+// a multiple of 8, so a vector lies wholly inside or outside the matrix);
+// the mirror tile goes through LDS.
 __global__ __launch_bounds__(256) void k_sym(const _Float16* X, float alpha, const _Float16* Y, float beta,
                                              _Float16* out, int m, int tiles) {
-  __shared__ float mir[32][33];
+  typedef __attribute__((ext_vector_type(8))) _Float16 h8;
+  __shared__ float mir[64][65];
   const int per = tiles * tiles;
   const int64_t slot = blockIdx.x / per;
   const int rest = blockIdx.x - (int)slot * per;
-  const int r0 = (rest / tiles) * 32, c0 = (rest % tiles) * 32;
+  const int r0 = (rest / tiles) * 64, c0 = (rest % tiles) * 64;
   const int64_t base = slot * (int64_t)m * m;
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  for (int k = ty; k < 32; k += 8) {   // mirror tile: Y[c0 + k][r0 + tx]
-    const int r = c0 + k, c = r0 + tx;
-    mir[k][tx] = (r < m && c < m) ? (float)Y[base + (int64_t)r * m + c] : 0.0f;
+  const int tv = threadIdx.x & 7, ty = threadIdx.x >> 3;   // 8 vectors per 64-wide row, 32 rows per pass
+  for (int k = ty; k < 64; k += 32) {   // mirror tile: mir[k][j] = Y[c0 + k][r0 + j]
+    const int r = c0 + k, c = r0 + 8 * tv;
+    h8 y = {};
+    if (r < m && c < m) y = *reinterpret_cast<const h8*>(Y + base + (int64_t)r * m + c);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mir[k][8 * tv + j] = (float)y[j];
   }
   __syncthreads();
-  for (int k = ty; k < 32; k += 8) {
-    const int r = r0 + k, c = c0 + tx;
+  for (int k = ty; k < 64; k += 32) {
+    const int r = r0 + k, c = c0 + 8 * tv;
     if (r >= m || c >= m) continue;
     const int64_t o = base + (int64_t)r * m + c;
-    float v = beta * ((float)Y[o] + mir[tx][k]);
-    if (X) v += alpha * (float)X[o];
-    out[o] = (_Float16)v;
+    const h8 y = *reinterpret_cast<const h8*>(Y + o);
+    h8 x = {};
+    if (X) x = *reinterpret_cast<const h8*>(X + o);
+    h8 v;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      float t = beta * ((float)y[j] + mir[8 * tv + j][k]);
+      if (X) t += alpha * (float)x[j];
+      v[j] = (_Float16)t;
+    }
+    *reinterpret_cast<h8*>(out + o) = v;
   }
 }
 
@@ -3065,9 +3096,12 @@ hipError_t launch_bwd_f16(const BwdArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_slot_dot(const float* x, const float* y, int S, int64_t len, float* out, hipStream_t s) {
+hipError_t launch_slot_dot(const float* x, const float* y, int S, int64_t len, float* out, float* part,
+                           hipStream_t s) {
   if (S <= 0) return hipSuccess;
-  k_slot_dot<<<(unsigned)S, 256, 0, s>>>(x, y, len, out);
+  if ((int64_t)S * kDotBlocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  k_slot_dot_part<<<(unsigned)(S * kDotBlocks), 256, 0, s>>>(x, y, len, part);
+  k_slot_dot_sum<<<(unsigned)S, 64, 0, s>>>(part, out);
   return hipGetLastError();
 }
 
@@ -3081,9 +3115,11 @@ hipError_t launch_ns_lin(const NsLinArgs& a, hipStream_t s) {
 
 hipError_t launch_sym(const _Float16* X, float alpha, const _Float16* Y, float beta, _Float16* out, int S, int m,
                       hipStream_t s) {
-  const int tiles = (m + 31) / 32;
+  if (m % 8) return hipErrorInvalidValue;
+  const int tiles = (m + 63) / 64;
   const int64_t blocks = (int64_t)S * tiles * tiles;
   if (blocks <= 0) return hipSuccess;
+  if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   k_sym<<<(unsigned)blocks, 256, 0, s>>>(X, alpha, Y, beta, out, m, tiles);
   return hipGetLastError();
 }

@@ -1932,6 +1932,32 @@ def test_schedule_backward_video_teacher_forcing_muon():
     check_sched_bwd(cfg, x, ct, sched, run_gpu_sched_bwd(cfg, x, ct, sched))
 
 
+def test_schedule_backward_without_updates():
+    # apply-only segments and a gap (no update: no replay, the final weights
+    # are the initial ones), with momentum: the state's cotangent passes
+    # through, beta gets none
+    C = 128
+    cfg = CONFIGS["lm32k"].with_(name="sched_bwd_apply_only", B=1, H=2, d=128, h=256, n_kv=256, n_q=600, chunk=C,
+                                 momentum=1)
+    x, ct, st = make_inputs(cfg, 115), make_cotangents(cfg, 115), make_momentum_state(cfg, 115)
+    sched = [("apply_only", 0, 300), ("apply_only", 340, 600)]
+    got = run_gpu_sched_bwd(cfg, x, ct, sched, st)
+    check_sched_bwd(cfg, x, ct, sched, got, st)
+    assert not np.any(got[1]) and not np.any(got[3]) and not np.any(got[4])
+    for a, b in zip(got[8:], (ct["dM1"], ct["dM2"], ct["dM3"])):
+        assert np.array_equal(a, b)
+
+
+def test_schedule_backward_empty():
+    cfg = CONFIGS["lm32k"].with_(name="sched_bwd_empty", B=1, H=2, d=128, h=256, n_kv=256, n_q=300, chunk=128)
+    x, ct = make_inputs(cfg, 116), make_cotangents(cfg, 116)
+    got = run_gpu_sched_bwd(cfg, x, ct, [])
+    for g in got[:4]:
+        assert not np.any(g)
+    for a, b in zip(got[4:], (ct["dW1"], ct["dW2"], ct["dW3"])):
+        assert np.array_equal(a, b)
+
+
 def test_schedule_backward_of_uniform_chunks_is_lact_backward_bitwise():
     cfg = CONFIGS["lm32k"].with_(name="sched_bwd_uniform", B=1, H=2, d=128, h=256, n_kv=600, n_q=640, chunk=256,
                                  order=1)

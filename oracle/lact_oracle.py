@@ -361,6 +361,77 @@ def rmsnorm_out(o, B: int, H: int, weight=None, eps: float = 1e-6):
     return np.ascontiguousarray(y.transpose(0, 2, 1, 3))
 
 
+def qkv_prologue_vjp(qkv, lr_raw, lr_bias: float, beta_raw, dq, dk, dv, deta, dbeta=None):
+    """Reverse of qkv_prologue (Alg. 1, layer; R11) for the path's inputs as
+    the path takes them: q for all L tokens, k, v, eta (and beta) for the
+    first n_kv = dk.shape[1] tokens. Given their cotangents (dq [B*H, L, hd],
+    dk, dv [B*H, n_kv, hd], deta [B*H, n_kv(, R)], dbeta [B*H, n_kv] or None),
+    returns (dqkv [B, L, 3, H, hd], dlr_raw [B, L, H, R], dbeta_raw [B, L, H]
+    or None); tokens past n_kv get no cotangent through k, v, eta, beta.
+
+    With u = SiLU(x) and y = u / |u| (q, k):  du = (dy - y (y . dy)) / |u|
+    (zero where u = 0, whose forward value is the constant 0); dx = du SiLU'(x).
+    v = SiLU(x): dx = dv SiLU'(x). eta = softplus(r + bias): dr = deta
+    sigmoid(r + bias). beta = sigmoid(z): dz = dbeta beta (1 - beta).
+    """
+    qkv = np.asarray(qkv, dtype=np.float64)
+    B, L, _, H, hd = qkv.shape
+    n_kv = np.asarray(dk).shape[1]
+    heads = lambda t: t.transpose(0, 2, 1, 3).reshape(B * H, L, hd)          # [B, L, H, hd] -> [BH, L, hd]
+    back = lambda t: t.reshape(B, H, L, hd).transpose(0, 2, 1, 3)             # the inverse
+    dqkv = np.zeros_like(qkv)
+
+    def unit_vjp(x, dy):
+        u = silu(x)
+        n = np.sqrt(np.sum(u * u, axis=-1, keepdims=True))
+        y = np.divide(u, n, out=np.zeros_like(u), where=n > 0)
+        du = np.divide(dy - y * np.sum(y * dy, axis=-1, keepdims=True), n, out=np.zeros_like(u), where=n > 0)
+        return du * silu_derivative(x)
+
+    dqkv[:, :, 0] = back(unit_vjp(heads(qkv[:, :, 0]), np.asarray(dq, dtype=np.float64)))
+    kx, vx = heads(qkv[:, :, 1])[:, :n_kv], heads(qkv[:, :, 2])[:, :n_kv]
+    dkx = np.zeros((B * H, L, hd))
+    dvx = np.zeros((B * H, L, hd))
+    dkx[:, :n_kv] = unit_vjp(kx, np.asarray(dk, dtype=np.float64))
+    dvx[:, :n_kv] = np.asarray(dv, dtype=np.float64) * silu_derivative(vx)
+    dqkv[:, :, 1] = back(dkx)
+    dqkv[:, :, 2] = back(dvx)
+    lr = np.asarray(lr_raw, dtype=np.float64)
+    R = lr.shape[-1]
+    de = np.asarray(deta, dtype=np.float64).reshape(B * H, n_kv, R)
+    dlr = np.zeros_like(lr)
+    dlr_kv = de * sigmoid(lr.transpose(0, 2, 1, 3).reshape(B * H, L, R)[:, :n_kv] + lr_bias)
+    dlr[:, :n_kv] = dlr_kv.reshape(B, H, n_kv, R).transpose(0, 2, 1, 3)
+    dbeta_raw = None
+    if beta_raw is not None:
+        z = np.asarray(beta_raw, dtype=np.float64)
+        dbeta_raw = np.zeros_like(z)
+        if dbeta is not None:
+            b = sigmoid(z.transpose(0, 2, 1).reshape(B * H, L)[:, :n_kv])
+            g = np.asarray(dbeta, dtype=np.float64) * b * (1.0 - b)
+            dbeta_raw[:, :n_kv] = g.reshape(B, H, n_kv).transpose(0, 2, 1)
+    return dqkv, dlr, dbeta_raw
+
+
+def rmsnorm_out_vjp(o, B: int, H: int, dy, weight=None, eps: float = 1e-6):
+    """Reverse of rmsnorm_out: from dy [B, L, H, hd], (do [B*H, L, hd],
+    dweight [H, hd] or None). Per vector, with r = 1 / sqrt(mean(o^2) + eps)
+    and g = w o dy (g = dy without a weight):
+        do = r g - (r^3 / hd) o (g . o),   dw = sum over (b, l) of dy o r o.
+    """
+    o = np.asarray(o, dtype=np.float64)
+    BH, L, hd = o.shape
+    d = np.asarray(dy, dtype=np.float64).transpose(0, 2, 1, 3).reshape(BH, L, hd)
+    r = 1.0 / np.sqrt(np.mean(o * o, axis=-1, keepdims=True) + eps)
+    w = None if weight is None else np.asarray(weight, dtype=np.float64)
+    g = d if w is None else d * np.tile(w, (B, 1))[:, None, :]   # instance b * H + h takes w[h]
+    do = r * g - (r ** 3 / hd) * o * np.sum(g * o, axis=-1, keepdims=True)
+    dw = None
+    if w is not None:
+        dw = (d * o * r).reshape(B, H, L, hd).sum(axis=(0, 2))
+    return do, dw
+
+
 def linear_gradient(W, K, V, eta):
     """Gradient of sum_i eta_i * (-(W k_i)^T v_i) w.r.t. W for the linear fast
     weight f_W(x) = W x (§5.4; §3.1 loss eq.): -sum_i eta_i v_i k_i^T, [d, d]."""

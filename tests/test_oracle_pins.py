@@ -1548,3 +1548,85 @@ def test_schedule_backward_batched_driver_stacks_instances():
                                               beta=beta[i], M=tuple(m[i] for m in M))
         for a, b in zip(got, r[:5] + r[5] + r[6]):
             assert np.array_equal(a[pos], b)
+
+
+# ----------------------------------------------------------------------------- backward of the prologue and output norm
+
+
+def _torch_prologue(qkv, lr_raw, lr_bias, beta_raw, n_kv):
+    """The prologue in torch (autograd sees it): F.silu, a per-vector norm,
+    softplus and sigmoid, k, v and the rates for the first n_kv tokens."""
+    B, L, _, H, hd = qkv.shape
+    act = F.silu(qkv)
+    heads = lambda t: t.permute(0, 2, 1, 3).reshape(B * H, L, hd)
+    q, k, v = (heads(act[:, :, j]) for j in range(3))
+    q = q / torch.linalg.vector_norm(q, dim=-1, keepdim=True)
+    k = k / torch.linalg.vector_norm(k, dim=-1, keepdim=True)
+    R = lr_raw.shape[-1]
+    eta = F.softplus(lr_raw + lr_bias).permute(0, 2, 1, 3).reshape(B * H, L, R)
+    beta = torch.sigmoid(beta_raw).permute(0, 2, 1).reshape(B * H, L)
+    return q, k[:, :n_kv], v[:, :n_kv], eta[:, :n_kv], beta[:, :n_kv]
+
+
+@pytest.mark.parametrize("R", [1, 3])
+def test_prologue_vjp_matches_autograd(R):
+    rng = _rng(170 + R)
+    B, L, H, hd, n_kv = 2, 7, 3, 5, 4
+    qkv = rng.standard_normal((B, L, 3, H, hd))
+    lr_raw, beta_raw = rng.standard_normal((B, L, H, R)), rng.standard_normal((B, L, H))
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    xt, lt, bt = t(qkv), t(lr_raw), t(beta_raw)
+    outs = _torch_prologue(xt, lt, -1.3, bt, n_kv)
+    cts = [rng.standard_normal(tuple(o.shape)) for o in outs]
+    sum((o * torch.tensor(c)).sum() for o, c in zip(outs, cts)).backward()
+    deta = cts[3] if R == 3 else cts[3][..., 0]
+    dqkv, dlr, dbr = O.qkv_prologue_vjp(qkv, lr_raw, -1.3, beta_raw, cts[0], cts[1], cts[2], deta, cts[4])
+    assert np.allclose(dqkv, xt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    assert np.allclose(dlr, lt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    assert np.allclose(dbr, bt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    # tokens past n_kv: nothing through k, v, the rates and beta
+    assert not np.any(dqkv[:, n_kv:, 1:]) and not np.any(dlr[:, n_kv:]) and not np.any(dbr[:, n_kv:])
+    # the forward this reverses is the oracle's own prologue
+    q, k, v, eta, beta = O.qkv_prologue(qkv, lr_raw, -1.3, beta_raw)
+    assert np.allclose(outs[0].detach().numpy(), q, rtol=1e-12) and np.allclose(outs[2].detach().numpy(), v[:, :n_kv])
+
+
+def test_prologue_vjp_zero_vector_and_scale_invariance():
+    # a q vector that SiLU maps to zero has no cotangent; the unit-norm map
+    # is blind to scaling u, so a cotangent along y itself has none either
+    rng = _rng(175)
+    B, L, H, hd = 1, 3, 1, 4
+    qkv = rng.standard_normal((B, L, 3, H, hd))
+    qkv[0, 1, 0, 0] = 0.0
+    lr = rng.standard_normal((B, L, H, 1))
+    q = O.qkv_prologue(qkv, lr, 0.0)[0]
+    qkv_z = qkv.copy()
+    qkv_z[0, 1, 0, 0] = np.zeros(hd)
+    dq = rng.standard_normal((H * B, L, hd))
+    dq_along = q * 2.5                                   # cotangent parallel to y
+    z = np.zeros((1, L, hd))
+    r = O.qkv_prologue_vjp(qkv_z, lr, 0.0, None, dq, z, z, np.zeros((1, L)))
+    assert not np.any(r[0][0, 1, 0, 0])
+    r = O.qkv_prologue_vjp(qkv, lr, 0.0, None, dq_along, z, z, np.zeros((1, L)))
+    assert np.allclose(r[0][:, :, 0], 0.0, atol=1e-13)
+
+
+@pytest.mark.parametrize("weighted", [False, True])
+def test_rmsnorm_out_vjp_matches_autograd(weighted):
+    rng = _rng(176 + weighted)
+    B, H, L, hd = 2, 3, 5, 6
+    o = rng.standard_normal((B * H, L, hd))
+    w = rng.standard_normal((H, hd)) if weighted else None
+    dy = rng.standard_normal((B, L, H, hd))
+    ot = torch.tensor(o, requires_grad=True)
+    wt = torch.tensor(w, requires_grad=True) if weighted else None
+    y = F.rms_norm(ot, (hd,), eps=1e-6).reshape(B, H, L, hd)
+    if weighted:
+        y = y * wt[None, :, None, :]
+    (y.permute(0, 2, 1, 3) * torch.tensor(dy)).sum().backward()
+    do, dw = O.rmsnorm_out_vjp(o, B, H, dy, w, 1e-6)
+    assert np.allclose(do, ot.grad.numpy(), rtol=1e-10, atol=1e-12)
+    if weighted:
+        assert np.allclose(dw, wt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    else:
+        assert dw is None

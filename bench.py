@@ -519,12 +519,37 @@ def measure(cfg, args, P, on_device=False):
                         + cfg.BH * (cfg.n_q * cfg.d * esz + cfg.n_kv * (2 * cfg.d * esz + 4 * R)),
             "rmsnorm": 2 * cfg.BH * cfg.n_q * cfg.d * esz + cfg.H * cfg.d * 4,
         }
+        if args.backward:
+            # the layer's training step: the norm's reverse (its dO feeds the
+            # path's reverse), the path's, then the prologue's; dy and the
+            # norm's input o seeded on the device like the projections
+            dy_l = torch.randn(cfg.B, cfg.n_q, cfg.H, cfg.d, generator=gen, device=dev).to(io)
+            o_l = torch.randn(cfg.B, cfg.H, cfg.n_q, cfg.d, generator=gen, device=dev).to(io)
+            dqkv_l, dlr_l, dw_l = torch.empty_like(qkv_raw), torch.empty_like(lr_raw), torch.empty_like(rms_w)
+            io_step = {
+                "rmsnorm_backward": lambda: P.rmsnorm_out_backward(o_l, dy_l, rms_w, 1e-6, out=(dout, dw_l),
+                                                                   stream=launch_stream()),
+                "prologue_backward": lambda: P.prologue_backward(qkv_raw, lr_raw, -4.6, None, grads[0], grads[1],
+                                                                 grads[2], grads[3], None, out=(dqkv_l, dlr_l, None),
+                                                                 stream=launch_stream()),
+            }
+            # algorithmic bytes: every input read once, every output written once
+            io_bytes = {
+                "prologue_backward": cfg.B * cfg.n_q * cfg.H * (6 * cfg.d * esz + 8 * R)
+                                     + cfg.BH * (cfg.n_q * cfg.d * esz + cfg.n_kv * (2 * cfg.d * esz + 4 * R)),
+                "rmsnorm_backward": 3 * cfg.BH * cfg.n_q * cfg.d * esz + 2 * cfg.H * cfg.d * 4,
+            }
     sched = None
     if cfg.schedule:
         from lact_synth import make_schedule
         sched = make_schedule(cfg)
 
     def step():
+        if io_step is not None and args.backward:
+            io_step["rmsnorm_backward"]()
+            path()
+            io_step["prologue_backward"]()
+            return
         if io_step is not None:
             io_step["prologue"]()
         path()
@@ -533,8 +558,8 @@ def measure(cfg, args, P, on_device=False):
 
     if args.backward:
         from lact_synth import make_cotangents
-        if cfg.layer_io or on_device or (cfg.use_muon and cfg.io != "bf16"):
-            raise SystemExit("--backward runs without the layer's prologue (Muon with bf16 I/O), host-drawn inputs")
+        if on_device or (cfg.use_muon and cfg.io != "bf16"):
+            raise SystemExit("--backward runs on host-drawn inputs (Muon with bf16 I/O)")
         ct = make_cotangents(cfg, 0)
         dout = torch.from_numpy(ct["do"].reshape(cfg.B, cfg.H, cfg.n_q, cfg.d)).to(dev, io)
         del ct
@@ -616,7 +641,9 @@ def measure(cfg, args, P, on_device=False):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if cfg.io == "bf16" else "fp32", "data": "synthetic",
-        "config": {"workload": describe(cfg) + ((", backward (lact_backward_schedule)" if cfg.schedule else
+        "config": {"workload": describe(cfg) + ((", backward (lact_rmsnorm_out_backward, lact_backward, "
+                                                 "lact_prologue_backward)" if cfg.layer_io else
+                                                 ", backward (lact_backward_schedule)" if cfg.schedule else
                                                  ", backward (lact_backward_momentum)" if cfg.momentum else
                                                  ", backward (lact_backward_linear)" if cfg.linear else
                                                  ", backward (lact_backward)") if args.backward else ""),

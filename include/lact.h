@@ -29,7 +29,7 @@
  * lact_backward_linear, lact_backward_momentum and lact_backward_schedule
  * (the reverse of the chunk loop: SwiGLU and linear fast weight, the
  * momentum optimizer, a general schedule),
- * lact_prologue and lact_rmsnorm_out
+ * lact_prologue and lact_rmsnorm_out (and their reverses)
  * (the layer's steps on either side of the path, Alg. 1); per-matrix learning
  * rates through lact_desc.eta_per_matrix.
  *
@@ -466,6 +466,42 @@ int lact_prologue(const lact_desc* desc, const void* qkv, const float* lr_raw, f
                   void* stream);
 int lact_rmsnorm_out(const lact_desc* desc, const void* o, const float* weight, float eps, void* y,
                      void* stream);
+
+/*
+ * Reverses of the layer's steps on either side of the path (Alg. 1, layer),
+ * for training with lact_backward*: the same descriptor fields and layouts.
+ *
+ * lact_prologue_backward: from the cotangents of lact_prologue's outputs,
+ * those of its inputs. Per (token, head) with u = SiLU(x): q and k
+ * (y = u / |u|) give du = (dy - y (y . dy)) / |u| (zero for a zero u, whose
+ * output is the constant 0), v gives du = dv; dx = du SiLU'(x). The rates
+ * give d raw = deta * sigmoid(raw + lr_bias) (the softplus' derivative), the
+ * momentum logits d beta_raw = dbeta * beta (1 - beta).
+ *   qkv, lr_raw, lr_bias, beta_raw  lact_prologue's inputs                     in
+ *   dq [B*H, n_q, d], dk, dv [B*H, n_kv, d]  io_dtype                         in
+ *   deta [B*H, n_kv(, 3)], dbeta [B*H, n_kv]  fp32                              in
+ *   dqkv     [B, n_q, 3, H, d]  io_dtype (k, v parts zero past n_kv)           out
+ *   dlr_raw  [B, n_q, H, R]     fp32 (zero past n_kv)                          out
+ *   dbeta_raw [B, n_q, H]       fp32 (zero past n_kv), with beta_raw and dbeta;
+ *                               all three NULL for no momentum logits          out
+ * Errors as lact_prologue; a mismatch of beta_raw, dbeta and dbeta_raw is
+ * LACT_EINVAL. Inputs must not alias outputs.
+ *
+ * lact_rmsnorm_out_backward: from dy [B, n_q, H, d] (io_dtype), d_o
+ * [B*H, n_q, d] (io_dtype) and, when dweight is not NULL (weight must then be
+ * given), dweight [H, d] (fp32). With r = 1 / sqrt(mean_d(o^2) + eps) and
+ * g = weight * dy per element: d_o = r g - (r^3 / d) o (g . o), and dweight
+ * sums dy o r over the batch and the tokens (a second pass, in a fixed order;
+ * its workspace, lact_rmsnorm_out_backward_workspace_bytes(desc, 1), holds
+ * the per-vector r and the pass's partial sums; 0 bytes without dweight).
+ */
+int lact_prologue_backward(const lact_desc* desc, const void* qkv, const float* lr_raw, float lr_bias,
+                           const float* beta_raw, const void* dq, const void* dk, const void* dv,
+                           const float* deta, const float* dbeta, void* dqkv, float* dlr_raw, float* dbeta_raw,
+                           void* stream);
+size_t lact_rmsnorm_out_backward_workspace_bytes(const lact_desc* desc, int with_weight, int* err);
+int lact_rmsnorm_out_backward(const lact_desc* desc, const void* o, const float* weight, float eps, const void* dy,
+                              void* d_o, float* dweight, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Kernel timing (instrumentation for benchmarks). While enabled, lact_forward

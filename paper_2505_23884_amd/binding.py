@@ -87,6 +87,12 @@ def load_library(path: str | None = None):
     L.lact_prologue.argtypes = [dp, vp, vp, f32, vp, vp, vp, vp, vp, vp, vp]
     L.lact_prologue.restype = i32
     L.lact_rmsnorm_out.argtypes = [dp, vp, vp, f32, vp, vp]
+    L.lact_prologue_backward.argtypes = [dp, vp, vp, f32] + [vp] * 10
+    L.lact_prologue_backward.restype = i32
+    L.lact_rmsnorm_out_backward_workspace_bytes.argtypes = [dp, i32, ctypes.POINTER(i32)]
+    L.lact_rmsnorm_out_backward_workspace_bytes.restype = sz
+    L.lact_rmsnorm_out_backward.argtypes = [dp, vp, vp, f32, vp, vp, vp, vp, sz, vp]
+    L.lact_rmsnorm_out_backward.restype = i32
     L.lact_rmsnorm_out.restype = i32
     L.lact_timing_enable.argtypes = [i32]
     L.lact_timing_enable.restype = i32
@@ -613,6 +619,84 @@ def rmsnorm_out(o, weight=None, eps=1e-6, out=None, stream=None):
     if rc:
         _raise(rc)
     return y
+
+
+def prologue_backward(qkv, lr_raw, lr_bias, beta_raw, dq, dk, dv, deta, dbeta=None, out=None, stream=None):
+    """Reverse of prologue() (lact_prologue_backward): the cotangents (dqkv
+    [B, L, 3, H, d], dlr_raw like lr_raw, dbeta_raw [B, L, H] or None) of the
+    prologue's inputs given those of its outputs (dq [B, H, L, d], dk, dv
+    [B, H, n_kv, d], deta like eta, dbeta [B, H, n_kv] or None)."""
+    import torch
+    if qkv.dim() != 5 or qkv.shape[2] != 3:
+        raise LactError(-1, "qkv must be [B, L, 3, H, d]")
+    B, L, _, H, d = qkv.shape
+    n_kv = dk.shape[-2]
+    lr3 = lr_raw.dim() == 4
+    if dq.shape != (B, H, L, d) or dk.shape != (B, H, n_kv, d) or dv.shape != dk.shape:
+        raise LactError(-1, "dq must be [B, H, L, d], dk and dv [B, H, n_kv, d]")
+    if deta.shape != (B, H, n_kv, *((3,) if lr3 else ())):
+        raise LactError(-1, "deta must be shaped like eta")
+    if (beta_raw is None) != (dbeta is None):
+        raise LactError(-1, "pass beta_raw and dbeta together")
+    for t in (qkv, lr_raw, beta_raw, dq, dk, dv, deta, dbeta):
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise LactError(-1, "inputs must be contiguous device tensors")
+    if any(t.dtype != qkv.dtype for t in (dq, dk, dv)):
+        raise LactError(-1, "dq, dk, dv must have qkv's dtype")
+    io = IO_BF16 if qkv.dtype == torch.bfloat16 else IO_FP32 if qkv.dtype == torch.float32 else None
+    if io is None:
+        raise LactError(-1, f"unsupported qkv dtype {qkv.dtype}")
+    if out is None:
+        out = (torch.empty_like(qkv), torch.empty_like(lr_raw),
+               torch.empty_like(beta_raw) if beta_raw is not None else None)
+    dqkv, dlr, dbr = out
+    desc = make_desc(B, H, d, d, n_kv, L, 1, 0, False, 0, io, lr3)   # h unused: any valid value
+    if stream is None:
+        stream = torch.cuda.current_stream(qkv.device).cuda_stream
+    rc = lib().lact_prologue_backward(ctypes.byref(desc), _ptr(qkv), _ptr(lr_raw), ctypes.c_float(lr_bias),
+                                      _ptr(beta_raw), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(deta), _ptr(dbeta),
+                                      _ptr(dqkv), _ptr(dlr), _ptr(dbr), ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return dqkv, dlr, dbr
+
+
+def rmsnorm_out_backward(o, dy, weight=None, eps=1e-6, with_dweight=True, out=None, workspace=None, stream=None):
+    """Reverse of rmsnorm_out() (lact_rmsnorm_out_backward): from dy [B, L,
+    H, d], returns (d_o [B, H, L, d], dweight [H, d] or None; dweight only
+    with a weight and with_dweight)."""
+    import torch
+    if o.dim() != 4:
+        raise LactError(-1, "o must be [B, H, L, d]")
+    B, H, L, d = o.shape
+    if dy.shape != (B, L, H, d) or dy.dtype != o.dtype:
+        raise LactError(-1, "dy must be [B, L, H, d] of o's dtype")
+    for t in (o, dy, weight):
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise LactError(-1, "inputs must be contiguous device tensors")
+    io = IO_BF16 if o.dtype == torch.bfloat16 else IO_FP32 if o.dtype == torch.float32 else None
+    if io is None:
+        raise LactError(-1, f"unsupported o dtype {o.dtype}")
+    want_dw = weight is not None and with_dweight
+    if out is None:
+        out = (torch.empty_like(o), torch.empty_like(weight) if want_dw else None)
+    d_o, dw = out
+    desc = make_desc(B, H, d, d, 0, L, 1, 0, False, 0, io)
+    if workspace is None and want_dw:
+        err = ctypes.c_int(0)
+        nb = lib().lact_rmsnorm_out_backward_workspace_bytes(ctypes.byref(desc), 1, ctypes.byref(err))
+        if err.value:
+            _raise(err.value)
+        workspace = torch.empty(max(int(nb), 1), dtype=torch.uint8, device=o.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if stream is None:
+        stream = torch.cuda.current_stream(o.device).cuda_stream
+    rc = lib().lact_rmsnorm_out_backward(ctypes.byref(desc), _ptr(o), _ptr(weight), ctypes.c_float(eps), _ptr(dy),
+                                         _ptr(d_o), _ptr(dw), _ptr(workspace), ctypes.c_size_t(nbytes),
+                                         ctypes.c_void_p(stream))
+    if rc:
+        _raise(rc)
+    return d_o, dw
 
 
 def timing_enable(on: bool = True):

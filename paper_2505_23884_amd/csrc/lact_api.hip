@@ -2620,6 +2620,94 @@ int lact_rmsnorm_out(const lact_desc* desc, const void* o, const float* weight, 
   return timed(LACT_KCLASS_IO, 0.0, s, [&] { return launch_rmsnorm_out(a, bf16, s); });
 }
 
+int lact_prologue_backward(const lact_desc* desc, const void* qkv, const float* lr_raw, float lr_bias,
+                           const float* beta_raw, const void* dq, const void* dk, const void* dv, const float* deta,
+                           const float* dbeta, void* dqkv, float* dlr_raw, float* dbeta_raw, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  const bool any_q = desc->n_q > 0, any_kv = desc->n_kv > 0;
+  if (any_q && (!qkv || !lr_raw || !dq || !dqkv || !dlr_raw)) return LACT_EINVAL;
+  if (any_kv && (!dk || !dv || !deta)) return LACT_EINVAL;
+  // the momentum logits' cotangent: beta_raw, dbeta and dbeta_raw together, or none
+  if ((beta_raw == nullptr) != (dbeta_raw == nullptr) || (dbeta_raw && any_kv && !dbeta)) return LACT_EINVAL;
+  if (!(lr_bias == lr_bias) || lr_bias - lr_bias != 0.0f) return LACT_EINVAL;   // finite
+  if (any_q && (misaligned(qkv) || misaligned(dq) || misaligned(dqkv) || ((uintptr_t)lr_raw & 3) ||
+                ((uintptr_t)dlr_raw & 3)))
+    return LACT_EALIGN;
+  if (any_kv && (misaligned(dk) || misaligned(dv) || ((uintptr_t)deta & 3))) return LACT_EALIGN;
+  if (dbeta_raw && (((uintptr_t)beta_raw & 3) || ((uintptr_t)dbeta_raw & 3) || ((uintptr_t)dbeta & 3)))
+    return LACT_EALIGN;
+  PrologueBwdArgs a{};
+  a.qkv = qkv;
+  a.lr_raw = lr_raw;
+  a.beta_raw = beta_raw;
+  a.lr_bias = lr_bias;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.deta = deta;
+  a.dbeta = dbeta;
+  a.dqkv = dqkv;
+  a.dlr_raw = dlr_raw;
+  a.dbeta_raw = dbeta_raw;
+  a.B = desc->B;
+  a.H = desc->H;
+  a.hd = desc->d;
+  a.R = desc->eta_per_matrix ? 3 : 1;
+  a.L = desc->n_q;
+  a.n_kv = desc->n_kv;
+  const bool bf16 = desc->io_dtype == LACT_IO_BF16;
+  hipStream_t s = (hipStream_t)stream;
+  return timed(LACT_KCLASS_IO, 0.0, s, [&] { return launch_prologue_bwd(a, bf16, s); });
+}
+
+size_t lact_rmsnorm_out_backward_workspace_bytes(const lact_desc* desc, int with_weight, int* err) {
+  const int rc = check_desc(desc);
+  if (err) *err = rc;
+  if (rc) return 0;
+  if (!with_weight) return 0;
+  const size_t r = align_up((size_t)desc->B * desc->n_q * desc->H * 4);
+  const size_t part = (size_t)rms_dw_splits(desc->B, desc->n_q, desc->H, desc->d) * desc->H * desc->d * 4;
+  return align_up(r + part);
+}
+
+int lact_rmsnorm_out_backward(const lact_desc* desc, const void* o, const float* weight, float eps, const void* dy,
+                              void* d_o, float* dweight, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  if (!(eps >= 0.0f) || eps - eps != 0.0f) return LACT_EINVAL;   // finite, >= 0
+  if (desc->n_q > 0 && (!o || !dy || !d_o)) return LACT_EINVAL;
+  if (dweight && !weight) return LACT_EINVAL;
+  if (desc->n_q > 0 && (misaligned(o) || misaligned(dy) || misaligned(d_o))) return LACT_EALIGN;
+  if ((weight && ((uintptr_t)weight & 3)) || (dweight && ((uintptr_t)dweight & 3))) return LACT_EALIGN;
+  const size_t need = lact_rmsnorm_out_backward_workspace_bytes(desc, dweight != nullptr, nullptr);
+  if (need && (!workspace || workspace_bytes < need)) return LACT_EWORKSPACE;
+  if (need && ((uintptr_t)workspace & (kAlign - 1))) return LACT_EALIGN;
+  RmsBwdArgs a{};
+  a.o = o;
+  a.weight = weight;
+  a.dy = dy;
+  a.d_o = d_o;
+  a.dweight = dweight;
+  a.r = dweight ? reinterpret_cast<float*>(workspace) : nullptr;
+  a.part = dweight ? reinterpret_cast<float*>((uint8_t*)workspace +
+                                              align_up((size_t)desc->B * desc->n_q * desc->H * 4))
+                   : nullptr;
+  a.eps = eps;
+  a.B = desc->B;
+  a.H = desc->H;
+  a.hd = desc->d;
+  a.L = desc->n_q;
+  const bool bf16 = desc->io_dtype == LACT_IO_BF16;
+  hipStream_t s = (hipStream_t)stream;
+  if (dweight && desc->n_q == 0) {   // no tokens: a zero cotangent
+    return timed(LACT_KCLASS_IO, 0.0, s, [&] {
+      return launch_zero_f32(dweight, 1, 0, 0, (int64_t)desc->H * desc->d, s);
+    });
+  }
+  return timed(LACT_KCLASS_IO, 0.0, s, [&] { return launch_rmsnorm_out_bwd(a, bf16, s); });
+}
+
 int lact_forward_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, const void* q,
                           const void* k, const void* v, const float* eta, const float* beta, float* W1, float* W2,
                           float* W3, float* M1, float* M2, float* M3, void* o, void* workspace,

@@ -253,6 +253,42 @@ struct RmsArgs {
 };
 hipError_t launch_prologue(PrologueArgs a, bool io_bf16, hipStream_t s);
 hipError_t launch_rmsnorm_out(RmsArgs a, bool io_bf16, hipStream_t s);
+// Reverse of the prologue: from the cotangents of q, k, v, eta (and beta),
+// those of the projections, the raw rates (and the raw momentum logits).
+struct PrologueBwdArgs {
+  const void* qkv;         // [B, L, 3, H, hd] io dtype
+  const float* lr_raw;     // [B, L, H, R]
+  const float* beta_raw;   // [B, L, H] or nullptr
+  float lr_bias;
+  const void *dq, *dk, *dv;   // [B*H, L, hd], [B*H, n_kv, hd] x 2
+  const float* deta;       // [B*H, n_kv, R]
+  const float* dbeta;      // [B*H, n_kv] or nullptr (with beta_raw and dbeta_raw)
+  void* dqkv;              // [B, L, 3, H, hd]
+  float* dlr_raw;          // [B, L, H, R]
+  float* dbeta_raw;        // [B, L, H] or nullptr
+  int B, H, hd, R;
+  int64_t L, n_kv;
+  int group;               // set by the launcher
+};
+hipError_t launch_prologue_bwd(PrologueBwdArgs a, bool io_bf16, hipStream_t s);
+// Reverse of the output RMSNorm: do from dy, and with dweight its cotangent
+// through a second pass (r: B*L*H floats of per-vector scales, part: the
+// pass's partial sums, rms_dw_splits(...) * H * hd floats).
+struct RmsBwdArgs {
+  const void* o;           // [B*H, L, hd]
+  const float* weight;     // [H, hd] or nullptr
+  const void* dy;          // [B, L, H, hd]
+  void* d_o;               // [B*H, L, hd]
+  float* dweight;          // [H, hd] or nullptr
+  float* r;                // scratch [B*L*H] (with dweight)
+  float* part;             // scratch (with dweight)
+  float eps;
+  int B, H, hd;
+  int64_t L;
+  int group;               // set by the launcher
+};
+int rms_dw_splits(int B, int64_t L, int H, int hd);
+hipError_t launch_rmsnorm_out_bwd(RmsBwdArgs a, bool io_bf16, hipStream_t s);
 
 // Workgroup tile of a contraction kind: output rows x output columns, threads.
 struct TileShape {

@@ -211,6 +211,185 @@ __global__ __launch_bounds__(256) void k_rmsnorm_out(const RmsArgs a) {
   }
 }
 
+// Reverse of k_prologue, one group per (token, head) as there. With u =
+// SiLU(x), s = sigmoid(x), SiLU'(x) = s + x s (1 - s); for q and k (y = u /
+// |u|): du = dy / |u| - u (u . dy) / |u|^3 (zero for a zero u); for v: du = dy;
+// dx = du SiLU'(x). Tokens past n_kv get zeros for k, v, the rates and beta.
+template <typename T, int NV, typename IX>
+__global__ __launch_bounds__(256) void k_prologue_bwd(const PrologueBwdArgs a) {
+  constexpr int EPV = Io<T>::EPV;
+  const int G = a.group;
+  const int lane_g = threadIdx.x & (G - 1);
+  const int64_t ngroups = (int64_t)a.B * a.L * a.H;
+  const int64_t gstride = (int64_t)gridDim.x * (256 / G);
+  const int nvec = a.hd / EPV;
+  for (int64_t g = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G; g < ngroups; g += gstride) {
+    int hh;
+    int64_t t, b, l;
+    split_g<IX>(g, a.H, a.L, hh, t, b, l);
+    const int64_t in = b * a.H + hh;
+    const bool kv = l < a.n_kv;
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+      const bool live = p == 0 || kv;
+      const T* src = reinterpret_cast<const T*>(a.qkv) + ((t * 3 + p) * a.H + hh) * a.hd;
+      const T* dsrc = live ? reinterpret_cast<const T*>(p == 0 ? a.dq : (p == 1 ? a.dk : a.dv)) +
+                                 (in * (p == 0 ? a.L : a.n_kv) + l) * a.hd
+                           : nullptr;
+      float x[NV][8], dy[NV][8], up[NV][8];
+      float ss = 0.0f, dot = 0.0f;
+#pragma unroll
+      for (int j = 0; j < NV; ++j) {
+        if (!(live && lane_g + j * G < nvec)) continue;
+        Io<T>::load(src + (lane_g + j * G) * EPV, x[j]);
+        Io<T>::load(dsrc + (lane_g + j * G) * EPV, dy[j]);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) {
+          const float z = x[j][e];
+          const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z * -1.4426950408889634f));
+          const float u = z * sg;
+          up[j][e] = sg + u * (1.0f - sg);
+          x[j][e] = u;
+          ss += u * u;
+          dot += u * dy[j][e];
+        }
+      }
+      float inv = 1.0f, c = 0.0f;
+      if (p < 2) {                    // the group shares `live`
+        ss = group_sum(ss, G);
+        dot = group_sum(dot, G);
+        inv = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
+        c = dot * inv * inv * inv;
+      }
+      T* dst = reinterpret_cast<T*>(a.dqkv) + ((t * 3 + p) * a.H + hh) * a.hd;
+#pragma unroll
+      for (int j = 0; j < NV; ++j) {
+        if (lane_g + j * G >= nvec) continue;
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) o[e] = live ? (inv * dy[j][e] - c * x[j][e]) * up[j][e] : 0.0f;
+        Io<T>::store(dst + (lane_g + j * G) * EPV, o);
+      }
+    }
+    for (int r = lane_g; r < a.R; r += G) {   // d softplus(z) = sigmoid(z)
+      const int64_t at = (t * a.H + hh) * a.R + r;
+      a.dlr_raw[at] = kv ? a.deta[(in * a.n_kv + l) * a.R + r] * sigmoid_acc(a.lr_raw[at] + a.lr_bias) : 0.0f;
+    }
+    if (a.dbeta_raw && lane_g == 0) {
+      const float bt = sigmoid_acc(a.beta_raw[t * a.H + hh]);
+      a.dbeta_raw[t * a.H + hh] = kv ? a.dbeta[in * a.n_kv + l] * bt * (1.0f - bt) : 0.0f;
+    }
+  }
+}
+
+// Reverse of k_rmsnorm_out, one group per output vector (b, l, h): with r =
+// 1 / sqrt(mean(o^2) + eps) and g = w dy, do = r g - (r^3 / hd) o (g . o);
+// with dweight the vector's r goes to a.r for the weight's pass.
+template <typename T, int NV, typename IX>
+__global__ __launch_bounds__(256) void k_rmsnorm_out_bwd(const RmsBwdArgs a) {
+  constexpr int EPV = Io<T>::EPV;
+  const int G = a.group;
+  const int lane_g = threadIdx.x & (G - 1);
+  const int64_t ngroups = (int64_t)a.B * a.L * a.H;
+  const int64_t gstride = (int64_t)gridDim.x * (256 / G);
+  const int nvec = a.hd / EPV;
+  for (int64_t g = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G; g < ngroups; g += gstride) {
+    int hh;
+    int64_t t, b, l;
+    split_g<IX>(g, a.H, a.L, hh, t, b, l);
+    const int64_t oo = ((b * a.H + hh) * a.L + l) * a.hd;
+    float x[NV][8], gv[NV][8];
+    float ss = 0.0f, dot = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      if (lane_g + j * G >= nvec) continue;
+      Io<T>::load(reinterpret_cast<const T*>(a.o) + oo + (lane_g + j * G) * EPV, x[j]);
+      Io<T>::load(reinterpret_cast<const T*>(a.dy) + g * a.hd + (lane_g + j * G) * EPV, gv[j]);
+      if (a.weight) {
+        float w[8];
+        Io<float>::load8(a.weight + (int64_t)hh * a.hd + (lane_g + j * G) * EPV, w, EPV);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) gv[j][e] *= w[e];
+      }
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        ss += x[j][e] * x[j][e];
+        dot += gv[j][e] * x[j][e];
+      }
+    }
+    ss = group_sum(ss, G);
+    dot = group_sum(dot, G);
+    const float r = 1.0f / sqrtf(ss / (float)a.hd + a.eps);
+    const float c = r * r * r * dot / (float)a.hd;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      if (lane_g + j * G >= nvec) continue;
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) o[e] = r * gv[j][e] - c * x[j][e];
+      Io<T>::store(reinterpret_cast<T*>(a.d_o) + oo + (lane_g + j * G) * EPV, o);
+    }
+    if (a.dweight && lane_g == 0) a.r[g] = r;
+  }
+}
+
+// The weight's cotangent, pass 1: workgroup (head h, 512 columns, split s)
+// sums dy o r over its split's tokens into part[s][h][col]. Each lane owns 8
+// columns (16-byte loads of bf16), each of the 4 waves every 4th token; the
+// waves' sums are then added in order.
+template <typename T>
+__device__ __forceinline__ void load8c(const T* p, float (&x)[8]);
+template <>
+__device__ __forceinline__ void load8c<__bf16>(const __bf16* p, float (&x)[8]) { Io<__bf16>::load(p, x); }
+template <>
+__device__ __forceinline__ void load8c<float>(const float* p, float (&x)[8]) { Io<float>::load8(p, x, 8); }
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_rms_dw_part(const RmsBwdArgs a, int nsplit, int64_t per) {
+  __shared__ float red[4][512];
+  const int cchunks = (a.hd + 511) / 512;
+  const int sidx = blockIdx.x % nsplit;
+  const int rest = blockIdx.x / nsplit;
+  const int hh = rest / cchunks, c0 = (rest - hh * cchunks) * 512;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = c0 + 8 * lane;
+  const bool on = col < a.hd;   // hd is a multiple of 8: a lane's columns are all in or all out
+  const int64_t ntok = (int64_t)a.B * a.L;
+  const int64_t t0 = sidx * per, t1 = t0 + per < ntok ? t0 + per : ntok;
+  const T* dy = reinterpret_cast<const T*>(a.dy);
+  const T* o = reinterpret_cast<const T*>(a.o);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (on) {
+    for (int64_t t = t0 + w; t < t1; t += 4) {
+      const int64_t b = t / a.L, l = t - b * a.L;
+      float x[8], y[8];
+      load8c<T>(dy + (t * a.H + hh) * a.hd + col, y);
+      load8c<T>(o + ((b * a.H + hh) * a.L + l) * a.hd + col, x);
+      const float rr = a.r[t * a.H + hh];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += y[e] * x[e] * rr;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[w][8 * lane + e] = acc[e];
+  __syncthreads();
+  if (w == 0 && on) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      a.part[((int64_t)sidx * a.H + hh) * a.hd + col + e] =
+          (red[0][8 * lane + e] + red[1][8 * lane + e]) + (red[2][8 * lane + e] + red[3][8 * lane + e]);
+  }
+}
+
+// Pass 2: dweight = the splits' partials summed in order.
+__global__ __launch_bounds__(256) void k_rms_dw_sum(const float* part, float* dweight, int nsplit, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float acc = 0.0f;
+  for (int sp = 0; sp < nsplit; ++sp) acc += part[(int64_t)sp * n + i];
+  dweight[i] = acc;
+}
+
 // Group size and accesses per lane for hd elements of esz bytes.
 void io_shape(int hd, int esz, int& group, int& nv) {
   const int nvec = hd * esz / 16;
@@ -259,10 +438,62 @@ template <typename T, int NV> struct RmsK {
   }
 };
 
+template <typename T, int NV> struct PrologueBwdK {
+  static void launch(const PrologueBwdArgs& a, hipStream_t s) {
+    const int64_t n = (int64_t)a.B * a.L * a.H;
+    const unsigned blocks = (unsigned)io_blocks(n, a.group);
+    if (n < ((int64_t)1 << 31)) k_prologue_bwd<T, NV, uint32_t><<<blocks, 256, 0, s>>>(a);
+    else k_prologue_bwd<T, NV, uint64_t><<<blocks, 256, 0, s>>>(a);
+  }
+};
+template <typename T, int NV> struct RmsBwdK {
+  static void launch(const RmsBwdArgs& a, hipStream_t s) {
+    const int64_t n = (int64_t)a.B * a.L * a.H;
+    const unsigned blocks = (unsigned)io_blocks(n, a.group);
+    if (n < ((int64_t)1 << 31)) k_rmsnorm_out_bwd<T, NV, uint32_t><<<blocks, 256, 0, s>>>(a);
+    else k_rmsnorm_out_bwd<T, NV, uint64_t><<<blocks, 256, 0, s>>>(a);
+  }
+};
+
 // hd <= 4096: at most 1024 accesses of 16 bytes per vector, 16 per lane
 int round_nv(int nv) { return nv <= 1 ? 1 : nv <= 2 ? 2 : nv <= 4 ? 4 : nv <= 8 ? 8 : 16; }
 
 }  // namespace
+
+hipError_t launch_prologue_bwd(PrologueBwdArgs a, bool io_bf16, hipStream_t s) {
+  int nv;
+  io_shape(a.hd, io_bf16 ? 2 : 4, a.group, nv);
+  if ((int64_t)a.B * a.L * a.H <= 0) return hipSuccess;
+  nv = round_nv(nv);
+  return io_bf16 ? launch_nv<PrologueBwdK, __bf16>(a, nv, s) : launch_nv<PrologueBwdK, float>(a, nv, s);
+}
+
+// Token splits of the weight's pass: about 2048 workgroups in all.
+int rms_dw_splits(int B, int64_t L, int H, int hd) {
+  const int64_t ntok = (int64_t)B * L, tiles = (int64_t)H * ((hd + 511) / 512);
+  int64_t sp = (2048 + tiles - 1) / tiles;
+  if (sp > 256) sp = 256;
+  if (sp > ntok) sp = ntok;
+  return (int)(sp < 1 ? 1 : sp);
+}
+
+hipError_t launch_rmsnorm_out_bwd(RmsBwdArgs a, bool io_bf16, hipStream_t s) {
+  int nv;
+  io_shape(a.hd, io_bf16 ? 2 : 4, a.group, nv);
+  if ((int64_t)a.B * a.L * a.H <= 0) return hipSuccess;
+  nv = round_nv(nv);
+  hipError_t e = io_bf16 ? launch_nv<RmsBwdK, __bf16>(a, nv, s) : launch_nv<RmsBwdK, float>(a, nv, s);
+  if (e != hipSuccess || !a.dweight) return e;
+  const int nsplit = rms_dw_splits(a.B, a.L, a.H, a.hd);
+  const int64_t ntok = (int64_t)a.B * a.L, per = (ntok + nsplit - 1) / nsplit;
+  const int64_t blocks = (int64_t)nsplit * a.H * ((a.hd + 511) / 512);
+  if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  if (io_bf16) k_rms_dw_part<__bf16><<<(unsigned)blocks, 256, 0, s>>>(a, nsplit, per);
+  else k_rms_dw_part<float><<<(unsigned)blocks, 256, 0, s>>>(a, nsplit, per);
+  const int64_t n = (int64_t)a.H * a.hd;
+  k_rms_dw_sum<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(a.part, a.dweight, nsplit, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_prologue(PrologueArgs a, bool io_bf16, hipStream_t s) {
   int nv;

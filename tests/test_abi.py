@@ -426,3 +426,47 @@ def test_schedule_backward_errors_before_any_hip_call():
     assert _bwd_sched(make_desc(**dict(GOOD, h=64, fast_weight=1)), segs) == -4
     # an empty schedule reaches the workspace check
     assert _bwd_sched(d, [], ws=0) == -3
+
+
+def test_prologue_and_norm_backward_errors_before_any_hip_call():
+    L = P.lib()
+    vp = ctypes.c_void_p
+    d = make_desc(**dict(GOOD, n_kv=100, n_q=120))
+    a = dict(qkv=0x1000, lr=0x2000, br=0, dq=0x3000, dk=0x4000, dv=0x5000, de=0x6000, db=0, dqkv=0x7000,
+             dlr=0x8000, dbr=0)
+
+    def pro(**kw):
+        x = dict(a)
+        x.update(kw)
+        return L.lact_prologue_backward(ctypes.byref(d), vp(x["qkv"]), vp(x["lr"]), ctypes.c_float(-1.0),
+                                        *(vp(x[n]) for n in ("br", "dq", "dk", "dv", "de", "db", "dqkv", "dlr", "dbr")),
+                                        vp(0))
+    assert pro(dq=0) == -1
+    assert pro(dlr=0) == -1
+    assert pro(de=0) == -1
+    assert pro(br=0x9000) == -1                 # beta_raw without dbeta_raw
+    assert pro(br=0x9000, dbr=0xA000) == -1     # ... and without dbeta
+    assert pro(dqkv=0x7008) == -2
+    assert pro(dlr=0x8002) == -2
+    assert L.lact_prologue_backward(ctypes.byref(d), vp(0x1000), vp(0x2000), ctypes.c_float(float("inf")),
+                                    *(vp(a[n]) for n in ("br", "dq", "dk", "dv", "de", "db", "dqkv", "dlr", "dbr")),
+                                    vp(0)) == -1
+
+    def rms(w=0x1000, dw=0x2000, ws=0x10000, nbytes=None, eps=1e-6, **kw):
+        x = dict(o=0x3000, dy=0x4000, do=0x5000)
+        x.update(kw)
+        if nbytes is None:
+            err = ctypes.c_int(0)
+            nbytes = L.lact_rmsnorm_out_backward_workspace_bytes(ctypes.byref(d), int(dw != 0), ctypes.byref(err))
+        return L.lact_rmsnorm_out_backward(ctypes.byref(d), vp(x["o"]), vp(w), ctypes.c_float(eps), vp(x["dy"]),
+                                           vp(x["do"]), vp(dw), vp(ws), ctypes.c_size_t(nbytes), vp(0))
+    err = ctypes.c_int(0)
+    assert L.lact_rmsnorm_out_backward_workspace_bytes(ctypes.byref(d), 0, ctypes.byref(err)) == 0 and err.value == 0
+    assert L.lact_rmsnorm_out_backward_workspace_bytes(ctypes.byref(d), 1, ctypes.byref(err)) > 0
+    assert rms(w=0) == -1                       # dweight needs the weight
+    assert rms(do=0) == -1
+    assert rms(eps=-1.0) == -1
+    assert rms(ws=0) == -3
+    assert rms(nbytes=1) == -3
+    assert rms(do=0x5008) == -2
+    assert rms(ws=0x10010) == -2

@@ -1192,6 +1192,89 @@ def test_output_rmsnorm_matches_oracle(io, d, weighted):
     assert rel(y.float().cpu().numpy(), ref) <= TOL[io]
 
 
+@pytest.mark.parametrize("io,d,R,n_kv_frac,beta", [("bf16", 128, 1, 1.0, True), ("bf16", 96, 3, 0.5, False),
+                                                   ("bf16", 4096, 3, 1.0, True), ("fp32", 40, 3, 0.7, True),
+                                                   ("fp32", 512, 1, 1.0, False)])
+def test_prologue_backward_matches_oracle(io, d, R, n_kv_frac, beta):
+    B, H = 2, 3
+    L = 37 if d >= 2048 else 301
+    n_kv = int(L * n_kv_frac)
+    qkv, lr, br = _raw_inputs(60 + d, B, L, H, d, R, io, beta)
+    rng = np.random.default_rng(61 + d)
+    rnd = lambda *sh: rng.standard_normal(sh, dtype=np.float32)
+    dq, dk, dv = rnd(B, H, L, d), rnd(B, H, n_kv, d), rnd(B, H, n_kv, d)
+    if io == "bf16":
+        from lact_synth import round_to_bf16
+        dq, dk, dv = (round_to_bf16(a) for a in (dq, dk, dv))
+    deta = rnd(B, H, n_kv, *((3,) if R == 3 else ()))
+    dbeta = rnd(B, H, n_kv) if beta else None
+    print(f"[gpu] prologue backward io={io} B={B} L={L} H={H} d={d} R={R} n_kv={n_kv} beta={beta}", flush=True)
+    dt = torch.bfloat16 if io == "bf16" else torch.float32
+    dev = lambda a, t=torch.float32: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to("cuda", t)
+    dqkv, dlr, dbr = P.prologue_backward(dev(qkv, dt), dev(lr), -0.7, dev(br), dev(dq, dt), dev(dk, dt), dev(dv, dt),
+                                         dev(deta), dev(dbeta))
+    torch.cuda.synchronize()
+    r = O.qkv_prologue_vjp(qkv, lr if R == 3 else lr[..., None], -0.7, br, dq.reshape(B * H, L, d),
+                           dk.reshape(B * H, n_kv, d), dv.reshape(B * H, n_kv, d), deta,
+                           None if dbeta is None else dbeta.reshape(B * H, n_kv))
+    g = dqkv.float().cpu().numpy()
+    assert not np.any(g[:, n_kv:, 1:])   # no k, v cotangent past the key tokens
+    errs = {p: rel(g[:, :, j], r[0][:, :, j]) for j, p in enumerate("qkv")}
+    print("[gpu] rel-L2", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for k, v in errs.items():
+        assert v <= TOL[io], (k, v)
+    np.testing.assert_allclose(dlr.cpu().numpy().reshape(r[1].shape), r[1], rtol=2e-6, atol=1e-7)
+    if beta:
+        np.testing.assert_allclose(dbr.cpu().numpy(), r[2], rtol=2e-6, atol=1e-7)
+    else:
+        assert dbr is None
+
+
+@pytest.mark.parametrize("io,d,weighted", [("bf16", 128, True), ("bf16", 4096, False), ("fp32", 40, True),
+                                           ("fp32", 768, True)])
+def test_output_rmsnorm_backward_matches_oracle(io, d, weighted):
+    B, H, L = 2, 3, 211 if d < 2048 else 19
+    rng = np.random.default_rng(90 + d)
+    o = rng.standard_normal((B, H, L, d), dtype=np.float32)
+    dy = rng.standard_normal((B, L, H, d), dtype=np.float32)
+    if io == "bf16":
+        from lact_synth import round_to_bf16
+        o, dy = round_to_bf16(o), round_to_bf16(dy)
+    w = rng.standard_normal((H, d), dtype=np.float32) if weighted else None
+    print(f"[gpu] rmsnorm backward io={io} B={B} H={H} L={L} d={d} weighted={weighted}", flush=True)
+    dt = torch.bfloat16 if io == "bf16" else torch.float32
+    d_o, dw = P.rmsnorm_out_backward(torch.from_numpy(o).to("cuda", dt), torch.from_numpy(dy).to("cuda", dt),
+                                     None if w is None else torch.from_numpy(w).cuda(), eps=1e-5)
+    torch.cuda.synchronize()
+    rdo, rdw = O.rmsnorm_out_vjp(o.reshape(B * H, L, d), B, H, dy, w, eps=1e-5)
+    e = {"do": rel(d_o.float().cpu().numpy().reshape(B * H, L, d), rdo)}
+    if weighted:
+        e["dweight"] = rel(dw.cpu().numpy(), rdw)
+    else:
+        assert dw is None
+    print("[gpu] rel-L2", {k: f"{v:.2e}" for k, v in e.items()}, flush=True)
+    for k, v in e.items():
+        assert v <= TOL[io], (k, v)
+
+
+def test_output_rmsnorm_backward_lm_tokens():
+    # the LM head layout (B = H = 4, d = 512) over 4096 tokens: the weight's
+    # cotangent sums 16384 vectors per head in token splits
+    B, H, L, d = 4, 4, 4096, 512
+    rng = np.random.default_rng(95)
+    from lact_synth import round_to_bf16
+    o = round_to_bf16(rng.standard_normal((B, H, L, d), dtype=np.float32))
+    dy = round_to_bf16(rng.standard_normal((B, L, H, d), dtype=np.float32))
+    w = rng.standard_normal((H, d), dtype=np.float32)
+    print(f"[gpu] rmsnorm backward LM layout B={B} H={H} L={L} d={d}", flush=True)
+    d_o, dw = P.rmsnorm_out_backward(torch.from_numpy(o).to("cuda", torch.bfloat16),
+                                     torch.from_numpy(dy).to("cuda", torch.bfloat16), torch.from_numpy(w).cuda())
+    torch.cuda.synchronize()
+    rdo, rdw = O.rmsnorm_out_vjp(o.reshape(B * H, L, d), B, H, dy, w)
+    assert rel(d_o.float().cpu().numpy().reshape(B * H, L, d), rdo) <= TOL["bf16"]
+    assert rel(dw.cpu().numpy(), rdw) <= 1e-4   # fp32 sums of bf16 products: far inside the bf16 bar
+
+
 def test_layer_chain_prologue_path_norm():
     # projections -> prologue -> path (momentum, per-matrix rates) -> RMSNorm,
     # all on the GPU, against the oracle's chain

@@ -268,8 +268,8 @@ int lact_forward_schedule(const lact_desc* desc,
  *
  * Requires desc->fast_weight == LACT_FW_LINEAR (else LACT_EUNSUPPORTED);
  * with use_muon the update's step Muon(g) goes back through the reverse of
- * every Newton-Schulz step (fp16 operands, fp32 iterates; bf16 I/O only,
- * else LACT_EUNSUPPORTED); other fields as lact_forward. The workspace size
+ * every Newton-Schulz step (fp32 iterates; fp16 operands with bf16 I/O,
+ * fp32 operands with fp32 I/O); other fields as lact_forward. The workspace size
  * (lact_backward_workspace_bytes) covers both backward entry points: it
  * follows desc->fast_weight.
  *
@@ -301,7 +301,7 @@ int lact_backward_linear(const lact_desc* desc,
 /*
  * Backward of lact_forward for the SwiGLU fast weight (§3.1 loss, chunk
  * gradient and SwiGLU eqs.; §3.2 per-row norm-preserving update; Alg. 1),
- * with or without Muon (App. A; with Muon bf16 I/O only), with one rate per
+ * with or without Muon (App. A; either I/O type), with one rate per
  * token or per-matrix rates (eta_per_matrix: each matrix's gradient weighted
  * by its own column, deta with one column per matrix); momentum:
  * lact_backward_momentum. Given the cotangent dO of the outputs and optionally
@@ -315,7 +315,9 @@ int lact_backward_linear(const lact_desc* desc,
  * weights it used (entering the chunk with apply-then-update, leaving it
  * with update-then-apply; the tail with the final weights). With Muon the
  * steps Muon(g_j) go back through every Newton-Schulz step (the iteration is
- * replayed per chunk; fp16 operands, fp32 iterates). Newton-Schulz
+ * run once per chunk in the replay, its iterates kept when they fit, else
+ * replayed in the reverse; fp16 operands with bf16 I/O, fp32 with fp32 I/O;
+ * fp32 iterates). Newton-Schulz
  * multiplies the null space of a rank-deficient gradient (a chunk shorter
  * than min(d, h)) by 3.4445 per step, and its reverse amplifies rounding
  * there by the same factor.
@@ -351,8 +353,7 @@ int lact_backward(const lact_desc* desc,
 
 /*
  * Backward of lact_forward_momentum (§3.2 momentum optimizer, App. A;
- * SwiGLU or linear fast weight, with or without Muon; with Muon bf16 I/O
- * only). Chunk c advances the state as M' = bbar_c M + g_c, bbar_c the mean
+ * SwiGLU or linear fast weight, with or without Muon). Chunk c advances the state as M' = bbar_c M + g_c, bbar_c the mean
  * of beta over the chunk's tokens, and updates W' = (n / u)(W - step(M')),
  * step the identity or Muon. Going back, the cotangent of M' is what later
  * chunks carry back to it plus what reaches it through the step; it is the

@@ -1094,12 +1094,13 @@ int run_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, 
 //   dB = dX' X^T,  S = dB + dB^T,  M = b S + c (S A + (S A)^T)  (= dA + dA^T),
 //   dX = a dX' + B dX' + M X,
 // and through the scaling X_0 = G / (||G|| + eps). Products: the k_bwd kinds
-// with fp16 operands (OUT for sums along rows, GRAD2 for sums down columns,
-// fp32 partials), fp32 iterates.
+// (OUT for sums along rows, GRAD2 for sums down columns, fp32 partials) on
+// fp16 operand copies with bf16 I/O, fp32 ones with fp32 I/O; fp32 iterates.
 struct NsBwdLayout {
   int S, m, n;
   int64_t iters;   // slices of the iterates and steps: 1 (replayed per chunk) or one per chunk (kept)
-  size_t g, x32, p1, p2, x16, a16, b16, t16, q16, s16, m16, db16, nrm, dot, dotp, pstep, ustep, ug, total;
+  int es;          // bytes per operand element: 2 (fp16) or 4 (fp32, with fp32 I/O)
+  size_t g, x32, p1, p2, xo, ao, bo, to, qo, so, mo, dbo, nrm, dot, dotp, pstep, ustep, ug, total;
 };
 
 // Chunks whose Newton-Schulz iterates and steps the backward keeps (each
@@ -1111,7 +1112,9 @@ size_t ns_bwd_layout(const Plan& p, int steps, size_t o, NsBwdLayout* N, int64_t
   N->m = std::min(p.d, p.h);
   N->n = std::max(p.d, p.h);
   const size_t mn = (size_t)N->m * N->n, mm = (size_t)N->m * N->m, S = N->S;
-  const double per = ((double)std::max(steps, 1) * S * (mn + 2 * mm) * 2.0 + (double)S * mn * 4.0);
+  N->es = p.bf16 ? 2 : 4;
+  const size_t es = (size_t)N->es;
+  const double per = ((double)std::max(steps, 1) * S * (mn + 2 * mm) * es + (double)S * mn * 4.0);
   N->iters = nch > 1 && per * nch <= kKeepIterBytes ? nch : 1;
   const size_t it = (size_t)N->iters;
   auto take = [&](size_t bytes) {
@@ -1123,14 +1126,14 @@ size_t ns_bwd_layout(const Plan& p, int steps, size_t o, NsBwdLayout* N, int64_t
   N->x32 = take(S * mn * 4);
   N->p1 = take(S * mn * 4);
   N->p2 = take(S * mn * 4);
-  N->x16 = take(it * std::max(steps, 1) * S * mn * 2);
-  N->a16 = take(it * std::max(steps, 1) * S * mm * 2);
-  N->b16 = take(it * std::max(steps, 1) * S * mm * 2);
-  N->t16 = take(S * mn * 2);
-  N->q16 = take(S * mm * 2);
-  N->s16 = take(S * mm * 2);
-  N->m16 = take(S * mm * 2);
-  N->db16 = take(S * mm * 2);
+  N->xo = take(it * std::max(steps, 1) * S * mn * es);
+  N->ao = take(it * std::max(steps, 1) * S * mm * es);
+  N->bo = take(it * std::max(steps, 1) * S * mm * es);
+  N->to = take(S * mn * es);
+  N->qo = take(S * mm * es);
+  N->so = take(S * mm * es);
+  N->mo = take(S * mm * es);
+  N->dbo = take(S * mm * es);
   N->nrm = take(S * 4);
   N->dot = take(S * 4);
   N->dotp = take(S * 32 * 4);   // the dot products' per-workgroup partials
@@ -1225,10 +1228,10 @@ struct NsBwd {
     return timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_copies_f32(cs, p.nmat, p.BH, s); });
   }
   // out[i][j] = sum_e a[i][e] b[j][e] over K per slot (rows of a: `rows`, of b: rows_out)
-  int out(const _Float16* a, int64_t a_ld, int64_t a_inst, const _Float16* b, int64_t b_ld, int64_t b_inst,
-          _Float16* o, int rows, int rows_out, int K) const {
+  int out(const void* a, int64_t a_ld, int64_t a_inst, const void* b, int64_t b_ld, int64_t b_inst,
+          void* o, int rows, int rows_out, int K) const {
     BwdArgs x{};
-    const TileShape t = bwd_tile(BWD_OUT, true, false);
+    const TileShape t = bwd_tile(BWD_OUT, !f32(), false);
     BwdSeg& g = x.seg[0];
     g.kind = BWD_OUT;
     g.tiles_m = (int)cdiv(rows_out, t.rows);
@@ -1246,12 +1249,13 @@ struct NsBwd {
     x.d = rows_out;
     x.h = K;
     x.narrow = 0;
-    return timed(LACT_KCLASS_NS, 2.0 * N.S * rows * rows_out * K, s, [&] { return launch_bwd_f16(x, s); });
+    return timed(LACT_KCLASS_NS, 2.0 * N.S * rows * rows_out * K, s,
+                 [&] { return f32() ? launch_bwd(x, false, s) : launch_bwd_f16(x, s); });
   }
   // out = a^T b per slot: a [m x m] (rows i), b [m x n] (rows i), fp32 [m x n]; up to two at once
-  int grad2(const _Float16* const* a, const _Float16* const* b, float* const* o, int nseg) const {
+  int grad2(const void* const* a, const void* const* b, float* const* o, int nseg) const {
     BwdArgs x{};
-    const TileShape t = bwd_tile(BWD_GRAD2, true, false);
+    const TileShape t = bwd_tile(BWD_GRAD2, !f32(), false);
     for (int i = 0; i < nseg; ++i) {
       BwdSeg& g = x.seg[i];
       g.kind = BWD_GRAD2;
@@ -1274,10 +1278,11 @@ struct NsBwd {
     x.d = N.m;
     x.h = N.n;
     x.narrow = 0;
-    return timed(LACT_KCLASS_NS, 2.0 * nseg * N.S * mm() * N.n, s, [&] { return launch_bwd_f16(x, s); });
+    return timed(LACT_KCLASS_NS, 2.0 * nseg * N.S * mm() * N.n, s,
+                 [&] { return f32() ? launch_bwd(x, false, s) : launch_bwd_f16(x, s); });
   }
   int lin(int mode, const float* x, const float* y, const float* p1, const float* p2, const float* sc,
-          const float* sc2, float a, float* o32, _Float16* o16) const {
+          const float* sc2, float a, float* o32, void* oc) const {
     NsLinArgs l{};
     l.mode = mode;
     l.x = x;
@@ -1289,15 +1294,27 @@ struct NsBwd {
     l.a = a;
     l.eps = (float)kNsEps;
     l.out32 = o32;
-    l.out16 = o16;
+    if (f32()) l.outc32 = reinterpret_cast<float*>(oc);   // the operand copy: fp32 with fp32 I/O, else fp16
+    else l.out16 = reinterpret_cast<_Float16*>(oc);
     l.S = N.S;
     l.len = mn();
     return timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_ns_lin(l, s); });
   }
   size_t sk(int k) const { return (size_t)(ci % N.iters) * steps + k; }   // step k of this chunk's slice
-  _Float16* X16(int k) const { return at<_Float16>(N.x16) + sk(k) * N.S * mn(); }
-  _Float16* A16(int k) const { return at<_Float16>(N.a16) + sk(k) * N.S * mm(); }
-  _Float16* B16(int k) const { return at<_Float16>(N.b16) + sk(k) * N.S * mm(); }
+  bool f32() const { return N.es == 4; }   // fp32 operands (fp32 I/O), else fp16
+  uint8_t* Xo(int k) const { return at<uint8_t>(N.xo) + sk(k) * N.S * mn() * N.es; }
+  uint8_t* Ao(int k) const { return at<uint8_t>(N.ao) + sk(k) * N.S * mm() * N.es; }
+  uint8_t* Bo(int k) const { return at<uint8_t>(N.bo) + sk(k) * N.S * mm() * N.es; }
+  uint8_t* buf(size_t off) const { return at<uint8_t>(off); }
+  // out = alpha X + beta (Y + Y^T) per [m x m] slot in the operand type (X may be nullptr)
+  int sym(const void* X, float alpha, const void* Y, float beta, void* o) const {
+    return timed(LACT_KCLASS_NS, 0.0, s, [&] {
+      return f32() ? launch_sym32(reinterpret_cast<const float*>(X), alpha, reinterpret_cast<const float*>(Y), beta,
+                                  reinterpret_cast<float*>(o), N.S, N.m, s)
+                   : launch_sym(reinterpret_cast<const _Float16*>(X), alpha, reinterpret_cast<const _Float16*>(Y),
+                                beta, reinterpret_cast<_Float16*>(o), N.S, N.m, s);
+    });
+  }
   float* pst() const { return at<float>(N.pstep) + (size_t)(ci % N.iters) * N.S * mn(); }   // the step, negated
   bool kept() const { return N.iters > 1; }
 
@@ -1319,19 +1336,17 @@ struct NsBwd {
     float* X = at<float>(N.x32);
     int rc = slabs ? gather_slabs(slabs, 1.0f, G) : gather(P, nsplit, split, -1.0f, G);
     if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] { return launch_slot_dot(G, G, N.S, mn(), at<float>(N.nrm), at<float>(N.dotp), s); });
-    if (!rc) rc = lin(0, G, nullptr, nullptr, nullptr, at<float>(N.nrm), nullptr, 0.f, X, steps > 0 ? X16(0) : nullptr);
+    if (!rc) rc = lin(0, G, nullptr, nullptr, nullptr, at<float>(N.nrm), nullptr, 0.f, X, steps > 0 ? Xo(0) : nullptr);
     for (int k = 0; k < steps && !rc; ++k) {
-      rc = out(X16(k), N.n, mn(), X16(k), N.n, mn(), A16(k), N.m, N.m, N.n);   // A = X X^T
-      if (!rc) rc = out(A16(k), N.m, mm(), A16(k), N.m, mm(), at<_Float16>(N.q16), N.m, N.m, N.m);   // A A
-      if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] {   // B = b A + c A A (symmetrised)
-        return launch_sym(A16(k), (float)kNsB, at<_Float16>(N.q16), 0.5f * (float)kNsC, B16(k), N.S, N.m, s);
-      });
-      const _Float16* a2[1] = {B16(k)};
-      const _Float16* b2[1] = {X16(k)};
+      rc = out(Xo(k), N.n, mn(), Xo(k), N.n, mn(), Ao(k), N.m, N.m, N.n);   // A = X X^T
+      if (!rc) rc = out(Ao(k), N.m, mm(), Ao(k), N.m, mm(), buf(N.qo), N.m, N.m, N.m);   // A A
+      if (!rc) rc = sym(Ao(k), (float)kNsB, buf(N.qo), 0.5f * (float)kNsC, Bo(k));   // B = b A + c A A (symmetrised)
+      const void* a2[1] = {Bo(k)};
+      const void* b2[1] = {Xo(k)};
       float* o2[1] = {at<float>(N.p1)};
       if (!rc) rc = grad2(a2, b2, o2, 1);   // B X
       if (!rc) rc = lin(1, X, nullptr, at<float>(N.p1), nullptr, nullptr, nullptr, (float)kNsA, X,
-                        k + 1 < steps ? X16(k + 1) : nullptr);
+                        k + 1 < steps ? Xo(k + 1) : nullptr);
     }
     if (!rc) rc = scatter(X, -1.0f, pst());
     return rc;
@@ -1341,21 +1356,16 @@ struct NsBwd {
   int reverse() const {
     float* G = at<float>(N.g);
     float* X = at<float>(N.x32);
-    _Float16* T = at<_Float16>(N.t16);
+    uint8_t* T = buf(N.to);
     int rc = gather(at<float>(N.ustep), 1, 0, -1.0f, X);   // d step = -dU
     if (!rc) rc = lin(1, X, nullptr, nullptr, nullptr, nullptr, nullptr, 1.0f, nullptr, T);
     for (int k = steps - 1; k >= 0 && !rc; --k) {
-      rc = out(T, N.n, mn(), X16(k), N.n, mn(), at<_Float16>(N.db16), N.m, N.m, N.n);   // dB = dX' X^T
-      if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] {
-        return launch_sym(nullptr, 0.f, at<_Float16>(N.db16), 1.0f, at<_Float16>(N.s16), N.S, N.m, s);
-      });
-      if (!rc) rc = out(at<_Float16>(N.s16), N.m, mm(), A16(k), N.m, mm(), at<_Float16>(N.q16), N.m, N.m, N.m);
-      if (!rc) rc = timed(LACT_KCLASS_NS, 0.0, s, [&] {   // M = b S + c (S A + (S A)^T)
-        return launch_sym(at<_Float16>(N.s16), (float)kNsB, at<_Float16>(N.q16), (float)kNsC, at<_Float16>(N.m16),
-                          N.S, N.m, s);
-      });
-      const _Float16* a2[2] = {B16(k), at<_Float16>(N.m16)};
-      const _Float16* b2[2] = {T, X16(k)};
+      rc = out(T, N.n, mn(), Xo(k), N.n, mn(), buf(N.dbo), N.m, N.m, N.n);   // dB = dX' X^T
+      if (!rc) rc = sym(nullptr, 0.f, buf(N.dbo), 1.0f, buf(N.so));
+      if (!rc) rc = out(buf(N.so), N.m, mm(), Ao(k), N.m, mm(), buf(N.qo), N.m, N.m, N.m);
+      if (!rc) rc = sym(buf(N.so), (float)kNsB, buf(N.qo), (float)kNsC, buf(N.mo));   // M = b S + c (S A + (S A)^T)
+      const void* a2[2] = {Bo(k), buf(N.mo)};
+      const void* b2[2] = {T, Xo(k)};
       float* o2[2] = {at<float>(N.p1), at<float>(N.p2)};
       if (!rc) rc = grad2(a2, b2, o2, 2);   // B dX', M X
       if (!rc) rc = lin(1, X, nullptr, at<float>(N.p1), at<float>(N.p2), nullptr, nullptr, (float)kNsA, X,
@@ -1402,7 +1412,6 @@ int bwd_layout(const lact_desc* dsc, BwdLayout* L, bool mom = false) {
   int rc = check_desc(dsc);
   if (rc) return rc;
   if (dsc->fast_weight != LACT_FW_LINEAR) return LACT_EUNSUPPORTED;
-  if (dsc->use_muon && dsc->io_dtype != LACT_IO_BF16) return LACT_EUNSUPPORTED;   // fp16 Newton-Schulz reverse
   L->p = make_plan(dsc);
   const Plan& p = L->p;
   const double dd = (double)p.d * p.d;
@@ -1802,7 +1811,6 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false, int64_
   int rc = check_desc(dsc);
   if (rc) return rc;
   if (dsc->fast_weight != LACT_FW_SWIGLU) return LACT_EUNSUPPORTED;
-  if (dsc->use_muon && dsc->io_dtype != LACT_IO_BF16) return LACT_EUNSUPPORTED;   // fp16 Newton-Schulz reverse
   L->p = make_plan(dsc, false);
   const Plan& p = L->p;
   const double dh = (double)p.d * p.h;
@@ -2077,7 +2085,7 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       for (int m = 0; m < 3; ++m) {
         ua.W[m] = traj(u + 1, m);
         ua.Wsrc[m] = traj(u, m);
-        ua.Wb[m] = c.wb[c.wset][m];
+        ua.Wb[m] = p.bf16 ? c.wb[c.wset][m] : nullptr;   // fp32: the next contractions read the state
       }
       ua.step = nb.pst();
       ua.nsplit = 1;

@@ -388,12 +388,16 @@ struct NsLinArgs {
   const float* sc; const float* sc2;
   float a, eps;
   float* out32; _Float16* out16;
+  float* outc32;   // an fp32 operand copy (fp32 I/O) in place of out16
   int S; int64_t len;
 };
 hipError_t launch_ns_lin(const NsLinArgs& a, hipStream_t s);
 // out = alpha X + beta (Y + Y^T) per slot of fp16 [m x m] matrices (X may be nullptr).
 hipError_t launch_sym(const _Float16* X, float alpha, const _Float16* Y, float beta, _Float16* out, int S, int m,
                       hipStream_t s);
+// The same for fp32 slots (fp32 I/O).
+hipError_t launch_sym32(const float* X, float alpha, const float* Y, float beta, float* out, int S, int m,
+                        hipStream_t s);
 // G = base + sum of the sets over BH instances of RL floats each (RL a
 // multiple of 4); base: 0 (mode 0), init (mode 1) or G itself (mode 2).
 hipError_t launch_accum(float* G, int64_t g_inst, const float* init, int64_t i_inst, int mode, PartSet s0, PartSet s1,

@@ -2595,6 +2595,7 @@ __global__ __launch_bounds__(256) void k_ns_lin(const NsLinArgs a) {
     }
     if (a.out32) reinterpret_cast<float4*>(a.out32)[q] = r;
     if (a.out16) st4<_Float16>(a.out16, 4 * q, r.x, r.y, r.z, r.w);
+    if (a.outc32) reinterpret_cast<float4*>(a.outc32)[q] = r;
   }
 }
 
@@ -2636,6 +2637,44 @@ __global__ __launch_bounds__(256) void k_sym(const _Float16* X, float alpha, con
       v[j] = (_Float16)t;
     }
     *reinterpret_cast<h8*>(out + o) = v;
+  }
+}
+
+// The fp32 form of k_sym: 64 x 64 tiles, float4 vectors (m a multiple of 4).
+__global__ __launch_bounds__(256) void k_sym32(const float* X, float alpha, const float* Y, float beta, float* out,
+                                               int m, int tiles) {
+  __shared__ float mir[64][65];
+  const int per = tiles * tiles;
+  const int64_t slot = blockIdx.x / per;
+  const int rest = blockIdx.x - (int)slot * per;
+  const int r0 = (rest / tiles) * 64, c0 = (rest % tiles) * 64;
+  const int64_t base = slot * (int64_t)m * m;
+  const int tv = threadIdx.x & 15, ty = threadIdx.x >> 4;   // 16 vectors per 64-wide row, 16 rows per pass
+  for (int k = ty; k < 64; k += 16) {   // mirror tile: mir[k][j] = Y[c0 + k][r0 + j]
+    const int r = c0 + k, c = r0 + 4 * tv;
+    float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < m && c < m) y = *reinterpret_cast<const float4*>(Y + base + (int64_t)r * m + c);
+    mir[k][4 * tv] = y.x;
+    mir[k][4 * tv + 1] = y.y;
+    mir[k][4 * tv + 2] = y.z;
+    mir[k][4 * tv + 3] = y.w;
+  }
+  __syncthreads();
+  for (int k = ty; k < 64; k += 16) {
+    const int r = r0 + k, c = c0 + 4 * tv;
+    if (r >= m || c >= m) continue;
+    const int64_t o = base + (int64_t)r * m + c;
+    const float4 y = *reinterpret_cast<const float4*>(Y + o);
+    float4 v = make_float4(beta * (y.x + mir[4 * tv][k]), beta * (y.y + mir[4 * tv + 1][k]),
+                           beta * (y.z + mir[4 * tv + 2][k]), beta * (y.w + mir[4 * tv + 3][k]));
+    if (X) {
+      const float4 x = *reinterpret_cast<const float4*>(X + o);
+      v.x += alpha * x.x;
+      v.y += alpha * x.y;
+      v.z += alpha * x.z;
+      v.w += alpha * x.w;
+    }
+    *reinterpret_cast<float4*>(out + o) = v;
   }
 }
 
@@ -3121,6 +3160,17 @@ hipError_t launch_sym(const _Float16* X, float alpha, const _Float16* Y, float b
   if (blocks <= 0) return hipSuccess;
   if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   k_sym<<<(unsigned)blocks, 256, 0, s>>>(X, alpha, Y, beta, out, m, tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_sym32(const float* X, float alpha, const float* Y, float beta, float* out, int S, int m,
+                        hipStream_t s) {
+  if (m % 4) return hipErrorInvalidValue;
+  const int tiles = (m + 63) / 64;
+  const int64_t blocks = (int64_t)S * tiles * tiles;
+  if (blocks <= 0) return hipSuccess;
+  if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  k_sym32<<<(unsigned)blocks, 256, 0, s>>>(X, alpha, Y, beta, out, m, tiles);
   return hipGetLastError();
 }
 

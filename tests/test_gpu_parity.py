@@ -1438,7 +1438,7 @@ def check_linear_bwd(cfg, x, ct, got, with_dW=True, instances=None):
         assert_errs(errs, TOL[cfg.io], blocks)
         return
     names = ("dq", "dk", "dv", "deta", "dW0")
-    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io])
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io], cfg.io)
     wb, bb = dict(zip(names, whole)), dict(zip(names, block))
     wb["deta/(|k||Z|)"] = max(TOL[cfg.io], wb["deta"])
     assert_bars(errs, blocks, wb, bb)
@@ -1548,24 +1548,27 @@ def worst_window(got, ref, rows):
     return worst, where
 
 
-def ulp_neighbour(x, seed):
-    """The bf16 token tensors q, k, v of `x` moved by at most one bf16 ulp
-    (a relative 2^-8 jitter, rounded back to bf16): another rounding of the
-    same data, equally valid as bf16 input."""
+def ulp_neighbour(x, seed, io="bf16"):
+    """The token tensors q, k, v of `x` moved by at most one ulp of the I/O
+    type (bf16: a relative 2^-8 jitter rounded back to bf16; fp32: a relative
+    2^-23 jitter): another rounding of the same data, equally valid input."""
     from lact_synth import round_to_bf16
     rng = np.random.default_rng(seed)
-    j = lambda a: round_to_bf16((a * (1.0 + 2.0 ** -8 * rng.uniform(-1.0, 1.0, a.shape))).astype(np.float32))
+    if io == "fp32":
+        j = lambda a: (a * (1.0 + 2.0 ** -23 * rng.uniform(-1.0, 1.0, a.shape))).astype(np.float32)
+    else:
+        j = lambda a: round_to_bf16((a * (1.0 + 2.0 ** -8 * rng.uniform(-1.0, 1.0, a.shape))).astype(np.float32))
     return dict(x, q=j(x["q"]), k=j(x["k"]), v=j(x["v"]))
 
 
-def muon_bars(ref_fn, x, ref, tol):
+def muon_bars(ref_fn, x, ref, tol, io="bf16"):
     """Bars of the Muon backward: Newton-Schulz amplifies small singular
     directions of the chunk gradient (a factor up to a^5 ~ 480), so its
     reverse is ill-conditioned in the gradient. The oracle's own results for
-    two bf16 roundings of the same inputs (ulp_neighbour) differ by spread_j
-    per output; the bar is max(tol, spread_j) over the tensor and
-    max(tol, 1.5 spread_j) over a block."""
-    alt = ref_fn(ulp_neighbour(x, 2505))
+    two roundings of the same inputs (ulp_neighbour) differ by spread_j per
+    output; the bar is max(tol, spread_j) over the tensor and max(tol,
+    1.5 spread_j) over a block."""
+    alt = ref_fn(ulp_neighbour(x, 2505, io))
     spread = [rel(a, b) for a, b in zip(alt, ref)]
     print("[gpu] oracle spread under one-ulp input changes", [f"{v:.2e}" for v in spread], flush=True)
     return [max(tol, v) for v in spread], [max(tol, 1.5 * v) for v in spread]
@@ -1604,7 +1607,7 @@ def check_swiglu_bwd(cfg, x, ct, got, with_dW=True, instances=None):
     if not cfg.use_muon:
         assert_errs(errs, TOL[cfg.io], blocks)
         return
-    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io])
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io], cfg.io)
     assert_bars(errs, blocks, dict(zip(names, whole)), dict(zip(names, block)))
 
 
@@ -1700,6 +1703,22 @@ def test_linear_muon_backward_two_chunks(d):
     check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct))
 
 
+@pytest.mark.parametrize("order", [0, 1])
+def test_swiglu_muon_backward_fp32(order):
+    # fp32 I/O: the Newton-Schulz reverse on fp32 operands, held to the fp32 bar
+    cfg = CONFIGS["tiny_fp32"].with_(name="swiglu_muon_bwd_fp32", B=1, H=2, d=40, h=56, n_kv=160, n_q=180, chunk=80,
+                                     order=order, use_muon=1, ns_steps=5)
+    x, ct = make_inputs(cfg, 84), make_cotangents(cfg, 84)
+    check_swiglu_bwd(cfg, x, ct, run_gpu_swiglu_bwd(cfg, x, ct))
+
+
+def test_linear_muon_backward_fp32():
+    cfg = CONFIGS["tiny_fp32"].with_(name="linear_muon_bwd_fp32", B=1, H=2, d=64, h=64, n_kv=128, n_q=150, chunk=64,
+                                     order=1, use_muon=1, ns_steps=5, linear=1)
+    x, ct = make_inputs(cfg, 85), make_cotangents(cfg, 85)
+    check_linear_bwd(cfg, x, ct, run_gpu_linear_bwd(cfg, x, ct))
+
+
 # ----------------------------------------------------------------------------- momentum backward
 # lact_backward_momentum: the reverse of the chunk loop with the momentum
 # optimizer (M' = bbar M + g, the step M' or Muon(M')) against the oracle's
@@ -1778,7 +1797,7 @@ def check_mom_bwd(cfg, x, ct, st, got, with_final=True, instances=None):
     if not cfg.use_muon:
         assert_errs(errs, TOL[cfg.io], blocks)
         return
-    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io])
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io], cfg.io)
     wb, bb = dict(zip(names, whole)), dict(zip(names, block))
     # with Muon, dbeta's per-chunk values are held to the scaled bound, with
     # the bar of dM' (that of the state's cotangents); the few per-chunk
@@ -1856,6 +1875,12 @@ def test_swiglu_muon_momentum_backward_small_matrices(order):
 
 def test_swiglu_muon_momentum_backward_lm_shape_two_chunks():
     cfg, x, ct, st = mom_case("lm32k_muon_mom", 98, name="swiglu_muon_mom_bwd_lm", B=1, H=2, n_kv=4096, n_q=4096)
+    check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
+
+
+def test_swiglu_muon_momentum_backward_fp32():
+    cfg, x, ct, st = mom_case("tiny_fp32", 100, name="swiglu_muon_mom_bwd_fp32", B=1, H=2, d=40, h=56, n_kv=160,
+                              n_q=160, chunk=80, use_muon=1, ns_steps=5)
     check_mom_bwd(cfg, x, ct, st, run_gpu_mom_bwd(cfg, x, ct, st))
 
 
@@ -1972,7 +1997,7 @@ def check_sched_bwd(cfg, x, ct, schedule, got, st=None, with_final=True):
     if not cfg.use_muon:
         assert_errs(errs, TOL[cfg.io], blocks)
         return
-    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io])
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io], cfg.io)
     wb, bb = dict(zip(names, whole)), dict(zip(names, block))
     if st is not None:   # as in the momentum backward's Muon tests: few per-update values
         wb["dbeta"], bb["dbeta"] = float("inf"), float("inf")

@@ -558,8 +558,8 @@ def measure(cfg, args, P, on_device=False):
 
     if args.backward:
         from lact_synth import make_cotangents
-        if on_device or (cfg.use_muon and cfg.io != "bf16"):
-            raise SystemExit("--backward runs on host-drawn inputs (Muon with bf16 I/O)")
+        if on_device:
+            raise SystemExit("--backward runs on host-drawn inputs")
         ct = make_cotangents(cfg, 0)
         dout = torch.from_numpy(ct["do"].reshape(cfg.B, cfg.H, cfg.n_q, cfg.d)).to(dev, io)
         del ct

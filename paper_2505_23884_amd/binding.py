@@ -340,7 +340,7 @@ def backward_linear(q, k, v, eta, W0, dout, chunk, order=APPLY_THEN_UPDATE, dW_f
 def backward(q, k, v, eta, W1, W2, W3, dout, chunk, order=APPLY_THEN_UPDATE, dW_final=None, use_muon=False,
              ns_steps=5, out=None, workspace=None, stream=None):
     """Backward of forward() for the SwiGLU fast weight (lact_backward), with
-    or without Muon (bf16 I/O for Muon), no momentum: the cotangents of q, k, v, eta and of the initial fast
+    or without Muon, one rate per token or per matrix, no momentum: the cotangents of q, k, v, eta and of the initial fast
     weights W1, W2, W3 (fp32, not written) given dout (q's shape and dtype)
     and, optionally, dW_final = (dW1, dW2, dW3) of the final fast weights (any
     of them None). Returns (dq, dk, dv, deta, dW1, dW2, dW3), written into

@@ -1275,6 +1275,50 @@ def test_output_rmsnorm_backward_lm_tokens():
     assert rel(dw.cpu().numpy(), rdw) <= 1e-4   # fp32 sums of bf16 products: far inside the bf16 bar
 
 
+def test_layer_training_step_chain():
+    # the layer's training step through the entry points (prologue, forward
+    # with momentum and per-matrix rates, RMSNorm, then the three reverses)
+    # against the oracle's chain from the same raw inputs
+    B, H, L, d, h, C = 1, 2, 384, 64, 128, 128
+    qkv, lr, br = _raw_inputs(120, B, L, H, d, 3, "bf16")
+    rng = np.random.default_rng(121)
+    from lact_synth import round_to_bf16
+    dy = round_to_bf16(rng.standard_normal((B, L, H, d), dtype=np.float32))
+    w = rng.standard_normal((H, d), dtype=np.float32)
+    cfg = CONFIGS["lm32k"].with_(name="train_chain", B=B, H=H, d=d, h=h, n_kv=L, n_q=L, chunk=C)
+    x = make_inputs(cfg, 122)
+    dev = lambda a, t=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", t)
+    print("[gpu] layer training step chain", flush=True)
+    qkv_d, lr_d, br_d = dev(qkv, torch.bfloat16), dev(lr), dev(br)
+    q, k, v, eta, beta = P.prologue(qkv_d, lr_d, -2.0, br_d)
+    W = [dev(x[n].reshape(B, H, *x[n].shape[1:])) for n in ("W1", "W2", "W3")]
+    W0 = tuple(t.clone() for t in W)
+    o, M = P.forward_momentum(q, k, v, eta, beta, *W, chunk=C)
+    M0 = tuple(torch.zeros_like(t) for t in W)
+    w_d = dev(w)
+    d_o, dw = P.rmsnorm_out_backward(o, dev(dy, torch.bfloat16), w_d)
+    dq, dk, dv, deta, dbeta, dW, dM = P.backward_momentum(q, k, v, eta, beta, W0, M0, d_o, C)
+    dqkv, dlr, dbr = P.prologue_backward(qkv_d, lr_d, -2.0, br_d, dq, dk, dv, deta, dbeta)
+    torch.cuda.synchronize()
+    # the oracle's chain in fp64
+    rq, rk, rv, reta, rbeta = O.qkv_prologue(qkv, lr, -2.0, br)
+    ro = O.lact_forward_momentum(rq, rk, rv, reta, rbeta, x["W1"], x["W2"], x["W3"], chunk=C, order=0)[0]
+    rdo, rdw = O.rmsnorm_out_vjp(ro, B, H, dy, w)
+    zeros = tuple(np.zeros_like(x[n]) for n in ("W1", "W2", "W3"))
+    r = O.lact_backward_momentum(rq, rk, rv, reta, rbeta, (x["W1"], x["W2"], x["W3"]), zeros, rdo, C, 0)
+    rq_, rk_, rv_, re_, rb_ = r[:5]
+    rdqkv, rdlr, rdbr = O.qkv_prologue_vjp(qkv, lr, -2.0, br, rq_, rk_, rv_, re_, rb_)
+    g = lambda t: t.float().cpu().numpy()
+    errs = {"dnorm_w": rel(g(dw), rdw), "dqkv": rel(g(dqkv), rdqkv), "dlr_raw": rel(g(dlr), rdlr),
+            "dbeta_raw": rel(g(dbr), rdbr)}
+    for j, n in enumerate(("dW1", "dW2", "dW3")):
+        errs[n] = rel(g(dW[j]).reshape(r[5][j].shape), r[5][j])
+        errs["dM" + n[2:]] = rel(g(dM[j]).reshape(r[6][j].shape), r[6][j])
+    print("[gpu] rel-L2", {k_: f"{v_:.2e}" for k_, v_ in errs.items()}, flush=True)
+    for k_, v_ in errs.items():
+        assert v_ <= TOL["bf16"], (k_, v_)
+
+
 def test_layer_chain_prologue_path_norm():
     # projections -> prologue -> path (momentum, per-matrix rates) -> RMSNorm,
     # all on the GPU, against the oracle's chain

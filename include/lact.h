@@ -225,9 +225,10 @@ int lact_forward_momentum(const lact_desc* desc,
  * Momentum: with M1 != NULL the updates use the momentum optimizer of
  * lact_forward_momentum (each update segment's own mean of beta), and beta,
  * M1, M2, M3 follow its rules; with M1 == NULL, beta, M2 and M3 are ignored
- * and the updates are plain. Other arguments, the workspace
- * (lact_workspace_bytes(desc)) and the errors are those of lact_forward; an
- * invalid segment is LACT_EINVAL.
+ * and the updates are plain. With the linear fast weight (desc->fast_weight,
+ * §5.4) W1 is the d x d weight and M1 its state; W2, W3, M2, M3 are unused.
+ * Other arguments, the workspace (lact_workspace_bytes(desc)) and the errors
+ * are those of lact_forward; an invalid segment is LACT_EINVAL.
  */
 #define LACT_SEG_APPLY_THEN_UPDATE 0
 #define LACT_SEG_UPDATE_THEN_APPLY 1
@@ -401,8 +402,10 @@ int lact_backward_momentum(const lact_desc* desc,
 /*
  * Backward of lact_forward_schedule (the ttt_config loop of Alg. 1: update,
  * apply, update-then-apply and apply-then-update segments, such as the
- * strided mask of teacher-forced video of §4.3), SwiGLU fast weight, with or
- * without Muon (bf16 I/O) and, with M1 != NULL, the momentum optimizer (as
+ * strided mask of teacher-forced video of §4.3), SwiGLU or linear fast
+ * weight (§5.4: W1 the d x d weight, M1 its state, dW1 and dM1 their
+ * cotangents; W2, W3, M2, M3 and their cotangents unused), with or
+ * without Muon and, with M1 != NULL, the momentum optimizer (as
  * lact_backward_momentum, each update segment's own mean of beta; with
  * M1 == NULL beta, M2, M3, their final cotangents, dbeta and dM are
  * ignored). The segments' events are replayed by the forward's launches and
@@ -418,8 +421,8 @@ int lact_backward_momentum(const lact_desc* desc,
  *               M1 != NULL), 256-byte aligned (it grows with the number of
  *               update segments)
  *
- * Errors as lact_backward_momentum; an invalid segment is LACT_EINVAL, the
- * linear fast weight LACT_EUNSUPPORTED.
+ * Errors as lact_backward_momentum; an invalid segment, or nseg < 0, is
+ * LACT_EINVAL.
  */
 size_t lact_backward_schedule_workspace_bytes(const lact_desc* desc, const lact_segment* segs, int64_t nseg,
                                               int momentum, int* err);

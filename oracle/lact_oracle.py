@@ -888,36 +888,50 @@ def lact_forward_schedule_instance(q, k, v, eta, W1, W2, W3, schedule, use_muon:
     index), each segment a single update and/or apply over tokens [begin, end)
     (reading R10). q [n_q, d]; k, v [n_kv, d]; eta [n_kv] or [n_kv, 3]; with
     ``beta`` the updates use momentum (state ``M``, zeros if omitted).
-    Returns (o [n_q, d], (W1, W2, W3)) or, with beta, (o, W, M).
+    With W2 and W3 None the fast weight is the linear one of §5.4 (W1 [d, d],
+    o = W1 q, g = linear_gradient, M a single [d, d] array).
+    Returns (o [n_q, d], (W1, W2, W3)) or, with beta, (o, W, M); W and M
+    single arrays for the linear fast weight.
     """
-    W = tuple(np.asarray(w, dtype=np.float64).copy() for w in (W1, W2, W3))
+    linear = W2 is None and W3 is None
+    W = tuple(np.asarray(w, dtype=np.float64).copy() for w in ((W1,) if linear else (W1, W2, W3)))
     mom = beta is not None
     if mom:
         M = tuple(np.zeros_like(w) for w in W) if M is None else tuple(
-            np.asarray(m, dtype=np.float64).copy() for m in M)
+            np.asarray(m, dtype=np.float64).copy() for m in ((M,) if linear else M))
     o = np.zeros((q.shape[0], q.shape[1]))
 
     def upd(W, M, b, e):
         assert e <= k.shape[0]
+        if linear:
+            g = linear_gradient(W[0], k[b:e], v[b:e], eta[b:e])
+            if mom:
+                M = (float(np.mean(np.asarray(beta[b:e], dtype=np.float64))) * M[0] + g,)
+                g = M[0]
+            return (weight_update(W[0], newton_schulz(g, ns_steps) if use_muon else g),), M
         if mom:
             return momentum_update(W, M, k[b:e], v[b:e], eta[b:e], beta[b:e], use_muon, ns_steps, token_block)
         return update(W, k[b:e], v[b:e], eta[b:e], use_muon, ns_steps, token_block), M
+
+    apply_fw = (lambda Wl, X: np.asarray(X, dtype=np.float64) @ Wl.T) if linear else swiglu_apply
 
     for mode, b, e in schedule:
         mode = SCHEDULE_MODES[mode] if not isinstance(mode, str) else mode
         assert 0 <= b < e, "segments are non-empty"
         if mode == "update_then_apply":
             W, M = upd(W, M, b, e)
-            o[b:e] = swiglu_apply(*W, q[b:e])
+            o[b:e] = apply_fw(*W, q[b:e])
         elif mode == "apply_then_update":
-            o[b:e] = swiglu_apply(*W, q[b:e])
+            o[b:e] = apply_fw(*W, q[b:e])
             W, M = upd(W, M, b, e)
         elif mode == "update_only":
             W, M = upd(W, M, b, e)
         elif mode == "apply_only":
-            o[b:e] = swiglu_apply(*W, q[b:e])
+            o[b:e] = apply_fw(*W, q[b:e])
         else:
             raise ValueError(mode)
+    if linear:
+        W, M = W[0], (M[0] if mom else M)
     return (o, W, M) if mom else (o, W)
 
 
@@ -925,16 +939,25 @@ def lact_forward_schedule(q, k, v, eta, W1, W2, W3, schedule, use_muon: bool = F
                           ns_steps: int = NS_STEPS_DEFAULT, beta=None, M1=None, M2=None, M3=None,
                           instances=None, token_block: int = 65536):
     """Batched driver of lact_forward_schedule_instance (one schedule for every
-    instance): returns (o, W1, W2, W3) stacked, plus (M1, M2, M3) with beta."""
+    instance): returns (o, W1, W2, W3) stacked, plus (M1, M2, M3) with beta;
+    with W2 and W3 None (the linear fast weight) (o, W) and (o, W, M)."""
+    linear = W2 is None and W3 is None
     idx = range(q.shape[0]) if instances is None else instances
     res = []
     for i in idx:
         kw = {}
         if beta is not None:
-            kw = dict(beta=beta[i], M=None if M1 is None else (M1[i], M2[i], M3[i]))
-        r = lact_forward_schedule_instance(q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], schedule,
-                                           use_muon, ns_steps, token_block=token_block, **kw)
-        res.append((r[0], *r[1]) + (tuple(r[2]) if beta is not None else ()))
+            if linear:
+                kw = dict(beta=beta[i], M=None if M1 is None else M1[i])
+            else:
+                kw = dict(beta=beta[i], M=None if M1 is None else (M1[i], M2[i], M3[i]))
+        r = lact_forward_schedule_instance(q[i], k[i], v[i], eta[i], W1[i], None if linear else W2[i],
+                                           None if linear else W3[i], schedule, use_muon, ns_steps,
+                                           token_block=token_block, **kw)
+        if linear:
+            res.append(tuple(r))
+        else:
+            res.append((r[0], *r[1]) + (tuple(r[2]) if beta is not None else ()))
     return tuple(np.stack(col) for col in zip(*res))
 
 
@@ -954,18 +977,27 @@ def lact_backward_schedule_instance(q, k, v, eta, W1, W2, W3, do, schedule, dW_f
     then chunk_gradient_vjp over its tokens. An output row written by more
     than one apply keeps the last value, so only the last apply of a row
     receives that row's cotangent; key rows used by more than one update
-    collect every update's share.
+    collect every update's share. With W2 and W3 None the fast weight is the
+    linear one (W1 [d, d]; M, dW_final, dM_final single arrays): an apply
+    gives dq = dO W and dW += dO^T q, an update's gradient cotangent dg
+    gives dv, dk, deta as in lact_backward_linear_instance.
     Returns (dq, dk, dv, deta, (dW1, dW2, dW3)) or, with beta,
-    (dq, dk, dv, deta, dbeta, (dW1, dW2, dW3), (dM1, dM2, dM3)).
+    (dq, dk, dv, deta, dbeta, (dW1, dW2, dW3), (dM1, dM2, dM3)); dW and dM
+    single arrays for the linear fast weight.
     """
     q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
     eta = np.asarray(eta, dtype=np.float64)
     do = np.asarray(do, dtype=np.float64)
     mom = beta is not None
+    linear = W2 is None and W3 is None
+    tup = (lambda a: (a,)) if linear else tuple
     step_of = (lambda g: newton_schulz(g, ns_steps)) if use_muon else (lambda g: g)
-    W = tuple(np.asarray(w, dtype=np.float64).copy() for w in (W1, W2, W3))
+    grad = (lambda Wc, b, e: (linear_gradient(Wc[0], k[b:e], v[b:e], eta[b:e]),)) if linear else \
+        (lambda Wc, b, e: chunk_gradient(*Wc, k[b:e], v[b:e], eta[b:e]))
+    W = tuple(np.asarray(w, dtype=np.float64).copy() for w in ((W1,) if linear else (W1, W2, W3)))
     Mc = tuple(np.zeros_like(w) for w in W) if M is None else tuple(np.asarray(m, dtype=np.float64).copy()
-                                                                    for m in M)
+                                                                    for m in tup(M))
+    nm = len(W)
     parts = {"update_then_apply": ("update", "apply"), "apply_then_update": ("apply", "update"),
              "update_only": ("update",), "apply_only": ("apply",)}
     Ws, Ms, steps, bbars, events = [W], [Mc], [], [], []
@@ -974,7 +1006,7 @@ def lact_backward_schedule_instance(q, k, v, eta, W1, W2, W3, do, schedule, dW_f
         for kind in parts[mode]:
             events.append((kind, b, e, len(Ws) - 1))
             if kind == "update":
-                g = chunk_gradient(*Ws[-1], k[b:e], v[b:e], eta[b:e])
+                g = grad(Ws[-1], b, e)
                 if mom:
                     bbar = float(np.mean(np.asarray(beta, dtype=np.float64)[b:e]))
                     src = tuple(bbar * m + gj for m, gj in zip(Ms[-1], g))
@@ -985,9 +1017,9 @@ def lact_backward_schedule_instance(q, k, v, eta, W1, W2, W3, do, schedule, dW_f
                 steps.append(src)
                 Ws.append(tuple(weight_update(w, step_of(x)) for w, x in zip(Ws[-1], src)))
     dW = [np.zeros_like(w) for w in W] if dW_final is None else [
-        np.asarray(x, dtype=np.float64).copy() for x in dW_final]
+        np.asarray(x, dtype=np.float64).copy() for x in tup(dW_final)]
     dM = [np.zeros_like(w) for w in W] if dM_final is None else [
-        np.asarray(x, dtype=np.float64).copy() for x in dM_final]
+        np.asarray(x, dtype=np.float64).copy() for x in tup(dM_final)]
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
     deta, dbeta = np.zeros(eta.shape), np.zeros(k.shape[0])
     claimed = np.zeros(q.shape[0], dtype=bool)
@@ -995,29 +1027,40 @@ def lact_backward_schedule_instance(q, k, v, eta, W1, W2, W3, do, schedule, dW_f
         if kind == "apply":
             dO = np.where(claimed[b:e, None], 0.0, do[b:e])
             claimed[b:e] = True
+            if linear:
+                dq[b:e] += dO @ Ws[wi][0]
+                dW[0] += dO.T @ q[b:e]
+                continue
             dx, a1, a2, a3 = swiglu_apply_vjp(*Ws[wi], q[b:e], dO)
             dq[b:e] += dx
             for j, a in enumerate((a1, a2, a3)):
                 dW[j] += a
             continue
         dg = []
-        for j in range(3):
+        for j in range(nm):
             dW[j], dst = weight_update_vjp(Ws[wi][j], step_of(steps[wi][j]), dW[j])
             dg.append(newton_schulz_vjp(steps[wi][j], dst, ns_steps) if use_muon else dst)
         if mom:
             dg = [a + x for a, x in zip(dM, dg)]
-        b1, b2, b3, dkc, dvc, detac = chunk_gradient_vjp(*Ws[wi], k[b:e], v[b:e], eta[b:e], *dg)
-        for j, x in enumerate((b1, b2, b3)):
-            dW[j] += x
-        dk[b:e] += dkc
-        dv[b:e] += dvc
-        deta[b:e] += detac
+        if linear:                          # g = -sum eta v k^T does not depend on W
+            kg = k[b:e] @ dg[0].T
+            dv[b:e] += -eta[b:e, None] * kg
+            dk[b:e] += -eta[b:e, None] * (v[b:e] @ dg[0])
+            deta[b:e] += -np.sum(v[b:e] * kg, axis=1)
+        else:
+            b1, b2, b3, dkc, dvc, detac = chunk_gradient_vjp(*Ws[wi], k[b:e], v[b:e], eta[b:e], *dg)
+            for j, x in enumerate((b1, b2, b3)):
+                dW[j] += x
+            dk[b:e] += dkc
+            dv[b:e] += dvc
+            deta[b:e] += detac
         if mom:
             dbeta[b:e] += sum(float(np.sum(a * m)) for a, m in zip(dg, Ms[wi])) / (e - b)
             dM = [bbars[wi] * a for a in dg]
+    out = (lambda t: t[0]) if linear else tuple
     if mom:
-        return dq, dk, dv, deta, dbeta, tuple(dW), tuple(dM)
-    return dq, dk, dv, deta, tuple(dW)
+        return dq, dk, dv, deta, dbeta, out(dW), out(dM)
+    return dq, dk, dv, deta, out(dW)
 
 
 def lact_backward_schedule(q, k, v, eta, W1, W2, W3, do, schedule, dW_final=None, use_muon: bool = False,
@@ -1025,15 +1068,24 @@ def lact_backward_schedule(q, k, v, eta, W1, W2, W3, do, schedule, dW_final=None
     """Batched driver of lact_backward_schedule_instance (one schedule for
     every instance): (dq, dk, dv, deta, dW1, dW2, dW3) stacked, and with beta
     (dq, dk, dv, deta, dbeta, dW1, dW2, dW3, dM1, dM2, dM3); W, M and the
-    final cotangents are triples of [BH, ...] arrays (or None)."""
+    final cotangents are triples of [BH, ...] arrays (or None). With W2 and
+    W3 None (the linear fast weight) they are single [BH, d, d] arrays and
+    dW (dM) one stacked array each."""
+    linear = W2 is None and W3 is None
     idx = range(q.shape[0]) if instances is None else instances
-    pick = lambda t, i: None if t is None else tuple(x[i] for x in t)
+    if linear:
+        pick = lambda t, i: None if t is None else t[i]
+        lst = lambda a: (a,)
+    else:
+        pick = lambda t, i: None if t is None else tuple(x[i] for x in t)
+        lst = tuple
     res = []
     for i in idx:
-        r = lact_backward_schedule_instance(q[i], k[i], v[i], eta[i], W1[i], W2[i], W3[i], do[i], schedule,
+        r = lact_backward_schedule_instance(q[i], k[i], v[i], eta[i], W1[i], None if linear else W2[i],
+                                            None if linear else W3[i], do[i], schedule,
                                             pick(dW_final, i), use_muon, ns_steps,
                                             None if beta is None else beta[i], pick(M, i), pick(dM_final, i))
-        flat = r[:4] + tuple(r[4]) if beta is None else r[:5] + tuple(r[5]) + tuple(r[6])
+        flat = r[:4] + lst(r[4]) if beta is None else r[:5] + lst(r[5]) + lst(r[6])
         res.append(flat)
     return tuple(np.stack(col) for col in zip(*res))
 

@@ -455,18 +455,30 @@ def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_s
     ``chunk`` (the workspace bound) defaults to the longest update segment.
     With ``beta`` the updates use momentum (M1..M3 updated in place, zeros
     allocated when omitted). Returns o, or (o, (M1, M2, M3)) with beta.
+    With W2 and W3 None the fast weight is the linear one (W1 [.., d, d];
+    M1 its state, returned alone; M2 and M3 unused).
     """
     import torch
     segs, longest = _segments(schedule)
+    linear = W2 is None and W3 is None
     extra = []
     if beta is not None:
-        if M1 is None and M2 is None and M3 is None:
-            M1, M2, M3 = (torch.zeros_like(w) for w in (W1, W2, W3))
-        if M1 is None or M2 is None or M3 is None:
-            raise LactError(-1, "pass all three momentum tensors or none")
-        extra = [(beta, "beta"), (M1, "M1"), (M2, "M2"), (M3, "M3")]
-    desc, out, workspace, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk or longest, 0, use_muon,
-                                            ns_steps, out, workspace, stream)
+        if linear:
+            M1 = torch.zeros_like(W1) if M1 is None else M1
+            if M1.shape != W1.shape:
+                raise LactError(-1, "M1 must have W1's shape")
+            extra = [(beta, "beta"), (M1, "M1")]
+        else:
+            if M1 is None and M2 is None and M3 is None:
+                M1, M2, M3 = (torch.zeros_like(w) for w in (W1, W2, W3))
+            if M1 is None or M2 is None or M3 is None:
+                raise LactError(-1, "pass all three momentum tensors or none")
+            extra = [(beta, "beta"), (M1, "M1"), (M2, "M2"), (M3, "M3")]
+    if linear and W1.shape[-1] != W1.shape[-2]:
+        raise LactError(-1, "the linear fast weight is square, [.., d, d]")
+    Wm = (W1, W1, W1) if linear else (W1, W2, W3)
+    desc, out, workspace, stream = _marshal(q, k, v, eta, *Wm, extra, chunk or longest, 0, use_muon,
+                                            ns_steps, out, workspace, stream, FW_LINEAR if linear else FW_SWIGLU)
     M = (M1, M2, M3) if beta is not None else (None, None, None)
     rc = lib().lact_forward_schedule(ctypes.byref(desc), segs, ctypes.c_int64(len(schedule)), _ptr(q), _ptr(k),
                                      _ptr(v), _ptr(eta), _ptr(beta), _ptr(W1), _ptr(W2), _ptr(W3),
@@ -475,7 +487,9 @@ def forward_schedule(q, k, v, eta, W1, W2, W3, schedule, *, use_muon=False, ns_s
                                      ctypes.c_void_p(stream))
     if rc:
         _raise(rc)
-    return (out, M) if beta is not None else out
+    if beta is not None:
+        return out, (M1 if linear else M)
+    return out
 
 
 def _segments(schedule):
@@ -508,15 +522,25 @@ def backward_schedule(q, k, v, eta, W1, W2, W3, dout, schedule, *, dW_final=None
     ``beta`` the momentum optimizer (M = (M1, M2, M3) the initial state, zeros
     when omitted; dM_final its final cotangents). Returns (dq, dk, dv, deta,
     (dW1, dW2, dW3)) or, with beta, (dq, dk, dv, deta, dbeta, (dW1, dW2, dW3),
-    (dM1, dM2, dM3)); written into ``out`` (that tuple) when given."""
+    (dM1, dM2, dM3)); written into ``out`` (that tuple) when given. With W2
+    and W3 None the fast weight is the linear one: W1 [.., d, d], and M,
+    dW_final, dM_final and the returned dW, dM single tensors."""
     import torch
     segs, longest = _segments(schedule)
-    W = (W1, W2, W3)
+    linear = W2 is None and W3 is None
+    if linear and W1.shape[-1] != W1.shape[-2]:
+        raise LactError(-1, "the linear fast weight is square, [.., d, d]")
+    one = lambda t: None if t is None else (t,)
+    W = (W1,) if linear else (W1, W2, W3)
     mom = beta is not None
+    if linear:
+        M, dW_final, dM_final = one(M), one(dW_final), one(dM_final)
+        if out is not None:
+            out = tuple(out[:-2]) + ((out[-2],), (out[-1],)) if mom else tuple(out[:-1]) + ((out[-1],),)
     if mom and M is None:
         M = tuple(torch.zeros_like(w) for w in W)
-    dWf = (None,) * 3 if dW_final is None else tuple(dW_final)
-    dMf = (None,) * 3 if (dM_final is None or not mom) else tuple(dM_final)
+    dWf = (None,) * len(W) if dW_final is None else tuple(dW_final)
+    dMf = (None,) * len(W) if (dM_final is None or not mom) else tuple(dM_final)
     for t, ref in zip(dWf + dMf + (tuple(M) if mom else ()), W * 3):
         if t is not None and (t.shape != ref.shape or t.dtype != torch.float32):
             raise LactError(-1, "momentum and final cotangents must have the fast weights' shapes, fp32")
@@ -525,8 +549,10 @@ def backward_schedule(q, k, v, eta, W1, W2, W3, dout, schedule, *, dW_final=None
     extra = [(t, "d_final") for t in dWf + dMf if t is not None]
     if mom:
         extra += [(beta, "beta")] + [(m, "M") for m in M]
-    desc, dq, _, stream = _marshal(q, k, v, eta, W1, W2, W3, extra, chunk or longest, 0, use_muon, ns_steps,
-                                   None if out is None else out[0], None, stream, FW_SWIGLU, need_workspace=False)
+    Wm = (W1, W1, W1) if linear else W
+    desc, dq, _, stream = _marshal(q, k, v, eta, *Wm, extra, chunk or longest, 0, use_muon, ns_steps,
+                                   None if out is None else out[0], None, stream,
+                                   FW_LINEAR if linear else FW_SWIGLU, need_workspace=False)
     if not dout.is_cuda or not dout.is_contiguous():
         raise LactError(-1, "dout must be a contiguous device tensor")
     if workspace is None:
@@ -536,21 +562,24 @@ def backward_schedule(q, k, v, eta, W1, W2, W3, dout, schedule, *, dW_final=None
         head = (dq, torch.empty_like(k), torch.empty_like(v), torch.empty_like(eta))
         dW = tuple(torch.empty_like(w) for w in W)
         dbeta = torch.empty_like(beta) if mom else None
-        dM = tuple(torch.empty_like(w) for w in W) if mom else (None,) * 3
+        dM = tuple(torch.empty_like(w) for w in W) if mom else (None,) * len(W)
     else:
         head = tuple(out[:4])
         dbeta = out[4] if mom else None
         dW = tuple(out[5] if mom else out[4])
-        dM = tuple(out[6]) if mom else (None,) * 3
-    Ms = tuple(M) if mom else (None,) * 3
-    args = ([_ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(beta)] + [_ptr(w) for w in W] + [_ptr(m) for m in Ms] +
-            [_ptr(dout)] + [_ptr(t) for t in dWf] + [_ptr(t) for t in dMf] + [_ptr(t) for t in head] +
-            [_ptr(dbeta)] + [_ptr(t) for t in dW] + [_ptr(t) for t in dM])
+        dM = tuple(out[6]) if mom else (None,) * len(W)
+    Ms = tuple(M) if mom else (None,) * len(W)
+    pad = lambda t: tuple(t) + (None,) * (3 - len(t))
+    args = ([_ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(beta)] + [_ptr(w) for w in pad(W)] +
+            [_ptr(m) for m in pad(Ms)] + [_ptr(dout)] + [_ptr(t) for t in pad(dWf)] + [_ptr(t) for t in pad(dMf)] +
+            [_ptr(t) for t in head] + [_ptr(dbeta)] + [_ptr(t) for t in pad(dW)] + [_ptr(t) for t in pad(dM)])
     rc = lib().lact_backward_schedule(ctypes.byref(desc), segs, ctypes.c_int64(len(schedule)), *args, _ptr(workspace),
                                       ctypes.c_size_t(workspace.numel() * workspace.element_size()),
                                       ctypes.c_void_p(stream))
     if rc:
         _raise(rc)
+    if linear:
+        dW, dM = dW[0], dM[0]
     if mom:
         return head + (dbeta, dW, dM)
     return head + (dW,)

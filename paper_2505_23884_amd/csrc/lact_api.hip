@@ -1378,6 +1378,77 @@ struct NsBwd {
   }
 };
 
+// One segment of the backward's schedule: a LACT_SEG_* mode over tokens
+// [b, e) and the number of updates before it: an update segment's own index
+// among the updates, and the index of the weight that an apply before its
+// update, or an apply-only segment, uses.
+struct BSeg {
+  int mode;
+  int64_t b, e;
+  int64_t before;
+};
+
+// The uniform schedule of lact_forward (chunks of desc->chunk, then the
+// apply-only tail), or the caller's segments checked for the backward: the
+// update ranges must not overlap each other, nor the apply ranges (the
+// reverse writes the cotangents of a token's rows once).
+int backward_segments(const lact_desc* desc, const lact_segment* segs, int64_t nseg, std::vector<BSeg>* out,
+                      int64_t* nupd, int64_t* longest_apply) {
+  out->clear();
+  *nupd = 0;
+  *longest_apply = 0;
+  if (nseg < 0) {
+    const int mode = desc->order == LACT_UPDATE_THEN_APPLY ? LACT_SEG_UPDATE_THEN_APPLY : LACT_SEG_APPLY_THEN_UPDATE;
+    for (int64_t s0 = 0; s0 < desc->n_kv; s0 += desc->chunk)
+      out->push_back(BSeg{mode, s0, std::min(desc->n_kv, s0 + desc->chunk), (*nupd)++});
+    if (desc->n_q > desc->n_kv) {
+      out->push_back(BSeg{LACT_SEG_APPLY_ONLY, desc->n_kv, desc->n_q, *nupd});
+      *longest_apply = desc->n_q - desc->n_kv;
+    }
+    return LACT_OK;
+  }
+  int rc = check_segments(desc, segs, nseg);
+  if (rc) return rc;
+  std::vector<std::pair<int64_t, int64_t>> ur, ar;
+  for (int64_t i = 0; i < nseg; ++i) {
+    const lact_segment& g = segs[i];
+    out->push_back(BSeg{g.mode, g.begin, g.end, *nupd});
+    if (is_update(g.mode)) {
+      ur.emplace_back(g.begin, g.end);
+      ++*nupd;
+    }
+    if (is_apply(g.mode)) ar.emplace_back(g.begin, g.end);
+    if (g.mode == LACT_SEG_APPLY_ONLY) *longest_apply = std::max(*longest_apply, g.end - g.begin);
+  }
+  for (auto* r : {&ur, &ar}) {
+    std::sort(r->begin(), r->end());
+    for (size_t i = 1; i < r->size(); ++i)
+      if ((*r)[i].first < (*r)[i - 1].second) return LACT_EUNSUPPORTED;
+  }
+  return LACT_OK;
+}
+
+// Zeroes rows [r0, r1) of every instance of a per-token fp32 array of `cols`
+// values per row ([BH][rows][cols]).
+int zero_f32_rows(float* x, int BH, int64_t rows, int cols, int64_t r0, int64_t r1, hipStream_t s) {
+  if (r1 <= r0) return LACT_OK;
+  return timed(LACT_KCLASS_PREP, 0.0, s,
+               [&] { return launch_zero_f32(x, BH, rows * cols, r0 * cols, (r1 - r0) * cols, s); });
+}
+
+// Rows of [0, n) that no range of `r` covers, as [b, e) pairs.
+std::vector<std::pair<int64_t, int64_t>> uncovered(std::vector<std::pair<int64_t, int64_t>> r, int64_t n) {
+  std::sort(r.begin(), r.end());
+  std::vector<std::pair<int64_t, int64_t>> gaps;
+  int64_t at = 0;
+  for (const auto& x : r) {
+    if (x.first > at) gaps.emplace_back(at, x.first);
+    at = std::max(at, x.second);
+  }
+  if (n > at) gaps.emplace_back(at, n);
+  return gaps;
+}
+
 // ---------------------------------------------------------------- backward
 // Reverse of the linear fast weight's chunk loop (§5.4 with the §3.1 chunk
 // gradient and the per-row norm-preserving update of §3.2). The linear
@@ -1408,14 +1479,16 @@ struct BwdLayout {
 
 constexpr int kMomBlocks = 64;   // workgroups per instance of the momentum reverse
 
-int bwd_layout(const lact_desc* dsc, BwdLayout* L, bool mom = false) {
+// nupd: the schedule's updates (negative: lact_forward's chunks); apply_len:
+// its longest apply-only segment (negative: the tail n_q - n_kv).
+int bwd_layout(const lact_desc* dsc, BwdLayout* L, bool mom = false, int64_t nupd = -1, int64_t apply_len = -1) {
   int rc = check_desc(dsc);
   if (rc) return rc;
   if (dsc->fast_weight != LACT_FW_LINEAR) return LACT_EUNSUPPORTED;
   L->p = make_plan(dsc);
   const Plan& p = L->p;
   const double dd = (double)p.d * p.d;
-  L->nch = dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0;
+  L->nch = nupd >= 0 ? nupd : (dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0);
   // per chunk: P, A and W (fp32) and a transposed copy; per key token eta k
   const double need = (double)L->nch * p.BH * dd * (12.0 + p.esz) + (double)p.BH * dsc->n_kv * p.d * p.esz;
   if (need > 4.0e18) return LACT_EUNSUPPORTED;
@@ -1438,7 +1511,7 @@ int bwd_layout(const lact_desc* dsc, BwdLayout* L, bool mom = false) {
   L->off_wt = o;
   o = align_up(o + (size_t)(L->nch + 1) * wio);
   L->off_tail = o;
-  o = align_up(o + (dsc->n_q > dsc->n_kv ? (size_t)p.nsplit * w4 : 0));
+  o = align_up(o + ((apply_len >= 0 ? apply_len : dsc->n_q - dsc->n_kv) > 0 ? (size_t)p.nsplit * w4 : 0));
   L->off_ub = o;
   o = align_up(o + wio);
   L->off_ut = o;
@@ -1510,10 +1583,17 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
                         const float* W0, const void* dout, const float* dWf, void* dq, void* dk, void* dv,
                         float* deta, float* dW0, void* workspace, size_t workspace_bytes, void* stream,
                         const float* beta = nullptr, const float* M0 = nullptr, const float* dMf = nullptr,
-                        float* dbeta = nullptr, float* dM0 = nullptr) {
+                        float* dbeta = nullptr, float* dM0 = nullptr, const lact_segment* sched = nullptr,
+                        int64_t nsched = -1) {
   const bool mom = M0 != nullptr;
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  std::vector<BSeg> segs;
+  int64_t nupd = 0, longest_apply = 0;
+  rc = backward_segments(desc, sched, nsched, &segs, &nupd, &longest_apply);
+  if (rc) return rc;
   BwdLayout L;
-  int rc = bwd_layout(desc, &L, mom);
+  rc = bwd_layout(desc, &L, mom, nsched >= 0 ? nupd : -1, nsched >= 0 ? longest_apply : -1);
   if (rc) return rc;
   const bool any_kv = desc->n_kv > 0, any_q = desc->n_q > 0;
   if (mom) {
@@ -1554,28 +1634,67 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
   };
   float* bbar_all = mom ? reinterpret_cast<float*>(ws + L.off_bbar_all) : nullptr;
   float* mu = mom ? reinterpret_cast<float*>(ws + L.off_mu) : nullptr;
-  if (mom && L.nch > 0) {   // every chunk's mean of beta, [BH][nch]
-    BetaArgs ba{};
-    ba.beta = beta;
-    ba.n_kv = n_kv;
-    ba.chunk = C;
-    ba.t0 = 0;
-    ba.end = n_kv;
-    ba.nchunks = (int)L.nch;
-    ba.BH = p.BH;
-    ba.bbar = bbar_all;
-    ba.stride = (int)L.nch;
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_beta_mean(ba, s); });
-    if (rc) return rc;
+  if (mom && L.nch > 0) {   // every update's mean of beta, [BH][nch]
+    for (const BSeg& g : segs) {   // lact_forward's chunks: all in one launch
+      if (!is_update(g.mode) || (nsched < 0 && g.before > 0)) continue;
+      BetaArgs ba{};
+      ba.beta = beta;
+      ba.n_kv = n_kv;
+      ba.chunk = nsched < 0 ? C : g.e - g.b;
+      ba.t0 = nsched < 0 ? 0 : g.b;
+      ba.end = nsched < 0 ? n_kv : g.e;
+      ba.nchunks = nsched < 0 ? (int)L.nch : 1;
+      ba.BH = p.BH;
+      ba.bbar = bbar_all + (nsched < 0 ? 0 : g.before);
+      ba.stride = (int)L.nch;
+      rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_beta_mean(ba, s); });
+      if (rc) return rc;
+    }
   }
-  // eta k of every key token, then P_c and A_c of every chunk
+  if (nsched >= 0) {   // rows of the cotangents that no apply or no update reaches
+    std::vector<std::pair<int64_t, int64_t>> ur, ar;
+    for (const BSeg& g : segs) {
+      if (is_update(g.mode)) ur.emplace_back(g.b, g.e);
+      if (is_apply(g.mode)) ar.emplace_back(g.b, g.e);
+    }
+    for (const auto& gap : uncovered(ar, n_q)) {
+      rc = timed(LACT_KCLASS_PREP, 0.0, s,
+                 [&] { return launch_zero_rows(dq, p.BH, d * esz, n_q, gap.first, gap.second, s); });
+      if (rc) return rc;
+    }
+    for (const auto& gap : uncovered(ur, n_kv)) {
+      rc = timed(LACT_KCLASS_PREP, 0.0, s,
+                 [&] { return launch_zero_rows(dk, p.BH, d * esz, n_kv, gap.first, gap.second, s); });
+      if (!rc) rc = timed(LACT_KCLASS_PREP, 0.0, s,
+                          [&] { return launch_zero_rows(dv, p.BH, d * esz, n_kv, gap.first, gap.second, s); });
+      if (!rc) rc = zero_f32_rows(deta, p.BH, n_kv, 1, gap.first, gap.second, s);
+      if (!rc && mom) rc = zero_f32_rows(dbeta, p.BH, n_kv, 1, gap.first, gap.second, s);
+      if (rc) return rc;
+    }
+  }
+  // eta k of every key token, then P_c and A_c of every chunk (of every
+  // update segment, and the apply of the same tokens when it has one)
   if (any_kv) {
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
       return launch_scale_rows(kb, eta, ek, p.BH, n_kv, p.d, n_kv * d, n_kv, n_kv * d, p.bf16, s);
     });
     if (rc) return rc;
   }
-  if (L.batched) {
+  if (nsched >= 0) {
+    for (const BSeg& g : segs) {
+      if (!is_update(g.mode)) continue;
+      const int64_t t0 = g.b, n = g.e - g.b, one = cdiv(n, 32) * 32, u = g.before;
+      BwdArgs b{};
+      lin_grad_seg(b.seg[0], p, op(vb + t0 * d * esz, d, n_kv * d), op(ek + t0 * d * esz, d, n_kv * d),
+                   Pall + u * psplit, n, one);
+      const bool app = is_apply(g.mode);
+      if (app)
+        lin_grad_seg(b.seg[1], p, op(ob + t0 * d * esz, d, n_q * d), op(qb + t0 * d * esz, d, n_q * d),
+                     Aall + u * psplit, n, one);
+      rc = lin_launch(p, s, b, app ? 2 : 1, (app ? 4.0 : 2.0) * BH * n * dd);
+      if (rc) return rc;
+    }
+  } else if (L.batched) {
     for (int64_t c0 = 0; c0 < L.nch; c0 += L.group) {
       const int64_t t0 = c0 * C, t1 = std::min(n_kv, (c0 + L.group) * C), n = t1 - t0;
       BwdArgs b{};
@@ -1654,43 +1773,46 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     }
   }
   float* G = dW0;
-  // tail [n_kv, n_q): applied with the final weight; its dO^T Q joins the
-  // cotangent of that weight (dW_final, or zero)
+  // The cotangent of the current weight lives in G; `first` while it still
+  // has to start from dW_final (or zero).
   bool first = true;
-  if (any_q && n_q > n_kv) {
-    float* tpart = reinterpret_cast<float*>(ws + L.off_tail);
-    for (int64_t a = n_kv; a < n_q; a += L.tail_len) {
-      const int64_t n = std::min(L.tail_len, n_q - a);
-      BwdArgs b{};
-      lin_grad_seg(b.seg[0], p, op(ob + a * d * esz, d, n_q * d), op(qb + a * d * esz, d, n_q * d), tpart, n,
-                   L.tail_split);
-      lin_out_seg(b.seg[1], p, op(ob + a * d * esz, d, n_q * d), op(wt(L.nch), d, dd), (uint8_t*)dq + a * d * esz,
-                  n_q * d, n);
-      rc = lin_launch(p, s, b, 2, 4.0 * BH * n * dd);
-      if (rc) return rc;
-      const int mode = first ? (dWf ? 1 : 0) : 2;
-      const PartSet ps{tpart, b.seg[0].nsplit, psplit, dd};
-      rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
+  auto add_g = [&](PartSet ps) -> int {
+    const int mode = first ? (dWf ? 1 : 0) : 2;
+    first = false;
+    return timed(LACT_KCLASS_UPDATE, 0.0, s,
                  [&] { return launch_accum(G, dd, dWf, dd, mode, ps, PartSet{}, p.BH, dd, s); });
-      if (rc) return rc;
-      first = false;
-    }
-  }
-  if (first) {
-    rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
-               [&] { return launch_accum(G, dd, dWf, dd, dWf ? 1 : 0, PartSet{}, PartSet{}, p.BH, dd, s); });
-    if (rc) return rc;
-  }
+  };
   if (mom) {   // the final state's cotangent, or zero
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s,
                [&] { return launch_accum(dM0, dd, dMf, dd, dMf ? 1 : 0, PartSet{}, PartSet{}, p.BH, dd, s); });
     if (rc) return rc;
   }
-  const bool then_apply = desc->order == LACT_UPDATE_THEN_APPLY;
   uint8_t* ub = ws + L.off_ub;
   uint8_t* ut = ws + L.off_ut;
-  for (int64_t ci = L.nch - 1; ci >= 0; --ci) {
-    const int64_t s0 = ci * C, n = std::min(n_kv, s0 + C) - s0;
+  for (auto it = segs.rbegin(); it != segs.rend(); ++it) {
+    const BSeg& g = *it;
+    if (g.mode == LACT_SEG_APPLY_ONLY) {   // applied with the weight of its time, in pieces
+      float* tpart = reinterpret_cast<float*>(ws + L.off_tail);
+      for (int64_t a = g.b; a < g.e; a += L.tail_len) {
+        const int64_t n = std::min(L.tail_len, g.e - a);
+        BwdArgs b{};
+        lin_grad_seg(b.seg[0], p, op(ob + a * d * esz, d, n_q * d), op(qb + a * d * esz, d, n_q * d), tpart, n,
+                     L.tail_split);
+        lin_out_seg(b.seg[1], p, op(ob + a * d * esz, d, n_q * d), op(wt(g.before), d, dd),
+                    (uint8_t*)dq + a * d * esz, n_q * d, n);
+        rc = lin_launch(p, s, b, 2, 4.0 * BH * n * dd);
+        if (!rc) rc = add_g(PartSet{tpart, b.seg[0].nsplit, psplit, dd});
+        if (rc) return rc;
+      }
+      continue;
+    }
+    if (first) {
+      rc = add_g(PartSet{});
+      if (rc) return rc;
+    }
+    const int64_t ci = g.before, s0 = g.b, n = g.e - g.b;
+    const bool then_apply = g.mode == LACT_SEG_UPDATE_THEN_APPLY;
+    const bool applies = g.mode != LACT_SEG_UPDATE_ONLY;
     const NsBwd nb{p, L.ns, ws, s, desc->ns_steps, {p.d, 0, 0}, {p.d, 0, 0}, ci};
     const float* slab[3] = {mom ? mtraj(ci + 1) : nullptr, nullptr, nullptr};
     if (p.muon) {   // the step is Muon(g), or Muon(M_{c+1}): its kept iterates, else replay the iteration
@@ -1704,8 +1826,8 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     va.P = p.muon ? PartSet{nb.pst(), 1, psplit, dd}
                   : (mom ? PartSet{mtraj(ci + 1), 1, 0, dd, -1.0f} : PartSet{Pall + ci * psplit, 1, psplit, dd});
     const PartSet ac{Aall + ci * psplit, 1, psplit, dd};
-    if (then_apply) va.pre[0] = ac;   // applied with the weights leaving the chunk
-    else va.post = ac;
+    if (applies && then_apply) va.pre[0] = ac;   // applied with the weights leaving the update
+    else if (applies) va.post = ac;
     va.G = G;
     va.g_inst = dd;
     va.Ub = ub;
@@ -1762,7 +1884,7 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     // dq = dO W with the weight the chunk was applied with
     lin_out_seg(b.seg[2], p, op(ob + s0 * d * esz, d, n_q * d), op(wt(then_apply ? ci + 1 : ci), d, dd),
                 (uint8_t*)dq + s0 * d * esz, n_q * d, n);
-    rc = lin_launch(p, s, b, 3, 6.0 * BH * n * dd);
+    rc = lin_launch(p, s, b, applies ? 3 : 2, (applies ? 6.0 : 4.0) * BH * n * dd);
     if (rc) return rc;
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] {
       return launch_lin_tokens(vb + s0 * d * esz, eta + s0, (uint8_t*)dv + s0 * d * esz, deta + s0, p.BH, n, p.d,
@@ -1770,6 +1892,7 @@ int run_backward_linear(const lact_desc* desc, const void* q, const void* k, con
     });
     if (rc) return rc;
   }
+  if (first) return add_g(PartSet{});   // no update: dW_final (or zero)
   return LACT_OK;
 }
 
@@ -1855,77 +1978,6 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false, int64_
   }
   L->total = o;
   return LACT_OK;
-}
-
-// One segment of the backward's schedule: a LACT_SEG_* mode over tokens
-// [b, e), the index of its update among the schedule's updates (upd) and
-// the number of updates before it (the weights an apply before its update,
-// or an apply-only segment, uses: W_before).
-struct BSeg {
-  int mode;
-  int64_t b, e;
-  int64_t before;
-};
-
-// The uniform schedule of lact_forward (chunks of desc->chunk, then the
-// apply-only tail), or the caller's segments checked for the backward: the
-// update ranges must not overlap each other, nor the apply ranges (the
-// reverse writes the cotangents of a token's rows once).
-int backward_segments(const lact_desc* desc, const lact_segment* segs, int64_t nseg, std::vector<BSeg>* out,
-                      int64_t* nupd, int64_t* longest_apply) {
-  out->clear();
-  *nupd = 0;
-  *longest_apply = 0;
-  if (nseg < 0) {
-    const int mode = desc->order == LACT_UPDATE_THEN_APPLY ? LACT_SEG_UPDATE_THEN_APPLY : LACT_SEG_APPLY_THEN_UPDATE;
-    for (int64_t s0 = 0; s0 < desc->n_kv; s0 += desc->chunk)
-      out->push_back(BSeg{mode, s0, std::min(desc->n_kv, s0 + desc->chunk), (*nupd)++});
-    if (desc->n_q > desc->n_kv) {
-      out->push_back(BSeg{LACT_SEG_APPLY_ONLY, desc->n_kv, desc->n_q, *nupd});
-      *longest_apply = desc->n_q - desc->n_kv;
-    }
-    return LACT_OK;
-  }
-  int rc = check_segments(desc, segs, nseg);
-  if (rc) return rc;
-  std::vector<std::pair<int64_t, int64_t>> ur, ar;
-  for (int64_t i = 0; i < nseg; ++i) {
-    const lact_segment& g = segs[i];
-    out->push_back(BSeg{g.mode, g.begin, g.end, *nupd});
-    if (is_update(g.mode)) {
-      ur.emplace_back(g.begin, g.end);
-      ++*nupd;
-    }
-    if (is_apply(g.mode)) ar.emplace_back(g.begin, g.end);
-    if (g.mode == LACT_SEG_APPLY_ONLY) *longest_apply = std::max(*longest_apply, g.end - g.begin);
-  }
-  for (auto* r : {&ur, &ar}) {
-    std::sort(r->begin(), r->end());
-    for (size_t i = 1; i < r->size(); ++i)
-      if ((*r)[i].first < (*r)[i - 1].second) return LACT_EUNSUPPORTED;
-  }
-  return LACT_OK;
-}
-
-// Zeroes rows [r0, r1) of every instance of a per-token fp32 array of `cols`
-// values per row ([BH][rows][cols]).
-int zero_f32_rows(float* x, int BH, int64_t rows, int cols, int64_t r0, int64_t r1, hipStream_t s) {
-  if (r1 <= r0) return LACT_OK;
-  return timed(LACT_KCLASS_PREP, 0.0, s,
-               [&] { return launch_zero_f32(x, BH, rows * cols, r0 * cols, (r1 - r0) * cols, s); });
-}
-
-// Rows of [0, n) that no range of `r` covers, as [b, e) pairs.
-std::vector<std::pair<int64_t, int64_t>> uncovered(std::vector<std::pair<int64_t, int64_t>> r, int64_t n) {
-  std::sort(r.begin(), r.end());
-  std::vector<std::pair<int64_t, int64_t>> gaps;
-  int64_t at = 0;
-  for (const auto& x : r) {
-    if (x.first > at) gaps.emplace_back(at, x.first);
-    at = std::max(at, x.second);
-  }
-  if (n > at) gaps.emplace_back(at, n);
-  return gaps;
 }
 
 // With beta != nullptr: the momentum optimizer (M0 the initial state, dMf
@@ -2519,12 +2571,20 @@ size_t lact_backward_schedule_workspace_bytes(const lact_desc* desc, const lact_
   int rc = check_desc(desc);
   std::vector<BSeg> bs;
   int64_t nupd = 0, longest = 0;
-  if (!rc && desc->fast_weight != LACT_FW_SWIGLU) rc = LACT_EUNSUPPORTED;
+  if (!rc && nseg < 0) rc = LACT_EINVAL;
   if (!rc) rc = backward_segments(desc, segs, nseg, &bs, &nupd, &longest);
-  SwBwdLayout L;
-  if (!rc) rc = sw_bwd_layout(desc, &L, momentum != 0, nupd, longest);
+  size_t total = 0;
+  if (!rc && desc->fast_weight == LACT_FW_LINEAR) {
+    BwdLayout L;
+    rc = bwd_layout(desc, &L, momentum != 0, nupd, longest);
+    total = L.total;
+  } else if (!rc) {
+    SwBwdLayout L;
+    rc = sw_bwd_layout(desc, &L, momentum != 0, nupd, longest);
+    total = L.total;
+  }
   if (err) *err = rc;
-  return rc ? 0 : L.total;
+  return rc ? 0 : total;
 }
 
 int lact_backward_schedule(const lact_desc* desc, const lact_segment* segs, int64_t nseg, const void* q,
@@ -2537,15 +2597,18 @@ int lact_backward_schedule(const lact_desc* desc, const lact_segment* segs, int6
                            void* stream) {
   const int rc = check_desc(desc);
   if (rc) return rc;
-  if (desc->fast_weight != LACT_FW_SWIGLU) return LACT_EUNSUPPORTED;
   if (nseg < 0 || (nseg > 0 && !segs)) return LACT_EINVAL;
+  const bool mom = M1 != nullptr;
+  if (desc->fast_weight == LACT_FW_LINEAR)
+    return run_backward_linear(desc, q, k, v, eta, W1, dout, dW1_final, dq, dk, dv, deta, dW1, workspace,
+                               workspace_bytes, stream, mom ? beta : nullptr, M1, mom ? dM1_final : nullptr,
+                               mom ? dbeta : nullptr, mom ? dM1 : nullptr, segs, nseg);
   const float* W0[3] = {W1, W2, W3};
   const float* dWf[3] = {dW1_final, dW2_final, dW3_final};
   float* const dW[3] = {dW1, dW2, dW3};
   const float* M0[3] = {M1, M2, M3};
   const float* dMf[3] = {dM1_final, dM2_final, dM3_final};
   float* const dMo[3] = {dM1, dM2, dM3};
-  const bool mom = M1 != nullptr;
   return run_backward_swiglu(desc, q, k, v, eta, W0, dout, dWf, dq, dk, dv, deta, dW, workspace, workspace_bytes,
                              stream, mom ? beta : nullptr, mom ? M0 : nullptr, mom ? dMf : nullptr,
                              mom ? dbeta : nullptr, mom ? dMo : nullptr, segs, nseg);

@@ -423,8 +423,21 @@ def test_schedule_backward_errors_before_any_hip_call():
     # overlapping applies, or overlapping updates: not differentiated
     assert _bwd_sched(d, [(3, 0, 100), (3, 50, 150)]) == -4
     assert _bwd_sched(d, [(2, 0, 100), (2, 50, 150)]) == -4
-    # the linear fast weight has no schedule backward
-    assert _bwd_sched(make_desc(**dict(GOOD, h=64, fast_weight=1)), segs) == -4
+    # the linear fast weight: a workspace of its own size, the same checks
+    dl = make_desc(**dict(GOOD, h=64, fast_weight=1))
+    nl = P.lib().lact_backward_schedule_workspace_bytes(ctypes.byref(dl), arr, len(segs), 0, ctypes.byref(err))
+    assert err.value == 0 and nl > 0
+    nlm = P.lib().lact_backward_schedule_workspace_bytes(ctypes.byref(dl), arr, len(segs), 1, ctypes.byref(err))
+    assert err.value == 0 and nlm > nl
+    assert _bwd_sched(dl, segs, nbytes=nl - 1) == -3
+    assert _bwd_sched(dl, segs, mom=True, nbytes=nlm - 1) == -3
+    assert _bwd_sched(dl, segs, mom=True, dbeta=0) == -1
+    assert _bwd_sched(dl, segs, mom=True, e1=0) == -1    # the state's cotangent
+    assert _bwd_sched(dl, segs, dk=0) == -1
+    assert _bwd_sched(dl, [(2, 0, 100), (2, 50, 150)]) == -4
+    assert _bwd_sched(dl, [(2, 0, 300)]) == -1
+    assert P.lib().lact_backward_schedule_workspace_bytes(ctypes.byref(dl), arr, -1, 0, ctypes.byref(err)) == 0
+    assert err.value == -1
     # an empty schedule reaches the workspace check
     assert _bwd_sched(d, [], ws=0) == -3
 

@@ -2121,6 +2121,167 @@ def test_schedule_backward_of_uniform_chunks_is_lact_backward_bitwise():
         assert np.array_equal(u, w), name
 
 
+
+# The linear fast weight over a general schedule: the forward and its reverse
+# against the oracle's (pinned to torch autograd of a linear schedule loop and
+# to the linear chunk loop's forward and backward for uniform chunks).
+
+
+def run_gpu_lin_sched(cfg, x, schedule, momentum=False):
+    print(f"[gpu] linear schedule {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} n_kv={cfg.n_kv} n_q={cfg.n_q} "
+          f"segments={len(schedule)} io={cfg.io} muon={cfg.use_muon} momentum={momentum}", flush=True)
+    n = len(x["q"])
+    sh = lambda a: a.reshape(cfg.B, cfg.H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    W = to_dev(sh(x["W1"]), cfg, torch.float32)
+    kw = {"beta": to_dev(sh(x["beta"]), cfg, torch.float32)} if momentum else {}
+    r = P.forward_schedule(q, k, v, eta, W, None, None, schedule, use_muon=bool(cfg.use_muon),
+                           ns_steps=cfg.ns_steps, chunk=cfg.chunk, **kw)
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    return (f(r[0]), f(W), f(r[1])) if momentum else (f(r), f(W))
+
+
+def run_gpu_lin_sched_bwd(cfg, x, ct, schedule, st=None, with_final=True):
+    print(f"[gpu] linear schedule backward {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} n_kv={cfg.n_kv} "
+          f"n_q={cfg.n_q} segments={len(schedule)} io={cfg.io} muon={cfg.use_muon} momentum={st is not None}",
+          flush=True)
+    n = len(x["q"])
+    sh = lambda a: a.reshape(cfg.B, cfg.H, *a.shape[1:])
+    q, k, v = (to_dev(sh(x[a]), cfg) for a in ("q", "k", "v"))
+    eta = to_dev(sh(x["eta"]), cfg, torch.float32)
+    W = to_dev(sh(x["W1"]), cfg, torch.float32)
+    dWf = to_dev(sh(ct["dW"]), cfg, torch.float32) if with_final else None
+    kw = {}
+    if st is not None:
+        kw = dict(beta=to_dev(sh(x["beta"]), cfg, torch.float32), M=to_dev(sh(st["M"]), cfg, torch.float32),
+                  dM_final=to_dev(sh(ct["dM"]), cfg, torch.float32) if with_final else None)
+    keep = [W] + ([kw["M"]] if st is not None else [])
+    before = [t.clone() for t in keep]
+    do = to_dev(sh(ct["do"]), cfg)
+    r = P.backward_schedule(q, k, v, eta, W, None, None, do, schedule, dW_final=dWf, use_muon=bool(cfg.use_muon),
+                            ns_steps=cfg.ns_steps, chunk=cfg.chunk, **kw)
+    torch.cuda.synchronize()
+    for a, b in zip(keep, before):
+        assert torch.equal(a, b)   # the initial weight and state are read only
+    f = lambda t: t.float().cpu().numpy().reshape(n, *t.shape[2:])
+    return tuple(f(t) for t in r)
+
+
+def check_lin_sched_bwd(cfg, x, ct, schedule, got, st=None, with_final=True):
+    def ref_fn(xx):
+        kw = {}
+        if st is not None:
+            kw = dict(beta=xx["beta"], M=st["M"], dM_final=ct["dM"] if with_final else None)
+        return O.lact_backward_schedule(xx["q"], xx["k"], xx["v"], xx["eta"], xx["W1"], None, None, ct["do"],
+                                        schedule, dW_final=ct["dW"] if with_final else None,
+                                        use_muon=bool(cfg.use_muon), ns_steps=cfg.ns_steps, **kw)
+    ref = ref_fn(x)
+    names = ["dq", "dk", "dv", "deta"] + (["dbeta"] if st is not None else []) + ["dW"] + \
+        (["dM"] if st is not None else [])
+    errs, blocks = {}, {}
+    for name, g, r in zip(names, got, ref):
+        if name in ("dq", "dk", "dv"):   # rows without a cotangent are exact zeros on both sides
+            zero = ~np.any(r != 0, axis=-1)
+            assert not np.any(g[zero]), name
+        errs[name] = rel(g, r)
+        if name in ("deta", "dbeta"):
+            blocks[name] = worst_window(g, r, O_BLOCK)
+        else:
+            blocks[name] = worst_block(g, r, W_BLOCK if name in ("dW", "dM") else O_BLOCK)
+    # deta_t = k_t . Z_t (Z = dk / eta) can cancel: per token its error is
+    # bounded by |k_t| |Z_t| times the operands' rounding (tokens an update uses)
+    zn = np.linalg.norm(ref[1], axis=-1) / x["eta"].astype(np.float64)
+    kn = np.linalg.norm(x["k"].astype(np.float64), axis=-1)
+    used = zn > 0
+    if np.any(used):
+        errs["deta/(|k||Z|)"] = float(np.max(np.abs(got[3] - ref[3])[used] / (kn * zn)[used]))
+    if not cfg.use_muon:
+        assert_errs(errs, TOL[cfg.io], blocks)
+        return
+    whole, block = muon_bars(ref_fn, x, ref, TOL[cfg.io], cfg.io)
+    wb, bb = dict(zip(names, whole)), dict(zip(names, block))
+    wb["deta/(|k||Z|)"] = max(TOL[cfg.io], wb["deta"])
+    if st is not None:
+        wb["dbeta"], bb["dbeta"] = float("inf"), float("inf")
+    assert_bars(errs, blocks, wb, bb)
+
+
+def lin_sched_case(base, seed, momentum=False, **kw):
+    cfg = CONFIGS[base].with_(linear=1, momentum=int(momentum), **kw)
+    x, ct = make_inputs(cfg, seed), make_cotangents(cfg, seed)
+    return cfg, x, ct, make_momentum_state(cfg, seed) if momentum else None
+
+
+@pytest.mark.parametrize("momentum", [False, True])
+def test_linear_schedule_forward_mixed(momentum):
+    C = 128
+    cfg, x, _, _ = lin_sched_case("lm32k", 120, momentum, name="lin_sched_fwd", B=1, H=2, d=128, h=128,
+                                  n_kv=6 * C, n_q=6 * C + 40, chunk=C)
+    sched = mixed_schedule(C)
+    got = run_gpu_lin_sched(cfg, x, sched, momentum)
+    ref = O.lact_forward_schedule(x["q"], x["k"], x["v"], x["eta"], x["W1"], None, None, sched,
+                                  beta=x["beta"] if momentum else None)
+    w0 = x["W1"].astype(np.float64)
+    errs = {"o": rel(got[0], ref[0]), "dW": rel(got[1] - w0, ref[1] - w0)}
+    blocks = {"o": worst_block(got[0], ref[0], O_BLOCK), "dW": worst_block(got[1] - w0, ref[1] - w0, W_BLOCK)}
+    if momentum:
+        errs["M"] = rel(got[2], ref[2])
+    assert_errs(errs, TOL[cfg.io], blocks)
+
+
+def test_linear_schedule_backward_mixed_bf16():
+    C = 128
+    cfg, x, ct, _ = lin_sched_case("lm32k", 121, name="lin_sched_bwd", B=1, H=2, d=256, h=256, n_kv=6 * C,
+                                   n_q=6 * C + 40, chunk=C)
+    sched = mixed_schedule(C)
+    check_lin_sched_bwd(cfg, x, ct, sched, run_gpu_lin_sched_bwd(cfg, x, ct, sched))
+
+
+def test_linear_schedule_backward_mixed_momentum_fp32():
+    C = 64
+    cfg, x, ct, st = lin_sched_case("tiny_fp32", 122, True, name="lin_sched_bwd_mom_fp32", B=2, H=1, d=40, h=40,
+                                    n_kv=6 * C, n_q=6 * C + 40, chunk=C)
+    sched = mixed_schedule(C)
+    check_lin_sched_bwd(cfg, x, ct, sched, run_gpu_lin_sched_bwd(cfg, x, ct, sched, st), st)
+
+
+def test_linear_schedule_backward_teacher_forcing_muon_bf16():
+    # the strided mask of teacher-forced video (noisy chunks applied only,
+    # clean ones update then apply): 2 updates, Muon
+    cfg, x, ct, _ = lin_sched_case("lm32k", 123, name="lin_sched_bwd_muon", B=1, H=2, d=128, h=128,
+                                   n_kv=5 * 256, n_q=5 * 256, chunk=256, use_muon=1)
+    sched = [("apply_only", 0, 256), ("update_then_apply", 256, 512), ("apply_only", 512, 768),
+             ("update_then_apply", 768, 1024), ("apply_only", 1024, 1280)]
+    check_lin_sched_bwd(cfg, x, ct, sched, run_gpu_lin_sched_bwd(cfg, x, ct, sched))
+
+
+def test_linear_schedule_backward_without_updates_momentum():
+    cfg, x, ct, st = lin_sched_case("lm32k", 124, True, name="lin_sched_bwd_apply_only", B=1, H=2, d=128, h=128,
+                                    n_kv=256, n_q=600, chunk=128)
+    sched = [("apply_only", 0, 300), ("apply_only", 340, 600)]
+    got = run_gpu_lin_sched_bwd(cfg, x, ct, sched, st)
+    check_lin_sched_bwd(cfg, x, ct, sched, got, st)
+    assert not np.any(got[1]) and not np.any(got[3]) and not np.any(got[4])
+    assert np.array_equal(got[6], ct["dM"])
+
+
+@pytest.mark.parametrize("momentum", [False, True])
+def test_linear_schedule_backward_of_uniform_chunks_is_the_chunk_loop_bitwise(momentum):
+    cfg, x, ct, st = lin_sched_case("lm32k", 125, momentum, name="lin_sched_bwd_uniform", B=1, H=2, d=128, h=128,
+                                    n_kv=600, n_q=640, chunk=256, order=1)
+    sched = [("update_then_apply", s, min(600, s + 256)) for s in range(0, 600, 256)] + [("apply_only", 600, 640)]
+    a = run_gpu_lin_sched_bwd(cfg, x, ct, sched, st)
+    if momentum:
+        b = run_gpu_mom_bwd(cfg, x, ct, st)
+        b = b[:5] + b[5] + b[6]
+    else:
+        b = run_gpu_linear_bwd(cfg, x, ct)
+    for i, (u, w) in enumerate(zip(a, b)):
+        assert np.array_equal(u, w), i
+
+
 # ----------------------------------------------------------------------------- envelope limits
 # The largest head and hidden dims (4096), very many instances, the most
 # Newton-Schulz steps, and a chunk longer than the sequence.

@@ -1550,6 +1550,118 @@ def test_schedule_backward_batched_driver_stacks_instances():
             assert np.array_equal(a[pos], b)
 
 
+
+def _torch_linear_schedule_layer(q, k, v, eta, W, schedule, beta=None, M=None, muon=False):
+    """The schedule's segments with the linear fast weight in torch: an apply
+    overwrites its rows of o with W q, an update takes the gradient of the
+    chunk loss -sum eta (W k) . v by autograd (kept in the graph), then the
+    momentum recurrence, Muon and the row-norm-preserving update."""
+    o = torch.zeros(q.shape, dtype=q.dtype)
+    parts = {"update_then_apply": ("update", "apply"), "apply_then_update": ("apply", "update"),
+             "update_only": ("update",), "apply_only": ("apply",)}
+    for mode, b, e in schedule:
+        for kind in parts[mode]:
+            if kind == "apply":
+                rows = torch.zeros(q.shape[0], 1, dtype=q.dtype)
+                rows[b:e] = 1.0
+                full = torch.zeros(q.shape, dtype=q.dtype)
+                full = torch.cat([full[:b], F.linear(q[b:e], W), full[e:]])
+                o = o * (1 - rows) + full
+                continue
+            loss = -(eta[b:e] * (F.linear(k[b:e], W) * v[b:e]).sum(-1)).sum()
+            g = torch.autograd.grad(loss, W, create_graph=True)[0]
+            if beta is not None:
+                M = beta[b:e].mean() * M + g
+                g = M
+            U = W - (_torch_newton_schulz(g) if muon else g)
+            W = U * (torch.linalg.vector_norm(W, dim=1, keepdim=True) / torch.linalg.vector_norm(U, dim=1, keepdim=True))
+    return o, W, M
+
+
+@pytest.mark.parametrize("mom,muon", [(False, False), (True, False), (False, True), (True, True)])
+def test_linear_schedule_backward_matches_autograd(mom, muon):
+    # the schedule of the SwiGLU test: every mode, rows applied twice, key
+    # rows updated twice, an unapplied row range and unused key rows
+    rng = _rng(170 + 2 * mom + muon)
+    d, n_kv, n_q = 5, 20, 26
+    schedule = [("apply_then_update", 0, 5), ("apply_only", 5, 9), ("update_then_apply", 5, 9),
+                ("update_only", 9, 14), ("apply_then_update", 3, 8), ("apply_only", 14, 20), ("apply_only", 22, 26)]
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random(n_kv)
+    beta = rng.random(n_kv) if mom else None
+    W0 = rng.standard_normal((d, d)) / np.sqrt(d)
+    M0 = 0.05 * rng.standard_normal((d, d)) if mom else None
+    do = rng.standard_normal((n_q, d))
+    dWf = rng.standard_normal((d, d))
+    dMf = rng.standard_normal((d, d)) if mom else None
+    t = lambda a: torch.tensor(a, requires_grad=True)
+    qt, kt, vt, et, Wt = t(q), t(k), t(v), t(eta), t(W0)
+    bt = t(beta) if mom else None
+    Mt = t(M0) if mom else None
+    o, Wfin, Mfin = _torch_linear_schedule_layer(qt, kt, vt, et, Wt, schedule, bt, Mt, muon)
+    loss = (o * torch.tensor(do)).sum() + (Wfin * torch.tensor(dWf)).sum()
+    if mom:
+        loss = loss + (Mfin * torch.tensor(dMf)).sum()
+    loss.backward()
+    r = O.lact_backward_schedule_instance(q, k, v, eta, W0, None, None, do, schedule, dWf, use_muon=muon,
+                                          beta=beta, M=M0, dM_final=dMf)
+    refs = (qt, kt, vt, et) + ((bt, Wt, Mt) if mom else (Wt,))
+    for name, g, ref in zip(("dq", "dk", "dv", "deta") + (("dbeta", "dW", "dM") if mom else ("dW",)), r, refs):
+        assert np.allclose(g, ref.grad.numpy(), rtol=1e-8, atol=1e-10), name
+    assert not np.any(r[0][20:22]) and not np.any(r[1][14:]) and not np.any(r[3][14:])
+    # the forward the backward replays is the oracle's own linear forward
+    fw = O.lact_forward_schedule_instance(q, k, v, eta, W0, None, None, schedule, use_muon=muon, beta=beta, M=M0)
+    assert np.allclose(o.detach().numpy(), fw[0], rtol=1e-12, atol=1e-13)
+    assert np.allclose(Wfin.detach().numpy(), fw[1], rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("order,muon", [(0, False), (1, False), (1, True)])
+def test_linear_schedule_of_uniform_chunks_is_the_linear_chunk_loop(order, muon):
+    rng = _rng(180 + order + 2 * muon)
+    d, n_kv, n_q, C = 4, 13, 17, 5
+    mode = "apply_then_update" if order == 0 else "update_then_apply"
+    schedule = [(mode, s, min(n_kv, s + C)) for s in range(0, n_kv, C)] + [("apply_only", n_kv, n_q)]
+    q, k, v = _tokens(rng, n_q, d), _tokens(rng, n_kv, d), _tokens(rng, n_kv, d)
+    eta = 0.1 + 0.4 * rng.random(n_kv)
+    W0 = rng.standard_normal((d, d)) / 2
+    do = rng.standard_normal((n_q, d))
+    dWf = rng.standard_normal((d, d))
+    fw = O.lact_forward_schedule_instance(q, k, v, eta, W0, None, None, schedule, use_muon=muon)
+    ref = O.lact_forward_linear_instance(q, k, v, eta, W0, C, order, use_muon=muon)
+    for a, b in zip(fw, ref):
+        assert np.allclose(a, b, rtol=1e-13, atol=1e-15)
+    got = O.lact_backward_schedule_instance(q, k, v, eta, W0, None, None, do, schedule, dWf, use_muon=muon)
+    ref = O.lact_backward_linear_instance(q, k, v, eta, W0, do, C, order, dWf, use_muon=muon)
+    for a, b in zip(got, ref):
+        assert np.allclose(a, b, rtol=1e-13, atol=1e-15)
+    beta = rng.random(n_kv)
+    M0 = 0.05 * rng.standard_normal((d, d))
+    dMf = rng.standard_normal((d, d))
+    got = O.lact_backward_schedule_instance(q, k, v, eta, W0, None, None, do, schedule, dWf, use_muon=muon,
+                                            beta=beta, M=M0, dM_final=dMf)
+    ref = O.lact_backward_momentum_instance(q, k, v, eta, beta, W0, M0, do, C, order, dWf, dMf, use_muon=muon)
+    for a, b in zip(got, ref):
+        assert np.allclose(a, b, rtol=1e-13, atol=1e-15)
+
+
+def test_linear_schedule_backward_batched_driver():
+    rng = _rng(185)
+    BH, d, n = 3, 4, 12
+    schedule = [("apply_only", 0, 4), ("update_then_apply", 4, 8), ("update_only", 0, 4)]
+    q, k, v = (np.stack([_tokens(rng, n, d) for _ in range(BH)]) for _ in range(3))
+    eta, beta = 0.1 + 0.3 * rng.random((BH, n)), rng.random((BH, n))
+    W = rng.standard_normal((BH, d, d))
+    M = 0.1 * rng.standard_normal((BH, d, d))
+    do = rng.standard_normal((BH, n, d))
+    got = O.lact_backward_schedule(q, k, v, eta, W, None, None, do, schedule, beta=beta, M=M, instances=[2, 0])
+    assert len(got) == 7
+    for pos, i in enumerate((2, 0)):
+        r = O.lact_backward_schedule_instance(q[i], k[i], v[i], eta[i], W[i], None, None, do[i], schedule,
+                                              beta=beta[i], M=M[i])
+        for a, b in zip(got, r):
+            assert np.array_equal(a[pos], b)
+
+
 # ----------------------------------------------------------------------------- backward of the prologue and output norm
 
 

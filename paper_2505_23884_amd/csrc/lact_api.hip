@@ -2179,19 +2179,27 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
   const int64_t T = L.T;
   const int64_t zi = T * h;   // elements between instances of a [T x h] buffer
   // one launch of up to three OUT segments, out[t][m] = sum_e a[t][e] b[m][e]
-  // over K columns (per segment), rows of out `rows_out` wide
+  // over K columns (per segment), rows of out `rows_out` wide; `pre` holds
+  // gradient segments (grads into a BwdArgs) that run first in the same launch
   struct Out {
     Operand a, b;
     void* out;
     int64_t out_inst;
     int64_t K;
   };
-  auto outs = [&](const Out* o, int nseg, int64_t n, int rows_out) -> int {
+  struct Pending {
+    BwdArgs b{};
+    double fl = 0.0;
+  };
+  auto outs = [&](const Out* o, int nseg, int64_t n, int rows_out, const Pending* pre = nullptr) -> int {
     BwdArgs b{};
     const TileShape t = bwd_tile(BWD_OUT, p.bf16, p.narrow);
     double fl = 0.0;
+    const int np = pre ? pre->b.nseg : 0;
+    for (int i = 0; i < np; ++i) b.seg[i] = pre->b.seg[i];
+    if (pre) fl = pre->fl;
     for (int i = 0; i < nseg; ++i) {
-      BwdSeg& g = b.seg[i];
+      BwdSeg& g = b.seg[np + i];
       g.kind = BWD_OUT;
       g.tiles_m = (int)cdiv(rows_out, t.rows);
       g.tiles_n = (int)cdiv(n, t.cols);
@@ -2205,18 +2213,20 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       g.klen = o[i].K;
       fl += 2.0 * BH * n * rows_out * o[i].K;
     }
-    b.nseg = nseg;
+    b.nseg = np + nseg;
     b.total_blocks = 0;
-    for (int i = 0; i < nseg; ++i) b.total_blocks += b.seg[i].nblocks;
-    b.d = rows_out;
-    b.h = (int)o[0].K;
+    for (int i = 0; i < b.nseg; ++i) b.total_blocks += b.seg[i].nblocks;
+    // the gradient kinds read d and h as the weights' shape; every OUT
+    // segment carries its own contraction length
+    b.d = np ? (int)d : rows_out;
+    b.h = np ? (int)h : (int)o[0].K;
     b.narrow = p.narrow;
     return timed(LACT_KCLASS_BWD, fl, s, [&] { return launch_bwd(b, p.bf16, s); });
   };
   // weight cotangents over rows [0, n): W1 += a1^T b, W3 += a3^T b (GRAD13)
   // and W2 += a2^T b2 (GRAD2), as split partials into `out`
   auto grads = [&](Operand a1, Operand a3, Operand b13, Operand a2, Operand b2, float* out, int64_t n,
-                   int64_t split_len, int* nsplit) -> int {
+                   int64_t split_len, int* nsplit, Pending* into = nullptr) -> int {
     const TileShape g13 = bwd_tile(BWD_GRAD13, p.bf16, p.narrow), g2 = bwd_tile(BWD_GRAD2, p.bf16, p.narrow);
     const int ns = (int)std::max<int64_t>(1, cdiv(n, split_len));
     BwdArgs b{};
@@ -2254,6 +2264,12 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     b.h = p.h;
     b.narrow = p.narrow;
     *nsplit = ns;
+    if (into) {   // joins a later launch (the caller keeps the order of reads and writes)
+      into->b.seg[into->b.nseg++] = x;
+      into->b.seg[into->b.nseg++] = y;
+      into->fl += 6.0 * BH * n * dh;
+      return LACT_OK;
+    }
     return timed(LACT_KCLASS_BWD, 6.0 * BH * n * dh, s, [&] { return launch_bwd(b, p.bf16, s); });
   };
   // operand copies of weights (W1, W2, W3): W1, W3 row-major and W2^T into
@@ -2272,7 +2288,7 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
   // the apply's reverse on query rows [a, a + n) up to its weight cotangents
   // (into apart) with the weights whose copies are in `u`; dq is left to
   // the caller's OUT launch (Pq against the transposed weights)
-  auto apply_back = [&](int64_t a, int64_t n, const size_t* u, int64_t split_len) -> int {
+  auto apply_back = [&](int64_t a, int64_t n, const size_t* u, int64_t split_len, Pending* into = nullptr) -> int {
     const Operand qo = op(qb + a * d * esz, d, n_q * d), doo = op(ob + a * d * esz, d, n_q * d);
     const Out h3[3] = {{qo, op(ws + u[0], d, dh), zb[0], zi, d},
                        {qo, op(ws + u[1], d, dh), zb[1], zi, d},
@@ -2284,7 +2300,7 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     });
     if (r) return r;
     return grads(op(pq, 2 * h, T * 2 * h), op(pq + h * esz, 2 * h, T * 2 * h), qo, doo, op(hq, h, zi), apart, n,
-                 split_len, &a_ns);
+                 split_len, &a_ns, into);
   };
   auto dq_out = [&](int64_t a, const uint8_t* bt, int64_t bt_ld) -> Out {
     return Out{op(pq, 2 * h, T * 2 * h), op(bt, bt_ld, d * bt_ld), (uint8_t*)dq + a * d * esz, n_q * d, 2 * h};
@@ -2321,10 +2337,11 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
       if (rc) return rc;
       for (int64_t a = g.b; a < g.e; a += T) {
         const int64_t na = std::min(T, g.e - a);
-        rc = apply_back(a, na, L.off_a, L.tail_split);
+        Pending pend;   // the apply's weight cotangents share the dq launch
+        rc = apply_back(a, na, L.off_a, L.tail_split, &pend);
         if (rc) return rc;
         const Out o = dq_out(a, bq, 2 * h);
-        rc = outs(&o, 1, na, (int)d);
+        rc = outs(&o, 1, na, (int)d, &pend);
         if (rc) return rc;
         a_pending = true;
         rc = flush();
@@ -2468,19 +2485,23 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     ra.h = (int)h;
     rc = timed(LACT_KCLASS_UPDATE, 0.0, s, [&] { return launch_swiglu_rows(ra, p.bf16, s); });
     if (rc) return rc;
+    // One launch: the weight cotangents of the apply with the entering
+    // weights (apart) and of the gradient's own dependence on W (bpart), then
+    // dk (a sum over 4h), dv and dq (over 2h). The five products read
+    // buffers that are complete by now and write disjoint ones.
+    Pending pend;
     if (applies && !then_apply) {   // applied with the weights entering the update (their copies are in place)
-      rc = apply_back(s0, n, L.off_u, p.split_len);
+      rc = apply_back(s0, n, L.off_u, p.split_len, &pend);
       if (rc) return rc;
     }
-    // dk (a sum over 4h), dv and dq (over 2h) in one launch
+    rc = grads(op(pk + 2 * h * esz, 4 * h, T * 4 * h), op(pk + 3 * h * esz, 4 * h, T * 4 * h), ko, vo,
+               op(pv + h * esz, 2 * h, T * 2 * h), bpart, n, p.split_len, &b_ns, &pend);
+    if (rc) return rc;
     const Out kvq[3] = {
         {op(pk, 4 * h, T * 4 * h), op(bk, 4 * h, d * 4 * h), (uint8_t*)dk + s0 * d * esz, n_kv * d, 4 * h},
         {op(pv, 2 * h, T * 2 * h), op(bv, 2 * h, d * 2 * h), (uint8_t*)dv + s0 * d * esz, n_kv * d, 2 * h},
         then_apply ? dq_out(s0, bq, 2 * h) : dq_out(s0, bk + 2 * h * esz, 4 * h)};
-    rc = outs(kvq, applies ? 3 : 2, n, (int)d);
-    if (rc) return rc;
-    rc = grads(op(pk + 2 * h * esz, 4 * h, T * 4 * h), op(pk + 3 * h * esz, 4 * h, T * 4 * h), ko, vo,
-               op(pv + h * esz, 2 * h, T * 2 * h), bpart, n, p.split_len, &b_ns);
+    rc = outs(kvq, applies ? 3 : 2, n, (int)d, &pend);
     if (rc) return rc;
     b_pending = true;
     a_pending = applies && !then_apply;   // the entering weights' apply joins before the previous update's reverse

@@ -83,8 +83,12 @@ struct BwdSeg {
   int sumsq_stride, sumsq_j, spi;
 };
 
+// Segments per k_bwd launch: independent products of one chunk's reverse
+// share a launch, so that the CUs one product's tiles leave idle take the
+// others' (up to two gradient pairs and three output products).
+constexpr int kMaxBwdSeg = 7;
 struct BwdArgs {
-  BwdSeg seg[3];
+  BwdSeg seg[kMaxBwdSeg];
   int nseg;
   int total_blocks;
   int d, h;

@@ -1285,15 +1285,11 @@ __device__ __forceinline__ void bwd_body(const BwdArgs& args, int blk, uint8_t* 
   constexpr int esz = sizeof(T);
   int bid = blk;
   int si = 0;
-  if (bid >= args.seg[0].nblocks) {
-    bid -= args.seg[0].nblocks;
-    si = 1;
-    if (bid >= args.seg[1].nblocks) {
-      bid -= args.seg[1].nblocks;
-      si = 2;
-    }
+  while (si + 1 < args.nseg && bid >= args.seg[si].nblocks) {
+    bid -= args.seg[si].nblocks;
+    ++si;
   }
-  const BwdSeg& sg = si == 0 ? args.seg[0] : (si == 1 ? args.seg[1] : args.seg[2]);
+  const BwdSeg& sg = args.seg[si];
   bid = xcd_remap(bid, sg.nblocks);
   const int d = args.d, h = args.h;
   const int per = sg.tiles_m * sg.tiles_n;

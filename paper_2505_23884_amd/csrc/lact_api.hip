@@ -296,6 +296,8 @@ struct Ctx {
   double out_flops = 0.0;
   bool has_out = false;
   bool grad_only = false;   // update_chunk stops after the gradient partials (the backward's own update follows)
+  void* keep[3] = {};       // or nullptr: where the key forward also writes Z1, Z3 and D (FwdSeg::keep)
+  int64_t keep_inst = 0;
   const float* Wsrc[3] = {};   // where the update reads the state (nullptr: W, in place)
 };
 
@@ -624,6 +626,8 @@ int update_chunk(Ctx& c, int64_t s0, int64_t s1, bool apply_too) {
     g.eta = c.eta + s0 * p.es;
     g.eta_inst = c.dsc->n_kv * p.es;
     g.eta_stride = p.es;
+    for (int m = 0; m < 3; ++m) g.keep[m] = c.keep[m];
+    g.keep_inst = c.keep_inst;
   }
   if (apply_too) {
     FwdSeg& g = f.seg[ns++];
@@ -1925,6 +1929,7 @@ struct SwBwdLayout {
   size_t slotP;         // bytes of one chunk's gradient partials
   size_t off_P, off_traj, off_z[6], off_pk, off_pv, off_pq, off_hq, off_u[3], off_a[3], off_bk, off_bv, off_bq,
       off_ur[3], off_apart, off_bpart, total;
+  size_t off_keep, keep_slot;   // per update: the replay's Z1, Z3, D ([BH][chunk][h] each, io dtype)
 };
 
 // nupd: the schedule's updates (negative: lact_forward's chunks);
@@ -1940,7 +1945,8 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false, int64_
   L->nch = nupd >= 0 ? nupd : (dsc->n_kv > 0 ? cdiv(dsc->n_kv, dsc->chunk) : 0);
   const int64_t tail = apply_len >= 0 ? apply_len : dsc->n_q - dsc->n_kv;
   L->T = std::max<int64_t>(1, std::max<int64_t>(p.C, std::min<int64_t>(tail, 4096)));
-  const double need = (double)L->nch * p.BH * dh * 12.0 * (p.nsplit + 1) + (double)p.BH * L->T * p.h * p.esz * 15.0;
+  const double need = (double)L->nch * p.BH * dh * 12.0 * (p.nsplit + 1) + (double)p.BH * L->T * p.h * p.esz * 15.0 +
+                      (double)L->nch * 3 * p.BH * p.C * p.h * p.esz;
   if (need > 4.0e18) return LACT_EUNSUPPORTED;
   L->tail_split = std::max<int64_t>(32, cdiv(cdiv(L->T, p.nsplit), 32) * 32);
   const size_t w4 = (size_t)p.BH * p.d * p.h * 4, wio = (size_t)p.BH * p.d * p.h * p.esz;
@@ -1968,6 +1974,8 @@ int sw_bwd_layout(const lact_desc* dsc, SwBwdLayout* L, bool mom = false, int64_
   for (int i = 0; i < 3; ++i) L->off_ur[i] = take(wio);   // U1, U3 row-major and U2^T
   L->off_apart = take((size_t)p.nsplit * 3 * w4);
   L->off_bpart = take((size_t)p.nsplit * 3 * w4);
+  L->keep_slot = align_up((size_t)3 * p.BH * p.C * p.h * p.esz);
+  L->off_keep = take((size_t)L->nch * L->keep_slot);
   if (p.muon) o = ns_bwd_layout(p, dsc->ns_steps, o, &L->ns, L->nch);
   L->mom = mom;
   if (mom) {
@@ -2114,8 +2122,11 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     }
     c.p.off_step = L.off_P + (size_t)u * L.slotP;
     c.grad_only = keep;
+    for (int m = 0; m < 3; ++m) c.keep[m] = ws + L.off_keep + (size_t)u * L.keep_slot + (size_t)m * p.BH * p.C * h * esz;
+    c.keep_inst = p.C * h;   // the reverse reads this update's Z1, Z3 and D from here
     rc = update_chunk(c, g.b, g.e, false);
     c.grad_only = false;
+    for (int m = 0; m < 3; ++m) c.keep[m] = nullptr;
     if (rc) return rc;
     if (keep) {
       float* gslot = reinterpret_cast<float*>(ws + c.p.off_step);
@@ -2454,20 +2465,19 @@ int run_backward_swiglu(const lact_desc* desc, const void* q, const void* k, con
     rc = weight_copies(u, L.off_u, bk + 2 * h * esz, 4 * h, bv + h * esz);
     if (rc) return rc;
     const Operand ko = op(kb + s0 * d * esz, d, n_kv * d), vo = op(vb + s0 * d * esz, d, n_kv * d);
-    const Out f3[3] = {{ko, op(ws + L.off_u[0], d, dh), zb[0], zi, d},
-                       {ko, op(ws + L.off_u[1], d, dh), zb[1], zi, d},
-                       {vo, op(ws + L.off_u[2], d, dh), zb[2], zi, d}};
-    rc = outs(f3, 3, n, (int)h);
-    if (rc) return rc;
+    // Z1 = K W1^T, Z3 = K W3^T and C = V W2 of this update: kept by its replay
+    uint8_t* kz = ws + L.off_keep + (size_t)u * L.keep_slot;
+    const size_t kzm = (size_t)p.BH * p.C * h * esz;
     const Out x3[3] = {{ko, op(ur[0], d, dh), zb[3], zi, d},
                        {ko, op(ur[1], d, dh), zb[4], zi, d},
                        {vo, op(ur[2], d, dh), zb[5], zi, d}};
     rc = outs(x3, 3, n, (int)h);
     if (rc) return rc;
     SwigluRowsArgs ra{};
-    ra.Z1 = zb[0];
-    ra.Z3 = zb[1];
-    ra.C = zb[2];
+    ra.Z1 = kz;
+    ra.Z3 = kz + kzm;
+    ra.C = kz + 2 * kzm;
+    ra.z_inst = p.C * h;
     ra.X1 = zb[3];
     ra.X3 = zb[4];
     ra.Y2 = zb[5];

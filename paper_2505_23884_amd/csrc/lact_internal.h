@@ -36,6 +36,11 @@ struct FwdSeg {
   const float* eta;     // UPDATE: learning rate(s) of token row 0
   int64_t eta_inst;     // floats between instances
   int eta_stride;       // floats per token: 1 (one rate) or 3 (lr1, lr2, lr3 for W1, W2, W3)
+  // UPDATE, or nullptr: Z1 = K W1^T, Z3 = K W3^T and D = V W2 themselves
+  // (token-major [tokens x h], io dtype, keep_inst elements between
+  // instances), kept for the backward's reverse of the same update
+  void* keep[3];
+  int64_t keep_inst;
 };
 
 struct FwdArgs {
@@ -438,6 +443,7 @@ hipError_t launch_lin_tokens(const void* V, const float* eta, void* dv, float* d
 struct SwigluRowsArgs {
   const void* Z1; const void* Z3; const void* C; const void* X1; const void* X3; const void* Y2;
   int64_t in_inst;                    // elements between instances of the six [n x h] inputs
+  int64_t z_inst;                     // the same for Z1, Z3 and C when nonzero (else in_inst)
   const float* eta; int64_t eta_inst;  // tokens between instances; eta_cols rates per token (1, or 3 per matrix)
   int eta_cols;                       // deta has the same layout
   void* Pk; int64_t pk_inst;          // [n x 4h]

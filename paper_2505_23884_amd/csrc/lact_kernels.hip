@@ -872,7 +872,7 @@ __device__ __forceinline__ void stage_flush(const uint8_t* buf, E* out, int64_t 
 // eta*hidden, eta*dz1 and eta*dz3 token-major, four hidden units per store.
 // With per-matrix rates (lr1, lr2, lr3) per token, hidden (the W2 gradient)
 // takes lr2, dz1 (W1) lr1 and dz3 (W3) lr3 (Alg. 1, update).
-template <typename T, class K>
+template <typename T, class K, bool KEEP = false>
 __device__ __forceinline__ void update_epilogue(const f32x16_t (&z1a)[K::MI][K::NI], const f32x16_t (&z3a)[K::MI][K::NI],
                                                 const f32x16_t (&dda)[K::MI][K::NI], const FwdSeg& sg, int inst,
                                                 int64_t j0, int64_t i0, int64_t hrows, int64_t ntok, int h) {
@@ -907,13 +907,20 @@ __device__ __forceinline__ void update_epilogue(const f32x16_t (&z1a)[K::MI][K::
         st4<T>(sg.out1, idx, vh[0], vh[1], vh[2], vh[3]);
         st4<T>(sg.out2, idx, vg[0], vg[1], vg[2], vg[3]);
         st4<T>(sg.out3, idx, vb[0], vb[1], vb[2], vb[3]);
+        if constexpr (KEEP) {
+          const int64_t kx = inst * sg.keep_inst + (i0 + tok) * h + j0 + hid;
+          const int r = 4 * g;
+          st4<T>(sg.keep[0], kx, z1a[mi][ni][r], z1a[mi][ni][r + 1], z1a[mi][ni][r + 2], z1a[mi][ni][r + 3]);
+          st4<T>(sg.keep[1], kx, z3a[mi][ni][r], z3a[mi][ni][r + 1], z3a[mi][ni][r + 2], z3a[mi][ni][r + 3]);
+          st4<T>(sg.keep[2], kx, dda[mi][ni][r], dda[mi][ni][r + 1], dda[mi][ni][r + 2], dda[mi][ni][r + 3]);
+        }
       }
   }
 }
 
 // The same for 16-bit outputs, staged through LDS (two 64 KiB buffers):
 // eta*hidden and eta*dz1 first, then eta*dz3.
-template <class K>
+template <class K, bool KEEP = false>
 __device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::MI][K::NI],
                                                        const f32x16_t (&z3a)[K::MI][K::NI],
                                                        const f32x16_t (&dda)[K::MI][K::NI], const FwdSeg& sg,
@@ -934,6 +941,37 @@ __device__ __forceinline__ void update_epilogue_staged(const f32x16_t (&z1a)[K::
     e1[ni] = in ? eta[tok * es] : 0.0f;
     e2[ni] = in ? eta[tok * es + o2] : 0.0f;
     e3[ni] = in ? eta[tok * es + 2 * o2] : 0.0f;
+  }
+  if constexpr (KEEP) {   // Z1 and Z3, then D, for the backward's reverse of this update (first:
+                           // every accumulator is live here anyway)
+    const int64_t kt = inst * sg.keep_inst + i0 * h + j0;
+#pragma unroll
+    for (int ni = 0; ni < K::NI; ++ni)
+#pragma unroll
+      for (int mi = 0; mi < K::MI; ++mi)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int tok = acc_col<K>(ni), row = hrow0 + mi * 32 + 8 * g, r = 4 * g;
+          stage_put<R>(buf0, tok, row, z1a[mi][ni][r], z1a[mi][ni][r + 1], z1a[mi][ni][r + 2], z1a[mi][ni][r + 3]);
+          stage_put<R>(buf1, tok, row, z3a[mi][ni][r], z3a[mi][ni][r + 1], z3a[mi][ni][r + 2], z3a[mi][ni][r + 3]);
+        }
+    lds_barrier();
+    stage_flush<R, C, K::THREADS>(buf0, reinterpret_cast<__bf16*>(sg.keep[0]) + kt, h, ntok, hrows);
+    stage_flush<R, C, K::THREADS>(buf1, reinterpret_cast<__bf16*>(sg.keep[1]) + kt, h, ntok, hrows);
+    lds_barrier();
+#pragma unroll
+    for (int ni = 0; ni < K::NI; ++ni)
+#pragma unroll
+      for (int mi = 0; mi < K::MI; ++mi)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int r = 4 * g;
+          stage_put<R>(buf0, acc_col<K>(ni), hrow0 + mi * 32 + 8 * g, dda[mi][ni][r], dda[mi][ni][r + 1],
+                       dda[mi][ni][r + 2], dda[mi][ni][r + 3]);
+        }
+    lds_barrier();
+    stage_flush<R, C, K::THREADS>(buf0, reinterpret_cast<__bf16*>(sg.keep[2]) + kt, h, ntok, hrows);
+    lds_barrier();
   }
 #pragma unroll
   for (int ni = 0; ni < K::NI; ++ni)
@@ -993,7 +1031,7 @@ constexpr int fwd_smem() {
                                                        : 0));
 }
 
-template <typename T, bool NARROW>
+template <typename T, bool NARROW, bool KEEP = false>
 __device__ __forceinline__ void fwd_body(const FwdArgs& args, uint8_t* smem) {
   using KA = typename FwdKinds<T, NARROW>::Apply;
   using KU = typename FwdKinds<T, NARROW>::Update;
@@ -1082,12 +1120,12 @@ __device__ __forceinline__ void fwd_body(const FwdArgs& args, uint8_t* smem) {
       static_assert(KU::NSTAGE * kSlot <= kSmem, "chained ring fits");
       mainloop_chain<T, KU, KD, kSlot>(smem, opz, d, az, opd, d, ad);
       static_assert(2 * KU::ROWS_A * KU::ROWS_B * 2 <= kSmem, "staging fits");
-      update_epilogue_staged<KU>(az[0], az[1], ad[0], sg, inst, j0, i0, hrows, ntok, h, smem);
+      update_epilogue_staged<KU, KEEP>(az[0], az[1], ad[0], sg, inst, j0, i0, hrows, ntok, h, smem);
     } else {
       const View ops[5] = {w1, w3, w2, kk, vv};
       Acc<KU> acc;
       mainloop<T, KU>(smem, ops, d, acc);
-      update_epilogue<T, KU>(acc[0], acc[1], acc[2], sg, inst, j0, i0, hrows, ntok, h);
+      update_epilogue<T, KU, KEEP>(acc[0], acc[1], acc[2], sg, inst, j0, i0, hrows, ntok, h);
     }
   }
 }
@@ -1103,6 +1141,21 @@ __global__ __launch_bounds__(KApplyN16::THREADS) __attribute__((amdgpu_waves_per
     const FwdArgs args) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[fwd_smem<__bf16, true>()];
   fwd_body<__bf16, true>(args, smem);
+}
+
+// The same two kernels with the key forward's Z1, Z3 and D written out too
+// (FwdSeg::keep): the backward's replay of an update, whose reverse reads
+// them instead of computing the three products again.
+template <typename T>
+__global__ __launch_bounds__(Kinds<T>::Apply::THREADS) void k_fwd_keep(const FwdArgs args) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[fwd_smem<T, false>()];
+  fwd_body<T, false, true>(args, smem);
+}
+
+__global__ __launch_bounds__(KApplyN16::THREADS) __attribute__((amdgpu_waves_per_eu(2))) void k_fwd_narrow_keep(
+    const FwdArgs args) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[fwd_smem<__bf16, true>()];
+  fwd_body<__bf16, true, true>(args, smem);
 }
 
 // The weight update of a GRAD_UPD tile from its accumulators P (= -g):
@@ -2745,7 +2798,7 @@ __global__ __launch_bounds__(256) void k_swiglu_rows(const SwigluRowsArgs a) {
   const int64_t total = (int64_t)a.BH * a.n;
   for (int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wave < total; wave += (int64_t)gridDim.x * 4) {
     const int64_t inst = wave / a.n, t = wave - inst * a.n;
-    const int64_t io = inst * a.in_inst + t * h;
+    const int64_t io = inst * a.in_inst + t * h, zo = inst * (a.z_inst ? a.z_inst : a.in_inst) + t * h;
     const int64_t ko = inst * a.pk_inst + t * 4 * h, vo = inst * a.pv_inst + t * 2 * h;
     const int64_t eo = (inst * a.eta_inst + t) * a.eta_cols;
     const float e1 = a.eta[eo];
@@ -2753,9 +2806,9 @@ __global__ __launch_bounds__(256) void k_swiglu_rows(const SwigluRowsArgs a) {
     float d1 = 0.0f, d2 = 0.0f, d3 = 0.0f;
     for (int j = 4 * lane; j < h; j += 256) {
       float z1[4], z3[4], c[4], x1[4], x3[4], y2[4];
-      ld4<T>(a.Z1, io + j, z1);
-      ld4<T>(a.Z3, io + j, z3);
-      ld4<T>(a.C, io + j, c);
+      ld4<T>(a.Z1, zo + j, z1);
+      ld4<T>(a.Z3, zo + j, z3);
+      ld4<T>(a.C, zo + j, c);
       ld4<T>(a.X1, io + j, x1);
       ld4<T>(a.X3, io + j, x3);
       ld4<T>(a.Y2, io + j, y2);
@@ -2974,6 +3027,14 @@ hipError_t launch_beta_mean(const BetaArgs& a, hipStream_t s) {
 
 hipError_t launch_fwd(const FwdArgs& a, bool io_bf16, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;
+  bool keep = false;
+  for (int i = 0; i < a.nseg; ++i) keep = keep || (a.seg[i].kind == FWD_UPDATE && a.seg[i].keep[0]);
+  if (keep) {
+    if (io_bf16 && a.narrow) k_fwd_narrow_keep<<<a.total_blocks, KApplyN16::THREADS, 0, s>>>(a);
+    else if (io_bf16) k_fwd_keep<__bf16><<<a.total_blocks, KApply16::THREADS, 0, s>>>(a);
+    else k_fwd_keep<float><<<a.total_blocks, KApply32::THREADS, 0, s>>>(a);
+    return hipGetLastError();
+  }
   if (io_bf16 && a.narrow) k_fwd_narrow<<<a.total_blocks, KApplyN16::THREADS, 0, s>>>(a);
   else if (io_bf16) k_fwd<__bf16><<<a.total_blocks, KApply16::THREADS, 0, s>>>(a);
   else k_fwd<float><<<a.total_blocks, KApply32::THREADS, 0, s>>>(a);

@@ -182,7 +182,7 @@ def _pmc(path, counter):
 
 def kernel_short_name(name):
     """k_fwd, k_bwd, ... from a mangled (…5k_fwdI…) or demangled (…::k_fwd<…) kernel name."""
-    for k in ("k_fwd_narrow", "k_fwd", "k_bwd", "k_update", "k_prep", "k_scale_rows", "k_beta_mean", "k_zero_rows",
+    for k in ("k_fwd_narrow_keep", "k_fwd_narrow", "k_fwd_keep", "k_fwd", "k_bwd", "k_update", "k_prep", "k_scale_rows", "k_beta_mean", "k_zero_rows",
               "k_ns_fused_pair_out", "k_ns_fused_pair", "k_ns_fused", "k_ns_final", "k_ns_prep", "k_ns_scale", "k_ns",
               "k_prologue", "k_rmsnorm_out", "k_vjp", "k_lin_tokens", "k_copies", "k_accum", "k_swiglu_apply_rows",
               "k_swiglu_rows", "k_mom_bwd", "k_mom_dbeta", "k_mom_adv", "k_slot_dot_part", "k_slot_dot_sum", "k_ns_lin", "k_sym"):

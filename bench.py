@@ -675,8 +675,10 @@ def measure(cfg, args, P, on_device=False):
         d = per[dom]
         achieved = d["tflops"] or 0.0
         kname = DOMINANT_KERNEL.get(dom, dom)
-        traffic = measured_traffic(cfg.name, kname)
-        alg = kernel_alg_bytes(cfg, kname, d["launches"] / max(args.steps, 1))
+        # the counter reports and the byte counts are the forward's launches;
+        # the backward's k_bwd launches are other products (no report: null)
+        traffic = None if args.backward else measured_traffic(cfg.name, kname)
+        alg = None if args.backward else kernel_alg_bytes(cfg, kname, d["launches"] / max(args.steps, 1))
         res["roofline"] = {"bound": "mfma", "kernel": kname,
                            "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                            "frac": round(achieved / peak, 4), "traffic": traffic,

@@ -2267,6 +2267,27 @@ def test_linear_schedule_backward_without_updates_momentum():
     assert np.array_equal(got[6], ct["dM"])
 
 
+def test_linear_schedule_backward_muon_momentum_fp32():
+    # every option at once with fp32 I/O: Muon on the state, an update-only
+    # segment, an apply-only stretch between updates and uncovered rows
+    C = 64
+    cfg, x, ct, st = lin_sched_case("tiny_fp32", 126, True, name="lin_sched_bwd_muon_mom_fp32", B=2, H=1, d=40, h=40,
+                                    n_kv=4 * C, n_q=4 * C + 40, chunk=C, use_muon=1)
+    sched = [("apply_then_update", 0, C), ("apply_only", C, 2 * C), ("update_only", C, 2 * C),
+             ("update_then_apply", 2 * C, 3 * C - 5), ("apply_only", 3 * C + 10, 4 * C + 40)]
+    check_lin_sched_bwd(cfg, x, ct, sched, run_gpu_lin_sched_bwd(cfg, x, ct, sched, st), st)
+
+
+def test_schedule_backward_long_apply_only_segments():
+    # apply-only segments longer than the reverse's 4096-row pieces, before
+    # and after an update: each piece's weight cotangents share the launch of
+    # its dq rows
+    C = 256
+    cfg = CONFIGS["lm32k"].with_(name="sched_bwd_long_apply", B=1, H=2, d=128, h=128, n_kv=C, n_q=10000, chunk=C)
+    x, ct = make_inputs(cfg, 117), make_cotangents(cfg, 117)
+    sched = [("apply_only", 300, 5000), ("apply_then_update", 0, C), ("apply_only", 5000, 10000)]
+    check_sched_bwd(cfg, x, ct, sched, run_gpu_sched_bwd(cfg, x, ct, sched))
+
 @pytest.mark.parametrize("momentum", [False, True])
 def test_linear_schedule_backward_of_uniform_chunks_is_the_chunk_loop_bitwise(momentum):
     cfg, x, ct, st = lin_sched_case("lm32k", 125, momentum, name="lin_sched_bwd_uniform", B=1, H=2, d=128, h=128,

@@ -335,8 +335,10 @@ int lact_backward_linear(const lact_desc* desc,
  *                         fast weights                                           out
  *   workspace   >= lact_backward_workspace_bytes(desc), 256-byte aligned (it
  *               holds every chunk's weights and gradient partials, about
- *               (3 + 3 * splits) * B*H * d*h * 4 bytes per chunk, plus buffers
- *               of a chunk's tokens)
+ *               (3 + 3 * splits) * B*H * d*h * 4 bytes per chunk, the replayed
+ *               key forward's K W1^T, K W3^T and V W2 of every chunk,
+ *               3 * B*H * chunk * h elements of io_dtype per chunk, plus
+ *               buffers of a chunk's tokens)
  *
  * Every element of the outputs is written. Pointers are device pointers,
  * 16-byte aligned (eta and deta: 4); outputs must not alias inputs, each

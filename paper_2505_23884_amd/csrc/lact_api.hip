@@ -1259,7 +1259,10 @@ struct NsBwd {
   // out = a^T b per slot: a [m x m] (rows i), b [m x n] (rows i), fp32 [m x n]; up to two at once
   int grad2(const void* const* a, const void* const* b, float* const* o, int nseg) const {
     BwdArgs x{};
-    const TileShape t = bwd_tile(BWD_GRAD2, !f32(), false);
+    // fp16: 128 x 256 tiles (the narrow kinds), twice the workgroups of the
+    // 256 x 256 ones, so that the slots' tiles fill the chip
+    const bool half = !f32();
+    const TileShape t = bwd_tile(BWD_GRAD2, !f32(), half);
     for (int i = 0; i < nseg; ++i) {
       BwdSeg& g = x.seg[i];
       g.kind = BWD_GRAD2;
@@ -1281,7 +1284,7 @@ struct NsBwd {
     for (int i = 0; i < nseg; ++i) x.total_blocks += x.seg[i].nblocks;
     x.d = N.m;
     x.h = N.n;
-    x.narrow = 0;
+    x.narrow = half ? 1 : 0;
     return timed(LACT_KCLASS_NS, 2.0 * nseg * N.S * mm() * N.n, s,
                  [&] { return f32() ? launch_bwd(x, false, s) : launch_bwd_f16(x, s); });
   }

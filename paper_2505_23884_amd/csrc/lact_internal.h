@@ -381,6 +381,7 @@ hipError_t launch_copies_f32(const CopySeg* c, int n, int BH, hipStream_t s);
 
 // ---- reverse of Newton-Schulz (slots of wide [m x n] fp32 matrices) --------
 // The k_bwd kinds with fp16 operands (fp16 OUT results, fp32 GRAD partials).
+// a.narrow: the narrow kinds (128-row GRAD2 tiles)
 hipError_t launch_bwd_f16(const BwdArgs& a, hipStream_t s);
 // out[s] = sum over len elements of x[s] * y[s] (slot s), in a fixed order
 // (32 workgroups per slot, then their partials in order).

@@ -279,6 +279,12 @@ struct BwdKinds<__bf16, true> {
   using Grad13 = KGrad13N16;
   using Grad2 = KGrad2N16;
 };
+template <>
+struct BwdKinds<_Float16, true> {   // the Newton-Schulz reverse's GRAD2 products on 128 x 256 tiles
+  using Out = KOutN16;
+  using Grad13 = KGrad13N16;
+  using Grad2 = KGrad2N16;
+};
 
 template <class K>
 using Acc = f32x16_t[K::NACC][K::MI][K::NI];
@@ -3188,7 +3194,8 @@ hipError_t launch_mom_adv(const float* M, const float* bbar, int64_t bbar_inst, 
 
 hipError_t launch_bwd_f16(const BwdArgs& a, hipStream_t s) {
   if (a.total_blocks <= 0) return hipSuccess;
-  k_bwd<_Float16, false><<<a.total_blocks, KOut16::THREADS, 0, s>>>(a);
+  if (a.narrow) k_bwd<_Float16, true><<<a.total_blocks, KOutN16::THREADS, 0, s>>>(a);
+  else k_bwd<_Float16, false><<<a.total_blocks, KOut16::THREADS, 0, s>>>(a);
   return hipGetLastError();
 }
 
